@@ -1,0 +1,153 @@
+/* rn18.h - C ABI of the gfx950 (MI355X) ResNet-18 training-step library.
+ *
+ * The library computes one ResNet-18 training step (forward, data- and
+ * weight-gradient convolutions, batch-norm / ReLU / residual, softmax
+ * cross-entropy, SGD with momentum) at any batch size and image resolution,
+ * the forward pass alone in inference mode, and the parameter-server merge of
+ * a small-batch and a large-batch worker's updates with the model-update
+ * factor of dual-batch learning.
+ *
+ * Paper: "Hybrid Dual-Batch and Cyclic Progressive Learning for Efficient
+ * Distributed Training" (arXiv 2509.26092). The training step is the unit of
+ * work that the dual-batch (Sec. 3) and cyclic-progressive (Sec. 4) schemes
+ * schedule at different (batch, resolution) pairs; SGD is Sec. 2.2, Eq. 1;
+ * the parameter-server pull/train/push cycle is Sec. 2.3; the model-update
+ * factor is Sec. 3.4.
+ *
+ * Conventions for every call
+ *  - Pointers are DEVICE pointers unless stated otherwise. The caller owns
+ *    them (typically torch tensors); the library never frees caller memory.
+ *  - Every float pointer must be 16-byte aligned.
+ *  - All work of a context is enqueued on that context's HIP stream and is
+ *    asynchronous; nothing synchronises the host except rn18_init (when it
+ *    writes the initial state), rn18_sync_status, rn18_destroy and the
+ *    workspace query functions.
+ *  - Errors the host can detect are returned at once, before anything is
+ *    launched: RN18_EINVAL for null pointers, non-positive sizes, a layer
+ *    whose output would be empty, a batch-norm layer with only one value per
+ *    channel (N*Ho*Wo == 1), or a non-finite factor. rn18_last_error()
+ *    returns a thread-local description of the last non-OK return.
+ *  - Errors found on the device (a label outside [0, C), a non-finite loss)
+ *    set a sticky flag of the context; rn18_sync_status reports and clears it.
+ *  - No C++ exception crosses this interface.
+ */
+#ifndef RN18_H
+#define RN18_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RN18_OK = 0,
+  RN18_EINVAL = -1,
+  RN18_ELABEL = -2,
+  RN18_ENOMEM = -3,
+  RN18_EHIP = -4,
+  RN18_ENONFINITE = -5
+} rn18_status;
+
+/* Network variants (the paper names ResNet-18, Sec. 5.1.1; the variants are
+ * the evaluation's CIFAR-100 32x32 and ImageNet shapes plus a one-block net):
+ *  RN18_TINY      3x3 s1 stem 3->16, one BasicBlock 16->16, FC 16->C
+ *  RN18_CIFAR     3x3 s1 stem 3->64, no max pool, stages 64/128/256/512 x 2
+ *  RN18_IMAGENET  7x7 s2 p3 stem 3->64, 3x3 s2 p1 max pool, same stages
+ * BasicBlock = conv3x3(s)-BN-ReLU-conv3x3-BN (+ shortcut) -ReLU; stride 2 in
+ * the first conv of stages 2-4; 1x1 stride-s conv + BN shortcut when the
+ * stride or width changes. Convs have no bias, the FC has one. */
+typedef enum { RN18_TINY = 0, RN18_CIFAR = 1, RN18_IMAGENET = 2 } rn18_arch;
+
+/* RN18_FP32: all tensors fp32 (fp32 MFMA for the convolutions).
+ * RN18_BF16: images, conv weights and activations (and their gradients) in
+ * bf16 with fp32 accumulation; master weights, momentum, BN statistics, the
+ * classifier and the loss in fp32. This is the mixed precision of the
+ * paper's ImageNet runs (Sec. 5.2.1), taken as bf16 without loss scaling. */
+typedef enum { RN18_FP32 = 0, RN18_BF16 = 1 } rn18_prec;
+
+typedef struct {
+  int arch;            /* rn18_arch */
+  int num_classes;     /* C >= 1 */
+  int prec;            /* rn18_prec */
+  float momentum;      /* SGD momentum, e.g. 0.9 */
+  float weight_decay;  /* L2 coefficient added to every trainable gradient, e.g. 5e-4 */
+  float bn_eps;        /* e.g. 1e-5 */
+  float bn_momentum;   /* running-stat update weight, e.g. 0.1 */
+} rn18_config;
+
+typedef struct rn18_ctx rn18_ctx; /* opaque: plans, momentum buffer, bf16 weight shadow */
+
+/* Flat parameter state, fp32, in this order:
+ *   for every conv in forward order (stem, then per block c1, c2, [ds]):
+ *       W [Cout][Cin][KH][KW], gamma [Cout], beta [Cout]
+ *   FC weight [C][F], FC bias [C]                      (P trainable floats)
+ *   for every BN in the same order: running_mean [Cout], running_var [Cout]
+ * Returns P+R and, if n_trainable is not NULL, stores P there.
+ * Returns 0 for an invalid config. */
+size_t rn18_state_floats(const rn18_config* cfg, size_t* n_trainable);
+
+/* Create a context bound to hip_stream (a hipStream_t; NULL = default
+ * stream). If state_out is not NULL, write a He-normal (fan-in) initial state
+ * drawn from `seed` (gamma 1, beta 0, FC bias 0, running mean 0, running var
+ * 1) and wait for the copy. The momentum buffer starts at zero. */
+int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* state_out, rn18_ctx** ctx);
+
+/* Device workspace needed by a train step or eval pass of shape (N,H,W), in
+ * bytes. Returns 0 if the shape is invalid. */
+size_t rn18_workspace_bytes(rn18_ctx* ctx, int N, int H, int W);
+
+/* Hand the library a caller-allocated device workspace (e.g. a torch uint8
+ * tensor). Steps whose workspace does not fit return RN18_ENOMEM. Without
+ * this call the library allocates and grows its own workspace. */
+int rn18_set_workspace(rn18_ctx* ctx, void* dev, size_t bytes);
+
+/* One training step on `state` (in/out, P+R floats): forward with batch
+ * statistics, softmax cross-entropy loss averaged over the batch, backward,
+ * BN running-stat update, then g' = g + wd*w, v = mu*v + g', w -= lr*v on all
+ * P trainable floats.
+ *   images  [N][3][H][W] fp32 (NCHW)
+ *   labels  [N] int32 in [0, C)   (out-of-range labels set RN18_ELABEL and
+ *                                  contribute neither loss nor gradient)
+ *   loss    1 fp32 (device), written with the pre-update loss; may be NULL */
+int rn18_train_step(rn18_ctx* ctx, float* state, const float* images, const int32_t* labels, int N, int H, int W,
+                    float lr, float* loss);
+
+/* Forward pass in inference mode (BN with the running statistics in
+ * `state`); writes logits [N][C] fp32. */
+int rn18_eval_logits(rn18_ctx* ctx, const float* state, const float* images, int N, int H, int W, float* logits);
+
+/* Parameter-server merge of dual-batch learning (Sec. 2.3 pull/train/push,
+ * Sec. 3.4 model-update factor). g_small and g_large are the update vectors
+ * the two workers push, Delta = p_pulled - p_after_local_step (see
+ * ps_worker_delta); the server applies
+ *     state[i] <- state[i] - (g_large[i] + factor * g_small[i]),  i < n,
+ * with factor = d_S/d_L for the paper's scheme (1 for the large worker is
+ * implicit). n is normally P+R (the BN running statistics merge by the same
+ * rule). g_small/g_large may alias each other but not `state`.
+ * RN18_EINVAL if a pointer is NULL or misaligned or factor is not finite. */
+int ps_dual_merge(float* state, const float* g_small, const float* g_large, size_t n, float factor, void* hip_stream);
+
+/* delta[i] = pulled[i] - local[i], i < n: the update vector a worker pushes
+ * after training on its pulled copy of the global model (Sec. 2.3). */
+int ps_worker_delta(const float* pulled, const float* local, float* delta, size_t n, void* hip_stream);
+
+/* Wait for the context's stream; return and clear the sticky device error
+ * (RN18_ELABEL, RN18_ENONFINITE) or RN18_OK. */
+int rn18_sync_status(rn18_ctx* ctx);
+
+/* Copy the momentum buffer (P floats, device) out / in, for checkpoint and
+ * resume of a worker. */
+int rn18_get_momentum(rn18_ctx* ctx, float* dst);
+int rn18_set_momentum(rn18_ctx* ctx, const float* src);
+
+/* Synchronise and free everything the context allocated. */
+void rn18_destroy(rn18_ctx* ctx);
+
+const char* rn18_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

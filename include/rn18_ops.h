@@ -1,0 +1,62 @@
+/* rn18_ops.h - single-operator entry points of the gfx950 ResNet-18 library.
+ *
+ * These expose the kernels the training step is built from, on the library's
+ * internal layouts, so each can be checked against a reference on its own.
+ * The operators are those of the ResNet-18 training step (the unit of work of
+ * the paper's Sec. 3 and 4 schemes); the paper itself gives no operator
+ * formulas, so each follows the textbook definition stated below.
+ *
+ * Common rules: device pointers, caller-owned, 16-byte aligned; `prec` is
+ * RN18_FP32 (float elements) or RN18_BF16 (bf16 elements as uint16 bit
+ * patterns); activations are NHWC; channel counts of activation tensors must
+ * be multiples of 4 (fp32) or 8 (bf16). Work is enqueued on `hip_stream`.
+ * Invalid arguments return RN18_EINVAL before any launch.
+ */
+#ifndef RN18_OPS_H
+#define RN18_OPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Convolution, no bias, zero padding, square kernel k, stride s, pad p:
+ *   y[n,i,j,o] = sum_{c,kh,kw} w[o,kh,kw,c] * x[n, i*s-p+kh, j*s-p+kw, c]
+ * x [N][H][W][Cin], w [Cout][k][k][Cin] (OHWI), y [N][Ho][Wo][Cout] with
+ * Ho = (H+2p-k)/s + 1. Implicit GEMM on MFMA, fp32 accumulation. */
+int rn18op_conv2d_fwd(int prec, const void* x, const void* w_ohwi, void* y, int N, int H, int W, int Cin, int Cout,
+                      int k, int s, int p, void* hip_stream);
+
+/* Data gradient (adjoint of the above in x):
+ *   dx[n,h,w,c] = sum over (i,j,kh,kw) with i*s-p+kh = h, j*s-p+kw = w of
+ *                 w[o,kh,kw,c] * dy[n,i,j,o]
+ * dy [N][Ho][Wo][Cout], w_ihwo [Cin][k][k][Cout] (the forward weights with
+ * the channel axes exchanged), dx [N][H][W][Cin]. Stride 2 runs as four
+ * parity-phase sub-convolutions (no multiplications by inserted zeros). */
+int rn18op_conv2d_dgrad(int prec, const void* dy, const void* w_ihwo, void* dx, int N, int H, int W, int Cin,
+                        int Cout, int k, int s, int p, void* hip_stream);
+
+/* Weight gradient: dw[o,c,kh,kw] = sum_{n,i,j} dy[n,i,j,o] * x[n,i*s-p+kh,j*s-p+kw,c]
+ * written fp32 in OIHW order for the first cin_real of the Cin channels.
+ * Needs `workspace` of rn18op_conv2d_wgrad_workspace(...) bytes for the
+ * deterministic split-K partial sums. */
+size_t rn18op_conv2d_wgrad_workspace(int prec, int N, int H, int W, int Cin, int Cout, int k, int s, int p);
+int rn18op_conv2d_wgrad(int prec, const void* dy, const void* x, float* dw_oihw, int N, int H, int W, int Cin,
+                        int cin_real, int Cout, int k, int s, int p, void* workspace, size_t workspace_bytes,
+                        void* hip_stream);
+
+/* Max pool 3x3, stride 2, padding 1 (padding never wins):
+ *   y[n,i,j,c] = max over the window; arg[n,i,j,c] = kh*3+kw of the FIRST
+ *   maximum in row-major (kh,kw) order (uint8).
+ * Backward: dx[n,h,w,c] = sum of dy over the outputs whose argmax is (h,w). */
+int rn18op_maxpool_fwd(int prec, const void* x, void* y, uint8_t* arg, int N, int H, int W, int C,
+                       void* hip_stream);
+int rn18op_maxpool_bwd(int prec, const void* dy, const uint8_t* arg, void* dx, int N, int H, int W, int C,
+                       void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

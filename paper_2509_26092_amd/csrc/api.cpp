@@ -1,0 +1,860 @@
+// Step executor and C ABI of the ResNet-18 training-step library.
+//
+// The host side builds, once per (N,H,W), a plan: every layer's shapes, the
+// workspace offset of every saved tensor, and the split counts of the weight
+// gradients. A step is then a fixed sequence of kernel launches on the
+// context's stream with no host synchronisation.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <map>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/rn18.h"
+#include "../../include/rn18_ops.h"
+#include "kernels.h"
+
+using namespace rn18;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIPCHK(x)                                                              \
+  do {                                                                         \
+    hipError_t e_ = (x);                                                       \
+    if (e_ != hipSuccess) return fail(RN18_EHIP, "%s: %s", #x, hipGetErrorString(e_)); \
+  } while (0)
+#define LCHK(x)                                                                \
+  do {                                                                         \
+    int r_ = (x);                                                              \
+    if (r_ != 0) return fail(RN18_EHIP, "launch failed: %s (%s)", #x, hipGetErrorString(hipGetLastError())); \
+  } while (0)
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+inline int out_size(int h, int k, int s, int p) { return (h + 2 * p - k) / s + 1; }
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ----------------------------------------------------------------------------
+// Architecture
+// ----------------------------------------------------------------------------
+struct ConvL {
+  int cin, cout, k, s, p;
+  int cin_p;               // channels of the NHWC input tensor (padded for the stem)
+  long w, g, b, rm, rv;    // offsets in the flat state (floats)
+  long wf, wd;             // element offsets in the weight shadows (wd = -1: none)
+};
+struct BlockL { int c1, c2, ds; };
+
+struct Arch {
+  std::vector<ConvL> convs;
+  std::vector<BlockL> blocks;
+  int feat = 0, classes = 0;
+  bool imagenet = false;
+  long fc_w = 0, fc_b = 0, P = 0, R = 0;
+  long wf_total = 0, wd_total = 0;
+};
+
+bool build_arch(const rn18_config& c, Arch* a) {
+  if (c.num_classes < 1 || c.arch < 0 || c.arch > 2 || c.prec < 0 || c.prec > 1) return false;
+  const int cp = c.prec == RN18_BF16 ? 8 : 4;
+  int stem_c, stem_k, stem_s, stem_p;
+  std::vector<int> widths, nblk, fstride;
+  if (c.arch == RN18_TINY) {
+    stem_c = 16; stem_k = 3; stem_s = 1; stem_p = 1;
+    widths = {16}; nblk = {1}; fstride = {1};
+  } else {
+    stem_c = 64;
+    if (c.arch == RN18_IMAGENET) { stem_k = 7; stem_s = 2; stem_p = 3; }
+    else { stem_k = 3; stem_s = 1; stem_p = 1; }
+    widths = {64, 128, 256, 512}; nblk = {2, 2, 2, 2}; fstride = {1, 2, 2, 2};
+  }
+  a->imagenet = c.arch == RN18_IMAGENET;
+  a->convs.clear();
+  a->blocks.clear();
+  a->convs.push_back(ConvL{3, stem_c, stem_k, stem_s, stem_p, cp});
+  int cin = stem_c;
+  for (size_t si = 0; si < widths.size(); ++si)
+    for (int bi = 0; bi < nblk[si]; ++bi) {
+      const int s = bi == 0 ? fstride[si] : 1, w = widths[si];
+      BlockL b;
+      b.c1 = (int)a->convs.size(); a->convs.push_back(ConvL{cin, w, 3, s, 1, cin});
+      b.c2 = (int)a->convs.size(); a->convs.push_back(ConvL{w, w, 3, 1, 1, w});
+      b.ds = -1;
+      if (s != 1 || cin != w) { b.ds = (int)a->convs.size(); a->convs.push_back(ConvL{cin, w, 1, s, 0, cin}); }
+      a->blocks.push_back(b);
+      cin = w;
+    }
+  a->feat = cin;
+  a->classes = c.num_classes;
+  long o = 0;
+  for (auto& L : a->convs) {
+    L.w = o; o += (long)L.cout * L.cin * L.k * L.k;
+    L.g = o; o += L.cout;
+    L.b = o; o += L.cout;
+  }
+  a->fc_w = o; o += (long)c.num_classes * a->feat;
+  a->fc_b = o; o += c.num_classes;
+  a->P = o;
+  for (auto& L : a->convs) {
+    L.rm = o; o += L.cout;
+    L.rv = o; o += L.cout;
+  }
+  a->R = o - a->P;
+  long f = 0, d = 0;
+  for (size_t i = 0; i < a->convs.size(); ++i) {
+    ConvL& L = a->convs[i];
+    L.wf = f; f += (long)L.cout * L.k * L.k * L.cin_p;
+    if (i == 0) L.wd = -1;
+    else { L.wd = d; d += (long)L.cout * L.k * L.k * L.cin_p; }
+  }
+  a->wf_total = f;
+  a->wd_total = d;
+  return true;
+}
+
+// ----------------------------------------------------------------------------
+// Plan for one (N,H,W)
+// ----------------------------------------------------------------------------
+struct ConvP {
+  int Hin, Win, Ho, Wo;
+  long M;                       // N*Ho*Wo
+  size_t x, y;                  // workspace offsets of input and output
+  size_t mean, rstd, scale, shift, coef;
+  int splits, pps;
+};
+struct BlockP { size_t in, z1, out; };
+
+struct Plan {
+  int N, H, W;
+  std::vector<ConvP> cp;
+  std::vector<BlockP> bp;
+  size_t x0, zstem, pool, parg;
+  int Hs, Ws, Hp, Wp;           // stem output and pool output sizes
+  int Hf, Wf;                   // final feature map
+  size_t f, logits, dlogits, df, rowloss, lossbuf;
+  size_t gA, gB, gz, gy, gyd;
+  size_t part, wpart, grad;
+  size_t total;
+};
+
+struct Ctx {
+  rn18_config cfg;
+  Arch arch;
+  int prec;
+  int es;                       // element size of activations
+  hipStream_t stream;
+  float* momentum = nullptr;
+  void* wf = nullptr;
+  void* wd = nullptr;
+  RepackEntry* tab = nullptr;
+  int ntab = 0;
+  unsigned* err = nullptr;
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  bool ws_owned = false;
+  std::map<std::tuple<int, int, int>, Plan> plans;
+};
+
+int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
+  const Arch& a = c.arch;
+  const int es = c.es;
+  char buf[256];
+  if (N < 1 || H < 1 || W < 1) { *why = "N, H and W must be >= 1"; return RN18_EINVAL; }
+  if ((long)N * H * W > (1l << 31) / 8) { *why = "input too large"; return RN18_EINVAL; }
+  pl->N = N; pl->H = H; pl->W = W;
+  size_t off = 0;
+  auto alloc = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  auto act = [&](int h, int w, int ch) { return alloc((size_t)N * h * w * ch * es); };
+  pl->cp.assign(a.convs.size(), ConvP{});
+  pl->bp.assign(a.blocks.size(), BlockP{});
+  size_t max_blockio = 0, max_z1 = 0, max_y = 0, max_yd = 0, max_wpart = 0;
+  long max_partC = 0;
+
+  auto conv_plan = [&](int li, int hin, int win, size_t xin) -> bool {
+    const ConvL& L = a.convs[li];
+    ConvP& P = pl->cp[li];
+    P.Hin = hin; P.Win = win;
+    P.Ho = out_size(hin, L.k, L.s, L.p);
+    P.Wo = out_size(win, L.k, L.s, L.p);
+    if (P.Ho < 1 || P.Wo < 1) {
+      snprintf(buf, sizeof buf, "conv %d: empty output for input %dx%d", li, hin, win);
+      *why = buf;
+      return false;
+    }
+    P.M = (long)N * P.Ho * P.Wo;
+    if (P.M < 2) {
+      snprintf(buf, sizeof buf, "batch norm after conv %d sees a single value per channel (N*Ho*Wo = 1)", li);
+      *why = buf;
+      return false;
+    }
+    P.x = xin;
+    P.y = act(P.Ho, P.Wo, L.cout);
+    P.mean = alloc(L.cout * 4); P.rstd = alloc(L.cout * 4);
+    P.scale = alloc(L.cout * 4); P.shift = alloc(L.cout * 4);
+    P.coef = alloc(3 * L.cout * 4);
+    const size_t ybytes = (size_t)P.M * L.cout * es;
+    if (ybytes > max_y) max_y = ybytes;
+    P.splits = conv_wgrad_splits(c.prec, L.cout, L.k * L.k * L.cin_p, P.M, &P.pps);
+    const size_t wp = (size_t)P.splits * L.cout * L.k * L.k * L.cin_p * 4;
+    if (wp > max_wpart) max_wpart = wp;
+    const long pc = 1024l * L.cout * 2;
+    if (pc > max_partC) max_partC = pc;
+    return true;
+  };
+
+  const int cp0 = a.convs[0].cin_p;
+  pl->x0 = act(H, W, cp0);
+  if (!conv_plan(0, H, W, pl->x0)) return RN18_EINVAL;
+  pl->Hs = pl->cp[0].Ho; pl->Ws = pl->cp[0].Wo;
+  pl->zstem = act(pl->Hs, pl->Ws, a.convs[0].cout);
+  size_t zs_bytes = (size_t)N * pl->Hs * pl->Ws * a.convs[0].cout * es;
+  max_blockio = zs_bytes;
+  size_t cur = pl->zstem;
+  int h = pl->Hs, w = pl->Ws;
+  if (a.imagenet) {
+    pl->Hp = out_size(h, 3, 2, 1); pl->Wp = out_size(w, 3, 2, 1);
+    pl->pool = act(pl->Hp, pl->Wp, a.convs[0].cout);
+    pl->parg = alloc((size_t)N * pl->Hp * pl->Wp * a.convs[0].cout);
+    cur = pl->pool; h = pl->Hp; w = pl->Wp;
+  } else {
+    pl->Hp = h; pl->Wp = w; pl->pool = pl->zstem; pl->parg = 0;
+  }
+  for (size_t bi = 0; bi < a.blocks.size(); ++bi) {
+    const BlockL& B = a.blocks[bi];
+    BlockP& bp = pl->bp[bi];
+    bp.in = cur;
+    if (!conv_plan(B.c1, h, w, cur)) return RN18_EINVAL;
+    const ConvP& p1 = pl->cp[B.c1];
+    bp.z1 = act(p1.Ho, p1.Wo, a.convs[B.c1].cout);
+    const size_t z1b = (size_t)p1.M * a.convs[B.c1].cout * es;
+    if (z1b > max_z1) max_z1 = z1b;
+    if (!conv_plan(B.c2, p1.Ho, p1.Wo, bp.z1)) return RN18_EINVAL;
+    if (B.ds >= 0) {
+      if (!conv_plan(B.ds, h, w, cur)) return RN18_EINVAL;
+      const size_t ydb = (size_t)pl->cp[B.ds].M * a.convs[B.ds].cout * es;
+      if (ydb > max_yd) max_yd = ydb;
+    }
+    const ConvP& p2 = pl->cp[B.c2];
+    bp.out = act(p2.Ho, p2.Wo, a.convs[B.c2].cout);
+    const size_t ob = (size_t)p2.M * a.convs[B.c2].cout * es;
+    const size_t ib = (size_t)N * h * w * a.convs[B.c1].cin * es;
+    if (ob > max_blockio) max_blockio = ob;
+    if (ib > max_blockio) max_blockio = ib;
+    cur = bp.out; h = p2.Ho; w = p2.Wo;
+  }
+  pl->Hf = h; pl->Wf = w;
+  const int C = a.classes;
+  pl->f = alloc((size_t)N * a.feat * 4);
+  pl->logits = alloc((size_t)N * C * 4);
+  pl->dlogits = alloc((size_t)N * C * 4);
+  pl->df = alloc((size_t)N * a.feat * 4);
+  pl->rowloss = alloc((size_t)N * 4);
+  pl->lossbuf = alloc(4);
+  pl->gA = alloc(max_blockio);
+  pl->gB = alloc(max_blockio);
+  pl->gz = alloc(max_z1 ? max_z1 : 16);
+  pl->gy = alloc(max_y);
+  pl->gyd = alloc(max_yd ? max_yd : 16);
+  pl->part = alloc((size_t)max_partC * 4);
+  pl->wpart = alloc(max_wpart);
+  pl->grad = alloc((size_t)a.P * 4);
+  pl->total = off;
+  return RN18_OK;
+}
+
+// ----------------------------------------------------------------------------
+// Conv launch helpers
+// ----------------------------------------------------------------------------
+ConvGather gather_fwd(const void* x, const void* w, void* y, int N, int Hin, int Win, int Cin, int Ho, int Wo,
+                      int Cout, int k, int s, int p) {
+  ConvGather g{};
+  g.A = x; g.B = w; g.C = y;
+  g.N = N; g.Hin = Hin; g.Win = Win; g.Cin = Cin;
+  g.Hm = Ho; g.Wm = Wo; g.M = N * Ho * Wo;
+  g.Hout = Ho; g.Wout = Wo; g.Cols = Cout;
+  g.os = 1; g.oph = 0; g.opw = 0;
+  g.is = s; g.ip = p;
+  g.nth = k; g.ntw = k;
+  g.dh0 = 0; g.dhs = 1; g.dw0 = 0; g.dws = 1;
+  g.wkh0 = 0; g.wkhs = 1; g.wkw0 = 0; g.wkws = 1; g.KW = k; g.KHW = k * k;
+  g.K = k * k * Cin;
+  g.mode = 0;
+  return g;
+}
+
+// Data gradient of a conv with input [N][H][W][Cin] and output [N][Ho][Wo][Cout].
+// mode: 0 store, 1 accumulate, 2 add masked residual (R, Rm).
+int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int H, int W, int Cin, int Ho, int Wo,
+                 int Cout, int k, int s, int p, int mode, const void* R, const void* Rm, hipStream_t st) {
+  if (s == 1) {
+    ConvGather g{};
+    g.A = dy; g.B = wd; g.C = dx; g.R = R; g.Rm = Rm;
+    g.N = N; g.Hin = Ho; g.Win = Wo; g.Cin = Cout;
+    g.Hm = H; g.Wm = W; g.M = N * H * W;
+    g.Hout = H; g.Wout = W; g.Cols = Cin;
+    g.os = 1; g.oph = 0; g.opw = 0;
+    g.is = 1; g.ip = k - 1 - p;
+    g.nth = k; g.ntw = k;
+    g.dh0 = 0; g.dhs = 1; g.dw0 = 0; g.dws = 1;
+    g.wkh0 = k - 1; g.wkhs = -1; g.wkw0 = k - 1; g.wkws = -1; g.KW = k; g.KHW = k * k;
+    g.K = k * k * Cout;
+    g.mode = mode;
+    return conv_gather_launch(prec, g, st);
+  }
+  if (s != 2) return -1;
+  for (int ph = 0; ph < 2; ++ph)
+    for (int pw = 0; pw < 2; ++pw) {
+      const int Hm = (H - ph + 1) / 2, Wm = (W - pw + 1) / 2;
+      if (Hm <= 0 || Wm <= 0) continue;
+      const int kh0 = (ph + p) & 1, kw0 = (pw + p) & 1;
+      const int nth = kh0 < k ? (k - kh0 + 1) / 2 : 0;
+      const int ntw = kw0 < k ? (k - kw0 + 1) / 2 : 0;
+      ConvGather g{};
+      g.A = dy; g.B = wd; g.C = dx; g.R = R; g.Rm = Rm;
+      g.N = N; g.Hin = Ho; g.Win = Wo; g.Cin = Cout;
+      g.Hm = Hm; g.Wm = Wm; g.M = N * Hm * Wm;
+      g.Hout = H; g.Wout = W; g.Cols = Cin;
+      g.os = 2; g.oph = ph; g.opw = pw;
+      g.is = 1; g.ip = 0;
+      g.nth = nth; g.ntw = ntw;
+      g.dh0 = (ph + p - kh0) / 2; g.dhs = -1; g.dw0 = (pw + p - kw0) / 2; g.dws = -1;
+      g.wkh0 = kh0; g.wkhs = 2; g.wkw0 = kw0; g.wkws = 2; g.KW = k; g.KHW = k * k;
+      g.K = nth * ntw * Cout;
+      g.mode = mode;
+      if (g.K == 0) {
+        if (mode == 1) continue;   // nothing to add
+        g.nth = 1; g.ntw = 1;      // K = 0: the kernel writes acc = 0 (+ residual)
+      }
+      const int r = conv_gather_launch(prec, g, st);
+      if (r) return r;
+    }
+  return 0;
+}
+
+int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float* wpart, int N, int H, int W, int Cin,
+                      int cin_real, int Ho, int Wo, int Cout, int k, int s, int p, int splits, int pps,
+                      hipStream_t st) {
+  ConvWgrad g{};
+  g.DY = dy; g.X = x; g.P = wpart;
+  g.N = N; g.H = H; g.W = W; g.Cin = Cin; g.Ho = Ho; g.Wo = Wo; g.Cout = Cout;
+  g.KH = k; g.KW = k; g.stride = s; g.pad = p;
+  g.Mpix = N * Ho * Wo;
+  g.Kcols = k * k * Cin;
+  g.pix_per_split = pps;
+  g.splits = splits;
+  int r = conv_wgrad_launch(prec, g, st);
+  if (r) return r;
+  return wgrad_reduce_launch(wpart, splits, Cout, k * k, Cin, cin_real, out, st);
+}
+
+// ----------------------------------------------------------------------------
+// Forward / backward
+// ----------------------------------------------------------------------------
+int ensure_ws(Ctx* c, const Plan& pl) {
+  if (c->ws_bytes >= pl.total) return RN18_OK;
+  if (!c->ws_owned && c->ws)
+    return fail(RN18_ENOMEM, "workspace of %zu bytes is smaller than the %zu this shape needs", c->ws_bytes, pl.total);
+  if (c->ws) {
+    HIPCHK(hipStreamSynchronize(c->stream));
+    HIPCHK(hipFree(c->ws));
+    c->ws = nullptr;
+    c->ws_bytes = 0;
+  }
+  if (hipMalloc(&c->ws, pl.total) != hipSuccess) {
+    c->ws = nullptr;
+    return fail(RN18_ENOMEM, "cannot allocate a %zu-byte workspace", pl.total);
+  }
+  c->ws_bytes = pl.total;
+  c->ws_owned = true;
+  return RN18_OK;
+}
+
+int get_plan(Ctx* c, int N, int H, int W, const Plan** out) {
+  auto key = std::make_tuple(N, H, W);
+  auto it = c->plans.find(key);
+  if (it == c->plans.end()) {
+    Plan pl;
+    std::string why;
+    int r = build_plan(*c, N, H, W, &pl, &why);
+    if (r) return fail(r, "%s", why.c_str());
+    it = c->plans.emplace(key, pl).first;
+  }
+  *out = &it->second;
+  return RN18_OK;
+}
+
+int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, const float* images, bool train) {
+  const Arch& a = c->arch;
+  char* ws = (char*)c->ws;
+  hipStream_t st = c->stream;
+  const int prec = c->prec;
+  const int N = pl.N;
+  const float eps = c->cfg.bn_eps, mom = c->cfg.bn_momentum;
+  auto W = [&](int li) { return (const char*)c->wf + (size_t)a.convs[li].wf * c->es; };
+
+  LCHK(repack_launch(prec, state_c, c->wf, c->wd, c->tab, c->ntab, a.wf_total, st));
+  LCHK(ingest_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, a.convs[0].cin_p, st));
+
+  auto conv_bn = [&](int li) -> int {
+    const ConvL& L = a.convs[li];
+    const ConvP& P = pl.cp[li];
+    ConvGather g = gather_fwd(ws + P.x, W(li), ws + P.y, N, P.Hin, P.Win, L.cin_p, P.Ho, P.Wo, L.cout, L.k, L.s, L.p);
+    LCHK(conv_gather_launch(prec, g, st));
+    float* mean = (float*)(ws + P.mean);
+    float* rstd = (float*)(ws + P.rstd);
+    float* sc = (float*)(ws + P.scale);
+    float* sf = (float*)(ws + P.shift);
+    if (train) {
+      int nblk = 0;
+      float* part = (float*)(ws + pl.part);
+      LCHK(bn_stats_partial_launch(prec, ws + P.y, P.M, L.cout, part, &nblk, st));
+      LCHK(bn_stats_final_launch(prec, ws + P.y, part, nblk, P.M, L.cout, state_c + L.g, state_c + L.b, eps, mom,
+                                 state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, st));
+    } else {
+      LCHK(bn_eval_coef_launch(state_c + L.g, state_c + L.b, state_c + L.rm, state_c + L.rv, eps, L.cout, sc, sf, st));
+    }
+    return 0;
+  };
+  auto apply = [&](int li, int relu, int res_mode, size_t r, int li2, size_t z) -> int {
+    const ConvL& L = a.convs[li];
+    const ConvP& P = pl.cp[li];
+    const float* sc2 = li2 >= 0 ? (const float*)(ws + pl.cp[li2].scale) : nullptr;
+    const float* sf2 = li2 >= 0 ? (const float*)(ws + pl.cp[li2].shift) : nullptr;
+    LCHK(bn_apply_launch(prec, ws + P.y, (float*)(ws + P.scale), (float*)(ws + P.shift), relu, res_mode,
+                         res_mode ? ws + r : nullptr, sc2, sf2, ws + z, P.M, L.cout, st));
+    return 0;
+  };
+
+  int r;
+  if ((r = conv_bn(0))) return r;
+  if ((r = apply(0, 1, 0, 0, -1, pl.zstem))) return r;
+  if (a.imagenet)
+    LCHK(maxpool_fwd_launch(prec, ws + pl.zstem, ws + pl.pool, (uint8_t*)(ws + pl.parg), N, pl.Hs, pl.Ws,
+                            a.convs[0].cout, pl.Hp, pl.Wp, st));
+  for (size_t bi = 0; bi < a.blocks.size(); ++bi) {
+    const BlockL& B = a.blocks[bi];
+    const BlockP& bp = pl.bp[bi];
+    if ((r = conv_bn(B.c1))) return r;
+    if ((r = apply(B.c1, 1, 0, 0, -1, bp.z1))) return r;
+    if ((r = conv_bn(B.c2))) return r;
+    if (B.ds >= 0) {
+      if ((r = conv_bn(B.ds))) return r;
+      if ((r = apply(B.c2, 1, 2, pl.cp[B.ds].y, B.ds, bp.out))) return r;
+    } else {
+      if ((r = apply(B.c2, 1, 1, bp.in, -1, bp.out))) return r;
+    }
+  }
+  const size_t last = pl.bp.back().out;
+  LCHK(avgpool_fwd_launch(prec, ws + last, (float*)(ws + pl.f), N, pl.Hf * pl.Wf, a.feat, st));
+  return RN18_OK;
+}
+
+int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const int32_t* labels, float lr,
+              float* loss) {
+  const Arch& a = c->arch;
+  char* ws = (char*)c->ws;
+  hipStream_t st = c->stream;
+  const int prec = c->prec;
+  const int N = pl.N, C = a.classes, F = a.feat;
+  int r;
+  if ((r = run_forward(c, pl, state, state, images, true))) return r;
+  float* f = (float*)(ws + pl.f);
+  float* logits = (float*)(ws + pl.logits);
+  float* dlog = (float*)(ws + pl.dlogits);
+  float* df = (float*)(ws + pl.df);
+  float* grad = (float*)(ws + pl.grad);
+  LCHK(gemm_f32_launch(f, F, 1, state + a.fc_w, 1, F, state + a.fc_b, logits, N, C, F, st));
+  LCHK(softmax_ce_launch(logits, labels, N, C, dlog, (float*)(ws + pl.rowloss), loss ? loss : (float*)(ws + pl.lossbuf),
+                         c->err, st));
+  // classifier backward: dW = dz^T f, db = sum dz, df = dz W
+  LCHK(gemm_f32_launch(dlog, 1, C, f, F, 1, nullptr, grad + a.fc_w, C, F, N, st));
+  LCHK(colsum_launch(dlog, N, C, grad + a.fc_b, st));
+  LCHK(gemm_f32_launch(dlog, C, 1, state + a.fc_w, F, 1, nullptr, df, N, F, C, st));
+  size_t gA = pl.gA, gB = pl.gB;
+  LCHK(avgpool_bwd_launch(prec, df, ws + gA, N, pl.Hf * pl.Wf, F, st));
+
+  auto W_d = [&](int li) { return (const char*)c->wd + (size_t)a.convs[li].wd * c->es; };
+  // BN backward of conv li: dz (with mask mz) -> dy written to `dy`
+  auto bn_back = [&](int li, size_t dz, size_t mz, size_t dy) -> int {
+    const ConvL& L = a.convs[li];
+    const ConvP& P = pl.cp[li];
+    int nblk = 0;
+    float* part = (float*)(ws + pl.part);
+    LCHK(bn_bwd_partial_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.rstd), P.M,
+                               L.cout, part, &nblk, st));
+    LCHK(bn_bwd_final_launch(part, nblk, P.M, L.cout, state + L.g, (float*)(ws + P.rstd), grad + L.g, grad + L.b,
+                             (float*)(ws + P.coef), st));
+    LCHK(bn_bwd_apply_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.coef), ws + dy,
+                             P.M, L.cout, st));
+    return 0;
+  };
+  auto wgrad = [&](int li, size_t dy) -> int {
+    const ConvL& L = a.convs[li];
+    const ConvP& P = pl.cp[li];
+    LCHK(launch_wgrad_full(prec, ws + dy, ws + P.x, grad + L.w, (float*)(ws + pl.wpart), pl.N, P.Hin, P.Win, L.cin_p,
+                           L.cin, P.Ho, P.Wo, L.cout, L.k, L.s, L.p, P.splits, P.pps, st));
+    return 0;
+  };
+  auto dgrad = [&](int li, size_t dy, size_t dx, int mode, size_t R, size_t Rm) -> int {
+    const ConvL& L = a.convs[li];
+    const ConvP& P = pl.cp[li];
+    LCHK(launch_dgrad(prec, ws + dy, W_d(li), ws + dx, pl.N, P.Hin, P.Win, L.cin_p, P.Ho, P.Wo, L.cout, L.k, L.s, L.p,
+                      mode, mode == 2 ? ws + R : nullptr, mode == 2 ? ws + Rm : nullptr, st));
+    return 0;
+  };
+
+  for (int bi = (int)a.blocks.size() - 1; bi >= 0; --bi) {
+    const BlockL& B = a.blocks[bi];
+    const BlockP& bp = pl.bp[bi];
+    // gA = gradient wrt the block output (before its ReLU mask)
+    if ((r = bn_back(B.c2, gA, bp.out, pl.gy))) return r;
+    if (B.ds >= 0 && (r = bn_back(B.ds, gA, bp.out, pl.gyd))) return r;
+    if ((r = wgrad(B.c2, pl.gy))) return r;
+    if ((r = dgrad(B.c2, pl.gy, pl.gz, 0, 0, 0))) return r;
+    if ((r = bn_back(B.c1, pl.gz, bp.z1, pl.gy))) return r;
+    if ((r = wgrad(B.c1, pl.gy))) return r;
+    if (B.ds >= 0) {
+      if ((r = dgrad(B.c1, pl.gy, gB, 0, 0, 0))) return r;
+      if ((r = wgrad(B.ds, pl.gyd))) return r;
+      if ((r = dgrad(B.ds, pl.gyd, gB, 1, 0, 0))) return r;
+    } else {
+      if ((r = dgrad(B.c1, pl.gy, gB, 2, gA, bp.out))) return r;
+    }
+    std::swap(gA, gB);
+  }
+  size_t gstem = gA;
+  if (a.imagenet) {
+    LCHK(maxpool_bwd_launch(prec, ws + gA, (const uint8_t*)(ws + pl.parg), ws + gB, N, pl.Hs, pl.Ws, a.convs[0].cout,
+                            pl.Hp, pl.Wp, st));
+    gstem = gB;
+  }
+  if ((r = bn_back(0, gstem, pl.zstem, pl.gy))) return r;
+  if ((r = wgrad(0, pl.gy))) return r;
+  LCHK(sgd_launch(state, grad, c->momentum, a.P, lr, c->cfg.momentum, c->cfg.weight_decay, st));
+  return RN18_OK;
+}
+
+// Host-side He-normal initial state (splitmix64 + Box-Muller).
+struct HostRng {
+  uint64_t s;
+  uint64_t next() {
+    uint64_t z = (s += 0x9E3779B97F4A7C15ull);
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+  }
+  double uniform() { return ((next() >> 11) + 0.5) * (1.0 / 9007199254740992.0); }
+  double normal() {
+    const double u1 = uniform(), u2 = uniform();
+    return sqrt(-2.0 * log(u1)) * cos(6.283185307179586 * u2);
+  }
+};
+
+void host_init(const Arch& a, uint64_t seed, std::vector<float>& st) {
+  st.assign(a.P + a.R, 0.f);
+  HostRng rng{seed};
+  for (const auto& L : a.convs) {
+    const double sd = sqrt(2.0 / (L.cin * L.k * L.k));
+    const long n = (long)L.cout * L.cin * L.k * L.k;
+    for (long i = 0; i < n; ++i) st[L.w + i] = (float)(rng.normal() * sd);
+    for (int i = 0; i < L.cout; ++i) { st[L.g + i] = 1.f; st[L.rv + i] = 1.f; }
+  }
+  const double sd = sqrt(2.0 / a.feat);
+  for (long i = 0; i < (long)a.classes * a.feat; ++i) st[a.fc_w + i] = (float)(rng.normal() * sd);
+}
+
+int check_cfg(const rn18_config* cfg) {
+  if (!cfg) return fail(RN18_EINVAL, "config is NULL");
+  if (cfg->arch < 0 || cfg->arch > 2) return fail(RN18_EINVAL, "unknown arch %d", cfg->arch);
+  if (cfg->prec < 0 || cfg->prec > 1) return fail(RN18_EINVAL, "unknown precision %d", cfg->prec);
+  if (cfg->num_classes < 1) return fail(RN18_EINVAL, "num_classes must be >= 1");
+  if (!isfinite(cfg->momentum) || !isfinite(cfg->weight_decay) || !isfinite(cfg->bn_eps) ||
+      !isfinite(cfg->bn_momentum) || cfg->bn_eps < 0.f)
+    return fail(RN18_EINVAL, "non-finite or negative hyper-parameter");
+  return RN18_OK;
+}
+
+}  // namespace
+
+struct rn18_ctx {
+  Ctx c;
+};
+
+extern "C" {
+
+const char* rn18_last_error(void) { return g_err.c_str(); }
+
+size_t rn18_state_floats(const rn18_config* cfg, size_t* n_trainable) {
+  Arch a;
+  if (!cfg || !build_arch(*cfg, &a)) return 0;
+  if (n_trainable) *n_trainable = (size_t)a.P;
+  return (size_t)(a.P + a.R);
+}
+
+int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* state_out, rn18_ctx** out) {
+  if (!out) return fail(RN18_EINVAL, "ctx out-pointer is NULL");
+  *out = nullptr;
+  int r = check_cfg(cfg);
+  if (r) return r;
+  if (state_out && !aligned16(state_out)) return fail(RN18_EINVAL, "state must be 16-byte aligned");
+  rn18_ctx* h = new (std::nothrow) rn18_ctx();
+  if (!h) return fail(RN18_ENOMEM, "out of host memory");
+  Ctx& c = h->c;
+  c.cfg = *cfg;
+  build_arch(*cfg, &c.arch);
+  c.prec = cfg->prec;
+  c.es = cfg->prec == RN18_BF16 ? 2 : 4;
+  c.stream = (hipStream_t)hip_stream;
+  const Arch& a = c.arch;
+  auto bail = [&](int code, const char* what) {
+    if (c.momentum) (void)hipFree(c.momentum);
+    if (c.wf) (void)hipFree(c.wf);
+    if (c.wd) (void)hipFree(c.wd);
+    if (c.tab) (void)hipFree(c.tab);
+    if (c.err) (void)hipFree(c.err);
+    delete h;
+    return fail(code, "%s", what);
+  };
+  if (hipMalloc(&c.momentum, a.P * 4) != hipSuccess) return bail(RN18_ENOMEM, "momentum allocation failed");
+  if (hipMalloc(&c.wf, a.wf_total * c.es + 16) != hipSuccess) return bail(RN18_ENOMEM, "weight shadow allocation failed");
+  if (hipMalloc(&c.wd, a.wd_total * c.es + 16) != hipSuccess) return bail(RN18_ENOMEM, "weight shadow allocation failed");
+  if (hipMalloc(&c.err, 256) != hipSuccess) return bail(RN18_ENOMEM, "flag allocation failed");
+  std::vector<RepackEntry> tab;
+  long pre = 0;
+  for (const auto& L : a.convs) {
+    RepackEntry e;
+    e.src = L.w; e.dst_f = L.wf; e.dst_d = L.wd;
+    e.Cout = L.cout; e.Cin = L.cin; e.Cin_p = L.cin_p; e.KHW = L.k * L.k;
+    e.n = (long)L.cout * L.k * L.k * L.cin_p;
+    e.nprefix = pre;
+    pre += e.n;
+    tab.push_back(e);
+  }
+  c.ntab = (int)tab.size();
+  if (hipMalloc(&c.tab, sizeof(RepackEntry) * tab.size()) != hipSuccess) return bail(RN18_ENOMEM, "table allocation failed");
+  if (hipMemcpy(c.tab, tab.data(), sizeof(RepackEntry) * tab.size(), hipMemcpyHostToDevice) != hipSuccess)
+    return bail(RN18_EHIP, "table upload failed");
+  if (fill_zero_launch(c.momentum, a.P * 4, c.stream) || fill_zero_launch(c.err, 256, c.stream))
+    return bail(RN18_EHIP, "initial fill failed");
+  if (state_out) {
+    std::vector<float> host;
+    host_init(a, seed, host);
+    if (hipMemcpyAsync(state_out, host.data(), host.size() * 4, hipMemcpyHostToDevice, c.stream) != hipSuccess ||
+        hipStreamSynchronize(c.stream) != hipSuccess)
+      return bail(RN18_EHIP, "state upload failed");
+  }
+  *out = h;
+  return RN18_OK;
+}
+
+size_t rn18_workspace_bytes(rn18_ctx* h, int N, int H, int W) {
+  if (!h) return 0;
+  const Plan* pl = nullptr;
+  if (get_plan(&h->c, N, H, W, &pl)) return 0;
+  return pl->total;
+}
+
+int rn18_set_workspace(rn18_ctx* h, void* dev, size_t bytes) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  if (!dev || !bytes) return fail(RN18_EINVAL, "workspace pointer or size is 0");
+  if (((uintptr_t)dev & 255u) != 0) return fail(RN18_EINVAL, "workspace must be 256-byte aligned");
+  Ctx& c = h->c;
+  if (c.ws_owned && c.ws) {
+    HIPCHK(hipStreamSynchronize(c.stream));
+    HIPCHK(hipFree(c.ws));
+  }
+  c.ws = dev;
+  c.ws_bytes = bytes;
+  c.ws_owned = false;
+  return RN18_OK;
+}
+
+int rn18_train_step(rn18_ctx* h, float* state, const float* images, const int32_t* labels, int N, int H, int W,
+                    float lr, float* loss) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  if (!state || !images || !labels) return fail(RN18_EINVAL, "state, images and labels must be non-NULL");
+  if (!aligned16(state) || !aligned16(images) || (loss && ((uintptr_t)loss & 3u)))
+    return fail(RN18_EINVAL, "misaligned pointer");
+  if (!isfinite(lr)) return fail(RN18_EINVAL, "lr is not finite");
+  Ctx& c = h->c;
+  const Plan* pl = nullptr;
+  int r = get_plan(&c, N, H, W, &pl);
+  if (r) return r;
+  if ((r = ensure_ws(&c, *pl))) return r;
+  return run_train(&c, *pl, state, images, labels, lr, loss);
+}
+
+int rn18_eval_logits(rn18_ctx* h, const float* state, const float* images, int N, int H, int W, float* logits) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  if (!state || !images || !logits) return fail(RN18_EINVAL, "state, images and logits must be non-NULL");
+  if (!aligned16(state) || !aligned16(images)) return fail(RN18_EINVAL, "misaligned pointer");
+  Ctx& c = h->c;
+  const Plan* pl = nullptr;
+  int r = get_plan(&c, N, H, W, &pl);
+  if (r) return r;
+  if ((r = ensure_ws(&c, *pl))) return r;
+  if ((r = run_forward(&c, *pl, state, nullptr, images, false))) return r;
+  char* ws = (char*)c.ws;
+  const Arch& a = c.arch;
+  LCHK(gemm_f32_launch((float*)(ws + pl->f), a.feat, 1, state + a.fc_w, 1, a.feat, state + a.fc_b, logits, N,
+                       a.classes, a.feat, c.stream));
+  return RN18_OK;
+}
+
+int ps_dual_merge(float* state, const float* g_small, const float* g_large, size_t n, float factor, void* hip_stream) {
+  if (!state || !g_small || !g_large) return fail(RN18_EINVAL, "NULL pointer");
+  if (!aligned16(state) || !aligned16(g_small) || !aligned16(g_large)) return fail(RN18_EINVAL, "misaligned pointer");
+  if (!isfinite(factor)) return fail(RN18_EINVAL, "factor is not finite");
+  if ((const float*)state == g_small || (const float*)state == g_large)
+    return fail(RN18_EINVAL, "state must not alias an update vector");
+  if (n == 0) return RN18_OK;
+  LCHK(merge_launch(state, g_small, g_large, (long)n, factor, (hipStream_t)hip_stream));
+  return RN18_OK;
+}
+
+int ps_worker_delta(const float* pulled, const float* local, float* delta, size_t n, void* hip_stream) {
+  if (!pulled || !local || !delta) return fail(RN18_EINVAL, "NULL pointer");
+  if (!aligned16(pulled) || !aligned16(local) || !aligned16(delta)) return fail(RN18_EINVAL, "misaligned pointer");
+  if (n == 0) return RN18_OK;
+  LCHK(delta_launch(pulled, local, delta, (long)n, (hipStream_t)hip_stream));
+  return RN18_OK;
+}
+
+int rn18_sync_status(rn18_ctx* h) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  Ctx& c = h->c;
+  unsigned e = 0;
+  HIPCHK(hipMemcpyAsync(&e, c.err, 4, hipMemcpyDeviceToHost, c.stream));
+  HIPCHK(hipStreamSynchronize(c.stream));
+  if (e) {
+    LCHK(fill_zero_launch(c.err, 4, c.stream));
+    HIPCHK(hipStreamSynchronize(c.stream));
+  }
+  if (e & DEVERR_LABEL) return fail(RN18_ELABEL, "a label was outside [0, num_classes)");
+  if (e & DEVERR_NONFINITE) return fail(RN18_ENONFINITE, "the loss was not finite");
+  return RN18_OK;
+}
+
+int rn18_get_momentum(rn18_ctx* h, float* dst) {
+  if (!h || !dst) return fail(RN18_EINVAL, "NULL pointer");
+  HIPCHK(hipMemcpyAsync(dst, h->c.momentum, h->c.arch.P * 4, hipMemcpyDeviceToDevice, h->c.stream));
+  return RN18_OK;
+}
+
+int rn18_set_momentum(rn18_ctx* h, const float* src) {
+  if (!h || !src) return fail(RN18_EINVAL, "NULL pointer");
+  HIPCHK(hipMemcpyAsync(h->c.momentum, src, h->c.arch.P * 4, hipMemcpyDeviceToDevice, h->c.stream));
+  return RN18_OK;
+}
+
+void rn18_destroy(rn18_ctx* h) {
+  if (!h) return;
+  Ctx& c = h->c;
+  (void)hipStreamSynchronize(c.stream);
+  if (c.momentum) (void)hipFree(c.momentum);
+  if (c.wf) (void)hipFree(c.wf);
+  if (c.wd) (void)hipFree(c.wd);
+  if (c.tab) (void)hipFree(c.tab);
+  if (c.err) (void)hipFree(c.err);
+  if (c.ws_owned && c.ws) (void)hipFree(c.ws);
+  delete h;
+}
+
+// ---------------------------------------------------------------------------
+// Single-operator entry points
+// ---------------------------------------------------------------------------
+static int op_check(int prec, int N, int H, int W, int Cin, int Cout, int k, int s, int p, int* Ho, int* Wo) {
+  if (prec != RN18_FP32 && prec != RN18_BF16) return fail(RN18_EINVAL, "bad precision");
+  const int vw = prec == RN18_BF16 ? 8 : 4;
+  if (N < 1 || H < 1 || W < 1 || Cin < 1 || Cout < 1 || k < 1 || s < 1 || p < 0)
+    return fail(RN18_EINVAL, "non-positive size");
+  if (Cin % vw || Cout % vw) return fail(RN18_EINVAL, "channel counts must be multiples of %d", vw);
+  if (s > 2) return fail(RN18_EINVAL, "stride must be 1 or 2");
+  *Ho = out_size(H, k, s, p);
+  *Wo = out_size(W, k, s, p);
+  if (*Ho < 1 || *Wo < 1) return fail(RN18_EINVAL, "empty output");
+  if ((long)N * H * W * (Cin > Cout ? Cin : Cout) >= (1l << 31)) return fail(RN18_EINVAL, "tensor too large");
+  return RN18_OK;
+}
+
+int rn18op_conv2d_fwd(int prec, const void* x, const void* w, void* y, int N, int H, int W, int Cin, int Cout, int k,
+                      int s, int p, void* stream) {
+  int Ho, Wo;
+  int r = op_check(prec, N, H, W, Cin, Cout, k, s, p, &Ho, &Wo);
+  if (r) return r;
+  if (!x || !w || !y || !aligned16(x) || !aligned16(w) || !aligned16(y)) return fail(RN18_EINVAL, "bad pointer");
+  ConvGather g = gather_fwd(x, w, y, N, H, W, Cin, Ho, Wo, Cout, k, s, p);
+  LCHK(conv_gather_launch(prec, g, (hipStream_t)stream));
+  return RN18_OK;
+}
+
+int rn18op_conv2d_dgrad(int prec, const void* dy, const void* w, void* dx, int N, int H, int W, int Cin, int Cout,
+                        int k, int s, int p, void* stream) {
+  int Ho, Wo;
+  int r = op_check(prec, N, H, W, Cin, Cout, k, s, p, &Ho, &Wo);
+  if (r) return r;
+  if (!dy || !w || !dx || !aligned16(dy) || !aligned16(w) || !aligned16(dx)) return fail(RN18_EINVAL, "bad pointer");
+  LCHK(launch_dgrad(prec, dy, w, dx, N, H, W, Cin, Ho, Wo, Cout, k, s, p, 0, nullptr, nullptr, (hipStream_t)stream));
+  return RN18_OK;
+}
+
+size_t rn18op_conv2d_wgrad_workspace(int prec, int N, int H, int W, int Cin, int Cout, int k, int s, int p) {
+  int Ho, Wo;
+  if (op_check(prec, N, H, W, Cin, Cout, k, s, p, &Ho, &Wo)) return 0;
+  int pps;
+  const int splits = conv_wgrad_splits(prec, Cout, k * k * Cin, (long)N * Ho * Wo, &pps);
+  return (size_t)splits * Cout * k * k * Cin * 4;
+}
+
+int rn18op_conv2d_wgrad(int prec, const void* dy, const void* x, float* dw, int N, int H, int W, int Cin, int cin_real,
+                        int Cout, int k, int s, int p, void* ws, size_t ws_bytes, void* stream) {
+  int Ho, Wo;
+  int r = op_check(prec, N, H, W, Cin, Cout, k, s, p, &Ho, &Wo);
+  if (r) return r;
+  if (cin_real < 1 || cin_real > Cin) return fail(RN18_EINVAL, "cin_real must be in [1, Cin]");
+  if (!dy || !x || !dw || !ws || !aligned16(dy) || !aligned16(x) || !aligned16(ws)) return fail(RN18_EINVAL, "bad pointer");
+  int pps;
+  const int splits = conv_wgrad_splits(prec, Cout, k * k * Cin, (long)N * Ho * Wo, &pps);
+  if (ws_bytes < (size_t)splits * Cout * k * k * Cin * 4) return fail(RN18_ENOMEM, "workspace too small");
+  LCHK(launch_wgrad_full(prec, dy, x, dw, (float*)ws, N, H, W, Cin, cin_real, Ho, Wo, Cout, k, s, p, splits, pps,
+                         (hipStream_t)stream));
+  return RN18_OK;
+}
+
+int rn18op_maxpool_fwd(int prec, const void* x, void* y, uint8_t* arg, int N, int H, int W, int C, void* stream) {
+  int Ho, Wo;
+  int r = op_check(prec, N, H, W, C, C, 3, 2, 1, &Ho, &Wo);
+  if (r) return r;
+  if (!x || !y || !arg || !aligned16(x) || !aligned16(y)) return fail(RN18_EINVAL, "bad pointer");
+  LCHK(maxpool_fwd_launch(prec, x, y, arg, N, H, W, C, Ho, Wo, (hipStream_t)stream));
+  return RN18_OK;
+}
+
+int rn18op_maxpool_bwd(int prec, const void* dy, const uint8_t* arg, void* dx, int N, int H, int W, int C,
+                       void* stream) {
+  int Ho, Wo;
+  int r = op_check(prec, N, H, W, C, C, 3, 2, 1, &Ho, &Wo);
+  if (r) return r;
+  if (!dy || !dx || !arg || !aligned16(dy) || !aligned16(dx)) return fail(RN18_EINVAL, "bad pointer");
+  LCHK(maxpool_bwd_launch(prec, dy, arg, dx, N, H, W, C, Ho, Wo, (hipStream_t)stream));
+  return RN18_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,75 @@
+// Shared device/host helpers for the gfx950 ResNet-18 training-step library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace rn18 {
+
+// bf16 is stored as its raw 16-bit pattern; MFMA operands reinterpret 16-byte
+// chunks as vectors of __bf16.
+typedef uint16_t bf16_t;
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+
+enum Prec { PREC_F32 = 0, PREC_BF16 = 1 };
+
+// Round-to-nearest-even float -> bf16 on the binary32 bit pattern; NaN stays
+// a quiet NaN.
+__device__ __host__ inline bf16_t f2bf(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+__device__ __host__ inline float bf2f(bf16_t b) {
+  return __builtin_bit_cast(float, ((uint32_t)b) << 16);
+}
+
+// Element-type traits: a 16-byte chunk holds VW elements.
+template <typename T> struct TT;
+template <> struct TT<float> {
+  static constexpr int VW = 4;
+  __device__ static inline float to_f(float v) { return v; }
+  __device__ static inline float from_f(float v) { return v; }
+};
+template <> struct TT<bf16_t> {
+  static constexpr int VW = 8;
+  __device__ static inline float to_f(bf16_t v) { return bf2f(v); }
+  __device__ static inline bf16_t from_f(float v) { return f2bf(v); }
+};
+
+// Unpack / pack a 16-byte chunk (uint4) to / from VW floats.
+template <typename T> __device__ inline void unpack(const uint4& q, float* f);
+template <> __device__ inline void unpack<float>(const uint4& q, float* f) {
+  f[0] = __builtin_bit_cast(float, q.x); f[1] = __builtin_bit_cast(float, q.y);
+  f[2] = __builtin_bit_cast(float, q.z); f[3] = __builtin_bit_cast(float, q.w);
+}
+template <> __device__ inline void unpack<bf16_t>(const uint4& q, float* f) {
+  uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __builtin_bit_cast(float, w[i] << 16);
+    f[2 * i + 1] = __builtin_bit_cast(float, w[i] & 0xffff0000u);
+  }
+}
+template <typename T> __device__ inline uint4 pack(const float* f);
+template <> __device__ inline uint4 pack<float>(const float* f) {
+  uint4 q;
+  q.x = __builtin_bit_cast(uint32_t, f[0]); q.y = __builtin_bit_cast(uint32_t, f[1]);
+  q.z = __builtin_bit_cast(uint32_t, f[2]); q.w = __builtin_bit_cast(uint32_t, f[3]);
+  return q;
+}
+template <> __device__ inline uint4 pack<bf16_t>(const float* f) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(f[2 * i]) | ((uint32_t)f2bf(f[2 * i + 1]) << 16);
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Sticky device error bits.
+enum DevErr { DEVERR_LABEL = 1, DEVERR_NONFINITE = 2 };
+
+inline int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
+
+}  // namespace rn18

@@ -1,0 +1,467 @@
+// Convolutions of the ResNet-18 training step as implicit GEMMs on CDNA4 MFMA.
+//
+// Layout: activations NHWC (channels innermost), weights [Cout][KH*KW][Cin]
+// for the forward pass and [Cin][KH*KW][Cout] for the data gradient; Cin is
+// padded to a multiple of the 16-byte vector width (4 fp32 / 8 bf16).
+//
+// One kernel family ("gather") computes the forward pass and the data
+// gradient. A GEMM row is an output pixel, a GEMM column an output channel,
+// and the reduction runs over (tap, input channel). The data gradient of a
+// stride-1 conv is a forward conv of dY with the taps mirrored; a stride-2
+// conv's data gradient is split by the parity of the output pixel into four
+// sub-convolutions, each with only its own taps, so no zero-inserted MACs are
+// done (the tap arithmetic is parameterised: offset and step per axis).
+//
+// Tiles of K are staged through LDS as rows of 128 bytes (one or more 16-byte
+// chunks of consecutive channels of one tap). Each MFMA lane supplies one
+// 16-byte chunk of A and the matching chunk of B; the order of the K index
+// inside an MFMA does not change the dot product, so fp32 (16x16x4) and bf16
+// (16x16x32) share the LDS layout and the loaders.
+//
+// The weight gradient reduces over pixels. Its tiles are loaded as 16-byte
+// channel chunks of consecutive pixels and transposed in registers so that the
+// LDS rows hold consecutive pixels of one channel; partial sums of a split of
+// the pixel range go to a scratch buffer that is summed in a fixed order
+// (deterministic, no float atomics).
+#include "kernels.h"
+
+namespace rn18 {
+
+namespace {
+
+constexpr int RSTR = 9;  // LDS row stride in 16-byte units: 8 data chunks + 1 pad
+
+__device__ inline int xcd_remap(int b, int nb) {
+  // Blocks are dealt round-robin to the 8 XCDs; give each XCD a contiguous
+  // range of logical tiles so neighbouring tiles share its L2.
+  int per = nb >> 3, rem = nb & 7;
+  int x = b & 7, r = b >> 3;
+  return x * per + (x < rem ? x : rem) + r;
+}
+
+template <typename T> struct Mma;
+template <> struct Mma<bf16_t> {
+  static constexpr int SUB = 1;
+  __device__ static inline void run(floatx4_t& acc, const uint4& a, const uint4& b, int) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                  __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+  }
+};
+template <> struct Mma<float> {
+  static constexpr int SUB = 4;
+  __device__ static inline float el(const uint4& q, int t) {
+    return __builtin_bit_cast(float, t == 0 ? q.x : t == 1 ? q.y : t == 2 ? q.z : q.w);
+  }
+  __device__ static inline void run(floatx4_t& acc, const uint4& a, const uint4& b, int t) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(el(a, t), el(b, t), acc, 0, 0, 0);
+  }
+};
+
+// One 128-byte K stage: two groups of four 16-byte chunks (one per lane group).
+template <typename T, int FM, int FN>
+__device__ inline void mma_stage(floatx4_t (&acc)[FM][FN], const uint4* As, const uint4* Bs,
+                                 int arow0, int brow0, int lane) {
+#pragma unroll
+  for (int kg = 0; kg < 2; ++kg) {
+    const int ch = kg * 4 + (lane >> 4);
+    uint4 a[FM], b[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) a[i] = As[(arow0 + i * 16 + (lane & 15)) * RSTR + ch];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) b[j] = Bs[(brow0 + j * 16 + (lane & 15)) * RSTR + ch];
+#pragma unroll
+    for (int t = 0; t < Mma<T>::SUB; ++t)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], a[i], b[j], t);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Gather conv (forward and data gradient)
+// ---------------------------------------------------------------------------
+template <typename T, int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(256) void conv_gather_kernel(ConvGather g) {
+  constexpr int VW = TT<T>::VW;
+  constexpr int KT = 128 / (int)sizeof(T);
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  constexpr int AQ = (BM + 31) / 32, BQ = (BN + 31) / 32;
+  constexpr int STAGE = (BM + BN) * RSTR;
+  constexpr int CSTR = BN + 4;
+  constexpr int SM_LOOP = 2 * STAGE;
+  constexpr int SM_EPI = (BM * CSTR + 3) / 4;
+  __shared__ uint4 smem[SM_LOOP > SM_EPI ? SM_LOOP : SM_EPI];
+  static_assert(WGM * WGN == 4, "4 waves");
+  static_assert(FM >= 1 && FN >= 1, "wave tile >= 16x16");
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int tiles_n = (g.Cols + BN - 1) / BN;
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int m0 = (t / tiles_n) * BM, n0 = (t % tiles_n) * BN;
+
+  const T* __restrict__ A = (const T*)g.A;
+  const T* __restrict__ B = (const T*)g.B;
+  const int c = tid & 7, r0 = tid >> 3;
+  const int HWm = g.Hm * g.Wm;
+
+  int a_img[AQ], a_hb[AQ], a_wb[AQ];
+  bool a_ok[AQ];
+#pragma unroll
+  for (int q = 0; q < AQ; ++q) {
+    int m = m0 + r0 + 32 * q;
+    a_ok[q] = m < g.M;
+    int mm = a_ok[q] ? m : 0;
+    int n = mm / HWm, rem = mm - n * HWm;
+    int i = rem / g.Wm, j = rem - i * g.Wm;
+    a_img[q] = n * g.Hin * g.Win;
+    a_hb[q] = i * g.is - g.ip;
+    a_wb[q] = j * g.is - g.ip;
+  }
+
+  uint4 ra[AQ], rb[BQ];
+  auto load = [&](int k0) {
+    const int k = k0 + c * VW;
+    const bool kok = k < g.K;
+    const int tap = kok ? k / g.Cin : 0;
+    const int ci = k - tap * g.Cin;
+    const int th = tap / g.ntw, tw = tap - th * g.ntw;
+    const int dh = g.dh0 + th * g.dhs, dw = g.dw0 + tw * g.dws;
+    const int wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
+#pragma unroll
+    for (int q = 0; q < AQ; ++q) {
+      const int hi = a_hb[q] + dh, wi = a_wb[q] + dw;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (kok && a_ok[q] && (unsigned)hi < (unsigned)g.Hin && (unsigned)wi < (unsigned)g.Win)
+        v = *(const uint4*)(A + (long)(a_img[q] + hi * g.Win + wi) * g.Cin + ci);
+      ra[q] = v;
+    }
+#pragma unroll
+    for (int q = 0; q < BQ; ++q) {
+      const int col = n0 + r0 + 32 * q;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (kok && col < g.Cols && r0 + 32 * q < BN) v = *(const uint4*)(B + ((long)col * g.KHW + wt) * g.Cin + ci);
+      rb[q] = v;
+    }
+  };
+  auto store = [&](int buf) {
+    uint4* As = smem + buf * STAGE;
+    uint4* Bs = As + BM * RSTR;
+#pragma unroll
+    for (int q = 0; q < AQ; ++q)
+      if (r0 + 32 * q < BM) As[(r0 + 32 * q) * RSTR + c] = ra[q];
+#pragma unroll
+    for (int q = 0; q < BQ; ++q)
+      if (r0 + 32 * q < BN) Bs[(r0 + 32 * q) * RSTR + c] = rb[q];
+  };
+
+  floatx4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int S = (g.K + KT - 1) / KT;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int s = 0; s < S; ++s) {
+    if (s + 1 < S) load((s + 1) * KT);
+    const uint4* As = smem + (s & 1) * STAGE;
+    mma_stage<T, FM, FN>(acc, As, As + BM * RSTR, wm * WTM, wn * WTN, lane);
+    if (s + 1 < S) store((s + 1) & 1);
+    __syncthreads();
+  }
+
+  // Epilogue through LDS so that global stores are 16-byte row chunks.
+  float* Cs = (float*)smem;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        Cs[(wm * WTM + i * 16 + 4 * (lane >> 4) + r) * CSTR + wn * WTN + j * 16 + (lane & 15)] = acc[i][j][r];
+  __syncthreads();
+
+  constexpr int CPR = BN / VW;
+  T* __restrict__ Cg = (T*)g.C;
+  for (int idx = tid; idx < BM * CPR; idx += 256) {
+    const int row = idx / CPR, cc = idx - row * CPR;
+    const int m = m0 + row, col = n0 + cc * VW;
+    if (m >= g.M || col >= g.Cols) continue;
+    const int n = m / HWm, rem = m - n * HWm;
+    const int i = rem / g.Wm, j = rem - i * g.Wm;
+    const long off = ((long)(n * g.Hout + i * g.os + g.oph) * g.Wout + j * g.os + g.opw) * g.Cols + col;
+    float v[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) v[e] = Cs[row * CSTR + cc * VW + e];
+    if (g.mode == 1) {
+      float o[VW];
+      unpack<T>(*(const uint4*)(Cg + off), o);
+#pragma unroll
+      for (int e = 0; e < VW; ++e) v[e] += o[e];
+    } else if (g.mode == 2) {
+      float rr[VW], mk[VW];
+      unpack<T>(*(const uint4*)((const T*)g.R + off), rr);
+      unpack<T>(*(const uint4*)((const T*)g.Rm + off), mk);
+#pragma unroll
+      for (int e = 0; e < VW; ++e) v[e] += mk[e] > 0.f ? rr[e] : 0.f;
+    }
+    *(uint4*)(Cg + off) = pack<T>(v);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Weight gradient
+// ---------------------------------------------------------------------------
+template <typename T> struct Tr;
+template <> struct Tr<bf16_t> {
+  // 8 pixels x 8 channels (bf16) -> 8 channels x 8 pixels
+  __device__ static inline void run(const uint4 (&in)[8], uint4 (&out)[8]) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      uint32_t x[8];
+#pragma unroll
+      for (int p = 0; p < 8; ++p) x[p] = d == 0 ? in[p].x : d == 1 ? in[p].y : d == 2 ? in[p].z : in[p].w;
+      uint32_t lo[4], hi[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        lo[q] = (x[2 * q] & 0xffffu) | (x[2 * q + 1] << 16);
+        hi[q] = (x[2 * q] >> 16) | (x[2 * q + 1] & 0xffff0000u);
+      }
+      out[2 * d] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      out[2 * d + 1] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+    }
+  }
+};
+template <> struct Tr<float> {
+  __device__ static inline void run(const uint4 (&in)[4], uint4 (&out)[4]) {
+    out[0] = make_uint4(in[0].x, in[1].x, in[2].x, in[3].x);
+    out[1] = make_uint4(in[0].y, in[1].y, in[2].y, in[3].y);
+    out[2] = make_uint4(in[0].z, in[1].z, in[2].z, in[3].z);
+    out[3] = make_uint4(in[0].w, in[1].w, in[2].w, in[3].w);
+  }
+};
+
+template <typename T, int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(256) void conv_wgrad_kernel(ConvWgrad g) {
+  constexpr int VW = TT<T>::VW;
+  constexpr int KTP = 128 / (int)sizeof(T);  // pixels per stage
+  constexpr int PG = KTP / VW;               // pixel groups per stage (8)
+  constexpr int NA = PG * (BM / VW), NB = PG * (BN / VW);
+  constexpr int NBLK = (NA + NB + 255) / 256;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  constexpr int STAGE = (BM + BN) * RSTR;
+  __shared__ uint4 smem[2 * STAGE];
+  static_assert(WGM * WGN == 4, "4 waves");
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int tiles_n = (g.Kcols + BN - 1) / BN;
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int co0 = (t / tiles_n) * BM, k0 = (t % tiles_n) * BN;
+  const int split = blockIdx.y;
+  const int p_begin = split * g.pix_per_split;
+  const int p_end = min(g.Mpix, p_begin + g.pix_per_split);
+  const int HWo = g.Ho * g.Wo;
+
+  const T* __restrict__ DY = (const T*)g.DY;
+  const T* __restrict__ X = (const T*)g.X;
+
+  uint4 rv[NBLK][VW];
+  auto load = [&](int p0) {
+#pragma unroll
+    for (int u = 0; u < NBLK; ++u) {
+      const int b = tid + 256 * u;
+      if (b < NA) {
+        const int cg = b % (BM / VW), pg = b / (BM / VW);
+        const int co = co0 + cg * VW;
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          const int p = p0 + pg * VW + e;
+          uint4 v = make_uint4(0, 0, 0, 0);
+          if (p < p_end && co < g.Cout) v = *(const uint4*)(DY + (long)p * g.Cout + co);
+          rv[u][e] = v;
+        }
+      } else if (b < NA + NB) {
+        const int bb = b - NA;
+        const int cc = bb % (BN / VW), pg = bb / (BN / VW);
+        const int kc = k0 + cc * VW;
+        const bool kok = kc < g.Kcols;
+        const int tap = kok ? kc / g.Cin : 0;
+        const int ci = kc - tap * g.Cin;
+        const int kh = tap / g.KW, kw = tap - kh * g.KW;
+        int p = p0 + pg * VW;
+        const int pc = p < g.Mpix ? p : 0;
+        int n = pc / HWo, rem = pc - n * HWo;
+        int ho = rem / g.Wo, wo = rem - ho * g.Wo;
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          uint4 v = make_uint4(0, 0, 0, 0);
+          const int hi = ho * g.stride - g.pad + kh, wi = wo * g.stride - g.pad + kw;
+          if (kok && p + e < p_end && (unsigned)hi < (unsigned)g.H && (unsigned)wi < (unsigned)g.W)
+            v = *(const uint4*)(X + ((long)(n * g.H + hi) * g.W + wi) * g.Cin + ci);
+          rv[u][e] = v;
+          if (++wo == g.Wo) { wo = 0; if (++ho == g.Ho) { ho = 0; ++n; } }
+        }
+      }
+    }
+  };
+  auto store = [&](int buf) {
+    uint4* As = smem + buf * STAGE;
+    uint4* Bs = As + BM * RSTR;
+#pragma unroll
+    for (int u = 0; u < NBLK; ++u) {
+      const int b = tid + 256 * u;
+      uint4 o[VW];
+      if (b < NA) {
+        const int cg = b % (BM / VW), pg = b / (BM / VW);
+        Tr<T>::run(rv[u], o);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) As[(cg * VW + e) * RSTR + pg] = o[e];
+      } else if (b < NA + NB) {
+        const int bb = b - NA;
+        const int cc = bb % (BN / VW), pg = bb / (BN / VW);
+        Tr<T>::run(rv[u], o);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) Bs[(cc * VW + e) * RSTR + pg] = o[e];
+      }
+    }
+  };
+
+  floatx4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int S = p_end > p_begin ? (p_end - p_begin + KTP - 1) / KTP : 0;
+  if (S > 0) {
+    load(p_begin);
+    store(0);
+  }
+  __syncthreads();
+  for (int s = 0; s < S; ++s) {
+    if (s + 1 < S) load(p_begin + (s + 1) * KTP);
+    const uint4* As = smem + (s & 1) * STAGE;
+    mma_stage<T, FM, FN>(acc, As, As + BM * RSTR, wm * WTM, wn * WTN, lane);
+    if (s + 1 < S) store((s + 1) & 1);
+    __syncthreads();
+  }
+
+  float* __restrict__ P = g.P + (long)split * g.Cout * g.Kcols;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int kc = k0 + wn * WTN + j * 16 + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int co = co0 + wm * WTM + i * 16 + 4 * (lane >> 4) + r;
+        if (co < g.Cout && kc < g.Kcols) P[(long)co * g.Kcols + kc] = acc[i][j][r];
+      }
+    }
+}
+
+__global__ void wgrad_reduce_kernel(const float* __restrict__ P, int splits, int Cout, int KHW, int Cin,
+                                    int Cin_real, float* __restrict__ out) {
+  const long total = (long)Cout * KHW * Cin;
+  const long stride = (long)Cout * KHW * Cin;
+  for (long idx = blockIdx.x * (long)blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
+    const int ci = (int)(idx % Cin);
+    if (ci >= Cin_real) continue;
+    const long rest = idx / Cin;
+    const int tap = (int)(rest % KHW);
+    const int co = (int)(rest / KHW);
+    float s = 0.f;
+    for (int z = 0; z < splits; ++z) s += P[z * stride + idx];
+    out[((long)co * Cin_real + ci) * KHW + tap] = s;
+  }
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN>
+int launch_gather(const ConvGather& g, hipStream_t s) {
+  const int tiles = ceil_div(g.M, BM) * ceil_div(g.Cols, BN);
+  hipLaunchKernelGGL((conv_gather_kernel<T, BM, BN, WGM, WGN>), dim3(tiles), dim3(256), 0, s, g);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+template <typename T>
+int gather_dispatch(const ConvGather& g, hipStream_t s) {
+  if (g.Cols <= 16) return launch_gather<T, 64, 16, 4, 1>(g, s);
+  if (g.Cols <= 64) {
+    if ((long)ceil_div(g.M, 128) >= 512) return launch_gather<T, 128, 64, 2, 2>(g, s);
+    return launch_gather<T, 64, 64, 2, 2>(g, s);
+  }
+  if ((long)ceil_div(g.M, 128) * ceil_div(g.Cols, 128) >= 512) return launch_gather<T, 128, 128, 2, 2>(g, s);
+  return launch_gather<T, 64, 64, 2, 2>(g, s);
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN>
+int launch_wgrad(const ConvWgrad& g, hipStream_t s) {
+  const int tiles = ceil_div(g.Cout, BM) * ceil_div(g.Kcols, BN);
+  hipLaunchKernelGGL((conv_wgrad_kernel<T, BM, BN, WGM, WGN>), dim3(tiles, g.splits), dim3(256), 0, s, g);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+void wgrad_tile(int Cout, int* bm, int* bn) {
+  if (Cout <= 16) { *bm = 16; *bn = 64; }
+  else if (Cout <= 64) { *bm = 64; *bn = 64; }
+  else { *bm = 128; *bn = 128; }
+}
+
+template <typename T>
+int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
+  if (g.Cout <= 16) return launch_wgrad<T, 16, 64, 1, 4>(g, s);
+  if (g.Cout <= 64) return launch_wgrad<T, 64, 64, 2, 2>(g, s);
+  return launch_wgrad<T, 128, 128, 2, 2>(g, s);
+}
+
+}  // namespace
+
+int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s) {
+  if (g.M <= 0) return 0;
+  return prec == PREC_BF16 ? gather_dispatch<bf16_t>(g, s) : gather_dispatch<float>(g, s);
+}
+
+int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split) {
+  const int ktp = prec == PREC_BF16 ? 64 : 32;
+  int bm, bn;
+  wgrad_tile(Cout, &bm, &bn);
+  const long tiles = (long)ceil_div(Cout, bm) * ceil_div(Kcols, bn);
+  long splits = (1024 + tiles - 1) / tiles;
+  const long per_split_bytes = (long)Cout * Kcols * 4;
+  long max_by_bytes = (32l << 20) / per_split_bytes;
+  if (max_by_bytes < 1) max_by_bytes = 1;
+  long max_by_len = Mpix / (ktp * 8);
+  if (max_by_len < 1) max_by_len = 1;
+  if (splits > max_by_bytes) splits = max_by_bytes;
+  if (splits > max_by_len) splits = max_by_len;
+  if (splits < 1) splits = 1;
+  long pps = (Mpix + splits - 1) / splits;
+  pps = (pps + ktp - 1) / ktp * ktp;
+  splits = (Mpix + pps - 1) / pps;
+  if (splits < 1) splits = 1;
+  *pix_per_split = (int)pps;
+  return (int)splits;
+}
+
+int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s) {
+  return prec == PREC_BF16 ? wgrad_dispatch<bf16_t>(g, s) : wgrad_dispatch<float>(g, s);
+}
+
+int wgrad_reduce_launch(const float* P, int splits, int Cout, int KHW, int Cin, int Cin_real,
+                        float* out_oihw, hipStream_t s) {
+  const long total = (long)Cout * KHW * Cin;
+  int blocks = (int)((total + 255) / 256);
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, s, P, splits, Cout, KHW, Cin, Cin_real,
+                     out_oihw);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+}  // namespace rn18

@@ -1,0 +1,98 @@
+// Host-side launchers of the gfx950 kernels (defined in the .hip files).
+#pragma once
+#include "common.h"
+
+namespace rn18 {
+
+// ---------------------------------------------------------------------------
+// Implicit-GEMM convolution "gather" form, used for the forward pass and the
+// data gradient: C[m][col] = sum_{tap,ci} A[pixel(m,tap)][ci] * B[col][wtap][ci]
+// ---------------------------------------------------------------------------
+struct ConvGather {
+  const void* A;   // NHWC activations [N][Hin][Win][Cin]
+  const void* B;   // weights [Cols][KHW][Cin]
+  void* C;         // NHWC output [N][Hout][Wout][Cols]
+  const void* R;   // epilogue: residual gradient (mode 2)
+  const void* Rm;  // epilogue: residual mask source (mode 2)
+  int N, Hin, Win, Cin;
+  int Hm, Wm, M;             // GEMM row grid per image; M = N*Hm*Wm
+  int Hout, Wout, Cols;
+  int os, oph, opw;          // output pixel (i*os+oph, j*os+opw)
+  int is, ip;                // input base (i*is-ip, j*is-ip)
+  int nth, ntw;              // taps along h and w
+  int dh0, dhs, dw0, dws;    // input offset of tap (th,tw): (dh0+th*dhs, dw0+tw*dws)
+  int wkh0, wkhs, wkw0, wkws, KW, KHW;  // weight tap (wkh0+th*wkhs)*KW + wkw0+tw*wkws
+  int K;                     // nth*ntw*Cin
+  int mode;                  // 0 store, 1 C += acc, 2 C = acc + (Rm>0 ? R : 0)
+  float* stats;              // optional BN partial sums [tiles_m][Cols][2] (mode 0 only)
+};
+int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s);
+
+// Weight gradient: P[split][co][tap*Cin+ci] = sum_pixels dY[p][co] * Xcol[p][tap,ci]
+struct ConvWgrad {
+  const void* DY;  // [N][Ho][Wo][Cout]
+  const void* X;   // [N][H][W][Cin]
+  float* P;        // split partials [splits][Cout][KHW*Cin]
+  int N, H, W, Cin, Ho, Wo, Cout, KH, KW, stride, pad;
+  int Mpix, Kcols, pix_per_split, splits;
+};
+int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s);
+// Choose the split count for a weight-gradient GEMM (deterministic function of the shape).
+int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split);
+// Sum partials in split order; write OIHW gradient (Cin_real of Cin channels kept).
+int wgrad_reduce_launch(const float* P, int splits, int Cout, int KHW, int Cin, int Cin_real,
+                        float* out_oihw, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Batch norm (per-channel over M = N*H*W rows of an [M][C] tensor)
+// ---------------------------------------------------------------------------
+// partial sums of (y - pivot) and (y - pivot)^2 per block; pivot = y[0][c]
+int bn_stats_partial_launch(int prec, const void* y, long M, int C, float* part, int* nblk, hipStream_t s);
+// combine partials (fp64), write mean/rstd/scale/shift, update running stats
+int bn_stats_final_launch(int prec, const void* y, const float* part, int nblk, long M, int C,
+                          const float* gamma, const float* beta, float eps, float momentum,
+                          float* run_mean, float* run_var, float* mean, float* rstd,
+                          float* scale, float* shift, hipStream_t s);
+// z = act(y*scale+shift [+ r] [+ (yd*scale2+shift2)])
+//  res_mode: 0 none, 1 identity residual r, 2 projected residual (yd, scale2, shift2)
+int bn_apply_launch(int prec, const void* y, const float* scale, const float* shift, int relu,
+                    int res_mode, const void* r, const float* scale2, const float* shift2,
+                    void* z, long M, int C, hipStream_t s);
+// eval-mode BN coefficients from running statistics
+int bn_eval_coef_launch(const float* gamma, const float* beta, const float* rm, const float* rv,
+                        float eps, int C, float* scale, float* shift, hipStream_t s);
+// backward partials of g = dz*(mz>0) (or dz): sum g, sum g*(y-mean)*rstd
+int bn_bwd_partial_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
+                          const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s);
+// dgamma, dbeta into grad; coefficients for the apply
+int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float* gamma, const float* rstd,
+                        float* dgamma, float* dbeta, float* coef, hipStream_t s);
+// dy = k1*g + k2*(y-mean) + k3
+int bn_bwd_apply_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
+                        const float* coef, void* dy, long M, int C, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Misc streams
+// ---------------------------------------------------------------------------
+int ingest_launch(int prec, const float* img, void* x, int N, int H, int W, int Cp, hipStream_t s);
+struct RepackEntry { long src; long dst_f; long dst_d; int Cout, Cin, Cin_p, KHW; long n; long nprefix; };
+int repack_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* table_dev,
+                  int nentries, long total, hipStream_t s);
+int maxpool_fwd_launch(int prec, const void* x, void* y, uint8_t* arg, int N, int H, int W, int C,
+                       int Ho, int Wo, hipStream_t s);
+int maxpool_bwd_launch(int prec, const void* dy, const uint8_t* arg, void* dx, int N, int H, int W, int C,
+                       int Ho, int Wo, hipStream_t s);
+int avgpool_fwd_launch(int prec, const void* x, float* f, int N, int HW, int C, hipStream_t s);
+int avgpool_bwd_launch(int prec, const float* df, void* dx, int N, int HW, int C, hipStream_t s);
+// C[m][n] = sum_k A(m,k) B(k,n) (+ bias[n]); A(m,k) = A[m*sam + k*sak], B(k,n) = B[k*sbk + n*sbn]
+int gemm_f32_launch(const float* A, long sam, long sak, const float* B, long sbk, long sbn,
+                    const float* bias, float* C, int M, int N, int K, hipStream_t s);
+int colsum_launch(const float* A, int M, int N, float* out, hipStream_t s);
+int softmax_ce_launch(const float* z, const int32_t* labels, int N, int C, float* dz, float* row_loss,
+                      float* loss, unsigned* err, hipStream_t s);
+int sgd_launch(float* w, const float* g, float* v, long n, float lr, float mom, float wd, hipStream_t s);
+int merge_launch(float* p, const float* ds, const float* dl, long n, float f, hipStream_t s);
+int delta_launch(const float* pulled, const float* local, float* delta, long n, hipStream_t s);
+int fill_zero_launch(void* p, size_t bytes, hipStream_t s);
+
+}  // namespace rn18

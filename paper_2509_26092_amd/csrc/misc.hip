@@ -1,0 +1,448 @@
+// Streams and small kernels of the training step: input ingest (NCHW fp32 ->
+// NHWC with channels padded to the 16-byte vector), weight repack (OIHW fp32
+// master -> forward and data-gradient layouts in the compute type), max pool
+// with first-maximum argmax and its gather-form backward, global average pool,
+// an LDS-tiled fp32 GEMM for the classifier, softmax cross-entropy with a
+// deterministic loss reduction, SGD-momentum, and the parameter-server merge.
+#include <math.h>
+
+#include "kernels.h"
+
+namespace rn18 {
+
+namespace {
+
+inline int ok() { return hipGetLastError() == hipSuccess ? 0 : -4; }
+
+int grid_for(long work, int per_block = 256, int cap = 16384) {
+  long b = (work + per_block - 1) / per_block;
+  if (b > cap) b = cap;
+  if (b < 1) b = 1;
+  return (int)b;
+}
+
+// ------------------------------------------------------------------ ingest
+template <typename T>
+__global__ void ingest_kernel(const float* __restrict__ img, T* __restrict__ x, long npix, int HW, int Cp) {
+  for (long p = blockIdx.x * 256l + threadIdx.x; p < npix; p += (long)gridDim.x * 256) {
+    const long n = p / HW, hw = p - n * HW;
+    const float* src = img + n * 3 * HW + hw;
+    float v[8] = {src[0], src[HW], src[2 * HW], 0.f, 0.f, 0.f, 0.f, 0.f};
+    ((uint4*)x)[p] = pack<T>(v);  // Cp elements = exactly 16 bytes
+  }
+}
+
+// ------------------------------------------------------------------ repack
+template <typename T>
+__global__ void repack_kernel(const float* __restrict__ st, T* __restrict__ wf, T* __restrict__ wd,
+                              const RepackEntry* __restrict__ tab, int nent, long total) {
+  __shared__ RepackEntry t[24];
+  for (int i = threadIdx.x; i < nent; i += blockDim.x) t[i] = tab[i];
+  __syncthreads();
+  for (long e = blockIdx.x * 256l + threadIdx.x; e < total; e += (long)gridDim.x * 256) {
+    int k = 0;
+    while (k + 1 < nent && e >= t[k + 1].nprefix) ++k;
+    const RepackEntry& r = t[k];
+    const long l = e - r.nprefix;
+    const int per_co = r.KHW * r.Cin_p;
+    const int co = (int)(l / per_co);
+    const int rem = (int)(l - (long)co * per_co);
+    const int tap = rem / r.Cin_p, ci = rem - tap * r.Cin_p;
+    const float v = ci < r.Cin ? st[r.src + ((long)co * r.Cin + ci) * r.KHW + tap] : 0.f;
+    const T tv = TT<T>::from_f(v);
+    wf[r.dst_f + l] = tv;
+    if (r.dst_d >= 0) wd[r.dst_d + ((long)ci * r.KHW + tap) * r.Cout + co] = tv;
+  }
+}
+
+// ------------------------------------------------------------------ max pool 3x3 s2 p1
+template <typename T>
+__global__ void maxpool_fwd_kernel(const T* __restrict__ x, T* __restrict__ y, uint8_t* __restrict__ arg, int N,
+                                   int H, int W, int C, int Ho, int Wo) {
+  constexpr int VW = TT<T>::VW;
+  const int cpr = C / VW;
+  const long total = (long)N * Ho * Wo * cpr;
+  for (long q = blockIdx.x * 256l + threadIdx.x; q < total; q += (long)gridDim.x * 256) {
+    const int cc = (int)(q % cpr);
+    const long pix = q / cpr;
+    const int j = (int)(pix % Wo);
+    const long t2 = pix / Wo;
+    const int i = (int)(t2 % Ho);
+    const int n = (int)(t2 / Ho);
+    float best[VW];
+    uint8_t bi[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) { best[e] = -INFINITY; bi[e] = 0; }
+    for (int kh = 0; kh < 3; ++kh) {
+      const int h = 2 * i - 1 + kh;
+      if ((unsigned)h >= (unsigned)H) continue;
+      for (int kw = 0; kw < 3; ++kw) {
+        const int w = 2 * j - 1 + kw;
+        if ((unsigned)w >= (unsigned)W) continue;
+        float v[VW];
+        unpack<T>(*(const uint4*)(x + (((long)n * H + h) * W + w) * C + cc * VW), v);
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+          if (v[e] > best[e]) { best[e] = v[e]; bi[e] = (uint8_t)(kh * 3 + kw); }
+      }
+    }
+    ((uint4*)y)[q] = pack<T>(best);
+    uint8_t* a = arg + q * VW;
+#pragma unroll
+    for (int e = 0; e < VW; ++e) a[e] = bi[e];
+  }
+}
+
+template <typename T>
+__global__ void maxpool_bwd_kernel(const T* __restrict__ dy, const uint8_t* __restrict__ arg, T* __restrict__ dx,
+                                   int N, int H, int W, int C, int Ho, int Wo) {
+  constexpr int VW = TT<T>::VW;
+  const int cpr = C / VW;
+  const long total = (long)N * H * W * cpr;
+  for (long q = blockIdx.x * 256l + threadIdx.x; q < total; q += (long)gridDim.x * 256) {
+    const int cc = (int)(q % cpr);
+    const long pix = q / cpr;
+    const int w = (int)(pix % W);
+    const long t2 = pix / W;
+    const int h = (int)(t2 % H);
+    const int n = (int)(t2 / H);
+    float acc[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) acc[e] = 0.f;
+    for (int kh = 0; kh < 3; ++kh) {
+      const int hh = h + 1 - kh;
+      if (hh < 0 || (hh & 1)) continue;
+      const int i = hh >> 1;
+      if (i >= Ho) continue;
+      for (int kw = 0; kw < 3; ++kw) {
+        const int ww = w + 1 - kw;
+        if (ww < 0 || (ww & 1)) continue;
+        const int j = ww >> 1;
+        if (j >= Wo) continue;
+        const long oq = (((long)n * Ho + i) * Wo + j) * cpr + cc;
+        float g[VW];
+        unpack<T>(((const uint4*)dy)[oq], g);
+        const uint8_t* a = arg + oq * VW;
+        const uint8_t tap = (uint8_t)(kh * 3 + kw);
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+          if (a[e] == tap) acc[e] += g[e];
+      }
+    }
+    ((uint4*)dx)[q] = pack<T>(acc);
+  }
+}
+
+// ------------------------------------------------------------------ avg pool
+template <typename T>
+__global__ void avgpool_fwd_kernel(const T* __restrict__ x, float* __restrict__ f, int N, int HW, int C) {
+  constexpr int VW = TT<T>::VW;
+  const int cpr = C / VW;
+  const long total = (long)N * cpr;
+  for (long q = blockIdx.x * 256l + threadIdx.x; q < total; q += (long)gridDim.x * 256) {
+    const int cc = (int)(q % cpr);
+    const long n = q / cpr;
+    float s[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) s[e] = 0.f;
+    for (int p = 0; p < HW; ++p) {
+      float v[VW];
+      unpack<T>(*(const uint4*)(x + (n * HW + p) * C + cc * VW), v);
+#pragma unroll
+      for (int e = 0; e < VW; ++e) s[e] += v[e];
+    }
+    const float inv = 1.0f / (float)HW;
+#pragma unroll
+    for (int e = 0; e < VW; ++e) f[n * C + cc * VW + e] = s[e] * inv;
+  }
+}
+
+template <typename T>
+__global__ void avgpool_bwd_kernel(const float* __restrict__ df, T* __restrict__ dx, int N, int HW, int C) {
+  constexpr int VW = TT<T>::VW;
+  const int cpr = C / VW;
+  const long total = (long)N * HW * cpr;
+  const float inv = 1.0f / (float)HW;
+  for (long q = blockIdx.x * 256l + threadIdx.x; q < total; q += (long)gridDim.x * 256) {
+    const int cc = (int)(q % cpr);
+    const long n = q / cpr / HW;
+    float v[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) v[e] = df[n * C + cc * VW + e] * inv;
+    ((uint4*)dx)[q] = pack<T>(v);
+  }
+}
+
+// ------------------------------------------------------------------ fp32 GEMM (classifier)
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, long sam, long sak,
+                                                       const float* __restrict__ B, long sbk, long sbn,
+                                                       const float* __restrict__ bias, float* __restrict__ C,
+                                                       int M, int N, int K) {
+  __shared__ float As[16][65], Bs[16][65];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += 16) {
+#pragma unroll
+    for (int l = 0; l < 4; ++l) {
+      const int e = tid + 256 * l;
+      const int mm = e & 63, kk = e >> 6;
+      As[kk][mm] = (m0 + mm < M && k0 + kk < K) ? A[(long)(m0 + mm) * sam + (long)(k0 + kk) * sak] : 0.f;
+      Bs[kk][mm] = (n0 + mm < N && k0 + kk < K) ? B[(long)(k0 + kk) * sbk + (long)(n0 + mm) * sbn] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { a[i] = As[kk][ty * 4 + i]; b[i] = Bs[kk][tx * 4 + i]; }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + ty * 4 + i;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + tx * 4 + j;
+      if (n < N) C[(long)m * N + n] = acc[i][j] + (bias ? bias[n] : 0.f);
+    }
+  }
+}
+
+__global__ void colsum_kernel(const float* __restrict__ A, int M, int N, float* __restrict__ out) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  float s = 0.f;
+  for (int m = 0; m < M; ++m) s += A[(long)m * N + n];
+  out[n] = s;
+}
+
+// ------------------------------------------------------------------ softmax cross-entropy
+__device__ inline float block_reduce(float v, float* sh, bool is_max) {
+  const int tid = threadIdx.x;
+  sh[tid] = v;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) sh[tid] = is_max ? fmaxf(sh[tid], sh[tid + s]) : sh[tid] + sh[tid + s];
+    __syncthreads();
+  }
+  const float r = sh[0];
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(256) void softmax_ce_kernel(const float* __restrict__ z, const int32_t* __restrict__ y,
+                                                         int N, int C, float* __restrict__ dz,
+                                                         float* __restrict__ row_loss, unsigned* err) {
+  __shared__ float sh[256];
+  const int n = blockIdx.x;
+  const float* zr = z + (long)n * C;
+  float* dr = dz + (long)n * C;
+  const int lab = y[n];
+  const bool bad = lab < 0 || lab >= C;
+  float mx = -INFINITY;
+  for (int c = threadIdx.x; c < C; c += 256) mx = fmaxf(mx, zr[c]);
+  mx = block_reduce(mx, sh, true);
+  float s = 0.f;
+  for (int c = threadIdx.x; c < C; c += 256) s += expf(zr[c] - mx);
+  s = block_reduce(s, sh, false);
+  const float inv_s = 1.0f / s, inv_n = 1.0f / (float)N;
+  for (int c = threadIdx.x; c < C; c += 256) {
+    const float p = expf(zr[c] - mx) * inv_s;
+    dr[c] = bad ? 0.f : (p - (c == lab ? 1.f : 0.f)) * inv_n;
+  }
+  if (threadIdx.x == 0) {
+    if (bad) {
+      atomicOr(err, (unsigned)DEVERR_LABEL);
+      row_loss[n] = 0.f;
+    } else {
+      row_loss[n] = logf(s) + mx - zr[lab];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void loss_reduce_kernel(const float* __restrict__ row_loss, int N,
+                                                          float* __restrict__ loss, unsigned* err) {
+  __shared__ double sh[256];
+  double a = 0.0;
+  for (int i = threadIdx.x; i < N; i += 256) a += (double)row_loss[i];
+  sh[threadIdx.x] = a;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (threadIdx.x < s) sh[threadIdx.x] += sh[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float l = (float)(sh[0] / (double)N);
+    if (loss) loss[0] = l;
+    if (!isfinite(l)) atomicOr(err, (unsigned)DEVERR_NONFINITE);
+  }
+}
+
+// ------------------------------------------------------------------ flat fp32 streams
+__global__ void sgd_kernel(float* __restrict__ w, const float* __restrict__ g, float* __restrict__ v, long n,
+                           float lr, float mom, float wd) {
+  const long n4 = n >> 2;
+  for (long i = blockIdx.x * 256l + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
+    float4 ww = ((float4*)w)[i], gg = ((const float4*)g)[i], vv = ((float4*)v)[i];
+    vv.x = mom * vv.x + (gg.x + wd * ww.x); ww.x -= lr * vv.x;
+    vv.y = mom * vv.y + (gg.y + wd * ww.y); ww.y -= lr * vv.y;
+    vv.z = mom * vv.z + (gg.z + wd * ww.z); ww.z -= lr * vv.z;
+    vv.w = mom * vv.w + (gg.w + wd * ww.w); ww.w -= lr * vv.w;
+    ((float4*)w)[i] = ww;
+    ((float4*)v)[i] = vv;
+  }
+  for (long i = (n4 << 2) + blockIdx.x * 256l + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
+    const float vv = mom * v[i] + (g[i] + wd * w[i]);
+    v[i] = vv;
+    w[i] -= lr * vv;
+  }
+}
+
+__global__ void merge_kernel(float* __restrict__ p, const float* __restrict__ ds, const float* __restrict__ dl,
+                             long n, float f) {
+  const long n4 = n >> 2;
+  for (long i = blockIdx.x * 256l + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
+    float4 pp = ((float4*)p)[i];
+    const float4 a = ((const float4*)ds)[i], b = ((const float4*)dl)[i];
+    pp.x -= b.x + f * a.x; pp.y -= b.y + f * a.y; pp.z -= b.z + f * a.z; pp.w -= b.w + f * a.w;
+    ((float4*)p)[i] = pp;
+  }
+  for (long i = (n4 << 2) + blockIdx.x * 256l + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+    p[i] -= dl[i] + f * ds[i];
+}
+
+__global__ void delta_kernel(const float* __restrict__ a, const float* __restrict__ b, float* __restrict__ d,
+                             long n) {
+  const long n4 = n >> 2;
+  for (long i = blockIdx.x * 256l + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
+    const float4 x = ((const float4*)a)[i], y = ((const float4*)b)[i];
+    ((float4*)d)[i] = make_float4(x.x - y.x, x.y - y.y, x.z - y.z, x.w - y.w);
+  }
+  for (long i = (n4 << 2) + blockIdx.x * 256l + threadIdx.x; i < n; i += (long)gridDim.x * 256) d[i] = a[i] - b[i];
+}
+
+__global__ void fill_zero_kernel(uint32_t* __restrict__ p, long nwords) {
+  for (long i = blockIdx.x * 256l + threadIdx.x; i < nwords; i += (long)gridDim.x * 256) p[i] = 0u;
+}
+
+}  // namespace
+
+int ingest_launch(int prec, const float* img, void* x, int N, int H, int W, int Cp, hipStream_t s) {
+  const long npix = (long)N * H * W;
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(ingest_kernel<bf16_t>, dim3(grid_for(npix)), dim3(256), 0, s, img, (bf16_t*)x, npix, H * W, Cp);
+  else
+    hipLaunchKernelGGL(ingest_kernel<float>, dim3(grid_for(npix)), dim3(256), 0, s, img, (float*)x, npix, H * W, Cp);
+  return ok();
+}
+
+int repack_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* tab, int nent, long total,
+                  hipStream_t s) {
+  if (nent > 24) return -1;
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(repack_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s, state, (bf16_t*)wf,
+                       (bf16_t*)wd, tab, nent, total);
+  else
+    hipLaunchKernelGGL(repack_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s, state, (float*)wf, (float*)wd,
+                       tab, nent, total);
+  return ok();
+}
+
+int maxpool_fwd_launch(int prec, const void* x, void* y, uint8_t* arg, int N, int H, int W, int C, int Ho, int Wo,
+                       hipStream_t s) {
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const long work = (long)N * Ho * Wo * (C / vw);
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(maxpool_fwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, (const bf16_t*)x,
+                       (bf16_t*)y, arg, N, H, W, C, Ho, Wo);
+  else
+    hipLaunchKernelGGL(maxpool_fwd_kernel<float>, dim3(grid_for(work)), dim3(256), 0, s, (const float*)x, (float*)y,
+                       arg, N, H, W, C, Ho, Wo);
+  return ok();
+}
+
+int maxpool_bwd_launch(int prec, const void* dy, const uint8_t* arg, void* dx, int N, int H, int W, int C, int Ho,
+                       int Wo, hipStream_t s) {
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const long work = (long)N * H * W * (C / vw);
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(maxpool_bwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, (const bf16_t*)dy, arg,
+                       (bf16_t*)dx, N, H, W, C, Ho, Wo);
+  else
+    hipLaunchKernelGGL(maxpool_bwd_kernel<float>, dim3(grid_for(work)), dim3(256), 0, s, (const float*)dy, arg,
+                       (float*)dx, N, H, W, C, Ho, Wo);
+  return ok();
+}
+
+int avgpool_fwd_launch(int prec, const void* x, float* f, int N, int HW, int C, hipStream_t s) {
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const long work = (long)N * (C / vw);
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(avgpool_fwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, (const bf16_t*)x, f, N, HW,
+                       C);
+  else
+    hipLaunchKernelGGL(avgpool_fwd_kernel<float>, dim3(grid_for(work)), dim3(256), 0, s, (const float*)x, f, N, HW,
+                       C);
+  return ok();
+}
+
+int avgpool_bwd_launch(int prec, const float* df, void* dx, int N, int HW, int C, hipStream_t s) {
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const long work = (long)N * HW * (C / vw);
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(avgpool_bwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, df, (bf16_t*)dx, N, HW, C);
+  else
+    hipLaunchKernelGGL(avgpool_bwd_kernel<float>, dim3(grid_for(work)), dim3(256), 0, s, df, (float*)dx, N, HW, C);
+  return ok();
+}
+
+int gemm_f32_launch(const float* A, long sam, long sak, const float* B, long sbk, long sbn, const float* bias,
+                    float* C, int M, int N, int K, hipStream_t s) {
+  if (M <= 0 || N <= 0) return 0;
+  hipLaunchKernelGGL(gemm_f32_kernel, dim3(ceil_div(N, 64), ceil_div(M, 64)), dim3(256), 0, s, A, sam, sak, B, sbk,
+                     sbn, bias, C, M, N, K);
+  return ok();
+}
+
+int colsum_launch(const float* A, int M, int N, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(colsum_kernel, dim3(ceil_div(N, 256)), dim3(256), 0, s, A, M, N, out);
+  return ok();
+}
+
+int softmax_ce_launch(const float* z, const int32_t* labels, int N, int C, float* dz, float* row_loss, float* loss,
+                      unsigned* err, hipStream_t s) {
+  hipLaunchKernelGGL(softmax_ce_kernel, dim3(N), dim3(256), 0, s, z, labels, N, C, dz, row_loss, err);
+  hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, row_loss, N, loss, err);
+  return ok();
+}
+
+int sgd_launch(float* w, const float* g, float* v, long n, float lr, float mom, float wd, hipStream_t s) {
+  hipLaunchKernelGGL(sgd_kernel, dim3(grid_for((n + 3) / 4, 256, 8192)), dim3(256), 0, s, w, g, v, n, lr, mom, wd);
+  return ok();
+}
+
+int merge_launch(float* p, const float* ds, const float* dl, long n, float f, hipStream_t s) {
+  hipLaunchKernelGGL(merge_kernel, dim3(grid_for((n + 3) / 4, 256, 8192)), dim3(256), 0, s, p, ds, dl, n, f);
+  return ok();
+}
+
+int delta_launch(const float* a, const float* b, float* d, long n, hipStream_t s) {
+  hipLaunchKernelGGL(delta_kernel, dim3(grid_for((n + 3) / 4, 256, 8192)), dim3(256), 0, s, a, b, d, n);
+  return ok();
+}
+
+int fill_zero_launch(void* p, size_t bytes, hipStream_t s) {
+  const long nw = (long)(bytes / 4);
+  if (nw <= 0) return 0;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(nw, 256, 8192)), dim3(256), 0, s, (uint32_t*)p, nw);
+  return ok();
+}
+
+}  // namespace rn18

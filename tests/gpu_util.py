@@ -1,0 +1,112 @@
+"""Helpers shared by the GPU parity tests: layout conversion between the
+oracle's NCHW float64 arrays and the library's NHWC device tensors, the
+parity metric, and a runner for one training step on either side."""
+import numpy as np
+
+from oracle import net, ops
+from paper_2509_26092_amd import binding as B
+from paper_2509_26092_amd import inputs
+
+PREC = {"fp32": B.RN18_FP32, "bf16": B.RN18_BF16}
+TOL = {"fp32": 1e-3, "bf16": 2e-2}
+
+
+def torch_dtype(prec):
+    import torch
+    return torch.float32 if prec == "fp32" else torch.bfloat16
+
+
+def to_dev_nhwc(x_nchw, prec, cpad=None):
+    """float array [N,C,H,W] -> device NHWC tensor (channels zero-padded to cpad)."""
+    import torch
+    x = np.asarray(x_nchw, np.float32)
+    if cpad and cpad > x.shape[1]:
+        x = np.concatenate([x, np.zeros((x.shape[0], cpad - x.shape[1]) + x.shape[2:], np.float32)], axis=1)
+    t = torch.from_numpy(np.ascontiguousarray(x.transpose(0, 2, 3, 1)))
+    return t.to(torch_dtype(prec)).cuda().contiguous()
+
+
+def from_dev_nhwc(t):
+    return t.float().cpu().numpy().astype(np.float64).transpose(0, 3, 1, 2)
+
+
+def rounded(x, prec):
+    """What the device holds for an fp32 input in the given precision, as f64."""
+    return ops.round_bf16(x) if prec == "bf16" else np.asarray(x, np.float32).astype(np.float64)
+
+
+def rel_errors(gpu, ref):
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert gpu.shape == ref.shape, (gpu.shape, ref.shape)
+    d = gpu - ref
+    nref = np.linalg.norm(ref)
+    mref = np.abs(ref).max() if ref.size else 0.0
+    rel = np.linalg.norm(d) / nref if nref > 0 else np.linalg.norm(d)
+    mx = np.abs(d).max() / mref if mref > 0 else (np.abs(d).max() if d.size else 0.0)
+    return rel, mx
+
+
+def assert_close(gpu, ref, tol, name=""):
+    """Parity metric: norm-wise relative error <= tol and, element by
+    element, |gpu - ref| <= tol * max|ref| (a purely relative element bound
+    is unbounded where ref crosses zero)."""
+    rel, mx = rel_errors(gpu, ref)
+    assert np.all(np.isfinite(gpu)), "%s: non-finite values" % name
+    assert rel <= tol and mx <= tol, "%s: norm-rel %.3e, max-elem %.3e > tol %.1e" % (name, rel, mx, tol)
+    return rel, mx
+
+
+def make_state(arch, classes, seed):
+    """Oracle-side initial state with every tensor kind non-trivial
+    (random gamma, beta, FC bias and running statistics)."""
+    L = net.Layout(arch, classes)
+    st = net.init_state(L, seed)
+    rng = np.random.default_rng(seed + 77)
+    for name, cin, cout, k, s, p in L.convs:
+        L.put(st, name + ".g", 1.0 + 0.1 * rng.standard_normal(cout))
+        L.put(st, name + ".b", 0.1 * rng.standard_normal(cout))
+        L.put(st, name + ".rm", 0.1 * rng.standard_normal(cout))
+        L.put(st, name + ".rv", 1.0 + 0.1 * np.abs(rng.standard_normal(cout)))
+    L.put(st, "fc.b", 0.1 * rng.standard_normal(classes))
+    return L, st.astype(np.float32).astype(np.float64)
+
+
+def gpu_train_step(arch, classes, prec, state64, x, y, lr, steps=1, momentum_in=None, worker=None):
+    import torch
+    w = worker or B.Worker(arch, classes, prec)
+    st = torch.from_numpy(np.asarray(state64, np.float32)).cuda()
+    xi = torch.from_numpy(np.asarray(x, np.float32)).cuda()
+    yi = torch.from_numpy(np.asarray(y, np.int32)).cuda()
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    if momentum_in is not None:
+        B.rn18_set_momentum(w.ctx, torch.from_numpy(np.asarray(momentum_in, np.float32)).cuda())
+    losses = []
+    for _ in range(steps):
+        w.train_step(st, xi, yi, lr, loss)
+        losses.append(float(loss.item()))
+    v = torch.zeros(w.n_trainable, dtype=torch.float32, device="cuda")
+    B.rn18_get_momentum(w.ctx, v)
+    status = w.sync_status()
+    out = st.cpu().numpy().astype(np.float64), v.cpu().numpy().astype(np.float64), losses, status
+    if worker is None:
+        w.close()
+    return out
+
+
+def compare_step(L, cfg, state0, x, y, lr, gpu_state, gpu_v, gpu_loss, tol, v0=None):
+    """Oracle train step from the same state; compare every tensor."""
+    P = L.n_trainable
+    v0 = np.zeros(P) if v0 is None else v0
+    new, v1, loss, grad = net.train_step(cfg, L, state0, v0, x, y, lr)
+    report = {}
+    assert abs(gpu_loss - loss) <= tol * abs(loss), ("loss", gpu_loss, loss)
+    for key in L.off:
+        o, shp = L.off[key]
+        n = int(np.prod(shp))
+        if o < P:
+            report[key + ".v"] = assert_close(gpu_v[o:o + n], v1[o:o + n], tol, key + " momentum (grad + wd*w)")
+            report[key + ".dw"] = assert_close(state0[o:o + n] - gpu_state[o:o + n], state0[o:o + n] - new[o:o + n],
+                                               tol, key + " update")
+        report[key] = assert_close(gpu_state[o:o + n], new[o:o + n], tol, key)
+    return report, loss

@@ -1,0 +1,82 @@
+"""GPU parity of the parameter-server merge (ps_dual_merge, ps_worker_delta)
+and of one simulated dual-batch round: both workers pull the same global
+state, take a local step at their own batch size with their own momentum,
+push their update vectors, and the server merges them with the
+model-update factor."""
+import numpy as np
+import pytest
+
+from oracle import merge, net
+from paper_2509_26092_amd import binding as B
+from paper_2509_26092_amd import inputs
+from gpu_util import assert_close, gpu_train_step, make_state
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("n", [11_689_512 + 9_600, 5_306 + 96, 1, 7, 4_099])
+@pytest.mark.parametrize("f", [0.25, 0.5, 1.0, 0.81])
+def test_merge_kernel(n, f):
+    import torch
+    p = inputs.tensor(1, (n,))
+    ds = inputs.tensor(2, (n,), 1e-2)
+    dl = inputs.tensor(3, (n,), 1e-2)
+    pt, dst, dlt = (torch.from_numpy(a).cuda() for a in (p, ds, dl))
+    B.ps_dual_merge(pt, dst, dlt, n, f)
+    ref = merge.dual_merge_r1(p, ds, dl, np.float32(f))
+    got = pt.cpu().numpy().astype(np.float64)
+    # fp32 evaluation of p - (dl + f*ds): a few ulps of the operands
+    bound = 4 * np.finfo(np.float32).eps * (np.abs(p) + np.abs(dl) + np.abs(f * ds)) + 1e-45
+    assert np.all(np.abs(got - ref) <= bound)
+
+
+def test_worker_delta_exact():
+    import torch
+    n = 10_001
+    a = inputs.tensor(4, (n,))
+    b = a + inputs.tensor(5, (n,), 1e-3)
+    d = torch.empty(n, device="cuda")
+    B.ps_worker_delta(torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda(), d, n)
+    np.testing.assert_array_equal(d.cpu().numpy(), a - b)   # IEEE subtraction is correctly rounded
+
+
+def test_merge_argument_errors():
+    import torch
+    x = torch.zeros(16, device="cuda")
+    y = torch.zeros(16, device="cuda")
+    with pytest.raises(B.Rn18Error):
+        B.ps_dual_merge(x, y, y, 16, float("nan"))
+    with pytest.raises(B.Rn18Error):
+        B.ps_dual_merge(x, x, y, 16, 0.5)
+
+
+@pytest.mark.parametrize("arch,classes,prec,H,bl,bs", [("imagenet", 1000, "bf16", 64, 8, 4),
+                                                        ("cifar", 100, "fp32", 16, 6, 3)])
+@pytest.mark.parametrize("factor", [0.25, 1.0])
+def test_dual_batch_round(arch, classes, prec, H, bl, bs, factor):
+    import torch
+    L, p0 = make_state(arch, classes, 200)
+    xl, yl = inputs.images(201, bl, H, H), inputs.labels(201, bl, classes)
+    xs, ys = inputs.images(202, bs, H, H), inputs.labels(202, bs, classes)
+    lr = 0.1
+    # GPU: two workers with their own contexts (momentum buffers)
+    pl, _, _, _ = gpu_train_step(arch, classes, prec, p0, xl, yl, lr)
+    ps, _, _, _ = gpu_train_step(arch, classes, prec, p0, xs, ys, lr)
+    n = L.n_state
+    g = torch.from_numpy(p0.astype(np.float32)).cuda()
+    dl = torch.empty(n, device="cuda")
+    dsm = torch.empty(n, device="cuda")
+    B.ps_worker_delta(g, torch.from_numpy(pl.astype(np.float32)).cuda(), dl, n)
+    B.ps_worker_delta(g, torch.from_numpy(ps.astype(np.float32)).cuda(), dsm, n)
+    B.ps_dual_merge(g, dsm, dl, n, factor)
+    got = g.cpu().numpy().astype(np.float64)
+    # oracle round
+    cfg = net.Config(arch, classes, bf16=(prec == "bf16"))
+    sl, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xl, yl, lr)
+    ss, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xs, ys, lr)
+    ref = merge.dual_merge_r1(p0, merge.worker_delta(p0, ss), merge.worker_delta(p0, sl), factor)
+    tol = 1e-3 if prec == "fp32" else 2e-2
+    for key in ("stem.w", "s1b1c1.w", "s2b1ds.w", "s4b2c2.w", "fc.w", "fc.b", "stem.rm", "s4b2c2.rv"):
+        o, shp = L.off[key]
+        k = int(np.prod(shp))
+        assert_close(p0[o:o + k] - got[o:o + k], p0[o:o + k] - ref[o:o + k], tol, key + " merged update")

@@ -1,0 +1,184 @@
+"""GPU parity of the whole training step (rn18_train_step through the C ABI)
+against the fp64 oracle on the same seeded inputs and the same initial
+state: loss, every parameter's gradient (read back as the momentum buffer
+v = g + wd*w after one step from v = 0), every update and the BN running
+statistics, per tensor at the training configurations' tolerance.
+
+Full configuration sizes where the oracle finishes in seconds (the tiny
+configuration, CIFAR batch 128 at 32x32); reduced batches (with ragged
+tails) at every resolution the cyclic and hybrid schedules visit; and, at
+the ImageNet batch-256 224x224 launch configuration itself, properties that
+hold at any size (duplicated-batch invariance, lr = 0) plus per-sample
+eval-mode logits checked against the oracle one image at a time."""
+import numpy as np
+import pytest
+
+from oracle import net
+from paper_2509_26092_amd import binding as B
+from paper_2509_26092_amd import inputs
+from gpu_util import TOL, compare_step, gpu_train_step, make_state
+
+pytestmark = pytest.mark.gpu
+
+LR = 0.1
+
+
+def _run_parity(arch, classes, prec, N, H, seed, lr=LR):
+    L, st = make_state(arch, classes, seed)
+    x = inputs.images(seed, N, H, H)
+    y = inputs.labels(seed, N, classes)
+    gs, gv, losses, status = gpu_train_step(arch, classes, prec, st, x, y, lr)
+    assert status == B.RN18_OK
+    cfg = net.Config(arch, classes, bf16=(prec == "bf16"))
+    report, loss = compare_step(L, cfg, st, x, y, lr, gs, gv, losses[0], TOL[prec])
+    worst = max(report.items(), key=lambda kv: kv[1][0])
+    print("%s %s N=%d H=%d loss %.6f (oracle %.6f) worst %s norm-rel %.2e" %
+          (arch, prec, N, H, losses[0], loss, worst[0], worst[1][0]))
+    return report
+
+
+def test_tiny_fp32_full_config():
+    _run_parity("tiny", 10, "fp32", 8, 16, seed=100)
+
+
+def test_tiny_fp32_ragged_batch():
+    _run_parity("tiny", 10, "fp32", 5, 13, seed=101)
+
+
+def test_cifar_fp32_b128_32_full_config():
+    _run_parity("cifar", 100, "fp32", 128, 32, seed=102)
+
+
+@pytest.mark.parametrize("N,H", [(8, 16), (6, 24), (5, 32)])
+def test_cifar_fp32_cyclic_resolutions(N, H):
+    _run_parity("cifar", 100, "fp32", N, H, seed=103 + H)
+
+
+@pytest.mark.parametrize("N,H", [(4, 224), (3, 128), (2, 160), (2, 192), (8, 64)])
+def test_imagenet_bf16_resolutions(N, H):
+    _run_parity("imagenet", 1000, "bf16", N, H, seed=110 + H)
+
+
+def test_imagenet_fp32_small():
+    """All op types (7x7 s2 stem, max pool, projections) in fp32 at 1e-3."""
+    _run_parity("imagenet", 1000, "fp32", 3, 64, seed=120)
+
+
+def test_two_steps_with_momentum():
+    arch, classes, prec, N, H, seed = "tiny", 10, "fp32", 8, 16, 130
+    L, st = make_state(arch, classes, seed)
+    x = inputs.images(seed, N, H, H)
+    y = inputs.labels(seed, N, classes)
+    gs, gv, losses, _ = gpu_train_step(arch, classes, prec, st, x, y, LR, steps=2)
+    cfg = net.Config(arch, classes)
+    s1, v1, l1, _ = net.train_step(cfg, L, st, np.zeros(L.n_trainable), x, y, LR)
+    s2, v2, l2, _ = net.train_step(cfg, L, s1, v1, x, y, LR)
+    from gpu_util import assert_close
+    assert abs(losses[1] - l2) <= 1e-3 * abs(l2)
+    assert_close(gs, s2, 1e-3, "state after 2 steps")
+    assert_close(gv, v2, 1e-3, "momentum after 2 steps")
+
+
+def test_eval_logits_parity():
+    import torch
+    for arch, classes, prec, N, H, seed in [("tiny", 10, "fp32", 8, 16, 140), ("cifar", 100, "fp32", 4, 32, 141),
+                                            ("imagenet", 1000, "bf16", 2, 96, 142)]:
+        L, st = make_state(arch, classes, seed)
+        x = inputs.images(seed, N, H, H)
+        w = B.Worker(arch, classes, prec)
+        logits = torch.empty((N, classes), dtype=torch.float32, device="cuda")
+        w.eval_logits(torch.from_numpy(st.astype(np.float32)).cuda(), torch.from_numpy(x).cuda(), logits)
+        ref = net.eval_logits(net.Config(arch, classes, bf16=(prec == "bf16")), L, st, x)
+        from gpu_util import assert_close
+        assert_close(logits.cpu().numpy(), ref, 1e-3 if prec == "fp32" else 2e-2, arch + " eval logits")
+        w.close()
+
+
+def test_imagenet_bf16_b256_224_launch_config_properties():
+    """At the full ImageNet batch-256 224x224 configuration: (a) a batch made
+    of two copies of 128 images has the same BN statistics, mean loss and
+    gradients as the 128 images alone (exactly, in real arithmetic); (b) the
+    step is deterministic; (c) eval logits of sampled images match the
+    oracle evaluated on those images alone."""
+    import torch
+    from gpu_util import assert_close
+    arch, classes, prec = "imagenet", 1000, "bf16"
+    L, st = make_state(arch, classes, 150)
+    x = inputs.images(150, 128, 224, 224)
+    y = inputs.labels(150, 128, classes)
+    xx = np.concatenate([x, x])
+    yy = np.concatenate([y, y])
+    w = B.Worker(arch, classes, prec)
+    s256, v256, l256, _ = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w)
+    s256b, v256b, _, _ = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w)
+    assert np.array_equal(v256, v256b), "train step is not deterministic"
+    s128, v128, l128, status = gpu_train_step(arch, classes, prec, st, x, y, LR, worker=w)
+    assert status == B.RN18_OK
+    assert abs(l256[0] - l128[0]) <= 2e-2 * abs(l128[0])
+    P = L.n_trainable
+    for key in ("stem.w", "s1b1c1.w", "s2b1ds.w", "s3b2c2.w", "s4b2c2.w", "s4b2c2.g", "fc.w", "fc.b"):
+        o, shp = L.off[key]
+        n = int(np.prod(shp))
+        assert_close(v256[o:o + n], v128[o:o + n], 2e-2, key + " duplicated-batch gradient")
+    # eval-mode logits of sampled images, one by one against the oracle
+    logits = torch.empty((256, classes), dtype=torch.float32, device="cuda")
+    w.eval_logits(torch.from_numpy(st.astype(np.float32)).cuda(), torch.from_numpy(xx).cuda(), logits)
+    lg = logits.cpu().numpy()
+    cfg = net.Config(arch, classes, bf16=True)
+    for i in (0, 77, 200):
+        ref = net.eval_logits(cfg, L, st, xx[i:i + 1])
+        assert_close(lg[i:i + 1], ref, 2e-2, "eval logits of image %d" % i)
+    w.close()
+
+
+def test_lr_zero_keeps_weights():
+    arch, classes, prec, N, H, seed = "cifar", 100, "fp32", 4, 16, 160
+    L, st = make_state(arch, classes, seed)
+    x = inputs.images(seed, N, H, H)
+    y = inputs.labels(seed, N, classes)
+    gs, gv, _, _ = gpu_train_step(arch, classes, prec, st, x, y, 0.0)
+    P = L.n_trainable
+    assert np.array_equal(gs[:P], st[:P].astype(np.float32).astype(np.float64))
+
+
+def test_bad_label_sets_sticky_error():
+    arch, classes, prec, N, H, seed = "tiny", 10, "fp32", 4, 16, 170
+    L, st = make_state(arch, classes, seed)
+    x = inputs.images(seed, N, H, H)
+    y = np.array([1, 2, 10, 3], np.int32)
+    _, _, _, status = gpu_train_step(arch, classes, prec, st, x, y, LR)
+    assert status == B.RN18_ELABEL
+
+
+def test_host_side_errors():
+    import torch
+    w = B.Worker("tiny", 10, "fp32")
+    st = torch.zeros(w.n_state, device="cuda")
+    x = torch.zeros((1, 3, 1, 1), device="cuda")
+    y = torch.zeros(1, dtype=torch.int32, device="cuda")
+    with pytest.raises(B.Rn18Error) as e:
+        B.rn18_train_step(w.ctx, st, x, y, 1, 1, 1, 0.1)      # BN over a single value
+    assert e.value.code == B.RN18_EINVAL
+    with pytest.raises(B.Rn18Error):
+        B.rn18_train_step(w.ctx, st, x, y, 0, 16, 16, 0.1)
+    w.close()
+
+
+def test_init_statistics():
+    """rn18_init: He-normal fan-in weights (sample std within CLT bounds),
+    gamma 1, beta 0, running var 1."""
+    import torch
+    cfg = B.make_config("cifar", 100)
+    n, P = B.rn18_state_floats(cfg)
+    st = torch.zeros(n, device="cuda")
+    ctx = B.rn18_init(cfg, 5, st)
+    B.rn18_destroy(ctx)
+    s = st.cpu().numpy().astype(np.float64)
+    L = net.Layout("cifar", 100)
+    for name, cin, cout, k, _, _ in L.convs:
+        w = L.get(s, name + ".w")
+        sd = np.sqrt(2.0 / (cin * k * k))
+        assert abs(w.mean()) < 5 * sd / np.sqrt(w.size)
+        assert abs(w.std() / sd - 1) < 5 * np.sqrt(0.5 / w.size) + 1e-3
+        assert np.all(L.get(s, name + ".g") == 1) and np.all(L.get(s, name + ".b") == 0)
+        assert np.all(L.get(s, name + ".rv") == 1) and np.all(L.get(s, name + ".rm") == 0)
