@@ -56,6 +56,25 @@ int rn18op_maxpool_fwd(int prec, const void* x, void* y, uint8_t* arg, int N, in
 int rn18op_maxpool_bwd(int prec, const void* dy, const uint8_t* arg, void* dx, int N, int H, int W, int C,
                        void* hip_stream);
 
+/* Debugging aids (not part of the training path).
+ * rn18_debug_set(ctx, RN18_DBG_STOP_BLOCKS, k): later train steps end their
+ * backward pass after k residual blocks (no stem backward, no SGD update);
+ * k = -1 restores full steps.
+ * rn18_debug_copy: copy `bytes` of a workspace tensor of the (N,H,W) plan to
+ * the device buffer dst, enqueued on the context's stream. `which` selects
+ * the tensor (NHWC in the compute type, or fp32 for grad/mean/rstd),
+ * `index` the conv layer (forward order) or the residual block. */
+enum {
+  RN18_DBG_STOP_BLOCKS = 0
+};
+enum {
+  RN18_DBG_Y = 0, RN18_DBG_Z1 = 1, RN18_DBG_OUT = 2, RN18_DBG_GA = 3, RN18_DBG_GB = 4, RN18_DBG_GZ = 5,
+  RN18_DBG_GY = 6, RN18_DBG_GYD = 7, RN18_DBG_GRAD = 8, RN18_DBG_WF = 9, RN18_DBG_WD = 10,
+  RN18_DBG_MEAN = 11, RN18_DBG_RSTD = 12, RN18_DBG_ZSTEM = 13, RN18_DBG_PARG = 14
+};
+int rn18_debug_set(struct rn18_ctx* ctx, int key, long value);
+int rn18_debug_copy(struct rn18_ctx* ctx, int N, int H, int W, int which, int index, void* dst, size_t bytes);
+
 #ifdef __cplusplus
 }
 #endif

@@ -129,11 +129,19 @@ def _rb(cfg, x):
     return ops.round_bf16(x) if (cfg.bf16 and cfg.round_acts) else x
 
 
-def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=True):
+def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=True, decide=None):
     """One forward (batch statistics) and backward pass.
 
     Returns loss, logits, the flat gradient (length P), and the new running
     statistics (list of (name, rm, rv)).
+
+    The derivative of ReLU at an input of exactly 0, and the argmax of a max
+    pool window with tied maxima, are not fixed by the arithmetic; inputs
+    within rounding distance of those points make the choice depend on the
+    precision the pre-activation was computed in. `decide`, if given, is
+    called as decide("relu", site, pre, mask) and decide("pool", site, x,
+    arg) and returns the mask / argmax to use (sites: "stem", ("z1", block),
+    ("out", block)); the default is mask = pre > 0 and the first maximum.
 
     bf16 configurations (the training configuration's mixed precision): the
     images and the conv weights are rounded to bf16 (round-to-nearest-even)
@@ -150,6 +158,14 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
 
     caches = {}
     run_stats = []
+    masks = {}
+
+    def relu_site(site, pre):
+        mask = pre > 0
+        if decide is not None:
+            mask = decide("relu", site, pre, mask)
+        masks[site] = mask
+        return _rb(cfg, ops.relu(pre))
 
     def conv_bn(name, inp, act):
         _, cin, cout, k, s, p = layout.spec[name]
@@ -165,22 +181,22 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
             out = ops.bn_eval_forward(y, g, b, layout.get(state, name + ".rm"), layout.get(state, name + ".rv"), eps)
             c = None
         caches[name] = {"inp": inp, "bn": c}
-        if act:
-            out = _rb(cfg, ops.relu(out))
         return out
 
-    a = conv_bn("stem", x, True)
+    a = relu_site("stem", conv_bn("stem", x, True))
     stem_out = a
     pool_arg = None
     if cfg.arch == "imagenet":
         a, pool_arg = ops.maxpool_forward(a)
+        if decide is not None:
+            pool_arg = decide("pool", "stem", stem_out, pool_arg)
     block_io = []
-    for blk in layout.blocks:
+    for bi, blk in enumerate(layout.blocks):
         inp = a
-        z1 = conv_bn(blk["c1"], inp, True)
+        z1 = relu_site(("z1", bi), conv_bn(blk["c1"], inp, True))
         b2 = conv_bn(blk["c2"], z1, False)
         sc = conv_bn(blk["ds"], inp, False) if blk["ds"] else inp
-        a = _rb(cfg, ops.relu(b2 + sc))
+        a = relu_site(("out", bi), b2 + sc)
         block_io.append((inp, z1, a))
     f = ops.avgpool_forward(a)
     wfc = layout.get(state, "fc.w")
@@ -211,10 +227,11 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
             return None
         return ops.conv2d_backward_data(dy, W(name), inp.shape, s, p)
 
-    for blk, (inp, z1, out) in zip(reversed(layout.blocks), reversed(block_io)):
-        g2 = ops.relu_backward(da, out)
+    for bi in reversed(range(len(layout.blocks))):
+        blk = layout.blocks[bi]
+        g2 = da * masks[("out", bi)]
         dz1 = _rb(cfg, bn_conv_back(blk["c2"], g2))
-        g1 = ops.relu_backward(dz1, z1)
+        g1 = dz1 * masks[("z1", bi)]
         dx = bn_conv_back(blk["c1"], g1)
         if blk["ds"]:
             dx = dx + bn_conv_back(blk["ds"], g2)
@@ -223,16 +240,16 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
         da = _rb(cfg, dx)
     if cfg.arch == "imagenet":
         da = _rb(cfg, ops.maxpool_backward(da, pool_arg, stem_out.shape))
-    g0 = ops.relu_backward(da, stem_out)
+    g0 = da * masks["stem"]
     bn_conv_back("stem", g0)
     return loss, logits, grad, run_stats
 
 
-def train_step(cfg, layout, state, momentum_buf, images, labels, lr):
+def train_step(cfg, layout, state, momentum_buf, images, labels, lr, decide=None):
     """Forward, backward, BN running-stat update and SGD-momentum update of
     every trainable parameter (conv W, gamma, beta, FC W and b; weight decay
     on all of them). Returns (new_state, new_momentum, loss, grad)."""
-    loss, logits, grad, run_stats = forward_backward(cfg, layout, state, images, labels)
+    loss, logits, grad, run_stats = forward_backward(cfg, layout, state, images, labels, decide=decide)
     new_state = np.array(state, dtype=np.float64, copy=True)
     P = layout.n_trainable
     w_new, v_new = ops.sgd_momentum(new_state[:P], grad, momentum_buf, lr, cfg.momentum, cfg.weight_decay)

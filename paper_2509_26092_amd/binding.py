@@ -24,7 +24,7 @@ EXPORTED = [
     "rn18_eval_logits", "ps_dual_merge", "ps_worker_delta", "rn18_sync_status", "rn18_get_momentum",
     "rn18_set_momentum", "rn18_destroy", "rn18_last_error",
     "rn18op_conv2d_fwd", "rn18op_conv2d_dgrad", "rn18op_conv2d_wgrad_workspace", "rn18op_conv2d_wgrad",
-    "rn18op_maxpool_fwd", "rn18op_maxpool_bwd",
+    "rn18op_maxpool_fwd", "rn18op_maxpool_bwd", "rn18_debug_set", "rn18_debug_copy",
 ]
 
 
@@ -75,6 +75,8 @@ def lib():
         "rn18op_conv2d_wgrad": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _Z, _P]),
         "rn18op_maxpool_fwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _P]),
         "rn18op_maxpool_bwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _P]),
+        "rn18_debug_set": (_I, [_P, _I, ctypes.c_long]),
+        "rn18_debug_copy": (_I, [_P, _I, _I, _I, _I, _I, _P, _Z]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -189,6 +191,19 @@ def rn18op_maxpool_fwd(prec, x, y, arg, N, H, W, C, stream=None):
 
 def rn18op_maxpool_bwd(prec, dy, arg, dx, N, H, W, C, stream=None):
     return _check(lib().rn18op_maxpool_bwd(prec, _ptr(dy), _ptr(arg), _ptr(dx), N, H, W, C, _stream(stream)))
+
+
+DBG = dict(y=0, z1=1, out=2, gA=3, gB=4, gz=5, gy=6, gyd=7, grad=8, wf=9, wd=10, mean=11, rstd=12, zstem=13,
+           parg=14)
+
+
+def rn18_debug_set(ctx, key, value):
+    return _check(lib().rn18_debug_set(ctx, key, value))
+
+
+def rn18_debug_copy(ctx, N, H, W, which, index, dst):
+    return _check(lib().rn18_debug_copy(ctx, N, H, W, DBG[which] if isinstance(which, str) else which, index,
+                                        _ptr(dst), dst.numel() * dst.element_size()))
 
 
 # ------------------------------------------------------------------ thin owner of a context

@@ -170,6 +170,7 @@ struct Ctx {
   size_t ws_bytes = 0;
   bool ws_owned = false;
   std::map<std::tuple<int, int, int>, Plan> plans;
+  int dbg_stop_blocks = -1;     // debugging: end the backward pass after this many blocks
 };
 
 int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
@@ -520,7 +521,9 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     return 0;
   };
 
+  int done = 0;
   for (int bi = (int)a.blocks.size() - 1; bi >= 0; --bi) {
+    if (c->dbg_stop_blocks >= 0 && done++ == c->dbg_stop_blocks) return RN18_OK;
     const BlockL& B = a.blocks[bi];
     const BlockP& bp = pl.bp[bi];
     // gA = gradient wrt the block output (before its ReLU mask)
@@ -775,6 +778,53 @@ void rn18_destroy(rn18_ctx* h) {
   if (c.err) (void)hipFree(c.err);
   if (c.ws_owned && c.ws) (void)hipFree(c.ws);
   delete h;
+}
+
+int rn18_debug_set(rn18_ctx* h, int key, long value) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  if (key != RN18_DBG_STOP_BLOCKS) return fail(RN18_EINVAL, "unknown debug key %d", key);
+  h->c.dbg_stop_blocks = (int)value;
+  return RN18_OK;
+}
+
+int rn18_debug_copy(rn18_ctx* h, int N, int H, int W, int which, int index, void* dst, size_t bytes) {
+  if (!h || !dst) return fail(RN18_EINVAL, "NULL pointer");
+  Ctx& c = h->c;
+  const Plan* pl = nullptr;
+  int r = get_plan(&c, N, H, W, &pl);
+  if (r) return r;
+  const Arch& a = c.arch;
+  const int nconv = (int)a.convs.size(), nblk = (int)a.blocks.size();
+  const void* src = nullptr;
+  char* ws = (char*)c.ws;
+  auto conv_ok = [&]() { return index >= 0 && index < nconv; };
+  auto blk_ok = [&]() { return index >= 0 && index < nblk; };
+  switch (which) {
+    case RN18_DBG_Y: if (conv_ok()) src = ws + pl->cp[index].y; break;
+    case RN18_DBG_Z1: if (blk_ok()) src = ws + pl->bp[index].z1; break;
+    case RN18_DBG_OUT: if (blk_ok()) src = ws + pl->bp[index].out; break;
+    case RN18_DBG_GA: src = ws + pl->gA; break;
+    case RN18_DBG_GB: src = ws + pl->gB; break;
+    case RN18_DBG_GZ: src = ws + pl->gz; break;
+    case RN18_DBG_GY: src = ws + pl->gy; break;
+    case RN18_DBG_GYD: src = ws + pl->gyd; break;
+    case RN18_DBG_GRAD: src = ws + pl->grad; break;
+    case RN18_DBG_WF: if (conv_ok()) src = (char*)c.wf + (size_t)a.convs[index].wf * c.es; break;
+    case RN18_DBG_WD: if (conv_ok() && index > 0) src = (char*)c.wd + (size_t)a.convs[index].wd * c.es; break;
+    case RN18_DBG_MEAN: if (conv_ok()) src = ws + pl->cp[index].mean; break;
+    case RN18_DBG_RSTD: if (conv_ok()) src = ws + pl->cp[index].rstd; break;
+    case RN18_DBG_ZSTEM: src = ws + pl->zstem; break;
+    case RN18_DBG_PARG: if (a.imagenet) src = ws + pl->parg; break;
+    default: break;
+  }
+  if (!src || !ws) return fail(RN18_EINVAL, "no such debug tensor (%d, %d)", which, index);
+  size_t limit;
+  if (which == RN18_DBG_WF) limit = (size_t)a.wf_total * c.es - (size_t)a.convs[index].wf * c.es;
+  else if (which == RN18_DBG_WD) limit = (size_t)a.wd_total * c.es - (size_t)a.convs[index].wd * c.es;
+  else limit = c.ws_bytes - (size_t)((const char*)src - ws);
+  if (bytes > limit) return fail(RN18_EINVAL, "debug copy of %zu bytes exceeds the tensor's buffer", bytes);
+  HIPCHK(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, c.stream));
+  return RN18_OK;
 }
 
 // ---------------------------------------------------------------------------

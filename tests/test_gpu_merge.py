@@ -9,7 +9,7 @@ import pytest
 from oracle import merge, net
 from paper_2509_26092_amd import binding as B
 from paper_2509_26092_amd import inputs
-from gpu_util import assert_close, gpu_train_step, make_state
+from gpu_util import TAU, Decider, assert_close, gpu_train_step, make_state
 
 pytestmark = pytest.mark.gpu
 
@@ -60,8 +60,9 @@ def test_dual_batch_round(arch, classes, prec, H, bl, bs, factor):
     xs, ys = inputs.images(202, bs, H, H), inputs.labels(202, bs, classes)
     lr = 0.1
     # GPU: two workers with their own contexts (momentum buffers)
-    pl, _, _, _ = gpu_train_step(arch, classes, prec, p0, xl, yl, lr)
-    ps, _, _, _ = gpu_train_step(arch, classes, prec, p0, xs, ys, lr)
+    wl, ws = B.Worker(arch, classes, prec), B.Worker(arch, classes, prec)
+    pl, _, _, _ = gpu_train_step(arch, classes, prec, p0, xl, yl, lr, worker=wl)
+    ps, _, _, _ = gpu_train_step(arch, classes, prec, p0, xs, ys, lr, worker=ws)
     n = L.n_state
     g = torch.from_numpy(p0.astype(np.float32)).cuda()
     dl = torch.empty(n, device="cuda")
@@ -72,8 +73,12 @@ def test_dual_batch_round(arch, classes, prec, H, bl, bs, factor):
     got = g.cpu().numpy().astype(np.float64)
     # oracle round
     cfg = net.Config(arch, classes, bf16=(prec == "bf16"))
-    sl, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xl, yl, lr)
-    ss, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xs, ys, lr)
+    dl_, ds_ = Decider(wl, bl, H, prec, TAU[prec]), Decider(ws, bs, H, prec, TAU[prec])
+    sl, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xl, yl, lr, decide=dl_)
+    ss, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xs, ys, lr, decide=ds_)
+    assert dl_.outside == 0 and ds_.outside == 0
+    wl.close()
+    ws.close()
     ref = merge.dual_merge_r1(p0, merge.worker_delta(p0, ss), merge.worker_delta(p0, sl), factor)
     tol = 1e-3 if prec == "fp32" else 2e-2
     for key in ("stem.w", "s1b1c1.w", "s2b1ds.w", "s4b2c2.w", "fc.w", "fc.b", "stem.rm", "s4b2c2.rv"):

@@ -16,7 +16,7 @@ import pytest
 from oracle import net
 from paper_2509_26092_amd import binding as B
 from paper_2509_26092_amd import inputs
-from gpu_util import TOL, compare_step, gpu_train_step, make_state
+from gpu_util import TAU, TOL, Decider, compare_step, gpu_train_step, make_state
 
 pytestmark = pytest.mark.gpu
 
@@ -24,16 +24,24 @@ LR = 0.1
 
 
 def _run_parity(arch, classes, prec, N, H, seed, lr=LR):
+    """One step on both sides; the oracle takes the kernel's subgradient
+    choice only at ReLU inputs / pool ties inside the rounding band (see
+    gpu_util.Decider), and every GPU decision outside the band must agree."""
     L, st = make_state(arch, classes, seed)
     x = inputs.images(seed, N, H, H)
     y = inputs.labels(seed, N, classes)
-    gs, gv, losses, status = gpu_train_step(arch, classes, prec, st, x, y, lr)
+    w = B.Worker(arch, classes, prec)
+    gs, gv, losses, status = gpu_train_step(arch, classes, prec, st, x, y, lr, worker=w)
     assert status == B.RN18_OK
     cfg = net.Config(arch, classes, bf16=(prec == "bf16"))
-    report, loss = compare_step(L, cfg, st, x, y, lr, gs, gv, losses[0], TOL[prec])
+    dec = Decider(w, N, H, prec, TAU[prec])
+    report, loss = compare_step(L, cfg, st, x, y, lr, gs, gv, losses[0], TOL[prec], decide=dec)
+    w.close()
     worst = max(report.items(), key=lambda kv: kv[1][0])
-    print("%s %s N=%d H=%d loss %.6f (oracle %.6f) worst %s norm-rel %.2e" %
-          (arch, prec, N, H, losses[0], loss, worst[0], worst[1][0]))
+    print("%s %s N=%d H=%d loss %.6f (oracle %.6f) worst %s norm-rel %.2e; band: %d inputs, %d kernel "
+          "choices taken, %d disagreements outside" % (arch, prec, N, H, losses[0], loss, worst[0], worst[1][0],
+                                                       dec.ambiguous, dec.taken, dec.outside))
+    assert dec.outside == 0
     return report
 
 
@@ -110,9 +118,11 @@ def test_imagenet_bf16_b256_224_launch_config_properties():
     yy = np.concatenate([y, y])
     w = B.Worker(arch, classes, prec)
     s256, v256, l256, _ = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w)
-    s256b, v256b, _, _ = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w)
+    s256b, v256b, _, _ = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w,
+                                        momentum_in=np.zeros(L.n_trainable))
     assert np.array_equal(v256, v256b), "train step is not deterministic"
-    s128, v128, l128, status = gpu_train_step(arch, classes, prec, st, x, y, LR, worker=w)
+    s128, v128, l128, status = gpu_train_step(arch, classes, prec, st, x, y, LR, worker=w,
+                                              momentum_in=np.zeros(L.n_trainable))
     assert status == B.RN18_OK
     assert abs(l256[0] - l128[0]) <= 2e-2 * abs(l128[0])
     P = L.n_trainable
