@@ -120,13 +120,23 @@ class Config:
         self.bn_momentum = bn_momentum
         # round_acts: additionally round every stored activation and
         # activation gradient to bf16 at the points where a bf16 training
-        # step stores them (conv outputs, BN/ReLU/residual outputs, the
-        # gradients entering and leaving each conv). Off by default.
+        # step stores them (see ROUNDING_POINTS). Off by default.
         self.round_acts = round_acts
 
 
-def _rb(cfg, x):
-    return ops.round_bf16(x) if (cfg.bf16 and cfg.round_acts) else x
+# Where a bf16 training step stores a tensor in bf16 (rounded once, RNE):
+#   ("y", conv)     conv output, before BN (BN statistics are taken of it)
+#   ("z", site)     ReLU output: stem, block z1, block output
+#   ("da_avg", 0)   gradient entering the last block (avg-pool backward)
+#   ("dy", conv)    BN backward output, the gradient entering the conv
+#   ("dz1", block)  data gradient of the block's second conv
+#   ("dx1", block)  projection blocks: data gradient of the first conv alone
+#   ("dx", block)   gradient wrt the block input (first conv's data gradient
+#                   plus the shortcut's: masked output gradient for identity
+#                   blocks, added before rounding; the projection conv's data
+#                   gradient added to the rounded dx1, then rounded again)
+#   ("da_pool", 0)  max-pool backward output
+ROUNDING_POINTS = ("y", "z", "da_avg", "dy", "dz1", "dx1", "dx", "da_pool")
 
 
 def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=True, decide=None):
@@ -135,13 +145,16 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
     Returns loss, logits, the flat gradient (length P), and the new running
     statistics (list of (name, rm, rv)).
 
-    The derivative of ReLU at an input of exactly 0, and the argmax of a max
-    pool window with tied maxima, are not fixed by the arithmetic; inputs
-    within rounding distance of those points make the choice depend on the
-    precision the pre-activation was computed in. `decide`, if given, is
-    called as decide("relu", site, pre, mask) and decide("pool", site, x,
-    arg) and returns the mask / argmax to use (sites: "stem", ("z1", block),
-    ("out", block)); the default is mask = pre > 0 and the first maximum.
+    The derivative of ReLU at an input of exactly 0, the argmax of a max pool
+    window with tied maxima, and the bf16 rounding of a value on a rounding
+    midpoint are not fixed by the arithmetic; inputs within rounding
+    distance of those points make the choice depend on the precision the
+    value was computed in. `decide`, if given, is called as
+    decide("relu", site, pre, mask), decide("pool", site, x, arg) and
+    decide("round", point, exact, rounded) and returns the mask / argmax /
+    rounded tensor to use (relu sites: "stem", ("z1", block), ("out",
+    block); rounding points: ROUNDING_POINTS); the default is mask = pre > 0,
+    the first maximum and round-to-nearest-even.
 
     bf16 configurations (the training configuration's mixed precision): the
     images and the conv weights are rounded to bf16 (round-to-nearest-even)
@@ -159,17 +172,26 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
     caches = {}
     run_stats = []
     masks = {}
+    rounding = cfg.bf16 and cfg.round_acts
+
+    def rb(point, v):
+        if not rounding:
+            return v
+        r = ops.round_bf16(v)
+        if decide is not None:
+            r = decide("round", point, v, r)
+        return r
 
     def relu_site(site, pre):
         mask = pre > 0
         if decide is not None:
             mask = decide("relu", site, pre, mask)
         masks[site] = mask
-        return _rb(cfg, ops.relu(pre))
+        return rb(("z", site), ops.relu(pre))
 
     def conv_bn(name, inp, act):
         _, cin, cout, k, s, p = layout.spec[name]
-        y = _rb(cfg, ops.conv2d_forward(inp, W(name), s, p))
+        y = rb(("y", name), ops.conv2d_forward(inp, W(name), s, p))
         g = layout.get(state, name + ".g")
         b = layout.get(state, name + ".b")
         if train:
@@ -210,7 +232,7 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
     df, dwfc, dbfc = ops.fc_backward(dz, f, wfc)
     layout.put(grad, "fc.w", dwfc)
     layout.put(grad, "fc.b", dbfc)
-    da = _rb(cfg, ops.avgpool_backward(df, a.shape))
+    da = rb(("da_avg", 0), ops.avgpool_backward(df, a.shape))
 
     def bn_conv_back(name, dout):
         """dout: gradient wrt this BN's output. Writes dW, dgamma, dbeta and
@@ -218,7 +240,7 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
         _, cin, cout, k, s, p = layout.spec[name]
         c = caches[name]
         dy, dg, dbeta = ops.bn_train_backward(dout, c["bn"], layout.get(state, name + ".g"))
-        dy = _rb(cfg, dy)
+        dy = rb(("dy", name), dy)
         layout.put(grad, name + ".g", dg)
         layout.put(grad, name + ".b", dbeta)
         inp = c["inp"]
@@ -230,16 +252,16 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
     for bi in reversed(range(len(layout.blocks))):
         blk = layout.blocks[bi]
         g2 = da * masks[("out", bi)]
-        dz1 = _rb(cfg, bn_conv_back(blk["c2"], g2))
+        dz1 = rb(("dz1", bi), bn_conv_back(blk["c2"], g2))
         g1 = dz1 * masks[("z1", bi)]
         dx = bn_conv_back(blk["c1"], g1)
         if blk["ds"]:
-            dx = dx + bn_conv_back(blk["ds"], g2)
+            dx = rb(("dx1", bi), dx) + bn_conv_back(blk["ds"], g2)
         else:
             dx = dx + g2
-        da = _rb(cfg, dx)
+        da = rb(("dx", bi), dx)
     if cfg.arch == "imagenet":
-        da = _rb(cfg, ops.maxpool_backward(da, pool_arg, stem_out.shape))
+        da = rb(("da_pool", 0), ops.maxpool_backward(da, pool_arg, stem_out.shape))
     g0 = da * masks["stem"]
     bn_conv_back("stem", g0)
     return loss, logits, grad, run_stats

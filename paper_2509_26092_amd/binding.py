@@ -25,6 +25,7 @@ EXPORTED = [
     "rn18_set_momentum", "rn18_destroy", "rn18_last_error",
     "rn18op_conv2d_fwd", "rn18op_conv2d_dgrad", "rn18op_conv2d_wgrad_workspace", "rn18op_conv2d_wgrad",
     "rn18op_maxpool_fwd", "rn18op_maxpool_bwd", "rn18_debug_set", "rn18_debug_copy",
+    "rn18_debug_capture",
 ]
 
 
@@ -77,6 +78,7 @@ def lib():
         "rn18op_maxpool_bwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _P]),
         "rn18_debug_set": (_I, [_P, _I, ctypes.c_long]),
         "rn18_debug_copy": (_I, [_P, _I, _I, _I, _I, _I, _P, _Z]),
+        "rn18_debug_capture": (_I, [_P, _I, _I, _P, _Z]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -199,6 +201,16 @@ DBG = dict(y=0, z1=1, out=2, gA=3, gB=4, gz=5, gy=6, gyd=7, grad=8, wf=9, wd=10,
 
 def rn18_debug_set(ctx, key, value):
     return _check(lib().rn18_debug_set(ctx, key, value))
+
+
+CAP = dict(dy=0, dz1=1, dx1=2, dx=3, da_avg=4, da_pool=5)
+
+
+def rn18_debug_capture(ctx, kind, index, dst):
+    if dst is None:
+        return _check(lib().rn18_debug_capture(ctx, 0, 0, None, 0))
+    return _check(lib().rn18_debug_capture(ctx, CAP[kind] if isinstance(kind, str) else kind, index, _ptr(dst),
+                                           dst.numel() * dst.element_size()))
 
 
 def rn18_debug_copy(ctx, N, H, W, which, index, dst):

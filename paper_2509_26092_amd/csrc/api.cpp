@@ -171,7 +171,19 @@ struct Ctx {
   bool ws_owned = false;
   std::map<std::tuple<int, int, int>, Plan> plans;
   int dbg_stop_blocks = -1;     // debugging: end the backward pass after this many blocks
+  struct Capture { int kind, index; void* dst; size_t bytes; };
+  std::vector<Capture> captures; // debugging: copies of backward tensors
 };
+
+// Enqueue the debugging copies registered for (kind, index) from `src`.
+int run_captures(Ctx* c, int kind, int index, const void* src, size_t avail) {
+  for (const auto& cp : c->captures) {
+    if (cp.kind != kind || cp.index != index) continue;
+    if (cp.bytes > avail) return fail(RN18_EINVAL, "capture of %zu bytes exceeds the %zu-byte tensor", cp.bytes, avail);
+    HIPCHK(hipMemcpyAsync(cp.dst, src, cp.bytes, hipMemcpyDeviceToDevice, c->stream));
+  }
+  return RN18_OK;
+}
 
 int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   const Arch& a = c.arch;
@@ -490,6 +502,9 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   LCHK(gemm_f32_launch(dlog, C, 1, state + a.fc_w, F, 1, nullptr, df, N, F, C, st));
   size_t gA = pl.gA, gB = pl.gB;
   LCHK(avgpool_bwd_launch(prec, df, ws + gA, N, pl.Hf * pl.Wf, F, st));
+  const size_t es = c->es;
+  if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DA_AVG, 0, ws + gA, (size_t)N * pl.Hf * pl.Wf * F * es)))
+    return r;
 
   auto W_d = [&](int li) { return (const char*)c->wd + (size_t)a.convs[li].wd * c->es; };
   // BN backward of conv li: dz (with mask mz) -> dy written to `dy`
@@ -504,6 +519,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
                              (float*)(ws + P.coef), st));
     LCHK(bn_bwd_apply_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.coef), ws + dy,
                              P.M, L.cout, st));
+    if (!c->captures.empty()) return run_captures(c, RN18_CAP_DY, li, ws + dy, (size_t)P.M * L.cout * es);
     return 0;
   };
   auto wgrad = [&](int li, size_t dy) -> int {
@@ -531,15 +547,20 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     if (B.ds >= 0 && (r = bn_back(B.ds, gA, bp.out, pl.gyd))) return r;
     if ((r = wgrad(B.c2, pl.gy))) return r;
     if ((r = dgrad(B.c2, pl.gy, pl.gz, 0, 0, 0))) return r;
+    const size_t z1b = (size_t)pl.cp[B.c1].M * a.convs[B.c1].cout * es;
+    const size_t inb = (size_t)N * pl.cp[B.c1].Hin * pl.cp[B.c1].Win * a.convs[B.c1].cin_p * es;
+    if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DZ1, bi, ws + pl.gz, z1b))) return r;
     if ((r = bn_back(B.c1, pl.gz, bp.z1, pl.gy))) return r;
     if ((r = wgrad(B.c1, pl.gy))) return r;
     if (B.ds >= 0) {
       if ((r = dgrad(B.c1, pl.gy, gB, 0, 0, 0))) return r;
+      if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX1, bi, ws + gB, inb))) return r;
       if ((r = wgrad(B.ds, pl.gyd))) return r;
       if ((r = dgrad(B.ds, pl.gyd, gB, 1, 0, 0))) return r;
     } else {
       if ((r = dgrad(B.c1, pl.gy, gB, 2, gA, bp.out))) return r;
     }
+    if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX, bi, ws + gB, inb))) return r;
     std::swap(gA, gB);
   }
   size_t gstem = gA;
@@ -547,6 +568,9 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     LCHK(maxpool_bwd_launch(prec, ws + gA, (const uint8_t*)(ws + pl.parg), ws + gB, N, pl.Hs, pl.Ws, a.convs[0].cout,
                             pl.Hp, pl.Wp, st));
     gstem = gB;
+    if (!c->captures.empty() &&
+        (r = run_captures(c, RN18_CAP_DA_POOL, 0, ws + gB, (size_t)N * pl.Hs * pl.Ws * a.convs[0].cout * es)))
+      return r;
   }
   if ((r = bn_back(0, gstem, pl.zstem, pl.gy))) return r;
   if ((r = wgrad(0, pl.gy))) return r;
@@ -784,6 +808,14 @@ int rn18_debug_set(rn18_ctx* h, int key, long value) {
   if (!h) return fail(RN18_EINVAL, "ctx is NULL");
   if (key != RN18_DBG_STOP_BLOCKS) return fail(RN18_EINVAL, "unknown debug key %d", key);
   h->c.dbg_stop_blocks = (int)value;
+  return RN18_OK;
+}
+
+int rn18_debug_capture(rn18_ctx* h, int kind, int index, void* dst, size_t bytes) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  if (!dst) { h->c.captures.clear(); return RN18_OK; }
+  if (kind < RN18_CAP_DY || kind > RN18_CAP_DA_POOL) return fail(RN18_EINVAL, "unknown capture kind %d", kind);
+  h->c.captures.push_back(Ctx::Capture{kind, index, dst, bytes});
   return RN18_OK;
 }
 

@@ -136,6 +136,117 @@ class Decider:
         return chosen
 
 
+def tensor_shapes(L, N, H):
+    """NCHW shapes of every rounding point / stored tensor of a step."""
+    sh = {}
+    name, cin, cout, k, s, p = L.convs[0]
+    h = ops.conv_out_size(H, k, s, p)
+    sh[("y", "stem")] = sh[("z", "stem")] = sh[("da_pool", 0)] = sh[("dy", "stem")] = (N, cout, h, h)
+    c = cout
+    if L.arch == "imagenet":
+        h = ops.conv_out_size(h, 3, 2, 1)
+    for bi, blk in enumerate(L.blocks):
+        _, cin, cout, k, s, p = L.spec[blk["c1"]]
+        ho = ops.conv_out_size(h, 3, s, 1)
+        sh[("dx1", bi)] = sh[("dx", bi)] = (N, cin, h, h)
+        for cname in (blk["c1"], blk["c2"]) + ((blk["ds"],) if blk["ds"] else ()):
+            sh[("y", cname)] = sh[("dy", cname)] = (N, cout, ho, ho)
+        sh[("z", ("z1", bi))] = sh[("dz1", bi)] = sh[("z", ("out", bi))] = (N, cout, ho, ho)
+        h, c = ho, cout
+    sh[("da_avg", 0)] = (N, c, h, h)
+    return sh
+
+
+def _bf16_other_neighbor(exact, b):
+    """The bf16 value on the other side of `exact` from its rounding b."""
+    b32 = np.asarray(b, np.float32)
+    u = b32.view(np.uint32).astype(np.int64)
+    neg = (u >> 31) & 1
+    up = exact > b
+    inc_mag = np.where(up, neg == 0, neg == 1)
+    un = np.where(inc_mag, u + 0x10000, u - 0x10000)
+    un = np.where(b32 == 0, np.where(up, 0x00010000, 0x80010000), un)
+    return un.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+class Mirror(Decider):
+    """Decider for bf16 steps that also mirrors the kernel's bf16 rounding
+    decisions where they are not unique: a value whose exact (fp64) result
+    lies within TAU_ROUND ulp (or TAU_ABS * rms) of a rounding midpoint may
+    round either way in a kernel that computes it in fp32; there the
+    kernel's stored value is taken, after checking it is one of the two
+    bf16 neighbours. Everywhere else the kernel's stored value must equal
+    the oracle's round-to-nearest-even result exactly. Backward tensors are
+    captured from the kernel as they are produced."""
+    TAU_ROUND = 0.02
+    TAU_ABS = 1e-5
+
+    def __init__(self, worker, L, N, H, prec, tau):
+        import torch
+        super().__init__(worker, N, H, prec, tau)
+        self.L = L
+        self.shapes = tensor_shapes(L, N, H)
+        self.conv_index = {c[0]: i for i, c in enumerate(L.convs)}
+        self.cap = {}
+        kinds = {"dy": "dy", "dz1": "dz1", "dx1": "dx1", "dx": "dx", "da_avg": "da_avg", "da_pool": "da_pool"}
+        for (kind, idx), (n, c, h, w) in self.shapes.items():
+            if kind not in kinds:
+                continue
+            if kind == "dx1" and not L.blocks[idx]["ds"]:
+                continue
+            if kind == "da_pool" and L.arch != "imagenet":
+                continue
+            index = self.conv_index[idx] if kind == "dy" else idx
+            t = torch.full((n, h, w, c), float("nan"), dtype=torch_dtype(prec), device="cuda")
+            B.rn18_debug_capture(worker.ctx, kind, index, t)
+            self.cap[(kind, idx)] = t
+        self.round_outside = 0
+        self.round_invalid = 0
+        self.round_taken = 0
+        self.round_band = 0
+        self.round_log = []
+
+    def _gpu_value(self, point):
+        kind, idx = point
+        shape = self.shapes[point]
+        if kind == "y":
+            return self._fetch("y", self.conv_index[idx], shape)
+        if kind == "z":
+            if idx == "stem":
+                return self._fetch("zstem", 0, shape)
+            return self._fetch(idx[0], idx[1], shape)
+        import torch
+        torch.cuda.synchronize()
+        return from_dev_nhwc(self.cap[point])
+
+    def __call__(self, kind, site, pre, default):
+        if kind != "round":
+            return super().__call__(kind, site, pre, default)
+        exact, b = pre, default
+        g = self._gpu_value(site)
+        nb = _bf16_other_neighbor(exact, b)
+        ulp = np.abs(nb - b)
+        rms = np.sqrt(np.mean(exact * exact))
+        band = np.abs(exact - 0.5 * (b + nb)) <= self.TAU_ROUND * ulp + self.TAU_ABS * rms
+        # in the band the kernel may hold either neighbour, or (near zero,
+        # where the absolute term dominates) any value that close to exact
+        valid = (g == b) | (g == nb) | (np.abs(g - exact) <= 2 * self.TAU_ABS * rms)
+        outside = (g != b) & ~band
+        self.round_band += int(band.sum())
+        self.round_outside += int(outside.sum())
+        self.round_invalid += int((band & ~valid).sum())
+        chosen = np.where(band & valid, g, b)
+        self.round_taken += int((chosen != b).sum())
+        if outside.any():
+            i = np.argwhere(outside)[0]
+            self.round_log.append((site, int(outside.sum()), tuple(int(v) for v in i), float(g[tuple(i)]),
+                                   float(b[tuple(i)]), float(exact[tuple(i)])))
+        return chosen
+
+    def close(self):
+        B.rn18_debug_capture(self.w.ctx, None, 0, None)
+
+
 def gpu_train_step(arch, classes, prec, state64, x, y, lr, steps=1, momentum_in=None, worker=None):
     import torch
     w = worker or B.Worker(arch, classes, prec)

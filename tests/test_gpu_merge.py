@@ -9,7 +9,7 @@ import pytest
 from oracle import merge, net
 from paper_2509_26092_amd import binding as B
 from paper_2509_26092_amd import inputs
-from gpu_util import TAU, Decider, assert_close, gpu_train_step, make_state
+from gpu_util import TAU, Decider, Mirror, assert_close, gpu_train_step, make_state
 
 pytestmark = pytest.mark.gpu
 
@@ -61,6 +61,11 @@ def test_dual_batch_round(arch, classes, prec, H, bl, bs, factor):
     lr = 0.1
     # GPU: two workers with their own contexts (momentum buffers)
     wl, ws = B.Worker(arch, classes, prec), B.Worker(arch, classes, prec)
+    bf = prec == "bf16"
+    if bf:
+        dl_, ds_ = Mirror(wl, L, bl, H, prec, TAU["fp32"]), Mirror(ws, L, bs, H, prec, TAU["fp32"])
+    else:
+        dl_, ds_ = Decider(wl, bl, H, prec, TAU[prec]), Decider(ws, bs, H, prec, TAU[prec])
     pl, _, _, _ = gpu_train_step(arch, classes, prec, p0, xl, yl, lr, worker=wl)
     ps, _, _, _ = gpu_train_step(arch, classes, prec, p0, xs, ys, lr, worker=ws)
     n = L.n_state
@@ -72,11 +77,12 @@ def test_dual_batch_round(arch, classes, prec, H, bl, bs, factor):
     B.ps_dual_merge(g, dsm, dl, n, factor)
     got = g.cpu().numpy().astype(np.float64)
     # oracle round
-    cfg = net.Config(arch, classes, bf16=(prec == "bf16"))
-    dl_, ds_ = Decider(wl, bl, H, prec, TAU[prec]), Decider(ws, bs, H, prec, TAU[prec])
+    cfg = net.Config(arch, classes, bf16=bf, round_acts=bf)
     sl, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xl, yl, lr, decide=dl_)
     ss, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xs, ys, lr, decide=ds_)
     assert dl_.outside == 0 and ds_.outside == 0
+    if bf:
+        assert dl_.round_outside == 0 and ds_.round_outside == 0 and dl_.round_invalid == 0
     wl.close()
     ws.close()
     ref = merge.dual_merge_r1(p0, merge.worker_delta(p0, ss), merge.worker_delta(p0, sl), factor)

@@ -16,7 +16,7 @@ import pytest
 from oracle import net
 from paper_2509_26092_amd import binding as B
 from paper_2509_26092_amd import inputs
-from gpu_util import TAU, TOL, Decider, compare_step, gpu_train_step, make_state
+from gpu_util import TAU, TOL, Decider, Mirror, compare_step, gpu_train_step, make_state
 
 pytestmark = pytest.mark.gpu
 
@@ -24,24 +24,33 @@ LR = 0.1
 
 
 def _run_parity(arch, classes, prec, N, H, seed, lr=LR):
-    """One step on both sides; the oracle takes the kernel's subgradient
-    choice only at ReLU inputs / pool ties inside the rounding band (see
-    gpu_util.Decider), and every GPU decision outside the band must agree."""
+    """One step on both sides. The oracle takes the kernel's choice only at
+    non-unique points inside the rounding band (ReLU kinks, pool ties and,
+    for bf16, rounding midpoints of the stored tensors; see gpu_util), and
+    every kernel decision outside the band must agree with the oracle's."""
     L, st = make_state(arch, classes, seed)
     x = inputs.images(seed, N, H, H)
     y = inputs.labels(seed, N, classes)
     w = B.Worker(arch, classes, prec)
+    bf = prec == "bf16"
+    dec = Mirror(w, L, N, H, prec, TAU["fp32"]) if bf else Decider(w, N, H, prec, TAU[prec])
     gs, gv, losses, status = gpu_train_step(arch, classes, prec, st, x, y, lr, worker=w)
     assert status == B.RN18_OK
-    cfg = net.Config(arch, classes, bf16=(prec == "bf16"))
-    dec = Decider(w, N, H, prec, TAU[prec])
-    report, loss = compare_step(L, cfg, st, x, y, lr, gs, gv, losses[0], TOL[prec], decide=dec)
-    w.close()
+    cfg = net.Config(arch, classes, bf16=bf, round_acts=bf)
+    try:
+        report, loss = compare_step(L, cfg, st, x, y, lr, gs, gv, losses[0], TOL[prec], decide=dec)
+    finally:
+        if bf:
+            print("bf16 rounding band %d, kernel choices taken %d, invalid %d, outside %d %s" %
+                  (dec.round_band, dec.round_taken, dec.round_invalid, dec.round_outside, dec.round_log[:4]))
+        print("relu/pool band %d, taken %d, outside %d" % (dec.ambiguous, dec.taken, dec.outside))
+        w.close()
     worst = max(report.items(), key=lambda kv: kv[1][0])
-    print("%s %s N=%d H=%d loss %.6f (oracle %.6f) worst %s norm-rel %.2e; band: %d inputs, %d kernel "
-          "choices taken, %d disagreements outside" % (arch, prec, N, H, losses[0], loss, worst[0], worst[1][0],
-                                                       dec.ambiguous, dec.taken, dec.outside))
+    print("%s %s N=%d H=%d loss %.6f (oracle %.6f) worst %s norm-rel %.2e" %
+          (arch, prec, N, H, losses[0], loss, worst[0], worst[1][0]))
     assert dec.outside == 0
+    if bf:
+        assert dec.round_outside == 0 and dec.round_invalid == 0
     return report
 
 
@@ -103,34 +112,51 @@ def test_eval_logits_parity():
 
 
 def test_imagenet_bf16_b256_224_launch_config_properties():
-    """At the full ImageNet batch-256 224x224 configuration: (a) a batch made
-    of two copies of 128 images has the same BN statistics, mean loss and
-    gradients as the 128 images alone (exactly, in real arithmetic); (b) the
-    step is deterministic; (c) eval logits of sampled images match the
-    oracle evaluated on those images alone."""
+    """At the ImageNet batch-256 224x224 launch configuration itself:
+    (a) the step is bitwise deterministic; (b) sampled stem-conv outputs
+    equal the oracle's conv of those images alone, rounded to bf16 (exact
+    except inside the rounding band); (c) a batch of two copies of 128
+    images has the same loss and the same stem BN statistics as the 128
+    images alone; (d) eval-mode logits of sampled images match the oracle
+    run on each image alone. (Full-step gradients at this size are checked
+    against the oracle at reduced batch with the same kernels; bf16
+    rounding differences are chaotic across two batch sizes, so no
+    GPU-vs-GPU gradient comparison is made.)"""
     import torch
-    from gpu_util import assert_close
+    from gpu_util import Mirror, assert_close, from_dev_nhwc
+    from oracle import ops
     arch, classes, prec = "imagenet", 1000, "bf16"
     L, st = make_state(arch, classes, 150)
     x = inputs.images(150, 128, 224, 224)
     y = inputs.labels(150, 128, classes)
     xx = np.concatenate([x, x])
     yy = np.concatenate([y, y])
+    z = np.zeros(L.n_trainable)
     w = B.Worker(arch, classes, prec)
-    s256, v256, l256, _ = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w)
-    s256b, v256b, _, _ = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w,
-                                        momentum_in=np.zeros(L.n_trainable))
-    assert np.array_equal(v256, v256b), "train step is not deterministic"
-    s128, v128, l128, status = gpu_train_step(arch, classes, prec, st, x, y, LR, worker=w,
-                                              momentum_in=np.zeros(L.n_trainable))
-    assert status == B.RN18_OK
-    assert abs(l256[0] - l128[0]) <= 2e-2 * abs(l128[0])
-    P = L.n_trainable
-    for key in ("stem.w", "s1b1c1.w", "s2b1ds.w", "s3b2c2.w", "s4b2c2.w", "s4b2c2.g", "fc.w", "fc.b"):
-        o, shp = L.off[key]
-        n = int(np.prod(shp))
-        assert_close(v256[o:o + n], v128[o:o + n], 2e-2, key + " duplicated-batch gradient")
-    # eval-mode logits of sampled images, one by one against the oracle
+    s256, v256, l256, st256 = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w, momentum_in=z)
+    ystem = torch.empty((256, 112, 112, 64), dtype=torch.bfloat16, device="cuda")
+    B.rn18_debug_copy(w.ctx, 256, 224, 224, "y", 0, ystem)
+    mean256 = torch.empty(64, device="cuda")
+    B.rn18_debug_copy(w.ctx, 256, 224, 224, "mean", 0, mean256)
+    s256b, v256b, _, _ = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w, momentum_in=z)
+    assert st256 == B.RN18_OK
+    assert np.array_equal(v256, v256b) and np.array_equal(s256, s256b), "train step is not deterministic"
+    # (b) sampled stem outputs, mirrored rounding check
+    wst = ops.round_bf16(L.get(st, "stem.w"))
+    for i in (0, 93, 255):
+        exact = ops.conv2d_forward(ops.round_bf16(xx[i:i + 1]), wst, 2, 3)
+        got = from_dev_nhwc(ystem[i:i + 1])
+        b = ops.round_bf16(exact)
+        mism = got != b
+        assert mism.mean() < 1e-3, mism.mean()            # 1-ulp differences at rounding midpoints only
+        assert_close(got, exact, 8e-3, "stem conv output of image %d" % i)
+    # (c) duplicated batch
+    s128, v128, l128, _ = gpu_train_step(arch, classes, prec, st, x, y, LR, worker=w, momentum_in=z)
+    mean128 = torch.empty(64, device="cuda")
+    B.rn18_debug_copy(w.ctx, 128, 224, 224, "mean", 0, mean128)
+    assert abs(l256[0] - l128[0]) <= 1e-2 * abs(l128[0])
+    assert_close(mean256.cpu().numpy(), mean128.cpu().numpy(), 1e-4, "stem BN mean, duplicated batch")
+    # (d) eval-mode logits of sampled images, one by one against the oracle
     logits = torch.empty((256, classes), dtype=torch.float32, device="cuda")
     w.eval_logits(torch.from_numpy(st.astype(np.float32)).cuda(), torch.from_numpy(xx).cuda(), logits)
     lg = logits.cpu().numpy()
@@ -138,6 +164,7 @@ def test_imagenet_bf16_b256_224_launch_config_properties():
     for i in (0, 77, 200):
         ref = net.eval_logits(cfg, L, st, xx[i:i + 1])
         assert_close(lg[i:i + 1], ref, 2e-2, "eval logits of image %d" % i)
+    assert np.all(np.isfinite(v256))
     w.close()
 
 
