@@ -147,6 +147,30 @@ void rn18_destroy(rn18_ctx* ctx);
 
 const char* rn18_last_error(void);
 
+/* Measurement. With profiling enabled, every kernel launch group of later
+ * calls on the context is bracketed by HIP events on the context stream.
+ * rn18_profile_read waits for the stream, returns up to `max` records in
+ * launch order (count = the number recorded) and clears them. flops and
+ * bytes are the algorithmic work of the launch (real channels only, no
+ * padding, no re-reads): multiply-adds x 2 for convolutions and the
+ * classifier, compulsory HBM bytes for the streaming kernels. */
+enum {
+  RN18_K_CONV_FWD = 0, RN18_K_CONV_DGRAD = 1, RN18_K_CONV_WGRAD = 2, RN18_K_WGRAD_REDUCE = 3,
+  RN18_K_BN_STATS = 4, RN18_K_BN_APPLY = 5, RN18_K_BN_BWD_REDUCE = 6, RN18_K_BN_BWD_APPLY = 7,
+  RN18_K_MAXPOOL = 8, RN18_K_AVGPOOL = 9, RN18_K_HEAD = 10, RN18_K_SGD = 11, RN18_K_PREP = 12
+};
+typedef struct {
+  int cls;       /* RN18_K_* */
+  int layer;     /* conv layer in forward order, or a sub-index */
+  int tile;      /* convolutions: tile shape BM*1000+BN of the kernel instance */
+  int pad_;
+  double flops;  /* algorithmic floating-point operations */
+  double bytes;  /* algorithmic bytes */
+  double ms;     /* event-measured duration */
+} rn18_prof_rec;
+int rn18_profile_enable(rn18_ctx* ctx, int on);
+int rn18_profile_read(rn18_ctx* ctx, rn18_prof_rec* out, int max, int* count);
+
 #ifdef __cplusplus
 }
 #endif

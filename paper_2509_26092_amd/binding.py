@@ -22,7 +22,7 @@ PREC_IDS = {"fp32": RN18_FP32, "bf16": RN18_BF16}
 EXPORTED = [
     "rn18_state_floats", "rn18_init", "rn18_workspace_bytes", "rn18_set_workspace", "rn18_train_step",
     "rn18_eval_logits", "ps_dual_merge", "ps_worker_delta", "rn18_sync_status", "rn18_get_momentum",
-    "rn18_set_momentum", "rn18_destroy", "rn18_last_error",
+    "rn18_set_momentum", "rn18_destroy", "rn18_last_error", "rn18_profile_enable", "rn18_profile_read",
     "rn18op_conv2d_fwd", "rn18op_conv2d_dgrad", "rn18op_conv2d_wgrad_workspace", "rn18op_conv2d_wgrad",
     "rn18op_maxpool_fwd", "rn18op_maxpool_bwd", "rn18_debug_set", "rn18_debug_copy",
     "rn18_debug_capture",
@@ -33,6 +33,15 @@ class Rn18Error(RuntimeError):
     def __init__(self, code, msg):
         super().__init__("rn18 error %d: %s" % (code, msg))
         self.code = code
+
+
+class rn18_prof_rec(ctypes.Structure):
+    _fields_ = [("cls", ctypes.c_int), ("layer", ctypes.c_int), ("tile", ctypes.c_int), ("pad_", ctypes.c_int),
+                ("flops", ctypes.c_double), ("bytes", ctypes.c_double), ("ms", ctypes.c_double)]
+
+
+K_NAMES = ["conv_fwd", "conv_dgrad", "conv_wgrad", "wgrad_reduce", "bn_stats", "bn_apply", "bn_bwd_reduce",
+           "bn_bwd_apply", "maxpool", "avgpool", "head", "sgd", "prep"]
 
 
 class rn18_config(ctypes.Structure):
@@ -77,6 +86,8 @@ def lib():
         "rn18op_maxpool_fwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _P]),
         "rn18op_maxpool_bwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _P]),
         "rn18_debug_set": (_I, [_P, _I, ctypes.c_long]),
+        "rn18_profile_enable": (_I, [_P, _I]),
+        "rn18_profile_read": (_I, [_P, ctypes.POINTER(rn18_prof_rec), _I, ctypes.POINTER(_I)]),
         "rn18_debug_copy": (_I, [_P, _I, _I, _I, _I, _I, _P, _Z]),
         "rn18_debug_capture": (_I, [_P, _I, _I, _P, _Z]),
     }
@@ -163,6 +174,19 @@ def rn18_set_momentum(ctx, src):
 
 def rn18_destroy(ctx):
     lib().rn18_destroy(ctx)
+
+
+def rn18_profile_enable(ctx, on):
+    return _check(lib().rn18_profile_enable(ctx, 1 if on else 0))
+
+
+def rn18_profile_read(ctx, max_records=4096):
+    """Profile records (kernel class, layer, tile, flops, bytes, ms) in launch order."""
+    buf = (rn18_prof_rec * max_records)()
+    n = _I(0)
+    _check(lib().rn18_profile_read(ctx, buf, max_records, ctypes.byref(n)))
+    return [dict(cls=K_NAMES[r.cls], layer=r.layer, tile=r.tile, flops=r.flops, bytes=r.bytes, ms=r.ms)
+            for r in buf[:min(n.value, max_records)]]
 
 
 def rn18_last_error():

@@ -173,7 +173,41 @@ struct Ctx {
   int dbg_stop_blocks = -1;     // debugging: end the backward pass after this many blocks
   struct Capture { int kind, index; void* dst; size_t bytes; };
   std::vector<Capture> captures; // debugging: copies of backward tensors
+  // optional per-launch timing with HIP events on the context stream
+  struct ProfEv { int cls, layer, tile; double flops, bytes; hipEvent_t a, b; };
+  bool prof_on = false;
+  std::vector<ProfEv> prof;
+  std::vector<hipEvent_t> prof_spare;
 };
+
+hipEvent_t prof_event(Ctx* c) {
+  if (!c->prof_spare.empty()) {
+    hipEvent_t e = c->prof_spare.back();
+    c->prof_spare.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Start a timed launch group; returns its index or -1 when profiling is off.
+int prof_begin(Ctx* c, int cls, int layer, int tile, double flops, double bytes) {
+  if (!c || !c->prof_on) return -1;
+  Ctx::ProfEv ev{cls, layer, tile, flops, bytes, prof_event(c), prof_event(c)};
+  if (!ev.a || !ev.b || hipEventRecord(ev.a, c->stream) != hipSuccess) return -1;
+  c->prof.push_back(ev);
+  return (int)c->prof.size() - 1;
+}
+void prof_end(Ctx* c, int idx) {
+  if (idx >= 0) (void)hipEventRecord(c->prof[idx].b, c->stream);
+}
+#define TIMED(cls, layer, tile, fl, by, expr) \
+  do {                                         \
+    const int pi_ = prof_begin(c, cls, layer, tile, fl, by); \
+    LCHK(expr);                                \
+    prof_end(c, pi_);                          \
+  } while (0)
 
 // Enqueue the debugging copies registered for (kind, index) from `src`.
 int run_captures(Ctx* c, int kind, int index, const void* src, size_t avail) {
@@ -315,7 +349,9 @@ ConvGather gather_fwd(const void* x, const void* w, void* y, int N, int Hin, int
 // Data gradient of a conv with input [N][H][W][Cin] and output [N][Ho][Wo][Cout].
 // mode: 0 store, 1 accumulate, 2 add masked residual (R, Rm).
 int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int H, int W, int Cin, int Ho, int Wo,
-                 int Cout, int k, int s, int p, int mode, const void* R, const void* Rm, hipStream_t st) {
+                 int Cout, int k, int s, int p, int mode, const void* R, const void* Rm, hipStream_t st,
+                 Ctx* c = nullptr, int layer = -1, int cin_real = 0) {
+  const double creal = cin_real > 0 ? cin_real : Cin;
   if (s == 1) {
     ConvGather g{};
     g.A = dy; g.B = wd; g.C = dx; g.R = R; g.Rm = Rm;
@@ -329,7 +365,10 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
     g.wkh0 = k - 1; g.wkhs = -1; g.wkw0 = k - 1; g.wkws = -1; g.KW = k; g.KHW = k * k;
     g.K = k * k * Cout;
     g.mode = mode;
-    return conv_gather_launch(prec, g, st);
+    const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(g), 2.0 * g.M * creal * g.K, 0.0);
+    const int r = conv_gather_launch(prec, g, st);
+    prof_end(c, pi);
+    return r;
   }
   if (s != 2) return -1;
   for (int ph = 0; ph < 2; ++ph)
@@ -355,7 +394,9 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
         if (mode == 1) continue;   // nothing to add
         g.nth = 1; g.ntw = 1;      // K = 0: the kernel writes acc = 0 (+ residual)
       }
+      const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(g), 2.0 * g.M * creal * g.K, 0.0);
       const int r = conv_gather_launch(prec, g, st);
+      prof_end(c, pi);
       if (r) return r;
     }
   return 0;
@@ -363,7 +404,7 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
 
 int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float* wpart, int N, int H, int W, int Cin,
                       int cin_real, int Ho, int Wo, int Cout, int k, int s, int p, int splits, int pps,
-                      hipStream_t st) {
+                      hipStream_t st, Ctx* c = nullptr, int layer = -1) {
   ConvWgrad g{};
   g.DY = dy; g.X = x; g.P = wpart;
   g.N = N; g.H = H; g.W = W; g.Cin = Cin; g.Ho = Ho; g.Wo = Wo; g.Cout = Cout;
@@ -372,9 +413,16 @@ int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float
   g.Kcols = k * k * Cin;
   g.pix_per_split = pps;
   g.splits = splits;
+  const double mpix = (double)N * Ho * Wo;
+  int pi = prof_begin(c, RN18_K_CONV_WGRAD, layer, conv_wgrad_tile(Cout), 2.0 * Cout * k * k * cin_real * mpix,
+                      (double)splits * Cout * g.Kcols * 4);
   int r = conv_wgrad_launch(prec, g, st);
+  prof_end(c, pi);
   if (r) return r;
-  return wgrad_reduce_launch(wpart, splits, Cout, k * k, Cin, cin_real, out, st);
+  pi = prof_begin(c, RN18_K_WGRAD_REDUCE, layer, 0, 0.0, ((double)splits + 1.0) * Cout * g.Kcols * 4);
+  r = wgrad_reduce_launch(wpart, splits, Cout, k * k, Cin, cin_real, out, st);
+  prof_end(c, pi);
+  return r;
 }
 
 // ----------------------------------------------------------------------------
@@ -422,14 +470,19 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
   const float eps = c->cfg.bn_eps, mom = c->cfg.bn_momentum;
   auto W = [&](int li) { return (const char*)c->wf + (size_t)a.convs[li].wf * c->es; };
 
-  LCHK(repack_launch(prec, state_c, c->wf, c->wd, c->tab, c->ntab, a.wf_total, st));
-  LCHK(ingest_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, a.convs[0].cin_p, st));
+  const double es = c->es;
+  TIMED(RN18_K_PREP, -1, 0, 0.0, (double)a.wf_total * (4.0 + 2.0 * es),
+        repack_launch(prec, state_c, c->wf, c->wd, c->tab, c->ntab, a.wf_total, st));
+  TIMED(RN18_K_PREP, -1, 1, 0.0, (double)N * pl.H * pl.W * (12.0 + a.convs[0].cin_p * es),
+        ingest_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, a.convs[0].cin_p, st));
 
   auto conv_bn = [&](int li) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     ConvGather g = gather_fwd(ws + P.x, W(li), ws + P.y, N, P.Hin, P.Win, L.cin_p, P.Ho, P.Wo, L.cout, L.k, L.s, L.p);
-    LCHK(conv_gather_launch(prec, g, st));
+    const double xb = (double)N * P.Hin * P.Win * L.cin_p * es, yb = (double)P.M * L.cout * es;
+    TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(g), 2.0 * P.M * L.cout * L.k * L.k * L.cin,
+          xb + yb + (double)L.cout * L.k * L.k * L.cin_p * es, conv_gather_launch(prec, g, st));
     float* mean = (float*)(ws + P.mean);
     float* rstd = (float*)(ws + P.rstd);
     float* sc = (float*)(ws + P.scale);
@@ -437,9 +490,10 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     if (train) {
       int nblk = 0;
       float* part = (float*)(ws + pl.part);
-      LCHK(bn_stats_partial_launch(prec, ws + P.y, P.M, L.cout, part, &nblk, st));
-      LCHK(bn_stats_final_launch(prec, ws + P.y, part, nblk, P.M, L.cout, state_c + L.g, state_c + L.b, eps, mom,
-                                 state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, st));
+      TIMED(RN18_K_BN_STATS, li, 0, 0.0, yb, bn_stats_partial_launch(prec, ws + P.y, P.M, L.cout, part, &nblk, st));
+      TIMED(RN18_K_BN_STATS, li, 1, 0.0, 0.0,
+            bn_stats_final_launch(prec, ws + P.y, part, nblk, P.M, L.cout, state_c + L.g, state_c + L.b, eps, mom,
+                                  state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, st));
     } else {
       LCHK(bn_eval_coef_launch(state_c + L.g, state_c + L.b, state_c + L.rm, state_c + L.rv, eps, L.cout, sc, sf, st));
     }
@@ -450,8 +504,9 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     const ConvP& P = pl.cp[li];
     const float* sc2 = li2 >= 0 ? (const float*)(ws + pl.cp[li2].scale) : nullptr;
     const float* sf2 = li2 >= 0 ? (const float*)(ws + pl.cp[li2].shift) : nullptr;
-    LCHK(bn_apply_launch(prec, ws + P.y, (float*)(ws + P.scale), (float*)(ws + P.shift), relu, res_mode,
-                         res_mode ? ws + r : nullptr, sc2, sf2, ws + z, P.M, L.cout, st));
+    TIMED(RN18_K_BN_APPLY, li, res_mode, 0.0, (double)P.M * L.cout * es * (res_mode ? 3 : 2),
+          bn_apply_launch(prec, ws + P.y, (float*)(ws + P.scale), (float*)(ws + P.shift), relu, res_mode,
+                          res_mode ? ws + r : nullptr, sc2, sf2, ws + z, P.M, L.cout, st));
     return 0;
   };
 
@@ -459,8 +514,10 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
   if ((r = conv_bn(0))) return r;
   if ((r = apply(0, 1, 0, 0, -1, pl.zstem))) return r;
   if (a.imagenet)
-    LCHK(maxpool_fwd_launch(prec, ws + pl.zstem, ws + pl.pool, (uint8_t*)(ws + pl.parg), N, pl.Hs, pl.Ws,
-                            a.convs[0].cout, pl.Hp, pl.Wp, st));
+    TIMED(RN18_K_MAXPOOL, 0, 0, 0.0,
+          (double)N * a.convs[0].cout * ((double)pl.Hs * pl.Ws * es + (double)pl.Hp * pl.Wp * (es + 1)),
+          maxpool_fwd_launch(prec, ws + pl.zstem, ws + pl.pool, (uint8_t*)(ws + pl.parg), N, pl.Hs, pl.Ws,
+                             a.convs[0].cout, pl.Hp, pl.Wp, st));
   for (size_t bi = 0; bi < a.blocks.size(); ++bi) {
     const BlockL& B = a.blocks[bi];
     const BlockP& bp = pl.bp[bi];
@@ -475,7 +532,8 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     }
   }
   const size_t last = pl.bp.back().out;
-  LCHK(avgpool_fwd_launch(prec, ws + last, (float*)(ws + pl.f), N, pl.Hf * pl.Wf, a.feat, st));
+  TIMED(RN18_K_AVGPOOL, 0, 0, 0.0, (double)N * a.feat * ((double)pl.Hf * pl.Wf * es + 4),
+        avgpool_fwd_launch(prec, ws + last, (float*)(ws + pl.f), N, pl.Hf * pl.Wf, a.feat, st));
   return RN18_OK;
 }
 
@@ -493,16 +551,19 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   float* dlog = (float*)(ws + pl.dlogits);
   float* df = (float*)(ws + pl.df);
   float* grad = (float*)(ws + pl.grad);
-  LCHK(gemm_f32_launch(f, F, 1, state + a.fc_w, 1, F, state + a.fc_b, logits, N, C, F, st));
-  LCHK(softmax_ce_launch(logits, labels, N, C, dlog, (float*)(ws + pl.rowloss), loss ? loss : (float*)(ws + pl.lossbuf),
-                         c->err, st));
+  const double fcf = 2.0 * N * C * F;
+  TIMED(RN18_K_HEAD, 0, 0, fcf, 0.0, gemm_f32_launch(f, F, 1, state + a.fc_w, 1, F, state + a.fc_b, logits, N, C, F, st));
+  TIMED(RN18_K_HEAD, 1, 0, 0.0, 8.0 * N * C,
+        softmax_ce_launch(logits, labels, N, C, dlog, (float*)(ws + pl.rowloss),
+                          loss ? loss : (float*)(ws + pl.lossbuf), c->err, st));
   // classifier backward: dW = dz^T f, db = sum dz, df = dz W
-  LCHK(gemm_f32_launch(dlog, 1, C, f, F, 1, nullptr, grad + a.fc_w, C, F, N, st));
-  LCHK(colsum_launch(dlog, N, C, grad + a.fc_b, st));
-  LCHK(gemm_f32_launch(dlog, C, 1, state + a.fc_w, F, 1, nullptr, df, N, F, C, st));
+  TIMED(RN18_K_HEAD, 2, 0, fcf, 0.0, gemm_f32_launch(dlog, 1, C, f, F, 1, nullptr, grad + a.fc_w, C, F, N, st));
+  TIMED(RN18_K_HEAD, 3, 0, 0.0, 4.0 * N * C, colsum_launch(dlog, N, C, grad + a.fc_b, st));
+  TIMED(RN18_K_HEAD, 4, 0, fcf, 0.0, gemm_f32_launch(dlog, C, 1, state + a.fc_w, F, 1, nullptr, df, N, F, C, st));
   size_t gA = pl.gA, gB = pl.gB;
-  LCHK(avgpool_bwd_launch(prec, df, ws + gA, N, pl.Hf * pl.Wf, F, st));
   const size_t es = c->es;
+  TIMED(RN18_K_AVGPOOL, 1, 0, 0.0, (double)N * F * ((double)pl.Hf * pl.Wf * es + 4),
+        avgpool_bwd_launch(prec, df, ws + gA, N, pl.Hf * pl.Wf, F, st));
   if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DA_AVG, 0, ws + gA, (size_t)N * pl.Hf * pl.Wf * F * es)))
     return r;
 
@@ -513,12 +574,16 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const ConvP& P = pl.cp[li];
     int nblk = 0;
     float* part = (float*)(ws + pl.part);
-    LCHK(bn_bwd_partial_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.rstd), P.M,
-                               L.cout, part, &nblk, st));
-    LCHK(bn_bwd_final_launch(part, nblk, P.M, L.cout, state + L.g, (float*)(ws + P.rstd), grad + L.g, grad + L.b,
-                             (float*)(ws + P.coef), st));
-    LCHK(bn_bwd_apply_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.coef), ws + dy,
-                             P.M, L.cout, st));
+    const double tb = (double)P.M * L.cout * es;
+    TIMED(RN18_K_BN_BWD_REDUCE, li, 0, 0.0, 3 * tb,
+          bn_bwd_partial_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.rstd), P.M,
+                                L.cout, part, &nblk, st));
+    TIMED(RN18_K_BN_BWD_REDUCE, li, 1, 0.0, 0.0,
+          bn_bwd_final_launch(part, nblk, P.M, L.cout, state + L.g, (float*)(ws + P.rstd), grad + L.g, grad + L.b,
+                              (float*)(ws + P.coef), st));
+    TIMED(RN18_K_BN_BWD_APPLY, li, 0, 0.0, 4 * tb,
+          bn_bwd_apply_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.coef), ws + dy,
+                              P.M, L.cout, st));
     if (!c->captures.empty()) return run_captures(c, RN18_CAP_DY, li, ws + dy, (size_t)P.M * L.cout * es);
     return 0;
   };
@@ -526,14 +591,14 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     LCHK(launch_wgrad_full(prec, ws + dy, ws + P.x, grad + L.w, (float*)(ws + pl.wpart), pl.N, P.Hin, P.Win, L.cin_p,
-                           L.cin, P.Ho, P.Wo, L.cout, L.k, L.s, L.p, P.splits, P.pps, st));
+                           L.cin, P.Ho, P.Wo, L.cout, L.k, L.s, L.p, P.splits, P.pps, st, c, li));
     return 0;
   };
   auto dgrad = [&](int li, size_t dy, size_t dx, int mode, size_t R, size_t Rm) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     LCHK(launch_dgrad(prec, ws + dy, W_d(li), ws + dx, pl.N, P.Hin, P.Win, L.cin_p, P.Ho, P.Wo, L.cout, L.k, L.s, L.p,
-                      mode, mode == 2 ? ws + R : nullptr, mode == 2 ? ws + Rm : nullptr, st));
+                      mode, mode == 2 ? ws + R : nullptr, mode == 2 ? ws + Rm : nullptr, st, c, li, L.cin));
     return 0;
   };
 
@@ -565,8 +630,10 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   }
   size_t gstem = gA;
   if (a.imagenet) {
-    LCHK(maxpool_bwd_launch(prec, ws + gA, (const uint8_t*)(ws + pl.parg), ws + gB, N, pl.Hs, pl.Ws, a.convs[0].cout,
-                            pl.Hp, pl.Wp, st));
+    TIMED(RN18_K_MAXPOOL, 1, 0, 0.0,
+          (double)N * a.convs[0].cout * ((double)pl.Hs * pl.Ws * es + (double)pl.Hp * pl.Wp * (es + 1)),
+          maxpool_bwd_launch(prec, ws + gA, (const uint8_t*)(ws + pl.parg), ws + gB, N, pl.Hs, pl.Ws,
+                             a.convs[0].cout, pl.Hp, pl.Wp, st));
     gstem = gB;
     if (!c->captures.empty() &&
         (r = run_captures(c, RN18_CAP_DA_POOL, 0, ws + gB, (size_t)N * pl.Hs * pl.Ws * a.convs[0].cout * es)))
@@ -574,7 +641,8 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   }
   if ((r = bn_back(0, gstem, pl.zstem, pl.gy))) return r;
   if ((r = wgrad(0, pl.gy))) return r;
-  LCHK(sgd_launch(state, grad, c->momentum, a.P, lr, c->cfg.momentum, c->cfg.weight_decay, st));
+  TIMED(RN18_K_SGD, 0, 0, 0.0, 20.0 * a.P,
+        sgd_launch(state, grad, c->momentum, a.P, lr, c->cfg.momentum, c->cfg.weight_decay, st));
   return RN18_OK;
 }
 
@@ -740,8 +808,13 @@ int rn18_eval_logits(rn18_ctx* h, const float* state, const float* images, int N
   if ((r = run_forward(&c, *pl, state, nullptr, images, false))) return r;
   char* ws = (char*)c.ws;
   const Arch& a = c.arch;
-  LCHK(gemm_f32_launch((float*)(ws + pl->f), a.feat, 1, state + a.fc_w, 1, a.feat, state + a.fc_b, logits, N,
-                       a.classes, a.feat, c.stream));
+  Ctx* cp_ = &c;
+  {
+    Ctx* c = cp_;
+    TIMED(RN18_K_HEAD, 0, 0, 2.0 * N * a.classes * a.feat, 0.0,
+          gemm_f32_launch((float*)(ws + pl->f), a.feat, 1, state + a.fc_w, 1, a.feat, state + a.fc_b, logits, N,
+                          a.classes, a.feat, c->stream));
+  }
   return RN18_OK;
 }
 
@@ -801,7 +874,34 @@ void rn18_destroy(rn18_ctx* h) {
   if (c.tab) (void)hipFree(c.tab);
   if (c.err) (void)hipFree(c.err);
   if (c.ws_owned && c.ws) (void)hipFree(c.ws);
+  for (auto& ev : c.prof) { (void)hipEventDestroy(ev.a); (void)hipEventDestroy(ev.b); }
+  for (auto e : c.prof_spare) (void)hipEventDestroy(e);
   delete h;
+}
+
+int rn18_profile_enable(rn18_ctx* h, int on) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  h->c.prof_on = on != 0;
+  return RN18_OK;
+}
+
+int rn18_profile_read(rn18_ctx* h, rn18_prof_rec* out, int max, int* count) {
+  if (!h || !count) return fail(RN18_EINVAL, "NULL pointer");
+  Ctx& c = h->c;
+  HIPCHK(hipStreamSynchronize(c.stream));
+  int n = 0;
+  for (auto& ev : c.prof) {
+    float ms = -1.f;
+    if (hipEventElapsedTime(&ms, ev.a, ev.b) != hipSuccess) ms = -1.f;
+    if (out && n < max) out[n] = rn18_prof_rec{ev.cls, ev.layer, ev.tile, 0, ev.flops, ev.bytes, (double)ms};
+    ++n;
+    c.prof_spare.push_back(ev.a);
+    c.prof_spare.push_back(ev.b);
+  }
+  (void)hipGetLastError();
+  c.prof.clear();
+  *count = n;
+  return RN18_OK;
 }
 
 int rn18_debug_set(rn18_ctx* h, int key, long value) {

@@ -390,15 +390,20 @@ int launch_gather(const ConvGather& g, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
+int gather_tile(const ConvGather& g) {
+  if (g.Cols <= 16) return 64016;
+  if (g.Cols <= 64) return (long)ceil_div(g.M, 128) >= 512 ? 128064 : 64064;
+  return (long)ceil_div(g.M, 128) * ceil_div(g.Cols, 128) >= 512 ? 128128 : 64064;
+}
+
 template <typename T>
 int gather_dispatch(const ConvGather& g, hipStream_t s) {
-  if (g.Cols <= 16) return launch_gather<T, 64, 16, 4, 1>(g, s);
-  if (g.Cols <= 64) {
-    if ((long)ceil_div(g.M, 128) >= 512) return launch_gather<T, 128, 64, 2, 2>(g, s);
-    return launch_gather<T, 64, 64, 2, 2>(g, s);
+  switch (gather_tile(g)) {
+    case 64016: return launch_gather<T, 64, 16, 4, 1>(g, s);
+    case 128064: return launch_gather<T, 128, 64, 2, 2>(g, s);
+    case 128128: return launch_gather<T, 128, 128, 2, 2>(g, s);
+    default: return launch_gather<T, 64, 64, 2, 2>(g, s);
   }
-  if ((long)ceil_div(g.M, 128) * ceil_div(g.Cols, 128) >= 512) return launch_gather<T, 128, 128, 2, 2>(g, s);
-  return launch_gather<T, 64, 64, 2, 2>(g, s);
 }
 
 template <typename T, int BM, int BN, int WGM, int WGN>
@@ -422,6 +427,14 @@ int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
 }
 
 }  // namespace
+
+int conv_gather_tile(const ConvGather& g) { return gather_tile(g); }
+
+int conv_wgrad_tile(int Cout) {
+  int bm, bn;
+  wgrad_tile(Cout, &bm, &bn);
+  return bm * 1000 + bn;
+}
 
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s) {
   if (g.M <= 0) return 0;

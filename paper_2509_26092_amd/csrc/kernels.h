@@ -27,6 +27,8 @@ struct ConvGather {
   float* stats;              // optional BN partial sums [tiles_m][Cols][2] (mode 0 only)
 };
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s);
+// Tile configuration (BM*1000 + BN) the dispatcher picks for a launch.
+int conv_gather_tile(const ConvGather& g);
 
 // Weight gradient: P[split][co][tap*Cin+ci] = sum_pixels dY[p][co] * Xcol[p][tap,ci]
 struct ConvWgrad {
@@ -37,6 +39,7 @@ struct ConvWgrad {
   int Mpix, Kcols, pix_per_split, splits;
 };
 int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s);
+int conv_wgrad_tile(int Cout);
 // Choose the split count for a weight-gradient GEMM (deterministic function of the shape).
 int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split);
 // Sum partials in split order; write OIHW gradient (Cin_real of Cin channels kept).
