@@ -65,7 +65,12 @@ int rn18op_maxpool_bwd(int prec, const void* dy, const uint8_t* arg, void* dx, i
  * the tensor (NHWC in the compute type, or fp32 for grad/mean/rstd),
  * `index` the conv layer (forward order) or the residual block. */
 enum {
-  RN18_DBG_STOP_BLOCKS = 0
+  RN18_DBG_STOP_BLOCKS = 0,
+  /* process-wide: force gather-conv kernel configuration `value` (1..12,
+   * see conv.hip) for every forward / data-gradient launch; 0 = automatic.
+   * ctx may be NULL for this key. For tuning and for testing every
+   * configuration. */
+  RN18_DBG_GATHER_CONFIG = 1
 };
 enum {
   RN18_DBG_Y = 0, RN18_DBG_Z1 = 1, RN18_DBG_OUT = 2, RN18_DBG_GA = 3, RN18_DBG_GB = 4, RN18_DBG_GZ = 5,

@@ -905,6 +905,10 @@ int rn18_profile_read(rn18_ctx* h, rn18_prof_rec* out, int max, int* count) {
 }
 
 int rn18_debug_set(rn18_ctx* h, int key, long value) {
+  if (key == RN18_DBG_GATHER_CONFIG) {
+    if (conv_gather_override((int)value)) return fail(RN18_EINVAL, "unknown gather configuration %ld", value);
+    return RN18_OK;
+  }
   if (!h) return fail(RN18_EINVAL, "ctx is NULL");
   if (key != RN18_DBG_STOP_BLOCKS) return fail(RN18_EINVAL, "unknown debug key %d", key);
   h->c.dbg_stop_blocks = (int)value;

@@ -215,6 +215,222 @@ __global__ __launch_bounds__(256) void conv_gather_kernel(ConvGather g) {
 }
 
 // ---------------------------------------------------------------------------
+// Gather conv, pipelined: the K loop streams 128-byte row stages from global
+// memory straight into an LDS ring of STAGES buffers (gfx950
+// global_load_lds_dwordx4, one 16-byte chunk per lane, written lane-contiguous
+// at the instruction's LDS base), so STAGES-1 stages are in flight while one
+// is multiplied. Rows are 128 bytes without padding; the chunk of row r that
+// goes to slot q is q ^ (r & 7), which spreads the 16 rows of an MFMA operand
+// read over all LDS banks. Taps outside the image and K beyond the end load
+// from a zero page. When Cin is a multiple of the stage width, a stage is one
+// tap and a contiguous block of channels, and the tap arithmetic is uniform.
+// ---------------------------------------------------------------------------
+__device__ uint4 g_zero_page[8];  // zero-initialised at load; never written
+
+typedef __attribute__((address_space(3))) void* lds_void_t;
+
+// 16-byte global -> LDS copy of each lane's chunk, written lane-contiguous at
+// the wave-uniform LDS byte address `lds`. Issued as inline assembly so that
+// the compiler's wait-count insertion does not treat every later LDS read as
+// dependent on it; completion is tracked by explicit vmcnt waits instead.
+__device__ inline void lds_dma16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
+}
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(lds_void_t)p;
+}
+
+// Workgroup barrier without the memory fence __syncthreads() implies (the
+// fence would wait for every outstanding LDS-DMA stage, not just the one
+// about to be read).
+__device__ inline void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
+
+template <int N>
+__device__ inline void wait_vmcnt() {
+  // s_waitcnt vmcnt(N), expcnt and lgkmcnt left at their maximum
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int IPW>
+__device__ inline void wait_stage(int later_issued) {
+  // wait until only `later_issued` stages of IPW loads each are outstanding
+  if (later_issued >= 2) wait_vmcnt<2 * IPW>();
+  else if (later_issued == 1) wait_vmcnt<IPW>();
+  else wait_vmcnt<0>();
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool UNI>
+__global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather g) {
+  constexpr int NW = WGM * WGN, NT = 64 * NW;
+  constexpr int VW = TT<T>::VW;
+  constexpr int KT = 128 / (int)sizeof(T);
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  constexpr int AI = BM / 8, BI = BN / 8;          // 8-row load instructions per stage
+  constexpr int NI = AI + BI, IPW = NI / NW;       // per wave
+  constexpr int STAGE_U4 = (BM + BN) * 8;
+  constexpr int CSTR = BN + 4;
+  constexpr int SM_LOOP = STAGES * STAGE_U4;
+  constexpr int SM_EPI = (BM * CSTR + 3) / 4;
+  __shared__ uint4 smem[SM_LOOP > SM_EPI ? SM_LOOP : SM_EPI];
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  static_assert(NI % NW == 0 && BN % 8 == 0, "whole load instructions per wave");
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int tiles_n = (g.Cols + BN - 1) / BN;
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int m0 = (t / tiles_n) * BM, n0 = (t % tiles_n) * BN;
+  const T* __restrict__ A = (const T*)g.A;
+  const T* __restrict__ B = (const T*)g.B;
+  const int HWm = g.Hm * g.Wm;
+  const int c = (lane & 7) ^ (lane >> 3);          // chunk this lane loads (slot lane&7, row lane>>3)
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t smem_lds = lds_addr(smem);
+  const void* const zero = g.zero;
+
+  // Per load instruction of this wave: the row it fills and that row's geometry.
+  bool isA[IPW], ok[IPW];
+  int pix[IPW], hb[IPW], wb[IPW];
+  long boff[IPW];
+#pragma unroll
+  for (int u = 0; u < IPW; ++u) {
+    const int j = wave_u + NW * u;
+    isA[u] = j < AI;
+    if (isA[u]) {
+      const int m = m0 + j * 8 + (lane >> 3);
+      ok[u] = m < g.M;
+      const int mm = ok[u] ? m : 0;
+      const int n = mm / HWm, rem = mm - n * HWm;
+      const int i = rem / g.Wm, jj = rem - i * g.Wm;
+      hb[u] = i * g.is - g.ip;
+      wb[u] = jj * g.is - g.ip;
+      pix[u] = (n * g.Hin + hb[u]) * g.Win + wb[u];
+      boff[u] = 0;
+    } else {
+      const int col = n0 + (j - AI) * 8 + (lane >> 3);
+      ok[u] = col < g.Cols;
+      boff[u] = (long)(ok[u] ? col : 0) * g.KHW * g.Cin;
+      hb[u] = wb[u] = pix[u] = 0;
+    }
+  }
+  const int CB = UNI ? g.Cin / KT : 1;
+
+  auto issue = [&](int s, int buf) {
+    int dh, dw, wt, ci;
+    bool kok;
+    if (UNI) {
+      const int tap = s / CB;
+      const int th = tap / g.ntw, tw = tap - th * g.ntw;
+      dh = g.dh0 + th * g.dhs;
+      dw = g.dw0 + tw * g.dws;
+      wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
+      ci = (s - tap * CB) * KT + c * VW;
+      kok = true;
+    } else {
+      const int k = s * KT + c * VW;
+      kok = k < g.K;
+      const int tap = kok ? k / g.Cin : 0;
+      ci = k - tap * g.Cin;
+      const int th = tap / g.ntw, tw = tap - th * g.ntw;
+      dh = g.dh0 + th * g.dhs;
+      dw = g.dw0 + tw * g.dws;
+      wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
+    }
+    const uint32_t base = smem_lds + (uint32_t)(buf * STAGE_U4 * 16);
+#pragma unroll
+    for (int u = 0; u < IPW; ++u) {
+      const int j = wave_u + NW * u;
+      const void* src;
+      if (isA[u]) {
+        const bool in = kok && ok[u] && (unsigned)(hb[u] + dh) < (unsigned)g.Hin &&
+                        (unsigned)(wb[u] + dw) < (unsigned)g.Win;
+        src = in ? (const void*)(A + (long)(pix[u] + dh * g.Win + dw) * g.Cin + ci) : zero;
+      } else {
+        src = kok && ok[u] ? (const void*)(B + boff[u] + (long)wt * g.Cin + ci) : zero;
+      }
+      lds_dma16(src, base + (uint32_t)(j * 1024));
+    }
+  };
+
+  floatx4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int S = (g.K + KT - 1) / KT;
+#pragma unroll
+  for (int p = 0; p < STAGES - 1; ++p)
+    if (p < S) issue(p, p);
+  const int arow0 = wm * WTM, brow0 = wn * WTN;
+  const int sw = lane & 7;
+  for (int s = 0; s < S; ++s) {
+    const int later = min(STAGES - 2, S - 1 - s);
+    wait_stage<IPW>(later);
+    barrier_only();
+    if (s + STAGES - 1 < S) issue(s + STAGES - 1, (s + STAGES - 1) % STAGES);
+    const uint4* As = smem + (s % STAGES) * STAGE_U4;
+    const uint4* Bs = As + BM * 8;
+#pragma unroll
+    for (int kg = 0; kg < 2; ++kg) {
+      const int slot = (kg * 4 + (lane >> 4)) ^ sw;
+      uint4 a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) a[i] = As[(arow0 + i * 16 + (lane & 15)) * 8 + slot];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) b[j] = Bs[(brow0 + j * 16 + (lane & 15)) * 8 + slot];
+#pragma unroll
+      for (int tt = 0; tt < Mma<T>::SUB; ++tt)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], a[i], b[j], tt);
+    }
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  float* Cs = (float*)smem;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        Cs[(wm * WTM + i * 16 + 4 * (lane >> 4) + r) * CSTR + wn * WTN + j * 16 + (lane & 15)] = acc[i][j][r];
+  __syncthreads();
+
+  constexpr int CPR = BN / VW;
+  T* __restrict__ Cg = (T*)g.C;
+  for (int idx = tid; idx < BM * CPR; idx += NT) {
+    const int row = idx / CPR, cc = idx - row * CPR;
+    const int m = m0 + row, col = n0 + cc * VW;
+    if (m >= g.M || col >= g.Cols) continue;
+    const int n = m / HWm, rem = m - n * HWm;
+    const int i = rem / g.Wm, j = rem - i * g.Wm;
+    const long off = ((long)(n * g.Hout + i * g.os + g.oph) * g.Wout + j * g.os + g.opw) * g.Cols + col;
+    float v[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) v[e] = Cs[row * CSTR + cc * VW + e];
+    if (g.mode == 1) {
+      float o[VW];
+      unpack<T>(*(const uint4*)(Cg + off), o);
+#pragma unroll
+      for (int e = 0; e < VW; ++e) v[e] += o[e];
+    } else if (g.mode == 2) {
+      float rr[VW], mk[VW];
+      unpack<T>(*(const uint4*)((const T*)g.R + off), rr);
+      unpack<T>(*(const uint4*)((const T*)g.Rm + off), mk);
+#pragma unroll
+      for (int e = 0; e < VW; ++e) v[e] += mk[e] > 0.f ? rr[e] : 0.f;
+    }
+    *(uint4*)(Cg + off) = pack<T>(v);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Weight gradient
 // ---------------------------------------------------------------------------
 template <typename T> struct Tr;
@@ -390,19 +606,78 @@ int launch_gather(const ConvGather& g, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
+const void* zero_page() {
+  static const void* zp[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  if (!zp[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(g_zero_page)) != hipSuccess) return nullptr;
+    zp[dev] = p;
+  }
+  return zp[dev];
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
+int launch_gather2(const ConvGather& g0, hipStream_t s) {
+  ConvGather g = g0;
+  g.zero = zero_page();
+  if (!g.zero) return -4;
+  const int tiles = ceil_div(g.M, BM) * ceil_div(g.Cols, BN);
+  const int kt = 128 / (int)sizeof(T);
+  const int nt = 64 * WGM * WGN;
+  if (g.Cin % kt == 0)
+    hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, true>), dim3(tiles), dim3(nt), 0, s, g);
+  else
+    hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, false>), dim3(tiles), dim3(nt), 0, s, g);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+// Kernel configurations: id -> (BM, BN, waves along M, waves along N, stages).
+//   1: 64x32  2x2 s3     2: 64x64  2x2 s3     3: 128x64 2x2 s3    4: 128x128 2x2 s3
+//   5: 256x128 4x2 s3    6: 256x128 2x2 s3    7: 256x64 4x2 s3    8: 128x128 2x4 s3
+//   9: 256x64 4x1 s3    10: 128x128 2x2 s2   11: 256x128 4x2 s2  12: 128x64 2x2 s4
+//  13: 128x64 2x2 s2    14: 64x64 2x2 s2     15: 256x64 4x2 s2   16: 128x128 2x4 s2
+constexpr int kGatherCfgs = 16;
+int g_gather_override = 0;
+
+// Choice measured on MI355X over the ResNet-18 shapes (bf16 224x224 batch 256,
+// fp32 32x32 batch 128): two-stage rings with two or more blocks per CU beat
+// deeper rings with one block; 8-wave blocks for the large tiles.
+int gather_cfg(const ConvGather& g) {
+  if (g_gather_override) return g_gather_override;
+  if (g.Cols <= 32) return 1;
+  if (g.Cols <= 64) return g.M >= 131072 ? 15 : g.M >= 65536 ? 13 : 14;
+  return (long)ceil_div(g.M, 128) * ceil_div(g.Cols, 128) >= 256 ? 16 : 14;
+}
+
 int gather_tile(const ConvGather& g) {
-  if (g.Cols <= 16) return 64016;
-  if (g.Cols <= 64) return (long)ceil_div(g.M, 128) >= 512 ? 128064 : 64064;
-  return (long)ceil_div(g.M, 128) * ceil_div(g.Cols, 128) >= 512 ? 128128 : 64064;
+  static const int tile[kGatherCfgs + 1] = {0, 64032, 64064, 128064, 128128, 256128, 256128, 256064, 128128,
+                                            256064, 128128, 256128, 128064, 128064, 64064, 256064, 128128};
+  const int id = gather_cfg(g);
+  return id >= 1 && id <= kGatherCfgs ? tile[id] : 0;
 }
 
 template <typename T>
 int gather_dispatch(const ConvGather& g, hipStream_t s) {
-  switch (gather_tile(g)) {
-    case 64016: return launch_gather<T, 64, 16, 4, 1>(g, s);
-    case 128064: return launch_gather<T, 128, 64, 2, 2>(g, s);
-    case 128128: return launch_gather<T, 128, 128, 2, 2>(g, s);
-    default: return launch_gather<T, 64, 64, 2, 2>(g, s);
+  switch (gather_cfg(g)) {
+    case 1: return launch_gather2<T, 64, 32, 2, 2, 3>(g, s);
+    case 2: return launch_gather2<T, 64, 64, 2, 2, 3>(g, s);
+    case 3: return launch_gather2<T, 128, 64, 2, 2, 3>(g, s);
+    case 4: return launch_gather2<T, 128, 128, 2, 2, 3>(g, s);
+    case 5: return launch_gather2<T, 256, 128, 4, 2, 3>(g, s);
+    case 6: return launch_gather2<T, 256, 128, 2, 2, 3>(g, s);
+    case 7: return launch_gather2<T, 256, 64, 4, 2, 3>(g, s);
+    case 8: return launch_gather2<T, 128, 128, 2, 4, 3>(g, s);
+    case 9: return launch_gather2<T, 256, 64, 4, 1, 3>(g, s);
+    case 10: return launch_gather2<T, 128, 128, 2, 2, 2>(g, s);
+    case 11: return launch_gather2<T, 256, 128, 4, 2, 2>(g, s);
+    case 12: return launch_gather2<T, 128, 64, 2, 2, 4>(g, s);
+    case 13: return launch_gather2<T, 128, 64, 2, 2, 2>(g, s);
+    case 14: return launch_gather2<T, 64, 64, 2, 2, 2>(g, s);
+    case 15: return launch_gather2<T, 256, 64, 4, 2, 2>(g, s);
+    case 16: return launch_gather2<T, 128, 128, 2, 4, 2>(g, s);
+    default: return -1;
   }
 }
 
@@ -429,6 +704,12 @@ int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
 }  // namespace
 
 int conv_gather_tile(const ConvGather& g) { return gather_tile(g); }
+
+int conv_gather_override(int id) {
+  if (id < 0 || id > kGatherCfgs) return -1;
+  g_gather_override = id;
+  return 0;
+}
 
 int conv_wgrad_tile(int Cout) {
   int bm, bn;

@@ -25,10 +25,13 @@ struct ConvGather {
   int K;                     // nth*ntw*Cin
   int mode;                  // 0 store, 1 C += acc, 2 C = acc + (Rm>0 ? R : 0)
   float* stats;              // optional BN partial sums [tiles_m][Cols][2] (mode 0 only)
+  const void* zero;          // 16-byte zero page (set by the launcher)
 };
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s);
 // Tile configuration (BM*1000 + BN) the dispatcher picks for a launch.
 int conv_gather_tile(const ConvGather& g);
+// Force one kernel configuration for every gather launch (0 = automatic choice).
+int conv_gather_override(int id);
 
 // Weight gradient: P[split][co][tap*Cin+ci] = sum_pixels dY[p][co] * Xcol[p][tap,ci]
 struct ConvWgrad {
