@@ -70,7 +70,11 @@ enum {
    * see conv.hip) for every forward / data-gradient launch; 0 = automatic.
    * ctx may be NULL for this key. For tuning and for testing every
    * configuration. */
-  RN18_DBG_GATHER_CONFIG = 1
+  RN18_DBG_GATHER_CONFIG = 1,
+  /* process-wide: force weight-gradient kernel configuration `value`
+   * (1..10, see conv.hip); 0 = automatic. Plans built afterwards size their
+   * split-K scratch for it. ctx may be NULL. */
+  RN18_DBG_WGRAD_CONFIG = 2
 };
 enum {
   RN18_DBG_Y = 0, RN18_DBG_Z1 = 1, RN18_DBG_OUT = 2, RN18_DBG_GA = 3, RN18_DBG_GB = 4, RN18_DBG_GZ = 5,

@@ -414,7 +414,7 @@ int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float
   g.pix_per_split = pps;
   g.splits = splits;
   const double mpix = (double)N * Ho * Wo;
-  int pi = prof_begin(c, RN18_K_CONV_WGRAD, layer, conv_wgrad_tile(Cout), 2.0 * Cout * k * k * cin_real * mpix,
+  int pi = prof_begin(c, RN18_K_CONV_WGRAD, layer, conv_wgrad_tile(prec, Cout), 2.0 * Cout * k * k * cin_real * mpix,
                       (double)splits * Cout * g.Kcols * 4);
   int r = conv_wgrad_launch(prec, g, st);
   prof_end(c, pi);
@@ -907,6 +907,10 @@ int rn18_profile_read(rn18_ctx* h, rn18_prof_rec* out, int max, int* count) {
 int rn18_debug_set(rn18_ctx* h, int key, long value) {
   if (key == RN18_DBG_GATHER_CONFIG) {
     if (conv_gather_override((int)value)) return fail(RN18_EINVAL, "unknown gather configuration %ld", value);
+    return RN18_OK;
+  }
+  if (key == RN18_DBG_WGRAD_CONFIG) {
+    if (conv_wgrad_override((int)value)) return fail(RN18_EINVAL, "unknown wgrad configuration %ld", value);
     return RN18_OK;
   }
   if (!h) return fail(RN18_EINVAL, "ctx is NULL");

@@ -583,19 +583,222 @@ __global__ __launch_bounds__(256) void conv_wgrad_kernel(ConvWgrad g) {
     }
 }
 
-__global__ void wgrad_reduce_kernel(const float* __restrict__ P, int splits, int Cout, int KHW, int Cin,
-                                    int Cin_real, float* __restrict__ out) {
+// ---------------------------------------------------------------------------
+// Weight gradient, pipelined. Both operand tiles are staged exactly as they
+// lie in memory, one pixel per 128-byte LDS row (dY: that pixel's output
+// channels; X: the input channels its tap reads, or the 16-byte chunks of
+// several taps when Cin is smaller than a row), loaded by the same LDS-DMA
+// ring as the gather kernel. The reduction runs over pixels, so the MFMA
+// operands need several pixels of one channel per lane: bf16 reads them with
+// the gfx950 LDS transpose read (ds_read_b64_tr_b16, four lanes' 8-byte row
+// pieces transposed across a 16-lane group), fp32 with one 4-byte read per
+// pixel. Partial sums of a pixel split go to a scratch buffer summed in a
+// fixed order afterwards.
+// ---------------------------------------------------------------------------
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) char lds_char_t;
+
+template <typename T> struct WOp;
+template <> struct WOp<bf16_t> {
+  static constexpr int KP = 64;      // pixels per stage
+  static constexpr int KSTEPS = 2;   // MFMA k-steps (32 pixels each) per stage
+  typedef uint4 frag_t;
+  // 16 channels [ch0, ch0+16) of a 64-channel sub-tile, pixels kk*32 + 8*(lane/16) + 0..7
+  __device__ static inline uint4 frag(const lds_char_t* sub, int ch0, int kk, int lane) {
+    const int r = lane & 15, kq = lane >> 4;
+    const int ch = ch0 + 4 * (r & 3);
+    const int c = ch >> 3, bo = (ch & 7) << 1;
+    int p = kk * 32 + 8 * kq + (r >> 2);
+    const lds_char_t* a1 = sub + p * 128 + ((c ^ (p & 7)) << 4) + bo;
+    p += 4;
+    const lds_char_t* a2 = sub + p * 128 + ((c ^ (p & 7)) << 4) + bo;
+    const v4i16_t x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16_t*)a1);
+    const v4i16_t y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16_t*)a2);
+    uint4 q;
+    q.x = (uint32_t)(uint16_t)x[0] | ((uint32_t)(uint16_t)x[1] << 16);
+    q.y = (uint32_t)(uint16_t)x[2] | ((uint32_t)(uint16_t)x[3] << 16);
+    q.z = (uint32_t)(uint16_t)y[0] | ((uint32_t)(uint16_t)y[1] << 16);
+    q.w = (uint32_t)(uint16_t)y[2] | ((uint32_t)(uint16_t)y[3] << 16);
+    return q;
+  }
+  __device__ static inline void mma(floatx4_t& acc, const uint4& a, const uint4& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                  acc, 0, 0, 0);
+  }
+};
+template <> struct WOp<float> {
+  static constexpr int KP = 32;      // pixels per stage
+  static constexpr int KSTEPS = 8;   // MFMA k-steps (4 pixels each) per stage
+  typedef float frag_t;
+  // channel ch0 + lane%16 of a 32-channel sub-tile, pixel kk*4 + lane/16
+  __device__ static inline float frag(const lds_char_t* sub, int ch0, int kk, int lane) {
+    const int ch = ch0 + (lane & 15), p = kk * 4 + (lane >> 4);
+    const int c = ch >> 2;
+    return *(const __attribute__((address_space(3))) float*)(sub + p * 128 + ((c ^ (p & 7)) << 4) + ((ch & 3) << 2));
+  }
+  __device__ static inline void mma(floatx4_t& acc, float a, float b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+  }
+};
+
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
+__global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g, const void* zero) {
+  typedef WOp<T> O;
+  constexpr int NW = WGM * WGN;
+  constexpr int VW = TT<T>::VW;
+  constexpr int CPS = 128 / (int)sizeof(T);     // channels per LDS row
+  constexpr int KP = O::KP;
+  constexpr int SA = BM / CPS, SB = BN / CPS;   // 128-byte-wide sub-tiles of each operand
+  constexpr int RI = KP / 8;                    // load instructions per sub-tile
+  constexpr int NI = (SA + SB) * RI, IPW = NI / NW;
+  constexpr int SUB_B = KP * 128, STAGE_B = (SA + SB) * SUB_B;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  __shared__ uint4 smem[STAGES * STAGE_B / 16];
+  static_assert(NI % NW == 0 && BM % CPS == 0 && BN % CPS == 0, "tile shape");
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave_u / WGN, wn = wave_u % WGN;
+  const int tiles_n = (g.Kcols + BN - 1) / BN;
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int co0 = (t / tiles_n) * BM, k0 = (t % tiles_n) * BN;
+  const int split = blockIdx.y;
+  const int p_begin = split * g.pix_per_split;
+  const int p_end = min(g.Mpix, p_begin + g.pix_per_split);
+  const int HWo = g.Ho * g.Wo;
+  const T* __restrict__ DY = (const T*)g.DY;
+  const T* __restrict__ X = (const T*)g.X;
+  const int c = (lane & 7) ^ (lane >> 3);
+  const uint32_t smem_lds = lds_addr(smem);
+
+  // Fixed geometry of each load instruction of this wave.
+  bool isA[IPW], ok[IPW];
+  int row[IPW], co_[IPW], dh[IPW], dw[IPW], ci_[IPW];
+#pragma unroll
+  for (int u = 0; u < IPW; ++u) {
+    const int j = wave_u + NW * u;
+    const int sub = j / RI;
+    row[u] = (j % RI) * 8 + (lane >> 3);
+    isA[u] = sub < SA;
+    if (isA[u]) {
+      co_[u] = co0 + sub * CPS + c * VW;
+      ok[u] = co_[u] < g.Cout;
+      dh[u] = dw[u] = ci_[u] = 0;
+    } else {
+      const int kc = k0 + (sub - SA) * CPS + c * VW;
+      ok[u] = kc < g.Kcols;
+      const int tap = ok[u] ? kc / g.Cin : 0;
+      ci_[u] = kc - tap * g.Cin;
+      const int kh = tap / g.KW, kw = tap - kh * g.KW;
+      dh[u] = kh - g.pad;
+      dw[u] = kw - g.pad;
+      co_[u] = 0;
+    }
+  }
+
+  auto issue = [&](int s, int buf) {
+    const int p0 = p_begin + s * KP;
+    const uint32_t base = smem_lds + (uint32_t)(buf * STAGE_B);
+#pragma unroll
+    for (int u = 0; u < IPW; ++u) {
+      const int j = wave_u + NW * u;
+      const int p = p0 + row[u];
+      const void* src = zero;
+      if (isA[u]) {
+        if (ok[u] && p < p_end) src = DY + (long)p * g.Cout + co_[u];
+      } else if (ok[u] && p < p_end) {
+        const int n = p / HWo, rem = p - n * HWo;
+        const int ho = rem / g.Wo, wo = rem - ho * g.Wo;
+        const int hi = ho * g.stride + dh[u], wi = wo * g.stride + dw[u];
+        if ((unsigned)hi < (unsigned)g.H && (unsigned)wi < (unsigned)g.W)
+          src = X + ((long)(n * g.H + hi) * g.W + wi) * g.Cin + ci_[u];
+      }
+      lds_dma16(src, base + (uint32_t)((j / RI) * SUB_B + (j % RI) * 1024));
+    }
+  };
+
+  floatx4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int S = p_end > p_begin ? (p_end - p_begin + KP - 1) / KP : 0;
+#pragma unroll
+  for (int q = 0; q < STAGES - 1; ++q)
+    if (q < S) issue(q, q);
+  const lds_char_t* lds = (const lds_char_t*)(lds_void_t)smem;
+  // wave tile rows: channels [wm*WTM, +WTM) of the A sub-tiles; cols: [wn*WTN, +WTN) of B
+  for (int s = 0; s < S; ++s) {
+    wait_stage<IPW>(min(STAGES - 2, S - 1 - s));
+    barrier_only();
+    if (s + STAGES - 1 < S) issue(s + STAGES - 1, (s + STAGES - 1) % STAGES);
+    const lds_char_t* st = lds + (s % STAGES) * STAGE_B;
+#pragma unroll
+    for (int kk = 0; kk < O::KSTEPS; ++kk) {
+      typename O::frag_t a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int ch = wm * WTM + i * 16;
+        a[i] = O::frag(st + (ch / CPS) * SUB_B, ch % CPS, kk, lane);
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int ch = wn * WTN + j * 16;
+        b[j] = O::frag(st + (SA + ch / CPS) * SUB_B, ch % CPS, kk, lane);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) O::mma(acc[i][j], a[i], b[j]);
+    }
+  }
+  wait_vmcnt<0>();
+
+  float* __restrict__ P = g.P + (long)split * g.Cout * g.Kcols;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int kc = k0 + wn * WTN + j * 16 + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int co = co0 + wm * WTM + i * 16 + 4 * (lane >> 4) + r;
+        if (co < g.Cout && kc < g.Kcols) P[(long)co * g.Kcols + kc] = acc[i][j][r];
+      }
+    }
+}
+
+// Sum of the split partials in a fixed order, written in OIHW order. A block
+// covers 64 consecutive (co, tap, ci) elements with 4 groups of 64 threads;
+// group q sums splits q, q+4, ... and the four sums are added in order, so
+// the result is deterministic and the split axis is read in parallel.
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ P, int splits, int Cout,
+                                                           int KHW, int Cin, int Cin_real, float* __restrict__ out) {
+  __shared__ float part[4][64];
   const long total = (long)Cout * KHW * Cin;
-  const long stride = (long)Cout * KHW * Cin;
-  for (long idx = blockIdx.x * (long)blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
-    const int ci = (int)(idx % Cin);
-    if (ci >= Cin_real) continue;
-    const long rest = idx / Cin;
-    const int tap = (int)(rest % KHW);
-    const int co = (int)(rest / KHW);
-    float s = 0.f;
-    for (int z = 0; z < splits; ++z) s += P[z * stride + idx];
-    out[((long)co * Cin_real + ci) * KHW + tap] = s;
+  const long stride = total;
+  const int e = threadIdx.x & 63, q = threadIdx.x >> 6;
+  for (long base = blockIdx.x * 64l; base < total; base += (long)gridDim.x * 64) {
+    const long idx = base + e;
+    float acc = 0.f;
+    if (idx < total)
+      for (int z = q; z < splits; z += 4) acc += P[z * stride + idx];
+    part[q][e] = acc;
+    __syncthreads();
+    if (q == 0 && idx < total) {
+      const float sum = ((part[0][e] + part[1][e]) + part[2][e]) + part[3][e];
+      const int ci = (int)(idx % Cin);
+      if (ci < Cin_real) {
+        const long rest = idx / Cin;
+        const int tap = (int)(rest % KHW);
+        const int co = (int)(rest / KHW);
+        out[((long)co * Cin_real + ci) * KHW + tap] = sum;
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -688,17 +891,55 @@ int launch_wgrad(const ConvWgrad& g, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
-void wgrad_tile(int Cout, int* bm, int* bn) {
-  if (Cout <= 16) { *bm = 16; *bn = 64; }
-  else if (Cout <= 64) { *bm = 64; *bn = 64; }
-  else { *bm = 128; *bn = 128; }
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
+int launch_wgrad2(const ConvWgrad& g, hipStream_t s) {
+  const void* zp = zero_page();
+  if (!zp) return -4;
+  const int tiles = ceil_div(g.Cout, BM) * ceil_div(g.Kcols, BN);
+  hipLaunchKernelGGL((conv_wgrad2_kernel<T, BM, BN, WGM, WGN, STAGES>), dim3(tiles, g.splits), dim3(64 * WGM * WGN), 0,
+                     s, g, zp);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+// Weight-gradient configurations: id -> kernel, BM (output channels) x BN
+// (tap x input channel columns), waves, stages.
+//   1-3: register-transposing kernel 16x64, 64x64, 128x128
+//   4: 64x128 1x4 s2   5: 64x128 2x2 s2   6: 128x128 2x2 s2   7: 128x128 2x2 s3
+//   8: 64x64 2x2 s2    9: 128x64 2x2 s2  10: 128x128 2x4 s2
+constexpr int kWgradCfgs = 10;
+int g_wgrad_override = 0;
+
+// Choice measured on MI355X (bf16 224x224 batch 256, fp32 32x32 batch 128).
+int wgrad_cfg(int prec, int Cout) {
+  if (g_wgrad_override) return g_wgrad_override;
+  if (Cout <= 16) return 1;
+  if (Cout <= 64) return prec == PREC_BF16 ? 10 : 8;
+  return 10;
+}
+
+void wgrad_tile(int prec, int Cout, int* bm, int* bn) {
+  static const int tile[kWgradCfgs + 1][2] = {{0, 0},   {16, 64},  {64, 64},  {128, 128}, {64, 128}, {64, 128},
+                                              {128, 128}, {128, 128}, {64, 64}, {128, 64},  {128, 128}};
+  const int id = wgrad_cfg(prec, Cout);
+  *bm = tile[id][0];
+  *bn = tile[id][1];
 }
 
 template <typename T>
 int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
-  if (g.Cout <= 16) return launch_wgrad<T, 16, 64, 1, 4>(g, s);
-  if (g.Cout <= 64) return launch_wgrad<T, 64, 64, 2, 2>(g, s);
-  return launch_wgrad<T, 128, 128, 2, 2>(g, s);
+  switch (wgrad_cfg(sizeof(T) == 2 ? PREC_BF16 : PREC_F32, g.Cout)) {
+    case 1: return launch_wgrad<T, 16, 64, 1, 4>(g, s);
+    case 2: return launch_wgrad<T, 64, 64, 2, 2>(g, s);
+    case 3: return launch_wgrad<T, 128, 128, 2, 2>(g, s);
+    case 4: return launch_wgrad2<T, 64, 128, 1, 4, 2>(g, s);
+    case 5: return launch_wgrad2<T, 64, 128, 2, 2, 2>(g, s);
+    case 6: return launch_wgrad2<T, 128, 128, 2, 2, 2>(g, s);
+    case 7: return launch_wgrad2<T, 128, 128, 2, 2, 3>(g, s);
+    case 8: return launch_wgrad2<T, 64, 64, 2, 2, 2>(g, s);
+    case 9: return launch_wgrad2<T, 128, 64, 2, 2, 2>(g, s);
+    case 10: return launch_wgrad2<T, 128, 128, 2, 4, 2>(g, s);
+    default: return -1;
+  }
 }
 
 }  // namespace
@@ -711,9 +952,15 @@ int conv_gather_override(int id) {
   return 0;
 }
 
-int conv_wgrad_tile(int Cout) {
+int conv_wgrad_override(int id) {
+  if (id < 0 || id > kWgradCfgs) return -1;
+  g_wgrad_override = id;
+  return 0;
+}
+
+int conv_wgrad_tile(int prec, int Cout) {
   int bm, bn;
-  wgrad_tile(Cout, &bm, &bn);
+  wgrad_tile(prec, Cout, &bm, &bn);
   return bm * 1000 + bn;
 }
 
@@ -725,7 +972,7 @@ int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s) {
 int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split) {
   const int ktp = prec == PREC_BF16 ? 64 : 32;
   int bm, bn;
-  wgrad_tile(Cout, &bm, &bn);
+  wgrad_tile(prec, Cout, &bm, &bn);
   const long tiles = (long)ceil_div(Cout, bm) * ceil_div(Kcols, bn);
   long splits = (1024 + tiles - 1) / tiles;
   const long per_split_bytes = (long)Cout * Kcols * 4;
@@ -751,8 +998,8 @@ int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s) {
 int wgrad_reduce_launch(const float* P, int splits, int Cout, int KHW, int Cin, int Cin_real,
                         float* out_oihw, hipStream_t s) {
   const long total = (long)Cout * KHW * Cin;
-  int blocks = (int)((total + 255) / 256);
-  if (blocks > 4096) blocks = 4096;
+  int blocks = (int)((total + 63) / 64);
+  if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, s, P, splits, Cout, KHW, Cin, Cin_real,
                      out_oihw);
   return hipGetLastError() == hipSuccess ? 0 : -4;

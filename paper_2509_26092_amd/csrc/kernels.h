@@ -42,7 +42,9 @@ struct ConvWgrad {
   int Mpix, Kcols, pix_per_split, splits;
 };
 int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s);
-int conv_wgrad_tile(int Cout);
+int conv_wgrad_tile(int prec, int Cout);
+// Force one weight-gradient configuration (0 = automatic choice).
+int conv_wgrad_override(int id);
 // Choose the split count for a weight-gradient GEMM (deterministic function of the shape).
 int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split);
 // Sum partials in split order; write OIHW gradient (Cin_real of Cin channels kept).

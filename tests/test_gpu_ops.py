@@ -95,6 +95,14 @@ def test_conv_wgrad(prec, case):
     assert_close(dw.cpu().numpy(), ref, tol, "conv wgrad")
 
 
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+@pytest.mark.parametrize("case", [(6, 64, 64, 24, 24, 64, 3, 1, 1), (4, 64, 64, 17, 19, 128, 3, 2, 1),
+                                  (5, 3, 0, 40, 40, 64, 7, 2, 3), (3, 128, 128, 9, 9, 256, 1, 2, 0)], ids=case_id)
+def test_conv_wgrad_split_k(prec, case):
+    """Pixel ranges long enough for several split-K partials."""
+    test_conv_wgrad(prec, case)
+
+
 def test_conv_wgrad_deterministic():
     import torch
     N, C, H, W, O, k, s, p = 8, 64, 28, 28, 64, 3, 1, 1
