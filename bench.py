@@ -206,6 +206,9 @@ def main():
     ap.add_argument("--headline-only", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=40)
+    ap.add_argument("--calibrate", action="store_true",
+                    help="also run ps_worker_delta over 2^26 floats (reads 512 MiB, writes 256 MiB) as the "
+                         "known-size kernel that scales HBM counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (the parameter-server merge is "
@@ -246,6 +249,13 @@ def main():
         per_shape.append({"workload": "ps_dual_merge_imagenet_state", "elements": n_state,
                           "ms": round(mms, 4), "GBps": round(mgbs, 1), "hbm_frac": round(mgbs / HBM_PEAK, 4),
                           "hybrid_rounds": rounds})
+
+    if args.calibrate:
+        n = 1 << 26
+        a, b, d = (torch.ones(n, device="cuda") for _ in range(3))
+        for _ in range(3):
+            B.ps_worker_delta(a, b, d, n)
+        torch.cuda.synchronize()
 
     cpu = None
     if not args.no_cpu:
