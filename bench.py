@@ -46,24 +46,9 @@ SHAPES = [
 
 
 def symbol(rec, prec):
-    t = "bf16" if prec == "bf16" else "f32"
-    c = rec["cls"]
-    if c in ("conv_fwd", "conv_dgrad"):
-        return "conv_gather_kernel<%s,%d,%d>" % (t, rec["tile"] // 1000, rec["tile"] % 1000)
-    if c == "conv_wgrad":
-        return "conv_wgrad_kernel<%s,%d,%d>" % (t, rec["tile"] // 1000, rec["tile"] % 1000)
-    sub = {"bn_stats": ["bn_stats_partial_kernel", "bn_stats_final_kernel"],
-           "bn_bwd_reduce": ["bn_bwd_partial_kernel", "bn_bwd_final_kernel"],
-           "prep": ["repack_kernel", "ingest_kernel"]}
-    if c in sub:
-        return sub[c][rec["tile"]]
-    if c == "maxpool":
-        return ["maxpool_fwd_kernel", "maxpool_bwd_kernel"][rec["layer"]]
-    if c == "avgpool":
-        return ["avgpool_fwd_kernel", "avgpool_bwd_kernel"][rec["layer"]]
-    if c == "head":
-        return ["gemm_f32_kernel", "softmax_ce_kernel", "gemm_f32_kernel", "colsum_kernel", "gemm_f32_kernel"][rec["layer"]]
-    return c + "_kernel"
+    """Kernel instance name of a profile record, as rocprofv3 prints it (the
+    library records it; namespace dropped, the bf16 storage type shown as bf16)."""
+    return rec["kernel"] or rec["cls"]
 
 
 def summarize(recs, prec, steps=1):

@@ -167,6 +167,10 @@ typedef struct {
   double flops;  /* algorithmic floating-point operations */
   double bytes;  /* algorithmic bytes */
   double ms;     /* event-measured duration */
+  char kernel[104]; /* NUL-terminated name of the (first) kernel of the group as a
+                       profiler demangles it, namespace dropped and the bf16
+                       storage type shown as bf16, e.g.
+                       "conv_gather2_kernel<bf16, 128, 128, 2, 4, 2, true>" */
 } rn18_prof_rec;
 int rn18_profile_enable(rn18_ctx* ctx, int on);
 int rn18_profile_read(rn18_ctx* ctx, rn18_prof_rec* out, int max, int* count);

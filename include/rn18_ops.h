@@ -66,7 +66,7 @@ int rn18op_maxpool_bwd(int prec, const void* dy, const uint8_t* arg, void* dx, i
  * `index` the conv layer (forward order) or the residual block. */
 enum {
   RN18_DBG_STOP_BLOCKS = 0,
-  /* process-wide: force gather-conv kernel configuration `value` (1..12,
+  /* process-wide: force gather-conv kernel configuration `value` (1..22,
    * see conv.hip) for every forward / data-gradient launch; 0 = automatic.
    * ctx may be NULL for this key. For tuning and for testing every
    * configuration. */

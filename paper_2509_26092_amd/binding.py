@@ -37,7 +37,8 @@ class Rn18Error(RuntimeError):
 
 class rn18_prof_rec(ctypes.Structure):
     _fields_ = [("cls", ctypes.c_int), ("layer", ctypes.c_int), ("tile", ctypes.c_int), ("pad_", ctypes.c_int),
-                ("flops", ctypes.c_double), ("bytes", ctypes.c_double), ("ms", ctypes.c_double)]
+                ("flops", ctypes.c_double), ("bytes", ctypes.c_double), ("ms", ctypes.c_double),
+                ("kernel", ctypes.c_char * 104)]
 
 
 K_NAMES = ["conv_fwd", "conv_dgrad", "conv_wgrad", "wgrad_reduce", "bn_stats", "bn_apply", "bn_bwd_reduce",
@@ -181,11 +182,12 @@ def rn18_profile_enable(ctx, on):
 
 
 def rn18_profile_read(ctx, max_records=4096):
-    """Profile records (kernel class, layer, tile, flops, bytes, ms) in launch order."""
+    """Profile records (kernel class, layer, tile, kernel name, flops, bytes, ms) in launch order."""
     buf = (rn18_prof_rec * max_records)()
     n = _I(0)
     _check(lib().rn18_profile_read(ctx, buf, max_records, ctypes.byref(n)))
-    return [dict(cls=K_NAMES[r.cls], layer=r.layer, tile=r.tile, flops=r.flops, bytes=r.bytes, ms=r.ms)
+    return [dict(cls=K_NAMES[r.cls], layer=r.layer, tile=r.tile, kernel=r.kernel.decode(), flops=r.flops,
+                 bytes=r.bytes, ms=r.ms)
             for r in buf[:min(n.value, max_records)]]
 
 
@@ -221,6 +223,9 @@ def rn18op_maxpool_bwd(prec, dy, arg, dx, N, H, W, C, stream=None):
 
 DBG = dict(y=0, z1=1, out=2, gA=3, gB=4, gz=5, gy=6, gyd=7, grad=8, wf=9, wd=10, mean=11, rstd=12, zstem=13,
            parg=14)
+
+
+RN18_DBG_STOP_BLOCKS, RN18_DBG_GATHER_CONFIG, RN18_DBG_WGRAD_CONFIG = 0, 1, 2
 
 
 def rn18_debug_set(ctx, key, value):

@@ -174,7 +174,7 @@ struct Ctx {
   struct Capture { int kind, index; void* dst; size_t bytes; };
   std::vector<Capture> captures; // debugging: copies of backward tensors
   // optional per-launch timing with HIP events on the context stream
-  struct ProfEv { int cls, layer, tile; double flops, bytes; hipEvent_t a, b; };
+  struct ProfEv { int cls, layer, tile; const char* name; double flops, bytes; hipEvent_t a, b; };
   bool prof_on = false;
   std::vector<ProfEv> prof;
   std::vector<hipEvent_t> prof_spare;
@@ -192,9 +192,9 @@ hipEvent_t prof_event(Ctx* c) {
 }
 
 // Start a timed launch group; returns its index or -1 when profiling is off.
-int prof_begin(Ctx* c, int cls, int layer, int tile, double flops, double bytes) {
+int prof_begin(Ctx* c, int cls, int layer, int tile, const char* name, double flops, double bytes) {
   if (!c || !c->prof_on) return -1;
-  Ctx::ProfEv ev{cls, layer, tile, flops, bytes, prof_event(c), prof_event(c)};
+  Ctx::ProfEv ev{cls, layer, tile, name, flops, bytes, prof_event(c), prof_event(c)};
   if (!ev.a || !ev.b || hipEventRecord(ev.a, c->stream) != hipSuccess) return -1;
   c->prof.push_back(ev);
   return (int)c->prof.size() - 1;
@@ -202,9 +202,9 @@ int prof_begin(Ctx* c, int cls, int layer, int tile, double flops, double bytes)
 void prof_end(Ctx* c, int idx) {
   if (idx >= 0) (void)hipEventRecord(c->prof[idx].b, c->stream);
 }
-#define TIMED(cls, layer, tile, fl, by, expr) \
-  do {                                         \
-    const int pi_ = prof_begin(c, cls, layer, tile, fl, by); \
+#define TIMED(cls, layer, tile, name, fl, by, expr)             \
+  do {                                                          \
+    const int pi_ = prof_begin(c, cls, layer, tile, name, fl, by); \
     LCHK(expr);                                \
     prof_end(c, pi_);                          \
   } while (0)
@@ -320,6 +320,11 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   pl->gy = alloc(max_y);
   pl->gyd = alloc(max_yd ? max_yd : 16);
   pl->part = alloc((size_t)max_partC * 4);
+  // the weight-gradient split-K scratch also holds the classifier's split-K
+  // partials (the classifier runs before any weight gradient)
+  for (size_t hw : {gemm_f32_workspace(N, C, a.feat), gemm_f32_workspace(C, a.feat, N),
+                    gemm_f32_workspace(N, a.feat, C)})
+    if (hw > max_wpart) max_wpart = hw;
   pl->wpart = alloc(max_wpart);
   pl->grad = alloc((size_t)a.P * 4);
   pl->total = off;
@@ -365,7 +370,7 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
     g.wkh0 = k - 1; g.wkhs = -1; g.wkw0 = k - 1; g.wkws = -1; g.KW = k; g.KHW = k * k;
     g.K = k * k * Cout;
     g.mode = mode;
-    const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(g), 2.0 * g.M * creal * g.K, 0.0);
+    const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(g), conv_gather_kernel_name(prec, g), 2.0 * g.M * creal * g.K, 0.0);
     const int r = conv_gather_launch(prec, g, st);
     prof_end(c, pi);
     return r;
@@ -394,7 +399,7 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
         if (mode == 1) continue;   // nothing to add
         g.nth = 1; g.ntw = 1;      // K = 0: the kernel writes acc = 0 (+ residual)
       }
-      const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(g), 2.0 * g.M * creal * g.K, 0.0);
+      const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(g), conv_gather_kernel_name(prec, g), 2.0 * g.M * creal * g.K, 0.0);
       const int r = conv_gather_launch(prec, g, st);
       prof_end(c, pi);
       if (r) return r;
@@ -414,12 +419,13 @@ int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float
   g.pix_per_split = pps;
   g.splits = splits;
   const double mpix = (double)N * Ho * Wo;
-  int pi = prof_begin(c, RN18_K_CONV_WGRAD, layer, conv_wgrad_tile(prec, Cout), 2.0 * Cout * k * k * cin_real * mpix,
+  int pi = prof_begin(c, RN18_K_CONV_WGRAD, layer, conv_wgrad_tile(prec, Cout, g.Kcols), conv_wgrad_kernel_name(prec, Cout, g.Kcols),
+                      2.0 * Cout * k * k * cin_real * mpix,
                       (double)splits * Cout * g.Kcols * 4);
   int r = conv_wgrad_launch(prec, g, st);
   prof_end(c, pi);
   if (r) return r;
-  pi = prof_begin(c, RN18_K_WGRAD_REDUCE, layer, 0, 0.0, ((double)splits + 1.0) * Cout * g.Kcols * 4);
+  pi = prof_begin(c, RN18_K_WGRAD_REDUCE, layer, 0, "wgrad_reduce_kernel", 0.0, ((double)splits + 1.0) * Cout * g.Kcols * 4);
   r = wgrad_reduce_launch(wpart, splits, Cout, k * k, Cin, cin_real, out, st);
   prof_end(c, pi);
   return r;
@@ -471,9 +477,9 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
   auto W = [&](int li) { return (const char*)c->wf + (size_t)a.convs[li].wf * c->es; };
 
   const double es = c->es;
-  TIMED(RN18_K_PREP, -1, 0, 0.0, (double)a.wf_total * (4.0 + 2.0 * es),
+  TIMED(RN18_K_PREP, -1, 0, kernel_instance_name("repack_kernel", prec), 0.0, (double)a.wf_total * (4.0 + 2.0 * es),
         repack_launch(prec, state_c, c->wf, c->wd, c->tab, c->ntab, a.wf_total, st));
-  TIMED(RN18_K_PREP, -1, 1, 0.0, (double)N * pl.H * pl.W * (12.0 + a.convs[0].cin_p * es),
+  TIMED(RN18_K_PREP, -1, 1, kernel_instance_name("ingest_kernel", prec), 0.0, (double)N * pl.H * pl.W * (12.0 + a.convs[0].cin_p * es),
         ingest_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, a.convs[0].cin_p, st));
 
   auto conv_bn = [&](int li) -> int {
@@ -481,7 +487,7 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     const ConvP& P = pl.cp[li];
     ConvGather g = gather_fwd(ws + P.x, W(li), ws + P.y, N, P.Hin, P.Win, L.cin_p, P.Ho, P.Wo, L.cout, L.k, L.s, L.p);
     const double xb = (double)N * P.Hin * P.Win * L.cin_p * es, yb = (double)P.M * L.cout * es;
-    TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(g), 2.0 * P.M * L.cout * L.k * L.k * L.cin,
+    TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(g), conv_gather_kernel_name(prec, g), 2.0 * P.M * L.cout * L.k * L.k * L.cin,
           xb + yb + (double)L.cout * L.k * L.k * L.cin_p * es, conv_gather_launch(prec, g, st));
     float* mean = (float*)(ws + P.mean);
     float* rstd = (float*)(ws + P.rstd);
@@ -490,8 +496,8 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     if (train) {
       int nblk = 0;
       float* part = (float*)(ws + pl.part);
-      TIMED(RN18_K_BN_STATS, li, 0, 0.0, yb, bn_stats_partial_launch(prec, ws + P.y, P.M, L.cout, part, &nblk, st));
-      TIMED(RN18_K_BN_STATS, li, 1, 0.0, 0.0,
+      TIMED(RN18_K_BN_STATS, li, 0, kernel_instance_name("bn_stats_partial_kernel", prec), 0.0, yb, bn_stats_partial_launch(prec, ws + P.y, P.M, L.cout, part, &nblk, st));
+      TIMED(RN18_K_BN_STATS, li, 1, kernel_instance_name("bn_stats_final_kernel", prec), 0.0, 0.0,
             bn_stats_final_launch(prec, ws + P.y, part, nblk, P.M, L.cout, state_c + L.g, state_c + L.b, eps, mom,
                                   state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, st));
     } else {
@@ -504,7 +510,7 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     const ConvP& P = pl.cp[li];
     const float* sc2 = li2 >= 0 ? (const float*)(ws + pl.cp[li2].scale) : nullptr;
     const float* sf2 = li2 >= 0 ? (const float*)(ws + pl.cp[li2].shift) : nullptr;
-    TIMED(RN18_K_BN_APPLY, li, res_mode, 0.0, (double)P.M * L.cout * es * (res_mode ? 3 : 2),
+    TIMED(RN18_K_BN_APPLY, li, res_mode, kernel_instance_name("bn_apply_kernel", prec), 0.0, (double)P.M * L.cout * es * (res_mode ? 3 : 2),
           bn_apply_launch(prec, ws + P.y, (float*)(ws + P.scale), (float*)(ws + P.shift), relu, res_mode,
                           res_mode ? ws + r : nullptr, sc2, sf2, ws + z, P.M, L.cout, st));
     return 0;
@@ -514,7 +520,7 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
   if ((r = conv_bn(0))) return r;
   if ((r = apply(0, 1, 0, 0, -1, pl.zstem))) return r;
   if (a.imagenet)
-    TIMED(RN18_K_MAXPOOL, 0, 0, 0.0,
+    TIMED(RN18_K_MAXPOOL, 0, 0, kernel_instance_name("maxpool_fwd_kernel", prec), 0.0,
           (double)N * a.convs[0].cout * ((double)pl.Hs * pl.Ws * es + (double)pl.Hp * pl.Wp * (es + 1)),
           maxpool_fwd_launch(prec, ws + pl.zstem, ws + pl.pool, (uint8_t*)(ws + pl.parg), N, pl.Hs, pl.Ws,
                              a.convs[0].cout, pl.Hp, pl.Wp, st));
@@ -532,7 +538,7 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     }
   }
   const size_t last = pl.bp.back().out;
-  TIMED(RN18_K_AVGPOOL, 0, 0, 0.0, (double)N * a.feat * ((double)pl.Hf * pl.Wf * es + 4),
+  TIMED(RN18_K_AVGPOOL, 0, 0, kernel_instance_name("avgpool_fwd_kernel", prec), 0.0, (double)N * a.feat * ((double)pl.Hf * pl.Wf * es + 4),
         avgpool_fwd_launch(prec, ws + last, (float*)(ws + pl.f), N, pl.Hf * pl.Wf, a.feat, st));
   return RN18_OK;
 }
@@ -552,17 +558,18 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   float* df = (float*)(ws + pl.df);
   float* grad = (float*)(ws + pl.grad);
   const double fcf = 2.0 * N * C * F;
-  TIMED(RN18_K_HEAD, 0, 0, fcf, 0.0, gemm_f32_launch(f, F, 1, state + a.fc_w, 1, F, state + a.fc_b, logits, N, C, F, st));
-  TIMED(RN18_K_HEAD, 1, 0, 0.0, 8.0 * N * C,
+  float* hpart = (float*)(ws + pl.wpart);
+  TIMED(RN18_K_HEAD, 0, 0, "gemm_f32_kernel", fcf, 0.0, gemm_f32_launch(f, F, 1, state + a.fc_w, 1, F, state + a.fc_b, logits, N, C, F, hpart, st));
+  TIMED(RN18_K_HEAD, 1, 0, "softmax_ce_kernel", 0.0, 8.0 * N * C,
         softmax_ce_launch(logits, labels, N, C, dlog, (float*)(ws + pl.rowloss),
                           loss ? loss : (float*)(ws + pl.lossbuf), c->err, st));
   // classifier backward: dW = dz^T f, db = sum dz, df = dz W
-  TIMED(RN18_K_HEAD, 2, 0, fcf, 0.0, gemm_f32_launch(dlog, 1, C, f, F, 1, nullptr, grad + a.fc_w, C, F, N, st));
-  TIMED(RN18_K_HEAD, 3, 0, 0.0, 4.0 * N * C, colsum_launch(dlog, N, C, grad + a.fc_b, st));
-  TIMED(RN18_K_HEAD, 4, 0, fcf, 0.0, gemm_f32_launch(dlog, C, 1, state + a.fc_w, F, 1, nullptr, df, N, F, C, st));
+  TIMED(RN18_K_HEAD, 2, 0, "gemm_f32_kernel", fcf, 0.0, gemm_f32_launch(dlog, 1, C, f, F, 1, nullptr, grad + a.fc_w, C, F, N, hpart, st));
+  TIMED(RN18_K_HEAD, 3, 0, "colsum_kernel", 0.0, 4.0 * N * C, colsum_launch(dlog, N, C, grad + a.fc_b, st));
+  TIMED(RN18_K_HEAD, 4, 0, "gemm_f32_kernel", fcf, 0.0, gemm_f32_launch(dlog, C, 1, state + a.fc_w, F, 1, nullptr, df, N, F, C, hpart, st));
   size_t gA = pl.gA, gB = pl.gB;
   const size_t es = c->es;
-  TIMED(RN18_K_AVGPOOL, 1, 0, 0.0, (double)N * F * ((double)pl.Hf * pl.Wf * es + 4),
+  TIMED(RN18_K_AVGPOOL, 1, 0, kernel_instance_name("avgpool_bwd_kernel", prec), 0.0, (double)N * F * ((double)pl.Hf * pl.Wf * es + 4),
         avgpool_bwd_launch(prec, df, ws + gA, N, pl.Hf * pl.Wf, F, st));
   if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DA_AVG, 0, ws + gA, (size_t)N * pl.Hf * pl.Wf * F * es)))
     return r;
@@ -575,13 +582,13 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     int nblk = 0;
     float* part = (float*)(ws + pl.part);
     const double tb = (double)P.M * L.cout * es;
-    TIMED(RN18_K_BN_BWD_REDUCE, li, 0, 0.0, 3 * tb,
+    TIMED(RN18_K_BN_BWD_REDUCE, li, 0, kernel_instance_name("bn_bwd_partial_kernel", prec), 0.0, 3 * tb,
           bn_bwd_partial_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.rstd), P.M,
                                 L.cout, part, &nblk, st));
-    TIMED(RN18_K_BN_BWD_REDUCE, li, 1, 0.0, 0.0,
+    TIMED(RN18_K_BN_BWD_REDUCE, li, 1, "bn_bwd_final_kernel", 0.0, 0.0,
           bn_bwd_final_launch(part, nblk, P.M, L.cout, state + L.g, (float*)(ws + P.rstd), grad + L.g, grad + L.b,
                               (float*)(ws + P.coef), st));
-    TIMED(RN18_K_BN_BWD_APPLY, li, 0, 0.0, 4 * tb,
+    TIMED(RN18_K_BN_BWD_APPLY, li, 0, kernel_instance_name("bn_bwd_apply_kernel", prec), 0.0, 4 * tb,
           bn_bwd_apply_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.coef), ws + dy,
                               P.M, L.cout, st));
     if (!c->captures.empty()) return run_captures(c, RN18_CAP_DY, li, ws + dy, (size_t)P.M * L.cout * es);
@@ -630,7 +637,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   }
   size_t gstem = gA;
   if (a.imagenet) {
-    TIMED(RN18_K_MAXPOOL, 1, 0, 0.0,
+    TIMED(RN18_K_MAXPOOL, 1, 0, kernel_instance_name("maxpool_bwd_kernel", prec), 0.0,
           (double)N * a.convs[0].cout * ((double)pl.Hs * pl.Ws * es + (double)pl.Hp * pl.Wp * (es + 1)),
           maxpool_bwd_launch(prec, ws + gA, (const uint8_t*)(ws + pl.parg), ws + gB, N, pl.Hs, pl.Ws,
                              a.convs[0].cout, pl.Hp, pl.Wp, st));
@@ -641,7 +648,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   }
   if ((r = bn_back(0, gstem, pl.zstem, pl.gy))) return r;
   if ((r = wgrad(0, pl.gy))) return r;
-  TIMED(RN18_K_SGD, 0, 0, 0.0, 20.0 * a.P,
+  TIMED(RN18_K_SGD, 0, 0, "sgd_kernel", 0.0, 20.0 * a.P,
         sgd_launch(state, grad, c->momentum, a.P, lr, c->cfg.momentum, c->cfg.weight_decay, st));
   return RN18_OK;
 }
@@ -811,9 +818,9 @@ int rn18_eval_logits(rn18_ctx* h, const float* state, const float* images, int N
   Ctx* cp_ = &c;
   {
     Ctx* c = cp_;
-    TIMED(RN18_K_HEAD, 0, 0, 2.0 * N * a.classes * a.feat, 0.0,
+    TIMED(RN18_K_HEAD, 0, 0, "gemm_f32_kernel", 2.0 * N * a.classes * a.feat, 0.0,
           gemm_f32_launch((float*)(ws + pl->f), a.feat, 1, state + a.fc_w, 1, a.feat, state + a.fc_b, logits, N,
-                          a.classes, a.feat, c->stream));
+                          a.classes, a.feat, (float*)(ws + pl->wpart), c->stream));
   }
   return RN18_OK;
 }
@@ -893,7 +900,13 @@ int rn18_profile_read(rn18_ctx* h, rn18_prof_rec* out, int max, int* count) {
   for (auto& ev : c.prof) {
     float ms = -1.f;
     if (hipEventElapsedTime(&ms, ev.a, ev.b) != hipSuccess) ms = -1.f;
-    if (out && n < max) out[n] = rn18_prof_rec{ev.cls, ev.layer, ev.tile, 0, ev.flops, ev.bytes, (double)ms};
+    if (out && n < max) {
+      rn18_prof_rec& o = out[n];
+      o = rn18_prof_rec{};
+      o.cls = ev.cls; o.layer = ev.layer; o.tile = ev.tile;
+      o.flops = ev.flops; o.bytes = ev.bytes; o.ms = ms;
+      snprintf(o.kernel, sizeof o.kernel, "%s", ev.name ? ev.name : "");
+    }
     ++n;
     c.prof_spare.push_back(ev.a);
     c.prof_spare.push_back(ev.b);

@@ -18,12 +18,19 @@
 // inside an MFMA does not change the dot product, so fp32 (16x16x4) and bf16
 // (16x16x32) share the LDS layout and the loaders.
 //
-// The weight gradient reduces over pixels. Its tiles are loaded as 16-byte
-// channel chunks of consecutive pixels and transposed in registers so that the
-// LDS rows hold consecutive pixels of one channel; partial sums of a split of
-// the pixel range go to a scratch buffer that is summed in a fixed order
+// The weight gradient reduces over pixels. Its dY and im2col X tiles are
+// staged as they lie in memory (one pixel's 128 bytes of channels per LDS row)
+// and the pixel-major MFMA operands are built on the way out of LDS (gfx950
+// transpose reads for bf16, 4-byte reads for fp32). The older kernel for
+// 16-channel outputs transposes in registers instead. Partial sums of a split
+// of the pixel range go to a scratch buffer that is summed in a fixed order
 // (deterministic, no float atomics).
 #include "kernels.h"
+
+#include <cstdio>
+#include <mutex>
+#include <set>
+#include <string>
 
 namespace rn18 {
 
@@ -236,6 +243,29 @@ typedef __attribute__((address_space(3))) void* lds_void_t;
 __device__ inline void lds_dma16(const void* src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
 }
+// Buffer resource of a raw byte range [base, base + bytes): a buffer load at
+// a byte offset >= bytes is out of range and returns zeros (written to LDS
+// as zeros by the DMA form), which is how padding taps are filled.
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+__device__ inline i32x4_t buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  i32x4_t r;
+  r[0] = (int)(uint32_t)a;
+  r[1] = (int)(uint32_t)(a >> 32);  // stride 0
+  r[2] = (int)bytes;
+  r[3] = 0x00020000;                // raw 32-bit dwords, no swizzle
+  return r;
+}
+constexpr uint32_t kOutOfRange = 0x80000000u;  // byte offset beyond every buffer used here
+
+// 16-byte buffer -> LDS copy of each lane's chunk at byte offset `voff` of
+// the buffer `rsrc`, written lane-contiguous at the wave-uniform LDS byte
+// address `lds`.
+__device__ inline void lds_dma16_buf(uint32_t voff, i32x4_t rsrc, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(rsrc), "s"(lds)
+               : "memory", "m0");
+}
+
 __device__ inline uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(lds_void_t)p;
 }
@@ -269,9 +299,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
   constexpr int AI = BM / 8, BI = BN / 8;          // 8-row load instructions per stage
   constexpr int NI = AI + BI, IPW = NI / NW;       // per wave
   constexpr int STAGE_U4 = (BM + BN) * 8;
-  constexpr int CSTR = BN + 4;
   constexpr int SM_LOOP = STAGES * STAGE_U4;
-  constexpr int SM_EPI = (BM * CSTR + 3) / 4;
+  constexpr int WSTR = WTN + 4;                    // epilogue strip row stride (floats)
+  constexpr int SM_EPI = NW * 16 * WSTR / 4;       // one 16-row strip per wave
   __shared__ uint4 smem[SM_LOOP > SM_EPI ? SM_LOOP : SM_EPI];
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   static_assert(NI % NW == 0 && BN % 8 == 0, "whole load instructions per wave");
@@ -316,6 +346,56 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
     }
   }
   const int CB = UNI ? g.Cin / KT : 1;
+
+  // Uniform path: per-lane byte offsets and tap-validity masks are fixed for
+  // the whole K loop; a stage only adds the wave-uniform offset of its tap
+  // and channel block, kept incrementally in scalars.
+  constexpr int UA = AI / NW, UB = BI / NW;        // A and B load instructions per wave
+  static_assert(AI % NW == 0 && BI % NW == 0, "loads split evenly between A and B");
+  const int es = (int)sizeof(T);
+  uint32_t uoff[UNI ? IPW : 1];
+  uint32_t umask[UNI ? UA : 1];
+  i32x4_t rsA, rsB;
+  int st_ti = 0, st_th = 0, st_tw = 0, st_cb = 0;  // tap (th, tw), channel block of the next stage issued
+  if (UNI) {
+    rsA = buffer_rsrc(A, (uint32_t)((long)g.N * g.Hin * g.Win * g.Cin * es));
+    rsB = buffer_rsrc(B, (uint32_t)((long)g.Cols * g.KHW * g.Cin * es));
+#pragma unroll
+    for (int u = 0; u < UA; ++u) {
+      uint32_t m = 0;
+      for (int th = 0; th < g.nth; ++th)
+        for (int tw = 0; tw < g.ntw; ++tw) {
+          const int h = hb[u] + g.dh0 + th * g.dhs, w = wb[u] + g.dw0 + tw * g.dws;
+          if (ok[u] && (unsigned)h < (unsigned)g.Hin && (unsigned)w < (unsigned)g.Win) m |= 1u << (th * g.ntw + tw);
+        }
+      umask[u] = m;
+      uoff[u] = (uint32_t)(pix[u] * g.Cin * es + c * 16);
+    }
+#pragma unroll
+    for (int u = UA; u < IPW; ++u) uoff[u] = ok[u] ? (uint32_t)(boff[u] * es + c * 16) : kOutOfRange;
+  }
+  auto issue_uni = [&](int buf) {
+    const int dh = g.dh0 + st_th * g.dhs, dw = g.dw0 + st_tw * g.dws;
+    const int wt = (g.wkh0 + st_th * g.wkhs) * g.KW + g.wkw0 + st_tw * g.wkws;
+    const uint32_t sa = (uint32_t)((dh * g.Win + dw) * g.Cin * es + st_cb * 128);
+    const uint32_t sb = (uint32_t)(wt * g.Cin * es + st_cb * 128);
+    const uint32_t base = smem_lds + (uint32_t)(buf * STAGE_U4 * 16);
+#pragma unroll
+    for (int u = 0; u < UA; ++u) {
+      const uint32_t v = (umask[u] >> st_ti) & 1u ? uoff[u] + sa : kOutOfRange;
+      lds_dma16_buf(v, rsA, base + (uint32_t)((wave_u + NW * u) * 1024));
+    }
+#pragma unroll
+    for (int u = UA; u < IPW; ++u) {
+      const uint32_t v = uoff[u] == kOutOfRange ? kOutOfRange : uoff[u] + sb;
+      lds_dma16_buf(v, rsB, base + (uint32_t)((AI + wave_u + NW * (u - UA)) * 1024));
+    }
+    if (++st_cb == CB) {
+      st_cb = 0;
+      ++st_ti;
+      if (++st_tw == g.ntw) { st_tw = 0; ++st_th; }
+    }
+  };
 
   auto issue = [&](int s, int buf) {
     int dh, dw, wt, ci;
@@ -363,14 +443,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
   const int S = (g.K + KT - 1) / KT;
 #pragma unroll
   for (int p = 0; p < STAGES - 1; ++p)
-    if (p < S) issue(p, p);
+    if (p < S) {
+      if (UNI) issue_uni(p);
+      else issue(p, p);
+    }
   const int arow0 = wm * WTM, brow0 = wn * WTN;
   const int sw = lane & 7;
   for (int s = 0; s < S; ++s) {
     const int later = min(STAGES - 2, S - 1 - s);
     wait_stage<IPW>(later);
     barrier_only();
-    if (s + STAGES - 1 < S) issue(s + STAGES - 1, (s + STAGES - 1) % STAGES);
+    if (s + STAGES - 1 < S) {
+      if (UNI) issue_uni((s + STAGES - 1) % STAGES);
+      else issue(s + STAGES - 1, (s + STAGES - 1) % STAGES);
+    }
     const uint4* As = smem + (s % STAGES) * STAGE_U4;
     const uint4* Bs = As + BM * 8;
 #pragma unroll
@@ -392,41 +478,44 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
   wait_vmcnt<0>();
   __syncthreads();
 
-  float* Cs = (float*)smem;
+  // Epilogue per wave, one 16-row strip at a time: the strip's accumulators
+  // go through a wave-private LDS buffer and leave as 16-byte chunks of
+  // consecutive output channels.
+  float* Ws = (float*)smem + wave_u * 16 * WSTR;
+  constexpr int CPW = WTN / VW;                    // chunks per strip row
+  T* __restrict__ Cg = (T*)g.C;
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+  for (int i = 0; i < FM; ++i) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        Cs[(wm * WTM + i * 16 + 4 * (lane >> 4) + r) * CSTR + wn * WTN + j * 16 + (lane & 15)] = acc[i][j][r];
-  __syncthreads();
-
-  constexpr int CPR = BN / VW;
-  T* __restrict__ Cg = (T*)g.C;
-  for (int idx = tid; idx < BM * CPR; idx += NT) {
-    const int row = idx / CPR, cc = idx - row * CPR;
-    const int m = m0 + row, col = n0 + cc * VW;
-    if (m >= g.M || col >= g.Cols) continue;
-    const int n = m / HWm, rem = m - n * HWm;
-    const int i = rem / g.Wm, j = rem - i * g.Wm;
-    const long off = ((long)(n * g.Hout + i * g.os + g.oph) * g.Wout + j * g.os + g.opw) * g.Cols + col;
-    float v[VW];
+      for (int r = 0; r < 4; ++r) Ws[(4 * (lane >> 4) + r) * WSTR + j * 16 + (lane & 15)] = acc[i][j][r];
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    for (int idx = lane; idx < 16 * CPW; idx += 64) {
+      const int row = idx / CPW, cc = idx - row * CPW;
+      const int m = m0 + arow0 + i * 16 + row, col = n0 + brow0 + cc * VW;
+      if (m >= g.M || col >= g.Cols) continue;
+      const int n = m / HWm, rem = m - n * HWm;
+      const int ii = rem / g.Wm, jj = rem - ii * g.Wm;
+      const long off = ((long)(n * g.Hout + ii * g.os + g.oph) * g.Wout + jj * g.os + g.opw) * g.Cols + col;
+      float v[VW];
 #pragma unroll
-    for (int e = 0; e < VW; ++e) v[e] = Cs[row * CSTR + cc * VW + e];
-    if (g.mode == 1) {
-      float o[VW];
-      unpack<T>(*(const uint4*)(Cg + off), o);
+      for (int e = 0; e < VW; ++e) v[e] = Ws[row * WSTR + cc * VW + e];
+      if (g.mode == 1) {
+        float o[VW];
+        unpack<T>(*(const uint4*)(Cg + off), o);
 #pragma unroll
-      for (int e = 0; e < VW; ++e) v[e] += o[e];
-    } else if (g.mode == 2) {
-      float rr[VW], mk[VW];
-      unpack<T>(*(const uint4*)((const T*)g.R + off), rr);
-      unpack<T>(*(const uint4*)((const T*)g.Rm + off), mk);
+        for (int e = 0; e < VW; ++e) v[e] += o[e];
+      } else if (g.mode == 2) {
+        float rr[VW], mk[VW];
+        unpack<T>(*(const uint4*)((const T*)g.R + off), rr);
+        unpack<T>(*(const uint4*)((const T*)g.Rm + off), mk);
 #pragma unroll
-      for (int e = 0; e < VW; ++e) v[e] += mk[e] > 0.f ? rr[e] : 0.f;
+        for (int e = 0; e < VW; ++e) v[e] += mk[e] > 0.f ? rr[e] : 0.f;
+      }
+      *(uint4*)(Cg + off) = pack<T>(v);
     }
-    *(uint4*)(Cg + off) = pack<T>(v);
   }
 }
 
@@ -477,10 +566,14 @@ __global__ __launch_bounds__(256) void conv_wgrad_kernel(ConvWgrad g) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
+  // One-dimensional grid over (split, tile), tile fastest; the XCD remap
+  // keeps all tiles of a pixel split on one XCD, so the split's dY and X rows
+  // are fetched from HBM once and re-read from that XCD's L2.
   const int tiles_n = (g.Kcols + BN - 1) / BN;
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int tiles = ((g.Cout + BM - 1) / BM) * tiles_n;
+  const int lt = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = lt / tiles, t = lt - split * tiles;
   const int co0 = (t / tiles_n) * BM, k0 = (t % tiles_n) * BN;
-  const int split = blockIdx.y;
   const int p_begin = split * g.pix_per_split;
   const int p_end = min(g.Mpix, p_begin + g.pix_per_split);
   const int HWo = g.Ho * g.Wo;
@@ -642,7 +735,7 @@ template <> struct WOp<float> {
 };
 
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
-__global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g, const void* zero) {
+__global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g) {
   typedef WOp<T> O;
   constexpr int NW = WGM * WGN;
   constexpr int VW = TT<T>::VW;
@@ -656,15 +749,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g
   constexpr int FM = WTM / 16, FN = WTN / 16;
   __shared__ uint4 smem[STAGES * STAGE_B / 16];
   static_assert(NI % NW == 0 && BM % CPS == 0 && BN % CPS == 0, "tile shape");
+  static_assert(RI % NW == 0 || NW % RI == 0, "load rows");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave_u / WGN, wn = wave_u % WGN;
+  // One-dimensional grid over (split, tile), tile fastest; the XCD remap
+  // keeps all tiles of a pixel split on one XCD, so the split's dY and X rows
+  // are fetched from HBM once and re-read from that XCD's L2.
   const int tiles_n = (g.Kcols + BN - 1) / BN;
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int tiles = ((g.Cout + BM - 1) / BM) * tiles_n;
+  const int lt = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = lt / tiles, t = lt - split * tiles;
   const int co0 = (t / tiles_n) * BM, k0 = (t % tiles_n) * BN;
-  const int split = blockIdx.y;
   const int p_begin = split * g.pix_per_split;
   const int p_end = min(g.Mpix, p_begin + g.pix_per_split);
   const int HWo = g.Ho * g.Wo;
@@ -673,50 +771,95 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g
   const int c = (lane & 7) ^ (lane >> 3);
   const uint32_t smem_lds = lds_addr(smem);
 
-  // Fixed geometry of each load instruction of this wave.
-  bool isA[IPW], ok[IPW];
-  int row[IPW], co_[IPW], dh[IPW], dw[IPW], ci_[IPW];
+  // Fixed geometry of each load instruction of this wave: its LDS row (a
+  // pixel of the stage), and the channel chunk it copies. The pixel of a
+  // lane's row advances by KP per stage; its (n, ho, wo) coordinates are
+  // carried incrementally, so no stage divides.
+  const int es = (int)sizeof(T);
+  const i32x4_t rsA = buffer_rsrc(DY, (uint32_t)((long)g.Mpix * g.Cout * es));
+  const i32x4_t rsB = buffer_rsrc(X, (uint32_t)((long)g.N * g.H * g.W * g.Cin * es));
+  // When NW is a multiple of RI every load of a wave fills the same LDS row
+  // (pixel), so one set of pixel coordinates serves all of them.
+  constexpr bool ONE_ROW = NW % RI == 0;
+  constexpr int NR = ONE_ROW ? 1 : IPW;
+  bool isA[IPW];
+  int row[IPW];
+  uint32_t coff[IPW];   // A: channel byte offset; B: tap + channel byte offset; or out of range
+  int tdh[IPW], tdw[IPW];
+  int pn[NR], pho[NR], pwo[NR];
 #pragma unroll
   for (int u = 0; u < IPW; ++u) {
-    const int j = wave_u + NW * u;
-    const int sub = j / RI;
-    row[u] = (j % RI) * 8 + (lane >> 3);
+    // load j = wave_u + NW*u fills row j % RI of sub-tile j / RI; written so
+    // that the sub-tile (and with it A or B) is a compile-time constant
+    // whenever NW divides RI
+    const int sub = RI % NW == 0 ? NW * u / RI : (NW / RI) * u + wave_u / RI;
+    row[u] = (RI % NW == 0 ? NW * u % RI + wave_u : wave_u % RI) * 8 + (lane >> 3);
     isA[u] = sub < SA;
+    tdh[u] = tdw[u] = 0;
     if (isA[u]) {
-      co_[u] = co0 + sub * CPS + c * VW;
-      ok[u] = co_[u] < g.Cout;
-      dh[u] = dw[u] = ci_[u] = 0;
+      const int co = co0 + sub * CPS + c * VW;
+      coff[u] = co < g.Cout ? (uint32_t)(co * es) : kOutOfRange;
     } else {
       const int kc = k0 + (sub - SA) * CPS + c * VW;
-      ok[u] = kc < g.Kcols;
-      const int tap = ok[u] ? kc / g.Cin : 0;
-      ci_[u] = kc - tap * g.Cin;
-      const int kh = tap / g.KW, kw = tap - kh * g.KW;
-      dh[u] = kh - g.pad;
-      dw[u] = kw - g.pad;
-      co_[u] = 0;
+      if (kc < g.Kcols) {
+        const int tap = kc / g.Cin, ci = kc - tap * g.Cin;
+        const int kh = tap / g.KW, kw = tap - kh * g.KW;
+        tdh[u] = kh - g.pad;
+        tdw[u] = kw - g.pad;
+        coff[u] = (uint32_t)(((kh - g.pad) * g.W + (kw - g.pad)) * g.Cin * es + ci * es);
+      } else {
+        coff[u] = kOutOfRange;
+      }
     }
   }
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int p = p_begin + row[r];
+    pn[r] = p / HWo;
+    const int rem = p - pn[r] * HWo;
+    pho[r] = rem / g.Wo;
+    pwo[r] = rem - pho[r] * g.Wo;
+  }
+  // advance of a pixel index by KP in (n, ho, wo) digits
+  const int adv_n = KP / HWo, adv_r = KP - adv_n * HWo;
+  const int adv_ho = adv_r / g.Wo, adv_wo = adv_r - adv_ho * g.Wo;
+  const int cin_es = g.Cin * es, cout_es = g.Cout * es;
 
-  auto issue = [&](int s, int buf) {
-    const int p0 = p_begin + s * KP;
+  int s_issue = 0;  // next stage to issue
+  auto issue = [&](int buf) {
+    const int p0 = p_begin + s_issue * KP;
+    const int lim = p_end - p0;   // rows < lim are pixels of this split
     const uint32_t base = smem_lds + (uint32_t)(buf * STAGE_B);
 #pragma unroll
     for (int u = 0; u < IPW; ++u) {
-      const int j = wave_u + NW * u;
-      const int p = p0 + row[u];
-      const void* src = zero;
+      const int r = ONE_ROW ? 0 : u;
+      const int sub = RI % NW == 0 ? NW * u / RI : (NW / RI) * u + wave_u / RI;
+      const int rq = RI % NW == 0 ? NW * u % RI + wave_u : wave_u % RI;
+      uint32_t v;
       if (isA[u]) {
-        if (ok[u] && p < p_end) src = DY + (long)p * g.Cout + co_[u];
-      } else if (ok[u] && p < p_end) {
-        const int n = p / HWo, rem = p - n * HWo;
-        const int ho = rem / g.Wo, wo = rem - ho * g.Wo;
-        const int hi = ho * g.stride + dh[u], wi = wo * g.stride + dw[u];
-        if ((unsigned)hi < (unsigned)g.H && (unsigned)wi < (unsigned)g.W)
-          src = X + ((long)(n * g.H + hi) * g.W + wi) * g.Cin + ci_[u];
+        const bool in = (row[u] < lim) & (coff[u] != kOutOfRange);
+        v = in ? (uint32_t)((p0 + row[u]) * cout_es) + coff[u] : kOutOfRange;
+      } else {
+        const int hs = pho[r] * g.stride, ws = pwo[r] * g.stride;
+        const bool in = (row[u] < lim) & (coff[u] != kOutOfRange) & ((unsigned)(hs + tdh[u]) < (unsigned)g.H) &
+                        ((unsigned)(ws + tdw[u]) < (unsigned)g.W);
+        v = in ? (uint32_t)(((pn[r] * g.H + hs) * g.W + ws) * cin_es) + coff[u] : kOutOfRange;
       }
-      lds_dma16(src, base + (uint32_t)((j / RI) * SUB_B + (j % RI) * 1024));
+      lds_dma16_buf(v, isA[u] ? rsA : rsB, base + (uint32_t)(sub * SUB_B + rq * 1024));
     }
+    // carry the pixel coordinates to the next stage
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      int wo = pwo[r] + adv_wo, ho = pho[r] + adv_ho, n = pn[r] + adv_n;
+      const bool cw = wo >= g.Wo;
+      wo = cw ? wo - g.Wo : wo;
+      ho = cw ? ho + 1 : ho;
+      const bool ch = ho >= g.Ho;
+      pwo[r] = wo;
+      pho[r] = ch ? ho - g.Ho : ho;
+      pn[r] = ch ? n + 1 : n;
+    }
+    ++s_issue;
   };
 
   floatx4_t acc[FM][FN];
@@ -728,13 +871,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g
   const int S = p_end > p_begin ? (p_end - p_begin + KP - 1) / KP : 0;
 #pragma unroll
   for (int q = 0; q < STAGES - 1; ++q)
-    if (q < S) issue(q, q);
+    if (q < S) issue(q);
   const lds_char_t* lds = (const lds_char_t*)(lds_void_t)smem;
   // wave tile rows: channels [wm*WTM, +WTM) of the A sub-tiles; cols: [wn*WTN, +WTN) of B
   for (int s = 0; s < S; ++s) {
     wait_stage<IPW>(min(STAGES - 2, S - 1 - s));
     barrier_only();
-    if (s + STAGES - 1 < S) issue(s + STAGES - 1, (s + STAGES - 1) % STAGES);
+    if (s + STAGES - 1 < S) issue((s + STAGES - 1) % STAGES);
     const lds_char_t* st = lds + (s % STAGES) * STAGE_B;
 #pragma unroll
     for (int kk = 0; kk < O::KSTEPS; ++kk) {
@@ -821,6 +964,14 @@ const void* zero_page() {
   return zp[dev];
 }
 
+// The uniform K loop needs whole 128-byte channel blocks per tap, at most 32
+// taps (one validity bit each) and buffers addressable with 31-bit offsets.
+bool gather_uniform(const ConvGather& g, int kt) {
+  const long es = 128 / kt;
+  return g.Cin % kt == 0 && g.nth * g.ntw <= 32 && (long)g.N * g.Hin * g.Win * g.Cin * es < (1l << 31) &&
+         (long)g.Cols * g.KHW * g.Cin * es < (1l << 31);
+}
+
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
 int launch_gather2(const ConvGather& g0, hipStream_t s) {
   ConvGather g = g0;
@@ -829,7 +980,7 @@ int launch_gather2(const ConvGather& g0, hipStream_t s) {
   const int tiles = ceil_div(g.M, BM) * ceil_div(g.Cols, BN);
   const int kt = 128 / (int)sizeof(T);
   const int nt = 64 * WGM * WGN;
-  if (g.Cin % kt == 0)
+  if (gather_uniform(g, kt))
     hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, true>), dim3(tiles), dim3(nt), 0, s, g);
   else
     hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, false>), dim3(tiles), dim3(nt), 0, s, g);
@@ -837,12 +988,23 @@ int launch_gather2(const ConvGather& g0, hipStream_t s) {
 }
 
 // Kernel configurations: id -> (BM, BN, waves along M, waves along N, stages).
-//   1: 64x32  2x2 s3     2: 64x64  2x2 s3     3: 128x64 2x2 s3    4: 128x128 2x2 s3
-//   5: 256x128 4x2 s3    6: 256x128 2x2 s3    7: 256x64 4x2 s3    8: 128x128 2x4 s3
-//   9: 256x64 4x1 s3    10: 128x128 2x2 s2   11: 256x128 4x2 s2  12: 128x64 2x2 s4
-//  13: 128x64 2x2 s2    14: 64x64 2x2 s2     15: 256x64 4x2 s2   16: 128x128 2x4 s2
-constexpr int kGatherCfgs = 16;
+#define RN18_GATHER_CONFIGS(X)                                                                   \
+  X(1, 64, 32, 2, 2, 3) X(2, 64, 64, 2, 2, 3) X(3, 128, 64, 2, 2, 3) X(4, 128, 128, 2, 2, 3)     \
+  X(5, 256, 128, 4, 2, 3) X(6, 256, 128, 2, 2, 3) X(7, 256, 64, 4, 2, 3) X(8, 128, 128, 2, 4, 3) \
+  X(9, 256, 64, 4, 1, 3) X(10, 128, 128, 2, 2, 2) X(11, 256, 128, 4, 2, 2) X(12, 128, 64, 2, 2, 4) \
+  X(13, 128, 64, 2, 2, 2) X(14, 64, 64, 2, 2, 2) X(15, 256, 64, 4, 2, 2) X(16, 128, 128, 2, 4, 2) \
+  X(17, 256, 128, 2, 2, 2) X(18, 512, 64, 4, 1, 2) X(19, 256, 128, 2, 2, 3) X(20, 128, 128, 2, 2, 4) \
+  X(21, 256, 64, 4, 1, 2) X(22, 256, 64, 2, 2, 2)
+constexpr int kGatherCfgs = 22;
 int g_gather_override = 0;
+
+struct GatherCfg { int bm, bn, wgm, wgn, stages; };
+constexpr GatherCfg kGather[kGatherCfgs + 1] = {
+    {0, 0, 0, 0, 0},
+#define RN18_X(id, bm, bn, wgm, wgn, st) {bm, bn, wgm, wgn, st},
+    RN18_GATHER_CONFIGS(RN18_X)
+#undef RN18_X
+};
 
 // Choice measured on MI355X over the ResNet-18 shapes (bf16 224x224 batch 256,
 // fp32 32x32 batch 128): two-stage rings with two or more blocks per CU beat
@@ -855,31 +1017,17 @@ int gather_cfg(const ConvGather& g) {
 }
 
 int gather_tile(const ConvGather& g) {
-  static const int tile[kGatherCfgs + 1] = {0, 64032, 64064, 128064, 128128, 256128, 256128, 256064, 128128,
-                                            256064, 128128, 256128, 128064, 128064, 64064, 256064, 128128};
   const int id = gather_cfg(g);
-  return id >= 1 && id <= kGatherCfgs ? tile[id] : 0;
+  return id >= 1 && id <= kGatherCfgs ? kGather[id].bm * 1000 + kGather[id].bn : 0;
 }
 
 template <typename T>
 int gather_dispatch(const ConvGather& g, hipStream_t s) {
   switch (gather_cfg(g)) {
-    case 1: return launch_gather2<T, 64, 32, 2, 2, 3>(g, s);
-    case 2: return launch_gather2<T, 64, 64, 2, 2, 3>(g, s);
-    case 3: return launch_gather2<T, 128, 64, 2, 2, 3>(g, s);
-    case 4: return launch_gather2<T, 128, 128, 2, 2, 3>(g, s);
-    case 5: return launch_gather2<T, 256, 128, 4, 2, 3>(g, s);
-    case 6: return launch_gather2<T, 256, 128, 2, 2, 3>(g, s);
-    case 7: return launch_gather2<T, 256, 64, 4, 2, 3>(g, s);
-    case 8: return launch_gather2<T, 128, 128, 2, 4, 3>(g, s);
-    case 9: return launch_gather2<T, 256, 64, 4, 1, 3>(g, s);
-    case 10: return launch_gather2<T, 128, 128, 2, 2, 2>(g, s);
-    case 11: return launch_gather2<T, 256, 128, 4, 2, 2>(g, s);
-    case 12: return launch_gather2<T, 128, 64, 2, 2, 4>(g, s);
-    case 13: return launch_gather2<T, 128, 64, 2, 2, 2>(g, s);
-    case 14: return launch_gather2<T, 64, 64, 2, 2, 2>(g, s);
-    case 15: return launch_gather2<T, 256, 64, 4, 2, 2>(g, s);
-    case 16: return launch_gather2<T, 128, 128, 2, 4, 2>(g, s);
+#define RN18_X(id, bm, bn, wgm, wgn, st) \
+  case id: return launch_gather2<T, bm, bn, wgm, wgn, st>(g, s);
+    RN18_GATHER_CONFIGS(RN18_X)
+#undef RN18_X
     default: return -1;
   }
 }
@@ -887,17 +1035,15 @@ int gather_dispatch(const ConvGather& g, hipStream_t s) {
 template <typename T, int BM, int BN, int WGM, int WGN>
 int launch_wgrad(const ConvWgrad& g, hipStream_t s) {
   const int tiles = ceil_div(g.Cout, BM) * ceil_div(g.Kcols, BN);
-  hipLaunchKernelGGL((conv_wgrad_kernel<T, BM, BN, WGM, WGN>), dim3(tiles, g.splits), dim3(256), 0, s, g);
+  hipLaunchKernelGGL((conv_wgrad_kernel<T, BM, BN, WGM, WGN>), dim3(tiles * g.splits), dim3(256), 0, s, g);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
 int launch_wgrad2(const ConvWgrad& g, hipStream_t s) {
-  const void* zp = zero_page();
-  if (!zp) return -4;
   const int tiles = ceil_div(g.Cout, BM) * ceil_div(g.Kcols, BN);
-  hipLaunchKernelGGL((conv_wgrad2_kernel<T, BM, BN, WGM, WGN, STAGES>), dim3(tiles, g.splits), dim3(64 * WGM * WGN), 0,
-                     s, g, zp);
+  hipLaunchKernelGGL((conv_wgrad2_kernel<T, BM, BN, WGM, WGN, STAGES>), dim3(tiles * g.splits), dim3(64 * WGM * WGN),
+                     0, s, g);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
@@ -910,24 +1056,27 @@ constexpr int kWgradCfgs = 10;
 int g_wgrad_override = 0;
 
 // Choice measured on MI355X (bf16 224x224 batch 256, fp32 32x32 batch 128).
-int wgrad_cfg(int prec, int Cout) {
+int wgrad_cfg(int prec, int Cout, int Kcols) {
   if (g_wgrad_override) return g_wgrad_override;
   if (Cout <= 16) return 1;
-  if (Cout <= 64) return prec == PREC_BF16 ? 10 : 8;
-  return 10;
+  if (prec == PREC_BF16) {
+    if (Cout <= 64) return 4;
+    return Kcols <= 576 ? 9 : 10;
+  }
+  return Cout <= 64 ? 8 : 6;
 }
 
-void wgrad_tile(int prec, int Cout, int* bm, int* bn) {
+void wgrad_tile(int prec, int Cout, int Kcols, int* bm, int* bn) {
   static const int tile[kWgradCfgs + 1][2] = {{0, 0},   {16, 64},  {64, 64},  {128, 128}, {64, 128}, {64, 128},
                                               {128, 128}, {128, 128}, {64, 64}, {128, 64},  {128, 128}};
-  const int id = wgrad_cfg(prec, Cout);
+  const int id = wgrad_cfg(prec, Cout, Kcols);
   *bm = tile[id][0];
   *bn = tile[id][1];
 }
 
 template <typename T>
 int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
-  switch (wgrad_cfg(sizeof(T) == 2 ? PREC_BF16 : PREC_F32, g.Cout)) {
+  switch (wgrad_cfg(sizeof(T) == 2 ? PREC_BF16 : PREC_F32, g.Cout, g.Kcols)) {
     case 1: return launch_wgrad<T, 16, 64, 1, 4>(g, s);
     case 2: return launch_wgrad<T, 64, 64, 2, 2>(g, s);
     case 3: return launch_wgrad<T, 128, 128, 2, 2>(g, s);
@@ -944,6 +1093,53 @@ int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
 
 }  // namespace
 
+namespace {
+
+// Instance names as a profiler prints them (namespace dropped, the bf16
+// storage type uint16_t written as bf16), interned for the life of the process.
+const char* intern_name(const std::string& s) {
+  static std::mutex mu;
+  static std::set<std::string> names;
+  std::lock_guard<std::mutex> lock(mu);
+  return names.insert(s).first->c_str();
+}
+
+const char* type_name(int prec) { return prec == PREC_BF16 ? "bf16" : "float"; }
+
+}  // namespace
+
+const char* conv_gather_kernel_name(int prec, const ConvGather& g) {
+  const int id = gather_cfg(g);
+  if (id < 1 || id > kGatherCfgs) return "conv_gather2_kernel";
+  const GatherCfg& c = kGather[id];
+  const int kt = prec == PREC_BF16 ? 64 : 32;
+  char buf[128];
+  snprintf(buf, sizeof buf, "conv_gather2_kernel<%s, %d, %d, %d, %d, %d, %s>", type_name(prec), c.bm, c.bn, c.wgm,
+           c.wgn, c.stages, gather_uniform(g, kt) ? "true" : "false");
+  return intern_name(buf);
+}
+
+const char* conv_wgrad_kernel_name(int prec, int Cout, int Kcols) {
+  static const int cfg[kWgradCfgs + 1][6] = {
+      {0, 0, 0, 0, 0, 0},     {1, 16, 64, 1, 4, 0},   {1, 64, 64, 2, 2, 0},  {1, 128, 128, 2, 2, 0},
+      {2, 64, 128, 1, 4, 2},  {2, 64, 128, 2, 2, 2},  {2, 128, 128, 2, 2, 2}, {2, 128, 128, 2, 2, 3},
+      {2, 64, 64, 2, 2, 2},   {2, 128, 64, 2, 2, 2},  {2, 128, 128, 2, 4, 2}};
+  const int id = wgrad_cfg(prec, Cout, Kcols);
+  if (id < 1 || id > kWgradCfgs) return "conv_wgrad_kernel";
+  const int* c = cfg[id];
+  char buf[128];
+  if (c[0] == 1)
+    snprintf(buf, sizeof buf, "conv_wgrad_kernel<%s, %d, %d, %d, %d>", type_name(prec), c[1], c[2], c[3], c[4]);
+  else
+    snprintf(buf, sizeof buf, "conv_wgrad2_kernel<%s, %d, %d, %d, %d, %d>", type_name(prec), c[1], c[2], c[3], c[4],
+             c[5]);
+  return intern_name(buf);
+}
+
+const char* kernel_instance_name(const char* base, int prec) {
+  return intern_name(std::string(base) + "<" + type_name(prec) + ">");
+}
+
 int conv_gather_tile(const ConvGather& g) { return gather_tile(g); }
 
 int conv_gather_override(int id) {
@@ -958,9 +1154,9 @@ int conv_wgrad_override(int id) {
   return 0;
 }
 
-int conv_wgrad_tile(int prec, int Cout) {
+int conv_wgrad_tile(int prec, int Cout, int Kcols) {
   int bm, bn;
-  wgrad_tile(prec, Cout, &bm, &bn);
+  wgrad_tile(prec, Cout, Kcols, &bm, &bn);
   return bm * 1000 + bn;
 }
 
@@ -972,7 +1168,7 @@ int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s) {
 int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split) {
   const int ktp = prec == PREC_BF16 ? 64 : 32;
   int bm, bn;
-  wgrad_tile(prec, Cout, &bm, &bn);
+  wgrad_tile(prec, Cout, Kcols, &bm, &bn);
   const long tiles = (long)ceil_div(Cout, bm) * ceil_div(Kcols, bn);
   long splits = (1024 + tiles - 1) / tiles;
   const long per_split_bytes = (long)Cout * Kcols * 4;
@@ -992,6 +1188,9 @@ int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_spl
 }
 
 int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s) {
+  // the pipelined kernels address both operands with 31-bit byte offsets
+  const long es = prec == PREC_BF16 ? 2 : 4;
+  if ((long)g.Mpix * g.Cout * es >= (1l << 31) || (long)g.N * g.H * g.W * g.Cin * es >= (1l << 31)) return -1;
   return prec == PREC_BF16 ? wgrad_dispatch<bf16_t>(g, s) : wgrad_dispatch<float>(g, s);
 }
 

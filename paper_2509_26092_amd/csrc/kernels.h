@@ -42,7 +42,13 @@ struct ConvWgrad {
   int Mpix, Kcols, pix_per_split, splits;
 };
 int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s);
-int conv_wgrad_tile(int prec, int Cout);
+int conv_wgrad_tile(int prec, int Cout, int Kcols);
+// Names of the kernel instance a launch would use, in the form a profiler's
+// demangler prints them (namespace dropped, uint16_t storage shown as bf16);
+// kernel_instance_name(base, prec) is base<bf16> or base<float>.
+const char* conv_gather_kernel_name(int prec, const ConvGather& g);
+const char* conv_wgrad_kernel_name(int prec, int Cout, int Kcols);
+const char* kernel_instance_name(const char* base, int prec);
 // Force one weight-gradient configuration (0 = automatic choice).
 int conv_wgrad_override(int id);
 // Choose the split count for a weight-gradient GEMM (deterministic function of the shape).
@@ -93,8 +99,12 @@ int maxpool_bwd_launch(int prec, const void* dy, const uint8_t* arg, void* dx, i
 int avgpool_fwd_launch(int prec, const void* x, float* f, int N, int HW, int C, hipStream_t s);
 int avgpool_bwd_launch(int prec, const float* df, void* dx, int N, int HW, int C, hipStream_t s);
 // C[m][n] = sum_k A(m,k) B(k,n) (+ bias[n]); A(m,k) = A[m*sam + k*sak], B(k,n) = B[k*sbk + n*sbn]
-int gemm_f32_launch(const float* A, long sam, long sak, const float* B, long sbk, long sbn,
-                    const float* bias, float* C, int M, int N, int K, hipStream_t s);
+// Classifier GEMM; `part` (gemm_f32_workspace bytes, may be NULL for one
+// split) holds split-K partial products.
+int gemm_f32_splits(int M, int N, int K);
+size_t gemm_f32_workspace(int M, int N, int K);
+int gemm_f32_launch(const float* A, long sam, long sak, const float* B, long sbk, long sbn, const float* bias,
+                    float* C, int M, int N, int K, float* part, hipStream_t s);
 int colsum_launch(const float* A, int M, int N, float* out, hipStream_t s);
 int softmax_ce_launch(const float* z, const int32_t* labels, int N, int C, float* dz, float* row_loss,
                       float* loss, unsigned* err, hipStream_t s);

@@ -174,21 +174,30 @@ __global__ void avgpool_bwd_kernel(const float* __restrict__ df, T* __restrict__
 }
 
 // ------------------------------------------------------------------ fp32 GEMM (classifier)
+// C[M][N] = A B (+ bias) with A(m,k) = A[m*sam + k*sak], B(k,n) = B[k*sbk + n*sbn].
+// The classifier GEMMs are small (M, N <= 1000) and long in K, so K is split
+// over blockIdx.z; with several splits each writes its partial product to
+// P[z][M][N] and gemm_splitk_reduce_kernel adds them in split order
+// (deterministic). Tiles are loaded along whichever operand stride is 1.
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, long sam, long sak,
                                                        const float* __restrict__ B, long sbk, long sbn,
                                                        const float* __restrict__ bias, float* __restrict__ C,
-                                                       int M, int N, int K) {
+                                                       int M, int N, int K, int kchunk, float* __restrict__ P) {
   __shared__ float As[16][65], Bs[16][65];
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
   const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  const int kb = blockIdx.z * kchunk, ke = min(K, kb + kchunk);
   float acc[4][4] = {};
-  for (int k0 = 0; k0 < K; k0 += 16) {
+  for (int k0 = kb; k0 < ke; k0 += 16) {
 #pragma unroll
     for (int l = 0; l < 4; ++l) {
       const int e = tid + 256 * l;
-      const int mm = e & 63, kk = e >> 6;
-      As[kk][mm] = (m0 + mm < M && k0 + kk < K) ? A[(long)(m0 + mm) * sam + (long)(k0 + kk) * sak] : 0.f;
-      Bs[kk][mm] = (n0 + mm < N && k0 + kk < K) ? B[(long)(k0 + kk) * sbk + (long)(n0 + mm) * sbn] : 0.f;
+      int mm, kk;
+      if (sak == 1) { kk = e & 15; mm = e >> 4; } else { mm = e & 63; kk = e >> 6; }
+      As[kk][mm] = (m0 + mm < M && k0 + kk < ke) ? A[(long)(m0 + mm) * sam + (long)(k0 + kk) * sak] : 0.f;
+      int nn, kq;
+      if (sbk == 1) { kq = e & 15; nn = e >> 4; } else { nn = e & 63; kq = e >> 6; }
+      Bs[kq][nn] = (n0 + nn < N && k0 + kq < ke) ? B[(long)(k0 + kq) * sbk + (long)(n0 + nn) * sbn] : 0.f;
     }
     __syncthreads();
 #pragma unroll
@@ -203,6 +212,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
     }
     __syncthreads();
   }
+  float* __restrict__ out = P ? P + (long)blockIdx.z * M * N : C;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = m0 + ty * 4 + i;
@@ -210,17 +220,33 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n = n0 + tx * 4 + j;
-      if (n < N) C[(long)m * N + n] = acc[i][j] + (bias ? bias[n] : 0.f);
+      if (n < N) out[(long)m * N + n] = acc[i][j] + (!P && bias ? bias[n] : 0.f);
     }
   }
 }
 
-__global__ void colsum_kernel(const float* __restrict__ A, int M, int N, float* __restrict__ out) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= N) return;
+__global__ void gemm_splitk_reduce_kernel(const float* __restrict__ P, int splits, long MN, int N,
+                                          const float* __restrict__ bias, float* __restrict__ C) {
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < MN; i += (long)gridDim.x * blockDim.x) {
+    float v = 0.f;
+    for (int z = 0; z < splits; ++z) v += P[z * MN + i];
+    C[i] = v + (bias ? bias[i % N] : 0.f);
+  }
+}
+
+// Column sums of A [M][N]: a block covers 64 columns with 4 row groups
+// (rows g, g+4, ...); the four group sums are added in order.
+__global__ __launch_bounds__(256) void colsum_kernel(const float* __restrict__ A, int M, int N,
+                                                     float* __restrict__ out) {
+  __shared__ float part[4][64];
+  const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int n = blockIdx.x * 64 + c;
   float s = 0.f;
-  for (int m = 0; m < M; ++m) s += A[(long)m * N + n];
-  out[n] = s;
+  if (n < N)
+    for (int m = q; m < M; m += 4) s += A[(long)m * N + n];
+  part[q][c] = s;
+  __syncthreads();
+  if (q == 0 && n < N) out[n] = ((part[0][c] + part[1][c]) + part[2][c]) + part[3][c];
 }
 
 // ------------------------------------------------------------------ softmax cross-entropy
@@ -403,16 +429,36 @@ int avgpool_bwd_launch(int prec, const float* df, void* dx, int N, int HW, int C
   return ok();
 }
 
+int gemm_f32_splits(int M, int N, int K) {
+  const long tiles = (long)ceil_div(N, 64) * ceil_div(M, 64);
+  int splits = 1;
+  while (tiles * splits < 512 && K / (2 * splits) >= 64) splits *= 2;
+  return splits;
+}
+
+size_t gemm_f32_workspace(int M, int N, int K) {
+  const int s = gemm_f32_splits(M, N, K);
+  return s > 1 ? (size_t)s * M * N * 4 : 0;
+}
+
 int gemm_f32_launch(const float* A, long sam, long sak, const float* B, long sbk, long sbn, const float* bias,
-                    float* C, int M, int N, int K, hipStream_t s) {
+                    float* C, int M, int N, int K, float* part, hipStream_t s) {
   if (M <= 0 || N <= 0) return 0;
-  hipLaunchKernelGGL(gemm_f32_kernel, dim3(ceil_div(N, 64), ceil_div(M, 64)), dim3(256), 0, s, A, sam, sak, B, sbk,
-                     sbn, bias, C, M, N, K);
+  int splits = part ? gemm_f32_splits(M, N, K) : 1;
+  const int kchunk = splits > 1 ? (ceil_div(K, splits) + 15) / 16 * 16 : (K > 0 ? K : 1);
+  splits = K > 0 ? ceil_div(K, kchunk) : 1;
+  hipLaunchKernelGGL(gemm_f32_kernel, dim3(ceil_div(N, 64), ceil_div(M, 64), splits), dim3(256), 0, s, A, sam, sak,
+                     B, sbk, sbn, bias, C, M, N, K, kchunk, splits > 1 ? part : nullptr);
+  if (splits > 1) {
+    const long mn = (long)M * N;
+    hipLaunchKernelGGL(gemm_splitk_reduce_kernel, dim3(grid_for(mn, 256, 1024)), dim3(256), 0, s, part, splits, mn,
+                       N, bias, C);
+  }
   return ok();
 }
 
 int colsum_launch(const float* A, int M, int N, float* out, hipStream_t s) {
-  hipLaunchKernelGGL(colsum_kernel, dim3(ceil_div(N, 256)), dim3(256), 0, s, A, M, N, out);
+  hipLaunchKernelGGL(colsum_kernel, dim3(ceil_div(N, 64)), dim3(256), 0, s, A, M, N, out);
   return ok();
 }
 

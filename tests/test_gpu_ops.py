@@ -153,3 +153,24 @@ def test_op_argument_errors():
     assert e.value.code == B.RN18_EINVAL
     with pytest.raises(B.Rn18Error):
         B.rn18op_conv2d_fwd(B.RN18_FP32, x, x, x, 1, 2, 2, 4, 4, 7, 1, 0)   # empty output
+
+
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_conv_every_kernel_configuration(prec):
+    """Every gather (forward / data-gradient) and weight-gradient kernel
+    configuration, forced in turn, on a ragged stride-1 and a stride-2 shape."""
+    cases = [(3, 64, 64, 13, 11, 128, 3, 1, 1), (2, 64, 64, 15, 15, 128, 3, 2, 1)]
+    try:
+        for cfg in range(1, 23):
+            B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, cfg)
+            for case in cases:
+                test_conv_fwd(prec, case)
+                test_conv_dgrad(prec, case)
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 0)
+        for cfg in range(1, 11):
+            B.rn18_debug_set(None, B.RN18_DBG_WGRAD_CONFIG, cfg)
+            for case in cases:
+                test_conv_wgrad(prec, case)
+    finally:
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 0)
+        B.rn18_debug_set(None, B.RN18_DBG_WGRAD_CONFIG, 0)
