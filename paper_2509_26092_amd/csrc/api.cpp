@@ -69,6 +69,7 @@ struct Arch {
   bool imagenet = false;
   long fc_w = 0, fc_b = 0, P = 0, R = 0;
   long wf_total = 0, wd_total = 0;
+  long wf_s2d = -1;      // ImageNet stem as a 4x4 conv over its space-to-depth input: [64][16][16]
 };
 
 bool build_arch(const rn18_config& c, Arch* a) {
@@ -124,6 +125,10 @@ bool build_arch(const rn18_config& c, Arch* a) {
     if (i == 0) L.wd = -1;
     else { L.wd = d; d += (long)L.cout * L.k * L.k * L.cin_p; }
   }
+  if (a->imagenet) {
+    a->wf_s2d = f;
+    f += (long)a->convs[0].cout * 16 * 16;
+  }
   a->wf_total = f;
   a->wd_total = d;
   return true;
@@ -133,7 +138,10 @@ bool build_arch(const rn18_config& c, Arch* a) {
 // Plan for one (N,H,W)
 // ----------------------------------------------------------------------------
 struct ConvP {
-  int Hin, Win, Ho, Wo;
+  int Hin, Win, Ho, Wo;         // stored input and output sizes
+  int k, s, p, cin;             // conv as computed: kernel, stride, pad, stored input channels
+  long wf;                      // its forward weight shadow offset
+  bool s2d;                     // ImageNet stem computed as a 4x4 conv over a space-to-depth input
   long M;                       // N*Ho*Wo
   size_t x, y;                  // workspace offsets of input and output
   size_t mean, rstd, scale, shift, coef;
@@ -240,6 +248,14 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     P.Hin = hin; P.Win = win;
     P.Ho = out_size(hin, L.k, L.s, L.p);
     P.Wo = out_size(win, L.k, L.s, L.p);
+    P.k = L.k; P.s = L.s; P.p = L.p; P.cin = L.cin_p; P.wf = L.wf; P.s2d = false;
+    if (li == 0 && a.wf_s2d >= 0 && hin % 2 == 0 && win % 2 == 0) {
+      // 7x7 stride-2 pad-3 stem == 4x4 stride-1 conv over the 2x2 space-to-depth
+      // input (H/2 x W/2 x 16), padded by 2 before and 1 after
+      P.s2d = true;
+      P.Hin = hin / 2; P.Win = win / 2;
+      P.k = 4; P.s = 1; P.p = 2; P.cin = 16; P.wf = a.wf_s2d;
+    }
     if (P.Ho < 1 || P.Wo < 1) {
       snprintf(buf, sizeof buf, "conv %d: empty output for input %dx%d", li, hin, win);
       *why = buf;
@@ -258,16 +274,16 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     P.coef = alloc(3 * L.cout * 4);
     const size_t ybytes = (size_t)P.M * L.cout * es;
     if (ybytes > max_y) max_y = ybytes;
-    P.splits = conv_wgrad_splits(c.prec, L.cout, L.k * L.k * L.cin_p, P.M, &P.pps);
-    const size_t wp = (size_t)P.splits * L.cout * L.k * L.k * L.cin_p * 4;
+    P.splits = conv_wgrad_splits(c.prec, L.cout, P.k * P.k * P.cin, P.M, &P.pps);
+    const size_t wp = (size_t)P.splits * L.cout * P.k * P.k * P.cin * 4;
     if (wp > max_wpart) max_wpart = wp;
     const long pc = 1024l * L.cout * 2;
     if (pc > max_partC) max_partC = pc;
     return true;
   };
 
-  const int cp0 = a.convs[0].cin_p;
-  pl->x0 = act(H, W, cp0);
+  const bool s2d = a.wf_s2d >= 0 && H % 2 == 0 && W % 2 == 0;
+  pl->x0 = s2d ? act(H / 2, W / 2, 16) : act(H, W, a.convs[0].cin_p);
   if (!conv_plan(0, H, W, pl->x0)) return RN18_EINVAL;
   pl->Hs = pl->cp[0].Ho; pl->Ws = pl->cp[0].Wo;
   pl->zstem = act(pl->Hs, pl->Ws, a.convs[0].cout);
@@ -407,9 +423,12 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
   return 0;
 }
 
+// s2d: the operands are the space-to-depth stem's (k = 4, Cin = 16) and the
+// result is mapped back to the 7x7 stem weights; flops are then those of the
+// 7x7 conv.
 int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float* wpart, int N, int H, int W, int Cin,
                       int cin_real, int Ho, int Wo, int Cout, int k, int s, int p, int splits, int pps,
-                      hipStream_t st, Ctx* c = nullptr, int layer = -1) {
+                      hipStream_t st, Ctx* c = nullptr, int layer = -1, bool s2d = false) {
   ConvWgrad g{};
   g.DY = dy; g.X = x; g.P = wpart;
   g.N = N; g.H = H; g.W = W; g.Cin = Cin; g.Ho = Ho; g.Wo = Wo; g.Cout = Cout;
@@ -420,13 +439,13 @@ int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float
   g.splits = splits;
   const double mpix = (double)N * Ho * Wo;
   int pi = prof_begin(c, RN18_K_CONV_WGRAD, layer, conv_wgrad_tile(prec, Cout, g.Kcols), conv_wgrad_kernel_name(prec, Cout, g.Kcols),
-                      2.0 * Cout * k * k * cin_real * mpix,
+                      2.0 * Cout * (s2d ? 49 : k * k) * cin_real * mpix,
                       (double)splits * Cout * g.Kcols * 4);
   int r = conv_wgrad_launch(prec, g, st);
   prof_end(c, pi);
   if (r) return r;
   pi = prof_begin(c, RN18_K_WGRAD_REDUCE, layer, 0, "wgrad_reduce_kernel", 0.0, ((double)splits + 1.0) * Cout * g.Kcols * 4);
-  r = wgrad_reduce_launch(wpart, splits, Cout, k * k, Cin, cin_real, out, st);
+  r = wgrad_reduce_launch(wpart, splits, Cout, k * k, Cin, cin_real, out, s2d ? 1 : 0, st);
   prof_end(c, pi);
   return r;
 }
@@ -474,21 +493,26 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
   const int prec = c->prec;
   const int N = pl.N;
   const float eps = c->cfg.bn_eps, mom = c->cfg.bn_momentum;
-  auto W = [&](int li) { return (const char*)c->wf + (size_t)a.convs[li].wf * c->es; };
+  auto W = [&](int li) { return (const char*)c->wf + (size_t)pl.cp[li].wf * c->es; };
 
   const double es = c->es;
   TIMED(RN18_K_PREP, -1, 0, kernel_instance_name("repack_kernel", prec), 0.0, (double)a.wf_total * (4.0 + 2.0 * es),
         repack_launch(prec, state_c, c->wf, c->wd, c->tab, c->ntab, a.wf_total, st));
-  TIMED(RN18_K_PREP, -1, 1, kernel_instance_name("ingest_kernel", prec), 0.0, (double)N * pl.H * pl.W * (12.0 + a.convs[0].cin_p * es),
-        ingest_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, a.convs[0].cin_p, st));
+  if (pl.cp[0].s2d)
+    TIMED(RN18_K_PREP, -1, 1, kernel_instance_name("ingest_s2d_kernel", prec), 0.0,
+          (double)N * pl.H * pl.W * (12.0 + 4.0 * es), ingest_s2d_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, st));
+  else
+    TIMED(RN18_K_PREP, -1, 1, kernel_instance_name("ingest_kernel", prec), 0.0,
+          (double)N * pl.H * pl.W * (12.0 + a.convs[0].cin_p * es),
+          ingest_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, a.convs[0].cin_p, st));
 
   auto conv_bn = [&](int li) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
-    ConvGather g = gather_fwd(ws + P.x, W(li), ws + P.y, N, P.Hin, P.Win, L.cin_p, P.Ho, P.Wo, L.cout, L.k, L.s, L.p);
-    const double xb = (double)N * P.Hin * P.Win * L.cin_p * es, yb = (double)P.M * L.cout * es;
+    ConvGather g = gather_fwd(ws + P.x, W(li), ws + P.y, N, P.Hin, P.Win, P.cin, P.Ho, P.Wo, L.cout, P.k, P.s, P.p);
+    const double xb = (double)N * P.Hin * P.Win * P.cin * es, yb = (double)P.M * L.cout * es;
     TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(g), conv_gather_kernel_name(prec, g), 2.0 * P.M * L.cout * L.k * L.k * L.cin,
-          xb + yb + (double)L.cout * L.k * L.k * L.cin_p * es, conv_gather_launch(prec, g, st));
+          xb + yb + (double)L.cout * P.k * P.k * P.cin * es, conv_gather_launch(prec, g, st));
     float* mean = (float*)(ws + P.mean);
     float* rstd = (float*)(ws + P.rstd);
     float* sc = (float*)(ws + P.scale);
@@ -518,12 +542,17 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
 
   int r;
   if ((r = conv_bn(0))) return r;
-  if ((r = apply(0, 1, 0, 0, -1, pl.zstem))) return r;
-  if (a.imagenet)
-    TIMED(RN18_K_MAXPOOL, 0, 0, kernel_instance_name("maxpool_fwd_kernel", prec), 0.0,
+  if (a.imagenet) {
+    // stem BN-apply + ReLU + max pool in one pass from the conv output
+    const ConvP& P0 = pl.cp[0];
+    TIMED(RN18_K_MAXPOOL, 0, 0, kernel_instance_name("bn_apply_pool_kernel", prec), 0.0,
           (double)N * a.convs[0].cout * ((double)pl.Hs * pl.Ws * es + (double)pl.Hp * pl.Wp * (es + 1)),
-          maxpool_fwd_launch(prec, ws + pl.zstem, ws + pl.pool, (uint8_t*)(ws + pl.parg), N, pl.Hs, pl.Ws,
-                             a.convs[0].cout, pl.Hp, pl.Wp, st));
+          bn_apply_pool_launch(prec, ws + P0.y, (const float*)(ws + P0.scale), (const float*)(ws + P0.shift),
+                               ws + pl.pool, (uint8_t*)(ws + pl.parg), N, pl.Hs, pl.Ws, a.convs[0].cout, pl.Hp,
+                               pl.Wp, st));
+  } else if ((r = apply(0, 1, 0, 0, -1, pl.zstem))) {
+    return r;
+  }
   for (size_t bi = 0; bi < a.blocks.size(); ++bi) {
     const BlockL& B = a.blocks[bi];
     const BlockP& bp = pl.bp[bi];
@@ -597,8 +626,8 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   auto wgrad = [&](int li, size_t dy) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
-    LCHK(launch_wgrad_full(prec, ws + dy, ws + P.x, grad + L.w, (float*)(ws + pl.wpart), pl.N, P.Hin, P.Win, L.cin_p,
-                           L.cin, P.Ho, P.Wo, L.cout, L.k, L.s, L.p, P.splits, P.pps, st, c, li));
+    LCHK(launch_wgrad_full(prec, ws + dy, ws + P.x, grad + L.w, (float*)(ws + pl.wpart), pl.N, P.Hin, P.Win, P.cin,
+                           L.cin, P.Ho, P.Wo, L.cout, P.k, P.s, P.p, P.splits, P.pps, st, c, li, P.s2d));
     return 0;
   };
   auto dgrad = [&](int li, size_t dy, size_t dx, int mode, size_t R, size_t Rm) -> int {
@@ -635,18 +664,35 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX, bi, ws + gB, inb))) return r;
     std::swap(gA, gB);
   }
-  size_t gstem = gA;
   if (a.imagenet) {
-    TIMED(RN18_K_MAXPOOL, 1, 0, kernel_instance_name("maxpool_bwd_kernel", prec), 0.0,
-          (double)N * a.convs[0].cout * ((double)pl.Hs * pl.Ws * es + (double)pl.Hp * pl.Wp * (es + 1)),
-          maxpool_bwd_launch(prec, ws + gA, (const uint8_t*)(ws + pl.parg), ws + gB, N, pl.Hs, pl.Ws,
-                             a.convs[0].cout, pl.Hp, pl.Wp, st));
-    gstem = gB;
-    if (!c->captures.empty() &&
-        (r = run_captures(c, RN18_CAP_DA_POOL, 0, ws + gB, (size_t)N * pl.Hs * pl.Ws * a.convs[0].cout * es)))
-      return r;
+    // stem BN backward straight from the pooled gradient (gA) and the argmax
+    const ConvL& L = a.convs[0];
+    const ConvP& P = pl.cp[0];
+    const int C0 = L.cout;
+    const uint8_t* parg = (const uint8_t*)(ws + pl.parg);
+    if (!c->captures.empty()) {
+      // debugging only: materialise the pool's input gradient to capture it
+      LCHK(maxpool_bwd_launch(prec, ws + gA, parg, ws + gB, N, pl.Hs, pl.Ws, C0, pl.Hp, pl.Wp, st));
+      if ((r = run_captures(c, RN18_CAP_DA_POOL, 0, ws + gB, (size_t)N * pl.Hs * pl.Ws * C0 * es))) return r;
+    }
+    int nblk = 0;
+    float* part = (float*)(ws + pl.part);
+    const float* sc = (const float*)(ws + P.scale);
+    const float* sf = (const float*)(ws + P.shift);
+    const double yb = (double)P.M * C0 * es, pb = (double)N * pl.Hp * pl.Wp * C0 * (es + 1);
+    TIMED(RN18_K_BN_BWD_REDUCE, 0, 0, kernel_instance_name("bn_bwd_partial_pool_kernel", prec), 0.0, yb + pb,
+          bn_bwd_partial_pool_launch(prec, ws + gA, parg, ws + P.y, sc, sf, (float*)(ws + P.mean),
+                                     (float*)(ws + P.rstd), N, pl.Hs, pl.Ws, C0, pl.Hp, pl.Wp, part, &nblk, st));
+    TIMED(RN18_K_BN_BWD_REDUCE, 0, 1, "bn_bwd_final_kernel", 0.0, 0.0,
+          bn_bwd_final_launch(part, nblk, P.M, C0, state + L.g, (float*)(ws + P.rstd), grad + L.g, grad + L.b,
+                              (float*)(ws + P.coef), st));
+    TIMED(RN18_K_BN_BWD_APPLY, 0, 0, kernel_instance_name("bn_bwd_apply_pool_kernel", prec), 0.0, 2 * yb + pb,
+          bn_bwd_apply_pool_launch(prec, ws + gA, parg, ws + P.y, sc, sf, (float*)(ws + P.mean),
+                                   (float*)(ws + P.coef), ws + pl.gy, N, pl.Hs, pl.Ws, C0, pl.Hp, pl.Wp, st));
+    if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DY, 0, ws + pl.gy, (size_t)P.M * C0 * es))) return r;
+  } else if ((r = bn_back(0, gA, pl.zstem, pl.gy))) {
+    return r;
   }
-  if ((r = bn_back(0, gstem, pl.zstem, pl.gy))) return r;
   if ((r = wgrad(0, pl.gy))) return r;
   TIMED(RN18_K_SGD, 0, 0, "sgd_kernel", 0.0, 20.0 * a.P,
         sgd_launch(state, grad, c->momentum, a.P, lr, c->cfg.momentum, c->cfg.weight_decay, st));
@@ -746,6 +792,18 @@ int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* st
     e.Cout = L.cout; e.Cin = L.cin; e.Cin_p = L.cin_p; e.KHW = L.k * L.k;
     e.n = (long)L.cout * L.k * L.k * L.cin_p;
     e.nprefix = pre;
+    e.mode = 0; e.pad_ = 0;
+    pre += e.n;
+    tab.push_back(e);
+  }
+  if (a.wf_s2d >= 0) {
+    const ConvL& L = a.convs[0];
+    RepackEntry e;
+    e.src = L.w; e.dst_f = a.wf_s2d; e.dst_d = -1;
+    e.Cout = L.cout; e.Cin = 3; e.Cin_p = 16; e.KHW = 16;
+    e.n = (long)L.cout * 16 * 16;
+    e.nprefix = pre;
+    e.mode = 1; e.pad_ = 0;
     pre += e.n;
     tab.push_back(e);
   }
@@ -966,7 +1024,17 @@ int rn18_debug_copy(rn18_ctx* h, int N, int H, int W, int which, int index, void
     case RN18_DBG_WD: if (conv_ok() && index > 0) src = (char*)c.wd + (size_t)a.convs[index].wd * c.es; break;
     case RN18_DBG_MEAN: if (conv_ok()) src = ws + pl->cp[index].mean; break;
     case RN18_DBG_RSTD: if (conv_ok()) src = ws + pl->cp[index].rstd; break;
-    case RN18_DBG_ZSTEM: src = ws + pl->zstem; break;
+    case RN18_DBG_ZSTEM:
+      src = ws + pl->zstem;
+      if (a.imagenet && ws) {
+        // the fused stem never stores its ReLU output; recompute it from the
+        // stem conv output with the coefficients of the last forward pass
+        const ConvP& P0 = pl->cp[0];
+        if (bn_apply_launch(c.prec, ws + P0.y, (const float*)(ws + P0.scale), (const float*)(ws + P0.shift), 1, 0,
+                            nullptr, nullptr, nullptr, ws + pl->zstem, P0.M, a.convs[0].cout, c.stream))
+          return fail(RN18_EHIP, "stem activation recompute failed");
+      }
+      break;
     case RN18_DBG_PARG: if (a.imagenet) src = ws + pl->parg; break;
     default: break;
   }

@@ -11,6 +11,7 @@
 // The elementwise passes (apply + ReLU + residual, backward apply) are 16-byte
 // HBM streams with the per-channel coefficients staged in LDS.
 #include "kernels.h"
+#include "pool.h"
 
 namespace rn18 {
 
@@ -133,7 +134,7 @@ __global__ __launch_bounds__(256) void bn_apply_kernel(const T* __restrict__ y, 
     float v[VW];
     unpack<T>(((const uint4*)y)[q], v);
 #pragma unroll
-    for (int e = 0; e < VW; ++e) v[e] = v[e] * sc[c0 + e] + sf[c0 + e];
+    for (int e = 0; e < VW; ++e) v[e] = bn_affine(v[e], sc[c0 + e], sf[c0 + e]);
     if (res_mode == 1) {
       float w[VW];
       unpack<T>(((const uint4*)r)[q], w);
@@ -271,6 +272,175 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const T* __restrict__
   }
 }
 
+// ---------------------------------------------------------------- stem + max pool
+// The stem's BN-apply + ReLU feeds only the 3x3 stride-2 max pool, so the
+// forward pass goes from the conv output y straight to the pooled tensor and
+// its argmax; the ReLU output itself is never stored. The backward pass reads
+// the pooled gradient and the argmax and gathers the gradient of each stem
+// pixel on the fly (rounded to the storage type, as a stored tensor would be),
+// with the ReLU mask recomputed from y by the same arithmetic.
+template <typename T>
+__device__ inline float stem_act(float y, float sc, float sf) {
+  const float t = bn_affine(y, sc, sf);
+  return TT<T>::to_f(TT<T>::from_f(t > 0.f ? t : 0.f));
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void bn_apply_pool_kernel(const T* __restrict__ y, const float* __restrict__ scale,
+                                                            const float* __restrict__ shift, T* __restrict__ pool,
+                                                            uint8_t* __restrict__ arg, int N, int H, int W, int C,
+                                                            int Ho, int Wo) {
+  constexpr int VW = TT<T>::VW;
+  __shared__ float sc[kMaxC], sf[kMaxC];
+  for (int c = threadIdx.x; c < C; c += 256) { sc[c] = scale[c]; sf[c] = shift[c]; }
+  __syncthreads();
+  const int cpr = C / VW;
+  const int total = N * Ho * Wo * cpr;
+  for (int q = blockIdx.x * 256 + threadIdx.x; q < total; q += gridDim.x * 256) {
+    const int pix = q / cpr, cc = q - pix * cpr;
+    const int t2 = pix / Wo, j = pix - t2 * Wo;
+    const int n = t2 / Ho, i = t2 - n * Ho;
+    const int c0 = cc * VW;
+    auto act = [&](float* v) {
+#pragma unroll
+      for (int e = 0; e < VW; ++e) v[e] = stem_act<T>(v[e], sc[c0 + e], sf[c0 + e]);
+    };
+    float best[VW];
+    uint8_t bi[VW];
+    pool_max_window<T>(y, n, i, j, cc, H, W, C, act, best, bi);
+    ((uint4*)pool)[q] = pack<T>(best);
+    ArgVec<VW>::store(arg + q * VW, bi);
+  }
+}
+
+// Masked stem gradients of the pixels of quad (n, qi, qj), chunk cg: g[p][]
+// (0 for pixels past the edge) and y[p][], p = 2*py + px.
+template <typename T>
+__device__ inline void stem_grad_quad(const T* __restrict__ dpool, const uint8_t* __restrict__ arg,
+                                      const T* __restrict__ y, const float* sc, const float* sf, int n, int qi, int qj,
+                                      int cg, int cpr, int H, int W, int Ho, int Wo, float (*g)[TT<T>::VW],
+                                      float (*yy)[TT<T>::VW]) {
+  constexpr int VW = TT<T>::VW;
+  pool_grad_quad<T>(dpool, arg, n, qi, qj, cg, cpr, Ho, Wo, g);
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int h = 2 * qi + (p >> 1), w = 2 * qj + (p & 1);
+    unpack<T>(((const uint4*)y)[((n * H + min(h, H - 1)) * W + min(w, W - 1)) * cpr + cg], yy[p]);
+  }
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int h = 2 * qi + (p >> 1), w = 2 * qj + (p & 1);
+    const bool in = h < H && w < W;
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+      const float gr = TT<T>::to_f(TT<T>::from_f(g[p][e]));
+      const bool live = in && stem_act<T>(yy[p][e], sc[cg * VW + e], sf[cg * VW + e]) > 0.f;
+      g[p][e] = live ? gr : 0.f;
+      yy[p][e] = in ? yy[p][e] : 0.f;
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void bn_bwd_partial_pool_kernel(const T* __restrict__ dpool,
+                                                                  const uint8_t* __restrict__ arg,
+                                                                  const T* __restrict__ y,
+                                                                  const float* __restrict__ scale,
+                                                                  const float* __restrict__ shift,
+                                                                  const float* __restrict__ mean,
+                                                                  const float* __restrict__ rstd, int N, int H, int W,
+                                                                  int C, int Ho, int Wo, float* __restrict__ part) {
+  constexpr int VW = TT<T>::VW;
+  __shared__ float red[2][256 * VW];
+  __shared__ float sc[kMaxC], sf[kMaxC];
+  for (int c = threadIdx.x; c < C; c += 256) { sc[c] = scale[c]; sf[c] = shift[c]; }
+  __syncthreads();
+  const int Hq = (H + 1) / 2, Wq = (W + 1) / 2;
+  const int Mq = N * Hq * Wq;
+  const int tpc = C / VW, rpi = 256 / tpc;
+  const int tid = threadIdx.x, cg = tid % tpc, rr = tid / tpc;
+  const int per_blk = (Mq + gridDim.x - 1) / gridDim.x;
+  const int q_begin = blockIdx.x * per_blk;
+  const int q_end = min(Mq, q_begin + per_blk);
+  float mu[VW], rs[VW], s1[VW], s2[VW];
+#pragma unroll
+  for (int e = 0; e < VW; ++e) {
+    mu[e] = mean[cg * VW + e];
+    rs[e] = rstd[cg * VW + e];
+    s1[e] = s2[e] = 0.f;
+  }
+  for (int q = q_begin + rr; q < q_end; q += rpi) {
+    const int t2 = q / Wq, qj = q - t2 * Wq;
+    const int n = t2 / Hq, qi = t2 - n * Hq;
+    float g[4][VW], yy[4][VW];
+    stem_grad_quad<T>(dpool, arg, y, sc, sf, n, qi, qj, cg, tpc, H, W, Ho, Wo, g, yy);
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+#pragma unroll
+      for (int e = 0; e < VW; ++e) {
+        s1[e] += g[p][e];
+        s2[e] += g[p][e] * ((yy[p][e] - mu[e]) * rs[e]);
+      }
+  }
+#pragma unroll
+  for (int e = 0; e < VW; ++e) {
+    red[0][rr * C + cg * VW + e] = s1[e];
+    red[1][rr * C + cg * VW + e] = s2[e];
+  }
+  __syncthreads();
+  for (int c = tid; c < C; c += 256) {
+    float a = 0.f, b = 0.f;
+    for (int q = 0; q < rpi; ++q) {
+      a += red[0][q * C + c];
+      b += red[1][q * C + c];
+    }
+    part[((long)blockIdx.x * C + c) * 2 + 0] = a;
+    part[((long)blockIdx.x * C + c) * 2 + 1] = b;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void bn_bwd_apply_pool_kernel(const T* __restrict__ dpool,
+                                                                const uint8_t* __restrict__ arg,
+                                                                const T* __restrict__ y,
+                                                                const float* __restrict__ scale,
+                                                                const float* __restrict__ shift,
+                                                                const float* __restrict__ mean,
+                                                                const float* __restrict__ coef, T* __restrict__ dy,
+                                                                int N, int H, int W, int C, int Ho, int Wo) {
+  constexpr int VW = TT<T>::VW;
+  __shared__ float k1[kMaxC], k2[kMaxC], k3[kMaxC], mu[kMaxC], sc[kMaxC], sf[kMaxC];
+  for (int c = threadIdx.x; c < C; c += 256) {
+    k1[c] = coef[3 * c];
+    k2[c] = coef[3 * c + 1];
+    k3[c] = coef[3 * c + 2];
+    mu[c] = mean[c];
+    sc[c] = scale[c];
+    sf[c] = shift[c];
+  }
+  __syncthreads();
+  const int cpr = C / VW;
+  const int Hq = (H + 1) / 2, Wq = (W + 1) / 2;
+  const int nq = N * Hq * Wq * cpr;
+  for (int q = blockIdx.x * 256 + threadIdx.x; q < nq; q += gridDim.x * 256) {
+    const int quad = q / cpr, cg = q - quad * cpr;
+    const int t2 = quad / Wq, qj = quad - t2 * Wq;
+    const int n = t2 / Hq, qi = t2 - n * Hq;
+    const int c0 = cg * VW;
+    float g[4][VW], yy[4][VW];
+    stem_grad_quad<T>(dpool, arg, y, sc, sf, n, qi, qj, cg, cpr, H, W, Ho, Wo, g, yy);
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int h = 2 * qi + (p >> 1), w = 2 * qj + (p & 1);
+      if (h >= H || w >= W) continue;
+      float o[VW];
+#pragma unroll
+      for (int e = 0; e < VW; ++e) o[e] = k1[c0 + e] * g[p][e] + k2[c0 + e] * (yy[p][e] - mu[c0 + e]) + k3[c0 + e];
+      ((uint4*)dy)[((n * H + h) * W + w) * cpr + cg] = pack<T>(o);
+    }
+  }
+}
+
 int stream_blocks(long nchunks) {
   long b = (nchunks + 255) / 256;
   if (b > 8192) b = 8192;
@@ -358,6 +528,55 @@ int bn_bwd_apply_launch(int prec, const void* dz, const void* mz, const void* y,
   else
     hipLaunchKernelGGL(bn_bwd_apply_kernel<float>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const float*)dz,
                        (const float*)mz, (const float*)y, mean, coef, (float*)dy, nchunks, C);
+  return ok();
+}
+
+int bn_apply_pool_launch(int prec, const void* y, const float* scale, const float* shift, void* pool, uint8_t* arg,
+                         int N, int H, int W, int C, int Ho, int Wo, hipStream_t s) {
+  if (C > kMaxC || (long)N * H * W * C >= (1l << 31)) return -1;
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const long total = (long)N * Ho * Wo * (C / vw);
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(bn_apply_pool_kernel<bf16_t>, dim3(stream_blocks(total)), dim3(256), 0, s, (const bf16_t*)y,
+                       scale, shift, (bf16_t*)pool, arg, N, H, W, C, Ho, Wo);
+  else
+    hipLaunchKernelGGL(bn_apply_pool_kernel<float>, dim3(stream_blocks(total)), dim3(256), 0, s, (const float*)y,
+                       scale, shift, (float*)pool, arg, N, H, W, C, Ho, Wo);
+  return ok();
+}
+
+int bn_bwd_partial_pool_launch(int prec, const void* dpool, const uint8_t* arg, const void* y, const float* scale,
+                               const float* shift, const float* mean, const float* rstd, int N, int H, int W, int C,
+                               int Ho, int Wo, float* part, int* nblk, hipStream_t s) {
+  if (C > kMaxC || (long)N * H * W * C >= (1l << 31)) return -1;
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const int rpi = 256 / (C / vw);
+  const long Mq = (long)N * ((H + 1) / 2) * ((W + 1) / 2);
+  const int nb = pick_blocks(Mq, rpi);
+  *nblk = nb;
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(bn_bwd_partial_pool_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, (const bf16_t*)dpool, arg,
+                       (const bf16_t*)y, scale, shift, mean, rstd, N, H, W, C, Ho, Wo, part);
+  else
+    hipLaunchKernelGGL(bn_bwd_partial_pool_kernel<float>, dim3(nb), dim3(256), 0, s, (const float*)dpool, arg,
+                       (const float*)y, scale, shift, mean, rstd, N, H, W, C, Ho, Wo, part);
+  return ok();
+}
+
+int bn_bwd_apply_pool_launch(int prec, const void* dpool, const uint8_t* arg, const void* y, const float* scale,
+                             const float* shift, const float* mean, const float* coef, void* dy, int N, int H, int W,
+                             int C, int Ho, int Wo, hipStream_t s) {
+  if (C > kMaxC || (long)N * H * W * C >= (1l << 31)) return -1;
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const long nchunks = (long)N * ((H + 1) / 2) * ((W + 1) / 2) * (C / vw);
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(bn_bwd_apply_pool_kernel<bf16_t>, dim3(stream_blocks(nchunks)), dim3(256), 0, s,
+                       (const bf16_t*)dpool, arg, (const bf16_t*)y, scale, shift, mean, coef, (bf16_t*)dy, N, H, W,
+                       C, Ho, Wo);
+  else
+    hipLaunchKernelGGL(bn_bwd_apply_pool_kernel<float>, dim3(stream_blocks(nchunks)), dim3(256), 0, s,
+                       (const float*)dpool, arg, (const float*)y, scale, shift, mean, coef, (float*)dy, N, H, W, C,
+                       Ho, Wo);
   return ok();
 }
 

@@ -345,28 +345,34 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
       hb[u] = wb[u] = pix[u] = 0;
     }
   }
-  const int CB = UNI ? g.Cin / KT : 1;
+  const int CB = UNI ? (g.Cin >= KT ? g.Cin / KT : 1) : 1;
 
   // Uniform path: per-lane byte offsets and tap-validity masks are fixed for
   // the whole K loop; a stage only adds the wave-uniform offset of its tap
-  // and channel block, kept incrementally in scalars.
+  // and channel block, kept incrementally in scalars. A 128-byte row is one
+  // tap and KT channels when Cin >= KT; with fewer channels it holds RT =
+  // KT / Cin consecutive taps along w (consecutive pixels, contiguous in
+  // NHWC), and each lane's chunk sits at its own pixel of the row.
   constexpr int UA = AI / NW, UB = BI / NW;        // A and B load instructions per wave
   static_assert(AI % NW == 0 && BI % NW == 0, "loads split evenly between A and B");
   const int es = (int)sizeof(T);
+  const int RT = UNI && g.Cin < KT ? KT / g.Cin : 1;   // taps per row
+  const int ntw_g = g.ntw / RT;                        // row groups along w
   uint32_t uoff[UNI ? IPW : 1];
   uint32_t umask[UNI ? UA : 1];
   i32x4_t rsA, rsB;
-  int st_ti = 0, st_th = 0, st_tw = 0, st_cb = 0;  // tap (th, tw), channel block of the next stage issued
+  int st_ti = 0, st_th = 0, st_tw = 0, st_cb = 0;  // tap (th, tw group), channel block of the next stage issued
   if (UNI) {
     rsA = buffer_rsrc(A, (uint32_t)((long)g.N * g.Hin * g.Win * g.Cin * es));
     rsB = buffer_rsrc(B, (uint32_t)((long)g.Cols * g.KHW * g.Cin * es));
+    const int lane_px = (c * VW) / g.Cin;              // pixel of this lane's chunk within a row
 #pragma unroll
     for (int u = 0; u < UA; ++u) {
       uint32_t m = 0;
       for (int th = 0; th < g.nth; ++th)
-        for (int tw = 0; tw < g.ntw; ++tw) {
-          const int h = hb[u] + g.dh0 + th * g.dhs, w = wb[u] + g.dw0 + tw * g.dws;
-          if (ok[u] && (unsigned)h < (unsigned)g.Hin && (unsigned)w < (unsigned)g.Win) m |= 1u << (th * g.ntw + tw);
+        for (int tg = 0; tg < ntw_g; ++tg) {
+          const int h = hb[u] + g.dh0 + th * g.dhs, w = wb[u] + g.dw0 + (tg * RT + lane_px) * g.dws;
+          if (ok[u] && (unsigned)h < (unsigned)g.Hin && (unsigned)w < (unsigned)g.Win) m |= 1u << (th * ntw_g + tg);
         }
       umask[u] = m;
       uoff[u] = (uint32_t)(pix[u] * g.Cin * es + c * 16);
@@ -375,8 +381,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
     for (int u = UA; u < IPW; ++u) uoff[u] = ok[u] ? (uint32_t)(boff[u] * es + c * 16) : kOutOfRange;
   }
   auto issue_uni = [&](int buf) {
-    const int dh = g.dh0 + st_th * g.dhs, dw = g.dw0 + st_tw * g.dws;
-    const int wt = (g.wkh0 + st_th * g.wkhs) * g.KW + g.wkw0 + st_tw * g.wkws;
+    const int dh = g.dh0 + st_th * g.dhs, dw = g.dw0 + st_tw * RT * g.dws;
+    const int wt = (g.wkh0 + st_th * g.wkhs) * g.KW + g.wkw0 + st_tw * RT * g.wkws;
     const uint32_t sa = (uint32_t)((dh * g.Win + dw) * g.Cin * es + st_cb * 128);
     const uint32_t sb = (uint32_t)(wt * g.Cin * es + st_cb * 128);
     const uint32_t base = smem_lds + (uint32_t)(buf * STAGE_U4 * 16);
@@ -393,31 +399,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
     if (++st_cb == CB) {
       st_cb = 0;
       ++st_ti;
-      if (++st_tw == g.ntw) { st_tw = 0; ++st_th; }
+      if (++st_tw == ntw_g) { st_tw = 0; ++st_th; }
     }
   };
 
+  // General path (channel chunks of different taps in one row): per-lane tap
+  // arithmetic and 64-bit addresses, padding read from the zero page.
   auto issue = [&](int s, int buf) {
-    int dh, dw, wt, ci;
-    bool kok;
-    if (UNI) {
-      const int tap = s / CB;
-      const int th = tap / g.ntw, tw = tap - th * g.ntw;
-      dh = g.dh0 + th * g.dhs;
-      dw = g.dw0 + tw * g.dws;
-      wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
-      ci = (s - tap * CB) * KT + c * VW;
-      kok = true;
-    } else {
-      const int k = s * KT + c * VW;
-      kok = k < g.K;
-      const int tap = kok ? k / g.Cin : 0;
-      ci = k - tap * g.Cin;
-      const int th = tap / g.ntw, tw = tap - th * g.ntw;
-      dh = g.dh0 + th * g.dhs;
-      dw = g.dw0 + tw * g.dws;
-      wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
-    }
+    const int k = s * KT + c * VW;
+    const bool kok = k < g.K;
+    const int tap = kok ? k / g.Cin : 0;
+    const int ci = k - tap * g.Cin;
+    const int th = tap / g.ntw, tw = tap - th * g.ntw;
+    const int dh = g.dh0 + th * g.dhs;
+    const int dw = g.dw0 + tw * g.dws;
+    const int wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
     const uint32_t base = smem_lds + (uint32_t)(buf * STAGE_U4 * 16);
 #pragma unroll
     for (int u = 0; u < IPW; ++u) {
@@ -919,7 +915,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g
 // group q sums splits q, q+4, ... and the four sums are added in order, so
 // the result is deterministic and the split axis is read in parallel.
 __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ P, int splits, int Cout,
-                                                           int KHW, int Cin, int Cin_real, float* __restrict__ out) {
+                                                           int KHW, int Cin, int Cin_real, float* __restrict__ out,
+                                                           int s2d) {
   __shared__ float part[4][64];
   const long total = (long)Cout * KHW * Cin;
   const long stride = total;
@@ -934,10 +931,17 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restri
     if (q == 0 && idx < total) {
       const float sum = ((part[0][e] + part[1][e]) + part[2][e]) + part[3][e];
       const int ci = (int)(idx % Cin);
-      if (ci < Cin_real) {
-        const long rest = idx / Cin;
-        const int tap = (int)(rest % KHW);
-        const int co = (int)(rest / KHW);
+      const long rest = idx / Cin;
+      const int tap = (int)(rest % KHW);
+      const int co = (int)(rest / KHW);
+      if (s2d) {
+        // 4x4 tap (a, b), channel (2*dy + dx)*3 + c  ->  7x7 tap (2a+dy-1, 2b+dx-1) of channel c
+        if (ci < 12) {
+          const int q = ci / 3, c = ci - 3 * q;
+          const int kh = 2 * (tap >> 2) + (q >> 1) - 1, kw = 2 * (tap & 3) + (q & 1) - 1;
+          if (kh >= 0 && kw >= 0) out[(((long)co * 3 + c) * 7 + kh) * 7 + kw] = sum;
+        }
+      } else if (ci < Cin_real) {
         out[((long)co * Cin_real + ci) * KHW + tap] = sum;
       }
     }
@@ -966,9 +970,21 @@ const void* zero_page() {
 
 // The uniform K loop needs whole 128-byte channel blocks per tap, at most 32
 // taps (one validity bit each) and buffers addressable with 31-bit offsets.
+// With fewer channels than a row (kt), a row must be whole consecutive taps
+// along w of a forward-ordered, stride-1 tap walk.
 bool gather_uniform(const ConvGather& g, int kt) {
   const long es = 128 / kt;
-  return g.Cin % kt == 0 && g.nth * g.ntw <= 32 && (long)g.N * g.Hin * g.Win * g.Cin * es < (1l << 31) &&
+  const int vw = 16 / (int)es;
+  bool rows_ok;
+  int groups = g.nth * g.ntw;
+  if (g.Cin % kt == 0) {
+    rows_ok = true;
+  } else {
+    const int rt = kt / g.Cin;
+    rows_ok = g.Cin % vw == 0 && kt % g.Cin == 0 && g.ntw % rt == 0 && g.dws == 1 && g.wkws == 1;
+    groups = g.nth * (g.ntw / (rows_ok ? rt : 1));
+  }
+  return rows_ok && groups <= 32 && (long)g.N * g.Hin * g.Win * g.Cin * es < (1l << 31) &&
          (long)g.Cols * g.KHW * g.Cin * es < (1l << 31);
 }
 
@@ -1195,12 +1211,13 @@ int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s) {
 }
 
 int wgrad_reduce_launch(const float* P, int splits, int Cout, int KHW, int Cin, int Cin_real,
-                        float* out_oihw, hipStream_t s) {
+                        float* out_oihw, int s2d, hipStream_t s) {
+  if (s2d && (KHW != 16 || Cin != 16 || Cin_real != 3)) return -1;
   const long total = (long)Cout * KHW * Cin;
   int blocks = (int)((total + 63) / 64);
   if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, s, P, splits, Cout, KHW, Cin, Cin_real,
-                     out_oihw);
+                     out_oihw, s2d);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 

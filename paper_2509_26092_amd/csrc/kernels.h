@@ -54,8 +54,11 @@ int conv_wgrad_override(int id);
 // Choose the split count for a weight-gradient GEMM (deterministic function of the shape).
 int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split);
 // Sum partials in split order; write OIHW gradient (Cin_real of Cin channels kept).
+// Fixed-order sum of the split partials [splits][Cout][KHW][Cin] into OIHW
+// [Cout][Cin_real][KHW]; s2d = 1 maps the space-to-depth stem partials
+// [Cout][4x4][16] back to the 7x7 stem [Cout][3][7][7].
 int wgrad_reduce_launch(const float* P, int splits, int Cout, int KHW, int Cin, int Cin_real,
-                        float* out_oihw, hipStream_t s);
+                        float* out_oihw, int s2d, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Batch norm (per-channel over M = N*H*W rows of an [M][C] tensor)
@@ -79,6 +82,17 @@ int bn_eval_coef_launch(const float* gamma, const float* beta, const float* rm, 
 int bn_bwd_partial_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
                           const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s);
 // dgamma, dbeta into grad; coefficients for the apply
+// ImageNet stem fused with its max pool (y = stem conv output [N][H][W][C],
+// pool / arg = pool output and argmax [N][Ho][Wo][C]): forward BN-apply +
+// ReLU + pool; backward BN reduce / apply reading the pooled gradient.
+int bn_apply_pool_launch(int prec, const void* y, const float* scale, const float* shift, void* pool, uint8_t* arg,
+                         int N, int H, int W, int C, int Ho, int Wo, hipStream_t s);
+int bn_bwd_partial_pool_launch(int prec, const void* dpool, const uint8_t* arg, const void* y, const float* scale,
+                               const float* shift, const float* mean, const float* rstd, int N, int H, int W, int C,
+                               int Ho, int Wo, float* part, int* nblk, hipStream_t s);
+int bn_bwd_apply_pool_launch(int prec, const void* dpool, const uint8_t* arg, const void* y, const float* scale,
+                             const float* shift, const float* mean, const float* coef, void* dy, int N, int H, int W,
+                             int C, int Ho, int Wo, hipStream_t s);
 int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float* gamma, const float* rstd,
                         float* dgamma, float* dbeta, float* coef, hipStream_t s);
 // dy = k1*g + k2*(y-mean) + k3
@@ -89,7 +103,14 @@ int bn_bwd_apply_launch(int prec, const void* dz, const void* mz, const void* y,
 // Misc streams
 // ---------------------------------------------------------------------------
 int ingest_launch(int prec, const float* img, void* x, int N, int H, int W, int Cp, hipStream_t s);
-struct RepackEntry { long src; long dst_f; long dst_d; int Cout, Cin, Cin_p, KHW; long n; long nprefix; };
+// NCHW fp32 images (3 channels, H and W even) -> 2x2 space-to-depth NHWC
+// [N][H/2][W/2][16]: channel (2*dy + dx)*3 + c holds pixel (2i+dy, 2j+dx) of
+// channel c; channels 12..15 are zero.
+int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, hipStream_t s);
+// mode 0: OIHW -> [Cout][KHW][Cin_p] (+ [Cin_p][KHW][Cout] when dst_d >= 0);
+// mode 1: the 7x7 stride-2 stem (Cin 3) as a 4x4 conv over its 2x2
+// space-to-depth input: [Cout][4x4][16], channel (2*dy + dx)*3 + c.
+struct RepackEntry { long src; long dst_f; long dst_d; int Cout, Cin, Cin_p, KHW; long n; long nprefix; int mode, pad_; };
 int repack_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* table_dev,
                   int nentries, long total, hipStream_t s);
 int maxpool_fwd_launch(int prec, const void* x, void* y, uint8_t* arg, int N, int H, int W, int C,

@@ -7,6 +7,7 @@
 #include <math.h>
 
 #include "kernels.h"
+#include "pool.h"
 
 namespace rn18 {
 
@@ -32,6 +33,28 @@ __global__ void ingest_kernel(const float* __restrict__ img, T* __restrict__ x, 
   }
 }
 
+template <typename T>
+__global__ void ingest_s2d_kernel(const float* __restrict__ img, T* __restrict__ x, long npix, int H, int W) {
+  constexpr int VW = TT<T>::VW;
+  const int Hs = H / 2, Ws = W / 2;
+  const long HW = (long)H * W;
+  for (long p = blockIdx.x * 256l + threadIdx.x; p < npix; p += (long)gridDim.x * 256) {
+    const long n = p / ((long)Hs * Ws);
+    const int r = (int)(p - n * Hs * Ws);
+    const int i = r / Ws, j = r - i * Ws;
+    const float* src = img + n * 3 * HW + (long)(2 * i) * W + 2 * j;
+    float v[16];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int c = 0; c < 3; ++c) v[q * 3 + c] = src[c * HW + (q >> 1) * W + (q & 1)];
+#pragma unroll
+    for (int c = 12; c < 16; ++c) v[c] = 0.f;
+#pragma unroll
+    for (int q = 0; q < 16 / VW; ++q) ((uint4*)x)[p * (16 / VW) + q] = pack<T>(v + q * VW);
+  }
+}
+
 // ------------------------------------------------------------------ repack
 template <typename T>
 __global__ void repack_kernel(const float* __restrict__ st, T* __restrict__ wf, T* __restrict__ wd,
@@ -48,7 +71,17 @@ __global__ void repack_kernel(const float* __restrict__ st, T* __restrict__ wf, 
     const int co = (int)(l / per_co);
     const int rem = (int)(l - (long)co * per_co);
     const int tap = rem / r.Cin_p, ci = rem - tap * r.Cin_p;
-    const float v = ci < r.Cin ? st[r.src + ((long)co * r.Cin + ci) * r.KHW + tap] : 0.f;
+    float v = 0.f;
+    if (r.mode == 1) {
+      // 4x4 tap (a, b), channel (2*dy + dx)*3 + c  <-  7x7 tap (2a+dy-1, 2b+dx-1) of channel c
+      if (ci < 12) {
+        const int q = ci / 3, c = ci - 3 * q;
+        const int kh = 2 * (tap >> 2) + (q >> 1) - 1, kw = 2 * (tap & 3) + (q & 1) - 1;
+        if (kh >= 0 && kw >= 0) v = st[r.src + (((long)co * 3 + c) * 7 + kh) * 7 + kw];
+      }
+    } else if (ci < r.Cin) {
+      v = st[r.src + ((long)co * r.Cin + ci) * r.KHW + tap];
+    }
     const T tv = TT<T>::from_f(v);
     wf[r.dst_f + l] = tv;
     if (r.dst_d >= 0) wd[r.dst_d + ((long)ci * r.KHW + tap) * r.Cout + co] = tv;
@@ -61,75 +94,38 @@ __global__ void maxpool_fwd_kernel(const T* __restrict__ x, T* __restrict__ y, u
                                    int H, int W, int C, int Ho, int Wo) {
   constexpr int VW = TT<T>::VW;
   const int cpr = C / VW;
-  const long total = (long)N * Ho * Wo * cpr;
-  for (long q = blockIdx.x * 256l + threadIdx.x; q < total; q += (long)gridDim.x * 256) {
-    const int cc = (int)(q % cpr);
-    const long pix = q / cpr;
-    const int j = (int)(pix % Wo);
-    const long t2 = pix / Wo;
-    const int i = (int)(t2 % Ho);
-    const int n = (int)(t2 / Ho);
+  const int total = N * Ho * Wo * cpr;
+  for (int q = blockIdx.x * 256 + threadIdx.x; q < total; q += gridDim.x * 256) {
+    const int pix = q / cpr, cc = q - pix * cpr;
+    const int t2 = pix / Wo, j = pix - t2 * Wo;
+    const int n = t2 / Ho, i = t2 - n * Ho;
     float best[VW];
     uint8_t bi[VW];
-#pragma unroll
-    for (int e = 0; e < VW; ++e) { best[e] = -INFINITY; bi[e] = 0; }
-    for (int kh = 0; kh < 3; ++kh) {
-      const int h = 2 * i - 1 + kh;
-      if ((unsigned)h >= (unsigned)H) continue;
-      for (int kw = 0; kw < 3; ++kw) {
-        const int w = 2 * j - 1 + kw;
-        if ((unsigned)w >= (unsigned)W) continue;
-        float v[VW];
-        unpack<T>(*(const uint4*)(x + (((long)n * H + h) * W + w) * C + cc * VW), v);
-#pragma unroll
-        for (int e = 0; e < VW; ++e)
-          if (v[e] > best[e]) { best[e] = v[e]; bi[e] = (uint8_t)(kh * 3 + kw); }
-      }
-    }
+    pool_max_window<T>(x, n, i, j, cc, H, W, C, [](float*) {}, best, bi);
     ((uint4*)y)[q] = pack<T>(best);
-    uint8_t* a = arg + q * VW;
-#pragma unroll
-    for (int e = 0; e < VW; ++e) a[e] = bi[e];
+    ArgVec<VW>::store(arg + q * VW, bi);
   }
 }
 
+// Gather form over 2x2 quads of input pixels (deterministic: no atomics).
 template <typename T>
 __global__ void maxpool_bwd_kernel(const T* __restrict__ dy, const uint8_t* __restrict__ arg, T* __restrict__ dx,
                                    int N, int H, int W, int C, int Ho, int Wo) {
   constexpr int VW = TT<T>::VW;
   const int cpr = C / VW;
-  const long total = (long)N * H * W * cpr;
-  for (long q = blockIdx.x * 256l + threadIdx.x; q < total; q += (long)gridDim.x * 256) {
-    const int cc = (int)(q % cpr);
-    const long pix = q / cpr;
-    const int w = (int)(pix % W);
-    const long t2 = pix / W;
-    const int h = (int)(t2 % H);
-    const int n = (int)(t2 / H);
-    float acc[VW];
+  const int Hq = (H + 1) / 2, Wq = (W + 1) / 2;
+  const int total = N * Hq * Wq * cpr;
+  for (int q = blockIdx.x * 256 + threadIdx.x; q < total; q += gridDim.x * 256) {
+    const int quad = q / cpr, cc = q - quad * cpr;
+    const int t2 = quad / Wq, qj = quad - t2 * Wq;
+    const int n = t2 / Hq, qi = t2 - n * Hq;
+    float acc[4][VW];
+    pool_grad_quad<T>(dy, arg, n, qi, qj, cc, cpr, Ho, Wo, acc);
 #pragma unroll
-    for (int e = 0; e < VW; ++e) acc[e] = 0.f;
-    for (int kh = 0; kh < 3; ++kh) {
-      const int hh = h + 1 - kh;
-      if (hh < 0 || (hh & 1)) continue;
-      const int i = hh >> 1;
-      if (i >= Ho) continue;
-      for (int kw = 0; kw < 3; ++kw) {
-        const int ww = w + 1 - kw;
-        if (ww < 0 || (ww & 1)) continue;
-        const int j = ww >> 1;
-        if (j >= Wo) continue;
-        const long oq = (((long)n * Ho + i) * Wo + j) * cpr + cc;
-        float g[VW];
-        unpack<T>(((const uint4*)dy)[oq], g);
-        const uint8_t* a = arg + oq * VW;
-        const uint8_t tap = (uint8_t)(kh * 3 + kw);
-#pragma unroll
-        for (int e = 0; e < VW; ++e)
-          if (a[e] == tap) acc[e] += g[e];
-      }
+    for (int p = 0; p < 4; ++p) {
+      const int h = 2 * qi + (p >> 1), w = 2 * qj + (p & 1);
+      if (h < H && w < W) ((uint4*)dx)[((n * H + h) * W + w) * cpr + cc] = pack<T>(acc[p]);
     }
-    ((uint4*)dx)[q] = pack<T>(acc);
   }
 }
 
@@ -369,6 +365,16 @@ int ingest_launch(int prec, const float* img, void* x, int N, int H, int W, int 
   return ok();
 }
 
+int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, hipStream_t s) {
+  if (H % 2 || W % 2) return -1;
+  const long npix = (long)N * (H / 2) * (W / 2);
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(ingest_s2d_kernel<bf16_t>, dim3(grid_for(npix)), dim3(256), 0, s, img, (bf16_t*)x, npix, H, W);
+  else
+    hipLaunchKernelGGL(ingest_s2d_kernel<float>, dim3(grid_for(npix)), dim3(256), 0, s, img, (float*)x, npix, H, W);
+  return ok();
+}
+
 int repack_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* tab, int nent, long total,
                   hipStream_t s) {
   if (nent > 24) return -1;
@@ -385,6 +391,7 @@ int maxpool_fwd_launch(int prec, const void* x, void* y, uint8_t* arg, int N, in
                        hipStream_t s) {
   const int vw = prec == PREC_BF16 ? 8 : 4;
   const long work = (long)N * Ho * Wo * (C / vw);
+  if ((long)N * H * W * C >= (1l << 31)) return -1;  // 32-bit chunk indices
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(maxpool_fwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, (const bf16_t*)x,
                        (bf16_t*)y, arg, N, H, W, C, Ho, Wo);
@@ -397,7 +404,8 @@ int maxpool_fwd_launch(int prec, const void* x, void* y, uint8_t* arg, int N, in
 int maxpool_bwd_launch(int prec, const void* dy, const uint8_t* arg, void* dx, int N, int H, int W, int C, int Ho,
                        int Wo, hipStream_t s) {
   const int vw = prec == PREC_BF16 ? 8 : 4;
-  const long work = (long)N * H * W * (C / vw);
+  const long work = (long)N * ((H + 1) / 2) * ((W + 1) / 2) * (C / vw);
+  if ((long)N * H * W * C >= (1l << 31)) return -1;  // 32-bit chunk indices
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(maxpool_bwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, (const bf16_t*)dy, arg,
                        (bf16_t*)dx, N, H, W, C, Ho, Wo);

@@ -81,6 +81,13 @@ def test_imagenet_fp32_small():
     _run_parity("imagenet", 1000, "fp32", 3, 64, seed=120)
 
 
+@pytest.mark.parametrize("prec,N,H", [("fp32", 2, 65), ("bf16", 3, 63)])
+def test_imagenet_odd_resolution(prec, N, H):
+    """Odd image sizes: the stem runs as the plain 7x7 stride-2 conv (even
+    sizes use its space-to-depth form)."""
+    _run_parity("imagenet", 1000, prec, N, H, seed=121 + H)
+
+
 def test_two_steps_with_momentum():
     arch, classes, prec, N, H, seed = "tiny", 10, "fp32", 8, 16, 130
     L, st = make_state(arch, classes, seed)
