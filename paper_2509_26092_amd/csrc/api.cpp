@@ -159,6 +159,7 @@ struct Plan {
   size_t f, logits, dlogits, df, rowloss, lossbuf;
   size_t gA, gB, gz, gy, gyd;
   size_t part, wpart, grad;
+  size_t bnst;                  // forward conv epilogue BN partials per tile (64 rows at least)
   size_t total;
 };
 
@@ -336,6 +337,12 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   pl->gy = alloc(max_y);
   pl->gyd = alloc(max_yd ? max_yd : 16);
   pl->part = alloc((size_t)max_partC * 4);
+  size_t max_bnst = 0;
+  for (size_t li = 0; li < a.convs.size(); ++li) {
+    const size_t b = (size_t)ceil_div(pl->cp[li].M, 64) * a.convs[li].cout * 4 * 4;
+    if (b > max_bnst) max_bnst = b;
+  }
+  pl->bnst = alloc(max_bnst);
   // the weight-gradient split-K scratch also holds the classifier's split-K
   // partials (the classifier runs before any weight gradient)
   for (size_t hw : {gemm_f32_workspace(N, C, a.feat), gemm_f32_workspace(C, a.feat, N),
@@ -510,6 +517,9 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     ConvGather g = gather_fwd(ws + P.x, W(li), ws + P.y, N, P.Hin, P.Win, P.cin, P.Ho, P.Wo, L.cout, P.k, P.s, P.p);
+    // training: the conv epilogue also writes per-tile BN partials of its output
+    float* tstats = (float*)(ws + pl.bnst);
+    if (train) g.stats = tstats;
     const double xb = (double)N * P.Hin * P.Win * P.cin * es, yb = (double)P.M * L.cout * es;
     TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(g), conv_gather_kernel_name(prec, g), 2.0 * P.M * L.cout * L.k * L.k * L.cin,
           xb + yb + (double)L.cout * P.k * P.k * P.cin * es, conv_gather_launch(prec, g, st));
@@ -518,12 +528,10 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     float* sc = (float*)(ws + P.scale);
     float* sf = (float*)(ws + P.shift);
     if (train) {
-      int nblk = 0;
-      float* part = (float*)(ws + pl.part);
-      TIMED(RN18_K_BN_STATS, li, 0, kernel_instance_name("bn_stats_partial_kernel", prec), 0.0, yb, bn_stats_partial_launch(prec, ws + P.y, P.M, L.cout, part, &nblk, st));
-      TIMED(RN18_K_BN_STATS, li, 1, kernel_instance_name("bn_stats_final_kernel", prec), 0.0, 0.0,
-            bn_stats_final_launch(prec, ws + P.y, part, nblk, P.M, L.cout, state_c + L.g, state_c + L.b, eps, mom,
-                                  state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, st));
+      const int ntiles = ceil_div(P.M, conv_gather_tile(g) / 1000);
+      TIMED(RN18_K_BN_STATS, li, 1, "bn_stats_tiles_final_kernel", 0.0, (double)ntiles * L.cout * 16,
+            bn_stats_tiles_final_launch(tstats, ntiles, L.cout, state_c + L.g, state_c + L.b, eps, mom,
+                                        state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, st));
     } else {
       LCHK(bn_eval_coef_launch(state_c + L.g, state_c + L.b, state_c + L.rm, state_c + L.rv, eps, L.cout, sc, sf, st));
     }

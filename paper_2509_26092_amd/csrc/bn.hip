@@ -1,12 +1,12 @@
 // Batch normalisation (training mode) over an NHWC tensor viewed as [M][C]:
 // statistics per channel over all M = N*H*W rows.
 //
-// Statistics are two-level and deterministic: each block reduces a contiguous
-// range of rows to per-channel partial sums in fp32 (16-byte row chunks read
-// coalesced, then a fixed-order LDS reduction), and a finalize kernel combines
-// the block partials in fp64. The forward sums are taken of (y - y[0][c]):
-// shifting by a sample of the channel keeps Sum(v^2) - (Sum v)^2/M well
-// conditioned when |mean| >> std.
+// Statistics are two-level and deterministic. Forward: the conv epilogue
+// writes per-tile partial sums of (v - shift) and (v - shift)^2 with a sample
+// of the channel as the shift (well conditioned when |mean| >> std), and a
+// finalize kernel merges the tiles in fp64. Backward: each block reduces a
+// contiguous range of rows to per-channel partial sums in fp32 (16-byte row
+// chunks read coalesced, then a fixed-order LDS reduction), combined in fp64.
 //
 // The elementwise passes (apply + ReLU + residual, backward apply) are 16-byte
 // HBM streams with the per-channel coefficients staged in LDS.
@@ -26,47 +26,6 @@ int pick_blocks(long M, int rows_per_iter) {
   return (int)b;
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void bn_stats_partial_kernel(const T* __restrict__ y, long M, int C,
-                                                               float* __restrict__ part) {
-  constexpr int VW = TT<T>::VW;
-  __shared__ float red[2][256 * VW];
-  const int tpc = C / VW, rpi = 256 / tpc;
-  const int tid = threadIdx.x, cg = tid % tpc, rr = tid / tpc;
-  const long rows_per_blk = (M + gridDim.x - 1) / gridDim.x;
-  const long r_begin = blockIdx.x * rows_per_blk;
-  const long r_end = min(M, r_begin + rows_per_blk);
-  float piv[VW], s1[VW], s2[VW];
-  unpack<T>(*(const uint4*)(y + cg * VW), piv);
-#pragma unroll
-  for (int e = 0; e < VW; ++e) s1[e] = s2[e] = 0.f;
-  for (long r = r_begin + rr; r < r_end; r += rpi) {
-    float v[VW];
-    unpack<T>(*(const uint4*)(y + r * C + cg * VW), v);
-#pragma unroll
-    for (int e = 0; e < VW; ++e) {
-      const float d = v[e] - piv[e];
-      s1[e] += d;
-      s2[e] += d * d;
-    }
-  }
-#pragma unroll
-  for (int e = 0; e < VW; ++e) {
-    red[0][rr * C + cg * VW + e] = s1[e];
-    red[1][rr * C + cg * VW + e] = s2[e];
-  }
-  __syncthreads();
-  for (int c = tid; c < C; c += 256) {
-    float a = 0.f, b = 0.f;
-    for (int q = 0; q < rpi; ++q) {
-      a += red[0][q * C + c];
-      b += red[1][q * C + c];
-    }
-    part[((long)blockIdx.x * C + c) * 2 + 0] = a;
-    part[((long)blockIdx.x * C + c) * 2 + 1] = b;
-  }
-}
-
 __device__ inline double block_sum_d(double v, double* sh) {
   const int tid = threadIdx.x;
   sh[tid] = v;
@@ -80,27 +39,47 @@ __device__ inline double block_sum_d(double v, double* sh) {
   return r;
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void bn_stats_final_kernel(const T* __restrict__ y, const float* __restrict__ part,
-                                                             int nblk, long M, int C, const float* gamma,
-                                                             const float* beta, float eps, float mom, float* rm,
-                                                             float* rv, float* mean_o, float* rstd_o,
-                                                             float* scale_o, float* shift_o) {
-  __shared__ double sh[256];
-  const int c = blockIdx.x;
-  double a = 0.0, b = 0.0;
-  for (int q = threadIdx.x; q < nblk; q += 256) {
-    a += part[((long)q * C + c) * 2 + 0];
-    b += part[((long)q * C + c) * 2 + 1];
+// Combine per-tile partials (rows, shift, shifted sum, shifted sum of
+// squares) of the forward conv epilogue into the batch statistics of channel
+// blockIdx.x: each tile's mean and M2 in fp64, then a fixed partition of the
+// tiles over the threads, Chan et al.'s pairwise update in fp64, then a
+// fixed-order tree over the threads. Biased variance M2/M for normalising,
+// unbiased M2/(M-1) for the running variance.
+__device__ inline void chan_merge(double& na, double& ma, double& qa, double nb, double mb, double qb) {
+  if (nb == 0.0) return;
+  if (na == 0.0) { na = nb; ma = mb; qa = qb; return; }
+  const double n = na + nb, d = mb - ma;
+  ma += d * (nb / n);
+  qa += qb + d * d * (na * nb / n);
+  na = n;
+}
+
+__global__ __launch_bounds__(256) void bn_stats_tiles_final_kernel(const float* __restrict__ st, int ntiles, int C,
+                                                                   const float* gamma, const float* beta, float eps,
+                                                                   float mom, float* rm, float* rv, float* mean_o,
+                                                                   float* rstd_o, float* scale_o, float* shift_o) {
+  __shared__ double sn[256], sm[256], sq[256];
+  const int c = blockIdx.x, t = threadIdx.x;
+  double na = 0.0, ma = 0.0, qa = 0.0;
+  for (int z = t; z < ntiles; z += 256) {
+    // tile partial: rows n, shift x0, sum of (v - x0), sum of (v - x0)^2
+    const float4 p = ((const float4*)st)[(long)z * C + c];
+    const double n = p.x, s1 = p.z;
+    if (n > 0.0) chan_merge(na, ma, qa, n, (double)p.y + s1 / n, fmax((double)p.w - s1 * s1 / n, 0.0));
   }
-  a = block_sum_d(a, sh);
-  b = block_sum_d(b, sh);
-  if (threadIdx.x == 0) {
-    const double piv = (double)TT<T>::to_f(y[c]);
-    const double md = a / (double)M;
-    double var = b / (double)M - md * md;
-    if (var < 0.0) var = 0.0;
-    const double mean = piv + md;
+  sn[t] = na; sm[t] = ma; sq[t] = qa;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (t < h) {
+      double a = sn[t], b = sm[t], q = sq[t];
+      chan_merge(a, b, q, sn[t + h], sm[t + h], sq[t + h]);
+      sn[t] = a; sm[t] = b; sq[t] = q;
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    const double M = sn[0], mean = sm[0];
+    const double var = M > 0.0 ? sq[0] / M : 0.0;
     const double rstd = 1.0 / sqrt(var + (double)eps);
     const double sc = (double)gamma[c] * rstd;
     mean_o[c] = (float)mean;
@@ -109,7 +88,7 @@ __global__ __launch_bounds__(256) void bn_stats_final_kernel(const T* __restrict
     shift_o[c] = (float)((double)beta[c] - mean * sc);
     if (rm) {
       rm[c] = (float)((1.0 - mom) * (double)rm[c] + mom * mean);
-      rv[c] = (float)((1.0 - mom) * (double)rv[c] + mom * var * ((double)M / (double)(M - 1)));
+      rv[c] = (float)((1.0 - mom) * (double)rv[c] + mom * (M > 1.0 ? sq[0] / (M - 1.0) : 0.0));
     }
   }
 }
@@ -452,30 +431,6 @@ inline int ok() { return hipGetLastError() == hipSuccess ? 0 : -4; }
 
 }  // namespace
 
-int bn_stats_partial_launch(int prec, const void* y, long M, int C, float* part, int* nblk, hipStream_t s) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
-  const int rpi = 256 / (C / vw);
-  const int nb = pick_blocks(M, rpi);
-  *nblk = nb;
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(bn_stats_partial_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, (const bf16_t*)y, M, C, part);
-  else
-    hipLaunchKernelGGL(bn_stats_partial_kernel<float>, dim3(nb), dim3(256), 0, s, (const float*)y, M, C, part);
-  return ok();
-}
-
-int bn_stats_final_launch(int prec, const void* y, const float* part, int nblk, long M, int C, const float* gamma,
-                          const float* beta, float eps, float momentum, float* run_mean, float* run_var,
-                          float* mean, float* rstd, float* scale, float* shift, hipStream_t s) {
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(bn_stats_final_kernel<bf16_t>, dim3(C), dim3(256), 0, s, (const bf16_t*)y, part, nblk, M, C,
-                       gamma, beta, eps, momentum, run_mean, run_var, mean, rstd, scale, shift);
-  else
-    hipLaunchKernelGGL(bn_stats_final_kernel<float>, dim3(C), dim3(256), 0, s, (const float*)y, part, nblk, M, C,
-                       gamma, beta, eps, momentum, run_mean, run_var, mean, rstd, scale, shift);
-  return ok();
-}
-
 int bn_apply_launch(int prec, const void* y, const float* scale, const float* shift, int relu, int res_mode,
                     const void* r, const float* scale2, const float* shift2, void* z, long M, int C, hipStream_t s) {
   const int vw = prec == PREC_BF16 ? 8 : 4;
@@ -577,6 +532,14 @@ int bn_bwd_apply_pool_launch(int prec, const void* dpool, const uint8_t* arg, co
     hipLaunchKernelGGL(bn_bwd_apply_pool_kernel<float>, dim3(stream_blocks(nchunks)), dim3(256), 0, s,
                        (const float*)dpool, arg, (const float*)y, scale, shift, mean, coef, (float*)dy, N, H, W, C,
                        Ho, Wo);
+  return ok();
+}
+
+int bn_stats_tiles_final_launch(const float* tile_stats, int ntiles, int C, const float* gamma, const float* beta,
+                                float eps, float momentum, float* run_mean, float* run_var, float* mean, float* rstd,
+                                float* scale, float* shift, hipStream_t s) {
+  hipLaunchKernelGGL(bn_stats_tiles_final_kernel, dim3(C), dim3(256), 0, s, tile_stats, ntiles, C, gamma, beta, eps,
+                     momentum, run_mean, run_var, mean, rstd, scale, shift);
   return ok();
 }
 

@@ -86,142 +86,6 @@ __device__ inline void mma_stage(floatx4_t (&acc)[FM][FN], const uint4* As, cons
 }
 
 // ---------------------------------------------------------------------------
-// Gather conv (forward and data gradient)
-// ---------------------------------------------------------------------------
-template <typename T, int BM, int BN, int WGM, int WGN>
-__global__ __launch_bounds__(256) void conv_gather_kernel(ConvGather g) {
-  constexpr int VW = TT<T>::VW;
-  constexpr int KT = 128 / (int)sizeof(T);
-  constexpr int WTM = BM / WGM, WTN = BN / WGN;
-  constexpr int FM = WTM / 16, FN = WTN / 16;
-  constexpr int AQ = (BM + 31) / 32, BQ = (BN + 31) / 32;
-  constexpr int STAGE = (BM + BN) * RSTR;
-  constexpr int CSTR = BN + 4;
-  constexpr int SM_LOOP = 2 * STAGE;
-  constexpr int SM_EPI = (BM * CSTR + 3) / 4;
-  __shared__ uint4 smem[SM_LOOP > SM_EPI ? SM_LOOP : SM_EPI];
-  static_assert(WGM * WGN == 4, "4 waves");
-  static_assert(FM >= 1 && FN >= 1, "wave tile >= 16x16");
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
-  const int tiles_n = (g.Cols + BN - 1) / BN;
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
-  const int m0 = (t / tiles_n) * BM, n0 = (t % tiles_n) * BN;
-
-  const T* __restrict__ A = (const T*)g.A;
-  const T* __restrict__ B = (const T*)g.B;
-  const int c = tid & 7, r0 = tid >> 3;
-  const int HWm = g.Hm * g.Wm;
-
-  int a_img[AQ], a_hb[AQ], a_wb[AQ];
-  bool a_ok[AQ];
-#pragma unroll
-  for (int q = 0; q < AQ; ++q) {
-    int m = m0 + r0 + 32 * q;
-    a_ok[q] = m < g.M;
-    int mm = a_ok[q] ? m : 0;
-    int n = mm / HWm, rem = mm - n * HWm;
-    int i = rem / g.Wm, j = rem - i * g.Wm;
-    a_img[q] = n * g.Hin * g.Win;
-    a_hb[q] = i * g.is - g.ip;
-    a_wb[q] = j * g.is - g.ip;
-  }
-
-  uint4 ra[AQ], rb[BQ];
-  auto load = [&](int k0) {
-    const int k = k0 + c * VW;
-    const bool kok = k < g.K;
-    const int tap = kok ? k / g.Cin : 0;
-    const int ci = k - tap * g.Cin;
-    const int th = tap / g.ntw, tw = tap - th * g.ntw;
-    const int dh = g.dh0 + th * g.dhs, dw = g.dw0 + tw * g.dws;
-    const int wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
-#pragma unroll
-    for (int q = 0; q < AQ; ++q) {
-      const int hi = a_hb[q] + dh, wi = a_wb[q] + dw;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (kok && a_ok[q] && (unsigned)hi < (unsigned)g.Hin && (unsigned)wi < (unsigned)g.Win)
-        v = *(const uint4*)(A + (long)(a_img[q] + hi * g.Win + wi) * g.Cin + ci);
-      ra[q] = v;
-    }
-#pragma unroll
-    for (int q = 0; q < BQ; ++q) {
-      const int col = n0 + r0 + 32 * q;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (kok && col < g.Cols && r0 + 32 * q < BN) v = *(const uint4*)(B + ((long)col * g.KHW + wt) * g.Cin + ci);
-      rb[q] = v;
-    }
-  };
-  auto store = [&](int buf) {
-    uint4* As = smem + buf * STAGE;
-    uint4* Bs = As + BM * RSTR;
-#pragma unroll
-    for (int q = 0; q < AQ; ++q)
-      if (r0 + 32 * q < BM) As[(r0 + 32 * q) * RSTR + c] = ra[q];
-#pragma unroll
-    for (int q = 0; q < BQ; ++q)
-      if (r0 + 32 * q < BN) Bs[(r0 + 32 * q) * RSTR + c] = rb[q];
-  };
-
-  floatx4_t acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-
-  const int S = (g.K + KT - 1) / KT;
-  load(0);
-  store(0);
-  __syncthreads();
-  for (int s = 0; s < S; ++s) {
-    if (s + 1 < S) load((s + 1) * KT);
-    const uint4* As = smem + (s & 1) * STAGE;
-    mma_stage<T, FM, FN>(acc, As, As + BM * RSTR, wm * WTM, wn * WTN, lane);
-    if (s + 1 < S) store((s + 1) & 1);
-    __syncthreads();
-  }
-
-  // Epilogue through LDS so that global stores are 16-byte row chunks.
-  float* Cs = (float*)smem;
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        Cs[(wm * WTM + i * 16 + 4 * (lane >> 4) + r) * CSTR + wn * WTN + j * 16 + (lane & 15)] = acc[i][j][r];
-  __syncthreads();
-
-  constexpr int CPR = BN / VW;
-  T* __restrict__ Cg = (T*)g.C;
-  for (int idx = tid; idx < BM * CPR; idx += 256) {
-    const int row = idx / CPR, cc = idx - row * CPR;
-    const int m = m0 + row, col = n0 + cc * VW;
-    if (m >= g.M || col >= g.Cols) continue;
-    const int n = m / HWm, rem = m - n * HWm;
-    const int i = rem / g.Wm, j = rem - i * g.Wm;
-    const long off = ((long)(n * g.Hout + i * g.os + g.oph) * g.Wout + j * g.os + g.opw) * g.Cols + col;
-    float v[VW];
-#pragma unroll
-    for (int e = 0; e < VW; ++e) v[e] = Cs[row * CSTR + cc * VW + e];
-    if (g.mode == 1) {
-      float o[VW];
-      unpack<T>(*(const uint4*)(Cg + off), o);
-#pragma unroll
-      for (int e = 0; e < VW; ++e) v[e] += o[e];
-    } else if (g.mode == 2) {
-      float rr[VW], mk[VW];
-      unpack<T>(*(const uint4*)((const T*)g.R + off), rr);
-      unpack<T>(*(const uint4*)((const T*)g.Rm + off), mk);
-#pragma unroll
-      for (int e = 0; e < VW; ++e) v[e] += mk[e] > 0.f ? rr[e] : 0.f;
-    }
-    *(uint4*)(Cg + off) = pack<T>(v);
-  }
-}
-
-// ---------------------------------------------------------------------------
 // Gather conv, pipelined: the K loop streams 128-byte row stages from global
 // memory straight into an LDS ring of STAGES buffers (gfx950
 // global_load_lds_dwordx4, one 16-byte chunk per lane, written lane-contiguous
@@ -302,7 +166,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
   constexpr int SM_LOOP = STAGES * STAGE_U4;
   constexpr int WSTR = WTN + 4;                    // epilogue strip row stride (floats)
   constexpr int SM_EPI = NW * 16 * WSTR / 4;       // one 16-row strip per wave
-  __shared__ uint4 smem[SM_LOOP > SM_EPI ? SM_LOOP : SM_EPI];
+  constexpr int ST_F = 2 * VW;                     // per-lane BN partial: VW shifted sums, VW squares
+  constexpr int SM_ST = SM_EPI + (BN + NW * 64 * ST_F + 3) / 4;
+  __shared__ uint4 smem[SM_LOOP > SM_ST ? SM_LOOP : SM_ST];
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   static_assert(NI % NW == 0 && BN % 8 == 0, "whole load instructions per wave");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
@@ -476,10 +342,33 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
 
   // Epilogue per wave, one 16-row strip at a time: the strip's accumulators
   // go through a wave-private LDS buffer and leave as 16-byte chunks of
-  // consecutive output channels.
+  // consecutive output channels. With g.stats set (forward pass followed by
+  // batch norm), the stored (rounded) values also feed per-channel partial
+  // statistics of the tile: sums of v - shift and (v - shift)^2, with the
+  // tile's first row as the shift (a sample of the channel keeps the sums
+  // well conditioned), summed over lanes and waves in a fixed order and
+  // written to g.stats[tile_m][col] as (rows, shift, sum, sum of squares).
   float* Ws = (float*)smem + wave_u * 16 * WSTR;
-  constexpr int CPW = WTN / VW;                    // chunks per strip row
+  constexpr int CPW = WTN / VW;                    // chunks per strip row; a lane's chunk column is lane % CPW
+  static_assert(64 % CPW == 0, "lane chunk column fixed across strips");
   T* __restrict__ Cg = (T*)g.C;
+  const bool stats = g.stats != nullptr;
+  float* Sh = (float*)smem + SM_EPI * 4;           // [BN] shifts, then [NW][64][ST_F] lane sums
+  float* St = Sh + BN;
+  float ssh[VW], ss1[VW], ss2[VW];
+#pragma unroll
+  for (int e = 0; e < VW; ++e) ssh[e] = ss1[e] = ss2[e] = 0.f;
+  if (stats) {
+    // tile row 0 sits in strip 0, register 0 of lanes 0..15 of the waves with wm == 0
+    if (wm == 0 && lane < 16) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) Sh[brow0 + j * 16 + lane] = TT<T>::to_f(TT<T>::from_f(acc[0][j][0]));
+    }
+    __syncthreads();
+    const int cc = lane % CPW;
+#pragma unroll
+    for (int e = 0; e < VW; ++e) ssh[e] = Sh[brow0 + cc * VW + e];
+  }
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -510,8 +399,41 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
 #pragma unroll
         for (int e = 0; e < VW; ++e) v[e] += mk[e] > 0.f ? rr[e] : 0.f;
       }
-      *(uint4*)(Cg + off) = pack<T>(v);
+      const uint4 pk = pack<T>(v);
+      *(uint4*)(Cg + off) = pk;
+      if (stats) {
+        float vr[VW];
+        unpack<T>(pk, vr);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          const float d = vr[e] - ssh[e];
+          ss1[e] += d;
+          ss2[e] = __builtin_fmaf(d, d, ss2[e]);
+        }
+      }
     }
+  }
+  if (!stats) return;
+  {
+    float* o = St + (wave_u * 64 + lane) * ST_F;
+#pragma unroll
+    for (int e = 0; e < VW; ++e) { o[e] = ss1[e]; o[VW + e] = ss2[e]; }
+  }
+  __syncthreads();
+  const int rows = min(BM, g.M - m0);
+  for (int cl = tid; cl < BN; cl += NT) {
+    const int col = n0 + cl;
+    if (col >= g.Cols) continue;
+    const int wn_c = cl / WTN, cw = cl - wn_c * WTN, cc = cw / VW, e = cw - cc * VW;
+    float a1 = 0.f, a2 = 0.f;
+    for (int wmi = 0; wmi < WGM; ++wmi)
+      for (int k = 0; k < 64 / CPW; ++k) {
+        const float* p = St + ((wmi * WGN + wn_c) * 64 + cc + CPW * k) * ST_F;
+        a1 += p[e];
+        a2 += p[VW + e];
+      }
+    float4* out = (float4*)g.stats + ((long)(m0 / BM) * g.Cols + col);
+    *out = make_float4((float)rows, Sh[cl], a1, a2);
   }
 }
 
@@ -947,13 +869,6 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restri
     }
     __syncthreads();
   }
-}
-
-template <typename T, int BM, int BN, int WGM, int WGN>
-int launch_gather(const ConvGather& g, hipStream_t s) {
-  const int tiles = ceil_div(g.M, BM) * ceil_div(g.Cols, BN);
-  hipLaunchKernelGGL((conv_gather_kernel<T, BM, BN, WGM, WGN>), dim3(tiles), dim3(256), 0, s, g);
-  return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
 const void* zero_page() {

@@ -24,7 +24,7 @@ struct ConvGather {
   int wkh0, wkhs, wkw0, wkws, KW, KHW;  // weight tap (wkh0+th*wkhs)*KW + wkw0+tw*wkws
   int K;                     // nth*ntw*Cin
   int mode;                  // 0 store, 1 C += acc, 2 C = acc + (Rm>0 ? R : 0)
-  float* stats;              // optional BN partial sums [tiles_m][Cols][2] (mode 0 only)
+  float* stats;              // optional BN partials (rows, shift, sum, sum sq) [tiles_m][Cols][4] of the stored output
   const void* zero;          // 16-byte zero page (set by the launcher)
 };
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s);
@@ -64,12 +64,11 @@ int wgrad_reduce_launch(const float* P, int splits, int Cout, int KHW, int Cin, 
 // Batch norm (per-channel over M = N*H*W rows of an [M][C] tensor)
 // ---------------------------------------------------------------------------
 // partial sums of (y - pivot) and (y - pivot)^2 per block; pivot = y[0][c]
-int bn_stats_partial_launch(int prec, const void* y, long M, int C, float* part, int* nblk, hipStream_t s);
-// combine partials (fp64), write mean/rstd/scale/shift, update running stats
-int bn_stats_final_launch(int prec, const void* y, const float* part, int nblk, long M, int C,
-                          const float* gamma, const float* beta, float eps, float momentum,
-                          float* run_mean, float* run_var, float* mean, float* rstd,
-                          float* scale, float* shift, hipStream_t s);
+// Batch statistics from the forward conv epilogue's per-tile partials
+// (rows, shift, sum of v - shift, sum of (v - shift)^2) [ntiles][C][4].
+int bn_stats_tiles_final_launch(const float* tile_stats, int ntiles, int C, const float* gamma, const float* beta,
+                                float eps, float momentum, float* run_mean, float* run_var, float* mean, float* rstd,
+                                float* scale, float* shift, hipStream_t s);
 // z = act(y*scale+shift [+ r] [+ (yd*scale2+shift2)])
 //  res_mode: 0 none, 1 identity residual r, 2 projected residual (yd, scale2, shift2)
 int bn_apply_launch(int prec, const void* y, const float* scale, const float* shift, int relu,
