@@ -278,7 +278,7 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     P.splits = conv_wgrad_splits(c.prec, L.cout, P.k * P.k * P.cin, P.M, &P.pps);
     const size_t wp = (size_t)P.splits * L.cout * P.k * P.k * P.cin * 4;
     if (wp > max_wpart) max_wpart = wp;
-    const long pc = 1024l * L.cout * 2;
+    const long pc = 1024l * L.cout * 2 > 256l * L.cout * 6 ? 1024l * L.cout * 2 : 256l * L.cout * 6;
     if (pc > max_partC) max_partC = pc;
     return true;
   };
@@ -529,8 +529,9 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     float* sf = (float*)(ws + P.shift);
     if (train) {
       const int ntiles = ceil_div(P.M, conv_gather_tile(g) / 1000);
-      TIMED(RN18_K_BN_STATS, li, 1, "bn_stats_tiles_final_kernel", 0.0, (double)ntiles * L.cout * 16,
-            bn_stats_tiles_final_launch(tstats, ntiles, L.cout, state_c + L.g, state_c + L.b, eps, mom,
+      TIMED(RN18_K_BN_STATS, li, 1, "bn_stats_tiles_reduce_kernel", 0.0, (double)ntiles * L.cout * 16,
+            bn_stats_tiles_final_launch(tstats, ntiles, L.cout, (double*)(ws + pl.part), state_c + L.g,
+                                        state_c + L.b, eps, mom,
                                         state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, st));
     } else {
       LCHK(bn_eval_coef_launch(state_c + L.g, state_c + L.b, state_c + L.rm, state_c + L.rv, eps, L.cout, sc, sf, st));

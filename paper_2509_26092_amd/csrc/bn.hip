@@ -39,57 +39,80 @@ __device__ inline double block_sum_d(double v, double* sh) {
   return r;
 }
 
-// Combine per-tile partials (rows, shift, shifted sum, shifted sum of
-// squares) of the forward conv epilogue into the batch statistics of channel
-// blockIdx.x: each tile's mean and M2 in fp64, then a fixed partition of the
-// tiles over the threads, Chan et al.'s pairwise update in fp64, then a
-// fixed-order tree over the threads. Biased variance M2/M for normalising,
-// unbiased M2/(M-1) for the running variance.
-__device__ inline void chan_merge(double& na, double& ma, double& qa, double nb, double mb, double qb) {
-  if (nb == 0.0) return;
-  if (na == 0.0) { na = nb; ma = mb; qa = qb; return; }
-  const double n = na + nb, d = mb - ma;
-  ma += d * (nb / n);
-  qa += qb + d * d * (na * nb / n);
-  na = n;
+// Batch statistics from the per-tile partials (rows n, shift x0, sum of
+// v - x0, sum of (v - x0)^2) of the forward conv epilogue. Every tile's sums
+// are re-referenced to one sample of the channel, K = tile 0's shift, in
+// fp64 (d = x0 - K: S1 += s1 + n d, S2 += s2 + 2 d s1 + n d^2), so the
+// tiles simply add. Stage 1: grid (channel groups of 64, tile chunks), 4
+// thread groups per block over a chunk's tiles, fixed-order combine; stage 2:
+// per channel, 4 thread groups over the chunks, fixed-order combine, then
+// mean = K + S1/M, biased variance
+// S2/M - (S1/M)^2 for normalising, unbiased (M/(M-1)) for the running one.
+__global__ __launch_bounds__(256) void bn_stats_tiles_reduce_kernel(const float* __restrict__ st, int ntiles, int C,
+                                                                    int per_chunk, double* __restrict__ red) {
+  __shared__ double sh[3][4][64];
+  const int cl = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + cl;
+  const int z0 = blockIdx.y * per_chunk, z1 = min(ntiles, z0 + per_chunk);
+  double N = 0.0, S1 = 0.0, S2 = 0.0;
+  if (c < C) {
+    const double K = (double)((const float4*)st)[c].y;
+#pragma unroll 8
+    for (int z = z0 + q; z < z1; z += 4) {
+      const float4 p = ((const float4*)st)[(long)z * C + c];
+      const double n = p.x, d = (double)p.y - K, s1 = p.z;
+      N += n;
+      S1 += s1 + n * d;
+      S2 += (double)p.w + 2.0 * d * s1 + n * d * d;
+    }
+  }
+  sh[0][q][cl] = N; sh[1][q][cl] = S1; sh[2][q][cl] = S2;
+  __syncthreads();
+  if (q == 0 && c < C) {
+    double* o = red + ((long)blockIdx.y * C + c) * 3;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) o[k] = ((sh[k][0][cl] + sh[k][1][cl]) + sh[k][2][cl]) + sh[k][3][cl];
+  }
 }
 
-__global__ __launch_bounds__(256) void bn_stats_tiles_final_kernel(const float* __restrict__ st, int ntiles, int C,
+__global__ __launch_bounds__(256) void bn_stats_tiles_final_kernel(const float* __restrict__ st,
+                                                                   const double* __restrict__ red, int nchunks, int C,
                                                                    const float* gamma, const float* beta, float eps,
                                                                    float mom, float* rm, float* rv, float* mean_o,
                                                                    float* rstd_o, float* scale_o, float* shift_o) {
-  __shared__ double sn[256], sm[256], sq[256];
-  const int c = blockIdx.x, t = threadIdx.x;
-  double na = 0.0, ma = 0.0, qa = 0.0;
-  for (int z = t; z < ntiles; z += 256) {
-    // tile partial: rows n, shift x0, sum of (v - x0), sum of (v - x0)^2
-    const float4 p = ((const float4*)st)[(long)z * C + c];
-    const double n = p.x, s1 = p.z;
-    if (n > 0.0) chan_merge(na, ma, qa, n, (double)p.y + s1 / n, fmax((double)p.w - s1 * s1 / n, 0.0));
+  __shared__ double sh[3][4][64];
+  const int cl = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + cl;
+  double N = 0.0, S1 = 0.0, S2 = 0.0;
+  if (c < C) {
+#pragma unroll 4
+    for (int r = q; r < nchunks; r += 4) {
+      const double* p = red + ((long)r * C + c) * 3;
+      N += p[0];
+      S1 += p[1];
+      S2 += p[2];
+    }
   }
-  sn[t] = na; sm[t] = ma; sq[t] = qa;
+  sh[0][q][cl] = N; sh[1][q][cl] = S1; sh[2][q][cl] = S2;
   __syncthreads();
-  for (int h = 128; h > 0; h >>= 1) {
-    if (t < h) {
-      double a = sn[t], b = sm[t], q = sq[t];
-      chan_merge(a, b, q, sn[t + h], sm[t + h], sq[t + h]);
-      sn[t] = a; sm[t] = b; sq[t] = q;
-    }
-    __syncthreads();
-  }
-  if (t == 0) {
-    const double M = sn[0], mean = sm[0];
-    const double var = M > 0.0 ? sq[0] / M : 0.0;
-    const double rstd = 1.0 / sqrt(var + (double)eps);
-    const double sc = (double)gamma[c] * rstd;
-    mean_o[c] = (float)mean;
-    rstd_o[c] = (float)rstd;
-    scale_o[c] = (float)sc;
-    shift_o[c] = (float)((double)beta[c] - mean * sc);
-    if (rm) {
-      rm[c] = (float)((1.0 - mom) * (double)rm[c] + mom * mean);
-      rv[c] = (float)((1.0 - mom) * (double)rv[c] + mom * (M > 1.0 ? sq[0] / (M - 1.0) : 0.0));
-    }
+  if (q != 0 || c >= C) return;
+  N = ((sh[0][0][cl] + sh[0][1][cl]) + sh[0][2][cl]) + sh[0][3][cl];
+  S1 = ((sh[1][0][cl] + sh[1][1][cl]) + sh[1][2][cl]) + sh[1][3][cl];
+  S2 = ((sh[2][0][cl] + sh[2][1][cl]) + sh[2][2][cl]) + sh[2][3][cl];
+  const double K = (double)((const float4*)st)[c].y;
+  const double m1 = S1 / N;
+  double var = S2 / N - m1 * m1;
+  if (var < 0.0) var = 0.0;
+  const double mean = K + m1;
+  const double rstd = 1.0 / sqrt(var + (double)eps);
+  const double sc = (double)gamma[c] * rstd;
+  mean_o[c] = (float)mean;
+  rstd_o[c] = (float)rstd;
+  scale_o[c] = (float)sc;
+  shift_o[c] = (float)((double)beta[c] - mean * sc);
+  if (rm) {
+    rm[c] = (float)((1.0 - mom) * (double)rm[c] + mom * mean);
+    rv[c] = (float)((1.0 - mom) * (double)rv[c] + mom * (N > 1.0 ? var * (N / (N - 1.0)) : 0.0));
   }
 }
 
@@ -535,11 +558,20 @@ int bn_bwd_apply_pool_launch(int prec, const void* dpool, const uint8_t* arg, co
   return ok();
 }
 
-int bn_stats_tiles_final_launch(const float* tile_stats, int ntiles, int C, const float* gamma, const float* beta,
-                                float eps, float momentum, float* run_mean, float* run_var, float* mean, float* rstd,
-                                float* scale, float* shift, hipStream_t s) {
-  hipLaunchKernelGGL(bn_stats_tiles_final_kernel, dim3(C), dim3(256), 0, s, tile_stats, ntiles, C, gamma, beta, eps,
-                     momentum, run_mean, run_var, mean, rstd, scale, shift);
+int bn_stats_tiles_chunks(int ntiles) {
+  int r = (ntiles + 63) / 64;
+  return r < 1 ? 1 : r > 64 ? 64 : r;
+}
+
+int bn_stats_tiles_final_launch(const float* tile_stats, int ntiles, int C, double* scratch, const float* gamma,
+                                const float* beta, float eps, float momentum, float* run_mean, float* run_var,
+                                float* mean, float* rstd, float* scale, float* shift, hipStream_t s) {
+  const int chunks = bn_stats_tiles_chunks(ntiles);
+  const int per_chunk = (ntiles + chunks - 1) / chunks;
+  hipLaunchKernelGGL(bn_stats_tiles_reduce_kernel, dim3((C + 63) / 64, chunks), dim3(256), 0, s, tile_stats, ntiles,
+                     C, per_chunk, scratch);
+  hipLaunchKernelGGL(bn_stats_tiles_final_kernel, dim3((C + 63) / 64), dim3(256), 0, s, tile_stats, scratch, chunks, C,
+                     gamma, beta, eps, momentum, run_mean, run_var, mean, rstd, scale, shift);
   return ok();
 }
 

@@ -67,6 +67,21 @@ template <> __device__ inline uint4 pack<bf16_t>(const float* f) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// Division by a runtime constant d >= 1 for numerators below 2^31, as a
+// multiply-high, an add and a shift (round-up multiplier of Granlund and
+// Montgomery): l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1,
+// n / d = (umulhi(n, m) + n) >> l.
+struct FastDiv {
+  uint32_t d, m, l;
+  FastDiv() : d(1), m(1), l(0) {}
+  explicit FastDiv(uint32_t dd) : d(dd ? dd : 1) {
+    l = 0;
+    while ((1ull << l) < d) ++l;
+    m = (uint32_t)((((1ull << 32) * ((1ull << l) - d)) / d) + 1);
+  }
+  __device__ inline uint32_t div(uint32_t n) const { return (__umulhi(n, m) + n) >> l; }
+};
+
 // Sticky device error bits.
 enum DevErr { DEVERR_LABEL = 1, DEVERR_NONFINITE = 2 };
 

@@ -198,8 +198,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
       const int m = m0 + j * 8 + (lane >> 3);
       ok[u] = m < g.M;
       const int mm = ok[u] ? m : 0;
-      const int n = mm / HWm, rem = mm - n * HWm;
-      const int i = rem / g.Wm, jj = rem - i * g.Wm;
+      const int n = (int)g.fd_hw.div(mm), rem = mm - n * HWm;
+      const int i = (int)g.fd_w.div(rem), jj = rem - i * g.Wm;
       hb[u] = i * g.is - g.ip;
       wb[u] = jj * g.is - g.ip;
       pix[u] = (n * g.Hin + hb[u]) * g.Win + wb[u];
@@ -234,13 +234,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
     const int lane_px = (c * VW) / g.Cin;              // pixel of this lane's chunk within a row
 #pragma unroll
     for (int u = 0; u < UA; ++u) {
-      uint32_t m = 0;
+      // valid tap rows x valid tap-group columns, as bit vectors
+      uint32_t vh = 0, vw = 0, m = 0;
       for (int th = 0; th < g.nth; ++th)
-        for (int tg = 0; tg < ntw_g; ++tg) {
-          const int h = hb[u] + g.dh0 + th * g.dhs, w = wb[u] + g.dw0 + (tg * RT + lane_px) * g.dws;
-          if (ok[u] && (unsigned)h < (unsigned)g.Hin && (unsigned)w < (unsigned)g.Win) m |= 1u << (th * ntw_g + tg);
-        }
-      umask[u] = m;
+        vh |= (unsigned)(hb[u] + g.dh0 + th * g.dhs) < (unsigned)g.Hin ? 1u << th : 0u;
+      for (int tg = 0; tg < ntw_g; ++tg)
+        vw |= (unsigned)(wb[u] + g.dw0 + (tg * RT + lane_px) * g.dws) < (unsigned)g.Win ? 1u << tg : 0u;
+      for (int th = 0; th < g.nth; ++th) m |= (vh >> th) & 1u ? vw << (th * ntw_g) : 0u;
+      umask[u] = ok[u] ? m : 0u;
       uoff[u] = (uint32_t)(pix[u] * g.Cin * es + c * 16);
     }
 #pragma unroll
@@ -381,8 +382,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
       const int row = idx / CPW, cc = idx - row * CPW;
       const int m = m0 + arow0 + i * 16 + row, col = n0 + brow0 + cc * VW;
       if (m >= g.M || col >= g.Cols) continue;
-      const int n = m / HWm, rem = m - n * HWm;
-      const int ii = rem / g.Wm, jj = rem - ii * g.Wm;
+      const int n = (int)g.fd_hw.div(m), rem = m - n * HWm;
+      const int ii = (int)g.fd_w.div(rem), jj = rem - ii * g.Wm;
       const long off = ((long)(n * g.Hout + ii * g.os + g.oph) * g.Wout + jj * g.os + g.opw) * g.Cols + col;
       float v[VW];
 #pragma unroll
@@ -833,39 +834,61 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g
 }
 
 // Sum of the split partials in a fixed order, written in OIHW order. A block
-// covers 64 consecutive (co, tap, ci) elements with 4 groups of 64 threads;
-// group q sums splits q, q+4, ... and the four sums are added in order, so
-// the result is deterministic and the split axis is read in parallel.
+// covers 256 consecutive (co, tap, ci) elements as 64 float4 columns with 4
+// groups of 64 threads; group q sums splits q, q+4, ... and the four sums are
+// added in order, so the result is deterministic and the split axis is read
+// in parallel with 16-byte loads.
+__device__ inline void wgrad_store(float* __restrict__ out, long idx, float sum, int KHW, int Cin, int Cin_real,
+                                   int s2d) {
+  const int ci = (int)(idx % Cin);
+  const long rest = idx / Cin;
+  const int tap = (int)(rest % KHW);
+  const int co = (int)(rest / KHW);
+  if (s2d) {
+    // 4x4 tap (a, b), channel (2*dy + dx)*3 + c  ->  7x7 tap (2a+dy-1, 2b+dx-1) of channel c
+    if (ci < 12) {
+      const int q = ci / 3, c = ci - 3 * q;
+      const int kh = 2 * (tap >> 2) + (q >> 1) - 1, kw = 2 * (tap & 3) + (q & 1) - 1;
+      if (kh >= 0 && kw >= 0) out[(((long)co * 3 + c) * 7 + kh) * 7 + kw] = sum;
+    }
+  } else if (ci < Cin_real) {
+    out[((long)co * Cin_real + ci) * KHW + tap] = sum;
+  }
+}
+
 __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ P, int splits, int Cout,
                                                            int KHW, int Cin, int Cin_real, float* __restrict__ out,
                                                            int s2d) {
-  __shared__ float part[4][64];
-  const long total = (long)Cout * KHW * Cin;
-  const long stride = total;
+  __shared__ float4 part[4][64];
+  const long total4 = (long)Cout * KHW * Cin / 4;   // Cin is a multiple of 4
   const int e = threadIdx.x & 63, q = threadIdx.x >> 6;
-  for (long base = blockIdx.x * 64l; base < total; base += (long)gridDim.x * 64) {
+  const float4* __restrict__ P4 = (const float4*)P;
+  for (long base = blockIdx.x * 64l; base < total4; base += (long)gridDim.x * 64) {
     const long idx = base + e;
-    float acc = 0.f;
-    if (idx < total)
-      for (int z = q; z < splits; z += 4) acc += P[z * stride + idx];
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (idx < total4) {
+      int z = q;
+      for (; z + 12 < splits; z += 16) {
+        const float4 a = P4[z * total4 + idx], b = P4[(z + 4) * total4 + idx];
+        const float4 c = P4[(z + 8) * total4 + idx], d = P4[(z + 12) * total4 + idx];
+        acc.x += a.x; acc.y += a.y; acc.z += a.z; acc.w += a.w;
+        acc.x += b.x; acc.y += b.y; acc.z += b.z; acc.w += b.w;
+        acc.x += c.x; acc.y += c.y; acc.z += c.z; acc.w += c.w;
+        acc.x += d.x; acc.y += d.y; acc.z += d.z; acc.w += d.w;
+      }
+      for (; z < splits; z += 4) {
+        const float4 a = P4[z * total4 + idx];
+        acc.x += a.x; acc.y += a.y; acc.z += a.z; acc.w += a.w;
+      }
+    }
     part[q][e] = acc;
     __syncthreads();
-    if (q == 0 && idx < total) {
-      const float sum = ((part[0][e] + part[1][e]) + part[2][e]) + part[3][e];
-      const int ci = (int)(idx % Cin);
-      const long rest = idx / Cin;
-      const int tap = (int)(rest % KHW);
-      const int co = (int)(rest / KHW);
-      if (s2d) {
-        // 4x4 tap (a, b), channel (2*dy + dx)*3 + c  ->  7x7 tap (2a+dy-1, 2b+dx-1) of channel c
-        if (ci < 12) {
-          const int q = ci / 3, c = ci - 3 * q;
-          const int kh = 2 * (tap >> 2) + (q >> 1) - 1, kw = 2 * (tap & 3) + (q & 1) - 1;
-          if (kh >= 0 && kw >= 0) out[(((long)co * 3 + c) * 7 + kh) * 7 + kw] = sum;
-        }
-      } else if (ci < Cin_real) {
-        out[((long)co * Cin_real + ci) * KHW + tap] = sum;
-      }
+    if (q == 0 && idx < total4) {
+      const float4 a = part[0][e], b = part[1][e], c = part[2][e], d = part[3][e];
+      const float sum[4] = {((a.x + b.x) + c.x) + d.x, ((a.y + b.y) + c.y) + d.y, ((a.z + b.z) + c.z) + d.z,
+                            ((a.w + b.w) + c.w) + d.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) wgrad_store(out, idx * 4 + k, sum[k], KHW, Cin, Cin_real, s2d);
     }
     __syncthreads();
   }
@@ -906,6 +929,8 @@ bool gather_uniform(const ConvGather& g, int kt) {
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
 int launch_gather2(const ConvGather& g0, hipStream_t s) {
   ConvGather g = g0;
+  g.fd_hw = FastDiv((uint32_t)(g.Hm * g.Wm));
+  g.fd_w = FastDiv((uint32_t)g.Wm);
   g.zero = zero_page();
   if (!g.zero) return -4;
   const int tiles = ceil_div(g.M, BM) * ceil_div(g.Cols, BN);
@@ -1128,8 +1153,9 @@ int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s) {
 int wgrad_reduce_launch(const float* P, int splits, int Cout, int KHW, int Cin, int Cin_real,
                         float* out_oihw, int s2d, hipStream_t s) {
   if (s2d && (KHW != 16 || Cin != 16 || Cin_real != 3)) return -1;
-  const long total = (long)Cout * KHW * Cin;
-  int blocks = (int)((total + 63) / 64);
+  if (Cin % 4) return -1;
+  const long total4 = (long)Cout * KHW * Cin / 4;
+  int blocks = (int)((total4 + 63) / 64);
   if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, s, P, splits, Cout, KHW, Cin, Cin_real,
                      out_oihw, s2d);

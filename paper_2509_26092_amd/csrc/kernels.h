@@ -24,6 +24,7 @@ struct ConvGather {
   int wkh0, wkhs, wkw0, wkws, KW, KHW;  // weight tap (wkh0+th*wkhs)*KW + wkw0+tw*wkws
   int K;                     // nth*ntw*Cin
   int mode;                  // 0 store, 1 C += acc, 2 C = acc + (Rm>0 ? R : 0)
+  FastDiv fd_hw, fd_w;       // division by Hm*Wm and by Wm (set by the launcher)
   float* stats;              // optional BN partials (rows, shift, sum, sum sq) [tiles_m][Cols][4] of the stored output
   const void* zero;          // 16-byte zero page (set by the launcher)
 };
@@ -66,9 +67,11 @@ int wgrad_reduce_launch(const float* P, int splits, int Cout, int KHW, int Cin, 
 // partial sums of (y - pivot) and (y - pivot)^2 per block; pivot = y[0][c]
 // Batch statistics from the forward conv epilogue's per-tile partials
 // (rows, shift, sum of v - shift, sum of (v - shift)^2) [ntiles][C][4].
-int bn_stats_tiles_final_launch(const float* tile_stats, int ntiles, int C, const float* gamma, const float* beta,
-                                float eps, float momentum, float* run_mean, float* run_var, float* mean, float* rstd,
-                                float* scale, float* shift, hipStream_t s);
+// scratch: bn_stats_tiles_chunks(ntiles) * C * 3 doubles
+int bn_stats_tiles_chunks(int ntiles);
+int bn_stats_tiles_final_launch(const float* tile_stats, int ntiles, int C, double* scratch, const float* gamma,
+                                const float* beta, float eps, float momentum, float* run_mean, float* run_var,
+                                float* mean, float* rstd, float* scale, float* shift, hipStream_t s);
 // z = act(y*scale+shift [+ r] [+ (yd*scale2+shift2)])
 //  res_mode: 0 none, 1 identity residual r, 2 projected residual (yd, scale2, shift2)
 int bn_apply_launch(int prec, const void* y, const float* scale, const float* shift, int relu,
