@@ -56,6 +56,12 @@ int rn18op_maxpool_fwd(int prec, const void* x, void* y, uint8_t* arg, int N, in
 int rn18op_maxpool_bwd(int prec, const void* dy, const uint8_t* arg, void* dx, int N, int H, int W, int C,
                        void* hip_stream);
 
+/* fp32 -> bf16 storage rounding exactly as every bf16 kernel stores values:
+ * round to nearest, ties to even (binary32 -> bfloat16; a NaN stays a NaN).
+ * x: n fp32, y: n uint16 bf16 bit patterns, n a multiple of 8, 16-byte
+ * aligned device pointers. The oracle's rounding points assume this rule. */
+int rn18op_round_bf16(const float* x, uint16_t* y, size_t n, void* hip_stream);
+
 /* Debugging aids (not part of the training path).
  * rn18_debug_set(ctx, RN18_DBG_STOP_BLOCKS, k): later train steps end their
  * backward pass after k residual blocks (no stem backward, no SGD update);

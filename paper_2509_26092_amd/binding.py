@@ -25,7 +25,7 @@ EXPORTED = [
     "rn18_set_momentum", "rn18_destroy", "rn18_last_error", "rn18_profile_enable", "rn18_profile_read",
     "rn18op_conv2d_fwd", "rn18op_conv2d_dgrad", "rn18op_conv2d_wgrad_workspace", "rn18op_conv2d_wgrad",
     "rn18op_maxpool_fwd", "rn18op_maxpool_bwd", "rn18_debug_set", "rn18_debug_copy",
-    "rn18_debug_capture",
+    "rn18_debug_capture", "rn18op_round_bf16",
 ]
 
 
@@ -86,6 +86,7 @@ def lib():
         "rn18op_conv2d_wgrad": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _Z, _P]),
         "rn18op_maxpool_fwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _P]),
         "rn18op_maxpool_bwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _P]),
+        "rn18op_round_bf16": (_I, [_P, _P, _Z, _P]),
         "rn18_debug_set": (_I, [_P, _I, ctypes.c_long]),
         "rn18_profile_enable": (_I, [_P, _I]),
         "rn18_profile_read": (_I, [_P, ctypes.POINTER(rn18_prof_rec), _I, ctypes.POINTER(_I)]),
@@ -219,6 +220,10 @@ def rn18op_maxpool_fwd(prec, x, y, arg, N, H, W, C, stream=None):
 
 def rn18op_maxpool_bwd(prec, dy, arg, dx, N, H, W, C, stream=None):
     return _check(lib().rn18op_maxpool_bwd(prec, _ptr(dy), _ptr(arg), _ptr(dx), N, H, W, C, _stream(stream)))
+
+
+def rn18op_round_bf16(x, y, n, stream=None):
+    return _check(lib().rn18op_round_bf16(_ptr(x), _ptr(y), n, _stream(stream)))
 
 
 DBG = dict(y=0, z1=1, out=2, gA=3, gB=4, gz=5, gy=6, gyd=7, grad=8, wf=9, wd=10, mean=11, rstd=12, zstem=13,

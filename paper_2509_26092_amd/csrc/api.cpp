@@ -1137,4 +1137,11 @@ int rn18op_maxpool_bwd(int prec, const void* dy, const uint8_t* arg, void* dx, i
   return RN18_OK;
 }
 
+int rn18op_round_bf16(const float* x, uint16_t* y, size_t n, void* stream) {
+  if (!x || !y || !aligned16(x) || !aligned16(y)) return fail(RN18_EINVAL, "bad pointer");
+  if (n % 8 || n > (size_t)1 << 40) return fail(RN18_EINVAL, "n must be a multiple of 8");
+  LCHK(round_bf16_launch(x, y, (long)n, (hipStream_t)stream));
+  return RN18_OK;
+}
+
 }  // extern "C"

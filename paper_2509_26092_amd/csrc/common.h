@@ -14,13 +14,14 @@ typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
 enum Prec { PREC_F32 = 0, PREC_BF16 = 1 };
 
-// Round-to-nearest-even float -> bf16 on the binary32 bit pattern; NaN stays
-// a quiet NaN.
-__device__ __host__ inline bf16_t f2bf(float f) {
-  uint32_t u = __builtin_bit_cast(uint32_t, f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float floatx2_t __attribute__((ext_vector_type(2)));
+
+// Round-to-nearest-even float -> bf16 (gfx950 v_cvt_pk_bf16_f32; a NaN stays
+// a NaN).
+__device__ inline bf16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+__device__ inline uint32_t f2bf2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2_t{lo, hi}, bf16x2_t));
 }
 __device__ __host__ inline float bf2f(bf16_t b) {
   return __builtin_bit_cast(float, ((uint32_t)b) << 16);
@@ -63,7 +64,7 @@ template <> __device__ inline uint4 pack<float>(const float* f) {
 template <> __device__ inline uint4 pack<bf16_t>(const float* f) {
   uint32_t w[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(f[2 * i]) | ((uint32_t)f2bf(f[2 * i + 1]) << 16);
+  for (int i = 0; i < 4; ++i) w[i] = f2bf2(f[2 * i], f[2 * i + 1]);
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 

@@ -384,7 +384,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
       if (m >= g.M || col >= g.Cols) continue;
       const int n = (int)g.fd_hw.div(m), rem = m - n * HWm;
       const int ii = (int)g.fd_w.div(rem), jj = rem - ii * g.Wm;
-      const long off = ((long)(n * g.Hout + ii * g.os + g.oph) * g.Wout + jj * g.os + g.opw) * g.Cols + col;
+      const uint32_t off = ((uint32_t)((n * g.Hout + ii * g.os + g.oph) * g.Wout + jj * g.os + g.opw)) * g.Cols + col;
       float v[VW];
 #pragma unroll
       for (int e = 0; e < VW; ++e) v[e] = Ws[row * WSTR + cc * VW + e];
@@ -931,6 +931,7 @@ int launch_gather2(const ConvGather& g0, hipStream_t s) {
   ConvGather g = g0;
   g.fd_hw = FastDiv((uint32_t)(g.Hm * g.Wm));
   g.fd_w = FastDiv((uint32_t)g.Wm);
+  if ((long)g.N * g.Hout * g.Wout * g.Cols >= (1l << 31)) return -1;  // 32-bit output offsets
   g.zero = zero_page();
   if (!g.zero) return -4;
   const int tiles = ceil_div(g.M, BM) * ceil_div(g.Cols, BN);

@@ -113,6 +113,8 @@ int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, 
 // mode 1: the 7x7 stride-2 stem (Cin 3) as a 4x4 conv over its 2x2
 // space-to-depth input: [Cout][4x4][16], channel (2*dy + dx)*3 + c.
 struct RepackEntry { long src; long dst_f; long dst_d; int Cout, Cin, Cin_p, KHW; long n; long nprefix; int mode, pad_; };
+// y = bf16(x), round to nearest even, as every kernel stores bf16 (n multiple of 8)
+int round_bf16_launch(const float* x, uint16_t* y, long n, hipStream_t s);
 int repack_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* table_dev,
                   int nentries, long total, hipStream_t s);
 int maxpool_fwd_launch(int prec, const void* x, void* y, uint8_t* arg, int N, int H, int W, int C,

@@ -350,6 +350,15 @@ __global__ void delta_kernel(const float* __restrict__ a, const float* __restric
   for (long i = (n4 << 2) + blockIdx.x * 256l + threadIdx.x; i < n; i += (long)gridDim.x * 256) d[i] = a[i] - b[i];
 }
 
+__global__ void round_bf16_kernel(const float* __restrict__ x, bf16_t* __restrict__ y, long nchunks) {
+  for (long q = blockIdx.x * 256l + threadIdx.x; q < nchunks; q += (long)gridDim.x * 256) {
+    float v[8];
+    unpack<float>(((const uint4*)x)[2 * q], v);
+    unpack<float>(((const uint4*)x)[2 * q + 1], v + 4);
+    ((uint4*)y)[q] = pack<bf16_t>(v);
+  }
+}
+
 __global__ void fill_zero_kernel(uint32_t* __restrict__ p, long nwords) {
   for (long i = blockIdx.x * 256l + threadIdx.x; i < nwords; i += (long)gridDim.x * 256) p[i] = 0u;
 }
@@ -372,6 +381,12 @@ int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, 
     hipLaunchKernelGGL(ingest_s2d_kernel<bf16_t>, dim3(grid_for(npix)), dim3(256), 0, s, img, (bf16_t*)x, npix, H, W);
   else
     hipLaunchKernelGGL(ingest_s2d_kernel<float>, dim3(grid_for(npix)), dim3(256), 0, s, img, (float*)x, npix, H, W);
+  return ok();
+}
+
+int round_bf16_launch(const float* x, uint16_t* y, long n, hipStream_t s) {
+  if (n % 8) return -1;
+  hipLaunchKernelGGL(round_bf16_kernel, dim3(grid_for(n / 8)), dim3(256), 0, s, x, (bf16_t*)y, n / 8);
   return ok();
 }
 

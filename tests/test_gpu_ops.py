@@ -174,3 +174,33 @@ def test_conv_every_kernel_configuration(prec):
     finally:
         B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 0)
         B.rn18_debug_set(None, B.RN18_DBG_WGRAD_CONFIG, 0)
+
+
+def test_bf16_storage_rounding_matches_oracle():
+    """The kernels' fp32 -> bf16 storage rounding (hardware conversion) is
+    bit-identical to the oracle's round-to-nearest-even on the binary32
+    pattern: random values over the whole exponent range, exact ties (odd and
+    even), values just around ties, signed zeros, subnormals, the bf16 overflow
+    boundary and infinities."""
+    import torch
+    from oracle.ops import round_bf16
+    rng = np.random.default_rng(7)
+    bits = [rng.integers(0, 2 ** 32, 200000, dtype=np.uint64).astype(np.uint32)]
+    hi = rng.integers(0, 2 ** 16, 20000, dtype=np.uint64).astype(np.uint32) << 16
+    for low in (0x8000, 0x7FFF, 0x8001, 0x0000, 0xFFFF):
+        bits.append(hi | low)
+    bits.append(np.array([0, 0x80000000, 1, 0x807FFFFF, 0x7F7FFFFF, 0x7F7F8000, 0x7F7F7FFF, 0x7F800000, 0xFF800000,
+                          0x00800000, 0x3F808000, 0x3F818000], dtype=np.uint32))
+    u = np.concatenate(bits)
+    u = u[(u & 0x7FFFFFFF) <= 0x7F800000]              # NaN payloads are not compared
+    u = u[: len(u) // 8 * 8]
+    x = u.view(np.float32)
+    xd = torch.from_numpy(x.copy()).cuda()
+    yd = torch.empty(len(x), dtype=torch.int16, device="cuda")
+    B.rn18op_round_bf16(xd, yd, len(x))
+    torch.cuda.synchronize()
+    got = yd.cpu().numpy().view(np.uint16)
+    ref = (round_bf16(x.astype(np.float64)).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    bad = np.nonzero(got != ref)[0]
+    assert bad.size == 0, "first mismatches: %s" % [(hex(int(u[i])), hex(int(got[i])), hex(int(ref[i])))
+                                                    for i in bad[:5]]
