@@ -14,6 +14,7 @@ by the library around each launch, on the stream the kernels run on, in a
 separate profiled step (the timed steps run without events).
 """
 import argparse
+import re
 import hashlib
 import json
 import os
@@ -97,15 +98,27 @@ def roofline(by_sym, prec, traffic_lookup):
             "share_of_kernel_time": None}
 
 
+KERNEL_SOURCES = os.path.join(ROOT, "paper_2509_26092_amd", "csrc")
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+CALIB_FLOATS = 1 << 26   # ps_worker_delta over 2^26 floats: reads 512 MiB, writes 256 MiB
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(KERNEL_SOURCES)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(KERNEL_SOURCES, name), "rb").read())
+    return h.hexdigest()
+
+
 def traffic_lookup_factory():
-    """HBM bytes per launch measured with rocprofv3 FETCH_SIZE/WRITE_SIZE, if a
-    committed measurement exists for the current conv kernel source."""
-    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-    src = os.path.join(ROOT, "paper_2509_26092_amd", "csrc", "conv.hip")
+    """HBM bytes per launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE,
+    if a committed measurement exists for the current kernel sources."""
     try:
-        with open(path) as f:
+        with open(TRAFFIC_JSON) as f:
             tab = json.load(f)
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        sha = kernel_source_sha()
     except (OSError, ValueError):
         return lambda name: None
 
@@ -115,6 +128,47 @@ def traffic_lookup_factory():
             return None
         return e.get("bytes_per_launch")
     return look
+
+
+def short_kernel_name(n):
+    n = n.replace("rn18::(anonymous namespace)::", "").replace("unsigned short", "bf16").replace("void ", "")
+    return re.sub(r"\(.*\)$", "", n)
+
+
+def ingest_counters(fetch_csv, write_csv, command):
+    """Per-kernel HBM bytes per dispatch from two rocprofv3 --pmc runs of the
+    same command (FETCH_SIZE, then WRITE_SIZE, in KiB per dispatch), each
+    scaled by what the counter reads for ps_worker_delta over 2^26 floats
+    (a copy-like kernel of known traffic: 512 MiB read, 256 MiB written)."""
+    import csv
+    import collections
+    def load(path, counter):
+        out = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == counter:
+                out[short_kernel_name(r["Kernel_Name"])].append((int(r["Grid_Size"]), float(r["Counter_Value"])))
+        return out
+    fetch, write = load(fetch_csv, "FETCH_SIZE"), load(write_csv, "WRITE_SIZE")
+    calib_grid = None
+    cal_f = [v for g, v in fetch.get("delta_kernel", []) if v > 100000]
+    cal_w = [v for g, v in write.get("delta_kernel", []) if v > 100000]
+    if not cal_f or not cal_w:
+        raise SystemExit("no calibration dispatch (run the counter passes with --calibrate)")
+    kf = (2.0 * CALIB_FLOATS * 4 / 1024) / (sum(cal_f) / len(cal_f))   # true KiB per counted KiB
+    kw = (1.0 * CALIB_FLOATS * 4 / 1024) / (sum(cal_w) / len(cal_w))
+    kernels = {}
+    for name in sorted(set(fetch) & set(write)):
+        if name == "delta_kernel":
+            continue
+        f = sum(v for _, v in fetch[name]) / len(fetch[name]) * kf * 1024
+        w = sum(v for _, v in write[name]) / len(write[name]) * kw * 1024
+        kernels[name] = {"dispatches": len(fetch[name]), "fetch_bytes_per_launch": round(f),
+                         "write_bytes_per_launch": round(w), "bytes_per_launch": round(f + w)}
+    tab = {"source_sha256": kernel_source_sha(), "command": command,
+           "fetch_scale": round(kf, 4), "write_scale": round(kw, 4), "kernels": kernels}
+    with open(TRAFFIC_JSON, "w") as f:
+        json.dump(tab, f, indent=1, sort_keys=True)
+    return tab
 
 
 def run_shape(B, torch, inputs, arch, classes, prec, N, H, steps, warmup, seed=1):
@@ -191,10 +245,20 @@ def main():
     ap.add_argument("--headline-only", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=40)
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/hbm_traffic.json from the counter_collection.csv files of a FETCH_SIZE "
+                         "and a WRITE_SIZE rocprofv3 --pmc run of this script with --calibrate, then exit")
+    ap.add_argument("--traffic-command", default="",
+                    help="the command the counter runs used, recorded with --traffic-from")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run ps_worker_delta over 2^26 floats (reads 512 MiB, writes 256 MiB) as the "
                          "known-size kernel that scales HBM counters")
     args = ap.parse_args()
+    if args.traffic_from:
+        tab = ingest_counters(args.traffic_from[0], args.traffic_from[1], args.traffic_command)
+        print(json.dumps({"fetch_scale": tab["fetch_scale"], "write_scale": tab["write_scale"],
+                          "kernels": len(tab["kernels"])}))
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (the parameter-server merge is "
               "simulated on one GPU); run with --gpus 1", file=sys.stderr)
@@ -236,7 +300,7 @@ def main():
                           "hybrid_rounds": rounds})
 
     if args.calibrate:
-        n = 1 << 26
+        n = CALIB_FLOATS
         a, b, d = (torch.ones(n, device="cuda") for _ in range(3))
         for _ in range(3):
             B.ps_worker_delta(a, b, d, n)
