@@ -322,21 +322,26 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
     }
     const uint4* As = smem + (s % STAGES) * STAGE_U4;
     const uint4* Bs = As + BM * 8;
+    // both 64-byte halves of the stage's rows are read before any MFMA, so
+    // the second half's LDS latency hides behind the first half's MFMAs
+    uint4 a[2][FM], b[2][FN];
 #pragma unroll
     for (int kg = 0; kg < 2; ++kg) {
       const int slot = (kg * 4 + (lane >> 4)) ^ sw;
-      uint4 a[FM], b[FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i) a[i] = As[(arow0 + i * 16 + (lane & 15)) * 8 + slot];
+      for (int i = 0; i < FM; ++i) a[kg][i] = As[(arow0 + i * 16 + (lane & 15)) * 8 + slot];
 #pragma unroll
-      for (int j = 0; j < FN; ++j) b[j] = Bs[(brow0 + j * 16 + (lane & 15)) * 8 + slot];
+      for (int j = 0; j < FN; ++j) b[kg][j] = Bs[(brow0 + j * 16 + (lane & 15)) * 8 + slot];
+    }
+    __builtin_amdgcn_sched_barrier(0);   // keep every LDS read ahead of the MFMAs
+#pragma unroll
+    for (int kg = 0; kg < 2; ++kg)
 #pragma unroll
       for (int tt = 0; tt < Mma<T>::SUB; ++tt)
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
-          for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], a[i], b[j], tt);
-    }
+          for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], a[kg][i], b[kg][j], tt);
   }
   wait_vmcnt<0>();
   __syncthreads();
@@ -798,24 +803,29 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g
     barrier_only();
     if (s + STAGES - 1 < S) issue((s + STAGES - 1) % STAGES);
     const lds_char_t* st = lds + (s % STAGES) * STAGE_B;
+    // every operand read of the stage issues before its MFMAs, so later
+    // k-steps' LDS latency hides behind earlier k-steps' MFMAs
+    typename O::frag_t a[O::KSTEPS][FM], b[O::KSTEPS][FN];
 #pragma unroll
     for (int kk = 0; kk < O::KSTEPS; ++kk) {
-      typename O::frag_t a[FM], b[FN];
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const int ch = wm * WTM + i * 16;
-        a[i] = O::frag(st + (ch / CPS) * SUB_B, ch % CPS, kk, lane);
+        a[kk][i] = O::frag(st + (ch / CPS) * SUB_B, ch % CPS, kk, lane);
       }
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int ch = wn * WTN + j * 16;
-        b[j] = O::frag(st + (SA + ch / CPS) * SUB_B, ch % CPS, kk, lane);
+        b[kk][j] = O::frag(st + (SA + ch / CPS) * SUB_B, ch % CPS, kk, lane);
       }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < O::KSTEPS; ++kk)
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) O::mma(acc[i][j], a[i], b[j]);
-    }
+        for (int j = 0; j < FN; ++j) O::mma(acc[i][j], a[kk][i], b[kk][j]);
   }
   wait_vmcnt<0>();
 
