@@ -171,6 +171,40 @@ def ingest_counters(fetch_csv, write_csv, command):
     return tab
 
 
+def counters_summary(csv_path, title, command):
+    """Markdown table of a rocprofv3 --pmc run's SQ counters per kernel
+    (averaged over its dispatches). With SQ_VALU_MFMA_BUSY_CYCLES and
+    SQ_BUSY_CYCLES the MFMA busy share of the shader engines' SIMDs (32 per
+    engine) is added."""
+    import csv
+    import collections
+    per = collections.defaultdict(lambda: collections.defaultdict(list))
+    for r in csv.DictReader(open(csv_path)):
+        per[short_kernel_name(r["Kernel_Name"])][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    names = sorted({c for v in per.values() for c in v})
+    lines = ["# %s" % title, "", "Command (from the repository root on the MI355X box, after "
+             "`cd /tmp && export TMPDIR=/tmp`):", "", "```", command, "```", "",
+             "Per-dispatch averages; MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (SQ_BUSY_CYCLES x 32 SIMDs per "
+             "shader engine).", ""]
+    head = ["kernel", "dispatches"] + names + (["MFMA busy"] if "SQ_VALU_MFMA_BUSY_CYCLES" in names else [])
+    lines.append("| " + " | ".join(head) + " |")
+    lines.append("|---|" + "---:|" * (len(head) - 1))
+    rows = []
+    for k, cs in per.items():
+        if k.startswith(("at::", "__amd")):
+            continue
+        avg = {c: sum(v) / len(v) for c, v in cs.items()}
+        n = len(next(iter(cs.values())))
+        row = ["`%s`" % k, str(n)] + ["%.0f" % avg.get(c, float("nan")) for c in names]
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in names:
+            busy = avg.get("SQ_BUSY_CYCLES", 0)
+            row.append("%.3f" % (avg.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) / (busy * 32)) if busy else "")
+        rows.append((avg.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) * n, row))
+    for _, row in sorted(rows, key=lambda t: -t[0]):
+        lines.append("| " + " | ".join(row) + " |")
+    return "\n".join(lines) + "\n"
+
+
 def run_shape(B, torch, inputs, arch, classes, prec, N, H, steps, warmup, seed=1):
     w = B.Worker(arch, classes, prec)
     st = torch.zeros(w.n_state, device="cuda")
@@ -212,6 +246,42 @@ def merge_rate(B, torch, n, reps=20):
     return ms, 16.0 * n / ms / 1e6
 
 
+def dbl_plan(B, torch, inputs, by, merge_ms, steps):
+    """The dual-batch planner on this GPU's measured step times: per hybrid
+    resolution, a and b of t = a*x + b fitted over batches 64, B_L/2 and B_L
+    (Sec. 3.1); the ImageNet split for one small and three large workers at
+    k = 1.05 (Eqs. 4-6), B_S from Eq. 8, the factor d_S/d_L (Sec. 3.4); then a
+    step at the planned B_S, the measured per-worker epoch times (Eq. 7 says
+    they match) and a ratio-faithful round: one large step, the small worker's
+    steps per large step, two deltas and the merge."""
+    from paper_2509_26092_amd import planner
+    d, k, n_s, n_l = 1281167, 1.05, 1, 3
+    out = []
+    for r, bl in ((128, 1024), (160, 640), (192, 448), (224, 256)):
+        pts = [(64, by["imagenet_hybrid_bf16_S64_%d" % r]["ms_per_step"]),
+               (bl, by["imagenet_hybrid_bf16_L%d_%d" % (bl, r)]["ms_per_step"])]
+        half = run_shape(B, torch, inputs, "imagenet", 1000, "bf16", bl // 2, r, steps, 2)[0] * 1e3
+        pts.append((bl // 2, half))
+        a, b = planner.fit_linear([p[0] for p in pts], [p[1] for p in pts])
+        p = planner.plan(a, b, bl, k, d, n_s, n_l, "ratio", whole_images=True)
+        ts = run_shape(B, torch, inputs, "imagenet", 1000, "bf16", p["B_S"], r, steps, 2)[0] * 1e3
+        tl = pts[1][1]
+        spr = planner.steps_per_round(p)
+        t_round = tl + spr * ts + 3 * merge_ms
+        out.append({"resolution": r, "a_ms_per_image": round(a, 6), "b_ms": round(b, 4),
+                    "fit_points_ms": [[x, round(t, 4)] for x, t in pts],
+                    "B_L": bl, "B_S": p["B_S"], "d_L": p["d_L"], "d_S": round(p["d_S"], 1),
+                    "factor": round(p["factor"], 4), "small_step_ms": round(ts, 4),
+                    "small_step_predicted_ms": round(a * p["B_S"] + b, 4),
+                    "epoch_s_large_measured": round(tl * p["d_L"] / bl / 1e3, 2),
+                    "epoch_s_small_measured": round(ts * p["d_S"] / p["B_S"] / 1e3, 2),
+                    "small_steps_per_large_step": round(spr, 3),
+                    "round_ms": round(t_round, 3),
+                    "round_images_per_s": round((bl + spr * p["B_S"]) / t_round * 1e3, 1)})
+    return {"workload": "dbl_planner_imagenet_n4_k1.05", "n_S": n_s, "n_L": n_l, "k": k, "d": d,
+            "stages": out}
+
+
 def cpu_baseline(arch, classes, prec, H, n_img, seed=3):
     """The fp64 oracle's training step, timed on the host cores on a bounded
     sample of the workload (n_img images at the workload's resolution)."""
@@ -248,12 +318,20 @@ def main():
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/hbm_traffic.json from the counter_collection.csv files of a FETCH_SIZE "
                          "and a WRITE_SIZE rocprofv3 --pmc run of this script with --calibrate, then exit")
+    ap.add_argument("--counters-summary", nargs=3, metavar=("CSV", "OUT_MD", "TITLE"),
+                    help="write a per-kernel markdown summary of a rocprofv3 --pmc counter_collection.csv "
+                         "(the command recorded with --traffic-command), then exit")
     ap.add_argument("--traffic-command", default="",
                     help="the command the counter runs used, recorded with --traffic-from")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run ps_worker_delta over 2^26 floats (reads 512 MiB, writes 256 MiB) as the "
                          "known-size kernel that scales HBM counters")
     args = ap.parse_args()
+    if args.counters_summary:
+        csv_path, out_md, title = args.counters_summary
+        with open(out_md, "w") as f:
+            f.write(counters_summary(csv_path, title, args.traffic_command))
+        return
     if args.traffic_from:
         tab = ingest_counters(args.traffic_from[0], args.traffic_from[1], args.traffic_command)
         print(json.dumps({"fetch_scale": tab["fetch_scale"], "write_scale": tab["write_scale"],
@@ -298,6 +376,7 @@ def main():
         per_shape.append({"workload": "ps_dual_merge_imagenet_state", "elements": n_state,
                           "ms": round(mms, 4), "GBps": round(mgbs, 1), "hbm_frac": round(mgbs / HBM_PEAK, 4),
                           "hybrid_rounds": rounds})
+        per_shape.append(dbl_plan(B, torch, inputs, by, mms, args.shape_steps))
 
     if args.calibrate:
         n = CALIB_FLOATS
