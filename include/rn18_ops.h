@@ -72,7 +72,7 @@ int rn18op_round_bf16(const float* x, uint16_t* y, size_t n, void* hip_stream);
  * `index` the conv layer (forward order) or the residual block. */
 enum {
   RN18_DBG_STOP_BLOCKS = 0,
-  /* process-wide: force gather-conv kernel configuration `value` (1..22,
+  /* process-wide: force gather-conv kernel configuration `value` (1..45,
    * see conv.hip) for every forward / data-gradient launch; 0 = automatic.
    * ctx may be NULL for this key. For tuning and for testing every
    * configuration. */

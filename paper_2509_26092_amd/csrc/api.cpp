@@ -159,7 +159,7 @@ struct Plan {
   size_t f, logits, dlogits, df, rowloss, lossbuf;
   size_t gA, gB, gz, gy, gyd;
   size_t part, wpart, grad;
-  size_t bnst;                  // forward conv epilogue BN partials per tile (64 rows at least)
+  size_t bnst;                  // forward conv epilogue BN partials (one entry per 32 rows at most)
   size_t total;
 };
 
@@ -339,7 +339,7 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   pl->part = alloc((size_t)max_partC * 4);
   size_t max_bnst = 0;
   for (size_t li = 0; li < a.convs.size(); ++li) {
-    const size_t b = (size_t)ceil_div(pl->cp[li].M, 64) * a.convs[li].cout * 4 * 4;
+    const size_t b = (size_t)ceil_div(pl->cp[li].M, 32) * a.convs[li].cout * 4 * 4;
     if (b > max_bnst) max_bnst = b;
   }
   pl->bnst = alloc(max_bnst);
@@ -393,12 +393,16 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
     g.wkh0 = k - 1; g.wkhs = -1; g.wkw0 = k - 1; g.wkws = -1; g.KW = k; g.KHW = k * k;
     g.K = k * k * Cout;
     g.mode = mode;
-    const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(g), conv_gather_kernel_name(prec, g), 2.0 * g.M * creal * g.K, 0.0);
+    const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(prec, g), conv_gather_kernel_name(prec, g), 2.0 * g.M * creal * g.K, 0.0);
     const int r = conv_gather_launch(prec, g, st);
     prof_end(c, pi);
     return r;
   }
   if (s != 2) return -1;
+  // the four parity phases, launched together
+  ConvGather ph4[4];
+  int np = 0;
+  double flops = 0.0;
   for (int ph = 0; ph < 2; ++ph)
     for (int pw = 0; pw < 2; ++pw) {
       const int Hm = (H - ph + 1) / 2, Wm = (W - pw + 1) / 2;
@@ -422,12 +426,16 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
         if (mode == 1) continue;   // nothing to add
         g.nth = 1; g.ntw = 1;      // K = 0: the kernel writes acc = 0 (+ residual)
       }
-      const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(g), conv_gather_kernel_name(prec, g), 2.0 * g.M * creal * g.K, 0.0);
-      const int r = conv_gather_launch(prec, g, st);
-      prof_end(c, pi);
-      if (r) return r;
+      flops += 2.0 * g.M * creal * g.K;
+      ph4[np++] = g;
     }
-  return 0;
+  if (np == 0) return 0;
+  const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile_multi(prec, ph4, np),
+                            conv_gather_kernel_name_multi(prec, ph4, np),
+                            flops, 0.0);
+  const int r = conv_gather_launch_multi(prec, ph4, np, st);
+  prof_end(c, pi);
+  return r;
 }
 
 // s2d: the operands are the space-to-depth stem's (k = 4, Cin = 16) and the
@@ -521,14 +529,14 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     float* tstats = (float*)(ws + pl.bnst);
     if (train) g.stats = tstats;
     const double xb = (double)N * P.Hin * P.Win * P.cin * es, yb = (double)P.M * L.cout * es;
-    TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(g), conv_gather_kernel_name(prec, g), 2.0 * P.M * L.cout * L.k * L.k * L.cin,
+    TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(prec, g), conv_gather_kernel_name(prec, g), 2.0 * P.M * L.cout * L.k * L.k * L.cin,
           xb + yb + (double)L.cout * P.k * P.k * P.cin * es, conv_gather_launch(prec, g, st));
     float* mean = (float*)(ws + P.mean);
     float* rstd = (float*)(ws + P.rstd);
     float* sc = (float*)(ws + P.scale);
     float* sf = (float*)(ws + P.shift);
     if (train) {
-      const int ntiles = ceil_div(P.M, conv_gather_tile(g) / 1000);
+      const int ntiles = conv_gather_stat_entries(prec, g);
       TIMED(RN18_K_BN_STATS, li, 1, "bn_stats_tiles_reduce_kernel", 0.0, (double)ntiles * L.cout * 16,
             bn_stats_tiles_final_launch(tstats, ntiles, L.cout, (double*)(ws + pl.part), state_c + L.g,
                                         state_c + L.b, eps, mom,

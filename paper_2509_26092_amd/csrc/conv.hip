@@ -153,8 +153,8 @@ __device__ inline void wait_stage(int later_issued) {
   else wait_vmcnt<0>();
 }
 
-template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool UNI>
-__global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather g) {
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool UNI, bool RP>
+__device__ inline void gather_impl(const ConvGather& g) {
   constexpr int NW = WGM * WGN, NT = 64 * NW;
   constexpr int VW = TT<T>::VW;
   constexpr int KT = 128 / (int)sizeof(T);
@@ -304,14 +304,74 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
     for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
   const int S = (g.K + KT - 1) / KT;
+  const int arow0 = wm * WTM, brow0 = wn * WTN;
+  const int sw = lane & 7;
+  if constexpr (RP) {
+    // Register-prefetched loop: the operand fragments of stage s+1 are read
+    // from LDS while the MFMAs of stage s run from registers, and a ring
+    // buffer is refilled as soon as every wave has read it (before its
+    // MFMAs), so all STAGES buffers are in flight.
+    auto read_stage = [&](int s, uint4(&a)[2][FM], uint4(&b)[2][FN]) {
+      const uint4* As = smem + (s % STAGES) * STAGE_U4;
+      const uint4* Bs = As + BM * 8;
+#pragma unroll
+      for (int kg = 0; kg < 2; ++kg) {
+        const int slot = (kg * 4 + (lane >> 4)) ^ sw;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[kg][i] = As[(arow0 + i * 16 + (lane & 15)) * 8 + slot];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[kg][j] = Bs[(brow0 + j * 16 + (lane & 15)) * 8 + slot];
+      }
+    };
+    auto mma_regs = [&](const uint4(&a)[2][FM], const uint4(&b)[2][FN]) {
+#pragma unroll
+      for (int kg = 0; kg < 2; ++kg)
+#pragma unroll
+        for (int tt = 0; tt < Mma<T>::SUB; ++tt)
+#pragma unroll
+          for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], a[kg][i], b[kg][j], tt);
+    };
+    auto body = [&](int s, const uint4(&ac)[2][FM], const uint4(&bc)[2][FN], uint4(&an)[2][FM],
+                    uint4(&bn)[2][FN]) {
+      // stage s+1 must have landed; the stages after it may stay in flight
+      if (s + 1 < S) wait_stage<IPW>(min(STAGES - 2, S - 2 - s));
+      // this wave's reads of stage s are complete (s_waitcnt lgkmcnt(0))
+      __builtin_amdgcn_s_waitcnt(0xC07F);
+      barrier_only();
+      if (s + STAGES < S) {
+        if (UNI) issue_uni(s % STAGES);
+        else issue(s + STAGES, s % STAGES);
+      }
+      if (s + 1 < S) read_stage(s + 1, an, bn);
+      __builtin_amdgcn_sched_barrier(0);
+      mma_regs(ac, bc);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+#pragma unroll
+    for (int p = 0; p < STAGES; ++p)
+      if (p < S) {
+        if (UNI) issue_uni(p);
+        else issue(p, p);
+      }
+    uint4 a0[2][FM], b0[2][FN], a1[2][FM], b1[2][FN];
+    if (S > 0) {
+      wait_stage<IPW>(min(STAGES - 1, S - 1));
+      barrier_only();
+      read_stage(0, a0, b0);
+    }
+    for (int s = 0; s < S; s += 2) {
+      body(s, a0, b0, a1, b1);
+      if (s + 1 < S) body(s + 1, a1, b1, a0, b0);
+    }
+  } else {
 #pragma unroll
   for (int p = 0; p < STAGES - 1; ++p)
     if (p < S) {
       if (UNI) issue_uni(p);
       else issue(p, p);
     }
-  const int arow0 = wm * WTM, brow0 = wn * WTN;
-  const int sw = lane & 7;
   for (int s = 0; s < S; ++s) {
     const int later = min(STAGES - 2, S - 1 - s);
     wait_stage<IPW>(later);
@@ -342,6 +402,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], a[kg][i], b[kg][j], tt);
+  }
   }
   wait_vmcnt<0>();
   __syncthreads();
@@ -441,6 +502,555 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
     float4* out = (float4*)g.stats + ((long)(m0 / BM) * g.Cols + col);
     *out = make_float4((float)rows, Sh[cl], a1, a2);
   }
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool UNI>
+__global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather g) {
+  gather_impl<T, BM, BN, WGM, WGN, STAGES, UNI, false>(g);
+}
+// Blocks per CU that the LDS ring of a configuration allows (160 KB per CU),
+// and the waves per SIMD they make; the register allocation of the kernels
+// that use this is bounded to match.
+constexpr int gather_blocks_per_cu(int bm, int bn, int stages) {
+  const int b = 163840 / (stages * (bm + bn) * 128);
+  return b < 1 ? 1 : b > 4 ? 4 : b;
+}
+constexpr int gather_occupancy(int bm, int bn, int nw, int stages) {
+  const int w = gather_blocks_per_cu(bm, bn, stages) * nw / 4;
+  return w < 1 ? 1 : w > 8 ? 8 : w;
+}
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool UNI>
+__global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN, STAGES)) void conv_gather_rp_kernel(
+    ConvGather g) {
+  gather_impl<T, BM, BN, WGM, WGN, STAGES, UNI, true>(g);
+}
+
+// ---------------------------------------------------------------------------
+// Persistent gather conv. A grid of at most as many blocks as fit on the chip
+// walks a list of tiles (of up to four sub-problems of one launch, e.g. the
+// four parity phases of a stride-2 data gradient): block b takes logical
+// tiles b', b' + G, b' + 2G, ... (b' its XCD-contiguous slot). The K stages
+// of consecutive tiles form one stream through the LDS ring, so the first
+// stages of the next tile are loading while the current tile finishes its
+// MFMAs and its epilogue. The epilogue stages its strips in the ring buffer
+// of the stage consumed last, which no load targets until the next barrier.
+// Only the uniform row layout (whole 128-byte channel blocks per tap, or
+// whole groups of consecutive w taps) is handled here.
+// ---------------------------------------------------------------------------
+struct GatherSet {
+  ConvGather p[4];
+  int np;
+  int tile_begin[5];  // sub-problem i owns logical tiles [tile_begin[i], tile_begin[i+1])
+};
+
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
+__global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN, STAGES)) void conv_gather_ps_kernel(
+    GatherSet gs) {
+  constexpr int NW = WGM * WGN, NT = 64 * NW;
+  constexpr int VW = TT<T>::VW;
+  constexpr int KT = 128 / (int)sizeof(T);
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  constexpr int AI = BM / 8, BI = BN / 8;
+  constexpr int NI = AI + BI, IPW = NI / NW;
+  constexpr int UA = AI / NW;
+  constexpr int STAGE_U4 = (BM + BN) * 8;
+  constexpr int WSTR = WTN + 4;
+  constexpr int CPW = WTN / VW;
+  constexpr int EPI_F = NW * 16 * WSTR + BN + NW * WTN * 2;
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  static_assert(NI % NW == 0 && AI % NW == 0 && BN % 8 == 0, "whole load instructions per wave");
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+  static_assert(EPI_F * 4 <= STAGE_U4 * 16, "epilogue fits in one ring buffer");
+  static_assert(64 % CPW == 0, "lane chunk column fixed across strips");
+  __shared__ uint4 smem[STAGES * STAGE_U4];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave_u / WGN, wn = wave_u % WGN;
+  const int c = (lane & 7) ^ (lane >> 3);
+  const uint32_t smem_lds = lds_addr(smem);
+  const int G = gridDim.x;
+  const int slot = xcd_remap(blockIdx.x, G);
+  const int total = gs.tile_begin[gs.np];
+  const int es = (int)sizeof(T);
+  const int arow0 = wm * WTM, brow0 = wn * WTN;
+  const int sw = lane & 7;
+
+  // ---- issue side: the tile whose stages are being loaded
+  int is_tile = slot - G, is_s = 0, is_S = 0;
+  uint32_t uoff[IPW], umask[UA];
+  i32x4_t rsA, rsB;
+  int st_ti = 0, st_th = 0, st_tw = 0, st_cb = 0;
+  int q_dh0 = 0, q_dhs = 0, q_dw0 = 0, q_dws = 0, q_wkh0 = 0, q_wkhs = 0, q_wkw0 = 0, q_wkws = 0;
+  int q_KW = 0, q_Win = 0, q_Cin = 0, q_RT = 1, q_ntwg = 1, q_CB = 1;
+  auto find_prob = [&](int t) {
+    int pr = 0;
+    while (pr + 1 < gs.np && t >= gs.tile_begin[pr + 1]) ++pr;
+    return pr;
+  };
+  // advance the issue side to its next tile with at least one stage
+  auto next_issue_tile = [&]() -> bool {
+    for (;;) {
+      is_tile += G;
+      if (is_tile >= total) return false;
+      const ConvGather& g = gs.p[find_prob(is_tile)];
+      is_S = (g.K + KT - 1) / KT;
+      is_s = 0;
+      if (is_S == 0) continue;
+      const int pr = find_prob(is_tile);
+      const int lt = is_tile - gs.tile_begin[pr];
+      const int tiles_n = (g.Cols + BN - 1) / BN;
+      const int m0 = (lt / tiles_n) * BM, n0 = (lt - (lt / tiles_n) * tiles_n) * BN;
+      const int HWm = g.Hm * g.Wm;
+      q_dh0 = g.dh0; q_dhs = g.dhs; q_dw0 = g.dw0; q_dws = g.dws;
+      q_wkh0 = g.wkh0; q_wkhs = g.wkhs; q_wkw0 = g.wkw0; q_wkws = g.wkws;
+      q_KW = g.KW; q_Win = g.Win; q_Cin = g.Cin;
+      q_CB = g.Cin >= KT ? g.Cin / KT : 1;
+      q_RT = g.Cin < KT ? KT / g.Cin : 1;
+      q_ntwg = g.ntw / q_RT;
+      rsA = buffer_rsrc(g.A, (uint32_t)((long)g.N * g.Hin * g.Win * g.Cin * es));
+      rsB = buffer_rsrc(g.B, (uint32_t)((long)g.Cols * g.KHW * g.Cin * es));
+      const int lane_px = (c * VW) / g.Cin;
+#pragma unroll
+      for (int u = 0; u < UA; ++u) {
+        const int m = m0 + (wave_u + NW * u) * 8 + (lane >> 3);
+        const bool ok = m < g.M;
+        const int mm = ok ? m : 0;
+        const int n = (int)g.fd_hw.div(mm), rem = mm - n * HWm;
+        const int i = (int)g.fd_w.div(rem), jj = rem - i * g.Wm;
+        const int hb = i * g.is - g.ip, wb = jj * g.is - g.ip;
+        uint32_t vh = 0, vw = 0, msk = 0;
+        for (int th = 0; th < g.nth; ++th)
+          vh |= (unsigned)(hb + g.dh0 + th * g.dhs) < (unsigned)g.Hin ? 1u << th : 0u;
+        for (int tg = 0; tg < q_ntwg; ++tg)
+          vw |= (unsigned)(wb + g.dw0 + (tg * q_RT + lane_px) * g.dws) < (unsigned)g.Win ? 1u << tg : 0u;
+        for (int th = 0; th < g.nth; ++th) msk |= (vh >> th) & 1u ? vw << (th * q_ntwg) : 0u;
+        umask[u] = ok ? msk : 0u;
+        uoff[u] = (uint32_t)(((n * g.Hin + hb) * g.Win + wb) * g.Cin * es + c * 16);
+      }
+#pragma unroll
+      for (int u = UA; u < IPW; ++u) {
+        const int col = n0 + (wave_u + NW * u - AI) * 8 + (lane >> 3);
+        uoff[u] = col < g.Cols ? (uint32_t)((long)col * g.KHW * g.Cin * es + c * 16) : kOutOfRange;
+      }
+      st_ti = st_th = st_tw = st_cb = 0;
+      return true;
+    }
+  };
+  int n_issued = 0;
+  bool more = next_issue_tile();
+  // issue the next stage of the stream into its ring buffer; false when the stream has ended
+  auto issue_next = [&]() {
+    if (!more) return;
+    const int dh = q_dh0 + st_th * q_dhs, dw = q_dw0 + st_tw * q_RT * q_dws;
+    const int wt = (q_wkh0 + st_th * q_wkhs) * q_KW + q_wkw0 + st_tw * q_RT * q_wkws;
+    const uint32_t sa = (uint32_t)((dh * q_Win + dw) * q_Cin * es + st_cb * 128);
+    const uint32_t sb = (uint32_t)(wt * q_Cin * es + st_cb * 128);
+    const uint32_t base =
+        __builtin_amdgcn_readfirstlane(smem_lds + (uint32_t)((n_issued % STAGES) * STAGE_U4 * 16));
+#pragma unroll
+    for (int u = 0; u < UA; ++u) {
+      const uint32_t v = (umask[u] >> st_ti) & 1u ? uoff[u] + sa : kOutOfRange;
+      lds_dma16_buf(v, rsA, base + (uint32_t)((wave_u + NW * u) * 1024));
+    }
+#pragma unroll
+    for (int u = UA; u < IPW; ++u) {
+      const uint32_t v = uoff[u] == kOutOfRange ? kOutOfRange : uoff[u] + sb;
+      lds_dma16_buf(v, rsB, base + (uint32_t)((AI + wave_u + NW * (u - UA)) * 1024));
+    }
+    ++n_issued;
+    if (++st_cb == q_CB) {
+      st_cb = 0;
+      ++st_ti;
+      if (++st_tw == q_ntwg) { st_tw = 0; ++st_th; }
+    }
+    if (++is_s == is_S) more = next_issue_tile();
+  };
+
+  for (int p = 0; p < STAGES - 1; ++p) issue_next();
+
+  // ---- compute side
+  int q = 0;  // stages consumed so far
+  for (int tile = slot; tile < total; tile += G) {
+    const int pr = find_prob(tile);
+    const ConvGather& g = gs.p[pr];
+    const int S = (g.K + KT - 1) / KT;
+    floatx4_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < S; ++s, ++q) {
+      wait_stage<IPW>(n_issued - 1 - q);
+      barrier_only();
+      while (more && n_issued < q + STAGES) issue_next();
+      const uint4* As = smem + (q % STAGES) * STAGE_U4;
+      const uint4* Bs = As + BM * 8;
+      uint4 a[2][FM], b[2][FN];
+#pragma unroll
+      for (int kg = 0; kg < 2; ++kg) {
+        const int sl = (kg * 4 + (lane >> 4)) ^ sw;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) a[kg][i] = As[(arow0 + i * 16 + (lane & 15)) * 8 + sl];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[kg][j] = Bs[(brow0 + j * 16 + (lane & 15)) * 8 + sl];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kg = 0; kg < 2; ++kg)
+#pragma unroll
+        for (int tt = 0; tt < Mma<T>::SUB; ++tt)
+#pragma unroll
+          for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], a[kg][i], b[kg][j], tt);
+    }
+
+    // ---- epilogue of this tile, staged in the ring buffer of the last consumed stage
+    const int lt = tile - gs.tile_begin[pr];
+    const int tiles_n = (g.Cols + BN - 1) / BN;
+    const int tm = lt / tiles_n;
+    const int m0 = tm * BM, n0 = (lt - tm * tiles_n) * BN;
+    const int HWm = g.Hm * g.Wm;
+    float* E = (float*)(smem + ((q + STAGES - 1) % STAGES) * STAGE_U4);
+    float* Ws = E + wave_u * 16 * WSTR;
+    float* Sh = E + NW * 16 * WSTR;
+    float* Sp = Sh + BN;
+    T* __restrict__ Cg = (T*)g.C;
+    const bool stats = g.stats != nullptr;
+    barrier_only();  // every wave is done with the stage data in E
+    float ssh[VW], ss1[VW], ss2[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) ssh[e] = ss1[e] = ss2[e] = 0.f;
+    const int cc = lane % CPW;
+    if (stats) {
+      if (wm == 0 && lane < 16) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Sh[brow0 + j * 16 + lane] = TT<T>::to_f(TT<T>::from_f(acc[0][j][0]));
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      barrier_only();
+#pragma unroll
+      for (int e = 0; e < VW; ++e) ssh[e] = Sh[brow0 + cc * VW + e];
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Ws[(4 * (lane >> 4) + r) * WSTR + j * 16 + (lane & 15)] = acc[i][j][r];
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      for (int idx = lane; idx < 16 * CPW; idx += 64) {
+        const int row = idx / CPW;
+        const int m = m0 + arow0 + i * 16 + row, col = n0 + brow0 + cc * VW;
+        if (m >= g.M || col >= g.Cols) continue;
+        const int n = (int)g.fd_hw.div(m), rem = m - n * HWm;
+        const int ii = (int)g.fd_w.div(rem), jj = rem - ii * g.Wm;
+        const uint32_t off =
+            ((uint32_t)((n * g.Hout + ii * g.os + g.oph) * g.Wout + jj * g.os + g.opw)) * g.Cols + col;
+        float v[VW];
+#pragma unroll
+        for (int e = 0; e < VW; ++e) v[e] = Ws[row * WSTR + cc * VW + e];
+        if (g.mode == 1) {
+          float o[VW];
+          unpack<T>(*(const uint4*)(Cg + off), o);
+#pragma unroll
+          for (int e = 0; e < VW; ++e) v[e] += o[e];
+        } else if (g.mode == 2) {
+          float rr[VW], mk[VW];
+          unpack<T>(*(const uint4*)((const T*)g.R + off), rr);
+          unpack<T>(*(const uint4*)((const T*)g.Rm + off), mk);
+#pragma unroll
+          for (int e = 0; e < VW; ++e) v[e] += mk[e] > 0.f ? rr[e] : 0.f;
+        }
+        const uint4 pk = pack<T>(v);
+        *(uint4*)(Cg + off) = pk;
+        if (stats) {
+          float vr[VW];
+          unpack<T>(pk, vr);
+#pragma unroll
+          for (int e = 0; e < VW; ++e) {
+            const float d = vr[e] - ssh[e];
+            ss1[e] += d;
+            ss2[e] = __builtin_fmaf(d, d, ss2[e]);
+          }
+        }
+      }
+    }
+    if (stats) {
+      // lanes with the same chunk column hold the same channels: butterfly sum
+#pragma unroll
+      for (int d = CPW; d < 64; d <<= 1)
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          ss1[e] += __shfl_xor(ss1[e], d);
+          ss2[e] += __shfl_xor(ss2[e], d);
+        }
+      if (lane < CPW) {
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          Sp[(wave_u * WTN + lane * VW + e) * 2] = ss1[e];
+          Sp[(wave_u * WTN + lane * VW + e) * 2 + 1] = ss2[e];
+        }
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      barrier_only();
+      const int rows = min(BM, g.M - m0);
+      for (int cl = tid; cl < BN; cl += NT) {
+        const int col = n0 + cl;
+        if (col >= g.Cols) continue;
+        const int wn_c = cl / WTN, cw = cl - wn_c * WTN;
+        float a1 = 0.f, a2 = 0.f;
+        for (int wmi = 0; wmi < WGM; ++wmi) {
+          a1 += Sp[((wmi * WGN + wn_c) * WTN + cw) * 2];
+          a2 += Sp[((wmi * WGN + wn_c) * WTN + cw) * 2 + 1];
+        }
+        float4* out = (float4*)g.stats + ((long)tm * g.Cols + col);
+        *out = make_float4((float)rows, Sh[cl], a1, a2);
+      }
+    }
+  }
+  wait_vmcnt<0>();
+}
+
+// ---------------------------------------------------------------------------
+// Halo conv for the 64 -> 64 channel 3x3 stride-1 convolutions (bf16): the
+// forward pass and the data gradient of the first stage. The whole weight
+// matrix [64 columns][9 taps][64 channels] (72 KB) stays in LDS for the
+// launch. A tile is TH whole output rows of one image; its input patch,
+// (TH + 2) x (W + 2) pixels of 64 channels with a zero halo, is loaded once
+// into LDS and all nine taps read it at a fixed pixel offset, so every input
+// pixel crosses from L2 about (TH + 2)(W + 2) / (TH W) times instead of nine.
+// Patches are double-buffered: the next tile's patch loads while the current
+// one is multiplied. Each of the 4 waves owns 64 pixels x 64 columns; the
+// operand fragments of the next K step are read while the MFMAs of the
+// current one run. One block per CU (the LDS holds exactly the weights and
+// two patches of up to 352 pixels).
+// The MFMAs take the weights as their first operand, so a lane's
+// accumulators are 4 consecutive output channels of one pixel: the epilogue
+// stores them as 8-byte chunks straight from registers. The BN partial
+// statistics of the stored values accumulate per lane over all of a wave's
+// tiles and are reduced over the lanes once at the end: one statistics entry
+// per wave of the grid.
+// ---------------------------------------------------------------------------
+struct ConvHalo {
+  ConvGather g;
+  int TH;          // output rows per tile (divides Hm)
+  int PH, PW;      // patch rows and columns
+  int tiles_img;   // Hm / TH
+  int tiles;       // N * tiles_img
+};
+
+constexpr int HALO_PROWS = 352;  // patch rows (pixels) per buffer
+constexpr int HALO_WAVES = 4;    // statistics entries per tile
+
+__global__ __launch_bounds__(256, 1) void conv_halo_kernel(ConvHalo h) {
+  typedef bf16_t T;
+  constexpr int NW = HALO_WAVES, FM = 4, FN = 4;
+  constexpr int B_U4 = 9 * 64 * 8;                  // resident weights, uint4 units
+  constexpr int P_U4 = HALO_PROWS * 8;              // one patch buffer
+  constexpr int PI = HALO_PROWS / 8 / NW;           // patch load instructions per wave
+  constexpr int BI = 9 * 64 / 8 / NW;               // weight load instructions per wave
+  __shared__ uint4 smem[B_U4 + 2 * P_U4];
+  static_assert((B_U4 + 2 * P_U4) * 16 <= 163840, "LDS");
+  static_assert(HALO_PROWS % (8 * NW) == 0, "whole patch load instructions per wave");
+  const ConvGather& g = h.g;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = (lane & 7) ^ (lane >> 3);
+  const uint32_t smem_lds = lds_addr(smem);
+  const int rowb = g.Cin * 2;                        // 128 bytes per pixel or weight tap
+  const i32x4_t rsA = buffer_rsrc(g.A, (uint32_t)((long)g.N * g.Hin * g.Win * rowb));
+  const i32x4_t rsB = buffer_rsrc(g.B, (uint32_t)((long)g.Cols * g.KHW * rowb));
+  const int G = gridDim.x;
+  const int slot = xcd_remap(blockIdx.x, G);
+  const int npx = h.TH * g.Wm;                       // output pixels per tile
+
+  // weights: row r = tap * 64 + column, tap = th * 3 + tw in the walk order
+#pragma unroll
+  for (int u = 0; u < BI; ++u) {
+    const int r = (wave + NW * u) * 8 + (lane >> 3);
+    const int t = r >> 6, col = r & 63, th = t / 3, tw = t - th * 3;
+    const int wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
+    lds_dma16_buf((uint32_t)((col * g.KHW + wt) * rowb + c * 16), rsB,
+                  smem_lds + (uint32_t)((wave + NW * u) * 1024));
+  }
+  // patch load geometry of this lane: patch pixel -> input offset relative to
+  // the tile's first output row, and the patch row (for the row bounds check)
+  int prel[PI], prow[PI];
+#pragma unroll
+  for (int u = 0; u < PI; ++u) {
+    const int p = (wave + NW * u) * 8 + (lane >> 3);
+    const int pr = p / h.PW, pc = p - pr * h.PW;
+    const int ir = -g.ip + g.dh0 + pr, ic = -g.ip + g.dw0 + pc;   // input row (relative to i0) and column
+    const bool ok = p < h.PH * h.PW && (unsigned)ic < (unsigned)g.Win;
+    prel[u] = (ir * g.Win + ic) * rowb + c * 16;
+    prow[u] = ok ? ir : -0x40000000;
+  }
+  auto issue_patch = [&](int tile, int buf) {
+    const int n = tile / h.tiles_img, i0 = (tile - n * h.tiles_img) * h.TH;
+    const int base = (n * g.Hin + i0) * g.Win * rowb;
+    const uint32_t lbase = smem_lds + (uint32_t)((B_U4 + buf * P_U4) * 16);
+#pragma unroll
+    for (int u = 0; u < PI; ++u) {
+      const bool ok = (unsigned)(i0 + prow[u]) < (unsigned)g.Hin;
+      lds_dma16_buf(ok ? (uint32_t)(base + prel[u]) : kOutOfRange, rsA, lbase + (uint32_t)((wave + NW * u) * 1024));
+    }
+  };
+  // A operand rows of this lane: tile pixel q -> patch pixel of tap (0, 0)
+  int abase[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int q = wave * 64 + i * 16 + (lane & 15);
+    const int ti = q < npx ? (int)g.fd_w.div(q) : 0;
+    abase[i] = q < npx ? ti * h.PW + (q - ti * g.Wm) : 0;
+  }
+  const int sw = lane & 7;                           // weight rows: row & 7 == lane & 7
+  const int kq = lane >> 4;
+  const int chl = 4 * (lane >> 4);                   // first of this lane's 4 channels within a 16-column block
+  const int rows_w = min(64, max(0, npx - wave * 64));
+  T* __restrict__ Cg = (T*)g.C;
+
+  // running BN partial statistics of this lane's 16 channels over the wave's pixels
+  float s1[FN][4], s2[FN][4], sh[FN][4];
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s1[j][e] = s2[j][e] = sh[j][e] = 0.f;
+  bool have_shift = false;
+  int rows_acc = 0;
+
+  if (slot < h.tiles) issue_patch(slot, 0);
+  int buf = 0;
+  for (int tile = slot; tile < h.tiles; tile += G, buf ^= 1) {
+    wait_vmcnt<0>();
+    barrier_only();
+    if (tile + G < h.tiles) issue_patch(tile + G, buf ^ 1);
+    const uint4* P = smem + B_U4 + buf * P_U4;
+    // output addresses of this lane's pixels; the residual modes' loads are
+    // issued now and land while the tile is multiplied
+    const int n = tile / h.tiles_img, i0 = (tile - n * h.tiles_img) * h.TH;
+    const long m0 = ((long)n * g.Hm + i0) * g.Wm;    // GEMM row of the tile's first pixel
+    uint32_t obase[FM];
+    bool okq[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int q = wave * 64 + i * 16 + (lane & 15);
+      okq[i] = q < npx;
+      obase[i] = (uint32_t)((m0 + (okq[i] ? q : 0)) * g.Cols) + chl;
+    }
+    uint2 ld0[FM][FN], ld1[FM][FN];
+    if (g.mode == 1 || g.mode == 2) {
+      const T* src0 = g.mode == 1 ? (const T*)Cg : (const T*)g.R;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          ld0[i][j] = *(const uint2*)(src0 + obase[i] + j * 16);
+          ld1[i][j] = g.mode == 2 ? *(const uint2*)((const T*)g.Rm + obase[i] + j * 16) : make_uint2(0, 0);
+        }
+    }
+    // acc[i][j][r]: output channel j * 16 + chl + r of tile pixel wave * 64 + i * 16 + lane % 16
+    floatx4_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    // K step s = 2 * tap + half: tap (th, tw), channels [32 half, 32 half + 32)
+    auto read_step = [&](int s, uint4(&a)[FM], uint4(&b)[FN]) {
+      const int t = s >> 1, kg = s & 1, th = t / 3, tw = t - th * 3;
+      const int off = th * h.PW + tw;
+      const int ch = kg * 4 + kq;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int pix = abase[i] + off;
+        a[i] = P[pix * 8 + (ch ^ (pix & 7))];
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) b[j] = smem[(t * 64 + j * 16 + (lane & 15)) * 8 + (ch ^ sw)];
+    };
+    uint4 a0[FM], b0[FN], a1[FM], b1[FN];
+    read_step(0, a0, b0);
+#pragma unroll
+    for (int s = 0; s < 18; s += 2) {
+      read_step(s + 1, a1, b1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b0[j], a0[i], 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (s + 2 < 18) read_step(s + 2, a0, b0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b1[j], a1[i], 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // every wave must be done with this patch before the next one is loaded into it
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+
+    // ---- epilogue straight from registers
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        float x[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        if (g.mode == 1 || g.mode == 2) {
+          const uint32_t rw[2] = {ld0[i][j].x, ld0[i][j].y}, mw[2] = {ld1[i][j].x, ld1[i][j].y};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float rv = bf2f((bf16_t)(e & 1 ? rw[e >> 1] >> 16 : rw[e >> 1] & 0xffffu));
+            const float mv = bf2f((bf16_t)(e & 1 ? mw[e >> 1] >> 16 : mw[e >> 1] & 0xffffu));
+            x[e] += g.mode == 1 || mv > 0.f ? rv : 0.f;
+          }
+        }
+        const uint2 pk = make_uint2(f2bf2(x[0], x[1]), f2bf2(x[2], x[3]));
+        if (okq[i]) *(uint2*)(Cg + obase[i] + j * 16) = pk;
+        if (g.stats != nullptr) {
+          const float vr[4] = {bf2f((bf16_t)(pk.x & 0xffffu)), bf2f((bf16_t)(pk.x >> 16)),
+                               bf2f((bf16_t)(pk.y & 0xffffu)), bf2f((bf16_t)(pk.y >> 16))};
+          if (!have_shift && i == 0) {
+            // the wave's first pixel (of its first tile) is its statistics shift
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sh[j][e] = __shfl(vr[e], lane & 48, 64);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float d = okq[i] ? vr[e] - sh[j][e] : 0.f;
+            s1[j][e] += d;
+            s2[j][e] = __builtin_fmaf(d, d, s2[j][e]);
+          }
+        }
+      }
+    have_shift = true;
+    rows_acc += rows_w;
+  }
+  if (g.stats != nullptr && slot < h.tiles) {
+    // one entry per wave: its pixels over all of its tiles, shifted by the
+    // first one; the sums over the 16 pixels of a lane row are shuffled
+    // together, then each lane writes one channel
+    const int kk = lane & 15, jj = kk >> 2, rr = kk & 3;
+    float o1 = 0.f, o2 = 0.f, osh = 0.f;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float a1 = s1[j][r], a2 = s2[j][r];
+#pragma unroll
+        for (int dd = 1; dd < 16; dd <<= 1) {
+          a1 += __shfl_xor(a1, dd, 16);
+          a2 += __shfl_xor(a2, dd, 16);
+        }
+        if (j == jj && r == rr) { o1 = a1; o2 = a2; osh = sh[j][r]; }
+      }
+    float4* out = (float4*)g.stats + ((long)(blockIdx.x * NW + wave) * g.Cols + jj * 16 + chl + rr);
+    *out = rows_acc > 0 ? make_float4((float)rows_acc, osh, o1, o2) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  wait_vmcnt<0>();
 }
 
 // ---------------------------------------------------------------------------
@@ -936,7 +1546,7 @@ bool gather_uniform(const ConvGather& g, int kt) {
          (long)g.Cols * g.KHW * g.Cin * es < (1l << 31);
 }
 
-template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool RP>
 int launch_gather2(const ConvGather& g0, hipStream_t s) {
   ConvGather g = g0;
   g.fd_hw = FastDiv((uint32_t)(g.Hm * g.Wm));
@@ -947,28 +1557,116 @@ int launch_gather2(const ConvGather& g0, hipStream_t s) {
   const int tiles = ceil_div(g.M, BM) * ceil_div(g.Cols, BN);
   const int kt = 128 / (int)sizeof(T);
   const int nt = 64 * WGM * WGN;
-  if (gather_uniform(g, kt))
-    hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, true>), dim3(tiles), dim3(nt), 0, s, g);
-  else
-    hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, false>), dim3(tiles), dim3(nt), 0, s, g);
+  if constexpr (RP) {
+    if (gather_uniform(g, kt))
+      hipLaunchKernelGGL((conv_gather_rp_kernel<T, BM, BN, WGM, WGN, STAGES, true>), dim3(tiles), dim3(nt), 0, s, g);
+    else
+      hipLaunchKernelGGL((conv_gather_rp_kernel<T, BM, BN, WGM, WGN, STAGES, false>), dim3(tiles), dim3(nt), 0, s, g);
+  } else {
+    if (gather_uniform(g, kt))
+      hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, true>), dim3(tiles), dim3(nt), 0, s, g);
+    else
+      hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, false>), dim3(tiles), dim3(nt), 0, s, g);
+  }
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
-// Kernel configurations: id -> (BM, BN, waves along M, waves along N, stages).
-#define RN18_GATHER_CONFIGS(X)                                                                   \
-  X(1, 64, 32, 2, 2, 3) X(2, 64, 64, 2, 2, 3) X(3, 128, 64, 2, 2, 3) X(4, 128, 128, 2, 2, 3)     \
-  X(5, 256, 128, 4, 2, 3) X(6, 256, 128, 2, 2, 3) X(7, 256, 64, 4, 2, 3) X(8, 128, 128, 2, 4, 3) \
-  X(9, 256, 64, 4, 1, 3) X(10, 128, 128, 2, 2, 2) X(11, 256, 128, 4, 2, 2) X(12, 128, 64, 2, 2, 4) \
-  X(13, 128, 64, 2, 2, 2) X(14, 64, 64, 2, 2, 2) X(15, 256, 64, 4, 2, 2) X(16, 128, 128, 2, 4, 2) \
-  X(17, 256, 128, 2, 2, 2) X(18, 512, 64, 4, 1, 2) X(19, 256, 128, 2, 2, 3) X(20, 128, 128, 2, 2, 4) \
-  X(21, 256, 64, 4, 1, 2) X(22, 256, 64, 2, 2, 2)
-constexpr int kGatherCfgs = 22;
+int cu_count() {
+  static int n[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (!n[dev] && hipDeviceGetAttribute(&n[dev], hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n[dev] = 0;
+  return n[dev];
+}
+
+// One persistent launch over the tiles of np sub-problems (all of the uniform
+// row layout); -1 if one is not.
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
+int launch_gather_ps(const ConvGather* probs, int np, hipStream_t s) {
+  if (np < 1 || np > 4) return -1;
+  GatherSet gs{};
+  gs.np = np;
+  const int kt = 128 / (int)sizeof(T);
+  long total = 0;
+  for (int i = 0; i < np; ++i) {
+    ConvGather g = probs[i];
+    if (!gather_uniform(g, kt)) return -1;
+    if ((long)g.N * g.Hout * g.Wout * g.Cols >= (1l << 31)) return -1;  // 32-bit output offsets
+    g.fd_hw = FastDiv((uint32_t)(g.Hm * g.Wm));
+    g.fd_w = FastDiv((uint32_t)g.Wm);
+    g.zero = nullptr;
+    gs.p[i] = g;
+    gs.tile_begin[i] = (int)total;
+    if (g.M > 0) total += (long)ceil_div(g.M, BM) * ceil_div(g.Cols, BN);
+  }
+  if (total >= (1l << 30)) return -1;
+  gs.tile_begin[np] = (int)total;
+  if (total == 0) return 0;
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int occ = gather_blocks_per_cu(BM, BN, STAGES);  // registers are bounded to match
+  const int cus = cu_count();
+  if (cus < 1) return -4;
+  const long grid = total < (long)occ * cus ? total : (long)occ * cus;
+  hipLaunchKernelGGL((conv_gather_ps_kernel<T, BM, BN, WGM, WGN, STAGES>), dim3((unsigned)grid), dim3(NT), 0, s, gs);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+// Tile height of the halo kernel for a launch, or 0 when the launch is not
+// one it handles (bf16, 64 -> 64 channels, 3x3 taps walked forward with
+// stride 1, output rows = GEMM rows, whole-row tiles that divide the image).
+int halo_rows(int prec, const ConvGather& g) {
+  if (prec != PREC_BF16 || g.Cin != 64 || g.Cols != 64 || g.nth != 3 || g.ntw != 3 || g.KHW != 9 || g.K != 576)
+    return 0;
+  if (g.is != 1 || g.os != 1 || g.oph != 0 || g.opw != 0 || g.dhs != 1 || g.dws != 1) return 0;
+  if (g.Hout != g.Hm || g.Wout != g.Wm || g.Hm < 1 || g.Wm < 1) return 0;
+  if ((long)g.N * g.Hin * g.Win * 128 >= (1l << 31) || (long)g.N * g.Hout * g.Wout * g.Cols >= (1l << 31)) return 0;
+  // at least 128 pixels per tile keeps the per-wave statistics entries at
+  // most one per 32 GEMM rows
+  for (int th = g.Hm; th >= 1; --th)
+    if (g.Hm % th == 0 && th * g.Wm <= 256 && th * g.Wm >= 128 && (th + 2) * (g.Wm + 2) <= HALO_PROWS) return th;
+  return 0;
+}
+
+int launch_halo(const ConvGather& g0, int th, hipStream_t s) {
+  ConvHalo h{};
+  h.g = g0;
+  h.g.fd_hw = FastDiv((uint32_t)(g0.Hm * g0.Wm));
+  h.g.fd_w = FastDiv((uint32_t)g0.Wm);
+  h.TH = th;
+  h.PH = th + 2;
+  h.PW = g0.Wm + 2;
+  h.tiles_img = g0.Hm / th;
+  h.tiles = g0.N * h.tiles_img;
+  if (h.tiles <= 0) return 0;
+  const int cus = cu_count();
+  if (cus < 1) return -4;
+  const int grid = h.tiles < cus ? h.tiles : cus;
+  hipLaunchKernelGGL(conv_halo_kernel, dim3(grid), dim3(256), 0, s, h);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+// Kernel configurations: id -> (BM, BN, waves along M, waves along N, stages,
+// kind: 0 plain loop, 1 register-prefetched loop, 2 persistent).
+#define RN18_GATHER_CONFIGS(X)                                                                                  \
+  X(1, 64, 32, 2, 2, 3, 0) X(2, 64, 64, 2, 2, 3, 0) X(3, 128, 64, 2, 2, 3, 0) X(4, 128, 128, 2, 2, 3, 0)        \
+  X(5, 256, 128, 4, 2, 3, 0) X(6, 256, 128, 2, 2, 3, 0) X(7, 256, 64, 4, 2, 3, 0) X(8, 128, 128, 2, 4, 3, 0)    \
+  X(9, 256, 64, 4, 1, 3, 0) X(10, 128, 128, 2, 2, 2, 0) X(11, 256, 128, 4, 2, 2, 0) X(12, 128, 64, 2, 2, 4, 0)  \
+  X(13, 128, 64, 2, 2, 2, 0) X(14, 64, 64, 2, 2, 2, 0) X(15, 256, 64, 4, 2, 2, 0) X(16, 128, 128, 2, 4, 2, 0)   \
+  X(17, 256, 128, 2, 2, 2, 0) X(18, 512, 64, 4, 1, 2, 0) X(19, 256, 128, 2, 2, 3, 0) X(20, 128, 128, 2, 2, 4, 0) \
+  X(21, 256, 64, 4, 1, 2, 0) X(22, 256, 64, 2, 2, 2, 0) X(23, 128, 128, 2, 2, 2, 1) X(24, 256, 128, 4, 2, 2, 1) \
+  X(25, 256, 64, 4, 1, 2, 1) X(26, 128, 128, 2, 4, 2, 1) X(27, 256, 64, 4, 2, 2, 1) X(28, 256, 128, 4, 2, 3, 1)  \
+  X(29, 128, 128, 2, 2, 3, 1) X(30, 512, 64, 8, 1, 2, 1) X(31, 128, 256, 2, 4, 2, 1) X(32, 128, 64, 2, 2, 2, 1)  \
+  X(33, 64, 64, 2, 2, 2, 1) X(34, 256, 64, 4, 1, 3, 1) X(35, 256, 64, 4, 2, 2, 2) X(36, 128, 128, 2, 4, 2, 2)   \
+  X(37, 128, 64, 2, 2, 2, 2) X(38, 64, 64, 2, 2, 2, 2) X(39, 256, 128, 4, 2, 2, 2) X(40, 128, 128, 2, 2, 2, 2)  \
+  X(41, 128, 256, 2, 4, 2, 2) X(42, 128, 128, 2, 4, 3, 2) X(43, 256, 64, 4, 2, 3, 2) X(44, 128, 64, 2, 2, 3, 2)
+constexpr int kGatherCfgs = 44;
+constexpr int kGatherHalo = 45;  // the halo kernel where it applies, else the automatic choice
 int g_gather_override = 0;
 
-struct GatherCfg { int bm, bn, wgm, wgn, stages; };
+struct GatherCfg { int bm, bn, wgm, wgn, stages, kind; };
 constexpr GatherCfg kGather[kGatherCfgs + 1] = {
-    {0, 0, 0, 0, 0},
-#define RN18_X(id, bm, bn, wgm, wgn, st) {bm, bn, wgm, wgn, st},
+    {0, 0, 0, 0, 0, 0},
+#define RN18_X(id, bm, bn, wgm, wgn, st, kind) {bm, bn, wgm, wgn, st, kind},
     RN18_GATHER_CONFIGS(RN18_X)
 #undef RN18_X
 };
@@ -977,22 +1675,49 @@ constexpr GatherCfg kGather[kGatherCfgs + 1] = {
 // fp32 32x32 batch 128): two-stage rings with two or more blocks per CU beat
 // deeper rings with one block; 8-wave blocks for the large tiles.
 int gather_cfg(const ConvGather& g) {
-  if (g_gather_override) return g_gather_override;
+  if (g_gather_override && g_gather_override != kGatherHalo) return g_gather_override;
   if (g.Cols <= 32) return 1;
   if (g.Cols <= 64) return g.M >= 131072 ? 15 : g.M >= 65536 ? 13 : 14;
   return (long)ceil_div(g.M, 128) * ceil_div(g.Cols, 128) >= 256 ? 16 : 14;
 }
 
-int gather_tile(const ConvGather& g) {
+bool use_halo(int prec, const ConvGather& g) {
+  return (g_gather_override == 0 || g_gather_override == kGatherHalo) && halo_rows(prec, g) > 0;
+}
+
+int gather_tile(int prec, const ConvGather& g) {
+  if (use_halo(prec, g)) return halo_rows(prec, g) * g.Wm * 1000 + 64;
   const int id = gather_cfg(g);
   return id >= 1 && id <= kGatherCfgs ? kGather[id].bm * 1000 + kGather[id].bn : 0;
 }
 
+// The sub-problems of one launch share the configuration chosen for the
+// first; a persistent configuration takes them all in one grid when every
+// one has the uniform row layout, the others launch one grid each.
+// The parity phases of a stride-2 data gradient run in one persistent grid
+// (measured on MI355X at bf16 224x224 batch 256: 256x64 tiles for up to 64
+// columns, 128x128 for 128, 128x64 above).
+int gather_cfg_multi(const ConvGather* g, int np) {
+  if (g_gather_override || np < 2) return gather_cfg(g[0]);
+  return g[0].Cols <= 64 ? 35 : g[0].Cols <= 128 ? 36 : 37;
+}
+
 template <typename T>
-int gather_dispatch(const ConvGather& g, hipStream_t s) {
-  switch (gather_cfg(g)) {
-#define RN18_X(id, bm, bn, wgm, wgn, st) \
-  case id: return launch_gather2<T, bm, bn, wgm, wgn, st>(g, s);
+int gather_dispatch(const ConvGather* g, int np, hipStream_t s) {
+  const int prec = sizeof(T) == 2 ? PREC_BF16 : PREC_F32;
+  if (np == 1 && use_halo(prec, g[0])) return launch_halo(g[0], halo_rows(prec, g[0]), s);
+  switch (gather_cfg_multi(g, np)) {
+#define RN18_X(id, bm, bn, wgm, wgn, st, kind)                                               \
+  case id:                                                                                 \
+    if constexpr (kind == 2) {                                                             \
+      const int r = launch_gather_ps<T, bm, bn, wgm, wgn, st>(g, np, s);                   \
+      if (r != -1) return r;                                                               \
+    }                                                                                      \
+    for (int i = 0; i < np; ++i) {                                                         \
+      const int r = g[i].M > 0 ? launch_gather2<T, bm, bn, wgm, wgn, st, kind == 1>(g[i], s) : 0; \
+      if (r) return r;                                                                     \
+    }                                                                                      \
+    return 0;
     RN18_GATHER_CONFIGS(RN18_X)
 #undef RN18_X
     default: return -1;
@@ -1075,14 +1800,30 @@ const char* type_name(int prec) { return prec == PREC_BF16 ? "bf16" : "float"; }
 
 }  // namespace
 
+const char* gather_kernel_name(int prec, const ConvGather& g, int id);
+
 const char* conv_gather_kernel_name(int prec, const ConvGather& g) {
-  const int id = gather_cfg(g);
+  if (use_halo(prec, g)) return "conv_halo_kernel";
+  return gather_kernel_name(prec, g, gather_cfg(g));
+}
+
+const char* conv_gather_kernel_name_multi(int prec, const ConvGather* g, int np) {
+  if (np == 1) return conv_gather_kernel_name(prec, g[0]);
+  return gather_kernel_name(prec, g[0], gather_cfg_multi(g, np));
+}
+
+const char* gather_kernel_name(int prec, const ConvGather& g, int id) {
   if (id < 1 || id > kGatherCfgs) return "conv_gather2_kernel";
   const GatherCfg& c = kGather[id];
   const int kt = prec == PREC_BF16 ? 64 : 32;
   char buf[128];
-  snprintf(buf, sizeof buf, "conv_gather2_kernel<%s, %d, %d, %d, %d, %d, %s>", type_name(prec), c.bm, c.bn, c.wgm,
-           c.wgn, c.stages, gather_uniform(g, kt) ? "true" : "false");
+  if (c.kind == 2 && gather_uniform(g, kt))
+    snprintf(buf, sizeof buf, "conv_gather_ps_kernel<%s, %d, %d, %d, %d, %d>", type_name(prec), c.bm, c.bn, c.wgm,
+             c.wgn, c.stages);
+  else
+    snprintf(buf, sizeof buf, "%s<%s, %d, %d, %d, %d, %d, %s>",
+             c.kind == 1 ? "conv_gather_rp_kernel" : "conv_gather2_kernel", type_name(prec), c.bm, c.bn, c.wgm, c.wgn,
+             c.stages, gather_uniform(g, kt) ? "true" : "false");
   return intern_name(buf);
 }
 
@@ -1107,10 +1848,25 @@ const char* kernel_instance_name(const char* base, int prec) {
   return intern_name(std::string(base) + "<" + type_name(prec) + ">");
 }
 
-int conv_gather_tile(const ConvGather& g) { return gather_tile(g); }
+int conv_gather_tile(int prec, const ConvGather& g) { return gather_tile(prec, g); }
+
+int conv_gather_tile_multi(int prec, const ConvGather* g, int np) {
+  if (np == 1) return gather_tile(prec, g[0]);
+  const int id = gather_cfg_multi(g, np);
+  return id >= 1 && id <= kGatherCfgs ? kGather[id].bm * 1000 + kGather[id].bn : 0;
+}
+
+int conv_gather_stat_entries(int prec, const ConvGather& g) {
+  if (use_halo(prec, g)) {
+    const int tiles = g.N * (g.Hm / halo_rows(prec, g)), cus = cu_count();
+    return (tiles < cus ? tiles : cus) * HALO_WAVES;
+  }
+  const int bm = gather_tile(prec, g) / 1000;
+  return bm > 0 ? ceil_div(g.M, bm) : 0;
+}
 
 int conv_gather_override(int id) {
-  if (id < 0 || id > kGatherCfgs) return -1;
+  if (id < 0 || id > kGatherHalo) return -1;
   g_gather_override = id;
   return 0;
 }
@@ -1129,7 +1885,12 @@ int conv_wgrad_tile(int prec, int Cout, int Kcols) {
 
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s) {
   if (g.M <= 0) return 0;
-  return prec == PREC_BF16 ? gather_dispatch<bf16_t>(g, s) : gather_dispatch<float>(g, s);
+  return prec == PREC_BF16 ? gather_dispatch<bf16_t>(&g, 1, s) : gather_dispatch<float>(&g, 1, s);
+}
+
+int conv_gather_launch_multi(int prec, const ConvGather* g, int np, hipStream_t s) {
+  if (np < 1 || np > 4) return -1;
+  return prec == PREC_BF16 ? gather_dispatch<bf16_t>(g, np, s) : gather_dispatch<float>(g, np, s);
 }
 
 int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split) {

@@ -29,8 +29,15 @@ struct ConvGather {
   const void* zero;          // 16-byte zero page (set by the launcher)
 };
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s);
+// Up to four sub-problems of one operation (the parity phases of a stride-2
+// data gradient) with one configuration; persistent configurations run them
+// in a single grid.
+int conv_gather_launch_multi(int prec, const ConvGather* g, int np, hipStream_t s);
 // Tile configuration (BM*1000 + BN) the dispatcher picks for a launch.
-int conv_gather_tile(const ConvGather& g);
+int conv_gather_tile(int prec, const ConvGather& g);
+// Number of BN partial-statistics entries a forward launch with g.stats set
+// writes (at most one per 32 GEMM rows).
+int conv_gather_stat_entries(int prec, const ConvGather& g);
 // Force one kernel configuration for every gather launch (0 = automatic choice).
 int conv_gather_override(int id);
 
@@ -48,6 +55,8 @@ int conv_wgrad_tile(int prec, int Cout, int Kcols);
 // demangler prints them (namespace dropped, uint16_t storage shown as bf16);
 // kernel_instance_name(base, prec) is base<bf16> or base<float>.
 const char* conv_gather_kernel_name(int prec, const ConvGather& g);
+const char* conv_gather_kernel_name_multi(int prec, const ConvGather* g, int np);
+int conv_gather_tile_multi(int prec, const ConvGather* g, int np);
 const char* conv_wgrad_kernel_name(int prec, int Cout, int Kcols);
 const char* kernel_instance_name(const char* base, int prec);
 // Force one weight-gradient configuration (0 = automatic choice).

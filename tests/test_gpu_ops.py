@@ -161,7 +161,7 @@ def test_conv_every_kernel_configuration(prec):
     configuration, forced in turn, on a ragged stride-1 and a stride-2 shape."""
     cases = [(3, 64, 64, 13, 11, 128, 3, 1, 1), (2, 64, 64, 15, 15, 128, 3, 2, 1)]
     try:
-        for cfg in range(1, 23):
+        for cfg in range(1, 46):
             B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, cfg)
             for case in cases:
                 test_conv_fwd(prec, case)
@@ -174,6 +174,22 @@ def test_conv_every_kernel_configuration(prec):
     finally:
         B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 0)
         B.rn18_debug_set(None, B.RN18_DBG_WGRAD_CONFIG, 0)
+
+
+@pytest.mark.parametrize("case", [(2, 64, 64, 56, 56, 64, 3, 1, 1), (3, 64, 64, 13, 11, 64, 3, 1, 1),
+                                  (2, 64, 64, 28, 28, 64, 3, 1, 1), (1, 64, 64, 40, 40, 64, 3, 1, 1),
+                                  (2, 64, 64, 9, 50, 64, 3, 1, 1)], ids=case_id)
+def test_conv_halo(case):
+    """The halo kernel (64 -> 64 channel 3x3 stride-1 convs in bf16, weights
+    resident in LDS, one input patch per tile of whole output rows): forward
+    and data gradient against the oracle, with one and several tiles per
+    image and ragged widths."""
+    try:
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 45)
+        test_conv_fwd("bf16", case)
+        test_conv_dgrad("bf16", case)
+    finally:
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 0)
 
 
 def test_bf16_storage_rounding_matches_oracle():
