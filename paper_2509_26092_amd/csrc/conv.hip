@@ -818,16 +818,19 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
 // ---------------------------------------------------------------------------
 // Halo conv for the 64 -> 64 channel 3x3 stride-1 convolutions (bf16): the
 // forward pass and the data gradient of the first stage. The whole weight
-// matrix [64 columns][9 taps][64 channels] (72 KB) stays in LDS for the
-// launch. A tile is TH whole output rows of one image; its input patch,
-// (TH + 2) x (W + 2) pixels of 64 channels with a zero halo, is loaded once
-// into LDS and all nine taps read it at a fixed pixel offset, so every input
-// pixel crosses from L2 about (TH + 2)(W + 2) / (TH W) times instead of nine.
-// Patches are double-buffered: the next tile's patch loads while the current
-// one is multiplied. Each of the 4 waves owns 64 pixels x 64 columns; the
-// operand fragments of the next K step are read while the MFMAs of the
-// current one run. One block per CU (the LDS holds exactly the weights and
-// two patches of up to 352 pixels).
+// matrix [9 taps][64 columns][64 channels] (72 KB) stays in LDS for the
+// launch. A tile is up to TH whole output rows of one image (up to 512
+// pixels); its input patch, (TH + 2) x (W + 2) pixels with a zero halo, is
+// loaded into LDS one 32-channel half at a time and all nine taps read it
+// at a fixed pixel offset, so an input pixel crosses from L2 about
+// (TH + 2)(W + 2) / (TH W) times instead of nine. Half-patches are
+// double-buffered: the next one loads while the current one is multiplied.
+// Eight waves (two per SIMD, for LDS throughput) each own 64 pixels x 64
+// columns; the operand fragments of the next K step are read while the
+// MFMAs of the current one run.
+// LDS rows are swizzled so that the 16 consecutive rows of an MFMA operand
+// read hit distinct banks: 128-byte weight rows by (row / 2) mod 8, 64-byte
+// patch rows by (row / 4) mod 4.
 // The MFMAs take the weights as their first operand, so a lane's
 // accumulators are 4 consecutive output channels of one pixel: the epilogue
 // stores them as 8-byte chunks straight from registers. The BN partial
@@ -837,61 +840,65 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
 // ---------------------------------------------------------------------------
 struct ConvHalo {
   ConvGather g;
-  int TH;          // output rows per tile (divides Hm)
+  int TH;          // output rows per tile
   int PH, PW;      // patch rows and columns
-  int tiles_img;   // Hm / TH
+  int tiles_img;   // ceil(Hm / TH)
   int tiles;       // N * tiles_img
 };
 
-constexpr int HALO_PROWS = 352;  // patch rows (pixels) per buffer
-constexpr int HALO_WAVES = 4;    // statistics entries per tile
+constexpr int HALO_PROWS = 640;  // patch pixels per half-patch buffer
+constexpr int HALO_WAVES = 8;    // waves per block = statistics entries per block
+constexpr int HALO_BM = 64 * HALO_WAVES;
 
-__global__ __launch_bounds__(256, 1) void conv_halo_kernel(ConvHalo h) {
+template <int MODE, bool STATS>
+__global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo h) {
   typedef bf16_t T;
   constexpr int NW = HALO_WAVES, FM = 4, FN = 4;
-  constexpr int B_U4 = 9 * 64 * 8;                  // resident weights, uint4 units
-  constexpr int P_U4 = HALO_PROWS * 8;              // one patch buffer
-  constexpr int PI = HALO_PROWS / 8 / NW;           // patch load instructions per wave
-  constexpr int BI = 9 * 64 / 8 / NW;               // weight load instructions per wave
+  constexpr int B_U4 = 9 * 64 * 8;                  // resident weights, uint4 units (128-byte rows)
+  constexpr int P_U4 = HALO_PROWS * 4;              // one half-patch buffer (64-byte rows)
+  constexpr int PI = HALO_PROWS / 16 / NW;          // half-patch load instructions per wave (16 rows each)
+  constexpr int BI = 9 * 64 / 8 / NW;               // weight load instructions per wave (8 rows each)
   __shared__ uint4 smem[B_U4 + 2 * P_U4];
   static_assert((B_U4 + 2 * P_U4) * 16 <= 163840, "LDS");
-  static_assert(HALO_PROWS % (8 * NW) == 0, "whole patch load instructions per wave");
+  static_assert(HALO_PROWS % (16 * NW) == 0 && (9 * 64) % (8 * NW) == 0, "whole load instructions per wave");
   const ConvGather& g = h.g;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int c = (lane & 7) ^ (lane >> 3);
   const uint32_t smem_lds = lds_addr(smem);
   const int rowb = g.Cin * 2;                        // 128 bytes per pixel or weight tap
   const i32x4_t rsA = buffer_rsrc(g.A, (uint32_t)((long)g.N * g.Hin * g.Win * rowb));
   const i32x4_t rsB = buffer_rsrc(g.B, (uint32_t)((long)g.Cols * g.KHW * rowb));
   const int G = gridDim.x;
   const int slot = xcd_remap(blockIdx.x, G);
-  const int npx = h.TH * g.Wm;                       // output pixels per tile
 
-  // weights: row r = tap * 64 + column, tap = th * 3 + tw in the walk order
+  // weights: row r = tap * 64 + column (tap = th * 3 + tw in the walk
+  // order); the lane's 16 bytes go to slot lane % 8 and hold chunk
+  // (lane % 8) ^ ((r / 2) % 8)
 #pragma unroll
   for (int u = 0; u < BI; ++u) {
     const int r = (wave + NW * u) * 8 + (lane >> 3);
     const int t = r >> 6, col = r & 63, th = t / 3, tw = t - th * 3;
     const int wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
+    const int c = (lane & 7) ^ ((r >> 1) & 7);
     lds_dma16_buf((uint32_t)((col * g.KHW + wt) * rowb + c * 16), rsB,
                   smem_lds + (uint32_t)((wave + NW * u) * 1024));
   }
-  // patch load geometry of this lane: patch pixel -> input offset relative to
-  // the tile's first output row, and the patch row (for the row bounds check)
+  // half-patch load geometry: row p = patch pixel; the lane's 16 bytes go to
+  // slot lane % 4 and hold chunk (lane % 4) ^ ((p / 4) % 4) of the half
   int prel[PI], prow[PI];
 #pragma unroll
   for (int u = 0; u < PI; ++u) {
-    const int p = (wave + NW * u) * 8 + (lane >> 3);
+    const int p = (wave + NW * u) * 16 + (lane >> 2);
     const int pr = p / h.PW, pc = p - pr * h.PW;
     const int ir = -g.ip + g.dh0 + pr, ic = -g.ip + g.dw0 + pc;   // input row (relative to i0) and column
     const bool ok = p < h.PH * h.PW && (unsigned)ic < (unsigned)g.Win;
+    const int c = (lane & 3) ^ ((p >> 2) & 3);
     prel[u] = (ir * g.Win + ic) * rowb + c * 16;
     prow[u] = ok ? ir : -0x40000000;
   }
-  auto issue_patch = [&](int tile, int buf) {
+  auto issue_patch = [&](int tile, int half, int buf) {
     const int n = tile / h.tiles_img, i0 = (tile - n * h.tiles_img) * h.TH;
-    const int base = (n * g.Hin + i0) * g.Win * rowb;
+    const int base = (n * g.Hin + i0) * g.Win * rowb + half * 64;
     const uint32_t lbase = smem_lds + (uint32_t)((B_U4 + buf * P_U4) * 16);
 #pragma unroll
     for (int u = 0; u < PI; ++u) {
@@ -904,14 +911,22 @@ __global__ __launch_bounds__(256, 1) void conv_halo_kernel(ConvHalo h) {
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     const int q = wave * 64 + i * 16 + (lane & 15);
-    const int ti = q < npx ? (int)g.fd_w.div(q) : 0;
-    abase[i] = q < npx ? ti * h.PW + (q - ti * g.Wm) : 0;
+    const int ti = (int)g.fd_w.div(q);
+    abase[i] = ti * h.PW + (q - ti * g.Wm);
   }
-  const int sw = lane & 7;                           // weight rows: row & 7 == lane & 7
   const int kq = lane >> 4;
   const int chl = 4 * (lane >> 4);                   // first of this lane's 4 channels within a 16-column block
-  const int rows_w = min(64, max(0, npx - wave * 64));
+  const int wsw = (lane >> 1) & 7;                   // weight rows: (row / 2) % 8 == (lane % 16) / 2
   T* __restrict__ Cg = (T*)g.C;
+  // output and residual operands as buffers: lanes of pixels beyond the tile
+  // use an out-of-range offset (loads read zeros, stores are dropped), so
+  // every tile issues the same number of vector memory instructions
+  const uint32_t out_bytes = (uint32_t)((long)g.N * g.Hout * g.Wout * g.Cols * 2);
+  const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, out_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsR = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(g.mode == 1 || !g.R ? (const void*)g.C : g.R), 0, out_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsRm =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(g.Rm ? g.Rm : (const void*)g.C), 0, out_bytes, 0x00020000);
 
   // running BN partial statistics of this lane's 16 channels over the wave's pixels
   float s1[FN][4], s2[FN][4], sh[FN][4];
@@ -922,16 +937,69 @@ __global__ __launch_bounds__(256, 1) void conv_halo_kernel(ConvHalo h) {
   bool have_shift = false;
   int rows_acc = 0;
 
-  if (slot < h.tiles) issue_patch(slot, 0);
+  // phases: (tile, half) in order; phase k uses buffer k % 2
+  if (slot < h.tiles) issue_patch(slot, 0, 0);
   int buf = 0;
-  for (int tile = slot; tile < h.tiles; tile += G, buf ^= 1) {
-    wait_vmcnt<0>();
-    barrier_only();
-    if (tile + G < h.tiles) issue_patch(tile + G, buf ^ 1);
-    const uint4* P = smem + B_U4 + buf * P_U4;
-    // output addresses of this lane's pixels; the residual modes' loads are
-    // issued now and land while the tile is multiplied
+  for (int tile = slot; tile < h.tiles; tile += G) {
     const int n = tile / h.tiles_img, i0 = (tile - n * h.tiles_img) * h.TH;
+    const int npx = min(h.TH, g.Hm - i0) * g.Wm;    // output pixels of this tile
+    floatx4_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int half = 0; half < 2; ++half, buf ^= 1) {
+      // this half-patch has landed. Vector memory operations complete in
+      // issue order; after the first half of a tile was requested, only the
+      // previous tile's epilogue issued vector memory instructions: its
+      // residual loads (consumed there) and exactly FM * FN stores, which
+      // may stay in flight.
+      if (half == 0 && tile != slot) wait_vmcnt<FM * FN>();
+      else wait_vmcnt<0>();
+      barrier_only();
+      if (half == 0) issue_patch(tile, 1, buf ^ 1);
+      else if (tile + G < h.tiles) issue_patch(tile + G, 0, buf ^ 1);
+      const uint4* P = smem + B_U4 + buf * P_U4;
+      // K step t: tap t (th, tw), this half's 32 channels
+      auto read_step = [&](int t, uint4(&a)[FM], uint4(&b)[FN]) {
+        const int th = t / 3, tw = t - th * 3;
+        const int off = th * h.PW + tw;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const int pix = abase[i] + off;
+          a[i] = P[pix * 4 + (kq ^ ((pix >> 2) & 3))];
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) b[j] = smem[(t * 64 + j * 16 + (lane & 15)) * 8 + ((half * 4 + kq) ^ wsw)];
+      };
+      uint4 a0[FM], b0[FN], a1[FM], b1[FN];
+      read_step(0, a0, b0);
+#pragma unroll
+      for (int t = 0; t < 9; t += 2) {
+        if (t + 1 < 9) read_step(t + 1, a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b0[j], a0[i], 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (t + 1 < 9) {
+          if (t + 2 < 9) read_step(t + 2, a0, b0);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b1[j], a1[i], 0);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+    // every wave must be done with the patch buffers before they are reloaded
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+
+    // ---- epilogue straight from registers; the residual operands of modes
+    // 1 and 2 are all requested before the first is used
     const long m0 = ((long)n * g.Hm + i0) * g.Wm;    // GEMM row of the tile's first pixel
     uint32_t obase[FM];
     bool okq[FM];
@@ -941,76 +1009,40 @@ __global__ __launch_bounds__(256, 1) void conv_halo_kernel(ConvHalo h) {
       okq[i] = q < npx;
       obase[i] = (uint32_t)((m0 + (okq[i] ? q : 0)) * g.Cols) + chl;
     }
-    uint2 ld0[FM][FN], ld1[FM][FN];
-    if (g.mode == 1 || g.mode == 2) {
-      const T* src0 = g.mode == 1 ? (const T*)Cg : (const T*)g.R;
+    typedef int i32x2_t __attribute__((ext_vector_type(2)));
+    i32x2_t ld0[MODE ? FM : 1][FN], ld1[MODE == 2 ? FM : 1][FN];
+    if constexpr (MODE != 0) {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          ld0[i][j] = *(const uint2*)(src0 + obase[i] + j * 16);
-          ld1[i][j] = g.mode == 2 ? *(const uint2*)((const T*)g.Rm + obase[i] + j * 16) : make_uint2(0, 0);
+          const uint32_t ob = okq[i] ? (obase[i] + j * 16) * 2 : kOutOfRange;
+          ld0[i][j] = __builtin_amdgcn_raw_buffer_load_b64(rsR, ob, 0, 0);
+          if constexpr (MODE == 2) ld1[i][j] = __builtin_amdgcn_raw_buffer_load_b64(rsRm, ob, 0, 0);
         }
     }
-    // acc[i][j][r]: output channel j * 16 + chl + r of tile pixel wave * 64 + i * 16 + lane % 16
-    floatx4_t acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-    // K step s = 2 * tap + half: tap (th, tw), channels [32 half, 32 half + 32)
-    auto read_step = [&](int s, uint4(&a)[FM], uint4(&b)[FN]) {
-      const int t = s >> 1, kg = s & 1, th = t / 3, tw = t - th * 3;
-      const int off = th * h.PW + tw;
-      const int ch = kg * 4 + kq;
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int pix = abase[i] + off;
-        a[i] = P[pix * 8 + (ch ^ (pix & 7))];
-      }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) b[j] = smem[(t * 64 + j * 16 + (lane & 15)) * 8 + (ch ^ sw)];
-    };
-    uint4 a0[FM], b0[FN], a1[FM], b1[FN];
-    read_step(0, a0, b0);
-#pragma unroll
-    for (int s = 0; s < 18; s += 2) {
-      read_step(s + 1, a1, b1);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b0[j], a0[i], 0);
-      __builtin_amdgcn_sched_barrier(0);
-      if (s + 2 < 18) read_step(s + 2, a0, b0);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b1[j], a1[i], 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // every wave must be done with this patch before the next one is loaded into it
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-
-    // ---- epilogue straight from registers
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         float x[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-        if (g.mode == 1 || g.mode == 2) {
-          const uint32_t rw[2] = {ld0[i][j].x, ld0[i][j].y}, mw[2] = {ld1[i][j].x, ld1[i][j].y};
+        if constexpr (MODE != 0) {
+          const uint32_t rw[2] = {(uint32_t)ld0[i][j].x, (uint32_t)ld0[i][j].y};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const float rv = bf2f((bf16_t)(e & 1 ? rw[e >> 1] >> 16 : rw[e >> 1] & 0xffffu));
-            const float mv = bf2f((bf16_t)(e & 1 ? mw[e >> 1] >> 16 : mw[e >> 1] & 0xffffu));
-            x[e] += g.mode == 1 || mv > 0.f ? rv : 0.f;
+            if constexpr (MODE == 2) {
+              const uint32_t mw = (uint32_t)(e >> 1 ? ld1[i][j].y : ld1[i][j].x);
+              x[e] += bf2f((bf16_t)(e & 1 ? mw >> 16 : mw & 0xffffu)) > 0.f ? rv : 0.f;
+            } else {
+              x[e] += rv;
+            }
           }
         }
         const uint2 pk = make_uint2(f2bf2(x[0], x[1]), f2bf2(x[2], x[3]));
-        if (okq[i]) *(uint2*)(Cg + obase[i] + j * 16) = pk;
-        if (g.stats != nullptr) {
+        __builtin_amdgcn_raw_buffer_store_b64(i32x2_t{(int)pk.x, (int)pk.y}, rsC,
+                                              okq[i] ? (obase[i] + j * 16) * 2 : kOutOfRange, 0, 0);
+        if constexpr (STATS) {
           const float vr[4] = {bf2f((bf16_t)(pk.x & 0xffffu)), bf2f((bf16_t)(pk.x >> 16)),
                                bf2f((bf16_t)(pk.y & 0xffffu)), bf2f((bf16_t)(pk.y >> 16))};
           if (!have_shift && i == 0) {
@@ -1026,10 +1058,12 @@ __global__ __launch_bounds__(256, 1) void conv_halo_kernel(ConvHalo h) {
           }
         }
       }
-    have_shift = true;
-    rows_acc += rows_w;
+    if (wave * 64 < npx) {
+      have_shift = true;
+      rows_acc += min(64, npx - wave * 64);
+    }
   }
-  if (g.stats != nullptr && slot < h.tiles) {
+  if (STATS && slot < h.tiles) {
     // one entry per wave: its pixels over all of its tiles, shifted by the
     // first one; the sums over the 16 pixels of a lane row are shuffled
     // together, then each lane writes one channel
@@ -1619,12 +1653,16 @@ int halo_rows(int prec, const ConvGather& g) {
     return 0;
   if (g.is != 1 || g.os != 1 || g.oph != 0 || g.opw != 0 || g.dhs != 1 || g.dws != 1) return 0;
   if (g.Hout != g.Hm || g.Wout != g.Wm || g.Hm < 1 || g.Wm < 1) return 0;
+  if (g.mode < 0 || g.mode > 2 || (g.mode != 0 && g.stats)) return 0;
   if ((long)g.N * g.Hin * g.Win * 128 >= (1l << 31) || (long)g.N * g.Hout * g.Wout * g.Cols >= (1l << 31)) return 0;
-  // at least 128 pixels per tile keeps the per-wave statistics entries at
-  // most one per 32 GEMM rows
-  for (int th = g.Hm; th >= 1; --th)
-    if (g.Hm % th == 0 && th * g.Wm <= 256 && th * g.Wm >= 128 && (th + 2) * (g.Wm + 2) <= HALO_PROWS) return th;
-  return 0;
+  // as many whole rows as fit 512 pixels and a 640-pixel patch; at least
+  // 256 pixels per tile keeps the per-wave statistics entries (8 per block,
+  // blocks <= tiles) at most one per 32 GEMM rows
+  int th = HALO_BM / g.Wm;
+  if (th > g.Hm) th = g.Hm;
+  while (th > 0 && (th + 2) * (g.Wm + 2) > HALO_PROWS) --th;
+  if (th < 1 || th * g.Wm < 256) return 0;
+  return th;
 }
 
 int launch_halo(const ConvGather& g0, int th, hipStream_t s) {
@@ -1635,13 +1673,19 @@ int launch_halo(const ConvGather& g0, int th, hipStream_t s) {
   h.TH = th;
   h.PH = th + 2;
   h.PW = g0.Wm + 2;
-  h.tiles_img = g0.Hm / th;
+  h.tiles_img = (g0.Hm + th - 1) / th;
   h.tiles = g0.N * h.tiles_img;
   if (h.tiles <= 0) return 0;
   const int cus = cu_count();
   if (cus < 1) return -4;
   const int grid = h.tiles < cus ? h.tiles : cus;
-  hipLaunchKernelGGL(conv_halo_kernel, dim3(grid), dim3(256), 0, s, h);
+  const bool st = g0.stats != nullptr;
+  constexpr int NT = 64 * HALO_WAVES;
+  if (g0.mode == 0 && st) hipLaunchKernelGGL((conv_halo_kernel<0, true>), dim3(grid), dim3(NT), 0, s, h);
+  else if (g0.mode == 0) hipLaunchKernelGGL((conv_halo_kernel<0, false>), dim3(grid), dim3(NT), 0, s, h);
+  else if (g0.mode == 1 && !st) hipLaunchKernelGGL((conv_halo_kernel<1, false>), dim3(grid), dim3(NT), 0, s, h);
+  else if (g0.mode == 2 && !st) hipLaunchKernelGGL((conv_halo_kernel<2, false>), dim3(grid), dim3(NT), 0, s, h);
+  else return -1;
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
@@ -1686,7 +1730,7 @@ bool use_halo(int prec, const ConvGather& g) {
 }
 
 int gather_tile(int prec, const ConvGather& g) {
-  if (use_halo(prec, g)) return halo_rows(prec, g) * g.Wm * 1000 + 64;
+  if (use_halo(prec, g)) return HALO_BM * 1000 + 64;
   const int id = gather_cfg(g);
   return id >= 1 && id <= kGatherCfgs ? kGather[id].bm * 1000 + kGather[id].bn : 0;
 }
@@ -1803,7 +1847,11 @@ const char* type_name(int prec) { return prec == PREC_BF16 ? "bf16" : "float"; }
 const char* gather_kernel_name(int prec, const ConvGather& g, int id);
 
 const char* conv_gather_kernel_name(int prec, const ConvGather& g) {
-  if (use_halo(prec, g)) return "conv_halo_kernel";
+  if (use_halo(prec, g)) {
+    char buf[64];
+    snprintf(buf, sizeof buf, "conv_halo_kernel<%d, %s>", g.mode, g.stats ? "true" : "false");
+    return intern_name(buf);
+  }
   return gather_kernel_name(prec, g, gather_cfg(g));
 }
 
@@ -1858,7 +1906,8 @@ int conv_gather_tile_multi(int prec, const ConvGather* g, int np) {
 
 int conv_gather_stat_entries(int prec, const ConvGather& g) {
   if (use_halo(prec, g)) {
-    const int tiles = g.N * (g.Hm / halo_rows(prec, g)), cus = cu_count();
+    const int th = halo_rows(prec, g);
+    const int tiles = g.N * ((g.Hm + th - 1) / th), cus = cu_count();
     return (tiles < cus ? tiles : cus) * HALO_WAVES;
   }
   const int bm = gather_tile(prec, g) / 1000;
