@@ -622,21 +622,28 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
 
   auto W_d = [&](int li) { return (const char*)c->wd + (size_t)a.convs[li].wd * c->es; };
   // BN backward of conv li: dz (with mask mz) -> dy written to `dy`
+  // mz: the tensor whose sign is the ReLU mask, or RECOMPUTE when the mask is
+  // that of relu(bn(y)) of this layer itself (recomputed from y)
+  const size_t RECOMPUTE = ~(size_t)0;
   auto bn_back = [&](int li, size_t dz, size_t mz, size_t dy) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     int nblk = 0;
     float* part = (float*)(ws + pl.part);
     const double tb = (double)P.M * L.cout * es;
-    TIMED(RN18_K_BN_BWD_REDUCE, li, 0, kernel_instance_name("bn_bwd_partial_kernel", prec), 0.0, 3 * tb,
-          bn_bwd_partial_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.rstd), P.M,
-                                L.cout, part, &nblk, st));
+    const bool rc = mz == RECOMPUTE;
+    const void* mzp = rc ? nullptr : ws + mz;
+    const float* msc = rc ? (const float*)(ws + P.scale) : nullptr;
+    const float* msf = rc ? (const float*)(ws + P.shift) : nullptr;
+    TIMED(RN18_K_BN_BWD_REDUCE, li, 0, kernel_instance_name("bn_bwd_partial_kernel", prec), 0.0, (rc ? 2 : 3) * tb,
+          bn_bwd_partial_launch(prec, ws + dz, mzp, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.rstd), P.M,
+                                L.cout, part, &nblk, st, msc, msf));
     TIMED(RN18_K_BN_BWD_REDUCE, li, 1, "bn_bwd_final_kernel", 0.0, 0.0,
           bn_bwd_final_launch(part, nblk, P.M, L.cout, state + L.g, (float*)(ws + P.rstd), grad + L.g, grad + L.b,
                               (float*)(ws + P.coef), st));
-    TIMED(RN18_K_BN_BWD_APPLY, li, 0, kernel_instance_name("bn_bwd_apply_kernel", prec), 0.0, 4 * tb,
-          bn_bwd_apply_launch(prec, ws + dz, ws + mz, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.coef), ws + dy,
-                              P.M, L.cout, st));
+    TIMED(RN18_K_BN_BWD_APPLY, li, 0, kernel_instance_name("bn_bwd_apply_kernel", prec), 0.0, (rc ? 3 : 4) * tb,
+          bn_bwd_apply_launch(prec, ws + dz, mzp, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.coef), ws + dy,
+                              P.M, L.cout, st, msc, msf));
     if (!c->captures.empty()) return run_captures(c, RN18_CAP_DY, li, ws + dy, (size_t)P.M * L.cout * es);
     return 0;
   };
@@ -668,7 +675,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const size_t z1b = (size_t)pl.cp[B.c1].M * a.convs[B.c1].cout * es;
     const size_t inb = (size_t)N * pl.cp[B.c1].Hin * pl.cp[B.c1].Win * a.convs[B.c1].cin_p * es;
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DZ1, bi, ws + pl.gz, z1b))) return r;
-    if ((r = bn_back(B.c1, pl.gz, bp.z1, pl.gy))) return r;
+    if ((r = bn_back(B.c1, pl.gz, RECOMPUTE, pl.gy))) return r;
     if ((r = wgrad(B.c1, pl.gy))) return r;
     if (B.ds >= 0) {
       if ((r = dgrad(B.c1, pl.gy, gB, 0, 0, 0))) return r;
@@ -707,7 +714,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
           bn_bwd_apply_pool_launch(prec, ws + gA, parg, ws + P.y, sc, sf, (float*)(ws + P.mean),
                                    (float*)(ws + P.coef), ws + pl.gy, N, pl.Hs, pl.Ws, C0, pl.Hp, pl.Wp, st));
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DY, 0, ws + pl.gy, (size_t)P.M * C0 * es))) return r;
-  } else if ((r = bn_back(0, gA, pl.zstem, pl.gy))) {
+  } else if ((r = bn_back(0, gA, RECOMPUTE, pl.gy))) {
     return r;
   }
   if ((r = wgrad(0, pl.gy))) return r;

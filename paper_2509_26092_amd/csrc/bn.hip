@@ -116,6 +116,15 @@ __global__ __launch_bounds__(256) void bn_stats_tiles_final_kernel(const float* 
   }
 }
 
+// relu(bn(y)) as the forward pass stores it (rounded to the storage type):
+// the backward pass recomputes ReLU masks from y with this, so each mask
+// decision equals the one the stored activation encodes.
+template <typename T>
+__device__ inline float relu_stored(float y, float sc, float sf) {
+  const float t = bn_affine(y, sc, sf);
+  return TT<T>::to_f(TT<T>::from_f(t > 0.f ? t : 0.f));
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void bn_apply_kernel(const T* __restrict__ y, const float* __restrict__ scale,
                                                        const float* __restrict__ shift, int relu, int res_mode,
@@ -169,7 +178,9 @@ __global__ void bn_eval_coef_kernel(const float* gamma, const float* beta, const
 template <typename T>
 __global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict__ dz, const T* __restrict__ mz,
                                                              const T* __restrict__ y, const float* __restrict__ mean,
-                                                             const float* __restrict__ rstd, long M, int C,
+                                                             const float* __restrict__ rstd,
+                                                             const float* __restrict__ mscale,
+                                                             const float* __restrict__ mshift, long M, int C,
                                                              float* __restrict__ part) {
   constexpr int VW = TT<T>::VW;
   __shared__ float red[2][256 * VW];
@@ -178,11 +189,13 @@ __global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict
   const long rows_per_blk = (M + gridDim.x - 1) / gridDim.x;
   const long r_begin = blockIdx.x * rows_per_blk;
   const long r_end = min(M, r_begin + rows_per_blk);
-  float mu[VW], rs[VW], s1[VW], s2[VW];
+  float mu[VW], rs[VW], s1[VW], s2[VW], msc[VW], msf[VW];
 #pragma unroll
   for (int e = 0; e < VW; ++e) {
     mu[e] = mean[cg * VW + e];
     rs[e] = rstd[cg * VW + e];
+    msc[e] = mscale ? mscale[cg * VW + e] : 0.f;
+    msf[e] = mscale ? mshift[cg * VW + e] : 0.f;
     s1[e] = s2[e] = 0.f;
   }
   for (long r = r_begin + rr; r < r_end; r += rpi) {
@@ -195,6 +208,10 @@ __global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict
       unpack<T>(*(const uint4*)(mz + o), m);
 #pragma unroll
       for (int e = 0; e < VW; ++e) g[e] = m[e] > 0.f ? g[e] : 0.f;
+    } else if (mscale) {
+      // the ReLU mask of relu(bn(y)), from the stored value's arithmetic
+#pragma unroll
+      for (int e = 0; e < VW; ++e) g[e] = relu_stored<T>(yy[e], msc[e], msf[e]) > 0.f ? g[e] : 0.f;
     }
 #pragma unroll
     for (int e = 0; e < VW; ++e) {
@@ -245,15 +262,18 @@ __global__ __launch_bounds__(256) void bn_bwd_final_kernel(const float* __restri
 template <typename T>
 __global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const T* __restrict__ dz, const T* __restrict__ mz,
                                                            const T* __restrict__ y, const float* __restrict__ mean,
-                                                           const float* __restrict__ coef, T* __restrict__ dy,
+                                                           const float* __restrict__ coef,
+                                                           const float* __restrict__ mscale,
+                                                           const float* __restrict__ mshift, T* __restrict__ dy,
                                                            long nchunks, int C) {
   constexpr int VW = TT<T>::VW;
-  __shared__ float k1[kMaxC], k2[kMaxC], k3[kMaxC], mu[kMaxC];
+  __shared__ float k1[kMaxC], k2[kMaxC], k3[kMaxC], mu[kMaxC], msc[kMaxC], msf[kMaxC];
   for (int c = threadIdx.x; c < C; c += 256) {
     k1[c] = coef[3 * c];
     k2[c] = coef[3 * c + 1];
     k3[c] = coef[3 * c + 2];
     mu[c] = mean[c];
+    if (mscale) { msc[c] = mscale[c]; msf[c] = mshift[c]; }
   }
   __syncthreads();
   const int cpr = C / VW;
@@ -267,6 +287,9 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const T* __restrict__
       unpack<T>(((const uint4*)mz)[q], m);
 #pragma unroll
       for (int e = 0; e < VW; ++e) g[e] = m[e] > 0.f ? g[e] : 0.f;
+    } else if (mscale) {
+#pragma unroll
+      for (int e = 0; e < VW; ++e) g[e] = relu_stored<T>(yy[e], msc[c0 + e], msf[c0 + e]) > 0.f ? g[e] : 0.f;
     }
 #pragma unroll
     for (int e = 0; e < VW; ++e) o[e] = k1[c0 + e] * g[e] + k2[c0 + e] * (yy[e] - mu[c0 + e]) + k3[c0 + e];
@@ -281,11 +304,6 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const T* __restrict__
 // the pooled gradient and the argmax and gathers the gradient of each stem
 // pixel on the fly (rounded to the storage type, as a stored tensor would be),
 // with the ReLU mask recomputed from y by the same arithmetic.
-template <typename T>
-__device__ inline float stem_act(float y, float sc, float sf) {
-  const float t = bn_affine(y, sc, sf);
-  return TT<T>::to_f(TT<T>::from_f(t > 0.f ? t : 0.f));
-}
 
 template <typename T>
 __global__ __launch_bounds__(256) void bn_apply_pool_kernel(const T* __restrict__ y, const float* __restrict__ scale,
@@ -305,7 +323,7 @@ __global__ __launch_bounds__(256) void bn_apply_pool_kernel(const T* __restrict_
     const int c0 = cc * VW;
     auto act = [&](float* v) {
 #pragma unroll
-      for (int e = 0; e < VW; ++e) v[e] = stem_act<T>(v[e], sc[c0 + e], sf[c0 + e]);
+      for (int e = 0; e < VW; ++e) v[e] = relu_stored<T>(v[e], sc[c0 + e], sf[c0 + e]);
     };
     float best[VW];
     uint8_t bi[VW];
@@ -336,7 +354,7 @@ __device__ inline void stem_grad_quad(const T* __restrict__ dpool, const uint8_t
 #pragma unroll
     for (int e = 0; e < VW; ++e) {
       const float gr = TT<T>::to_f(TT<T>::from_f(g[p][e]));
-      const bool live = in && stem_act<T>(yy[p][e], sc[cg * VW + e], sf[cg * VW + e]) > 0.f;
+      const bool live = in && relu_stored<T>(yy[p][e], sc[cg * VW + e], sf[cg * VW + e]) > 0.f;
       g[p][e] = live ? gr : 0.f;
       yy[p][e] = in ? yy[p][e] : 0.f;
     }
@@ -475,17 +493,18 @@ int bn_eval_coef_launch(const float* gamma, const float* beta, const float* rm, 
 }
 
 int bn_bwd_partial_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
-                          const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s) {
+                          const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s,
+                          const float* mscale, const float* mshift) {
   const int vw = prec == PREC_BF16 ? 8 : 4;
   const int rpi = 256 / (C / vw);
   const int nb = pick_blocks(M, rpi);
   *nblk = nb;
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(bn_bwd_partial_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, (const bf16_t*)dz,
-                       (const bf16_t*)mz, (const bf16_t*)y, mean, rstd, M, C, part);
+                       (const bf16_t*)mz, (const bf16_t*)y, mean, rstd, mscale, mshift, M, C, part);
   else
     hipLaunchKernelGGL(bn_bwd_partial_kernel<float>, dim3(nb), dim3(256), 0, s, (const float*)dz, (const float*)mz,
-                       (const float*)y, mean, rstd, M, C, part);
+                       (const float*)y, mean, rstd, mscale, mshift, M, C, part);
   return ok();
 }
 
@@ -497,15 +516,16 @@ int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float*
 }
 
 int bn_bwd_apply_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean, const float* coef,
-                        void* dy, long M, int C, hipStream_t s) {
+                        void* dy, long M, int C, hipStream_t s, const float* mscale, const float* mshift) {
   const int vw = prec == PREC_BF16 ? 8 : 4;
   const long nchunks = M * C / vw;
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(bn_bwd_apply_kernel<bf16_t>, dim3(stream_blocks(nchunks)), dim3(256), 0, s,
-                       (const bf16_t*)dz, (const bf16_t*)mz, (const bf16_t*)y, mean, coef, (bf16_t*)dy, nchunks, C);
+                       (const bf16_t*)dz, (const bf16_t*)mz, (const bf16_t*)y, mean, coef, mscale, mshift,
+                       (bf16_t*)dy, nchunks, C);
   else
     hipLaunchKernelGGL(bn_bwd_apply_kernel<float>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const float*)dz,
-                       (const float*)mz, (const float*)y, mean, coef, (float*)dy, nchunks, C);
+                       (const float*)mz, (const float*)y, mean, coef, mscale, mshift, (float*)dy, nchunks, C);
   return ok();
 }
 

@@ -961,10 +961,14 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
       if (half == 0) issue_patch(tile, 1, buf ^ 1);
       else if (tile + G < h.tiles) issue_patch(tile + G, 0, buf ^ 1);
       const uint4* P = smem + B_U4 + buf * P_U4;
+      // the patch width is made opaque here so that the operand addresses are
+      // recomputed per phase rather than held in registers across phases
+      int pw = h.PW;
+      asm volatile("" : "+s"(pw));
       // K step t: tap t (th, tw), this half's 32 channels
       auto read_step = [&](int t, uint4(&a)[FM], uint4(&b)[FN]) {
         const int th = t / 3, tw = t - th * 3;
-        const int off = th * h.PW + tw;
+        const int off = th * pw + tw;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           const int pix = abase[i] + off;
@@ -1067,6 +1071,204 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
     // one entry per wave: its pixels over all of its tiles, shifted by the
     // first one; the sums over the 16 pixels of a lane row are shuffled
     // together, then each lane writes one channel
+    const int kk = lane & 15, jj = kk >> 2, rr = kk & 3;
+    float o1 = 0.f, o2 = 0.f, osh = 0.f;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float a1 = s1[j][r], a2 = s2[j][r];
+#pragma unroll
+        for (int dd = 1; dd < 16; dd <<= 1) {
+          a1 += __shfl_xor(a1, dd, 16);
+          a2 += __shfl_xor(a2, dd, 16);
+        }
+        if (j == jj && r == rr) { o1 = a1; o2 = a2; osh = sh[j][r]; }
+      }
+    float4* out = (float4*)g.stats + ((long)(blockIdx.x * NW + wave) * g.Cols + jj * 16 + chl + rr);
+    *out = rows_acc > 0 ? make_float4((float)rows_acc, osh, o1, o2) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  wait_vmcnt<0>();
+}
+
+// ---------------------------------------------------------------------------
+// Halo conv for the space-to-depth stem: 16 input channels (32-byte pixels),
+// a 4x4 stride-1 forward tap walk, 64 output channels (bf16). Same scheme as
+// the 64-channel halo kernel: the weights [16 taps][64 columns][16 channels]
+// (32 KB) stay in LDS, a tile is up to 256 pixels of whole output rows, and
+// its input patch (TH + 3) x (W + 3) pixels is loaded once (double-buffered)
+// for all sixteen taps. Blocks of 4 waves use 72 KB of LDS, so two share a
+// CU and one block's epilogue (stores and statistics) overlaps the other's
+// MFMAs. A K step of 32 covers two taps of the same tap row;
+// the lane group kq reads tap 2 * (step % 2) + kq / 2, channels 8 (kq % 2) ..
+// +8. LDS rows of 32 bytes are swizzled by (row / 8) mod 2, which keeps the
+// 16 consecutive rows of an operand read on distinct banks.
+// ---------------------------------------------------------------------------
+constexpr int HALO16_PROWS = 640;   // patch pixels per buffer
+constexpr int HALO16_WAVES = 4;     // waves per block; two blocks per CU overlap each other's epilogues
+constexpr int HALO16_BM = 64 * HALO16_WAVES;
+
+template <bool STATS>
+__global__ __launch_bounds__(64 * HALO16_WAVES, 2) void conv_halo16_kernel(ConvHalo h) {
+  typedef bf16_t T;
+  typedef int i32x2_t __attribute__((ext_vector_type(2)));
+  constexpr int NW = HALO16_WAVES, FM = 4, FN = 4;
+  constexpr int B_U4 = 16 * 64 * 2;                 // resident weights, uint4 units (32-byte rows)
+  constexpr int P_U4 = HALO16_PROWS * 2;            // one patch buffer
+  constexpr int PI = HALO16_PROWS / 32 / NW;        // patch load instructions per wave (32 rows each)
+  constexpr int BI = 16 * 64 / 32 / NW;             // weight load instructions per wave
+  __shared__ uint4 smem[B_U4 + 2 * P_U4];
+  static_assert((B_U4 + 2 * P_U4) * 16 * 2 <= 163840, "two blocks per CU");
+  static_assert(HALO16_PROWS % (32 * NW) == 0 && (16 * 64) % (32 * NW) == 0, "whole load instructions per wave");
+  const ConvGather& g = h.g;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t smem_lds = lds_addr(smem);
+  const i32x4_t rsA = buffer_rsrc(g.A, (uint32_t)((long)g.N * g.Hin * g.Win * 32));
+  const i32x4_t rsB = buffer_rsrc(g.B, (uint32_t)((long)g.Cols * 16 * 32));
+  const int G = gridDim.x;
+  const int slot = xcd_remap(blockIdx.x, G);
+
+  // weights: row r = tap * 64 + column; the lane's 16 bytes go to slot
+  // lane % 2 and hold half (lane % 2) ^ ((r / 8) % 2) of the tap's channels
+#pragma unroll
+  for (int u = 0; u < BI; ++u) {
+    const int r = (wave + NW * u) * 32 + (lane >> 1);
+    const int t = r >> 6, col = r & 63;
+    const int c = (lane & 1) ^ ((r >> 3) & 1);
+    lds_dma16_buf((uint32_t)((col * 16 + t) * 32 + c * 16), rsB, smem_lds + (uint32_t)((wave + NW * u) * 1024));
+  }
+  int prel[PI], prow[PI];
+#pragma unroll
+  for (int u = 0; u < PI; ++u) {
+    const int p = (wave + NW * u) * 32 + (lane >> 1);
+    const int pr = p / h.PW, pc = p - pr * h.PW;
+    const int ir = -g.ip + pr, ic = -g.ip + pc;      // input row (relative to i0) and column
+    const bool ok = p < h.PH * h.PW && (unsigned)ic < (unsigned)g.Win;
+    const int c = (lane & 1) ^ ((p >> 3) & 1);
+    prel[u] = (ir * g.Win + ic) * 32 + c * 16;
+    prow[u] = ok ? ir : -0x40000000;
+  }
+  auto issue_patch = [&](int tile, int buf) {
+    const int n = tile / h.tiles_img, i0 = (tile - n * h.tiles_img) * h.TH;
+    const int base = (n * g.Hin + i0) * g.Win * 32;
+    const uint32_t lbase = smem_lds + (uint32_t)((B_U4 + buf * P_U4) * 16);
+#pragma unroll
+    for (int u = 0; u < PI; ++u) {
+      const bool ok = (unsigned)(i0 + prow[u]) < (unsigned)g.Hin;
+      lds_dma16_buf(ok ? (uint32_t)(base + prel[u]) : kOutOfRange, rsA, lbase + (uint32_t)((wave + NW * u) * 1024));
+    }
+  };
+  int abase[FM];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int q = wave * 64 + i * 16 + (lane & 15);
+    const int ti = (int)g.fd_w.div(q);
+    abase[i] = ti * h.PW + (q - ti * g.Wm);
+  }
+  const int kq = lane >> 4, kh = kq & 1, kt = kq >> 1;
+  const int chl = 4 * (lane >> 4);
+  const int bsw = (lane >> 3) & 1;                   // weight rows: (row / 8) % 2 == (lane % 16) / 8
+  const uint32_t out_bytes = (uint32_t)((long)g.N * g.Hout * g.Wout * g.Cols * 2);
+  const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, out_bytes, 0x00020000);
+
+  float s1[FN][4], s2[FN][4], sh[FN][4];
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s1[j][e] = s2[j][e] = sh[j][e] = 0.f;
+  bool have_shift = false;
+  int rows_acc = 0;
+
+  if (slot < h.tiles) issue_patch(slot, 0);
+  int buf = 0;
+  for (int tile = slot; tile < h.tiles; tile += G, buf ^= 1) {
+    // this tile's patch has landed (vector memory operations complete in
+    // issue order; the previous tile issued exactly FM * FN stores after it)
+    if (tile == slot) wait_vmcnt<0>();
+    else wait_vmcnt<FM * FN>();
+    barrier_only();
+    if (tile + G < h.tiles) issue_patch(tile + G, buf ^ 1);
+    const int n = tile / h.tiles_img, i0 = (tile - n * h.tiles_img) * h.TH;
+    const int npx = min(h.TH, g.Hm - i0) * g.Wm;
+    const uint4* P = smem + B_U4 + buf * P_U4;
+    floatx4_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    // the patch width is made opaque here so that the operand addresses are
+    // recomputed per tile rather than held in registers across tiles
+    int pw = h.PW;
+    asm volatile("" : "+s"(pw));
+    // K step s: tap row s / 2, taps 2 (s % 2) and 2 (s % 2) + 1 of it
+    auto read_step = [&](int s, uint4(&a)[FM], uint4(&b)[FN]) {
+      const int th = s >> 1, tw = 2 * (s & 1) + kt;
+      const int off = th * pw + tw;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int pix = abase[i] + off;
+        a[i] = P[pix * 2 + (kh ^ ((pix >> 3) & 1))];
+      }
+      const int t = th * 4 + tw;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) b[j] = smem[(t * 64 + j * 16 + (lane & 15)) * 2 + (kh ^ bsw)];
+    };
+    uint4 a0[FM], b0[FN], a1[FM], b1[FN];
+    read_step(0, a0, b0);
+#pragma unroll
+    for (int s = 0; s < 8; s += 2) {
+      read_step(s + 1, a1, b1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b0[j], a0[i], 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (s + 2 < 8) read_step(s + 2, a0, b0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b1[j], a1[i], 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+
+    // ---- epilogue straight from registers (as in the 64-channel kernel)
+    const long m0 = ((long)n * g.Hm + i0) * g.Wm;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int q = wave * 64 + i * 16 + (lane & 15);
+      const bool ok = q < npx;
+      const uint32_t ob = (uint32_t)((m0 + (ok ? q : 0)) * g.Cols) + chl;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const uint2 pk = make_uint2(f2bf2(acc[i][j][0], acc[i][j][1]), f2bf2(acc[i][j][2], acc[i][j][3]));
+        __builtin_amdgcn_raw_buffer_store_b64(i32x2_t{(int)pk.x, (int)pk.y}, rsC, ok ? (ob + j * 16) * 2 : kOutOfRange,
+                                              0, 0);
+        if constexpr (STATS) {
+          const float vr[4] = {bf2f((bf16_t)(pk.x & 0xffffu)), bf2f((bf16_t)(pk.x >> 16)),
+                               bf2f((bf16_t)(pk.y & 0xffffu)), bf2f((bf16_t)(pk.y >> 16))};
+          if (!have_shift && i == 0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sh[j][e] = __shfl(vr[e], lane & 48, 64);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float d = ok ? vr[e] - sh[j][e] : 0.f;
+            s1[j][e] += d;
+            s2[j][e] = __builtin_fmaf(d, d, s2[j][e]);
+          }
+        }
+      }
+    }
+    if (wave * 64 < npx) {
+      have_shift = true;
+      rows_acc += min(64, npx - wave * 64);
+    }
+  }
+  if (STATS && slot < h.tiles) {
     const int kk = lane & 15, jj = kk >> 2, rr = kk & 3;
     float o1 = 0.f, o2 = 0.f, osh = 0.f;
 #pragma unroll
@@ -1665,6 +1867,46 @@ int halo_rows(int prec, const ConvGather& g) {
   return th;
 }
 
+// Tile height of the stem halo kernel, or 0 when the launch is not one it
+// handles (bf16, 16 -> 64 channels, a forward 4x4 stride-1 tap walk, mode 0).
+int halo16_rows(int prec, const ConvGather& g) {
+  if (prec != PREC_BF16 || g.Cin != 16 || g.Cols != 64 || g.nth != 4 || g.ntw != 4 || g.KHW != 16 || g.KW != 4 ||
+      g.K != 256)
+    return 0;
+  if (g.is != 1 || g.os != 1 || g.oph != 0 || g.opw != 0 || g.dh0 != 0 || g.dw0 != 0 || g.dhs != 1 || g.dws != 1 ||
+      g.wkh0 != 0 || g.wkw0 != 0 || g.wkhs != 1 || g.wkws != 1 || g.mode != 0)
+    return 0;
+  if (g.Hout != g.Hm || g.Wout != g.Wm || g.Hm < 1 || g.Wm < 1) return 0;
+  if ((long)g.N * g.Hin * g.Win * 32 >= (1l << 31) || (long)g.N * g.Hout * g.Wout * g.Cols * 2 >= (1l << 31)) return 0;
+  // at least 128 pixels per tile keeps the per-wave statistics entries (4
+  // per block, blocks <= tiles) at most one per 32 GEMM rows
+  int th = HALO16_BM / g.Wm;
+  if (th > g.Hm) th = g.Hm;
+  while (th > 0 && (th + 3) * (g.Wm + 3) > HALO16_PROWS) --th;
+  if (th < 1 || th * g.Wm < 128) return 0;
+  return th;
+}
+
+int launch_halo16(const ConvGather& g0, int th, hipStream_t s) {
+  ConvHalo h{};
+  h.g = g0;
+  h.g.fd_hw = FastDiv((uint32_t)(g0.Hm * g0.Wm));
+  h.g.fd_w = FastDiv((uint32_t)g0.Wm);
+  h.TH = th;
+  h.PH = th + 3;
+  h.PW = g0.Wm + 3;
+  h.tiles_img = (g0.Hm + th - 1) / th;
+  h.tiles = g0.N * h.tiles_img;
+  if (h.tiles <= 0) return 0;
+  const int slots = 2 * cu_count();
+  if (slots < 1) return -4;
+  const int grid = h.tiles < slots ? h.tiles : slots;
+  constexpr int NT = 64 * HALO16_WAVES;
+  if (g0.stats) hipLaunchKernelGGL((conv_halo16_kernel<true>), dim3(grid), dim3(NT), 0, s, h);
+  else hipLaunchKernelGGL((conv_halo16_kernel<false>), dim3(grid), dim3(NT), 0, s, h);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
 int launch_halo(const ConvGather& g0, int th, hipStream_t s) {
   ConvHalo h{};
   h.g = g0;
@@ -1728,9 +1970,13 @@ int gather_cfg(const ConvGather& g) {
 bool use_halo(int prec, const ConvGather& g) {
   return (g_gather_override == 0 || g_gather_override == kGatherHalo) && halo_rows(prec, g) > 0;
 }
+bool use_halo16(int prec, const ConvGather& g) {
+  return (g_gather_override == 0 || g_gather_override == kGatherHalo) && halo16_rows(prec, g) > 0;
+}
 
 int gather_tile(int prec, const ConvGather& g) {
   if (use_halo(prec, g)) return HALO_BM * 1000 + 64;
+  if (use_halo16(prec, g)) return HALO16_BM * 1000 + 64;
   const int id = gather_cfg(g);
   return id >= 1 && id <= kGatherCfgs ? kGather[id].bm * 1000 + kGather[id].bn : 0;
 }
@@ -1750,6 +1996,7 @@ template <typename T>
 int gather_dispatch(const ConvGather* g, int np, hipStream_t s) {
   const int prec = sizeof(T) == 2 ? PREC_BF16 : PREC_F32;
   if (np == 1 && use_halo(prec, g[0])) return launch_halo(g[0], halo_rows(prec, g[0]), s);
+  if (np == 1 && use_halo16(prec, g[0])) return launch_halo16(g[0], halo16_rows(prec, g[0]), s);
   switch (gather_cfg_multi(g, np)) {
 #define RN18_X(id, bm, bn, wgm, wgn, st, kind)                                               \
   case id:                                                                                 \
@@ -1852,6 +2099,7 @@ const char* conv_gather_kernel_name(int prec, const ConvGather& g) {
     snprintf(buf, sizeof buf, "conv_halo_kernel<%d, %s>", g.mode, g.stats ? "true" : "false");
     return intern_name(buf);
   }
+  if (use_halo16(prec, g)) return g.stats ? "conv_halo16_kernel<true>" : "conv_halo16_kernel<false>";
   return gather_kernel_name(prec, g, gather_cfg(g));
 }
 
@@ -1909,6 +2157,11 @@ int conv_gather_stat_entries(int prec, const ConvGather& g) {
     const int th = halo_rows(prec, g);
     const int tiles = g.N * ((g.Hm + th - 1) / th), cus = cu_count();
     return (tiles < cus ? tiles : cus) * HALO_WAVES;
+  }
+  if (use_halo16(prec, g)) {
+    const int th = halo16_rows(prec, g);
+    const int tiles = g.N * ((g.Hm + th - 1) / th), slots = 2 * cu_count();
+    return (tiles < slots ? tiles : slots) * HALO16_WAVES;
   }
   const int bm = gather_tile(prec, g) / 1000;
   return bm > 0 ? ceil_div(g.M, bm) : 0;

@@ -90,8 +90,13 @@ int bn_apply_launch(int prec, const void* y, const float* scale, const float* sh
 int bn_eval_coef_launch(const float* gamma, const float* beta, const float* rm, const float* rv,
                         float eps, int C, float* scale, float* shift, hipStream_t s);
 // backward partials of g = dz*(mz>0) (or dz): sum g, sum g*(y-mean)*rstd
+// The ReLU mask is mz > 0 when mz is given; with mz = NULL and mscale set it
+// is recomputed as relu(y * mscale + mshift) > 0 of the stored value (the
+// first BN of a block, whose ReLU output feeds only the next conv); with
+// neither, there is no mask.
 int bn_bwd_partial_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
-                          const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s);
+                          const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s,
+                          const float* mscale = nullptr, const float* mshift = nullptr);
 // dgamma, dbeta into grad; coefficients for the apply
 // ImageNet stem fused with its max pool (y = stem conv output [N][H][W][C],
 // pool / arg = pool output and argmax [N][Ho][Wo][C]): forward BN-apply +
@@ -108,7 +113,8 @@ int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float*
                         float* dgamma, float* dbeta, float* coef, hipStream_t s);
 // dy = k1*g + k2*(y-mean) + k3
 int bn_bwd_apply_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
-                        const float* coef, void* dy, long M, int C, hipStream_t s);
+                        const float* coef, void* dy, long M, int C, hipStream_t s, const float* mscale = nullptr,
+                        const float* mshift = nullptr);
 
 // ---------------------------------------------------------------------------
 // Misc streams
