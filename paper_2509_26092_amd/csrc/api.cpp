@@ -275,7 +275,12 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     P.coef = alloc(3 * L.cout * 4);
     const size_t ybytes = (size_t)P.M * L.cout * es;
     if (ybytes > max_y) max_y = ybytes;
-    P.splits = conv_wgrad_splits(c.prec, L.cout, P.k * P.k * P.cin, P.M, &P.pps);
+    {
+      ConvWgrad wg{};
+      wg.N = N; wg.H = P.Hin; wg.W = P.Win; wg.Cin = P.cin; wg.Ho = P.Ho; wg.Wo = P.Wo; wg.Cout = L.cout;
+      wg.KH = P.k; wg.KW = P.k; wg.stride = P.s; wg.pad = P.p;
+      P.splits = conv_wgrad_splits_shape(c.prec, wg, &P.pps);
+    }
     const size_t wp = (size_t)P.splits * L.cout * P.k * P.k * P.cin * 4;
     if (wp > max_wpart) max_wpart = wp;
     const long pc = 1024l * L.cout * 2 > 256l * L.cout * 6 ? 1024l * L.cout * 2 : 256l * L.cout * 6;
@@ -453,7 +458,7 @@ int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float
   g.pix_per_split = pps;
   g.splits = splits;
   const double mpix = (double)N * Ho * Wo;
-  int pi = prof_begin(c, RN18_K_CONV_WGRAD, layer, conv_wgrad_tile(prec, Cout, g.Kcols), conv_wgrad_kernel_name(prec, Cout, g.Kcols),
+  int pi = prof_begin(c, RN18_K_CONV_WGRAD, layer, conv_wgrad_tile(prec, Cout, g.Kcols), conv_wgrad_kernel_name_shape(prec, g),
                       2.0 * Cout * (s2d ? 49 : k * k) * cin_real * mpix,
                       (double)splits * Cout * g.Kcols * 4);
   int r = conv_wgrad_launch(prec, g, st);
@@ -1110,11 +1115,20 @@ int rn18op_conv2d_dgrad(int prec, const void* dy, const void* w, void* dx, int N
   return RN18_OK;
 }
 
+namespace {
+int wgrad_op_splits(int prec, int N, int H, int W, int Cin, int Ho, int Wo, int Cout, int k, int s, int p, int* pps) {
+  ConvWgrad wg{};
+  wg.N = N; wg.H = H; wg.W = W; wg.Cin = Cin; wg.Ho = Ho; wg.Wo = Wo; wg.Cout = Cout;
+  wg.KH = k; wg.KW = k; wg.stride = s; wg.pad = p;
+  return conv_wgrad_splits_shape(prec, wg, pps);
+}
+}  // namespace
+
 size_t rn18op_conv2d_wgrad_workspace(int prec, int N, int H, int W, int Cin, int Cout, int k, int s, int p) {
   int Ho, Wo;
   if (op_check(prec, N, H, W, Cin, Cout, k, s, p, &Ho, &Wo)) return 0;
   int pps;
-  const int splits = conv_wgrad_splits(prec, Cout, k * k * Cin, (long)N * Ho * Wo, &pps);
+  const int splits = wgrad_op_splits(prec, N, H, W, Cin, Ho, Wo, Cout, k, s, p, &pps);
   return (size_t)splits * Cout * k * k * Cin * 4;
 }
 
@@ -1126,7 +1140,7 @@ int rn18op_conv2d_wgrad(int prec, const void* dy, const void* x, float* dw, int 
   if (cin_real < 1 || cin_real > Cin) return fail(RN18_EINVAL, "cin_real must be in [1, Cin]");
   if (!dy || !x || !dw || !ws || !aligned16(dy) || !aligned16(x) || !aligned16(ws)) return fail(RN18_EINVAL, "bad pointer");
   int pps;
-  const int splits = conv_wgrad_splits(prec, Cout, k * k * Cin, (long)N * Ho * Wo, &pps);
+  const int splits = wgrad_op_splits(prec, N, H, W, Cin, Ho, Wo, Cout, k, s, p, &pps);
   if (ws_bytes < (size_t)splits * Cout * k * k * Cin * 4) return fail(RN18_ENOMEM, "workspace too small");
   LCHK(launch_wgrad_full(prec, dy, x, dw, (float*)ws, N, H, W, Cin, cin_real, Ho, Wo, Cout, k, s, p, splits, pps,
                          (hipStream_t)stream));

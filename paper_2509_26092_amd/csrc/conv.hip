@@ -1689,6 +1689,182 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g
     }
 }
 
+// ---------------------------------------------------------------------------
+// Halo weight gradient for the 64 -> 64 channel 3x3 stride-1 convolutions
+// (bf16). A block walks row strips (up to 256 output pixels of whole rows of
+// one image); per strip it stages the strip's dY rows and the input patch
+// (TH + 2) x (W + 2) with a zero halo in LDS (double-buffered), and all nine
+// taps read the patch at a fixed pixel offset, so each input pixel crosses
+// from L2 about (TH + 2)(W + 2) / (TH W) times instead of nine. Wave w owns
+// input channels [16 w, 16 w + 16) of all nine taps: 64 x 144 fp32
+// accumulators (36 MFMA tiles). The pixel-major MFMA operands come from the
+// gfx950 transposing LDS read (ds_read_b64_tr_b16: in a 16-lane group, lane
+// 4 j + q addresses the 8-byte piece of pixel j, channels 4 q .. 4 q + 3, and
+// output lane 4 a + b receives channel 4 a + b of pixels 0..3). A block's sum
+// over its strips is one split of the fixed-order split-K reduction. LDS rows
+// are 128 bytes, swizzled by (row ^ row / 8) mod 8.
+// ---------------------------------------------------------------------------
+struct WgradHalo {
+  const void* DY;
+  const void* X;
+  float* P;
+  int N, H, W, TH, PW, PH, strips_img, strips, steps;
+  FastDiv fd_w;
+};
+
+constexpr int WGH_PROWS = 352;   // patch rows per buffer
+constexpr int WGH_YROWS = 256;   // dY rows per buffer
+
+__device__ inline int wgh_sw(int row) { return (row ^ (row >> 3)) & 7; }
+
+__global__ __launch_bounds__(256, 1) void conv_wgrad_halo_kernel(WgradHalo h) {
+  constexpr int P_U4 = WGH_PROWS * 8, Y_U4 = WGH_YROWS * 8;
+  constexpr int BUF_U4 = P_U4 + Y_U4;
+  constexpr int PI = WGH_PROWS / 8 / 4, YI = WGH_YROWS / 8 / 4;   // load instructions per wave
+  __shared__ uint4 smem[2 * BUF_U4];
+  static_assert(2 * BUF_U4 * 16 <= 163840, "LDS");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t smem_lds = lds_addr(smem);
+  const i32x4_t rsX = buffer_rsrc(h.X, (uint32_t)((long)h.N * h.H * h.W * 128));
+  const i32x4_t rsY = buffer_rsrc(h.DY, (uint32_t)((long)h.N * h.H * h.W * 128));
+  const int G = gridDim.x;
+
+  // load geometry of this lane: patch rows (pixel -> input offset relative to
+  // the strip's first row, and its row for the bounds check) and dY rows
+  int prel[PI], prow[PI];
+#pragma unroll
+  for (int u = 0; u < PI; ++u) {
+    const int p = (wave + 4 * u) * 8 + (lane >> 3);
+    const int pr = p / h.PW, pc = p - pr * h.PW;
+    const int ir = pr - 1, ic = pc - 1;
+    const bool ok = p < h.PH * h.PW && (unsigned)ic < (unsigned)h.W;
+    const int c = (lane & 7) ^ wgh_sw(p);
+    prel[u] = (ir * h.W + ic) * 128 + c * 16;
+    prow[u] = ok ? ir : -0x40000000;
+  }
+  auto issue_strip = [&](int strip, int buf) {
+    const int n = strip / h.strips_img, i0 = (strip - n * h.strips_img) * h.TH;
+    const int npx = min(h.TH, h.H - i0) * h.W;
+    const int base = (n * h.H + i0) * h.W * 128;
+    const uint32_t lb = smem_lds + (uint32_t)(buf * BUF_U4 * 16);
+#pragma unroll
+    for (int u = 0; u < PI; ++u) {
+      const bool ok = (unsigned)(i0 + prow[u]) < (unsigned)h.H;
+      lds_dma16_buf(ok ? (uint32_t)(base + prel[u]) : kOutOfRange, rsX, lb + (uint32_t)((wave + 4 * u) * 1024));
+    }
+#pragma unroll
+    for (int u = 0; u < YI; ++u) {
+      const int q = (wave + 4 * u) * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ wgh_sw(q);
+      lds_dma16_buf(q < npx ? (uint32_t)(base + q * 128 + c * 16) : kOutOfRange, rsY,
+                    lb + (uint32_t)(P_U4 * 16 + (wave + 4 * u) * 1024));
+    }
+  };
+
+  floatx4_t acc[4][9];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int t = 0; t < 9; ++t) acc[i][t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int j4 = (lane & 15) >> 2, qq = lane & 3, kq = lane >> 4;
+  // byte offsets within a 128-byte row of this lane's 8-byte pieces: dY
+  // channels 16 i + 4 qq (co fragment i), X channels 16 wave + 4 qq
+  const int bo = (qq & 1) * 8;
+  auto tr = [&](const lds_char_t* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16_t*)p);
+  };
+  auto pack2 = [&](v4i16_t x, v4i16_t y) {
+    uint4 r;
+    r.x = (uint32_t)(uint16_t)x[0] | ((uint32_t)(uint16_t)x[1] << 16);
+    r.y = (uint32_t)(uint16_t)x[2] | ((uint32_t)(uint16_t)x[3] << 16);
+    r.z = (uint32_t)(uint16_t)y[0] | ((uint32_t)(uint16_t)y[1] << 16);
+    r.w = (uint32_t)(uint16_t)y[2] | ((uint32_t)(uint16_t)y[3] << 16);
+    return r;
+  };
+
+  int buf = 0;
+  if (blockIdx.x < h.strips) issue_strip(blockIdx.x, 0);
+  for (int strip = blockIdx.x; strip < h.strips; strip += G, buf ^= 1) {
+    wait_vmcnt<0>();
+    barrier_only();
+    if (strip + G < h.strips) issue_strip(strip + G, buf ^ 1);
+    const int n = strip / h.strips_img, i0 = (strip - n * h.strips_img) * h.TH;
+    const int npx = min(h.TH, h.H - i0) * h.W;
+    const lds_char_t* PX = (const lds_char_t*)(lds_void_t)(smem + buf * BUF_U4);
+    const lds_char_t* PY = PX + P_U4 * 16;
+    int pw = h.PW;
+    asm volatile("" : "+s"(pw));
+    // K step s: output pixels 32 s .. 32 s + 31 of the strip; this lane's
+    // pieces are pixels 32 s + 8 kq + j4 (+ 4)
+    auto read_step = [&](int s, uint4(&a)[4], uint4(&b)[9]) {
+      int qv[2], pp[2];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int q = 32 * s + 8 * kq + j4 + 4 * h2;
+        const int qc = q < npx ? q : 0;
+        const int ti = (int)h.fd_w.div(qc);
+        qv[h2] = q;
+        pp[h2] = ti * pw + (qc - ti * h.W);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = 2 * i + (qq >> 1);
+        v4i16_t x[2];
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) x[h2] = tr(PY + qv[h2] * 128 + ((c ^ wgh_sw(qv[h2])) << 4) + bo);
+        a[i] = pack2(x[0], x[1]);
+      }
+      const int cx = 2 * wave + (qq >> 1);
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int off = (t / 3) * pw + (t % 3);
+        v4i16_t x[2];
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+          const int r = pp[h2] + off;
+          x[h2] = tr(PX + r * 128 + ((cx ^ wgh_sw(r)) << 4) + bo);
+        }
+        b[t] = pack2(x[0], x[1]);
+      }
+    };
+    auto mma_step = [&](const uint4(&a)[4], const uint4(&b)[9]) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int t = 0; t < 9; ++t)
+          acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[i]),
+                                                              __builtin_bit_cast(bf16x8_t, b[t]), acc[i][t], 0, 0, 0);
+    };
+    uint4 a0[4], b0[9], a1[4], b1[9];
+    const int S = (npx + 31) / 32;
+    read_step(0, a0, b0);
+    for (int s = 0; s < S; s += 2) {
+      if (s + 1 < S) read_step(s + 1, a1, b1);
+      __builtin_amdgcn_sched_barrier(0);
+      mma_step(a0, b0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (s + 1 < S) {
+        if (s + 2 < S) read_step(s + 2, a0, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_step(a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
+  // this block's split: P[block][co][tap * 64 + ci]
+  float* __restrict__ P = h.P + (long)blockIdx.x * 64 * 576;
+  const int ci = 16 * wave + (lane & 15);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int t = 0; t < 9; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) P[(16 * i + 4 * kq + r) * 576 + t * 64 + ci] = acc[i][t][r];
+}
+
 // Sum of the split partials in a fixed order, written in OIHW order. A block
 // covers 256 consecutive (co, tap, ci) elements as 64 float4 columns with 4
 // groups of 64 threads; group q sums splits q, q+4, ... and the four sums are
@@ -2074,6 +2250,42 @@ int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
   }
 }
 
+// Strip height of the halo weight-gradient kernel, or 0 when the shape is not
+// one it handles (bf16, 64 -> 64 channels, 3x3, stride 1, padding 1).
+int wgrad_halo_rows(int prec, const ConvWgrad& g) {
+  if (prec != PREC_BF16 || g.Cin != 64 || g.Cout != 64 || g.KH != 3 || g.KW != 3 || g.stride != 1 || g.pad != 1)
+    return 0;
+  if (g.Ho != g.H || g.Wo != g.W || g.H < 1 || g.W < 1 || g.W > 256) return 0;
+  if ((long)g.N * g.H * g.W * 128 >= (1l << 31)) return 0;
+  int th = WGH_YROWS / g.W;
+  if (th > g.H) th = g.H;
+  while (th > 0 && (th + 2) * (g.W + 2) > WGH_PROWS) --th;
+  return th;
+}
+
+bool use_wgrad_halo(int prec, const ConvWgrad& g) { return g_wgrad_override == 0 && wgrad_halo_rows(prec, g) > 0; }
+
+int wgrad_halo_grid(int prec, const ConvWgrad& g) {
+  const int th = wgrad_halo_rows(prec, g);
+  const long strips = (long)g.N * ((g.H + th - 1) / th);
+  const int cus = cu_count();
+  return (int)(strips < cus ? strips : cus);
+}
+
+int launch_wgrad_halo(const ConvWgrad& g, hipStream_t s) {
+  WgradHalo h{};
+  h.DY = g.DY; h.X = g.X; h.P = g.P;
+  h.N = g.N; h.H = g.H; h.W = g.W;
+  h.TH = wgrad_halo_rows(PREC_BF16, g);
+  h.PW = g.W + 2; h.PH = h.TH + 2;
+  h.strips_img = (g.H + h.TH - 1) / h.TH;
+  h.strips = g.N * h.strips_img;
+  h.fd_w = FastDiv((uint32_t)g.W);
+  if (g.splits != wgrad_halo_grid(PREC_BF16, g) || g.splits < 1) return -1;   // split count planned for this kernel
+  hipLaunchKernelGGL(conv_wgrad_halo_kernel, dim3(g.splits), dim3(256), 0, s, h);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
 }  // namespace
 
 namespace {
@@ -2217,7 +2429,21 @@ int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_spl
   return (int)splits;
 }
 
+int conv_wgrad_splits_shape(int prec, const ConvWgrad& g, int* pix_per_split) {
+  if (use_wgrad_halo(prec, g)) {
+    *pix_per_split = 0;
+    return wgrad_halo_grid(prec, g);
+  }
+  return conv_wgrad_splits(prec, g.Cout, g.KH * g.KW * g.Cin, (long)g.N * g.Ho * g.Wo, pix_per_split);
+}
+
+const char* conv_wgrad_kernel_name_shape(int prec, const ConvWgrad& g) {
+  if (use_wgrad_halo(prec, g)) return "conv_wgrad_halo_kernel";
+  return conv_wgrad_kernel_name(prec, g.Cout, g.KH * g.KW * g.Cin);
+}
+
 int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s) {
+  if (use_wgrad_halo(prec, g)) return launch_wgrad_halo(g, s);
   // the pipelined kernels address both operands with 31-bit byte offsets
   const long es = prec == PREC_BF16 ? 2 : 4;
   if ((long)g.Mpix * g.Cout * es >= (1l << 31) || (long)g.N * g.H * g.W * g.Cin * es >= (1l << 31)) return -1;

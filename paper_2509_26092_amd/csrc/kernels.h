@@ -63,6 +63,11 @@ const char* kernel_instance_name(const char* base, int prec);
 int conv_wgrad_override(int id);
 // Choose the split count for a weight-gradient GEMM (deterministic function of the shape).
 int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split);
+// Split count (and pixels per split) for a weight-gradient launch of this
+// shape (N, H, W, Cin, Ho, Wo, Cout, KH, KW, stride, pad set in g): the
+// 64-channel 3x3 stride-1 shape runs the halo kernel, one split per block.
+int conv_wgrad_splits_shape(int prec, const ConvWgrad& g, int* pix_per_split);
+const char* conv_wgrad_kernel_name_shape(int prec, const ConvWgrad& g);
 // Sum partials in split order; write OIHW gradient (Cin_real of Cin channels kept).
 // Fixed-order sum of the split partials [splits][Cout][KHW][Cin] into OIHW
 // [Cout][Cin_real][KHW]; s2d = 1 maps the space-to-depth stem partials

@@ -103,6 +103,16 @@ def test_conv_wgrad_split_k(prec, case):
     test_conv_wgrad(prec, case)
 
 
+@pytest.mark.parametrize("case", [(2, 64, 64, 56, 56, 64, 3, 1, 1), (3, 64, 64, 13, 11, 64, 3, 1, 1),
+                                  (1, 64, 64, 40, 40, 64, 3, 1, 1), (4, 64, 64, 7, 7, 64, 3, 1, 1),
+                                  (2, 64, 64, 9, 50, 64, 3, 1, 1)], ids=case_id)
+def test_conv_wgrad_halo(case):
+    """The halo weight-gradient kernel (64 -> 64 channel 3x3 stride-1 bf16
+    shapes, picked automatically): row strips with a partial last strip,
+    single-strip images and strips spread over many blocks."""
+    test_conv_wgrad("bf16", case)
+
+
 def test_conv_wgrad_deterministic():
     import torch
     N, C, H, W, O, k, s, p = 8, 64, 28, 28, 64, 3, 1, 1
