@@ -1693,29 +1693,29 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_wgrad2_kernel(ConvWgrad g
 // Halo weight gradient for the 64 -> 64 channel 3x3 stride-1 convolutions
 // (bf16). A block walks row strips (up to 256 output pixels of whole rows of
 // one image); per strip it stages the strip's dY rows and the input patch
-// (TH + 2) x (W + 2) with a zero halo in LDS (double-buffered), and all nine
-// taps read the patch at a fixed pixel offset, so each input pixel crosses
-// from L2 about (TH + 2)(W + 2) / (TH W) times instead of nine. Wave w owns
-// input channels [16 w, 16 w + 16) of all nine taps: 64 x 144 fp32
-// accumulators (36 MFMA tiles). The pixel-major MFMA operands come from the
-// gfx950 transposing LDS read (ds_read_b64_tr_b16: in a 16-lane group, lane
-// 4 j + q addresses the 8-byte piece of pixel j, channels 4 q .. 4 q + 3, and
-// output lane 4 a + b receives channel 4 a + b of pixels 0..3). A block's sum
-// over its strips is one split of the fixed-order split-K reduction. LDS rows
-// are 128 bytes, swizzled by (row ^ row / 8) mod 8.
+// (TH + 2) x PW with a zero halo in LDS (double-buffered), and all nine taps
+// read the patch at a fixed pixel offset, so each input pixel crosses from
+// L2 about (TH + 2) PW / (TH W) times instead of nine. Wave w owns input
+// channels [16 w, 16 w + 16) of all nine taps: 64 x 144 fp32 accumulators
+// (36 MFMA tiles). The pixel-major MFMA operands come from the gfx950
+// transposing LDS read (ds_read_b64_tr_b16: in a 16-lane group, lane 4 j + q
+// addresses the 8-byte piece of pixel j, channels 4 q .. 4 q + 3, and output
+// lane 4 a + b receives channel 4 a + b of pixels 0..3). A block's sum over
+// its strips is one split of the fixed-order split-K reduction.
+// LDS rows are 128 bytes, swizzled by row mod 8; the patch width PW is a
+// multiple of 8, so a tap-row shift keeps a row's swizzle and a K step (32
+// pixels) keeps every dY row's: the per-step address arithmetic is a few
+// adds.
 // ---------------------------------------------------------------------------
 struct WgradHalo {
   const void* DY;
   const void* X;
   float* P;
-  int N, H, W, TH, PW, PH, strips_img, strips, steps;
-  FastDiv fd_w;
+  int N, H, W, TH, PW, PH, strips_img, strips;
 };
 
-constexpr int WGH_PROWS = 352;   // patch rows per buffer
+constexpr int WGH_PROWS = 384;   // patch rows per buffer
 constexpr int WGH_YROWS = 256;   // dY rows per buffer
-
-__device__ inline int wgh_sw(int row) { return (row ^ (row >> 3)) & 7; }
 
 __global__ __launch_bounds__(256, 1) void conv_wgrad_halo_kernel(WgradHalo h) {
   constexpr int P_U4 = WGH_PROWS * 8, Y_U4 = WGH_YROWS * 8;
@@ -1739,7 +1739,7 @@ __global__ __launch_bounds__(256, 1) void conv_wgrad_halo_kernel(WgradHalo h) {
     const int pr = p / h.PW, pc = p - pr * h.PW;
     const int ir = pr - 1, ic = pc - 1;
     const bool ok = p < h.PH * h.PW && (unsigned)ic < (unsigned)h.W;
-    const int c = (lane & 7) ^ wgh_sw(p);
+    const int c = (lane & 7) ^ (p & 7);
     prel[u] = (ir * h.W + ic) * 128 + c * 16;
     prow[u] = ok ? ir : -0x40000000;
   }
@@ -1756,7 +1756,7 @@ __global__ __launch_bounds__(256, 1) void conv_wgrad_halo_kernel(WgradHalo h) {
 #pragma unroll
     for (int u = 0; u < YI; ++u) {
       const int q = (wave + 4 * u) * 8 + (lane >> 3);
-      const int c = (lane & 7) ^ wgh_sw(q);
+      const int c = (lane & 7) ^ (q & 7);
       lds_dma16_buf(q < npx ? (uint32_t)(base + q * 128 + c * 16) : kOutOfRange, rsY,
                     lb + (uint32_t)(P_U4 * 16 + (wave + 4 * u) * 1024));
     }
@@ -1769,9 +1769,18 @@ __global__ __launch_bounds__(256, 1) void conv_wgrad_halo_kernel(WgradHalo h) {
     for (int t = 0; t < 9; ++t) acc[i][t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
   const int j4 = (lane & 15) >> 2, qq = lane & 3, kq = lane >> 4;
-  // byte offsets within a 128-byte row of this lane's 8-byte pieces: dY
-  // channels 16 i + 4 qq (co fragment i), X channels 16 wave + 4 qq
   const int bo = (qq & 1) * 8;
+  const int cx = 2 * wave + (qq >> 1);             // X chunk of this lane's 4 channels
+  // dY rows of step s are 32 s + 8 kq + j4 + 4 h2: their row mod 8 is j4 + 4 h2,
+  // so the byte offset of each fragment piece is fixed up to 4096 s
+  int yoff[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int r = 8 * kq + j4 + 4 * h2;
+      yoff[i][h2] = r * 128 + (((2 * i + (qq >> 1)) ^ (r & 7)) << 4) + bo;
+    }
   auto tr = [&](const lds_char_t* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16_t*)p);
   };
@@ -1794,39 +1803,45 @@ __global__ __launch_bounds__(256, 1) void conv_wgrad_halo_kernel(WgradHalo h) {
     const int npx = min(h.TH, h.H - i0) * h.W;
     const lds_char_t* PX = (const lds_char_t*)(lds_void_t)(smem + buf * BUF_U4);
     const lds_char_t* PY = PX + P_U4 * 16;
-    int pw = h.PW;
-    asm volatile("" : "+s"(pw));
-    // K step s: output pixels 32 s .. 32 s + 31 of the strip; this lane's
-    // pieces are pixels 32 s + 8 kq + j4 (+ 4)
-    auto read_step = [&](int s, uint4(&a)[4], uint4(&b)[9]) {
-      int qv[2], pp[2];
+    const int rowb = h.PW * 128;                     // one patch row of pixels, in bytes
+    // patch pixel of tap (0, 0) of this lane's two pixels of step 0; pixels
+    // beyond the strip read patch pixel 0 (their dY rows are zero)
+    int ti[2], tj[2];
 #pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        const int q = 32 * s + 8 * kq + j4 + 4 * h2;
-        const int qc = q < npx ? q : 0;
-        const int ti = (int)h.fd_w.div(qc);
-        qv[h2] = q;
-        pp[h2] = ti * pw + (qc - ti * h.W);
-      }
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int q = 8 * kq + j4 + 4 * h2;
+      ti[h2] = q / h.W;
+      tj[h2] = q - ti[h2] * h.W;
+    }
+    auto read_step = [&](int s, uint4(&a)[4], uint4(&b)[9]) {
+      const int ys = s * 4096;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int c = 2 * i + (qq >> 1);
         v4i16_t x[2];
 #pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2) x[h2] = tr(PY + qv[h2] * 128 + ((c ^ wgh_sw(qv[h2])) << 4) + bo);
+        for (int h2 = 0; h2 < 2; ++h2) x[h2] = tr(PY + ys + yoff[i][h2]);
         a[i] = pack2(x[0], x[1]);
       }
-      const int cx = 2 * wave + (qq >> 1);
+      int pb[2][3];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const bool ok = 32 * s + 8 * kq + j4 + 4 * h2 < npx;
+        const int pp = ok ? ti[h2] * h.PW + tj[h2] : 0;
+#pragma unroll
+        for (int tw = 0; tw < 3; ++tw) pb[h2][tw] = (pp + tw) * 128 + ((cx ^ ((pp + tw) & 7)) << 4) + bo;
+      }
 #pragma unroll
       for (int t = 0; t < 9; ++t) {
-        const int off = (t / 3) * pw + (t % 3);
         v4i16_t x[2];
 #pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2) {
-          const int r = pp[h2] + off;
-          x[h2] = tr(PX + r * 128 + ((cx ^ wgh_sw(r)) << 4) + bo);
-        }
+        for (int h2 = 0; h2 < 2; ++h2) x[h2] = tr(PX + (t / 3) * rowb + pb[h2][t % 3]);
         b[t] = pack2(x[0], x[1]);
+      }
+      // advance this lane's pixels by 32 for the next step
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        tj[h2] += 32;
+        while (tj[h2] >= h.W) { tj[h2] -= h.W; ++ti[h2]; }
       }
     };
     auto mma_step = [&](const uint4(&a)[4], const uint4(&b)[9]) {
@@ -2252,6 +2267,8 @@ int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
 
 // Strip height of the halo weight-gradient kernel, or 0 when the shape is not
 // one it handles (bf16, 64 -> 64 channels, 3x3, stride 1, padding 1).
+int wgrad_halo_pw(const ConvWgrad& g) { return (g.W + 2 + 7) / 8 * 8; }
+
 int wgrad_halo_rows(int prec, const ConvWgrad& g) {
   if (prec != PREC_BF16 || g.Cin != 64 || g.Cout != 64 || g.KH != 3 || g.KW != 3 || g.stride != 1 || g.pad != 1)
     return 0;
@@ -2259,7 +2276,7 @@ int wgrad_halo_rows(int prec, const ConvWgrad& g) {
   if ((long)g.N * g.H * g.W * 128 >= (1l << 31)) return 0;
   int th = WGH_YROWS / g.W;
   if (th > g.H) th = g.H;
-  while (th > 0 && (th + 2) * (g.W + 2) > WGH_PROWS) --th;
+  while (th > 0 && (th + 2) * wgrad_halo_pw(g) > WGH_PROWS) --th;
   return th;
 }
 
@@ -2277,10 +2294,9 @@ int launch_wgrad_halo(const ConvWgrad& g, hipStream_t s) {
   h.DY = g.DY; h.X = g.X; h.P = g.P;
   h.N = g.N; h.H = g.H; h.W = g.W;
   h.TH = wgrad_halo_rows(PREC_BF16, g);
-  h.PW = g.W + 2; h.PH = h.TH + 2;
+  h.PW = wgrad_halo_pw(g); h.PH = h.TH + 2;
   h.strips_img = (g.H + h.TH - 1) / h.TH;
   h.strips = g.N * h.strips_img;
-  h.fd_w = FastDiv((uint32_t)g.W);
   if (g.splits != wgrad_halo_grid(PREC_BF16, g) || g.splits < 1) return -1;   // split count planned for this kernel
   hipLaunchKernelGGL(conv_wgrad_halo_kernel, dim3(g.splits), dim3(256), 0, s, h);
   return hipGetLastError() == hipSuccess ? 0 : -4;
