@@ -283,7 +283,12 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     }
     const size_t wp = (size_t)P.splits * L.cout * P.k * P.k * P.cin * 4;
     if (wp > max_wpart) max_wpart = wp;
-    const long pc = 1024l * L.cout * 2 > 256l * L.cout * 6 ? 1024l * L.cout * 2 : 256l * L.cout * 6;
+    // backward partials (2 floats per block and channel) or the forward
+    // statistics' chunk sums (3 doubles per chunk and channel, <= 64 chunks)
+    long pc = (long)bn_bwd_partial_blocks(c.prec, P.M, L.cout) * L.cout * 2;
+    if (li == 0 && a.imagenet)
+      pc = std::max(pc, (long)bn_bwd_partial_pool_blocks(c.prec, N, P.Ho, P.Wo, L.cout) * L.cout * 2);
+    pc = std::max(pc, 64l * L.cout * 6);
     if (pc > max_partC) max_partC = pc;
     return true;
   };

@@ -19,8 +19,10 @@ namespace {
 
 constexpr int kMaxC = 512;
 
+// Blocks of a backward partial reduction over M rows: at least 8 rows per
+// thread, at most 1024.
 int pick_blocks(long M, int rows_per_iter) {
-  long b = M / ((long)rows_per_iter * 8);  // >= 8 rows per thread
+  long b = M / ((long)rows_per_iter * 8);
   if (b > 1024) b = 1024;
   if (b < 1) b = 1;
   return (int)b;
@@ -198,25 +200,41 @@ __global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict
     msf[e] = mscale ? mshift[cg * VW + e] : 0.f;
     s1[e] = s2[e] = 0.f;
   }
-  for (long r = r_begin + rr; r < r_end; r += rpi) {
-    const long o = r * C + cg * VW;
-    float g[VW], yy[VW];
-    unpack<T>(*(const uint4*)(dz + o), g);
-    unpack<T>(*(const uint4*)(y + o), yy);
-    if (mz) {
-      float m[VW];
-      unpack<T>(*(const uint4*)(mz + o), m);
+  // four rows per step, all loads issued before any is used (rows past the
+  // range load the thread's first row and add nothing)
+  constexpr int U = 4;
+  for (long r0 = r_begin + rr; r0 < r_end; r0 += U * rpi) {
+    uint4 qg[U], qy[U], qm[U];
 #pragma unroll
-      for (int e = 0; e < VW; ++e) g[e] = m[e] > 0.f ? g[e] : 0.f;
-    } else if (mscale) {
-      // the ReLU mask of relu(bn(y)), from the stored value's arithmetic
-#pragma unroll
-      for (int e = 0; e < VW; ++e) g[e] = relu_stored<T>(yy[e], msc[e], msf[e]) > 0.f ? g[e] : 0.f;
+    for (int u = 0; u < U; ++u) {
+      const long r = r0 + u * rpi < r_end ? r0 + u * rpi : r0;
+      const long o = r * C + cg * VW;
+      qg[u] = *(const uint4*)(dz + o);
+      qy[u] = *(const uint4*)(y + o);
+      if (mz) qm[u] = *(const uint4*)(mz + o);
     }
 #pragma unroll
-    for (int e = 0; e < VW; ++e) {
-      s1[e] += g[e];
-      s2[e] += g[e] * ((yy[e] - mu[e]) * rs[e]);
+    for (int u = 0; u < U; ++u) {
+      const bool live_row = r0 + u * rpi < r_end;
+      float g[VW], yy[VW];
+      unpack<T>(qg[u], g);
+      unpack<T>(qy[u], yy);
+      if (mz) {
+        float m[VW];
+        unpack<T>(qm[u], m);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) g[e] = m[e] > 0.f ? g[e] : 0.f;
+      } else if (mscale) {
+        // the ReLU mask of relu(bn(y)), from the stored value's arithmetic
+#pragma unroll
+        for (int e = 0; e < VW; ++e) g[e] = relu_stored<T>(yy[e], msc[e], msf[e]) > 0.f ? g[e] : 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < VW; ++e) {
+        const float gv = live_row ? g[e] : 0.f;
+        s1[e] += gv;
+        s2[e] += gv * ((yy[e] - mu[e]) * rs[e]);
+      }
     }
   }
 #pragma unroll
@@ -492,12 +510,21 @@ int bn_eval_coef_launch(const float* gamma, const float* beta, const float* rm, 
   return ok();
 }
 
+int bn_bwd_partial_blocks(int prec, long M, int C) {
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  return pick_blocks(M, 256 / (C / vw));
+}
+
+int bn_bwd_partial_pool_blocks(int prec, int N, int H, int W, int C) {
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const int rpi = 256 / (C / vw);
+  return pick_blocks((long)N * ((H + 1) / 2) * ((W + 1) / 2), rpi);
+}
+
 int bn_bwd_partial_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
                           const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s,
                           const float* mscale, const float* mshift) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
-  const int rpi = 256 / (C / vw);
-  const int nb = pick_blocks(M, rpi);
+  const int nb = bn_bwd_partial_blocks(prec, M, C);
   *nblk = nb;
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(bn_bwd_partial_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, (const bf16_t*)dz,
@@ -547,10 +574,7 @@ int bn_bwd_partial_pool_launch(int prec, const void* dpool, const uint8_t* arg, 
                                const float* shift, const float* mean, const float* rstd, int N, int H, int W, int C,
                                int Ho, int Wo, float* part, int* nblk, hipStream_t s) {
   if (C > kMaxC || (long)N * H * W * C >= (1l << 31)) return -1;
-  const int vw = prec == PREC_BF16 ? 8 : 4;
-  const int rpi = 256 / (C / vw);
-  const long Mq = (long)N * ((H + 1) / 2) * ((W + 1) / 2);
-  const int nb = pick_blocks(Mq, rpi);
+  const int nb = bn_bwd_partial_pool_blocks(prec, N, H, W, C);
   *nblk = nb;
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(bn_bwd_partial_pool_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, (const bf16_t*)dpool, arg,

@@ -263,10 +263,12 @@ __device__ inline void gather_impl(const ConvGather& g) {
       const uint32_t v = uoff[u] == kOutOfRange ? kOutOfRange : uoff[u] + sb;
       lds_dma16_buf(v, rsB, base + (uint32_t)((AI + wave_u + NW * (u - UA)) * 1024));
     }
-    if (++st_cb == CB) {
-      st_cb = 0;
-      ++st_ti;
-      if (++st_tw == ntw_g) { st_tw = 0; ++st_th; }
+    // taps inner, channel blocks outer: consecutive stages of a channel block
+    // read input rows shifted by one tap, which L2 (and at times L1) still holds
+    ++st_ti;
+    if (++st_tw == ntw_g) {
+      st_tw = 0;
+      if (++st_th == g.nth) { st_th = 0; st_ti = 0; ++st_cb; }
     }
   };
 

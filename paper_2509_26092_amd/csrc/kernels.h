@@ -102,6 +102,10 @@ int bn_eval_coef_launch(const float* gamma, const float* beta, const float* rm, 
 int bn_bwd_partial_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
                           const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s,
                           const float* mscale = nullptr, const float* mshift = nullptr);
+// blocks (= partial entries of 2 floats per channel) that the two backward
+// partial launches use for a shape; `part` must hold blocks * C * 2 floats
+int bn_bwd_partial_blocks(int prec, long M, int C);
+int bn_bwd_partial_pool_blocks(int prec, int N, int H, int W, int C);
 // dgamma, dbeta into grad; coefficients for the apply
 // ImageNet stem fused with its max pool (y = stem conv output [N][H][W][C],
 // pool / arg = pool output and argmax [N][Ho][Wo][C]): forward BN-apply +

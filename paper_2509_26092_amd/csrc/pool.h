@@ -43,32 +43,33 @@ template <> struct ArgVec<4> {
   }
 };
 
+// Output gradients and argmax bytes of the two pool windows (i, j) and
+// (i, j + 1), channel chunk cc. The loads are branch-free (clamped to a valid
+// window) so that both are in flight together; windows past the output edge
+// get argmax 0xff, which matches no tap.
+template <typename T>
+__device__ inline void pool_window_pair(const T* __restrict__ dy, const uint8_t* __restrict__ arg, int n, int i,
+                                        int j, int cc, int cpr, int Ho, int Wo, float (*g)[TT<T>::VW],
+                                        uint8_t (*a)[TT<T>::VW]) {
+  constexpr int VW = TT<T>::VW;
+#pragma unroll
+  for (int dj = 0; dj < 2; ++dj) {
+    const bool in = i < Ho && j + dj < Wo;
+    const int oq = ((n * Ho + min(i, Ho - 1)) * Wo + min(j + dj, Wo - 1)) * cpr + cc;
+    unpack<T>(((const uint4*)dy)[oq], g[dj]);
+    ArgVec<VW>::load(arg + oq * VW, a[dj]);
+#pragma unroll
+    for (int e = 0; e < VW; ++e) a[dj][e] = in ? a[dj][e] : (uint8_t)0xff;
+  }
+}
+
 // Gradient of the pool input at the 2x2 quad of pixels (2qi + py, 2qj + px),
 // py, px in {0, 1}: the sum over the windows whose (first) maximum is the
-// pixel of their output gradients, in tap order (kh, kw). The four windows
-// (qi + di, qj + dj) that can pick a pixel of the quad are loaded once.
-// acc[2*py + px][] receives VW fp32 sums, not yet rounded (pixels past the
-// input edge get 0).
-template <typename T>
-__device__ inline void pool_grad_quad(const T* __restrict__ dy, const uint8_t* __restrict__ arg, int n, int qi,
-                                      int qj, int cc, int cpr, int Ho, int Wo, float (*acc)[TT<T>::VW]) {
-  constexpr int VW = TT<T>::VW;
-  // branch-free loads (clamped to a valid window, then masked) so that all
-  // four are in flight together
-  float g[2][2][VW];
-  uint8_t a[2][2][VW];
-#pragma unroll
-  for (int di = 0; di < 2; ++di)
-#pragma unroll
-    for (int dj = 0; dj < 2; ++dj) {
-      const int i = qi + di, j = qj + dj;
-      const bool in = i < Ho && j < Wo;
-      const int oq = ((n * Ho + min(i, Ho - 1)) * Wo + min(j, Wo - 1)) * cpr + cc;
-      unpack<T>(((const uint4*)dy)[oq], g[di][dj]);
-      ArgVec<VW>::load(arg + oq * VW, a[di][dj]);
-#pragma unroll
-      for (int e = 0; e < VW; ++e) a[di][dj][e] = in ? a[di][dj][e] : (uint8_t)0xff;
-    }
+// pixel of their output gradients, in tap order (kh, kw). g[di][dj], a[di][dj]
+// are the four windows (qi + di, qj + dj) that can pick a pixel of the quad.
+// acc[2*py + px][] receives VW fp32 sums, not yet rounded.
+template <int VW>
+__device__ inline void pool_quad_combine(const float (*g)[2][VW], const uint8_t (*a)[2][VW], float (*acc)[VW]) {
   // pixel row offset py takes window rows (tap row kh, window di) in kh order:
   // py = 0: (1, 0); py = 1: (0, 1), (2, 0). Columns likewise.
 #pragma unroll
@@ -93,6 +94,18 @@ __device__ inline void pool_grad_quad(const T* __restrict__ dy, const uint8_t* _
         }
       }
     }
+}
+
+// The same for one quad, loading its four windows.
+template <typename T>
+__device__ inline void pool_grad_quad(const T* __restrict__ dy, const uint8_t* __restrict__ arg, int n, int qi,
+                                      int qj, int cc, int cpr, int Ho, int Wo, float (*acc)[TT<T>::VW]) {
+  constexpr int VW = TT<T>::VW;
+  float g[2][2][VW];
+  uint8_t a[2][2][VW];
+  pool_window_pair<T>(dy, arg, n, qi, qj, cc, cpr, Ho, Wo, g[0], a[0]);
+  pool_window_pair<T>(dy, arg, n, qi + 1, qj, cc, cpr, Ho, Wo, g[1], a[1]);
+  pool_quad_combine<VW>(g, a, acc);
 }
 
 // Max over the 3x3 window of output (n, i, j), channel chunk cc, of the
