@@ -1292,6 +1292,379 @@ __global__ __launch_bounds__(64 * HALO16_WAVES, 2) void conv_halo16_kernel(ConvH
 }
 
 // ---------------------------------------------------------------------------
+// Halo conv with streamed weights for the 3x3 stride-1 convolutions with 128
+// or more input channels (bf16; forward and stride-1 data gradient). A tile is
+// TH whole output rows of one image by 128 output columns. For each half of a
+// 64-channel block (32 channels) the input patch (TH + 2) x (W + 2) with its
+// zero halo is staged in LDS once (double-buffered across halves) and all
+// nine taps read it at a fixed pixel offset, so an input pixel crosses from L2
+// about (TH + 2) / TH times per half instead of nine; the weights of a (half,
+// tap) step, 128 columns x 64 bytes, stream through an LDS ring of HW_RING
+// slots, HW_RING - 2 steps ahead.
+// The GEMM rows of a tile are the patch-width grid: row v = r (W + 2) + c is
+// output pixel (r, c) for c < W, and the two columns past the row end are
+// computed and dropped. Tap (th, tw) of row v then reads patch pixel v + th
+// (W + 2) + tw: 16 consecutive rows read 16 consecutive patch pixels (no LDS
+// bank conflicts) at a constant offset per tap (no per-step address
+// arithmetic).
+// Four waves, one per SIMD: two along rows (7 groups of 16 each, so at most
+// 224 rows per tile) and two along columns (64 each), 16x16x32 MFMAs with the
+// weight fragment as the first operand, so a lane holds four consecutive
+// channels of one row. Persistent blocks walk the tiles; the epilogue stores
+// from registers and, in the forward pass, writes BN partial statistics per
+// (tile, row wave): 2 entries per tile.
+// Patch and ring rows are 64 bytes; chunk c of row p sits in slot c ^ ((p / 4)
+// % 4), which keeps 16 consecutive rows of an operand read on distinct banks,
+// and since a shift by 16 rows keeps the swizzle, the 16-row groups of one tap
+// are constant offsets from one address per tap. One LDS-DMA instruction
+// fills 16 rows (16 cache lines).
+// ---------------------------------------------------------------------------
+struct ConvHaloW {
+  ConvGather g;
+  int TH;          // output rows per tile
+  int PW;          // patch columns (W + 2)
+  int PP;          // patch pixels (TH + 2) * PW
+  int tiles_img;   // ceil(Hm / TH)
+  int tiles_m;     // N * tiles_img
+  int tiles;       // tiles_m * Cols / 128
+  FastDiv fd_pw;   // division by PW
+};
+
+#ifndef RN18_HW_RING
+#define RN18_HW_RING 3
+#endif
+#ifndef RN18_HW_BPC
+#define RN18_HW_BPC 1
+#endif
+#ifndef RN18_HW_WGN
+#define RN18_HW_WGN 4
+#endif
+constexpr int HW_WGN = RN18_HW_WGN;          // column waves: 2 (64 columns each) or 4 (32 each)
+constexpr int HW_WAVES = 2 * HW_WGN;
+constexpr int HW_FM = 7;                     // 16-row groups per row wave
+constexpr int HW_ROWS = 2 * HW_FM * 16;      // GEMM rows per tile (224)
+constexpr int HW_BN = 128;
+constexpr int HW_PROWS = HW_WGN == 2 ? 320 : 384;  // patch pixels per half buffer
+constexpr int HW_RING = RN18_HW_RING;        // weight ring slots: 3 or 6 (a divisor of 18)
+constexpr int HW_BPC = RN18_HW_BPC;          // blocks per CU
+// (at most 6: the weights that the wait before a half's first read covers are
+// issued after that half's patch pieces)
+static_assert(HW_RING == 3 || HW_RING == 6, "ring depth");
+
+// s_waitcnt vmcnt(n) for a wave-uniform n in 0..31
+__device__ inline void wait_vmcnt_dyn(int n) {
+  switch (n) {
+#define RN18_W(N) case N: wait_vmcnt<N>(); break;
+    RN18_W(0) RN18_W(1) RN18_W(2) RN18_W(3) RN18_W(4) RN18_W(5) RN18_W(6) RN18_W(7) RN18_W(8) RN18_W(9)
+    RN18_W(10) RN18_W(11) RN18_W(12) RN18_W(13) RN18_W(14) RN18_W(15) RN18_W(16) RN18_W(17) RN18_W(18)
+    RN18_W(19) RN18_W(20) RN18_W(21) RN18_W(22) RN18_W(23) RN18_W(24) RN18_W(25) RN18_W(26) RN18_W(27)
+    RN18_W(28) RN18_W(29) RN18_W(30)
+#undef RN18_W
+    default: wait_vmcnt<0>(); break;
+  }
+}
+
+template <int MODE, bool STATS>
+__global__ __launch_bounds__(64 * HW_WAVES, HW_BPC) void conv_halo_wide_kernel(ConvHaloW h) {
+  typedef bf16_t T;
+  constexpr int NW = HW_WAVES, FM = HW_FM, FN = HW_BN / HW_WGN / 16, WTN = HW_BN / HW_WGN;
+  constexpr int BUF_P = HW_PROWS * 64;              // bytes of one patch buffer
+  constexpr int SLOT_R = HW_BN * 64;                // one ring slot
+  constexpr int PI = HW_PROWS / 16 / NW;            // patch load instructions per wave, one per step
+  constexpr int BI = HW_BN / 16 / NW;               // ring load instructions per wave and step
+  static_assert(PI <= 5 && BI >= 1 && HW_PROWS % (16 * NW) == 0 && HW_BN % (16 * NW) == 0,
+                "patch pieces at steps 0..4, whole ring loads per wave");
+  __shared__ uint4 smem[(2 * BUF_P + HW_RING * SLOT_R) / 16];
+  static_assert(HW_BPC * (2 * BUF_P + HW_RING * SLOT_R) <= 163840, "LDS");
+  const ConvGather& g = h.g;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / HW_WGN, wn = wave % HW_WGN;
+  const uint32_t smem_lds = lds_addr(smem);
+  const int rowb = g.Cin * 2;                        // bytes per input pixel and per weight tap row
+  const int HC = g.Cin / 32;                         // channel halves (even)
+  const i32x4_t rsA = buffer_rsrc(g.A, (uint32_t)((long)g.N * g.Hin * g.Win * rowb));
+  const i32x4_t rsB = buffer_rsrc(g.B, (uint32_t)((long)g.Cols * g.KHW * rowb));
+  const int G = gridDim.x;
+  const int slot = xcd_remap(blockIdx.x, G);
+  const int NT = g.Cols / HW_BN;
+
+  // patch loads: instruction u of wave w covers patch pixels (w + 4 u) * 16 ..
+  // + 15; the lane's 16 bytes go to slot lane % 4 of pixel p and hold chunk
+  // (lane % 4) ^ ((p / 4) % 4)
+  int prel[PI], prow[PI];
+#pragma unroll
+  for (int u = 0; u < PI; ++u) {
+    const int p = (wave + NW * u) * 16 + (lane >> 2);
+    const int pr = p / h.PW, pc = p - pr * h.PW;
+    const int ir = -g.ip + g.dh0 + pr, ic = -g.ip + g.dw0 + pc;
+    const bool ok = p < h.PP && (unsigned)ic < (unsigned)g.Win;
+    prel[u] = (ir * g.Win + ic) * rowb + (((lane & 3) ^ ((p >> 2) & 3)) * 16);
+    prow[u] = ok ? ir : -0x40000000;
+  }
+  auto issue_patch = [&](int tile, int half, int buf, int u) {
+    const int mt = tile / NT;
+    const int n = mt / h.tiles_img, i0 = (mt - n * h.tiles_img) * h.TH;
+    const int base = (n * g.Hin + i0) * g.Win * rowb + half * 64;
+    const bool ok = (unsigned)(i0 + prow[u]) < (unsigned)g.Hin;
+    lds_dma16_buf(ok ? (uint32_t)(base + prel[u]) : kOutOfRange, rsA,
+                  smem_lds + (uint32_t)(buf * BUF_P + (wave + NW * u) * 1024));
+  };
+  // weight loads: instruction v of wave w covers tile columns (w + 4 v) * 16
+  // .. + 15, same slot layout. wlane[v]: the lane's column offset within the
+  // tile's first column (set per tile); a step adds a scalar offset.
+  const int colstride = g.KHW * rowb;                // bytes between weight columns
+  uint32_t wlane[BI];
+  auto issue_w = [&](int half, int t, int rs) {
+    const int th = t / 3, tw = t - th * 3;
+    const int wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
+    const uint32_t so = (uint32_t)(wt * rowb + half * 64);
+#pragma unroll
+    for (int v = 0; v < BI; ++v)
+      lds_dma16_buf(wlane[v] + so, rsB,
+                    smem_lds + (uint32_t)(2 * BUF_P + rs * SLOT_R + (wave + NW * v) * 1024));
+  };
+
+  const int kq = lane >> 4;
+  const int chl = 4 * (lane >> 4);
+  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) const u32x4_t* lds_u4_t;
+  // B operand rows of this lane in ring slot 0 (a slot or 16-column group is a
+  // constant element offset)
+  const int bcol = wn * WTN + (lane & 15);
+  const lds_u4_t bptr = (lds_u4_t)smem + (2 * BUF_P) / 16 + bcol * 4 + (kq ^ ((bcol >> 2) & 3));
+  const int v0 = wm * FM * 16 + (lane & 15);          // this lane's GEMM row in group 0
+  const uint32_t out_bytes = (uint32_t)((long)g.N * g.Hout * g.Wout * g.Cols * 2);
+  const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, out_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsR = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(g.mode == 1 || !g.R ? (const void*)g.C : g.R), 0, out_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsRm =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(g.Rm ? g.Rm : (const void*)g.C), 0, out_bytes, 0x00020000);
+  typedef int i32x2_t __attribute__((ext_vector_type(2)));
+
+  bool first = true;
+  if (slot < h.tiles) {
+#pragma unroll
+    for (int u = 0; u < PI; ++u) issue_patch(slot, 0, 0, u);
+  }
+  for (int tile = slot; tile < h.tiles; tile += G) {
+    const int mt = tile / NT, n0 = (tile % NT) * HW_BN;
+    const int n = mt / h.tiles_img, i0 = (mt - n * h.tiles_img) * h.TH;
+    const int rows_t = min(h.TH, g.Hm - i0);          // output rows of this tile
+    // A operand rows per tap (patch buffer 0, group 0): group i adds 16 rows
+    // (same swizzle), the buffer a constant
+    lds_u4_t atap[9];
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int p = v0 + (t / 3) * h.PW + t % 3;
+      atap[t] = (lds_u4_t)smem + p * 4 + (kq ^ ((p >> 2) & 3));
+    }
+#pragma unroll
+    for (int v = 0; v < BI; ++v) {
+      const int col = n0 + (wave + NW * v) * 16 + (lane >> 2);
+      wlane[v] = (uint32_t)(col * colstride + ((lane & 3) ^ ((col >> 2) & 3)) * 16);
+    }
+    floatx4_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+    // tile prologue: the ring slots are reloaded with the tile's first
+    // HW_RING - 1 steps once every wave is done with the previous tile's
+    // reads; the tile's first half-patch was issued before (block start or
+    // the previous tile's last half)
+    if (!first) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      barrier_only();
+    }
+    first = false;
+#pragma unroll
+    for (int q = 0; q < HW_RING - 1; ++q) issue_w(0, q, q);
+    wait_vmcnt<BI * (HW_RING - 2)>();
+    barrier_only();
+    const int next = tile + G < h.tiles ? tile + G : -1;
+    // operands of pair step k (half k / 9 of the pair, tap t = k % 9): patch
+    // buffer (k / 9) % 2 at tap offset t / 3 rows, t % 3 columns; ring slot
+    // k % HW_RING
+    auto read_step = [&](int k, uint4(&a)[FM], uint4(&b)[FN]) {
+      const int t = k % 9;
+      const int bo = ((k / 9) & 1) * (BUF_P / 16);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) a[i] = __builtin_bit_cast(uint4, atap[t][i * 64 + bo]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        b[j] = __builtin_bit_cast(uint4, bptr[(k % HW_RING) * (SLOT_R / 16) + j * 64]);
+    };
+    auto mma_step = [&](const uint4(&a)[FM], const uint4(&b)[FN]) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b[j], a[i], 0);
+    };
+    uint4 a0[FM], b0[FN], a1[FM], b1[FN];
+    read_step(0, a0, b0);
+    // pairs of halves: 18 steps, step k reads step k+1's operands (the next
+    // pair's first step at k = 17) into the other register set before its
+    // MFMAs. The next half-patch (or the next tile's first) goes out one
+    // piece per step at the first PI steps of a half.
+    for (int hp = 0; hp < HC; hp += 2) {
+      const bool more_pair = hp + 2 < HC;
+      const bool pn2 = more_pair || next >= 0;       // the pair's second half issues patch pieces
+#pragma unroll
+      for (int k = 0; k < 18; ++k) {
+        const int half = hp + k / 9, t = k % 9;
+        const bool more = k < 9 || more_pair;        // a half follows this one in the tile
+        const bool patch_next = more || next >= 0;
+        const bool last = !more_pair && k == 17;
+        if (!last) {
+          // the weights of step k+1 (issued HW_RING - 2 steps ago, or in the
+          // prologue) have landed; the weights and patch pieces issued after
+          // them may stay in flight. Vector memory operations complete in
+          // issue order.
+          {
+            // later weight steps: k+2 .. k+HW_RING-2 that exist in the tile
+            int later = HW_RING - 3;
+            if (!more_pair) later = min(later, 16 - k);
+            later *= BI;
+            // patch pieces from steps max(k - HW_RING + 2, tile start) .. k-1
+#pragma unroll
+            for (int d = 1; d <= HW_RING - 2; ++d) {
+              const int kp = k - d;
+              const int tp = ((kp % 9) + 9) % 9;
+              if (tp >= PI) continue;
+              if (kp < 0) {
+                if (hp > 0) later += 1;                 // previous pair's second half (more follows)
+              } else if (kp < 9) {
+                later += 1;                             // this pair's first half (more follows)
+              } else if (pn2) {
+                later += 1;
+              }
+            }
+            // before the next half's first read, its patch pieces (steps
+            // 0..PI-1 of this half) must have landed too
+            if (t == 8) later = min(later, BI * (8 - PI));
+            wait_vmcnt_dyn(later);
+          }
+          barrier_only();
+          // the weights of step k + HW_RING - 1 into the slot step k-1 used
+          {
+            const int kn = k + HW_RING - 1;
+            const int rs = kn % HW_RING;
+            if (kn < 18) issue_w(hp + kn / 9, kn % 9, rs);
+            else if (more_pair) issue_w(hp + 2, kn - 18, rs);
+          }
+          if (t < PI && patch_next) {
+            if (more) issue_patch(tile, half + 1, (half + 1) & 1, t);
+            else issue_patch(next, 0, 0, t);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if ((k & 1) == 0) {
+          read_step(k + 1, a1, b1);
+          __builtin_amdgcn_sched_barrier(0);
+          mma_step(a0, b0);
+        } else {
+          if (!last) read_step((k + 1) % 18, a0, b0);
+          __builtin_amdgcn_sched_barrier(0);
+          mma_step(a1, b1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+
+    // ---- epilogue straight from registers
+    const long m0 = ((long)n * g.Hm + i0) * g.Wm;
+    float s1[FN][4], s2[FN][4], sh[FN][4];
+    float cnt = 0.f;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s1[j][e] = s2[j][e] = sh[j][e] = 0.f;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int v = v0 + i * 16;
+      const int r = (int)h.fd_pw.div(v), c = v - r * h.PW;
+      const bool okq = r < rows_t && c < g.Wm;
+      const uint32_t ob = (uint32_t)((m0 + (okq ? r * g.Wm + c : 0)) * g.Cols) + n0 + wn * WTN + chl;
+      i32x2_t ld0[FN], ld1[FN];
+      if constexpr (MODE != 0) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const uint32_t o = okq ? (ob + j * 16) * 2 : kOutOfRange;
+          ld0[j] = __builtin_amdgcn_raw_buffer_load_b64(rsR, o, 0, 0);
+          if constexpr (MODE == 2) ld1[j] = __builtin_amdgcn_raw_buffer_load_b64(rsRm, o, 0, 0);
+        }
+      }
+      cnt += okq ? 1.f : 0.f;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        float x[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        if constexpr (MODE != 0) {
+          const uint32_t rw[2] = {(uint32_t)ld0[j].x, (uint32_t)ld0[j].y};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float rv = bf2f((bf16_t)(e & 1 ? rw[e >> 1] >> 16 : rw[e >> 1] & 0xffffu));
+            if constexpr (MODE == 2) {
+              const uint32_t mw = (uint32_t)(e >> 1 ? ld1[j].y : ld1[j].x);
+              x[e] += bf2f((bf16_t)(e & 1 ? mw >> 16 : mw & 0xffffu)) > 0.f ? rv : 0.f;
+            } else {
+              x[e] += rv;
+            }
+          }
+        }
+        const uint2 pk = make_uint2(f2bf2(x[0], x[1]), f2bf2(x[2], x[3]));
+        __builtin_amdgcn_raw_buffer_store_b64(i32x2_t{(int)pk.x, (int)pk.y}, rsC,
+                                              okq ? (ob + j * 16) * 2 : kOutOfRange, 0, 0);
+        if constexpr (STATS) {
+          const float vr[4] = {bf2f((bf16_t)(pk.x & 0xffffu)), bf2f((bf16_t)(pk.x >> 16)),
+                               bf2f((bf16_t)(pk.y & 0xffffu)), bf2f((bf16_t)(pk.y >> 16))};
+          if (i == 0) {
+            // the value of the wave's first GEMM row is its statistics shift
+            // (a conv output of the tile's data, valid or one of the dropped
+            // columns)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sh[j][e] = __shfl(vr[e], lane & 48, 64);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float d = okq ? vr[e] - sh[j][e] : 0.f;
+            s1[j][e] += d;
+            s2[j][e] = __builtin_fmaf(d, d, s2[j][e]);
+          }
+        }
+      }
+    }
+    if constexpr (STATS) {
+      // one entry per (tile, row wave) for this wave's 64 columns: the sums
+      // over the 16 rows of a lane group are shuffled together, then each
+      // lane writes one channel
+      const int kk = lane & 15, jj = kk >> 2, rr = kk & 3;
+      float o1 = 0.f, o2 = 0.f, osh = 0.f;
+#pragma unroll
+      for (int dd = 1; dd < 16; dd <<= 1) cnt += __shfl_xor(cnt, dd, 16);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float a1v = s1[j][r], a2v = s2[j][r];
+#pragma unroll
+          for (int dd = 1; dd < 16; dd <<= 1) {
+            a1v += __shfl_xor(a1v, dd, 16);
+            a2v += __shfl_xor(a2v, dd, 16);
+          }
+          if (j == jj && r == rr) { o1 = a1v; o2 = a2v; osh = sh[j][r]; }
+        }
+      if (jj < FN) {
+        float4* out = (float4*)g.stats + ((long)(mt * 2 + wm) * g.Cols + n0 + wn * WTN + jj * 16 + chl + rr);
+        *out = cnt > 0.f ? make_float4(cnt, osh, o1, o2) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  }
+  wait_vmcnt<0>();
+}
+
+// ---------------------------------------------------------------------------
 // Weight gradient
 // ---------------------------------------------------------------------------
 template <typename T> struct Tr;
@@ -2124,6 +2497,65 @@ int launch_halo(const ConvGather& g0, int th, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
+// Tile height of the streamed-weight halo kernel, or 0 when the launch is
+// not one it handles (bf16, 128..512 input channels in 64-channel blocks,
+// output columns in 128-column tiles, a 3x3 stride-1 tap walk, modes 0-2 with
+// statistics only in mode 0). Rows are balanced across an image's tiles;
+// tiles of fewer than 128 pixels (small images) are left to the gather kernel.
+int haloW_rows(int prec, const ConvGather& g) {
+  if (prec != PREC_BF16 || g.Cin % 64 != 0 || g.Cin < 128 || g.Cin > 512 || g.Cols % HW_BN != 0 || g.nth != 3 ||
+      g.ntw != 3 || g.KHW != 9 || g.K != 9 * g.Cin)
+    return 0;
+  if (g.is != 1 || g.os != 1 || g.oph != 0 || g.opw != 0 || g.dhs != 1 || g.dws != 1) return 0;
+  if (g.Hout != g.Hm || g.Wout != g.Wm || g.Hm < 1 || g.Wm < 1) return 0;
+  if (g.mode < 0 || g.mode > 2 || (g.mode != 0 && g.stats)) return 0;
+  if ((long)g.N * g.Hin * g.Win * g.Cin * 2 >= (1l << 31) || (long)g.N * g.Hout * g.Wout * g.Cols * 2 >= (1l << 31) ||
+      (long)g.Cols * g.KHW * g.Cin * 2 >= (1l << 31))
+    return 0;
+  // GEMM rows TH (W + 2) <= 224; every row's taps stay inside the patch
+  // buffer: 224 + 2 (W + 2) + 2 <= 320
+  const int pw = g.Wm + 2;
+  if (HW_ROWS + 2 * pw + 2 > HW_PROWS) return 0;
+  int thmax = HW_ROWS / pw;
+  if (thmax > g.Hm) thmax = g.Hm;
+  if (thmax < 1) return 0;
+  const int tiles_img = (g.Hm + thmax - 1) / thmax;
+  const int th = (g.Hm + tiles_img - 1) / tiles_img;
+  const int last = g.Hm - (tiles_img - 1) * th;
+  if (last * g.Wm < 96) return 0;
+  // two statistics entries per tile: at most one per 32 GEMM rows
+  if (g.stats && (long)g.N * tiles_img * 2 > ((long)g.M + 31) / 32) return 0;
+  return th;
+}
+
+int launch_haloW(const ConvGather& g0, int th, hipStream_t s) {
+  ConvHaloW h{};
+  h.g = g0;
+  h.g.fd_hw = FastDiv((uint32_t)(g0.Hm * g0.Wm));
+  h.g.fd_w = FastDiv((uint32_t)g0.Wm);
+  h.TH = th;
+  h.PW = g0.Wm + 2;
+  h.PP = (th + 2) * h.PW;
+  h.fd_pw = FastDiv((uint32_t)h.PW);
+  h.tiles_img = (g0.Hm + th - 1) / th;
+  h.tiles_m = g0.N * h.tiles_img;
+  h.tiles = h.tiles_m * (g0.Cols / HW_BN);
+  if (h.tiles <= 0) return 0;
+  if (h.PP > HW_PROWS || th * h.PW > HW_ROWS || HW_ROWS + 2 * h.PW + 2 > HW_PROWS) return -1;
+  const int cus = cu_count();
+  if (cus < 1) return -4;
+  const int slots = HW_BPC * cus;
+  const int grid = h.tiles < slots ? h.tiles : slots;
+  const bool st = g0.stats != nullptr;
+  constexpr int NT = 64 * HW_WAVES;
+  if (g0.mode == 0 && st) hipLaunchKernelGGL((conv_halo_wide_kernel<0, true>), dim3(grid), dim3(NT), 0, s, h);
+  else if (g0.mode == 0) hipLaunchKernelGGL((conv_halo_wide_kernel<0, false>), dim3(grid), dim3(NT), 0, s, h);
+  else if (g0.mode == 1 && !st) hipLaunchKernelGGL((conv_halo_wide_kernel<1, false>), dim3(grid), dim3(NT), 0, s, h);
+  else if (g0.mode == 2 && !st) hipLaunchKernelGGL((conv_halo_wide_kernel<2, false>), dim3(grid), dim3(NT), 0, s, h);
+  else return -1;
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
 // Kernel configurations: id -> (BM, BN, waves along M, waves along N, stages,
 // kind: 0 plain loop, 1 register-prefetched loop, 2 persistent).
 #define RN18_GATHER_CONFIGS(X)                                                                                  \
@@ -2166,10 +2598,17 @@ bool use_halo(int prec, const ConvGather& g) {
 bool use_halo16(int prec, const ConvGather& g) {
   return (g_gather_override == 0 || g_gather_override == kGatherHalo) && halo16_rows(prec, g) > 0;
 }
+// Measured on MI355X (bf16, batch 256, 28x28x128 and 14x14x256): within a
+// few percent of the 128x128 gather tile, so the automatic choice keeps the
+// gather kernel and this one runs when selected explicitly.
+bool use_haloW(int prec, const ConvGather& g) {
+  return g_gather_override == kGatherHalo && haloW_rows(prec, g) > 0;
+}
 
 int gather_tile(int prec, const ConvGather& g) {
   if (use_halo(prec, g)) return HALO_BM * 1000 + 64;
   if (use_halo16(prec, g)) return HALO16_BM * 1000 + 64;
+  if (use_haloW(prec, g)) return haloW_rows(prec, g) * (g.Wm + 2) * 1000 + HW_BN;
   const int id = gather_cfg(g);
   return id >= 1 && id <= kGatherCfgs ? kGather[id].bm * 1000 + kGather[id].bn : 0;
 }
@@ -2190,6 +2629,7 @@ int gather_dispatch(const ConvGather* g, int np, hipStream_t s) {
   const int prec = sizeof(T) == 2 ? PREC_BF16 : PREC_F32;
   if (np == 1 && use_halo(prec, g[0])) return launch_halo(g[0], halo_rows(prec, g[0]), s);
   if (np == 1 && use_halo16(prec, g[0])) return launch_halo16(g[0], halo16_rows(prec, g[0]), s);
+  if (np == 1 && use_haloW(prec, g[0])) return launch_haloW(g[0], haloW_rows(prec, g[0]), s);
   switch (gather_cfg_multi(g, np)) {
 #define RN18_X(id, bm, bn, wgm, wgn, st, kind)                                               \
   case id:                                                                                 \
@@ -2330,6 +2770,11 @@ const char* conv_gather_kernel_name(int prec, const ConvGather& g) {
     return intern_name(buf);
   }
   if (use_halo16(prec, g)) return g.stats ? "conv_halo16_kernel<true>" : "conv_halo16_kernel<false>";
+  if (use_haloW(prec, g)) {
+    char buf[64];
+    snprintf(buf, sizeof buf, "conv_halo_wide_kernel<%d, %s>", g.mode, g.stats ? "true" : "false");
+    return intern_name(buf);
+  }
   return gather_kernel_name(prec, g, gather_cfg(g));
 }
 
@@ -2392,6 +2837,10 @@ int conv_gather_stat_entries(int prec, const ConvGather& g) {
     const int th = halo16_rows(prec, g);
     const int tiles = g.N * ((g.Hm + th - 1) / th), slots = 2 * cu_count();
     return (tiles < slots ? tiles : slots) * HALO16_WAVES;
+  }
+  if (use_haloW(prec, g)) {
+    const int th = haloW_rows(prec, g);
+    return g.N * ((g.Hm + th - 1) / th) * 2;
   }
   const int bm = gather_tile(prec, g) / 1000;
   return bm > 0 ? ceil_div(g.M, bm) : 0;

@@ -202,6 +202,25 @@ def test_conv_halo(case):
         B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 0)
 
 
+@pytest.mark.parametrize("case", [(2, 128, 128, 28, 28, 128, 3, 1, 1), (2, 256, 256, 14, 14, 256, 3, 1, 1),
+                                  (3, 128, 128, 13, 11, 256, 3, 1, 1), (1, 192, 192, 20, 30, 128, 3, 1, 1),
+                                  (2, 128, 128, 9, 50, 128, 3, 1, 1), (1, 512, 512, 12, 12, 128, 3, 1, 1)],
+                         ids=case_id)
+def test_conv_halo_wide(case):
+    """The streamed-weight halo kernel (3x3 stride-1 bf16 convs with 128..512
+    input channels and 128-column output tiles):
+    forward and data gradient against the oracle, with one and two tiles per
+    image, both pixel-wave depths, ragged widths, three and sixteen channel
+    halves per block, and shapes whose data gradient falls back to the gather
+    kernel (selected with the halo configuration)."""
+    try:
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 45)
+        test_conv_fwd("bf16", case)
+        test_conv_dgrad("bf16", case)
+    finally:
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 0)
+
+
 def test_bf16_storage_rounding_matches_oracle():
     """The kernels' fp32 -> bf16 storage rounding (hardware conversion) is
     bit-identical to the oracle's round-to-nearest-even on the binary32

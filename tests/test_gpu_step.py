@@ -76,6 +76,18 @@ def test_imagenet_bf16_resolutions(N, H):
     _run_parity("imagenet", 1000, "bf16", N, H, seed=110 + H)
 
 
+def test_imagenet_bf16_halo_configuration():
+    """The step with every convolution the halo kernels handle routed to them
+    (gather configuration 45): the streamed-weight halo kernel then runs the
+    stage-2 and stage-3 3x3 convolutions, forward with the BN statistics
+    epilogue and data gradients with the masked-residual epilogue."""
+    try:
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 45)
+        _run_parity("imagenet", 1000, "bf16", 2, 224, seed=131)
+    finally:
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 0)
+
+
 def test_imagenet_fp32_small():
     """All op types (7x7 s2 stem, max pool, projections) in fp32 at 1e-3."""
     _run_parity("imagenet", 1000, "fp32", 3, 64, seed=120)
