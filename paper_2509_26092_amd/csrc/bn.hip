@@ -188,9 +188,10 @@ __global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict
   __shared__ float red[2][256 * VW];
   const int tpc = C / VW, rpi = 256 / tpc;
   const int tid = threadIdx.x, cg = tid % tpc, rr = tid / tpc;
-  const long rows_per_blk = (M + gridDim.x - 1) / gridDim.x;
-  const long r_begin = blockIdx.x * rows_per_blk;
-  const long r_end = min(M, r_begin + rows_per_blk);
+  // the grid sweeps the rows together: at each step block b takes rows
+  // (step * G + b) * rpi .. + rpi - 1, so the whole grid reads one contiguous
+  // stretch of each tensor at a time
+  const long gstride = (long)gridDim.x * rpi;
   float mu[VW], rs[VW], s1[VW], s2[VW], msc[VW], msf[VW];
 #pragma unroll
   for (int e = 0; e < VW; ++e) {
@@ -201,13 +202,13 @@ __global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict
     s1[e] = s2[e] = 0.f;
   }
   // four rows per step, all loads issued before any is used (rows past the
-  // range load the thread's first row and add nothing)
+  // end load the thread's first row of the step and add nothing)
   constexpr int U = 4;
-  for (long r0 = r_begin + rr; r0 < r_end; r0 += U * rpi) {
+  for (long r0 = (long)blockIdx.x * rpi + rr; r0 < M; r0 += U * gstride) {
     uint4 qg[U], qy[U], qm[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const long r = r0 + u * rpi < r_end ? r0 + u * rpi : r0;
+      const long r = r0 + u * gstride < M ? r0 + u * gstride : r0;
       const long o = r * C + cg * VW;
       qg[u] = *(const uint4*)(dz + o);
       qy[u] = *(const uint4*)(y + o);
@@ -215,7 +216,7 @@ __global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const bool live_row = r0 + u * rpi < r_end;
+      const bool live_row = r0 + u * gstride < M;
       float g[VW], yy[VW];
       unpack<T>(qg[u], g);
       unpack<T>(qy[u], yy);
