@@ -142,6 +142,21 @@ int rn18_sync_status(rn18_ctx* ctx);
 int rn18_get_momentum(rn18_ctx* ctx, float* dst);
 int rn18_set_momentum(rn18_ctx* ctx, const float* src);
 
+/* Dropout on the classifier input during training steps (the adaptive
+ * regularisation of Sec. 4.1, whose rates 0.1-0.3 rise with the resolution;
+ * the paper does not place the dropout, this library puts it before the
+ * fully connected layer). p in [0, 1); p = 0 (the default) turns it off.
+ * Feature j of sample n is kept in a training step with counter t iff
+ *   (x >> 8) >= floor(p * 2^24),  x = word (nF + j) mod 4 of
+ *   Philox4x32-10 (Salmon et al., SC'11) with key (seed mod 2^32,
+ *   seed div 2^32) and counter (q mod 2^32, q div 2^32, t mod 2^32,
+ *   t div 2^32), q = (nF + j) div 4, F the feature width;
+ * kept features are multiplied by (float)(1 / (1 - p)) and the backward pass
+ * applies the same mask. t starts at `step` and advances by one with every
+ * successful rn18_train_step (whether or not dropout is on); evaluation never
+ * drops. RN18_EINVAL for a NULL ctx or p outside [0, 1). */
+int rn18_set_dropout(rn18_ctx* ctx, float p, uint64_t seed, uint64_t step);
+
 /* Synchronise and free everything the context allocated. */
 void rn18_destroy(rn18_ctx* ctx);
 

@@ -18,6 +18,7 @@ Modules
            eval forward
   merge    parameter-server merge with the model-update factor (Sec. 3.4)
            and the dual-batch planner arithmetic (Eqs. 2-8)
+  philox   Philox4x32-10 and the dropout masks drawn from it
 
 Parity status: every function is pinned by a ``-m "not gpu"`` test against
 something other than itself (dense-matrix brute force, finite differences,

@@ -25,7 +25,7 @@ Flat state (float32 on the device, float64 here), in this order:
 """
 import numpy as np
 
-from . import ops
+from . import ops, philox
 
 ARCHS = ("tiny", "cifar", "imagenet")
 
@@ -110,7 +110,7 @@ def init_state(layout, seed):
 
 class Config:
     def __init__(self, arch, num_classes, bf16=False, momentum=0.9, weight_decay=5e-4,
-                 bn_eps=1e-5, bn_momentum=0.1, round_acts=False):
+                 bn_eps=1e-5, bn_momentum=0.1, round_acts=False, dropout=0.0, dropout_seed=0, dropout_step=0):
         self.arch = arch
         self.num_classes = num_classes
         self.bf16 = bf16
@@ -122,6 +122,12 @@ class Config:
         # activation gradient to bf16 at the points where a bf16 training
         # step stores them (see ROUNDING_POINTS). Off by default.
         self.round_acts = round_acts
+        # dropout before the classifier in training-mode passes (the paper's
+        # adaptive regularisation, Sec. 4.1): rate, generator key and the
+        # training step whose mask is used (see philox.py); 0 = off
+        self.dropout = dropout
+        self.dropout_seed = dropout_seed
+        self.dropout_step = dropout_step
 
 
 # Where a bf16 training step stores a tensor in bf16 (rounded once, RNE):
@@ -221,6 +227,13 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
         a = relu_site(("out", bi), b2 + sc)
         block_io.append((inp, z1, a))
     f = ops.avgpool_forward(a)
+    drop = None
+    if train and cfg.dropout > 0.0:
+        # inverted dropout on the classifier input: kept features scaled by
+        # 1 / (1 - p), so the expected input is unchanged
+        _, scale = philox.dropout_params(cfg.dropout)
+        drop = philox.dropout_keep(cfg.dropout_seed, cfg.dropout_step, f.shape[0], f.shape[1], cfg.dropout) * scale
+        f = f * drop
     wfc = layout.get(state, "fc.w")
     bfc = layout.get(state, "fc.b")
     logits = ops.fc_forward(f, wfc, bfc)
@@ -230,6 +243,8 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
 
     grad = np.zeros(layout.n_trainable)
     df, dwfc, dbfc = ops.fc_backward(dz, f, wfc)
+    if drop is not None:
+        df = df * drop
     layout.put(grad, "fc.w", dwfc)
     layout.put(grad, "fc.b", dbfc)
     da = rb(("da_avg", 0), ops.avgpool_backward(df, a.shape))

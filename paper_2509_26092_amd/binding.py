@@ -22,7 +22,8 @@ PREC_IDS = {"fp32": RN18_FP32, "bf16": RN18_BF16}
 EXPORTED = [
     "rn18_state_floats", "rn18_init", "rn18_workspace_bytes", "rn18_set_workspace", "rn18_train_step",
     "rn18_eval_logits", "ps_dual_merge", "ps_worker_delta", "rn18_sync_status", "rn18_get_momentum",
-    "rn18_set_momentum", "rn18_destroy", "rn18_last_error", "rn18_profile_enable", "rn18_profile_read",
+    "rn18_set_momentum", "rn18_set_dropout", "rn18_destroy", "rn18_last_error", "rn18_profile_enable",
+    "rn18_profile_read",
     "rn18op_conv2d_fwd", "rn18op_conv2d_dgrad", "rn18op_conv2d_wgrad_workspace", "rn18op_conv2d_wgrad",
     "rn18op_maxpool_fwd", "rn18op_maxpool_bwd", "rn18_debug_set", "rn18_debug_copy",
     "rn18_debug_capture", "rn18op_round_bf16",
@@ -78,6 +79,7 @@ def lib():
         "rn18_sync_status": (_I, [_P]),
         "rn18_get_momentum": (_I, [_P, _P]),
         "rn18_set_momentum": (_I, [_P, _P]),
+        "rn18_set_dropout": (_I, [_P, _F, ctypes.c_uint64, ctypes.c_uint64]),
         "rn18_destroy": (None, [_P]),
         "rn18_last_error": (ctypes.c_char_p, []),
         "rn18op_conv2d_fwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P]),
@@ -164,6 +166,10 @@ def ps_worker_delta(pulled, local, delta, n, stream=None):
 
 def rn18_sync_status(ctx):
     return lib().rn18_sync_status(ctx)
+
+
+def rn18_set_dropout(ctx, p, seed, step):
+    return _check(lib().rn18_set_dropout(ctx, ctypes.c_float(p), ctypes.c_uint64(seed), ctypes.c_uint64(step)))
 
 
 def rn18_get_momentum(ctx, dst):

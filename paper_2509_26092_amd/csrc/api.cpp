@@ -175,6 +175,13 @@ struct Ctx {
   RepackEntry* tab = nullptr;
   int ntab = 0;
   unsigned* err = nullptr;
+  // dropout before the classifier: on iff the rate is > 0, keep threshold,
+  // scale, and the
+  // Philox key and step counter of the next training step
+  bool drop_on = false;
+  uint32_t drop_thresh = 0;
+  float drop_scale = 1.f;
+  uint64_t drop_seed = 0, drop_step = 0;
   void* ws = nullptr;
   size_t ws_bytes = 0;
   bool ws_owned = false;
@@ -615,6 +622,10 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   float* grad = (float*)(ws + pl.grad);
   const double fcf = 2.0 * N * C * F;
   float* hpart = (float*)(ws + pl.wpart);
+  const bool drop = c->drop_on;
+  if (drop)
+    TIMED(RN18_K_HEAD, 5, 0, "dropout_kernel", 0.0, 8.0 * N * F,
+          dropout_launch(f, (long)N * F, c->drop_seed, c->drop_step, c->drop_thresh, c->drop_scale, st));
   TIMED(RN18_K_HEAD, 0, 0, "gemm_f32_kernel", fcf, 0.0, gemm_f32_launch(f, F, 1, state + a.fc_w, 1, F, state + a.fc_b, logits, N, C, F, hpart, st));
   TIMED(RN18_K_HEAD, 1, 0, "softmax_ce_kernel", 0.0, 8.0 * N * C,
         softmax_ce_launch(logits, labels, N, C, dlog, (float*)(ws + pl.rowloss),
@@ -623,6 +634,9 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   TIMED(RN18_K_HEAD, 2, 0, "gemm_f32_kernel", fcf, 0.0, gemm_f32_launch(dlog, 1, C, f, F, 1, nullptr, grad + a.fc_w, C, F, N, hpart, st));
   TIMED(RN18_K_HEAD, 3, 0, "colsum_kernel", 0.0, 4.0 * N * C, colsum_launch(dlog, N, C, grad + a.fc_b, st));
   TIMED(RN18_K_HEAD, 4, 0, "gemm_f32_kernel", fcf, 0.0, gemm_f32_launch(dlog, C, 1, state + a.fc_w, F, 1, nullptr, df, N, F, C, hpart, st));
+  if (drop)  // the same mask on the classifier-input gradient
+    TIMED(RN18_K_HEAD, 6, 0, "dropout_kernel", 0.0, 8.0 * N * F,
+          dropout_launch(df, (long)N * F, c->drop_seed, c->drop_step, c->drop_thresh, c->drop_scale, st));
   size_t gA = pl.gA, gB = pl.gB;
   const size_t es = c->es;
   TIMED(RN18_K_AVGPOOL, 1, 0, kernel_instance_name("avgpool_bwd_kernel", prec), 0.0, (double)N * F * ((double)pl.Hf * pl.Wf * es + 4),
@@ -892,7 +906,21 @@ int rn18_train_step(rn18_ctx* h, float* state, const float* images, const int32_
   int r = get_plan(&c, N, H, W, &pl);
   if (r) return r;
   if ((r = ensure_ws(&c, *pl))) return r;
-  return run_train(&c, *pl, state, images, labels, lr, loss);
+  if ((r = run_train(&c, *pl, state, images, labels, lr, loss))) return r;
+  ++c.drop_step;
+  return RN18_OK;
+}
+
+int rn18_set_dropout(rn18_ctx* h, float p, uint64_t seed, uint64_t step) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  if (!(p >= 0.f && p < 1.f)) return fail(RN18_EINVAL, "dropout rate must be in [0, 1)");
+  Ctx& c = h->c;
+  c.drop_on = p > 0.f;
+  c.drop_thresh = (uint32_t)floor((double)p * 16777216.0);
+  c.drop_scale = (float)(1.0 / (1.0 - (double)p));
+  c.drop_seed = seed;
+  c.drop_step = step;
+  return RN18_OK;
 }
 
 int rn18_eval_logits(rn18_ctx* h, const float* state, const float* images, int N, int H, int W, float* logits) {

@@ -157,6 +157,10 @@ int gemm_f32_launch(const float* A, long sam, long sak, const float* B, long sbk
 int colsum_launch(const float* A, int M, int N, float* out, hipStream_t s);
 int softmax_ce_launch(const float* z, const int32_t* labels, int N, int C, float* dz, float* row_loss,
                       float* loss, unsigned* err, hipStream_t s);
+// In-place dropout of n (a multiple of 4) fp32 values with the Philox4x32-10
+// mask of (seed, step) and keep threshold thresh (top 24 bits of a word),
+// kept values multiplied by scale.
+int dropout_launch(float* x, long n, uint64_t seed, uint64_t step, uint32_t thresh, float scale, hipStream_t s);
 int sgd_launch(float* w, const float* g, float* v, long n, float lr, float mom, float wd, hipStream_t s);
 int merge_launch(float* p, const float* ds, const float* dl, long n, float f, hipStream_t s);
 int delta_launch(const float* pulled, const float* local, float* delta, long n, hipStream_t s);

@@ -88,6 +88,49 @@ __global__ void repack_kernel(const float* __restrict__ st, T* __restrict__ wf, 
   }
 }
 
+// ------------------------------------------------------------------ dropout
+// Philox4x32-10 (Salmon et al., SC'11): ten rounds of two 32x32 -> 64-bit
+// products mixed with the other counter words and the key, the key bumped by
+// the Weyl constants between rounds.
+__device__ inline void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c[0], p1 = (uint64_t)0xCD9E8D57u * c[2];
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k0, n2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = (uint32_t)p1;
+    c[2] = n2;
+    c[3] = (uint32_t)p0;
+  }
+}
+
+// In-place dropout of n fp32 values, four per counter: group q draws one
+// Philox output (counter (q, step), key seed); value 4q + w is kept iff the
+// top 24 bits of word w are >= thresh, and kept values are scaled. A ragged
+// last group (n not a multiple of 4) uses the leading words of its output.
+__global__ void dropout_kernel(float* __restrict__ x, long n, uint32_t k0, uint32_t k1, uint32_t s0, uint32_t s1,
+                               uint32_t thresh, float scale) {
+  const long n4 = (n + 3) / 4;
+  for (long q = blockIdx.x * (long)blockDim.x + threadIdx.x; q < n4; q += (long)gridDim.x * blockDim.x) {
+    uint32_t c[4] = {(uint32_t)q, (uint32_t)(q >> 32), s0, s1};
+    philox4x32_10(c, k0, k1);
+    if (4 * q + 4 <= n) {
+      float4 v = ((float4*)x)[q];
+      v.x = (c[0] >> 8) >= thresh ? v.x * scale : 0.f;
+      v.y = (c[1] >> 8) >= thresh ? v.y * scale : 0.f;
+      v.z = (c[2] >> 8) >= thresh ? v.z * scale : 0.f;
+      v.w = (c[3] >> 8) >= thresh ? v.w * scale : 0.f;
+      ((float4*)x)[q] = v;
+    } else {
+      for (int w = 0; w < 4 && 4 * q + w < n; ++w) x[4 * q + w] = (c[w] >> 8) >= thresh ? x[4 * q + w] * scale : 0.f;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ max pool 3x3 s2 p1
 template <typename T>
 __global__ void maxpool_fwd_kernel(const T* __restrict__ x, T* __restrict__ y, uint8_t* __restrict__ arg, int N,
@@ -490,6 +533,17 @@ int softmax_ce_launch(const float* z, const int32_t* labels, int N, int C, float
   hipLaunchKernelGGL(softmax_ce_kernel, dim3(N), dim3(256), 0, s, z, labels, N, C, dz, row_loss, err);
   hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, row_loss, N, loss, err);
   return ok();
+}
+
+int dropout_launch(float* x, long n, uint64_t seed, uint64_t step, uint32_t thresh, float scale, hipStream_t s) {
+  if (n < 0 || ((uintptr_t)x & 15)) return -1;
+  const long n4 = (n + 3) / 4;
+  if (n4 == 0) return 0;
+  long blocks = (n4 + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(dropout_kernel, dim3(blocks), dim3(256), 0, s, x, n, (uint32_t)seed, (uint32_t)(seed >> 32),
+                     (uint32_t)step, (uint32_t)(step >> 32), thresh, scale);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
 int sgd_launch(float* w, const float* g, float* v, long n, float lr, float mom, float wd, hipStream_t s) {

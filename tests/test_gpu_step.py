@@ -23,20 +23,25 @@ pytestmark = pytest.mark.gpu
 LR = 0.1
 
 
-def _run_parity(arch, classes, prec, N, H, seed, lr=LR):
+def _run_parity(arch, classes, prec, N, H, seed, lr=LR, dropout=None):
     """One step on both sides. The oracle takes the kernel's choice only at
     non-unique points inside the rounding band (ReLU kinks, pool ties and,
     for bf16, rounding midpoints of the stored tensors; see gpu_util), and
-    every kernel decision outside the band must agree with the oracle's."""
+    every kernel decision outside the band must agree with the oracle's.
+    dropout: (rate, seed, step) of the classifier-input dropout on both."""
     L, st = make_state(arch, classes, seed)
     x = inputs.images(seed, N, H, H)
     y = inputs.labels(seed, N, classes)
     w = B.Worker(arch, classes, prec)
+    drop = {}
+    if dropout is not None:
+        B.rn18_set_dropout(w.ctx, *dropout)
+        drop = dict(dropout=dropout[0], dropout_seed=dropout[1], dropout_step=dropout[2])
     bf = prec == "bf16"
     dec = Mirror(w, L, N, H, prec, TAU["fp32"]) if bf else Decider(w, N, H, prec, TAU[prec])
     gs, gv, losses, status = gpu_train_step(arch, classes, prec, st, x, y, lr, worker=w)
     assert status == B.RN18_OK
-    cfg = net.Config(arch, classes, bf16=bf, round_acts=bf)
+    cfg = net.Config(arch, classes, bf16=bf, round_acts=bf, **drop)
     try:
         report, loss = compare_step(L, cfg, st, x, y, lr, gs, gv, losses[0], TOL[prec], decide=dec)
     finally:
@@ -113,6 +118,58 @@ def test_two_steps_with_momentum():
     assert abs(losses[1] - l2) <= 1e-3 * abs(l2)
     assert_close(gs, s2, 1e-3, "state after 2 steps")
     assert_close(gv, v2, 1e-3, "momentum after 2 steps")
+
+
+@pytest.mark.parametrize("arch,classes,prec,N,H,p", [("tiny", 10, "fp32", 8, 16, 0.3), ("cifar", 100, "fp32", 4, 32, 0.1),
+                                                     ("imagenet", 1000, "bf16", 3, 64, 0.2)])
+def test_dropout_step(arch, classes, prec, N, H, p):
+    """Classifier-input dropout (the paper's adaptive regularisation rates):
+    the step against the oracle drawing the same Philox4x32-10 mask, with a
+    64-bit key and a step counter above 2^32."""
+    _run_parity(arch, classes, prec, N, H, seed=140 + H, dropout=(p, 0x0123456789ABCDEF, 2 ** 32 + 7))
+
+
+def test_dropout_counter_advances_per_step():
+    """Two steps draw the masks of steps t and t + 1; rate 0 leaves the step
+    unchanged."""
+    arch, classes, prec, N, H, seed = "tiny", 10, "fp32", 8, 16, 150
+    L, st = make_state(arch, classes, seed)
+    x = inputs.images(seed, N, H, H)
+    y = inputs.labels(seed, N, classes)
+    w = B.Worker(arch, classes, prec)
+    try:
+        B.rn18_set_dropout(w.ctx, 0.3, 77, 10)
+        gs, gv, losses, _ = gpu_train_step(arch, classes, prec, st, x, y, LR, steps=2, worker=w)
+    finally:
+        w.close()
+    v0 = np.zeros(L.n_trainable)
+    s1, v1, _, _ = net.train_step(net.Config(arch, classes, dropout=0.3, dropout_seed=77, dropout_step=10),
+                                  L, st, v0, x, y, LR)
+    s2, v2, l2, _ = net.train_step(net.Config(arch, classes, dropout=0.3, dropout_seed=77, dropout_step=11),
+                                   L, s1, v1, x, y, LR)
+    from gpu_util import assert_close
+    assert abs(losses[1] - l2) <= 1e-3 * abs(l2)
+    assert_close(gs, s2, 1e-3, "state after 2 dropout steps")
+    assert_close(gv, v2, 1e-3, "momentum after 2 dropout steps")
+    w = B.Worker(arch, classes, prec)
+    try:
+        B.rn18_set_dropout(w.ctx, 0.0, 77, 10)
+        g0, _, l0, _ = gpu_train_step(arch, classes, prec, st, x, y, LR, worker=w)
+    finally:
+        w.close()
+    s_ref, _, l_ref, _ = net.train_step(net.Config(arch, classes), L, st, v0, x, y, LR)
+    assert abs(l0[0] - l_ref) <= 1e-3 * abs(l_ref)
+    assert_close(g0, s_ref, 1e-3, "state, dropout rate 0")
+
+
+def test_dropout_rejects_bad_rates():
+    w = B.Worker("tiny", 10, "fp32")
+    try:
+        for bad in (-0.1, 1.0, float("nan")):
+            with pytest.raises(B.Rn18Error):
+                B.rn18_set_dropout(w.ctx, bad, 1, 0)
+    finally:
+        w.close()
 
 
 def test_eval_logits_parity():

@@ -61,6 +61,27 @@ def test_fd_tiny_config():
     _directional_check(cfg, layout, state, x, y, keys, rng)
 
 
+def test_fd_tiny_config_with_dropout():
+    """Dropout before the classifier (a fixed mask for the given step): the
+    gradient still matches finite differences of the training loss, the mask
+    changes the loss, and evaluation ignores it."""
+    rng = np.random.default_rng(12)
+    layout = net.Layout("tiny", 10)
+    cfg = net.Config("tiny", 10, dropout=0.3, dropout_seed=99, dropout_step=4)
+    state = net.init_state(layout, 2)
+    state[:layout.n_trainable] += 0.05 * rng.standard_normal(layout.n_trainable)
+    x = rng.standard_normal((8, 3, 16, 16))
+    y = rng.integers(0, 10, 8)
+    _directional_check(cfg, layout, state, x, y, ["s1b1c2.w", "s1b1c2.g", "fc.w", "fc.b"], rng)
+    plain = net.Config("tiny", 10)
+    assert abs(net.loss_only(cfg, layout, state, x, y) - net.loss_only(plain, layout, state, x, y)) > 1e-6
+    np.testing.assert_array_equal(net.eval_logits(cfg, layout, state, x), net.eval_logits(plain, layout, state, x))
+    # the FC input gradient is zero exactly where the mask drops a feature
+    _, _, g, _ = net.forward_backward(cfg, layout, state, x, y)
+    keep = net.philox.dropout_keep(99, 4, 8, layout.feat, 0.3)
+    assert 0 < keep.sum() < keep.size
+
+
 def test_fd_imagenet_shaped_small():
     rng = np.random.default_rng(12)
     layout = net.Layout("imagenet", 7)
