@@ -205,6 +205,11 @@ def counters_summary(csv_path, title, command):
     return "\n".join(lines) + "\n"
 
 
+def progress(msg):
+    """A progress line on stderr (the JSON result alone goes to stdout)."""
+    print("bench: " + msg, file=sys.stderr, flush=True)
+
+
 def run_shape(B, torch, inputs, arch, classes, prec, N, H, steps, warmup, seed=1, dropout=0.0):
     w = B.Worker(arch, classes, prec)
     if dropout:
@@ -284,6 +289,37 @@ def dbl_plan(B, torch, inputs, by, merge_ms, steps):
             "stages": out}
 
 
+def memory_model(B, torch):
+    """Sec. 5.3: device memory of steps at B = 64..512 (hipMemGetInfo), the
+    Eq. 9 fit, the largest batch for this GPU's memory, the library's own
+    bound from its 32-bit tensor addressing, and the model checked against a
+    measured step at the smaller of the two."""
+    from paper_2509_26092_amd import memory as Mm
+    _, m_gpu = torch.cuda.mem_get_info()
+    out = []
+    for wl, arch, classes, prec, H in (("cifar100_fp32_32", "cifar", 100, "fp32", 32),
+                                       ("imagenet_bf16_224", "imagenet", 1000, "bf16", 224)):
+        bs = [64, 128, 192, 256, 320, 384, 448, 512]
+        ms = Mm.profile(B, torch, arch, classes, prec, H, bs)
+        p, a = Mm.fit(bs, ms)
+        b_mem = Mm.max_batch(p, a, m_gpu)
+        w = B.Worker(arch, classes, prec)
+        b_addr = Mm.addressing_max_batch(B, w.ctx, H, H)
+        w.close()
+        b_v = min(b_mem, b_addr)
+        used, status = Mm.measure_step(B, torch, arch, classes, prec, b_v, H)
+        pred = Mm.predict(p, a, b_v)
+        progress("memory model %s: B_max %d (memory) / %d (addressing), error %.4f at B=%d"
+                 % (wl, b_mem, b_addr, abs(pred - used) / used, b_v))
+        out.append({"workload": wl, "fit_batches": bs, "measured_GB": [round(m / 1e9, 3) for m in ms],
+                    "sum_p_GB": round(p / 1e9, 4), "sum_a_MB_per_image": round(a / 1e6, 4),
+                    "M_GPU_GB": round(m_gpu / 1e9, 2), "B_max_memory": b_mem, "B_max_addressing": b_addr,
+                    "verified_at": b_v, "measured_at_verified_GB": round(used / 1e9, 3),
+                    "predicted_at_verified_GB": round(pred / 1e9, 3),
+                    "relative_error": round(abs(pred - used) / used, 5), "status": status})
+    return {"workload": "memory_model_eq9", "configs": out}
+
+
 def cpu_baseline(arch, classes, prec, H, n_img, seed=3):
     """The fp64 oracle's training step, timed on the host cores on a bounded
     sample of the workload (n_img images at the workload's resolution)."""
@@ -359,6 +395,7 @@ def main():
     if not args.headline_only:
         for sname, sarch, scls, sprec, sN, sH in SHAPES:
             sdt, srecs, sstatus, _ = run_shape(B, torch, inputs, sarch, scls, sprec, sN, sH, args.shape_steps, 2)
+            progress("%s: %.3f ms/step" % (sname, sdt * 1e3))
             ssum, _ = summarize(srecs, sprec)
             per_shape.append({"workload": sname, "batch": sN, "resolution": sH, "dtype": sprec,
                               "images_per_s": round(sN / sdt, 1), "ms_per_step": round(sdt * 1e3, 3),
@@ -384,6 +421,7 @@ def main():
                           "ms": round(mms, 4), "GBps": round(mgbs, 1), "hbm_frac": round(mgbs / HBM_PEAK, 4),
                           "hybrid_rounds": rounds})
         per_shape.append(dbl_plan(B, torch, inputs, by, mms, args.shape_steps))
+        per_shape.append(memory_model(B, torch))
 
     if args.calibrate:
         n = CALIB_FLOATS

@@ -10,7 +10,8 @@
  * RN18_FP32 (float elements) or RN18_BF16 (bf16 elements as uint16 bit
  * patterns); activations are NHWC; channel counts of activation tensors must
  * be multiples of 4 (fp32) or 8 (bf16). Work is enqueued on `hip_stream`.
- * Invalid arguments return RN18_EINVAL before any launch.
+ * Invalid arguments return RN18_EINVAL before any launch, among them any
+ * tensor of more than 2^31 - 2^24 bytes (32-bit byte offsets in the kernels).
  */
 #ifndef RN18_OPS_H
 #define RN18_OPS_H

@@ -10,6 +10,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <map>
 #include <string>
 #include <tuple>
@@ -50,6 +51,13 @@ int fail(int code, const char* fmt, ...) {
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 inline int out_size(int h, int k, int s, int p) { return (h + 2 * p - k) / s + 1; }
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// The kernels address each tensor with 32-bit byte offsets: buffer resources
+// sized to the tensor, an out-of-range sentinel of 2^31, and unsigned offset
+// arithmetic that may run a tile (< 1 MiB) past the end. Every tensor a step
+// or an operator touches is therefore kept below 2^31 bytes minus a 16 MiB
+// margin; larger shapes are rejected when they are planned.
+constexpr size_t kMaxTensorBytes = ((size_t)1 << 31) - ((size_t)1 << 24);
 
 // ----------------------------------------------------------------------------
 // Architecture
@@ -242,8 +250,13 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   if (N < 1 || H < 1 || W < 1) { *why = "N, H and W must be >= 1"; return RN18_EINVAL; }
   if ((long)N * H * W > (1l << 31) / 8) { *why = "input too large"; return RN18_EINVAL; }
   pl->N = N; pl->H = H; pl->W = W;
-  size_t off = 0;
-  auto alloc = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  size_t off = 0, max_tensor = (size_t)N * 3 * H * W * 4;  // the caller's NCHW fp32 images
+  auto alloc = [&](size_t bytes) {
+    if (bytes > max_tensor) max_tensor = bytes;
+    size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
   auto act = [&](int h, int w, int ch) { return alloc((size_t)N * h * w * ch * es); };
   pl->cp.assign(a.convs.size(), ConvP{});
   pl->bp.assign(a.blocks.size(), BlockP{});
@@ -368,6 +381,12 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   pl->wpart = alloc(max_wpart);
   pl->grad = alloc((size_t)a.P * 4);
   pl->total = off;
+  if (max_tensor > kMaxTensorBytes) {
+    snprintf(buf, sizeof buf, "a %zu-byte tensor exceeds the kernels' per-tensor limit of %zu bytes", max_tensor,
+             kMaxTensorBytes);
+    *why = buf;
+    return RN18_EINVAL;
+  }
   return RN18_OK;
 }
 
@@ -1123,7 +1142,10 @@ static int op_check(int prec, int N, int H, int W, int Cin, int Cout, int k, int
   *Ho = out_size(H, k, s, p);
   *Wo = out_size(W, k, s, p);
   if (*Ho < 1 || *Wo < 1) return fail(RN18_EINVAL, "empty output");
-  if ((long)N * H * W * (Cin > Cout ? Cin : Cout) >= (1l << 31)) return fail(RN18_EINVAL, "tensor too large");
+  const size_t es = prec == RN18_BF16 ? 2 : 4;
+  const size_t pix = std::max((size_t)H * W, (size_t)*Ho * *Wo), ch = std::max(Cin, Cout);
+  if ((size_t)N * pix * ch * es > kMaxTensorBytes || (size_t)Cout * k * k * Cin * es > kMaxTensorBytes)
+    return fail(RN18_EINVAL, "tensor larger than the kernels' per-tensor limit of %zu bytes", kMaxTensorBytes);
   return RN18_OK;
 }
 

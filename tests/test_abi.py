@@ -49,3 +49,18 @@ def test_invalid_config_rejected():
         pytest.skip("library not built")
     with pytest.raises(B.Rn18Error):
         B.rn18_state_floats(B.make_config(3, 10))
+
+
+def test_operator_tensor_limit_is_checked_on_the_host():
+    """4096 x 64 x 64 x 64 fp32 activations are 4 GiB: beyond the kernels'
+    32-bit byte offsets, so the operator returns RN18_EINVAL before it
+    touches a pointer or the device (fake, aligned pointers here)."""
+    if not os.path.exists(B.LIB_PATH):
+        pytest.skip("library not built")
+    f = B.lib().rn18op_conv2d_fwd
+    fake = ctypes.c_void_p(1 << 20)
+    r = f(B.RN18_FP32, fake, fake, fake, 4096, 64, 64, 64, 64, 3, 1, 1, None)
+    assert r == B.RN18_EINVAL
+    assert "per-tensor limit" in B.rn18_last_error()
+    r = f(B.RN18_BF16, fake, fake, fake, 4096, 64, 64, 64, 64, 3, 1, 1, None)   # 2 GiB in bf16
+    assert r == B.RN18_EINVAL
