@@ -155,7 +155,8 @@ struct ConvP {
   size_t mean, rstd, scale, shift, coef;
   int splits, pps;
 };
-struct BlockP { size_t in, z1, out; };
+// mbits: ReLU mask bytes of the block output (one byte per 16-byte chunk)
+struct BlockP { size_t in, z1, out, mbits; };
 
 struct Plan {
   int N, H, W;
@@ -347,6 +348,7 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     }
     const ConvP& p2 = pl->cp[B.c2];
     bp.out = act(p2.Ho, p2.Wo, a.convs[B.c2].cout);
+    bp.mbits = alloc((size_t)p2.M * a.convs[B.c2].cout * es / 16);
     const size_t ob = (size_t)p2.M * a.convs[B.c2].cout * es;
     const size_t ib = (size_t)N * h * w * a.convs[B.c1].cin * es;
     if (ob > max_blockio) max_blockio = ob;
@@ -582,14 +584,18 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     }
     return 0;
   };
-  auto apply = [&](int li, int relu, int res_mode, size_t r, int li2, size_t z) -> int {
+  // mb: offset of the mask bytes to write (block outputs of a training step), or 0
+  auto apply = [&](int li, int relu, int res_mode, size_t r, int li2, size_t z, size_t mb = 0) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     const float* sc2 = li2 >= 0 ? (const float*)(ws + pl.cp[li2].scale) : nullptr;
     const float* sf2 = li2 >= 0 ? (const float*)(ws + pl.cp[li2].shift) : nullptr;
-    TIMED(RN18_K_BN_APPLY, li, res_mode, kernel_instance_name("bn_apply_kernel", prec), 0.0, (double)P.M * L.cout * es * (res_mode ? 3 : 2),
+    const double tb = (double)P.M * L.cout * es;
+    TIMED(RN18_K_BN_APPLY, li, res_mode, kernel_instance_name("bn_apply_kernel", prec), 0.0,
+          tb * (res_mode ? 3 : 2) + (mb ? tb / 16 : 0.0),
           bn_apply_launch(prec, ws + P.y, (float*)(ws + P.scale), (float*)(ws + P.shift), relu, res_mode,
-                          res_mode ? ws + r : nullptr, sc2, sf2, ws + z, P.M, L.cout, st));
+                          res_mode ? ws + r : nullptr, sc2, sf2, ws + z, P.M, L.cout, st,
+                          mb ? (uint8_t*)(ws + mb) : nullptr));
     return 0;
   };
 
@@ -614,9 +620,9 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     if ((r = conv_bn(B.c2))) return r;
     if (B.ds >= 0) {
       if ((r = conv_bn(B.ds))) return r;
-      if ((r = apply(B.c2, 1, 2, pl.cp[B.ds].y, B.ds, bp.out))) return r;
+      if ((r = apply(B.c2, 1, 2, pl.cp[B.ds].y, B.ds, bp.out, train ? bp.mbits : 0))) return r;
     } else {
-      if ((r = apply(B.c2, 1, 1, bp.in, -1, bp.out))) return r;
+      if ((r = apply(B.c2, 1, 1, bp.in, -1, bp.out, train ? bp.mbits : 0))) return r;
     }
   }
   const size_t last = pl.bp.back().out;
@@ -664,27 +670,29 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     return r;
 
   auto W_d = [&](int li) { return (const char*)c->wd + (size_t)a.convs[li].wd * c->es; };
-  // BN backward of conv li: dz (with mask mz) -> dy written to `dy`
-  // mz: the tensor whose sign is the ReLU mask, or RECOMPUTE when the mask is
-  // that of relu(bn(y)) of this layer itself (recomputed from y)
+  // BN backward of conv li: dz (with a ReLU mask) -> dy written to `dy`
+  // mb: the ReLU mask bytes of the block output, or RECOMPUTE when the mask
+  // is that of relu(bn(y)) of this layer itself (recomputed from y)
   const size_t RECOMPUTE = ~(size_t)0;
-  auto bn_back = [&](int li, size_t dz, size_t mz, size_t dy) -> int {
+  auto bn_back = [&](int li, size_t dz, size_t mb, size_t dy) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     int nblk = 0;
     float* part = (float*)(ws + pl.part);
     const double tb = (double)P.M * L.cout * es;
-    const bool rc = mz == RECOMPUTE;
-    const void* mzp = rc ? nullptr : ws + mz;
+    const bool rc = mb == RECOMPUTE;
+    const uint8_t* mzp = rc ? nullptr : (const uint8_t*)(ws + mb);
     const float* msc = rc ? (const float*)(ws + P.scale) : nullptr;
     const float* msf = rc ? (const float*)(ws + P.shift) : nullptr;
-    TIMED(RN18_K_BN_BWD_REDUCE, li, 0, kernel_instance_name("bn_bwd_partial_kernel", prec), 0.0, (rc ? 2 : 3) * tb,
+    TIMED(RN18_K_BN_BWD_REDUCE, li, 0, kernel_instance_name("bn_bwd_partial_kernel", prec), 0.0,
+          2 * tb + (rc ? 0.0 : tb / 16),
           bn_bwd_partial_launch(prec, ws + dz, mzp, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.rstd), P.M,
                                 L.cout, part, &nblk, st, msc, msf));
     TIMED(RN18_K_BN_BWD_REDUCE, li, 1, "bn_bwd_final_kernel", 0.0, 0.0,
           bn_bwd_final_launch(part, nblk, P.M, L.cout, state + L.g, (float*)(ws + P.rstd), grad + L.g, grad + L.b,
                               (float*)(ws + P.coef), st));
-    TIMED(RN18_K_BN_BWD_APPLY, li, 0, kernel_instance_name("bn_bwd_apply_kernel", prec), 0.0, (rc ? 3 : 4) * tb,
+    TIMED(RN18_K_BN_BWD_APPLY, li, 0, kernel_instance_name("bn_bwd_apply_kernel", prec), 0.0,
+          3 * tb + (rc ? 0.0 : tb / 16),
           bn_bwd_apply_launch(prec, ws + dz, mzp, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.coef), ws + dy,
                               P.M, L.cout, st, msc, msf));
     if (!c->captures.empty()) return run_captures(c, RN18_CAP_DY, li, ws + dy, (size_t)P.M * L.cout * es);
@@ -711,8 +719,8 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const BlockL& B = a.blocks[bi];
     const BlockP& bp = pl.bp[bi];
     // gA = gradient wrt the block output (before its ReLU mask)
-    if ((r = bn_back(B.c2, gA, bp.out, pl.gy))) return r;
-    if (B.ds >= 0 && (r = bn_back(B.ds, gA, bp.out, pl.gyd))) return r;
+    if ((r = bn_back(B.c2, gA, bp.mbits, pl.gy))) return r;
+    if (B.ds >= 0 && (r = bn_back(B.ds, gA, bp.mbits, pl.gyd))) return r;
     if ((r = wgrad(B.c2, pl.gy))) return r;
     if ((r = dgrad(B.c2, pl.gy, pl.gz, 0, 0, 0))) return r;
     const size_t z1b = (size_t)pl.cp[B.c1].M * a.convs[B.c1].cout * es;
@@ -726,7 +734,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
       if ((r = wgrad(B.ds, pl.gyd))) return r;
       if ((r = dgrad(B.ds, pl.gyd, gB, 1, 0, 0))) return r;
     } else {
-      if ((r = dgrad(B.c1, pl.gy, gB, 2, gA, bp.out))) return r;
+      if ((r = dgrad(B.c1, pl.gy, gB, 2, gA, bp.mbits))) return r;
     }
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX, bi, ws + gB, inb))) return r;
     std::swap(gA, gB);

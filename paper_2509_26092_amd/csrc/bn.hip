@@ -132,7 +132,7 @@ __global__ __launch_bounds__(256) void bn_apply_kernel(const T* __restrict__ y, 
                                                        const float* __restrict__ shift, int relu, int res_mode,
                                                        const T* __restrict__ r, const float* __restrict__ scale2,
                                                        const float* __restrict__ shift2, T* __restrict__ z,
-                                                       long nchunks, int C) {
+                                                       long nchunks, int C, uint8_t* __restrict__ mbits) {
   constexpr int VW = TT<T>::VW;
   __shared__ float sc[kMaxC], sf[kMaxC], sc2[kMaxC], sf2[kMaxC];
   for (int c = threadIdx.x; c < C; c += 256) {
@@ -163,7 +163,17 @@ __global__ __launch_bounds__(256) void bn_apply_kernel(const T* __restrict__ y, 
 #pragma unroll
       for (int e = 0; e < VW; ++e) v[e] = v[e] > 0.f ? v[e] : 0.f;
     }
-    ((uint4*)z)[q] = pack<T>(v);
+    const uint4 pk = pack<T>(v);
+    ((uint4*)z)[q] = pk;
+    if (mbits) {
+      // bit e: element e of the chunk as stored is > 0 (its ReLU mask)
+      float vr[VW];
+      unpack<T>(pk, vr);
+      uint32_t b = 0;
+#pragma unroll
+      for (int e = 0; e < VW; ++e) b |= (vr[e] > 0.f ? 1u : 0u) << e;
+      mbits[q] = (uint8_t)b;
+    }
   }
 }
 
@@ -178,7 +188,7 @@ __global__ void bn_eval_coef_kernel(const float* gamma, const float* beta, const
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict__ dz, const T* __restrict__ mz,
+__global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict__ dz, const uint8_t* __restrict__ mb,
                                                              const T* __restrict__ y, const float* __restrict__ mean,
                                                              const float* __restrict__ rstd,
                                                              const float* __restrict__ mscale,
@@ -205,14 +215,15 @@ __global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict
   // end load the thread's first row of the step and add nothing)
   constexpr int U = 4;
   for (long r0 = (long)blockIdx.x * rpi + rr; r0 < M; r0 += U * gstride) {
-    uint4 qg[U], qy[U], qm[U];
+    uint4 qg[U], qy[U];
+    uint32_t qm[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const long r = r0 + u * gstride < M ? r0 + u * gstride : r0;
       const long o = r * C + cg * VW;
       qg[u] = *(const uint4*)(dz + o);
       qy[u] = *(const uint4*)(y + o);
-      if (mz) qm[u] = *(const uint4*)(mz + o);
+      if (mb) qm[u] = mb[r * tpc + cg];
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -220,11 +231,9 @@ __global__ __launch_bounds__(256) void bn_bwd_partial_kernel(const T* __restrict
       float g[VW], yy[VW];
       unpack<T>(qg[u], g);
       unpack<T>(qy[u], yy);
-      if (mz) {
-        float m[VW];
-        unpack<T>(qm[u], m);
+      if (mb) {
 #pragma unroll
-        for (int e = 0; e < VW; ++e) g[e] = m[e] > 0.f ? g[e] : 0.f;
+        for (int e = 0; e < VW; ++e) g[e] = (qm[u] >> e) & 1u ? g[e] : 0.f;
       } else if (mscale) {
         // the ReLU mask of relu(bn(y)), from the stored value's arithmetic
 #pragma unroll
@@ -279,7 +288,7 @@ __global__ __launch_bounds__(256) void bn_bwd_final_kernel(const float* __restri
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const T* __restrict__ dz, const T* __restrict__ mz,
+__global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const T* __restrict__ dz, const uint8_t* __restrict__ mb,
                                                            const T* __restrict__ y, const float* __restrict__ mean,
                                                            const float* __restrict__ coef,
                                                            const float* __restrict__ mscale,
@@ -301,11 +310,10 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const T* __restrict__
     float g[VW], yy[VW], o[VW];
     unpack<T>(((const uint4*)dz)[q], g);
     unpack<T>(((const uint4*)y)[q], yy);
-    if (mz) {
-      float m[VW];
-      unpack<T>(((const uint4*)mz)[q], m);
+    if (mb) {
+      const uint32_t m = mb[q];
 #pragma unroll
-      for (int e = 0; e < VW; ++e) g[e] = m[e] > 0.f ? g[e] : 0.f;
+      for (int e = 0; e < VW; ++e) g[e] = (m >> e) & 1u ? g[e] : 0.f;
     } else if (mscale) {
 #pragma unroll
       for (int e = 0; e < VW; ++e) g[e] = relu_stored<T>(yy[e], msc[c0 + e], msf[c0 + e]) > 0.f ? g[e] : 0.f;
@@ -492,15 +500,16 @@ inline int ok() { return hipGetLastError() == hipSuccess ? 0 : -4; }
 }  // namespace
 
 int bn_apply_launch(int prec, const void* y, const float* scale, const float* shift, int relu, int res_mode,
-                    const void* r, const float* scale2, const float* shift2, void* z, long M, int C, hipStream_t s) {
+                    const void* r, const float* scale2, const float* shift2, void* z, long M, int C, hipStream_t s,
+                    uint8_t* mbits) {
   const int vw = prec == PREC_BF16 ? 8 : 4;
   const long nchunks = M * C / vw;
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(bn_apply_kernel<bf16_t>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const bf16_t*)y,
-                       scale, shift, relu, res_mode, (const bf16_t*)r, scale2, shift2, (bf16_t*)z, nchunks, C);
+                       scale, shift, relu, res_mode, (const bf16_t*)r, scale2, shift2, (bf16_t*)z, nchunks, C, mbits);
   else
     hipLaunchKernelGGL(bn_apply_kernel<float>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const float*)y, scale,
-                       shift, relu, res_mode, (const float*)r, scale2, shift2, (float*)z, nchunks, C);
+                       shift, relu, res_mode, (const float*)r, scale2, shift2, (float*)z, nchunks, C, mbits);
   return ok();
 }
 
@@ -522,16 +531,16 @@ int bn_bwd_partial_pool_blocks(int prec, int N, int H, int W, int C) {
   return pick_blocks((long)N * ((H + 1) / 2) * ((W + 1) / 2), rpi);
 }
 
-int bn_bwd_partial_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
+int bn_bwd_partial_launch(int prec, const void* dz, const uint8_t* mb, const void* y, const float* mean,
                           const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s,
                           const float* mscale, const float* mshift) {
   const int nb = bn_bwd_partial_blocks(prec, M, C);
   *nblk = nb;
   if (prec == PREC_BF16)
-    hipLaunchKernelGGL(bn_bwd_partial_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, (const bf16_t*)dz,
-                       (const bf16_t*)mz, (const bf16_t*)y, mean, rstd, mscale, mshift, M, C, part);
+    hipLaunchKernelGGL(bn_bwd_partial_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, (const bf16_t*)dz, mb,
+                       (const bf16_t*)y, mean, rstd, mscale, mshift, M, C, part);
   else
-    hipLaunchKernelGGL(bn_bwd_partial_kernel<float>, dim3(nb), dim3(256), 0, s, (const float*)dz, (const float*)mz,
+    hipLaunchKernelGGL(bn_bwd_partial_kernel<float>, dim3(nb), dim3(256), 0, s, (const float*)dz, mb,
                        (const float*)y, mean, rstd, mscale, mshift, M, C, part);
   return ok();
 }
@@ -543,17 +552,17 @@ int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float*
   return ok();
 }
 
-int bn_bwd_apply_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean, const float* coef,
+int bn_bwd_apply_launch(int prec, const void* dz, const uint8_t* mb, const void* y, const float* mean, const float* coef,
                         void* dy, long M, int C, hipStream_t s, const float* mscale, const float* mshift) {
   const int vw = prec == PREC_BF16 ? 8 : 4;
   const long nchunks = M * C / vw;
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(bn_bwd_apply_kernel<bf16_t>, dim3(stream_blocks(nchunks)), dim3(256), 0, s,
-                       (const bf16_t*)dz, (const bf16_t*)mz, (const bf16_t*)y, mean, coef, mscale, mshift,
+                       (const bf16_t*)dz, mb, (const bf16_t*)y, mean, coef, mscale, mshift,
                        (bf16_t*)dy, nchunks, C);
   else
     hipLaunchKernelGGL(bn_bwd_apply_kernel<float>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const float*)dz,
-                       (const float*)mz, (const float*)y, mean, coef, mscale, mshift, (float*)dy, nchunks, C);
+                       mb, (const float*)y, mean, coef, mscale, mshift, (float*)dy, nchunks, C);
   return ok();
 }
 

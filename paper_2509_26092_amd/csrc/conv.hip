@@ -462,11 +462,11 @@ __device__ inline void gather_impl(const ConvGather& g) {
 #pragma unroll
         for (int e = 0; e < VW; ++e) v[e] += o[e];
       } else if (g.mode == 2) {
-        float rr[VW], mk[VW];
+        float rr[VW];
         unpack<T>(*(const uint4*)((const T*)g.R + off), rr);
-        unpack<T>(*(const uint4*)((const T*)g.Rm + off), mk);
+        const uint32_t mk = ((const uint8_t*)g.Rm)[off / VW];    // mask byte of this 16-byte chunk
 #pragma unroll
-        for (int e = 0; e < VW; ++e) v[e] += mk[e] > 0.f ? rr[e] : 0.f;
+        for (int e = 0; e < VW; ++e) v[e] += (mk >> e) & 1u ? rr[e] : 0.f;
       }
       const uint4 pk = pack<T>(v);
       *(uint4*)(Cg + off) = pk;
@@ -761,11 +761,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
 #pragma unroll
           for (int e = 0; e < VW; ++e) v[e] += o[e];
         } else if (g.mode == 2) {
-          float rr[VW], mk[VW];
+          float rr[VW];
           unpack<T>(*(const uint4*)((const T*)g.R + off), rr);
-          unpack<T>(*(const uint4*)((const T*)g.Rm + off), mk);
+          const uint32_t mk = ((const uint8_t*)g.Rm)[off / VW];  // mask byte of this 16-byte chunk
 #pragma unroll
-          for (int e = 0; e < VW; ++e) v[e] += mk[e] > 0.f ? rr[e] : 0.f;
+          for (int e = 0; e < VW; ++e) v[e] += (mk >> e) & 1u ? rr[e] : 0.f;
         }
         const uint4 pk = pack<T>(v);
         *(uint4*)(Cg + off) = pk;
@@ -927,8 +927,9 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
   const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, out_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rsR = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(g.mode == 1 || !g.R ? (const void*)g.C : g.R), 0, out_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rsRm =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(g.Rm ? g.Rm : (const void*)g.C), 0, out_bytes, 0x00020000);
+  // ReLU mask bytes of the residual: one byte per 8 output elements
+  const __amdgpu_buffer_rsrc_t rsRm = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(g.Rm ? g.Rm : (const void*)g.C), 0, out_bytes / 16, 0x00020000);
 
   // running BN partial statistics of this lane's 16 channels over the wave's pixels
   float s1[FN][4], s2[FN][4], sh[FN][4];
@@ -1016,7 +1017,8 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
       obase[i] = (uint32_t)((m0 + (okq[i] ? q : 0)) * g.Cols) + chl;
     }
     typedef int i32x2_t __attribute__((ext_vector_type(2)));
-    i32x2_t ld0[MODE ? FM : 1][FN], ld1[MODE == 2 ? FM : 1][FN];
+    i32x2_t ld0[MODE ? FM : 1][FN];
+    uint32_t ld1[MODE == 2 ? FM : 1][FN];
     if constexpr (MODE != 0) {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -1024,7 +1026,8 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
         for (int j = 0; j < FN; ++j) {
           const uint32_t ob = okq[i] ? (obase[i] + j * 16) * 2 : kOutOfRange;
           ld0[i][j] = __builtin_amdgcn_raw_buffer_load_b64(rsR, ob, 0, 0);
-          if constexpr (MODE == 2) ld1[i][j] = __builtin_amdgcn_raw_buffer_load_b64(rsRm, ob, 0, 0);
+          if constexpr (MODE == 2)
+            ld1[i][j] = __builtin_amdgcn_raw_buffer_load_b8(rsRm, okq[i] ? (obase[i] + j * 16) >> 3 : kOutOfRange, 0, 0);
         }
     }
 #pragma unroll
@@ -1038,8 +1041,8 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
           for (int e = 0; e < 4; ++e) {
             const float rv = bf2f((bf16_t)(e & 1 ? rw[e >> 1] >> 16 : rw[e >> 1] & 0xffffu));
             if constexpr (MODE == 2) {
-              const uint32_t mw = (uint32_t)(e >> 1 ? ld1[i][j].y : ld1[i][j].x);
-              x[e] += bf2f((bf16_t)(e & 1 ? mw >> 16 : mw & 0xffffu)) > 0.f ? rv : 0.f;
+              // this lane's 4 channels are the low or high half of the byte
+              x[e] += (ld1[i][j] >> ((chl & 4) + e)) & 1u ? rv : 0.f;
             } else {
               x[e] += rv;
             }
@@ -1438,8 +1441,9 @@ __global__ __launch_bounds__(64 * HW_WAVES, HW_BPC) void conv_halo_wide_kernel(C
   const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, out_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rsR = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(g.mode == 1 || !g.R ? (const void*)g.C : g.R), 0, out_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rsRm =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(g.Rm ? g.Rm : (const void*)g.C), 0, out_bytes, 0x00020000);
+  // ReLU mask bytes of the residual: one byte per 8 output elements
+  const __amdgpu_buffer_rsrc_t rsRm = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(g.Rm ? g.Rm : (const void*)g.C), 0, out_bytes / 16, 0x00020000);
   typedef int i32x2_t __attribute__((ext_vector_type(2)));
 
   bool first = true;
@@ -1587,13 +1591,15 @@ __global__ __launch_bounds__(64 * HW_WAVES, HW_BPC) void conv_halo_wide_kernel(C
       const int r = (int)h.fd_pw.div(v), c = v - r * h.PW;
       const bool okq = r < rows_t && c < g.Wm;
       const uint32_t ob = (uint32_t)((m0 + (okq ? r * g.Wm + c : 0)) * g.Cols) + n0 + wn * WTN + chl;
-      i32x2_t ld0[FN], ld1[FN];
+      i32x2_t ld0[FN];
+      uint32_t ld1[FN];
       if constexpr (MODE != 0) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const uint32_t o = okq ? (ob + j * 16) * 2 : kOutOfRange;
           ld0[j] = __builtin_amdgcn_raw_buffer_load_b64(rsR, o, 0, 0);
-          if constexpr (MODE == 2) ld1[j] = __builtin_amdgcn_raw_buffer_load_b64(rsRm, o, 0, 0);
+          if constexpr (MODE == 2)
+            ld1[j] = __builtin_amdgcn_raw_buffer_load_b8(rsRm, okq ? (ob + j * 16) >> 3 : kOutOfRange, 0, 0);
         }
       }
       cnt += okq ? 1.f : 0.f;
@@ -1606,8 +1612,8 @@ __global__ __launch_bounds__(64 * HW_WAVES, HW_BPC) void conv_halo_wide_kernel(C
           for (int e = 0; e < 4; ++e) {
             const float rv = bf2f((bf16_t)(e & 1 ? rw[e >> 1] >> 16 : rw[e >> 1] & 0xffffu));
             if constexpr (MODE == 2) {
-              const uint32_t mw = (uint32_t)(e >> 1 ? ld1[j].y : ld1[j].x);
-              x[e] += bf2f((bf16_t)(e & 1 ? mw >> 16 : mw & 0xffffu)) > 0.f ? rv : 0.f;
+              // this lane's 4 channels are the low or high half of the byte
+              x[e] += (ld1[j] >> ((chl & 4) + e)) & 1u ? rv : 0.f;
             } else {
               x[e] += rv;
             }

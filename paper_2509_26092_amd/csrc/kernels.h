@@ -13,7 +13,7 @@ struct ConvGather {
   const void* B;   // weights [Cols][KHW][Cin]
   void* C;         // NHWC output [N][Hout][Wout][Cols]
   const void* R;   // epilogue: residual gradient (mode 2)
-  const void* Rm;  // epilogue: residual mask source (mode 2)
+  const void* Rm;  // epilogue: ReLU mask bytes of the residual (mode 2; bn_apply_launch's layout)
   int N, Hin, Win, Cin;
   int Hm, Wm, M;             // GEMM row grid per image; M = N*Hm*Wm
   int Hout, Wout, Cols;
@@ -23,7 +23,7 @@ struct ConvGather {
   int dh0, dhs, dw0, dws;    // input offset of tap (th,tw): (dh0+th*dhs, dw0+tw*dws)
   int wkh0, wkhs, wkw0, wkws, KW, KHW;  // weight tap (wkh0+th*wkhs)*KW + wkw0+tw*wkws
   int K;                     // nth*ntw*Cin
-  int mode;                  // 0 store, 1 C += acc, 2 C = acc + (Rm>0 ? R : 0)
+  int mode;                  // 0 store, 1 C += acc, 2 C = acc + (mask ? R : 0)
   FastDiv fd_hw, fd_w;       // division by Hm*Wm and by Wm (set by the launcher)
   float* stats;              // optional BN partials (rows, shift, sum, sum sq) [tiles_m][Cols][4] of the stored output
   const void* zero;          // 16-byte zero page (set by the launcher)
@@ -88,18 +88,22 @@ int bn_stats_tiles_final_launch(const float* tile_stats, int ntiles, int C, doub
                                 float* mean, float* rstd, float* scale, float* shift, hipStream_t s);
 // z = act(y*scale+shift [+ r] [+ (yd*scale2+shift2)])
 //  res_mode: 0 none, 1 identity residual r, 2 projected residual (yd, scale2, shift2)
+// ReLU mask bytes (mbits, optional, M*C/VW bytes): one byte per 16-byte
+// storage chunk of z (VW = 8 bf16 or 4 fp32 elements), bit e set iff element
+// e of the chunk as stored is > 0.
 int bn_apply_launch(int prec, const void* y, const float* scale, const float* shift, int relu,
                     int res_mode, const void* r, const float* scale2, const float* shift2,
-                    void* z, long M, int C, hipStream_t s);
+                    void* z, long M, int C, hipStream_t s, uint8_t* mbits = nullptr);
 // eval-mode BN coefficients from running statistics
 int bn_eval_coef_launch(const float* gamma, const float* beta, const float* rm, const float* rv,
                         float eps, int C, float* scale, float* shift, hipStream_t s);
-// backward partials of g = dz*(mz>0) (or dz): sum g, sum g*(y-mean)*rstd
-// The ReLU mask is mz > 0 when mz is given; with mz = NULL and mscale set it
-// is recomputed as relu(y * mscale + mshift) > 0 of the stored value (the
-// first BN of a block, whose ReLU output feeds only the next conv); with
-// neither, there is no mask.
-int bn_bwd_partial_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
+// backward partials of g = dz*mask (or dz): sum g, sum g*(y-mean)*rstd
+// The ReLU mask comes from mask bytes mb (the layout bn_apply_launch writes)
+// when given; with mb = NULL and mscale set it is recomputed as
+// relu(y * mscale + mshift) > 0 of the stored value (the first BN of a
+// block, whose ReLU output feeds only the next conv); with neither, there is
+// no mask.
+int bn_bwd_partial_launch(int prec, const void* dz, const uint8_t* mb, const void* y, const float* mean,
                           const float* rstd, long M, int C, float* part, int* nblk, hipStream_t s,
                           const float* mscale = nullptr, const float* mshift = nullptr);
 // blocks (= partial entries of 2 floats per channel) that the two backward
@@ -121,7 +125,7 @@ int bn_bwd_apply_pool_launch(int prec, const void* dpool, const uint8_t* arg, co
 int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float* gamma, const float* rstd,
                         float* dgamma, float* dbeta, float* coef, hipStream_t s);
 // dy = k1*g + k2*(y-mean) + k3
-int bn_bwd_apply_launch(int prec, const void* dz, const void* mz, const void* y, const float* mean,
+int bn_bwd_apply_launch(int prec, const void* dz, const uint8_t* mb, const void* y, const float* mean,
                         const float* coef, void* dy, long M, int C, hipStream_t s, const float* mscale = nullptr,
                         const float* mshift = nullptr);
 
