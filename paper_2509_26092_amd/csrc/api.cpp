@@ -181,12 +181,12 @@ struct Ctx {
   float* momentum = nullptr;
   void* wf = nullptr;
   void* wd = nullptr;
-  RepackEntry* tab = nullptr;
-  int ntab = 0;
+  RepackEntry* tab = nullptr;   // element-wise repack entries, then the tiled ones (one allocation)
+  int ntab = 0, nttab = 0, ntiles = 0;
+  long tab_total = 0;           // elements over the element-wise entries
   unsigned* err = nullptr;
   // dropout before the classifier: on iff the rate is > 0, keep threshold,
-  // scale, and the
-  // Philox key and step counter of the next training step
+  // scale, and the Philox key and step counter of the next training step
   bool drop_on = false;
   uint32_t drop_thresh = 0;
   float drop_scale = 1.f;
@@ -549,8 +549,12 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
   auto W = [&](int li) { return (const char*)c->wf + (size_t)pl.cp[li].wf * c->es; };
 
   const double es = c->es;
-  TIMED(RN18_K_PREP, -1, 0, kernel_instance_name("repack_kernel", prec), 0.0, (double)a.wf_total * (4.0 + 2.0 * es),
-        repack_launch(prec, state_c, c->wf, c->wd, c->tab, c->ntab, a.wf_total, st));
+  TIMED(RN18_K_PREP, -1, 2, kernel_instance_name("repack_tiled_kernel", prec), 0.0,
+        (double)(a.wf_total - c->tab_total) * (4.0 + 2.0 * es),
+        repack_tiled_launch(prec, state_c, c->wf, c->wd, c->tab + c->ntab, c->nttab, c->ntiles, st));
+  if (c->tab_total > 0)
+    TIMED(RN18_K_PREP, -1, 0, kernel_instance_name("repack_kernel", prec), 0.0, (double)c->tab_total * (4.0 + 2.0 * es),
+          repack_launch(prec, state_c, c->wf, c->wd, c->tab, c->ntab, c->tab_total, st));
   if (pl.cp[0].s2d)
     TIMED(RN18_K_PREP, -1, 1, kernel_instance_name("ingest_s2d_kernel", prec), 0.0,
           (double)N * pl.H * pl.W * (12.0 + 4.0 * es), ingest_s2d_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, st));
@@ -859,15 +863,22 @@ int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* st
   if (hipMalloc(&c.wf, a.wf_total * c.es + 16) != hipSuccess) return bail(RN18_ENOMEM, "weight shadow allocation failed");
   if (hipMalloc(&c.wd, a.wd_total * c.es + 16) != hipSuccess) return bail(RN18_ENOMEM, "weight shadow allocation failed");
   if (hipMalloc(&c.err, 256) != hipSuccess) return bail(RN18_ENOMEM, "flag allocation failed");
-  std::vector<RepackEntry> tab;
-  long pre = 0;
+  std::vector<RepackEntry> tab, ttab;
+  long pre = 0, tpre = 0;
   for (const auto& L : a.convs) {
     RepackEntry e;
     e.src = L.w; e.dst_f = L.wf; e.dst_d = L.wd;
     e.Cout = L.cout; e.Cin = L.cin; e.Cin_p = L.cin_p; e.KHW = L.k * L.k;
+    e.mode = 0; e.pad_ = 0;
+    if (repack_tiled_fits(e.KHW)) {
+      e.n = repack_tiles(e.Cout, e.Cin_p);
+      e.nprefix = tpre;
+      tpre += e.n;
+      ttab.push_back(e);
+      continue;
+    }
     e.n = (long)L.cout * L.k * L.k * L.cin_p;
     e.nprefix = pre;
-    e.mode = 0; e.pad_ = 0;
     pre += e.n;
     tab.push_back(e);
   }
@@ -883,6 +894,11 @@ int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* st
     tab.push_back(e);
   }
   c.ntab = (int)tab.size();
+  c.nttab = (int)ttab.size();
+  c.ntiles = (int)tpre;
+  c.tab_total = pre;
+  if (c.ntab > 24 || c.nttab > 24) return bail(RN18_EINVAL, "too many repack entries");
+  tab.insert(tab.end(), ttab.begin(), ttab.end());
   if (hipMalloc(&c.tab, sizeof(RepackEntry) * tab.size()) != hipSuccess) return bail(RN18_ENOMEM, "table allocation failed");
   if (hipMemcpy(c.tab, tab.data(), sizeof(RepackEntry) * tab.size(), hipMemcpyHostToDevice) != hipSuccess)
     return bail(RN18_EHIP, "table upload failed");

@@ -143,8 +143,16 @@ int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, 
 struct RepackEntry { long src; long dst_f; long dst_d; int Cout, Cin, Cin_p, KHW; long n; long nprefix; int mode, pad_; };
 // y = bf16(x), round to nearest even, as every kernel stores bf16 (n multiple of 8)
 int round_bf16_launch(const float* x, uint16_t* y, long n, hipStream_t s);
+// Weight shadows from the fp32 state: entries repacked element by element
+// (total elements over them), and entries of kernels with at most 9 taps
+// through an LDS-tiled transpose (n = tiles, nprefix = tile prefix; ntiles
+// blocks in all).
 int repack_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* table_dev,
                   int nentries, long total, hipStream_t s);
+int repack_tiled_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* table_dev,
+                        int nentries, int ntiles, hipStream_t s);
+bool repack_tiled_fits(int khw);
+int repack_tiles(int cout, int cin_p);
 int maxpool_fwd_launch(int prec, const void* x, void* y, uint8_t* arg, int N, int H, int W, int C,
                        int Ho, int Wo, hipStream_t s);
 int maxpool_bwd_launch(int prec, const void* dy, const uint8_t* arg, void* dx, int N, int H, int W, int C,

@@ -88,6 +88,60 @@ __global__ void repack_kernel(const float* __restrict__ st, T* __restrict__ wf, 
   }
 }
 
+// Weight shadows of the 3x3 and 1x1 convs through LDS, one block per tile of
+// 32 output x 32 input channels with all its taps: the fp32 weights
+// [Cout][Cin][KHW] are read in contiguous rows, and both layouts are written
+// in runs of consecutive channels. Entry fields: n = tiles of the conv,
+// nprefix = tiles before it.
+constexpr int kRepackT = 32, kRepackMaxKHW = 9;
+template <typename T>
+__global__ __launch_bounds__(256) void repack_tiled_kernel(const float* __restrict__ st, T* __restrict__ wf,
+                                                           T* __restrict__ wd, const RepackEntry* __restrict__ tab,
+                                                           int nent) {
+  __shared__ RepackEntry t[24];
+  __shared__ float s[kRepackT * (kRepackT * kRepackMaxKHW + 1)];
+  for (int i = threadIdx.x; i < nent; i += blockDim.x) t[i] = tab[i];
+  __syncthreads();
+  int k = 0;
+  while (k + 1 < nent && (long)blockIdx.x >= t[k + 1].nprefix) ++k;
+  const RepackEntry& r = t[k];
+  const int KHW = r.KHW, Cin = r.Cin, Cin_p = r.Cin_p, Cout = r.Cout;
+  const int ntci = (Cin_p + kRepackT - 1) / kRepackT;
+  const int l = (int)(blockIdx.x - r.nprefix);
+  const int co0 = (l / ntci) * kRepackT, ci0 = (l % ntci) * kRepackT;
+  const int nco = min(kRepackT, Cout - co0), nci = min(kRepackT, Cin_p - ci0);
+  const int row = nci * KHW, RS = kRepackT * KHW + 1;   // odd row stride: no bank conflicts across rows
+  const int valid = (Cin - ci0) * KHW;                  // row entries with a real input channel
+  // twelve loads in flight per thread before any is stored
+  constexpr int U = 12;
+  const int nld = nco * row;
+  for (int b = threadIdx.x; b < nld; b += 256 * U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int idx = b + u * 256, co = idx / row, j = idx - co * row;
+      v[u] = idx < nld && j < valid ? st[r.src + ((long)(co0 + co) * Cin + ci0) * KHW + j] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int idx = b + u * 256, co = idx / row, j = idx - co * row;
+      if (idx < nld) s[co * RS + j] = v[u];
+    }
+  }
+  __syncthreads();
+  // forward layout [Cout][KHW][Cin_p]: consecutive input channels
+  for (int idx = threadIdx.x; idx < nco * KHW * nci; idx += 256) {
+    const int ci = idx % nci, rest = idx / nci, tap = rest % KHW, co = rest / KHW;
+    wf[r.dst_f + ((long)(co0 + co) * KHW + tap) * Cin_p + ci0 + ci] = TT<T>::from_f(s[co * RS + ci * KHW + tap]);
+  }
+  // data-gradient layout [Cin_p][KHW][Cout]: consecutive output channels
+  if (r.dst_d >= 0)
+    for (int idx = threadIdx.x; idx < nci * KHW * nco; idx += 256) {
+      const int co = idx % nco, rest = idx / nco, tap = rest % KHW, ci = rest / KHW;
+      wd[r.dst_d + ((long)(ci0 + ci) * KHW + tap) * Cout + co0 + co] = TT<T>::from_f(s[co * RS + ci * KHW + tap]);
+    }
+}
+
 // ------------------------------------------------------------------ dropout
 // Philox4x32-10 (Salmon et al., SC'11): ten rounds of two 32x32 -> 64-bit
 // products mixed with the other counter words and the key, the key bumped by
@@ -436,6 +490,7 @@ int round_bf16_launch(const float* x, uint16_t* y, long n, hipStream_t s) {
 int repack_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* tab, int nent, long total,
                   hipStream_t s) {
   if (nent > 24) return -1;
+  if (total <= 0) return 0;
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(repack_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s, state, (bf16_t*)wf,
                        (bf16_t*)wd, tab, nent, total);
@@ -443,6 +498,24 @@ int repack_launch(int prec, const float* state, void* wf, void* wd, const Repack
     hipLaunchKernelGGL(repack_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s, state, (float*)wf, (float*)wd,
                        tab, nent, total);
   return ok();
+}
+
+int repack_tiled_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* tab, int nent,
+                        int ntiles, hipStream_t s) {
+  if (nent > 24) return -1;
+  if (ntiles <= 0) return 0;
+  if (prec == PREC_BF16)
+    hipLaunchKernelGGL(repack_tiled_kernel<bf16_t>, dim3(ntiles), dim3(256), 0, s, state, (bf16_t*)wf, (bf16_t*)wd,
+                       tab, nent);
+  else
+    hipLaunchKernelGGL(repack_tiled_kernel<float>, dim3(ntiles), dim3(256), 0, s, state, (float*)wf, (float*)wd, tab,
+                       nent);
+  return ok();
+}
+
+bool repack_tiled_fits(int khw) { return khw <= kRepackMaxKHW; }
+int repack_tiles(int cout, int cin_p) {
+  return ((cout + kRepackT - 1) / kRepackT) * ((cin_p + kRepackT - 1) / kRepackT);
 }
 
 int maxpool_fwd_launch(int prec, const void* x, void* y, uint8_t* arg, int N, int H, int W, int C, int Ho, int Wo,
