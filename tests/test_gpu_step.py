@@ -244,6 +244,56 @@ def test_imagenet_bf16_b256_224_launch_config_properties():
     w.close()
 
 
+def test_imagenet_bf16_largest_planned_batch_224():
+    """The largest batch the planner accepts at 224x224 (its stem output,
+    1.6 MB per image, just under the kernels' per-tensor limit), run as two
+    copies of 663 images: the step succeeds; stem-conv outputs of images at
+    the start, middle and end of the batch (byte offsets close to 2^31) equal
+    the oracle's conv of those images; the loss and the stem BN mean equal
+    those of the 663 images alone; eval logits of the last image match the
+    oracle run on it alone."""
+    import torch
+    from gpu_util import assert_close, from_dev_nhwc
+    from oracle import ops
+    arch, classes, prec, half = "imagenet", 1000, "bf16", 663
+    N = 2 * half
+    limit = (1 << 31) - (1 << 24)
+    assert N * 112 * 112 * 64 * 2 <= limit < (N + 2) * 112 * 112 * 64 * 2
+    L, st = make_state(arch, classes, 151)
+    x = inputs.images(151, half, 224, 224)
+    y = inputs.labels(151, half, classes)
+    xx = np.concatenate([x, x])
+    yy = np.concatenate([y, y])
+    z = np.zeros(L.n_trainable)
+    w = B.Worker(arch, classes, prec)
+    try:
+        print("largest batch: N=%d at 224" % N, flush=True)
+        sN, vN, lN, stN = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w, momentum_in=z)
+        assert stN == B.RN18_OK and np.all(np.isfinite(vN))
+        wst = ops.round_bf16(L.get(st, "stem.w"))
+        yall = torch.empty((N, 112, 112, 64), dtype=torch.bfloat16, device="cuda")
+        B.rn18_debug_copy(w.ctx, N, 224, 224, "y", 0, yall)
+        for i in (0, half + 17, N - 1):
+            exact = ops.conv2d_forward(ops.round_bf16(xx[i:i + 1]), wst, 2, 3)
+            got = from_dev_nhwc(yall[i:i + 1])
+            assert (got != ops.round_bf16(exact)).mean() < 1e-3
+            assert_close(got, exact, 8e-3, "stem conv output of image %d" % i)
+        del yall
+        meanN = torch.empty(64, device="cuda")
+        B.rn18_debug_copy(w.ctx, N, 224, 224, "mean", 0, meanN)
+        sh, vh, lh, _ = gpu_train_step(arch, classes, prec, st, x, y, LR, worker=w, momentum_in=z)
+        meanh = torch.empty(64, device="cuda")
+        B.rn18_debug_copy(w.ctx, half, 224, 224, "mean", 0, meanh)
+        assert abs(lN[0] - lh[0]) <= 1e-2 * abs(lh[0])
+        assert_close(meanN.cpu().numpy(), meanh.cpu().numpy(), 1e-4, "stem BN mean, duplicated batch")
+        logits = torch.empty((N, classes), dtype=torch.float32, device="cuda")
+        w.eval_logits(torch.from_numpy(st.astype(np.float32)).cuda(), torch.from_numpy(xx).cuda(), logits)
+        ref = net.eval_logits(net.Config(arch, classes, bf16=True), L, st, xx[N - 1:N])
+        assert_close(logits[N - 1:N].cpu().numpy(), ref, 2e-2, "eval logits of the last image")
+    finally:
+        w.close()
+
+
 def test_lr_zero_keeps_weights():
     arch, classes, prec, N, H, seed = "cifar", 100, "fp32", 4, 16, 160
     L, st = make_state(arch, classes, seed)
