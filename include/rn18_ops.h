@@ -81,7 +81,12 @@ enum {
   /* process-wide: force weight-gradient kernel configuration `value`
    * (1..10, see conv.hip); 0 = automatic. Plans built afterwards size their
    * split-K scratch for it. ctx may be NULL. */
-  RN18_DBG_WGRAD_CONFIG = 2
+  RN18_DBG_WGRAD_CONFIG = 2,
+  /* per context: launch each convolution of a training step or eval pass
+   * over batch chunks of at most `value` images (0 = only where a tensor
+   * would exceed the kernels' 32-bit byte offsets). Plans built before are
+   * dropped. For testing the chunked path at small sizes. */
+  RN18_DBG_CONV_CHUNK = 3
 };
 enum {
   RN18_DBG_Y = 0, RN18_DBG_Z1 = 1, RN18_DBG_OUT = 2, RN18_DBG_GA = 3, RN18_DBG_GB = 4, RN18_DBG_GZ = 5,

@@ -52,12 +52,17 @@ inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 inline int out_size(int h, int k, int s, int p) { return (h + 2 * p - k) / s + 1; }
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// The kernels address each tensor with 32-bit byte offsets: buffer resources
-// sized to the tensor, an out-of-range sentinel of 2^31, and unsigned offset
-// arithmetic that may run a tile (< 1 MiB) past the end. Every tensor a step
-// or an operator touches is therefore kept below 2^31 bytes minus a 16 MiB
-// margin; larger shapes are rejected when they are planned.
+// The convolution kernels address each tensor with 32-bit byte offsets:
+// buffer resources sized to the tensor, an out-of-range sentinel of 2^31, and
+// unsigned offset arithmetic that may run a tile (< 1 MiB) past the end. A
+// convolution launch therefore sees tensors below 2^31 bytes minus a 16 MiB
+// margin: a training step launches each convolution over batch chunks that
+// fit, and the single-operator entry points reject larger tensors.
 constexpr size_t kMaxTensorBytes = ((size_t)1 << 31) - ((size_t)1 << 24);
+// The other kernels index whole tensors by 16-byte chunk in 32-bit integers
+// (or by element in 64-bit ones): every tensor of a step stays below 16 times
+// the bound above.
+constexpr size_t kMaxWholeTensorBytes = 16 * kMaxTensorBytes;
 
 // ----------------------------------------------------------------------------
 // Architecture
@@ -153,7 +158,10 @@ struct ConvP {
   long M;                       // N*Ho*Wo
   size_t x, y;                  // workspace offsets of input and output
   size_t mean, rstd, scale, shift, coef;
-  int splits, pps;
+  int nb;                       // images per launch (batch chunk whose tensors fit 32-bit offsets)
+  int splits, pps;              // weight-gradient split-K of a full chunk of nb images
+  int splits_r, pps_r;          // ... and of the last, shorter chunk (N % nb images), if any
+  int wslots;                   // split-K partial slots over all chunks
 };
 // mbits: ReLU mask bytes of the block output (one byte per 16-byte chunk)
 struct BlockP { size_t in, z1, out, mbits; };
@@ -196,6 +204,7 @@ struct Ctx {
   bool ws_owned = false;
   std::map<std::tuple<int, int, int>, Plan> plans;
   int dbg_stop_blocks = -1;     // debugging: end the backward pass after this many blocks
+  int dbg_chunk = 0;            // debugging: at most this many images per convolution launch (0 = as needed)
   struct Capture { int kind, index; void* dst; size_t bytes; };
   std::vector<Capture> captures; // debugging: copies of backward tensors
   // optional per-launch timing with HIP events on the context stream
@@ -249,7 +258,7 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   const int es = c.es;
   char buf[256];
   if (N < 1 || H < 1 || W < 1) { *why = "N, H and W must be >= 1"; return RN18_EINVAL; }
-  if ((long)N * H * W > (1l << 31) / 8) { *why = "input too large"; return RN18_EINVAL; }
+  if ((long)N * H * W >= (1l << 31)) { *why = "input too large"; return RN18_EINVAL; }
   pl->N = N; pl->H = H; pl->W = W;
   size_t off = 0, max_tensor = (size_t)N * 3 * H * W * 4;  // the caller's NCHW fp32 images
   auto alloc = [&](size_t bytes) {
@@ -289,6 +298,18 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
       *why = buf;
       return false;
     }
+    {
+      const size_t in_img = (size_t)P.Hin * P.Win * P.cin * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
+      const size_t per_img = std::max(in_img, out_img);
+      if (per_img > kMaxTensorBytes) {
+        snprintf(buf, sizeof buf, "one image of conv %d needs %zu bytes, beyond the per-launch limit", li, per_img);
+        *why = buf;
+        return false;
+      }
+      long nb = std::min((long)N, (long)(kMaxTensorBytes / per_img));
+      if (c.dbg_chunk > 0) nb = std::min(nb, (long)c.dbg_chunk);
+      P.nb = (int)nb;
+    }
     P.x = xin;
     P.y = act(P.Ho, P.Wo, L.cout);
     P.mean = alloc(L.cout * 4); P.rstd = alloc(L.cout * 4);
@@ -298,11 +319,18 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     if (ybytes > max_y) max_y = ybytes;
     {
       ConvWgrad wg{};
-      wg.N = N; wg.H = P.Hin; wg.W = P.Win; wg.Cin = P.cin; wg.Ho = P.Ho; wg.Wo = P.Wo; wg.Cout = L.cout;
+      wg.N = P.nb; wg.H = P.Hin; wg.W = P.Win; wg.Cin = P.cin; wg.Ho = P.Ho; wg.Wo = P.Wo; wg.Cout = L.cout;
       wg.KH = P.k; wg.KW = P.k; wg.stride = P.s; wg.pad = P.p;
       P.splits = conv_wgrad_splits_shape(c.prec, wg, &P.pps);
+      const int rem = N % P.nb;
+      P.splits_r = P.pps_r = 0;
+      if (rem) {
+        wg.N = rem;
+        P.splits_r = conv_wgrad_splits_shape(c.prec, wg, &P.pps_r);
+      }
+      P.wslots = (N / P.nb) * P.splits + P.splits_r;
     }
-    const size_t wp = (size_t)P.splits * L.cout * P.k * P.k * P.cin * 4;
+    const size_t wp = (size_t)P.wslots * L.cout * P.k * P.k * P.cin * 4;
     if (wp > max_wpart) max_wpart = wp;
     // backward partials (2 floats per block and channel) or the forward
     // statistics' chunk sums (3 doubles per chunk and channel, <= 64 chunks)
@@ -371,7 +399,9 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   pl->part = alloc((size_t)max_partC * 4);
   size_t max_bnst = 0;
   for (size_t li = 0; li < a.convs.size(); ++li) {
-    const size_t b = (size_t)ceil_div(pl->cp[li].M, 32) * a.convs[li].cout * 4 * 4;
+    // at most one entry per 32 GEMM rows of each launch
+    const ConvP& P = pl->cp[li];
+    const size_t b = (size_t)(ceil_div(P.M, 32) + ceil_div(N, P.nb)) * a.convs[li].cout * 4 * 4;
     if (b > max_bnst) max_bnst = b;
   }
   pl->bnst = alloc(max_bnst);
@@ -383,9 +413,9 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   pl->wpart = alloc(max_wpart);
   pl->grad = alloc((size_t)a.P * 4);
   pl->total = off;
-  if (max_tensor > kMaxTensorBytes) {
+  if (max_tensor > kMaxWholeTensorBytes) {
     snprintf(buf, sizeof buf, "a %zu-byte tensor exceeds the kernels' per-tensor limit of %zu bytes", max_tensor,
-             kMaxTensorBytes);
+             kMaxWholeTensorBytes);
     *why = buf;
     return RN18_EINVAL;
   }
@@ -479,7 +509,8 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
 // s2d: the operands are the space-to-depth stem's (k = 4, Cin = 16) and the
 // result is mapped back to the 7x7 stem weights; flops are then those of the
 // 7x7 conv.
-int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float* wpart, int N, int H, int W, int Cin,
+// Weight-gradient split-K partials of one launch into wpart[splits][Cout][k*k*Cin].
+int launch_wgrad_part(int prec, const void* dy, const void* x, float* wpart, int N, int H, int W, int Cin,
                       int cin_real, int Ho, int Wo, int Cout, int k, int s, int p, int splits, int pps,
                       hipStream_t st, Ctx* c = nullptr, int layer = -1, bool s2d = false) {
   ConvWgrad g{};
@@ -496,11 +527,27 @@ int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float
                       (double)splits * Cout * g.Kcols * 4);
   int r = conv_wgrad_launch(prec, g, st);
   prof_end(c, pi);
-  if (r) return r;
-  pi = prof_begin(c, RN18_K_WGRAD_REDUCE, layer, 0, "wgrad_reduce_kernel", 0.0, ((double)splits + 1.0) * Cout * g.Kcols * 4);
-  r = wgrad_reduce_launch(wpart, splits, Cout, k * k, Cin, cin_real, out, s2d ? 1 : 0, st);
+  return r;
+}
+
+// Sum of `splits` partial slots into the OIHW fp32 weight gradient.
+int launch_wgrad_reduce(const float* wpart, int splits, int Cout, int k, int Cin, int cin_real, float* out, bool s2d,
+                        hipStream_t st, Ctx* c = nullptr, int layer = -1) {
+  const double kcols = (double)k * k * Cin;
+  const int pi = prof_begin(c, RN18_K_WGRAD_REDUCE, layer, 0, "wgrad_reduce_kernel", 0.0,
+                            ((double)splits + 1.0) * Cout * kcols * 4);
+  const int r = wgrad_reduce_launch(wpart, splits, Cout, k * k, Cin, cin_real, out, s2d ? 1 : 0, st);
   prof_end(c, pi);
   return r;
+}
+
+int launch_wgrad_full(int prec, const void* dy, const void* x, float* out, float* wpart, int N, int H, int W, int Cin,
+                      int cin_real, int Ho, int Wo, int Cout, int k, int s, int p, int splits, int pps,
+                      hipStream_t st, Ctx* c = nullptr, int layer = -1, bool s2d = false) {
+  const int r = launch_wgrad_part(prec, dy, x, wpart, N, H, W, Cin, cin_real, Ho, Wo, Cout, k, s, p, splits, pps, st, c,
+                                  layer, s2d);
+  if (r) return r;
+  return launch_wgrad_reduce(wpart, splits, Cout, k, Cin, cin_real, out, s2d, st, c, layer);
 }
 
 // ----------------------------------------------------------------------------
@@ -566,21 +613,29 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
   auto conv_bn = [&](int li) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
-    ConvGather g = gather_fwd(ws + P.x, W(li), ws + P.y, N, P.Hin, P.Win, P.cin, P.Ho, P.Wo, L.cout, P.k, P.s, P.p);
-    // training: the conv epilogue also writes per-tile BN partials of its output
+    // training: the conv epilogue also writes per-tile BN partials of its
+    // output; the batch chunks append their entries one after another
     float* tstats = (float*)(ws + pl.bnst);
-    if (train) g.stats = tstats;
-    const double xb = (double)N * P.Hin * P.Win * P.cin * es, yb = (double)P.M * L.cout * es;
-    TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(prec, g), conv_gather_kernel_name(prec, g), 2.0 * P.M * L.cout * L.k * L.k * L.cin,
-          xb + yb + (double)L.cout * P.k * P.k * P.cin * es, conv_gather_launch(prec, g, st));
+    const size_t in_img = (size_t)P.Hin * P.Win * P.cin * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
+    long ntiles = 0;
+    for (int n0 = 0; n0 < N; n0 += P.nb) {
+      const int nc = std::min(P.nb, N - n0);
+      ConvGather g = gather_fwd(ws + P.x + n0 * in_img, W(li), ws + P.y + n0 * out_img, nc, P.Hin, P.Win, P.cin,
+                                P.Ho, P.Wo, L.cout, P.k, P.s, P.p);
+      if (train) g.stats = tstats + ntiles * L.cout * 4;
+      const double mc = (double)nc * P.Ho * P.Wo;
+      TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(prec, g), conv_gather_kernel_name(prec, g),
+            2.0 * mc * L.cout * L.k * L.k * L.cin,
+            (double)nc * (in_img + out_img) + (double)L.cout * P.k * P.k * P.cin * es, conv_gather_launch(prec, g, st));
+      if (train) ntiles += conv_gather_stat_entries(prec, g);
+    }
     float* mean = (float*)(ws + P.mean);
     float* rstd = (float*)(ws + P.rstd);
     float* sc = (float*)(ws + P.scale);
     float* sf = (float*)(ws + P.shift);
     if (train) {
-      const int ntiles = conv_gather_stat_entries(prec, g);
       TIMED(RN18_K_BN_STATS, li, 1, "bn_stats_tiles_reduce_kernel", 0.0, (double)ntiles * L.cout * 16,
-            bn_stats_tiles_final_launch(tstats, ntiles, L.cout, (double*)(ws + pl.part), state_c + L.g,
+            bn_stats_tiles_final_launch(tstats, (int)ntiles, L.cout, (double*)(ws + pl.part), state_c + L.g,
                                         state_c + L.b, eps, mom,
                                         state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, st));
     } else {
@@ -702,18 +757,39 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     if (!c->captures.empty()) return run_captures(c, RN18_CAP_DY, li, ws + dy, (size_t)P.M * L.cout * es);
     return 0;
   };
+  // weight gradient: every batch chunk writes its split-K partials to slots
+  // of its own, and one reduction sums all of them
   auto wgrad = [&](int li, size_t dy) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
-    LCHK(launch_wgrad_full(prec, ws + dy, ws + P.x, grad + L.w, (float*)(ws + pl.wpart), pl.N, P.Hin, P.Win, P.cin,
-                           L.cin, P.Ho, P.Wo, L.cout, P.k, P.s, P.p, P.splits, P.pps, st, c, li, P.s2d));
+    const size_t in_img = (size_t)P.Hin * P.Win * P.cin * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
+    const size_t slot = (size_t)L.cout * P.k * P.k * P.cin;
+    float* wpart = (float*)(ws + pl.wpart);
+    int used = 0;
+    for (int n0 = 0; n0 < N; n0 += P.nb) {
+      const int nc = std::min(P.nb, N - n0);
+      const bool full = nc == P.nb;
+      LCHK(launch_wgrad_part(prec, ws + dy + n0 * out_img, ws + P.x + n0 * in_img, wpart + used * slot, nc, P.Hin,
+                             P.Win, P.cin, L.cin, P.Ho, P.Wo, L.cout, P.k, P.s, P.p, full ? P.splits : P.splits_r,
+                             full ? P.pps : P.pps_r, st, c, li, P.s2d));
+      used += full ? P.splits : P.splits_r;
+    }
+    if (used != P.wslots) return fail(RN18_EINVAL, "conv %d: %d weight-gradient partials, planned %d", li, used, P.wslots);
+    LCHK(launch_wgrad_reduce(wpart, used, L.cout, P.k, P.cin, L.cin, grad + L.w, P.s2d, st, c, li));
     return 0;
   };
+  // data gradient over the batch chunks; R (shaped like dx) and its mask
+  // bytes Rm (1/16 of its size) are cut at the same images
   auto dgrad = [&](int li, size_t dy, size_t dx, int mode, size_t R, size_t Rm) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
-    LCHK(launch_dgrad(prec, ws + dy, W_d(li), ws + dx, pl.N, P.Hin, P.Win, L.cin_p, P.Ho, P.Wo, L.cout, L.k, L.s, L.p,
-                      mode, mode == 2 ? ws + R : nullptr, mode == 2 ? ws + Rm : nullptr, st, c, li, L.cin));
+    const size_t in_img = (size_t)P.Hin * P.Win * L.cin_p * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
+    for (int n0 = 0; n0 < N; n0 += P.nb) {
+      const int nc = std::min(P.nb, N - n0);
+      LCHK(launch_dgrad(prec, ws + dy + n0 * out_img, W_d(li), ws + dx + n0 * in_img, nc, P.Hin, P.Win, L.cin_p,
+                        P.Ho, P.Wo, L.cout, L.k, L.s, L.p, mode, mode == 2 ? ws + R + n0 * in_img : nullptr,
+                        mode == 2 ? ws + Rm + n0 * in_img / 16 : nullptr, st, c, li, L.cin));
+    }
     return 0;
   };
 
@@ -1090,6 +1166,14 @@ int rn18_debug_set(rn18_ctx* h, int key, long value) {
     return RN18_OK;
   }
   if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  if (key == RN18_DBG_CONV_CHUNK) {
+    if (value < 0 || value > (1l << 30)) return fail(RN18_EINVAL, "bad chunk size %ld", value);
+    // plans size their scratch for the chunking: drop the ones built so far
+    HIPCHK(hipStreamSynchronize(h->c.stream));
+    h->c.plans.clear();
+    h->c.dbg_chunk = (int)value;
+    return RN18_OK;
+  }
   if (key != RN18_DBG_STOP_BLOCKS) return fail(RN18_EINVAL, "unknown debug key %d", key);
   h->c.dbg_stop_blocks = (int)value;
   return RN18_OK;

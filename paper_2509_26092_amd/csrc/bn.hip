@@ -356,7 +356,7 @@ __global__ __launch_bounds__(256) void bn_apply_pool_kernel(const T* __restrict_
     uint8_t bi[VW];
     pool_max_window<T>(y, n, i, j, cc, H, W, C, act, best, bi);
     ((uint4*)pool)[q] = pack<T>(best);
-    ArgVec<VW>::store(arg + q * VW, bi);
+    ArgVec<VW>::store(arg + (long)q * VW, bi);
   }
 }
 
@@ -568,8 +568,8 @@ int bn_bwd_apply_launch(int prec, const void* dz, const uint8_t* mb, const void*
 
 int bn_apply_pool_launch(int prec, const void* y, const float* scale, const float* shift, void* pool, uint8_t* arg,
                          int N, int H, int W, int C, int Ho, int Wo, hipStream_t s) {
-  if (C > kMaxC || (long)N * H * W * C >= (1l << 31)) return -1;
   const int vw = prec == PREC_BF16 ? 8 : 4;
+  if (C > kMaxC || (long)N * H * W * (C / vw) >= (1l << 31)) return -1;  // 32-bit chunk indices
   const long total = (long)N * Ho * Wo * (C / vw);
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(bn_apply_pool_kernel<bf16_t>, dim3(stream_blocks(total)), dim3(256), 0, s, (const bf16_t*)y,
@@ -583,7 +583,8 @@ int bn_apply_pool_launch(int prec, const void* y, const float* scale, const floa
 int bn_bwd_partial_pool_launch(int prec, const void* dpool, const uint8_t* arg, const void* y, const float* scale,
                                const float* shift, const float* mean, const float* rstd, int N, int H, int W, int C,
                                int Ho, int Wo, float* part, int* nblk, hipStream_t s) {
-  if (C > kMaxC || (long)N * H * W * C >= (1l << 31)) return -1;
+  const int vw = prec == PREC_BF16 ? 8 : 4;
+  if (C > kMaxC || (long)N * H * W * (C / vw) >= (1l << 31)) return -1;  // 32-bit chunk indices
   const int nb = bn_bwd_partial_pool_blocks(prec, N, H, W, C);
   *nblk = nb;
   if (prec == PREC_BF16)
@@ -598,8 +599,8 @@ int bn_bwd_partial_pool_launch(int prec, const void* dpool, const uint8_t* arg, 
 int bn_bwd_apply_pool_launch(int prec, const void* dpool, const uint8_t* arg, const void* y, const float* scale,
                              const float* shift, const float* mean, const float* coef, void* dy, int N, int H, int W,
                              int C, int Ho, int Wo, hipStream_t s) {
-  if (C > kMaxC || (long)N * H * W * C >= (1l << 31)) return -1;
   const int vw = prec == PREC_BF16 ? 8 : 4;
+  if (C > kMaxC || (long)N * H * W * (C / vw) >= (1l << 31)) return -1;  // 32-bit chunk indices
   const long nchunks = (long)N * ((H + 1) / 2) * ((W + 1) / 2) * (C / vw);
   if (prec == PREC_BF16)
     hipLaunchKernelGGL(bn_bwd_apply_pool_kernel<bf16_t>, dim3(stream_blocks(nchunks)), dim3(256), 0, s,

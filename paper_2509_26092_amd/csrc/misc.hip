@@ -200,7 +200,7 @@ __global__ void maxpool_fwd_kernel(const T* __restrict__ x, T* __restrict__ y, u
     uint8_t bi[VW];
     pool_max_window<T>(x, n, i, j, cc, H, W, C, [](float*) {}, best, bi);
     ((uint4*)y)[q] = pack<T>(best);
-    ArgVec<VW>::store(arg + q * VW, bi);
+    ArgVec<VW>::store(arg + (long)q * VW, bi);
   }
 }
 

@@ -57,7 +57,7 @@ __device__ inline void pool_window_pair(const T* __restrict__ dy, const uint8_t*
     const bool in = i < Ho && j + dj < Wo;
     const int oq = ((n * Ho + min(i, Ho - 1)) * Wo + min(j + dj, Wo - 1)) * cpr + cc;
     unpack<T>(((const uint4*)dy)[oq], g[dj]);
-    ArgVec<VW>::load(arg + oq * VW, a[dj]);
+    ArgVec<VW>::load(arg + (long)oq * VW, a[dj]);
 #pragma unroll
     for (int e = 0; e < VW; ++e) a[dj][e] = in ? a[dj][e] : (uint8_t)0xff;
   }

@@ -11,10 +11,11 @@ Here a "measurement" is the device memory in use (hipMemGetInfo) after one
 training step of a fresh context minus the memory in use before it was
 created: the context (momentum, weight shadows, workspace) and the caller's
 state, images, labels and loss. This library adds a second bound besides the
-memory: its kernels address each tensor with 32-bit byte offsets, so a step
-is only planned while every tensor stays below a fixed size;
-`addressing_max_batch` finds that bound with the library's own planner
-(rn18_workspace_bytes returns 0 for a shape it rejects).
+memory: its kernels index each tensor with 32-bit offsets (convolutions are
+launched over batch chunks to stay inside them), so a step is only planned
+while every tensor stays below a fixed size; `addressing_max_batch` finds
+that bound with the library's own planner (rn18_workspace_bytes returns 0
+for a shape it rejects).
 """
 import math
 

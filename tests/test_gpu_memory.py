@@ -9,7 +9,7 @@ from paper_2509_26092_amd import memory as Mm
 
 pytestmark = pytest.mark.gpu
 
-LIMIT = (1 << 31) - (1 << 24)      # per-tensor bytes the kernels address
+LIMIT = 16 * ((1 << 31) - (1 << 24))   # whole-tensor bytes the kernels index (16-byte chunks, 32-bit)
 
 
 def test_memory_model_predicts_larger_steps():
@@ -24,7 +24,7 @@ def test_memory_model_predicts_larger_steps():
     # within the paper's 3.5% (CIFAR-100) at every fitting batch
     for b, m in zip(bs, ms):
         assert abs(m - Mm.predict(p, a, b)) <= 0.035 * m, (b, m)
-    for b in (1024, 2048):
+    for b in (1024, 2048, 9000):                   # 9000: stage-1 convs in two launches
         used, status = Mm.measure_step(B, torch, arch, classes, prec, b, H)
         assert status == B.RN18_OK
         pred = Mm.predict(p, a, b)
@@ -39,6 +39,9 @@ def test_memory_model_predicts_larger_steps():
     ("cifar", 100, "fp32", 16, 16 * 16 * 64 * 4),
 ])
 def test_addressing_bound(arch, classes, prec, H, per_image):
+    """The planner accepts a batch while its largest tensor stays inside the
+    whole-tensor bound (convolutions are launched over batch chunks below
+    the per-launch bound), and rejects the next one."""
     w = B.Worker(arch, classes, prec)
     try:
         nmax = LIMIT // per_image

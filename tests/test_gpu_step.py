@@ -23,16 +23,19 @@ pytestmark = pytest.mark.gpu
 LR = 0.1
 
 
-def _run_parity(arch, classes, prec, N, H, seed, lr=LR, dropout=None):
+def _run_parity(arch, classes, prec, N, H, seed, lr=LR, dropout=None, chunk=0):
     """One step on both sides. The oracle takes the kernel's choice only at
     non-unique points inside the rounding band (ReLU kinks, pool ties and,
     for bf16, rounding midpoints of the stored tensors; see gpu_util), and
     every kernel decision outside the band must agree with the oracle's.
-    dropout: (rate, seed, step) of the classifier-input dropout on both."""
+    dropout: (rate, seed, step) of the classifier-input dropout on both.
+    chunk: launch every convolution over batch chunks of this many images."""
     L, st = make_state(arch, classes, seed)
     x = inputs.images(seed, N, H, H)
     y = inputs.labels(seed, N, classes)
     w = B.Worker(arch, classes, prec)
+    if chunk:
+        B.rn18_debug_set(w.ctx, B.RN18_DBG_CONV_CHUNK, chunk)
     drop = {}
     if dropout is not None:
         B.rn18_set_dropout(w.ctx, *dropout)
@@ -103,6 +106,17 @@ def test_imagenet_odd_resolution(prec, N, H):
     """Odd image sizes: the stem runs as the plain 7x7 stride-2 conv (even
     sizes use its space-to-depth form)."""
     _run_parity("imagenet", 1000, prec, N, H, seed=121 + H)
+
+
+@pytest.mark.parametrize("arch,classes,prec,N,H,chunk", [("tiny", 10, "fp32", 8, 16, 5), ("cifar", 100, "fp32", 8, 16, 3),
+                                                         ("imagenet", 1000, "bf16", 5, 64, 2),
+                                                         ("imagenet", 1000, "fp32", 3, 33, 1)])
+def test_chunked_convolutions(arch, classes, prec, N, H, chunk):
+    """Convolutions launched over batch chunks (as a step does when a tensor
+    would pass the kernels' 32-bit byte offsets), forced small here: BN
+    statistics entries, weight-gradient partials, residual and mask operands
+    are cut at the chunk boundaries, including a shorter last chunk."""
+    _run_parity(arch, classes, prec, N, H, seed=180 + N, chunk=chunk)
 
 
 def test_two_steps_with_momentum():
@@ -244,21 +258,22 @@ def test_imagenet_bf16_b256_224_launch_config_properties():
     w.close()
 
 
-def test_imagenet_bf16_largest_planned_batch_224():
-    """The largest batch the planner accepts at 224x224 (its stem output,
-    1.6 MB per image, just under the kernels' per-tensor limit), run as two
-    copies of 663 images: the step succeeds; stem-conv outputs of images at
-    the start, middle and end of the batch (byte offsets close to 2^31) equal
-    the oracle's conv of those images; the loss and the stem BN mean equal
-    those of the 663 images alone; eval logits of the last image match the
-    oracle run on it alone."""
+def test_imagenet_bf16_first_chunked_batch_224():
+    """Two copies of 664 images at 224x224: 1,328 stem outputs (1.6 MB each)
+    pass the kernels' per-launch limit by one image, so the stem conv runs
+    as a chunk of 1,327 images and one of 1; later layers still run whole.
+    The step succeeds; stem-conv outputs of images at the start, middle and
+    end of the batch (the last one alone in its chunk) equal the oracle's
+    conv of those images; the loss and the stem BN mean equal those of the
+    664 images alone; eval logits of the last image match the oracle run on
+    it alone."""
     import torch
     from gpu_util import assert_close, from_dev_nhwc
     from oracle import ops
-    arch, classes, prec, half = "imagenet", 1000, "bf16", 663
+    arch, classes, prec, half = "imagenet", 1000, "bf16", 664
     N = 2 * half
     limit = (1 << 31) - (1 << 24)
-    assert N * 112 * 112 * 64 * 2 <= limit < (N + 2) * 112 * 112 * 64 * 2
+    assert (N - 1) * 112 * 112 * 64 * 2 <= limit < N * 112 * 112 * 64 * 2
     L, st = make_state(arch, classes, 151)
     x = inputs.images(151, half, 224, 224)
     y = inputs.labels(151, half, classes)
@@ -267,7 +282,7 @@ def test_imagenet_bf16_largest_planned_batch_224():
     z = np.zeros(L.n_trainable)
     w = B.Worker(arch, classes, prec)
     try:
-        print("largest batch: N=%d at 224" % N, flush=True)
+        print("chunked stem: N=%d at 224" % N, flush=True)
         sN, vN, lN, stN = gpu_train_step(arch, classes, prec, st, xx, yy, LR, worker=w, momentum_in=z)
         assert stN == B.RN18_OK and np.all(np.isfinite(vN))
         wst = ops.round_bf16(L.get(st, "stem.w"))
