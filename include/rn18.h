@@ -26,9 +26,11 @@
  *    launched: RN18_EINVAL for null pointers, non-positive sizes, a layer
  *    whose output would be empty, a batch-norm layer with only one value per
  *    channel (N*Ho*Wo == 1), a shape with a tensor of more than
- *    2^31 - 2^24 bytes (the kernels address each tensor with 32-bit byte
- *    offsets; at 224x224 that caps an ImageNet bf16 step near 1,300 images,
- *    see rn18_workspace_bytes), or a non-finite factor. rn18_last_error()
+ *    16 * (2^31 - 2^24) bytes (about 34 GB: the kernels index tensors with
+ *    32-bit offsets, and a step launches each convolution over batch chunks
+ *    whose tensors stay below 2^31 - 2^24 bytes; at 224x224 an ImageNet bf16
+ *    step takes up to 21,232 images, more than 288 GB of memory hold; see
+ *    rn18_workspace_bytes), or a non-finite factor. rn18_last_error()
  *    returns a thread-local description of the last non-OK return.
  *  - Errors found on the device (a label outside [0, C), a non-finite loss)
  *    set a sticky flag of the context; rn18_sync_status reports and clears it.
