@@ -174,7 +174,7 @@ struct Plan {
   int Hs, Ws, Hp, Wp;           // stem output and pool output sizes
   int Hf, Wf;                   // final feature map
   size_t f, logits, dlogits, df, rowloss, lossbuf;
-  size_t gA, gB, gz, gy, gyd;
+  size_t gA, gB, gz, gy, gy2, gyd;  // gy, gy2: dY of the second and first conv of a block
   size_t part, wpart, grad;
   size_t bnst;                  // forward conv epilogue BN partials (one entry per 32 rows at most)
   size_t total;
@@ -199,6 +199,10 @@ struct Ctx {
   uint32_t drop_thresh = 0;
   float drop_scale = 1.f;
   uint64_t drop_seed = 0, drop_step = 0;
+  // weight gradients run on a second stream (default priority) beside the
+  // data-gradient chain: events hand each dY buffer over and back
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_buf[3] = {nullptr, nullptr, nullptr};
   void* ws = nullptr;
   size_t ws_bytes = 0;
   bool ws_owned = false;
@@ -395,6 +399,7 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   pl->gB = alloc(max_blockio);
   pl->gz = alloc(max_z1 ? max_z1 : 16);
   pl->gy = alloc(max_y);
+  pl->gy2 = alloc(max_y);
   pl->gyd = alloc(max_yd ? max_yd : 16);
   pl->part = alloc((size_t)max_partC * 4);
   size_t max_bnst = 0;
@@ -586,6 +591,16 @@ int get_plan(Ctx* c, int N, int H, int W, const Plan** out) {
   return RN18_OK;
 }
 
+void destroy_side(Ctx& c) {
+  if (c.side) {
+    (void)hipStreamSynchronize(c.side);
+    (void)hipStreamDestroy(c.side);
+    c.side = nullptr;
+  }
+  for (hipEvent_t* e : {&c.ev_fork, &c.ev_join, &c.ev_buf[0], &c.ev_buf[1], &c.ev_buf[2]})
+    if (*e) { (void)hipEventDestroy(*e); *e = nullptr; }
+}
+
 int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, const float* images, bool train) {
   const Arch& a = c->arch;
   char* ws = (char*)c->ws;
@@ -759,7 +774,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   };
   // weight gradient: every batch chunk writes its split-K partials to slots
   // of its own, and one reduction sums all of them
-  auto wgrad = [&](int li, size_t dy) -> int {
+  auto wgrad_on = [&](int li, size_t dy, hipStream_t ws_st) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     const size_t in_img = (size_t)P.Hin * P.Win * P.cin * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
@@ -771,13 +786,51 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
       const bool full = nc == P.nb;
       LCHK(launch_wgrad_part(prec, ws + dy + n0 * out_img, ws + P.x + n0 * in_img, wpart + used * slot, nc, P.Hin,
                              P.Win, P.cin, L.cin, P.Ho, P.Wo, L.cout, P.k, P.s, P.p, full ? P.splits : P.splits_r,
-                             full ? P.pps : P.pps_r, st, c, li, P.s2d));
+                             full ? P.pps : P.pps_r, ws_st, c, li, P.s2d));
       used += full ? P.splits : P.splits_r;
     }
     if (used != P.wslots) return fail(RN18_EINVAL, "conv %d: %d weight-gradient partials, planned %d", li, used, P.wslots);
-    LCHK(launch_wgrad_reduce(wpart, used, L.cout, P.k, P.cin, L.cin, grad + L.w, P.s2d, st, c, li));
+    LCHK(launch_wgrad_reduce(wpart, used, L.cout, P.k, P.cin, L.cin, grad + L.w, P.s2d, ws_st, c, li));
     return 0;
   };
+  // With the side stream (not while profiling or capturing): a weight
+  // gradient starts on it once its dY buffer is written on the main stream,
+  // and the main stream waits for it before it writes that buffer again and
+  // before the SGD update. The weight gradients only read dY, the forward
+  // activations and their own split-K scratch, and write their own slices
+  // of the gradient, so the data-gradient chain runs on meanwhile.
+  const bool ov = c->side && !c->prof_on && c->captures.empty();
+  const size_t dybuf[3] = {pl.gy, pl.gy2, pl.gyd};
+  bool pending[3] = {false, false, false}, forked = false;
+  auto buf_id = [&](size_t b) { return b == pl.gy ? 0 : b == pl.gy2 ? 1 : 2; };
+  auto before_write = [&](size_t b) -> int {
+    const int i = buf_id(b);
+    if (ov && pending[i]) {
+      HIPCHK(hipStreamWaitEvent(st, c->ev_buf[i], 0));
+      pending[i] = false;
+    }
+    return 0;
+  };
+  auto wgrad = [&](int li, size_t dy) -> int {
+    if (!ov) return wgrad_on(li, dy, st);
+    HIPCHK(hipEventRecord(c->ev_fork, st));
+    HIPCHK(hipStreamWaitEvent(c->side, c->ev_fork, 0));
+    forked = true;
+    if (int r2 = wgrad_on(li, dy, c->side)) return r2;
+    const int i = buf_id(dy);
+    HIPCHK(hipEventRecord(c->ev_buf[i], c->side));
+    pending[i] = true;
+    return 0;
+  };
+  auto join = [&]() -> int {
+    if (!forked) return 0;
+    HIPCHK(hipEventRecord(c->ev_join, c->side));
+    HIPCHK(hipStreamWaitEvent(st, c->ev_join, 0));
+    forked = false;
+    pending[0] = pending[1] = pending[2] = false;
+    return 0;
+  };
+  (void)dybuf;
   // data gradient over the batch chunks; R (shaped like dx) and its mask
   // bytes Rm (1/16 of its size) are cut at the same images
   auto dgrad = [&](int li, size_t dy, size_t dx, int mode, size_t R, size_t Rm) -> int {
@@ -795,26 +848,26 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
 
   int done = 0;
   for (int bi = (int)a.blocks.size() - 1; bi >= 0; --bi) {
-    if (c->dbg_stop_blocks >= 0 && done++ == c->dbg_stop_blocks) return RN18_OK;
+    if (c->dbg_stop_blocks >= 0 && done++ == c->dbg_stop_blocks) return join();
     const BlockL& B = a.blocks[bi];
     const BlockP& bp = pl.bp[bi];
     // gA = gradient wrt the block output (before its ReLU mask)
-    if ((r = bn_back(B.c2, gA, bp.mbits, pl.gy))) return r;
-    if (B.ds >= 0 && (r = bn_back(B.ds, gA, bp.mbits, pl.gyd))) return r;
-    if ((r = wgrad(B.c2, pl.gy))) return r;
-    if ((r = dgrad(B.c2, pl.gy, pl.gz, 0, 0, 0))) return r;
+    if ((r = before_write(pl.gy)) || (r = bn_back(B.c2, gA, bp.mbits, pl.gy))) return join(), r;
+    if (B.ds >= 0 && ((r = before_write(pl.gyd)) || (r = bn_back(B.ds, gA, bp.mbits, pl.gyd)))) return join(), r;
+    if ((r = wgrad(B.c2, pl.gy))) return join(), r;
+    if ((r = dgrad(B.c2, pl.gy, pl.gz, 0, 0, 0))) return join(), r;
     const size_t z1b = (size_t)pl.cp[B.c1].M * a.convs[B.c1].cout * es;
     const size_t inb = (size_t)N * pl.cp[B.c1].Hin * pl.cp[B.c1].Win * a.convs[B.c1].cin_p * es;
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DZ1, bi, ws + pl.gz, z1b))) return r;
-    if ((r = bn_back(B.c1, pl.gz, RECOMPUTE, pl.gy))) return r;
-    if ((r = wgrad(B.c1, pl.gy))) return r;
+    if ((r = before_write(pl.gy2)) || (r = bn_back(B.c1, pl.gz, RECOMPUTE, pl.gy2))) return join(), r;
+    if ((r = wgrad(B.c1, pl.gy2))) return join(), r;
     if (B.ds >= 0) {
-      if ((r = dgrad(B.c1, pl.gy, gB, 0, 0, 0))) return r;
+      if ((r = dgrad(B.c1, pl.gy2, gB, 0, 0, 0))) return join(), r;
       if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX1, bi, ws + gB, inb))) return r;
-      if ((r = wgrad(B.ds, pl.gyd))) return r;
-      if ((r = dgrad(B.ds, pl.gyd, gB, 1, 0, 0))) return r;
+      if ((r = wgrad(B.ds, pl.gyd))) return join(), r;
+      if ((r = dgrad(B.ds, pl.gyd, gB, 1, 0, 0))) return join(), r;
     } else {
-      if ((r = dgrad(B.c1, pl.gy, gB, 2, gA, bp.mbits))) return r;
+      if ((r = dgrad(B.c1, pl.gy2, gB, 2, gA, bp.mbits))) return join(), r;
     }
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX, bi, ws + gB, inb))) return r;
     std::swap(gA, gB);
@@ -835,6 +888,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const float* sc = (const float*)(ws + P.scale);
     const float* sf = (const float*)(ws + P.shift);
     const double yb = (double)P.M * C0 * es, pb = (double)N * pl.Hp * pl.Wp * C0 * (es + 1);
+    if ((r = before_write(pl.gy))) return join(), r;
     TIMED(RN18_K_BN_BWD_REDUCE, 0, 0, kernel_instance_name("bn_bwd_partial_pool_kernel", prec), 0.0, yb + pb,
           bn_bwd_partial_pool_launch(prec, ws + gA, parg, ws + P.y, sc, sf, (float*)(ws + P.mean),
                                      (float*)(ws + P.rstd), N, pl.Hs, pl.Ws, C0, pl.Hp, pl.Wp, part, &nblk, st));
@@ -845,10 +899,10 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
           bn_bwd_apply_pool_launch(prec, ws + gA, parg, ws + P.y, sc, sf, (float*)(ws + P.mean),
                                    (float*)(ws + P.coef), ws + pl.gy, N, pl.Hs, pl.Ws, C0, pl.Hp, pl.Wp, st));
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DY, 0, ws + pl.gy, (size_t)P.M * C0 * es))) return r;
-  } else if ((r = bn_back(0, gA, RECOMPUTE, pl.gy))) {
-    return r;
+  } else if ((r = before_write(pl.gy)) || (r = bn_back(0, gA, RECOMPUTE, pl.gy))) {
+    return join(), r;
   }
-  if ((r = wgrad(0, pl.gy))) return r;
+  if ((r = wgrad(0, pl.gy)) || (r = join())) return join(), r;
   TIMED(RN18_K_SGD, 0, 0, "sgd_kernel", 0.0, 20.0 * a.P,
         sgd_launch(state, grad, c->momentum, a.P, lr, c->cfg.momentum, c->cfg.weight_decay, st));
   return RN18_OK;
@@ -939,6 +993,15 @@ int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* st
   if (hipMalloc(&c.wf, a.wf_total * c.es + 16) != hipSuccess) return bail(RN18_ENOMEM, "weight shadow allocation failed");
   if (hipMalloc(&c.wd, a.wd_total * c.es + 16) != hipSuccess) return bail(RN18_ENOMEM, "weight shadow allocation failed");
   if (hipMalloc(&c.err, 256) != hipSuccess) return bail(RN18_ENOMEM, "flag allocation failed");
+  if (hipStreamCreateWithFlags(&c.side, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&c.ev_fork, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c.ev_join, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c.ev_buf[0], hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c.ev_buf[1], hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c.ev_buf[2], hipEventDisableTiming) != hipSuccess) {
+    destroy_side(c);
+    return bail(RN18_EHIP, "stream or event creation failed");
+  }
   std::vector<RepackEntry> tab, ttab;
   long pre = 0, tpre = 0;
   for (const auto& L : a.convs) {
@@ -1120,6 +1183,7 @@ void rn18_destroy(rn18_ctx* h) {
   if (c.tab) (void)hipFree(c.tab);
   if (c.err) (void)hipFree(c.err);
   if (c.ws_owned && c.ws) (void)hipFree(c.ws);
+  destroy_side(c);
   for (auto& ev : c.prof) { (void)hipEventDestroy(ev.a); (void)hipEventDestroy(ev.b); }
   for (auto e : c.prof_spare) (void)hipEventDestroy(e);
   delete h;

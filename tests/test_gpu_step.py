@@ -119,6 +119,29 @@ def test_chunked_convolutions(arch, classes, prec, N, H, chunk):
     _run_parity(arch, classes, prec, N, H, seed=180 + N, chunk=chunk)
 
 
+@pytest.mark.parametrize("arch,classes,prec,N,H", [("imagenet", 1000, "bf16", 16, 64), ("cifar", 100, "fp32", 16, 32)])
+def test_weight_gradients_on_side_stream_match_serial(arch, classes, prec, N, H):
+    """The weight gradients run on a second stream beside the data-gradient
+    chain; with profiling on, every launch stays on the caller's stream. Two
+    steps from the same state, one each way, agree bit for bit."""
+    L, st = make_state(arch, classes, 190)
+    x = inputs.images(190, N, H, H)
+    y = inputs.labels(190, N, classes)
+    z = np.zeros(L.n_trainable)
+    out = []
+    for serial in (False, True):
+        w = B.Worker(arch, classes, prec)
+        try:
+            B.rn18_profile_enable(w.ctx, serial)
+            s1, v1, l1, status = gpu_train_step(arch, classes, prec, st, x, y, LR, steps=2, worker=w, momentum_in=z)
+            assert status == B.RN18_OK
+            out.append((s1, v1, l1))
+        finally:
+            w.close()
+    assert np.array_equal(out[0][0], out[1][0]) and np.array_equal(out[0][1], out[1][1])
+    assert out[0][2] == out[1][2]
+
+
 def test_two_steps_with_momentum():
     arch, classes, prec, N, H, seed = "tiny", 10, "fp32", 8, 16, 130
     L, st = make_state(arch, classes, seed)
