@@ -210,8 +210,10 @@ def progress(msg):
     print("bench: " + msg, file=sys.stderr, flush=True)
 
 
-def run_shape(B, torch, inputs, arch, classes, prec, N, H, steps, warmup, seed=1, dropout=0.0):
+def run_shape(B, torch, inputs, arch, classes, prec, N, H, steps, warmup, seed=1, dropout=0.0, serial=False):
     w = B.Worker(arch, classes, prec)
+    if serial:
+        B.rn18_debug_set(w.ctx, B.RN18_DBG_SERIAL, 1)
     if dropout:
         B.rn18_set_dropout(w.ctx, dropout, seed, 0)
     st = torch.zeros(w.n_state, device="cuda")
@@ -359,6 +361,9 @@ def main():
     ap.add_argument("--shape-steps", type=int, default=8, help="timed steps per additional step shape")
     ap.add_argument("--headline-only", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--serial", action="store_true",
+                    help="keep every launch of the headline steps on one stream (no weight-gradient overlap), so "
+                         "that a kernel trace times each kernel alone, as the profiled step does")
     ap.add_argument("--cpu-images", type=int, default=40)
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/hbm_traffic.json from the counter_collection.csv files of a FETCH_SIZE "
@@ -393,7 +398,8 @@ def main():
     look = traffic_lookup_factory()
 
     name, arch, classes, prec, N, H = HEADLINE
-    dt, recs, status, lval = run_shape(B, torch, inputs, arch, classes, prec, N, H, args.steps, args.warmup)
+    dt, recs, status, lval = run_shape(B, torch, inputs, arch, classes, prec, N, H, args.steps, args.warmup,
+                                       serial=args.serial)
     head_sum, by_sym = summarize(recs, prec)
     roof = roofline(by_sym, prec, look)
     roof["share_of_kernel_time"] = round(by_sym[roof["kernel"]]["ms"] / head_sum["kernel_ms"], 4)

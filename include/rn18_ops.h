@@ -86,7 +86,11 @@ enum {
    * over batch chunks of at most `value` images (0 = only where a tensor
    * would exceed the kernels' 32-bit byte offsets). Plans built before are
    * dropped. For testing the chunked path at small sizes. */
-  RN18_DBG_CONV_CHUNK = 3
+  RN18_DBG_CONV_CHUNK = 3,
+  /* per context: value != 0 keeps every launch of a training step on the
+   * caller's stream (the weight gradients otherwise run on a second stream
+   * beside the data-gradient chain). For timing kernels one at a time. */
+  RN18_DBG_SERIAL = 4
 };
 enum {
   RN18_DBG_Y = 0, RN18_DBG_Z1 = 1, RN18_DBG_OUT = 2, RN18_DBG_GA = 3, RN18_DBG_GB = 4, RN18_DBG_GZ = 5,

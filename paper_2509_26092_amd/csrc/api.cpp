@@ -209,6 +209,7 @@ struct Ctx {
   std::map<std::tuple<int, int, int>, Plan> plans;
   int dbg_stop_blocks = -1;     // debugging: end the backward pass after this many blocks
   int dbg_chunk = 0;            // debugging: at most this many images per convolution launch (0 = as needed)
+  bool dbg_serial = false;      // debugging: every launch on the caller's stream (no side stream)
   struct Capture { int kind, index; void* dst; size_t bytes; };
   std::vector<Capture> captures; // debugging: copies of backward tensors
   // optional per-launch timing with HIP events on the context stream
@@ -799,7 +800,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   // before the SGD update. The weight gradients only read dY, the forward
   // activations and their own split-K scratch, and write their own slices
   // of the gradient, so the data-gradient chain runs on meanwhile.
-  const bool ov = c->side && !c->prof_on && c->captures.empty();
+  const bool ov = c->side && !c->dbg_serial && !c->prof_on && c->captures.empty();
   const size_t dybuf[3] = {pl.gy, pl.gy2, pl.gyd};
   bool pending[3] = {false, false, false}, forked = false;
   auto buf_id = [&](size_t b) { return b == pl.gy ? 0 : b == pl.gy2 ? 1 : 2; };
@@ -1236,6 +1237,10 @@ int rn18_debug_set(rn18_ctx* h, int key, long value) {
     HIPCHK(hipStreamSynchronize(h->c.stream));
     h->c.plans.clear();
     h->c.dbg_chunk = (int)value;
+    return RN18_OK;
+  }
+  if (key == RN18_DBG_SERIAL) {
+    h->c.dbg_serial = value != 0;
     return RN18_OK;
   }
   if (key != RN18_DBG_STOP_BLOCKS) return fail(RN18_EINVAL, "unknown debug key %d", key);
