@@ -177,6 +177,7 @@ struct Plan {
   size_t gA, gB, gz, gy, gy2, gyd;  // gy, gy2: dY of the second and first conv of a block
   size_t part, wpart, grad;
   size_t bnst;                  // forward conv epilogue BN partials (one entry per 32 rows at most)
+  size_t bnst2, part2;          // the same scratch for the projection convs, which run on the side stream
   size_t total;
 };
 
@@ -202,7 +203,7 @@ struct Ctx {
   // weight gradients run on a second stream (default priority) beside the
   // data-gradient chain: events hand each dY buffer over and back
   hipStream_t side = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_buf[3] = {nullptr, nullptr, nullptr};
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_ds = nullptr, ev_buf[3] = {nullptr, nullptr, nullptr};
   void* ws = nullptr;
   size_t ws_bytes = 0;
   bool ws_owned = false;
@@ -411,6 +412,18 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     if (b > max_bnst) max_bnst = b;
   }
   pl->bnst = alloc(max_bnst);
+  {
+    size_t mb = 16, mp = 16;
+    for (const BlockL& B : a.blocks) {
+      if (B.ds < 0) continue;
+      const ConvP& P = pl->cp[B.ds];
+      const size_t cout = a.convs[B.ds].cout;
+      mb = std::max(mb, (size_t)(ceil_div(P.M, 32) + ceil_div(N, P.nb)) * cout * 16);
+      mp = std::max(mp, (size_t)64 * cout * 3 * 8);
+    }
+    pl->bnst2 = alloc(mb);
+    pl->part2 = alloc(mp);
+  }
   // the weight-gradient split-K scratch also holds the classifier's split-K
   // partials (the classifier runs before any weight gradient)
   for (size_t hw : {gemm_f32_workspace(N, C, a.feat), gemm_f32_workspace(C, a.feat, N),
@@ -598,7 +611,7 @@ void destroy_side(Ctx& c) {
     (void)hipStreamDestroy(c.side);
     c.side = nullptr;
   }
-  for (hipEvent_t* e : {&c.ev_fork, &c.ev_join, &c.ev_buf[0], &c.ev_buf[1], &c.ev_buf[2]})
+  for (hipEvent_t* e : {&c.ev_fork, &c.ev_join, &c.ev_ds, &c.ev_buf[0], &c.ev_buf[1], &c.ev_buf[2]})
     if (*e) { (void)hipEventDestroy(*e); *e = nullptr; }
 }
 
@@ -626,12 +639,14 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
           (double)N * pl.H * pl.W * (12.0 + a.convs[0].cin_p * es),
           ingest_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, a.convs[0].cin_p, st));
 
-  auto conv_bn = [&](int li) -> int {
+  // conv + BN statistics of layer li on stream cs with the BN scratch at
+  // bnst_off / part_off
+  auto conv_bn_on = [&](int li, hipStream_t cs, size_t bnst_off, size_t part_off) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     // training: the conv epilogue also writes per-tile BN partials of its
     // output; the batch chunks append their entries one after another
-    float* tstats = (float*)(ws + pl.bnst);
+    float* tstats = (float*)(ws + bnst_off);
     const size_t in_img = (size_t)P.Hin * P.Win * P.cin * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
     long ntiles = 0;
     for (int n0 = 0; n0 < N; n0 += P.nb) {
@@ -642,7 +657,7 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
       const double mc = (double)nc * P.Ho * P.Wo;
       TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(prec, g), conv_gather_kernel_name(prec, g),
             2.0 * mc * L.cout * L.k * L.k * L.cin,
-            (double)nc * (in_img + out_img) + (double)L.cout * P.k * P.k * P.cin * es, conv_gather_launch(prec, g, st));
+            (double)nc * (in_img + out_img) + (double)L.cout * P.k * P.k * P.cin * es, conv_gather_launch(prec, g, cs));
       if (train) ntiles += conv_gather_stat_entries(prec, g);
     }
     float* mean = (float*)(ws + P.mean);
@@ -651,14 +666,18 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     float* sf = (float*)(ws + P.shift);
     if (train) {
       TIMED(RN18_K_BN_STATS, li, 1, "bn_stats_tiles_reduce_kernel", 0.0, (double)ntiles * L.cout * 16,
-            bn_stats_tiles_final_launch(tstats, (int)ntiles, L.cout, (double*)(ws + pl.part), state_c + L.g,
+            bn_stats_tiles_final_launch(tstats, (int)ntiles, L.cout, (double*)(ws + part_off), state_c + L.g,
                                         state_c + L.b, eps, mom,
-                                        state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, st));
+                                        state_rs + L.rm, state_rs + L.rv, mean, rstd, sc, sf, cs));
     } else {
-      LCHK(bn_eval_coef_launch(state_c + L.g, state_c + L.b, state_c + L.rm, state_c + L.rv, eps, L.cout, sc, sf, st));
+      LCHK(bn_eval_coef_launch(state_c + L.g, state_c + L.b, state_c + L.rm, state_c + L.rv, eps, L.cout, sc, sf, cs));
     }
     return 0;
   };
+  auto conv_bn = [&](int li) -> int { return conv_bn_on(li, st, pl.bnst, pl.part); };
+  // the projection conv of a downsampling block reads only the block input:
+  // with the side stream it runs there beside the block's first two convs
+  const bool ovf = c->side && !c->dbg_serial && !c->prof_on && c->captures.empty();
   // mb: offset of the mask bytes to write (block outputs of a training step), or 0
   auto apply = [&](int li, int relu, int res_mode, size_t r, int li2, size_t z, size_t mb = 0) -> int {
     const ConvL& L = a.convs[li];
@@ -690,11 +709,22 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
   for (size_t bi = 0; bi < a.blocks.size(); ++bi) {
     const BlockL& B = a.blocks[bi];
     const BlockP& bp = pl.bp[bi];
+    const bool side_ds = ovf && B.ds >= 0;
+    if (side_ds) {
+      HIPCHK(hipEventRecord(c->ev_fork, st));
+      HIPCHK(hipStreamWaitEvent(c->side, c->ev_fork, 0));
+      if ((r = conv_bn_on(B.ds, c->side, pl.bnst2, pl.part2))) return r;
+      HIPCHK(hipEventRecord(c->ev_ds, c->side));
+    }
     if ((r = conv_bn(B.c1))) return r;
     if ((r = apply(B.c1, 1, 0, 0, -1, bp.z1))) return r;
     if ((r = conv_bn(B.c2))) return r;
     if (B.ds >= 0) {
-      if ((r = conv_bn(B.ds))) return r;
+      if (side_ds) {
+        HIPCHK(hipStreamWaitEvent(st, c->ev_ds, 0));
+      } else if ((r = conv_bn(B.ds))) {
+        return r;
+      }
       if ((r = apply(B.c2, 1, 2, pl.cp[B.ds].y, B.ds, bp.out, train ? bp.mbits : 0))) return r;
     } else {
       if ((r = apply(B.c2, 1, 1, bp.in, -1, bp.out, train ? bp.mbits : 0))) return r;
@@ -997,6 +1027,7 @@ int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* st
   if (hipStreamCreateWithFlags(&c.side, hipStreamNonBlocking) != hipSuccess ||
       hipEventCreateWithFlags(&c.ev_fork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c.ev_join, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c.ev_ds, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c.ev_buf[0], hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c.ev_buf[1], hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c.ev_buf[2], hipEventDisableTiming) != hipSuccess) {
