@@ -291,6 +291,72 @@ def dbl_plan(B, torch, inputs, by, merge_ms, steps):
             "stages": out}
 
 
+def measured_rounds(B, torch, inputs, reps, factor=0.5):
+    """Dual-batch rounds of the ImageNet hybrid schedule timed end to end:
+    both workers pull the global state, the large worker (B_L at the stage's
+    resolution) and the small worker (batch 64) take one step each, push
+    their deltas, and ps_dual_merge applies them with the model-update
+    factor (Sec. 3.4). 'sequential' runs everything on one stream;
+    'concurrent' gives each worker its own stream (default priority), so the
+    small step fills what the large one leaves of the chip, as two workers
+    sharing one GPU would."""
+    cfg = B.make_config("imagenet", 1000, "bf16")
+    n = B.rn18_state_floats(cfg)[0]
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    out = []
+    for r, bl in ((128, 1024), (160, 640), (192, 448), (224, 256)):
+        xl = torch.from_numpy(inputs.images(11, bl, r, r)).cuda()
+        yl = torch.from_numpy(inputs.labels(11, bl, 1000)).cuda()
+        xs = torch.from_numpy(inputs.images(12, 64, r, r)).cuda()
+        ys = torch.from_numpy(inputs.labels(12, 64, 1000)).cuda()
+        row = {"resolution": r, "B_L": bl, "B_S": 64, "factor": factor}
+        for mode in ("sequential", "concurrent"):
+            s2 = sb if mode == "concurrent" else sa
+            g = torch.zeros(n, device="cuda")
+            B.rn18_destroy(B.rn18_init(cfg, 1, g))
+            with torch.cuda.stream(sa):
+                wl = B.Worker("imagenet", 1000, "bf16")
+            with torch.cuda.stream(s2):
+                wsm = B.Worker("imagenet", 1000, "bf16")
+            sl, ss, dl, ds = (torch.empty_like(g) for _ in range(4))
+            ll, ls = torch.zeros(1, device="cuda"), torch.zeros(1, device="cuda")
+            torch.cuda.synchronize()
+
+            def one_round():
+                e = torch.cuda.Event()
+                e.record(sa)                      # the merged global state
+                with torch.cuda.stream(sa):
+                    sl.copy_(g)
+                    wl.train_step(sl, xl, yl, 0.01, ll)
+                s2.wait_event(e)
+                with torch.cuda.stream(s2):
+                    ss.copy_(g)
+                    wsm.train_step(ss, xs, ys, 0.01, ls)
+                sa.wait_stream(s2)
+                with torch.cuda.stream(sa):
+                    B.ps_worker_delta(g, sl, dl, n)
+                    B.ps_worker_delta(g, ss, ds, n)
+                    B.ps_dual_merge(g, ds, dl, n, factor)
+
+            for _ in range(2):
+                one_round()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                one_round()
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) / reps * 1e3
+            status = max(abs(wl.sync_status()), abs(wsm.sync_status()))
+            wl.close()
+            wsm.close()
+            row[mode] = {"round_ms": round(ms, 3), "round_images_per_s": round((bl + 64) / ms * 1e3, 1),
+                         "status": status}
+        progress("rounds at %d: sequential %.3f ms, concurrent %.3f ms"
+                 % (r, row["sequential"]["round_ms"], row["concurrent"]["round_ms"]))
+        out.append(row)
+    return {"workload": "dbl_rounds_measured_imagenet_bf16", "stages": out}
+
+
 def memory_model(B, torch):
     """Sec. 5.3: device memory of steps at B = 64..512 (hipMemGetInfo), the
     Eq. 9 fit, the largest batch for this GPU's memory, the library's own
@@ -434,6 +500,7 @@ def main():
                           "ms": round(mms, 4), "GBps": round(mgbs, 1), "hbm_frac": round(mgbs / HBM_PEAK, 4),
                           "hybrid_rounds": rounds})
         per_shape.append(dbl_plan(B, torch, inputs, by, mms, args.shape_steps))
+        per_shape.append(measured_rounds(B, torch, inputs, args.shape_steps))
         per_shape.append(memory_model(B, torch))
 
     if args.calibrate:
