@@ -91,3 +91,53 @@ def test_dual_batch_round(arch, classes, prec, H, bl, bs, factor):
         o, shp = L.off[key]
         k = int(np.prod(shp))
         assert_close(p0[o:o + k] - got[o:o + k], p0[o:o + k] - ref[o:o + k], tol, key + " merged update")
+
+
+@pytest.mark.parametrize("prec,H,bl,bs", [("bf16", 64, 24, 8), ("fp32", 33, 6, 3)])
+def test_round_with_a_stream_per_worker_matches_one_stream(prec, H, bl, bs):
+    """Two dual-batch rounds with each worker's context on its own stream
+    (they run concurrently on the GPU) end in the same global state, bit for
+    bit, as the same rounds with both workers on one stream."""
+    import torch
+    arch, classes = "imagenet", 1000
+    L, st = make_state(arch, classes, 210)
+    xl = torch.from_numpy(inputs.images(211, bl, H, H)).cuda()
+    yl = torch.from_numpy(inputs.labels(211, bl, classes)).cuda()
+    xs = torch.from_numpy(inputs.images(212, bs, H, H)).cuda()
+    ys = torch.from_numpy(inputs.labels(212, bs, classes)).cuda()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    finals = []
+    for concurrent in (False, True):
+        s2 = sb if concurrent else sa
+        g = torch.from_numpy(st.astype(np.float32)).cuda()
+        n = g.numel()
+        with torch.cuda.stream(sa):
+            wl = B.Worker(arch, classes, prec)
+        with torch.cuda.stream(s2):
+            wsm = B.Worker(arch, classes, prec)
+        sl, ss, dl, ds = (torch.empty_like(g) for _ in range(4))
+        torch.cuda.synchronize()
+        try:
+            for _ in range(2):
+                e = torch.cuda.Event()
+                e.record(sa)
+                with torch.cuda.stream(sa):
+                    sl.copy_(g)
+                    wl.train_step(sl, xl, yl, 0.05)
+                s2.wait_event(e)
+                with torch.cuda.stream(s2):
+                    ss.copy_(g)
+                    wsm.train_step(ss, xs, ys, 0.05)
+                sa.wait_stream(s2)
+                with torch.cuda.stream(sa):
+                    B.ps_worker_delta(g, sl, dl, n)
+                    B.ps_worker_delta(g, ss, ds, n)
+                    B.ps_dual_merge(g, ds, dl, n, 0.5)
+            torch.cuda.synchronize()
+            assert wl.sync_status() == B.RN18_OK and wsm.sync_status() == B.RN18_OK
+            finals.append(g.cpu().numpy())
+        finally:
+            wl.close()
+            wsm.close()
+    assert np.all(np.isfinite(finals[0]))
+    assert np.array_equal(finals[0], finals[1])
