@@ -100,13 +100,14 @@ enum {
 /* rn18_debug_capture(ctx, kind, index, dst, bytes): during later train
  * steps, copy a backward-pass tensor to dst as soon as it is produced:
  * RN18_CAP_DY (index = conv layer: the gradient entering its conv),
- * RN18_CAP_DZ1 (block: data gradient of its second conv), RN18_CAP_DX1
- * (projection block: data gradient of its first conv alone), RN18_CAP_DX
- * (block: gradient wrt the block input), RN18_CAP_DA_AVG (gradient entering
+ * RN18_CAP_DZ1 (block: data gradient of its second conv), RN18_CAP_DX
+ * (block: gradient wrt the block input; in a projection block the data
+ * gradients of the first conv and of the projection are summed in one GEMM
+ * and rounded once), RN18_CAP_DA_AVG (gradient entering
  * the last block from the average pool), RN18_CAP_DA_POOL (max-pool data
  * gradient). dst = NULL clears every capture. */
 enum {
-  RN18_CAP_DY = 0, RN18_CAP_DZ1 = 1, RN18_CAP_DX1 = 2, RN18_CAP_DX = 3, RN18_CAP_DA_AVG = 4, RN18_CAP_DA_POOL = 5
+  RN18_CAP_DY = 0, RN18_CAP_DZ1 = 1, RN18_CAP_DX = 3, RN18_CAP_DA_AVG = 4, RN18_CAP_DA_POOL = 5
 };
 int rn18_debug_capture(struct rn18_ctx* ctx, int kind, int index, void* dst, size_t bytes);
 int rn18_debug_set(struct rn18_ctx* ctx, int key, long value);

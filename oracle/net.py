@@ -136,13 +136,14 @@ class Config:
 #   ("da_avg", 0)   gradient entering the last block (avg-pool backward)
 #   ("dy", conv)    BN backward output, the gradient entering the conv
 #   ("dz1", block)  data gradient of the block's second conv
-#   ("dx1", block)  projection blocks: data gradient of the first conv alone
-#   ("dx", block)   gradient wrt the block input (first conv's data gradient
-#                   plus the shortcut's: masked output gradient for identity
-#                   blocks, added before rounding; the projection conv's data
-#                   gradient added to the rounded dx1, then rounded again)
+#   ("dx", block)   gradient wrt the block input: the first conv's data
+#                   gradient plus the shortcut's (the masked output gradient
+#                   of an identity block, the projection conv's data gradient
+#                   otherwise), summed exactly and rounded once
 #   ("da_pool", 0)  max-pool backward output
-ROUNDING_POINTS = ("y", "z", "da_avg", "dy", "dz1", "dx1", "dx", "da_pool")
+# Every stored tensor is rounded once, from its exact value, and is consumed
+# only in its rounded form.
+ROUNDING_POINTS = ("y", "z", "da_avg", "dy", "dz1", "dx", "da_pool")
 
 
 def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=True, decide=None):
@@ -270,10 +271,7 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
         dz1 = rb(("dz1", bi), bn_conv_back(blk["c2"], g2))
         g1 = dz1 * masks[("z1", bi)]
         dx = bn_conv_back(blk["c1"], g1)
-        if blk["ds"]:
-            dx = rb(("dx1", bi), dx) + bn_conv_back(blk["ds"], g2)
-        else:
-            dx = dx + g2
+        dx = dx + (bn_conv_back(blk["ds"], g2) if blk["ds"] else g2)
         da = rb(("dx", bi), dx)
     if cfg.arch == "imagenet":
         da = rb(("da_pool", 0), ops.maxpool_backward(da, pool_arg, stem_out.shape))

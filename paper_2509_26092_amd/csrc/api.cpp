@@ -463,10 +463,16 @@ ConvGather gather_fwd(const void* x, const void* w, void* y, int N, int Hin, int
 
 // Data gradient of a conv with input [N][H][W][Cin] and output [N][Ho][Wo][Cout].
 // mode: 0 store, 1 accumulate, 2 add masked residual (R, Rm).
+// dy2, wd2 (stride 2 only): the data gradient of a 1x1 stride-2 pad-0
+// projection of the same input ([N][Ho][Wo][Cout] and [Cin][Cout]) is added
+// inside the GEMM of parity phase (0,0), the only phase it reaches, so the
+// block-input gradient is rounded once.
 int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int H, int W, int Cin, int Ho, int Wo,
                  int Cout, int k, int s, int p, int mode, const void* R, const void* Rm, hipStream_t st,
-                 Ctx* c = nullptr, int layer = -1, int cin_real = 0) {
+                 Ctx* c = nullptr, int layer = -1, int cin_real = 0, const void* dy2 = nullptr,
+                 const void* wd2 = nullptr) {
   const double creal = cin_real > 0 ? cin_real : Cin;
+  if (dy2 && (s != 2 || !wd2)) return -1;
   if (s == 1) {
     ConvGather g{};
     g.A = dy; g.B = wd; g.C = dx; g.R = R; g.Rm = Rm;
@@ -509,11 +515,15 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
       g.wkh0 = kh0; g.wkhs = 2; g.wkw0 = kw0; g.wkws = 2; g.KW = k; g.KHW = k * k;
       g.K = nth * ntw * Cout;
       g.mode = mode;
-      if (g.K == 0) {
+      if (dy2 && ph == 0 && pw == 0) {
+        // output pixel (2i, 2j) of the projection's data gradient is dy2[i][j] x wd2
+        g.A2 = dy2; g.B2 = wd2; g.K2 = Cout;
+      }
+      if (g.K == 0 && g.K2 == 0) {
         if (mode == 1) continue;   // nothing to add
         g.nth = 1; g.ntw = 1;      // K = 0: the kernel writes acc = 0 (+ residual)
       }
-      flops += 2.0 * g.M * creal * g.K;
+      flops += 2.0 * g.M * creal * (g.K + g.K2);
       ph4[np++] = g;
     }
   if (np == 0) return 0;
@@ -633,11 +643,12 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
           repack_launch(prec, state_c, c->wf, c->wd, c->tab, c->ntab, c->tab_total, st));
   if (pl.cp[0].s2d)
     TIMED(RN18_K_PREP, -1, 1, kernel_instance_name("ingest_s2d_kernel", prec), 0.0,
-          (double)N * pl.H * pl.W * (12.0 + 4.0 * es), ingest_s2d_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, st));
+          (double)N * pl.H * pl.W * (12.0 + 4.0 * es),
+          ingest_s2d_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, c->err, st));
   else
     TIMED(RN18_K_PREP, -1, 1, kernel_instance_name("ingest_kernel", prec), 0.0,
           (double)N * pl.H * pl.W * (12.0 + a.convs[0].cin_p * es),
-          ingest_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, a.convs[0].cin_p, st));
+          ingest_launch(prec, images, ws + pl.x0, N, pl.H, pl.W, a.convs[0].cin_p, c->err, st));
 
   // conv + BN statistics of layer li on stream cs with the BN scratch at
   // bnst_off / part_off
@@ -863,16 +874,27 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   };
   (void)dybuf;
   // data gradient over the batch chunks; R (shaped like dx) and its mask
-  // bytes Rm (1/16 of its size) are cut at the same images
-  auto dgrad = [&](int li, size_t dy, size_t dx, int mode, size_t R, size_t Rm) -> int {
+  // bytes Rm (1/16 of its size) are cut at the same images. With lds >= 0
+  // (the block's projection conv, dY in dys) the projection's data gradient
+  // is summed into the same GEMM (phase (0,0) of the stride-2 data gradient).
+  auto dgrad = [&](int li, size_t dy, size_t dx, int mode, size_t R, size_t Rm, int lds = -1,
+                   size_t dys = 0) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     const size_t in_img = (size_t)P.Hin * P.Win * L.cin_p * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
+    if (lds >= 0) {
+      const ConvL& D = a.convs[lds];
+      const ConvP& PD = pl.cp[lds];
+      if (L.s != 2 || D.k != 1 || D.s != 2 || D.p != 0 || D.cin != L.cin || D.cout != L.cout || PD.Ho != P.Ho ||
+          PD.Wo != P.Wo || PD.nb != P.nb)
+        return fail(RN18_EINVAL, "conv %d: projection %d cannot join its data gradient", li, lds);
+    }
     for (int n0 = 0; n0 < N; n0 += P.nb) {
       const int nc = std::min(P.nb, N - n0);
       LCHK(launch_dgrad(prec, ws + dy + n0 * out_img, W_d(li), ws + dx + n0 * in_img, nc, P.Hin, P.Win, L.cin_p,
                         P.Ho, P.Wo, L.cout, L.k, L.s, L.p, mode, mode == 2 ? ws + R + n0 * in_img : nullptr,
-                        mode == 2 ? ws + Rm + n0 * in_img / 16 : nullptr, st, c, li, L.cin));
+                        mode == 2 ? ws + Rm + n0 * in_img / 16 : nullptr, st, c, li, L.cin,
+                        lds >= 0 ? ws + dys + n0 * out_img : nullptr, lds >= 0 ? W_d(lds) : nullptr));
     }
     return 0;
   };
@@ -893,10 +915,8 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     if ((r = before_write(pl.gy2)) || (r = bn_back(B.c1, pl.gz, RECOMPUTE, pl.gy2))) return join(), r;
     if ((r = wgrad(B.c1, pl.gy2))) return join(), r;
     if (B.ds >= 0) {
-      if ((r = dgrad(B.c1, pl.gy2, gB, 0, 0, 0))) return join(), r;
-      if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX1, bi, ws + gB, inb))) return r;
       if ((r = wgrad(B.ds, pl.gyd))) return join(), r;
-      if ((r = dgrad(B.ds, pl.gyd, gB, 1, 0, 0))) return join(), r;
+      if ((r = dgrad(B.c1, pl.gy2, gB, 0, 0, 0, B.ds, pl.gyd))) return join(), r;
     } else {
       if ((r = dgrad(B.c1, pl.gy2, gB, 2, gA, bp.mbits))) return join(), r;
     }
@@ -1282,7 +1302,8 @@ int rn18_debug_set(rn18_ctx* h, int key, long value) {
 int rn18_debug_capture(rn18_ctx* h, int kind, int index, void* dst, size_t bytes) {
   if (!h) return fail(RN18_EINVAL, "ctx is NULL");
   if (!dst) { h->c.captures.clear(); return RN18_OK; }
-  if (kind < RN18_CAP_DY || kind > RN18_CAP_DA_POOL) return fail(RN18_EINVAL, "unknown capture kind %d", kind);
+  if (kind < RN18_CAP_DY || kind > RN18_CAP_DA_POOL || kind == 2)
+    return fail(RN18_EINVAL, "unknown capture kind %d", kind);
   h->c.captures.push_back(Ctx::Capture{kind, index, dst, bytes});
   return RN18_OK;
 }

@@ -580,9 +580,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
   const int sw = lane & 7;
 
   // ---- issue side: the tile whose stages are being loaded
-  int is_tile = slot - G, is_s = 0, is_S = 0;
+  constexpr int UB = IPW - UA;
+  int is_tile = slot - G, is_s = 0, is_S = 0, is_S1 = 0;
   uint32_t uoff[IPW], umask[UA];
-  i32x4_t rsA, rsB;
+  uint32_t uoff2[UB], umask2 = 0;   // second K segment: B2 offsets, A2 row validity (bit u)
+  i32x4_t rsA, rsB, rsA2, rsB2;
   int st_ti = 0, st_th = 0, st_tw = 0, st_cb = 0;
   int q_dh0 = 0, q_dhs = 0, q_dw0 = 0, q_dws = 0, q_wkh0 = 0, q_wkhs = 0, q_wkw0 = 0, q_wkws = 0;
   int q_KW = 0, q_Win = 0, q_Cin = 0, q_RT = 1, q_ntwg = 1, q_CB = 1;
@@ -597,7 +599,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
       is_tile += G;
       if (is_tile >= total) return false;
       const ConvGather& g = gs.p[find_prob(is_tile)];
-      is_S = (g.K + KT - 1) / KT;
+      is_S1 = (g.K + KT - 1) / KT;
+      is_S = is_S1 + g.K2 / KT;
       is_s = 0;
       if (is_S == 0) continue;
       const int pr = find_prob(is_tile);
@@ -614,6 +617,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
       rsA = buffer_rsrc(g.A, (uint32_t)((long)g.N * g.Hin * g.Win * g.Cin * es));
       rsB = buffer_rsrc(g.B, (uint32_t)((long)g.Cols * g.KHW * g.Cin * es));
       const int lane_px = (c * VW) / g.Cin;
+      umask2 = 0;
 #pragma unroll
       for (int u = 0; u < UA; ++u) {
         const int m = m0 + (wave_u + NW * u) * 8 + (lane >> 3);
@@ -630,11 +634,17 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
         for (int th = 0; th < g.nth; ++th) msk |= (vh >> th) & 1u ? vw << (th * q_ntwg) : 0u;
         umask[u] = ok ? msk : 0u;
         uoff[u] = (uint32_t)(((n * g.Hin + hb) * g.Win + wb) * g.Cin * es + c * 16);
+        if (ok && (unsigned)hb < (unsigned)g.Hin && (unsigned)wb < (unsigned)g.Win) umask2 |= 1u << u;
       }
 #pragma unroll
       for (int u = UA; u < IPW; ++u) {
         const int col = n0 + (wave_u + NW * u - AI) * 8 + (lane >> 3);
         uoff[u] = col < g.Cols ? (uint32_t)((long)col * g.KHW * g.Cin * es + c * 16) : kOutOfRange;
+        uoff2[u - UA] = col < g.Cols ? (uint32_t)((long)col * g.Cin * es + c * 16) : kOutOfRange;
+      }
+      if (g.K2 > 0) {
+        rsA2 = buffer_rsrc(g.A2, (uint32_t)((long)g.N * g.Hin * g.Win * g.Cin * es));
+        rsB2 = buffer_rsrc(g.B2, (uint32_t)((long)g.Cols * g.Cin * es));
       }
       st_ti = st_th = st_tw = st_cb = 0;
       return true;
@@ -645,28 +655,43 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
   // issue the next stage of the stream into its ring buffer; false when the stream has ended
   auto issue_next = [&]() {
     if (!more) return;
-    const int dh = q_dh0 + st_th * q_dhs, dw = q_dw0 + st_tw * q_RT * q_dws;
-    const int wt = (q_wkh0 + st_th * q_wkhs) * q_KW + q_wkw0 + st_tw * q_RT * q_wkws;
-    const uint32_t sa = (uint32_t)((dh * q_Win + dw) * q_Cin * es + st_cb * 128);
-    const uint32_t sb = (uint32_t)(wt * q_Cin * es + st_cb * 128);
     const uint32_t base =
         __builtin_amdgcn_readfirstlane(smem_lds + (uint32_t)((n_issued % STAGES) * STAGE_U4 * 16));
+    if (is_s >= is_S1) {
+      // second K segment: channel block is_s - is_S1 of A2 at the row's own pixel, and of B2
+      const uint32_t s2 = (uint32_t)((is_s - is_S1) * 128);
 #pragma unroll
-    for (int u = 0; u < UA; ++u) {
-      const uint32_t v = (umask[u] >> st_ti) & 1u ? uoff[u] + sa : kOutOfRange;
-      lds_dma16_buf(v, rsA, base + (uint32_t)((wave_u + NW * u) * 1024));
-    }
+      for (int u = 0; u < UA; ++u) {
+        const uint32_t v = (umask2 >> u) & 1u ? uoff[u] + s2 : kOutOfRange;
+        lds_dma16_buf(v, rsA2, base + (uint32_t)((wave_u + NW * u) * 1024));
+      }
 #pragma unroll
-    for (int u = UA; u < IPW; ++u) {
-      const uint32_t v = uoff[u] == kOutOfRange ? kOutOfRange : uoff[u] + sb;
-      lds_dma16_buf(v, rsB, base + (uint32_t)((AI + wave_u + NW * (u - UA)) * 1024));
+      for (int u = UA; u < IPW; ++u) {
+        const uint32_t v = uoff2[u - UA] == kOutOfRange ? kOutOfRange : uoff2[u - UA] + s2;
+        lds_dma16_buf(v, rsB2, base + (uint32_t)((AI + wave_u + NW * (u - UA)) * 1024));
+      }
+    } else {
+      const int dh = q_dh0 + st_th * q_dhs, dw = q_dw0 + st_tw * q_RT * q_dws;
+      const int wt = (q_wkh0 + st_th * q_wkhs) * q_KW + q_wkw0 + st_tw * q_RT * q_wkws;
+      const uint32_t sa = (uint32_t)((dh * q_Win + dw) * q_Cin * es + st_cb * 128);
+      const uint32_t sb = (uint32_t)(wt * q_Cin * es + st_cb * 128);
+#pragma unroll
+      for (int u = 0; u < UA; ++u) {
+        const uint32_t v = (umask[u] >> st_ti) & 1u ? uoff[u] + sa : kOutOfRange;
+        lds_dma16_buf(v, rsA, base + (uint32_t)((wave_u + NW * u) * 1024));
+      }
+#pragma unroll
+      for (int u = UA; u < IPW; ++u) {
+        const uint32_t v = uoff[u] == kOutOfRange ? kOutOfRange : uoff[u] + sb;
+        lds_dma16_buf(v, rsB, base + (uint32_t)((AI + wave_u + NW * (u - UA)) * 1024));
+      }
+      if (++st_cb == q_CB) {
+        st_cb = 0;
+        ++st_ti;
+        if (++st_tw == q_ntwg) { st_tw = 0; ++st_th; }
+      }
     }
     ++n_issued;
-    if (++st_cb == q_CB) {
-      st_cb = 0;
-      ++st_ti;
-      if (++st_tw == q_ntwg) { st_tw = 0; ++st_th; }
-    }
     if (++is_s == is_S) more = next_issue_tile();
   };
 
@@ -677,7 +702,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
   for (int tile = slot; tile < total; tile += G) {
     const int pr = find_prob(tile);
     const ConvGather& g = gs.p[pr];
-    const int S = (g.K + KT - 1) / KT;
+    const int S = (g.K + KT - 1) / KT + g.K2 / KT;
     floatx4_t acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -2387,8 +2412,16 @@ int cu_count() {
   return n[dev];
 }
 
+// A second K segment must have whole channel blocks, A2 shaped like A and
+// B2 [Cols][Cin], within the 32-bit buffer offsets.
+bool gather_seg2_ok(const ConvGather& g, int kt) {
+  const long es = 128 / kt;
+  return g.A2 && g.B2 && g.K2 == g.Cin && g.Cin % kt == 0 &&
+         (long)g.N * g.Hin * g.Win * g.Cin * es < (1l << 31) && (long)g.Cols * g.Cin * es < (1l << 31);
+}
+
 // One persistent launch over the tiles of np sub-problems (all of the uniform
-// row layout); -1 if one is not.
+// row layout); -1 if one is not, -2 if a second K segment cannot run.
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES>
 int launch_gather_ps(const ConvGather* probs, int np, hipStream_t s) {
   if (np < 1 || np > 4) return -1;
@@ -2398,8 +2431,9 @@ int launch_gather_ps(const ConvGather* probs, int np, hipStream_t s) {
   long total = 0;
   for (int i = 0; i < np; ++i) {
     ConvGather g = probs[i];
-    if (!gather_uniform(g, kt)) return -1;
+    if (!gather_uniform(g, kt)) return g.K2 ? -2 : -1;
     if ((long)g.N * g.Hout * g.Wout * g.Cols >= (1l << 31)) return -1;  // 32-bit output offsets
+    if (g.K2 && !gather_seg2_ok(g, kt)) return -2;
     g.fd_hw = FastDiv((uint32_t)(g.Hm * g.Wm));
     g.fd_w = FastDiv((uint32_t)g.Wm);
     g.zero = nullptr;
@@ -2625,23 +2659,31 @@ int gather_tile(int prec, const ConvGather& g) {
 // The parity phases of a stride-2 data gradient run in one persistent grid
 // (measured on MI355X at bf16 224x224 batch 256: 256x64 tiles for up to 64
 // columns, 128x128 for 128, 128x64 above).
+// A launch with a second K segment always takes the persistent kernel (the
+// only one that runs it), whatever configuration is forced.
+bool gather_has_seg2(const ConvGather* g, int np) {
+  for (int i = 0; i < np; ++i)
+    if (g[i].K2) return true;
+  return false;
+}
 int gather_cfg_multi(const ConvGather* g, int np) {
-  if (g_gather_override || np < 2) return gather_cfg(g[0]);
+  if (!gather_has_seg2(g, np) && (g_gather_override || np < 2)) return gather_cfg(g[0]);
   return g[0].Cols <= 64 ? 35 : g[0].Cols <= 128 ? 36 : 37;
 }
 
 template <typename T>
 int gather_dispatch(const ConvGather* g, int np, hipStream_t s) {
   const int prec = sizeof(T) == 2 ? PREC_BF16 : PREC_F32;
-  if (np == 1 && use_halo(prec, g[0])) return launch_halo(g[0], halo_rows(prec, g[0]), s);
-  if (np == 1 && use_halo16(prec, g[0])) return launch_halo16(g[0], halo16_rows(prec, g[0]), s);
-  if (np == 1 && use_haloW(prec, g[0])) return launch_haloW(g[0], haloW_rows(prec, g[0]), s);
+  const bool seg2 = gather_has_seg2(g, np);
+  if (!seg2 && np == 1 && use_halo(prec, g[0])) return launch_halo(g[0], halo_rows(prec, g[0]), s);
+  if (!seg2 && np == 1 && use_halo16(prec, g[0])) return launch_halo16(g[0], halo16_rows(prec, g[0]), s);
+  if (!seg2 && np == 1 && use_haloW(prec, g[0])) return launch_haloW(g[0], haloW_rows(prec, g[0]), s);
   switch (gather_cfg_multi(g, np)) {
 #define RN18_X(id, bm, bn, wgm, wgn, st, kind)                                               \
   case id:                                                                                 \
     if constexpr (kind == 2) {                                                             \
       const int r = launch_gather_ps<T, bm, bn, wgm, wgn, st>(g, np, s);                   \
-      if (r != -1) return r;                                                               \
+      if (r != -1 || seg2) return r;                                                       \
     }                                                                                      \
     for (int i = 0; i < np; ++i) {                                                         \
       const int r = g[i].M > 0 ? launch_gather2<T, bm, bn, wgm, wgn, st, kind == 1>(g[i], s) : 0; \
@@ -2785,7 +2827,7 @@ const char* conv_gather_kernel_name(int prec, const ConvGather& g) {
 }
 
 const char* conv_gather_kernel_name_multi(int prec, const ConvGather* g, int np) {
-  if (np == 1) return conv_gather_kernel_name(prec, g[0]);
+  if (np == 1 && !g[0].K2) return conv_gather_kernel_name(prec, g[0]);
   return gather_kernel_name(prec, g[0], gather_cfg_multi(g, np));
 }
 
@@ -2828,7 +2870,7 @@ const char* kernel_instance_name(const char* base, int prec) {
 int conv_gather_tile(int prec, const ConvGather& g) { return gather_tile(prec, g); }
 
 int conv_gather_tile_multi(int prec, const ConvGather* g, int np) {
-  if (np == 1) return gather_tile(prec, g[0]);
+  if (np == 1 && !g[0].K2) return gather_tile(prec, g[0]);
   const int id = gather_cfg_multi(g, np);
   return id >= 1 && id <= kGatherCfgs ? kGather[id].bm * 1000 + kGather[id].bn : 0;
 }

@@ -27,6 +27,16 @@ struct ConvGather {
   FastDiv fd_hw, fd_w;       // division by Hm*Wm and by Wm (set by the launcher)
   float* stats;              // optional BN partials (rows, shift, sum, sum sq) [tiles_m][Cols][4] of the stored output
   const void* zero;          // 16-byte zero page (set by the launcher)
+  // Optional second K segment, summed into the same accumulators before the
+  // epilogue: C[m][col] += sum_ci A2[pixel(hb, wb)][ci] * B2[col][ci], where
+  // (hb, wb) = (i*is-ip, j*is-ip) is the row's input base itself (tap offset
+  // 0). A2 is shaped like A ([N][Hin][Win][Cin]) and B2 is [Cols][Cin];
+  // K2 = Cin, or 0 for none. Only the persistent multi-phase kernel takes
+  // it (the projection shortcut's data gradient fused into parity phase
+  // (0,0) of the block's stride-2 data gradient).
+  const void* A2;
+  const void* B2;
+  int K2;
 };
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s);
 // Up to four sub-problems of one operation (the parity phases of a stride-2
@@ -132,11 +142,12 @@ int bn_bwd_apply_launch(int prec, const void* dz, const uint8_t* mb, const void*
 // ---------------------------------------------------------------------------
 // Misc streams
 // ---------------------------------------------------------------------------
-int ingest_launch(int prec, const float* img, void* x, int N, int H, int W, int Cp, hipStream_t s);
+// A non-finite image value sets DEVERR_NONFINITE in *err.
+int ingest_launch(int prec, const float* img, void* x, int N, int H, int W, int Cp, unsigned* err, hipStream_t s);
 // NCHW fp32 images (3 channels, H and W even) -> 2x2 space-to-depth NHWC
 // [N][H/2][W/2][16]: channel (2*dy + dx)*3 + c holds pixel (2i+dy, 2j+dx) of
 // channel c; channels 12..15 are zero.
-int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, hipStream_t s);
+int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, unsigned* err, hipStream_t s);
 // mode 0: OIHW -> [Cout][KHW][Cin_p] (+ [Cin_p][KHW][Cout] when dst_d >= 0);
 // mode 1: the 7x7 stride-2 stem (Cin 3) as a 4x4 conv over its 2x2
 // space-to-depth input: [Cout][4x4][16], channel (2*dy + dx)*3 + c.

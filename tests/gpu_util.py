@@ -74,24 +74,30 @@ def make_state(arch, classes, seed):
 
 # Width of the band around a ReLU kink (|pre-activation| <= TAU * rms of the
 # site) and around a max-pool tie (top-2 gap) inside which the choice of
-# subgradient depends on the precision the value was computed in: the GPU's
-# fp32 conv sums differ from exact ones by ~1e-6 relative; bf16 storage of
-# every activation moves values by ~0.4% per layer.
-TAU = {"fp32": 1e-4, "bf16": 5e-2}
+# subgradient depends on the order of the fp32 sums that produced the value:
+# the GPU's fp32 conv sums differ from exact ones by ~1e-6 relative. The
+# same band serves bf16 steps, whose stored values the oracle mirrors
+# exactly (see Mirror), so their kinks and ties are decided on the same
+# values on both sides.
+TAU = 1e-4
 
 
 class Decider:
     """Decision rule for the oracle at non-unique points: keep the oracle's
     own ReLU mask / argmax everywhere, except at inputs the oracle itself
     finds within the rounding band, where the kernel's choice (read back
-    from the stored activations) is taken. Counts how many choices were
-    taken and how many GPU decisions outside the band disagree (must be 0)."""
+    from the stored activations) is taken if it is a valid one (a pool tap
+    inside the image whose value is within the band of the window maximum).
+    Counts how many choices were taken, how many in-band choices were
+    invalid and how many GPU decisions outside the band disagree (both must
+    be 0)."""
 
     def __init__(self, worker, N, H, prec, tau):
         self.w, self.N, self.H, self.prec, self.tau = worker, N, H, prec, tau
         self.ambiguous = 0
         self.taken = 0
         self.outside = 0
+        self.invalid = 0
         self.sites = 0
         self.log = []
 
@@ -129,6 +135,12 @@ class Decider:
             amb = (top2[0] - top2[1]) <= self.tau * rms
             garg = self._fetch("parg", 0, arg.shape, torch.uint8).astype(np.int64)
             gmask = garg
+            # a kernel's tap is acceptable only if it lies inside the image
+            # and its value is within the band of the window's maximum
+            tap = np.take_along_axis(taps, np.clip(garg, 0, 8)[None], axis=0)[0]
+            valid = (garg >= 0) & (garg <= 8) & np.isfinite(tap) & (top2[0] - tap <= self.tau * rms)
+            self.invalid += int((amb & ~valid).sum())
+            amb = amb & valid
         self.ambiguous += int(amb.sum())
         self.outside += int(((gmask != default) & ~amb).sum())
         chosen = np.where(amb, gmask, default)
@@ -148,7 +160,7 @@ def tensor_shapes(L, N, H):
     for bi, blk in enumerate(L.blocks):
         _, cin, cout, k, s, p = L.spec[blk["c1"]]
         ho = ops.conv_out_size(h, 3, s, 1)
-        sh[("dx1", bi)] = sh[("dx", bi)] = (N, cin, h, h)
+        sh[("dx", bi)] = (N, cin, h, h)
         for cname in (blk["c1"], blk["c2"]) + ((blk["ds"],) if blk["ds"] else ()):
             sh[("y", cname)] = sh[("dy", cname)] = (N, cout, ho, ho)
         sh[("z", ("z1", bi))] = sh[("dz1", bi)] = sh[("z", ("out", bi))] = (N, cout, ho, ho)
@@ -188,11 +200,9 @@ class Mirror(Decider):
         self.shapes = tensor_shapes(L, N, H)
         self.conv_index = {c[0]: i for i, c in enumerate(L.convs)}
         self.cap = {}
-        kinds = {"dy": "dy", "dz1": "dz1", "dx1": "dx1", "dx": "dx", "da_avg": "da_avg", "da_pool": "da_pool"}
+        kinds = {"dy": "dy", "dz1": "dz1", "dx": "dx", "da_avg": "da_avg", "da_pool": "da_pool"}
         for (kind, idx), (n, c, h, w) in self.shapes.items():
             if kind not in kinds:
-                continue
-            if kind == "dx1" and not L.blocks[idx]["ds"]:
                 continue
             if kind == "da_pool" and L.arch != "imagenet":
                 continue
@@ -200,6 +210,8 @@ class Mirror(Decider):
             t = torch.full((n, h, w, c), float("nan"), dtype=torch_dtype(prec), device="cuda")
             B.rn18_debug_capture(worker.ctx, kind, index, t)
             self.cap[(kind, idx)] = t
+        import time
+        self.t0 = time.time()
         self.round_outside = 0
         self.round_invalid = 0
         self.round_taken = 0
@@ -220,6 +232,10 @@ class Mirror(Decider):
         return from_dev_nhwc(self.cap[point])
 
     def __call__(self, kind, site, pre, default):
+        if self.N * self.H * self.H >= 1 << 22:
+            # large comparisons take minutes: report each stored tensor as it is checked
+            import time
+            print("  %s %s  %.1f s" % (kind, site, time.time() - self.t0), flush=True)
         if kind != "round":
             return super().__call__(kind, site, pre, default)
         exact, b = pre, default

@@ -63,9 +63,9 @@ def test_dual_batch_round(arch, classes, prec, H, bl, bs, factor):
     wl, ws = B.Worker(arch, classes, prec), B.Worker(arch, classes, prec)
     bf = prec == "bf16"
     if bf:
-        dl_, ds_ = Mirror(wl, L, bl, H, prec, TAU["fp32"]), Mirror(ws, L, bs, H, prec, TAU["fp32"])
+        dl_, ds_ = Mirror(wl, L, bl, H, prec, TAU), Mirror(ws, L, bs, H, prec, TAU)
     else:
-        dl_, ds_ = Decider(wl, bl, H, prec, TAU[prec]), Decider(ws, bs, H, prec, TAU[prec])
+        dl_, ds_ = Decider(wl, bl, H, prec, TAU), Decider(ws, bs, H, prec, TAU)
     pl, _, _, _ = gpu_train_step(arch, classes, prec, p0, xl, yl, lr, worker=wl)
     ps, _, _, _ = gpu_train_step(arch, classes, prec, p0, xs, ys, lr, worker=ws)
     n = L.n_state
@@ -80,7 +80,7 @@ def test_dual_batch_round(arch, classes, prec, H, bl, bs, factor):
     cfg = net.Config(arch, classes, bf16=bf, round_acts=bf)
     sl, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xl, yl, lr, decide=dl_)
     ss, _, _, _ = net.train_step(cfg, L, p0, np.zeros(L.n_trainable), xs, ys, lr, decide=ds_)
-    assert dl_.outside == 0 and ds_.outside == 0
+    assert dl_.outside == 0 and ds_.outside == 0 and dl_.invalid == 0 and ds_.invalid == 0
     if bf:
         assert dl_.round_outside == 0 and ds_.round_outside == 0 and dl_.round_invalid == 0
     wl.close()
