@@ -32,8 +32,10 @@
  *    step takes up to 21,232 images, more than 288 GB of memory hold; see
  *    rn18_workspace_bytes), or a non-finite factor. rn18_last_error()
  *    returns a thread-local description of the last non-OK return.
- *  - Errors found on the device (a label outside [0, C), a non-finite loss)
- *    set a sticky flag of the context; rn18_sync_status reports and clears it.
+ *  - Errors found on the device (a label outside [0, C), a non-finite image
+ *    value or a non-finite loss) set a sticky flag of the context; the call
+ *    still runs to completion, and rn18_sync_status reports and clears the
+ *    flag.
  *  - No C++ exception crosses this interface.
  */
 #ifndef RN18_H
@@ -69,7 +71,7 @@ typedef enum { RN18_TINY = 0, RN18_CIFAR = 1, RN18_IMAGENET = 2 } rn18_arch;
  * RN18_BF16: images, conv weights and activations (and their gradients) in
  * bf16 with fp32 accumulation; master weights, momentum, BN statistics, the
  * classifier and the loss in fp32. This is the mixed precision of the
- * paper's ImageNet runs (Sec. 5.2.1), taken as bf16 without loss scaling. */
+ * paper's ImageNet runs (Sec. 5.2.3), taken as bf16 without loss scaling. */
 typedef enum { RN18_FP32 = 0, RN18_BF16 = 1 } rn18_prec;
 
 typedef struct {

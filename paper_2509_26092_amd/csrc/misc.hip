@@ -23,18 +23,24 @@ int grid_for(long work, int per_block = 256, int cap = 16384) {
 }
 
 // ------------------------------------------------------------------ ingest
+// A non-finite image value sets the sticky DEVERR_NONFINITE flag (a NaN
+// could otherwise vanish in a ReLU and leave a finite loss).
 template <typename T>
-__global__ void ingest_kernel(const float* __restrict__ img, T* __restrict__ x, long npix, int HW, int Cp) {
+__global__ void ingest_kernel(const float* __restrict__ img, T* __restrict__ x, long npix, int HW, int Cp,
+                              unsigned* err) {
   for (long p = blockIdx.x * 256l + threadIdx.x; p < npix; p += (long)gridDim.x * 256) {
     const long n = p / HW, hw = p - n * HW;
     const float* src = img + n * 3 * HW + hw;
     float v[8] = {src[0], src[HW], src[2 * HW], 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (!(__builtin_isfinite(v[0]) && __builtin_isfinite(v[1]) && __builtin_isfinite(v[2])))
+      atomicOr(err, (unsigned)DEVERR_NONFINITE);
     ((uint4*)x)[p] = pack<T>(v);  // Cp elements = exactly 16 bytes
   }
 }
 
 template <typename T>
-__global__ void ingest_s2d_kernel(const float* __restrict__ img, T* __restrict__ x, long npix, int H, int W) {
+__global__ void ingest_s2d_kernel(const float* __restrict__ img, T* __restrict__ x, long npix, int H, int W,
+                                  unsigned* err) {
   constexpr int VW = TT<T>::VW;
   const int Hs = H / 2, Ws = W / 2;
   const long HW = (long)H * W;
@@ -48,6 +54,10 @@ __global__ void ingest_s2d_kernel(const float* __restrict__ img, T* __restrict__
     for (int q = 0; q < 4; ++q)
 #pragma unroll
       for (int c = 0; c < 3; ++c) v[q * 3 + c] = src[c * HW + (q >> 1) * W + (q & 1)];
+    bool fin = true;
+#pragma unroll
+    for (int c = 0; c < 12; ++c) fin = fin && __builtin_isfinite(v[c]);
+    if (!fin) atomicOr(err, (unsigned)DEVERR_NONFINITE);
 #pragma unroll
     for (int c = 12; c < 16; ++c) v[c] = 0.f;
 #pragma unroll
@@ -462,22 +472,26 @@ __global__ void fill_zero_kernel(uint32_t* __restrict__ p, long nwords) {
 
 }  // namespace
 
-int ingest_launch(int prec, const float* img, void* x, int N, int H, int W, int Cp, hipStream_t s) {
+int ingest_launch(int prec, const float* img, void* x, int N, int H, int W, int Cp, unsigned* err, hipStream_t s) {
   const long npix = (long)N * H * W;
   if (prec == PREC_BF16)
-    hipLaunchKernelGGL(ingest_kernel<bf16_t>, dim3(grid_for(npix)), dim3(256), 0, s, img, (bf16_t*)x, npix, H * W, Cp);
+    hipLaunchKernelGGL(ingest_kernel<bf16_t>, dim3(grid_for(npix)), dim3(256), 0, s, img, (bf16_t*)x, npix, H * W, Cp,
+                       err);
   else
-    hipLaunchKernelGGL(ingest_kernel<float>, dim3(grid_for(npix)), dim3(256), 0, s, img, (float*)x, npix, H * W, Cp);
+    hipLaunchKernelGGL(ingest_kernel<float>, dim3(grid_for(npix)), dim3(256), 0, s, img, (float*)x, npix, H * W, Cp,
+                       err);
   return ok();
 }
 
-int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, hipStream_t s) {
+int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, unsigned* err, hipStream_t s) {
   if (H % 2 || W % 2) return -1;
   const long npix = (long)N * (H / 2) * (W / 2);
   if (prec == PREC_BF16)
-    hipLaunchKernelGGL(ingest_s2d_kernel<bf16_t>, dim3(grid_for(npix)), dim3(256), 0, s, img, (bf16_t*)x, npix, H, W);
+    hipLaunchKernelGGL(ingest_s2d_kernel<bf16_t>, dim3(grid_for(npix)), dim3(256), 0, s, img, (bf16_t*)x, npix, H, W,
+                       err);
   else
-    hipLaunchKernelGGL(ingest_s2d_kernel<float>, dim3(grid_for(npix)), dim3(256), 0, s, img, (float*)x, npix, H, W);
+    hipLaunchKernelGGL(ingest_s2d_kernel<float>, dim3(grid_for(npix)), dim3(256), 0, s, img, (float*)x, npix, H, W,
+                       err);
   return ok();
 }
 
