@@ -10,6 +10,9 @@ tails) at every resolution the cyclic and hybrid schedules visit; and, at
 the ImageNet batch-256 224x224 launch configuration itself, properties that
 hold at any size (duplicated-batch invariance, lr = 0) plus per-sample
 eval-mode logits checked against the oracle one image at a time."""
+import resource
+import time
+
 import numpy as np
 import pytest
 
@@ -41,22 +44,26 @@ def _run_parity(arch, classes, prec, N, H, seed, lr=LR, dropout=None, chunk=0):
         B.rn18_set_dropout(w.ctx, *dropout)
         drop = dict(dropout=dropout[0], dropout_seed=dropout[1], dropout_step=dropout[2])
     bf = prec == "bf16"
-    dec = Mirror(w, L, N, H, prec, TAU["fp32"]) if bf else Decider(w, N, H, prec, TAU[prec])
+    dec = Mirror(w, L, N, H, prec, TAU) if bf else Decider(w, N, H, prec, TAU)
     gs, gv, losses, status = gpu_train_step(arch, classes, prec, st, x, y, lr, worker=w)
     assert status == B.RN18_OK
     cfg = net.Config(arch, classes, bf16=bf, round_acts=bf, **drop)
+    t0 = time.time()
     try:
         report, loss = compare_step(L, cfg, st, x, y, lr, gs, gv, losses[0], TOL[prec], decide=dec)
     finally:
+        print("oracle step and comparison %.1f s, host peak RSS %.1f GB" %
+              (time.time() - t0, resource.getrusage(resource.RUSAGE_SELF).ru_maxrss / 2 ** 20), flush=True)
         if bf:
             print("bf16 rounding band %d, kernel choices taken %d, invalid %d, outside %d %s" %
                   (dec.round_band, dec.round_taken, dec.round_invalid, dec.round_outside, dec.round_log[:4]))
-        print("relu/pool band %d, taken %d, outside %d" % (dec.ambiguous, dec.taken, dec.outside))
+        print("relu/pool band %d, taken %d, invalid %d, outside %d" % (dec.ambiguous, dec.taken, dec.invalid,
+                                                                       dec.outside))
         w.close()
     worst = max(report.items(), key=lambda kv: kv[1][0])
     print("%s %s N=%d H=%d loss %.6f (oracle %.6f) worst %s norm-rel %.2e" %
           (arch, prec, N, H, losses[0], loss, worst[0], worst[1][0]))
-    assert dec.outside == 0
+    assert dec.outside == 0 and dec.invalid == 0
     if bf:
         assert dec.round_outside == 0 and dec.round_invalid == 0
     return report
@@ -82,6 +89,34 @@ def test_cifar_fp32_cyclic_resolutions(N, H):
 @pytest.mark.parametrize("N,H", [(4, 224), (3, 128), (2, 160), (2, 192), (8, 64)])
 def test_imagenet_bf16_resolutions(N, H):
     _run_parity("imagenet", 1000, "bf16", N, H, seed=110 + H)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("N,H", [(512, 16), (256, 24)])
+def test_cifar_fp32_cyclic_full_batch(N, H):
+    """The cyclic schedule's first two stages at their full batch sizes
+    (512 at 16x16, 256 at 24x24; the 128 at 32x32 stage is the full
+    CIFAR configuration above)."""
+    _run_parity("cifar", 100, "fp32", N, H, seed=160 + H)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("H", [128, 160, 192, 224])
+def test_imagenet_bf16_small_worker_b64(H):
+    """The hybrid schedule's small-batch worker (batch 64) at every
+    resolution it visits. At batch 64 every persistent grid walks several
+    tiles per block (the stage-1 halo conv needs 37 images at 224x224 for
+    more than one row strip per block, the stem halo conv 10) and the
+    weight-gradient split counts reach their caps."""
+    _run_parity("imagenet", 1000, "bf16", 64, H, seed=170 + H)
+
+
+@pytest.mark.timeout(900)
+def test_imagenet_bf16_b256_224_full_step():
+    """The headline configuration itself, batch 256 at 224x224 in bf16:
+    the whole training step against the oracle, element by element, in the
+    launch configuration the benchmark times."""
+    _run_parity("imagenet", 1000, "bf16", 256, 224, seed=175)
 
 
 def test_imagenet_bf16_halo_configuration():
