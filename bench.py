@@ -258,7 +258,7 @@ def merge_rate(B, torch, n, reps=20):
 def dbl_plan(B, torch, inputs, by, merge_ms, steps):
     """The dual-batch planner on this GPU's measured step times: per hybrid
     resolution, a and b of t = a*x + b fitted over batches 64, B_L/2 and B_L
-    (Sec. 3.1); the ImageNet split for one small and three large workers at
+    (Sec. 3.2); the ImageNet split for one small and three large workers at
     k = 1.05 (Eqs. 4-6), B_S from Eq. 8, the factor d_S/d_L (Sec. 3.4); then a
     step at the planned B_S, the measured per-worker epoch times (Eq. 7 says
     they match) and a ratio-faithful round: one large step, the small worker's

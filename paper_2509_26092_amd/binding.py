@@ -26,7 +26,7 @@ EXPORTED = [
     "rn18_profile_read",
     "rn18op_conv2d_fwd", "rn18op_conv2d_dgrad", "rn18op_conv2d_wgrad_workspace", "rn18op_conv2d_wgrad",
     "rn18op_maxpool_fwd", "rn18op_maxpool_bwd", "rn18_debug_set", "rn18_debug_copy",
-    "rn18_debug_capture", "rn18op_round_bf16",
+    "rn18_debug_capture", "rn18op_round_bf16"
 ]
 
 
@@ -243,7 +243,7 @@ def rn18_debug_set(ctx, key, value):
     return _check(lib().rn18_debug_set(ctx, key, value))
 
 
-CAP = dict(dy=0, dz1=1, dx1=2, dx=3, da_avg=4, da_pool=5)
+CAP = dict(dy=0, dz1=1, dx=3, da_avg=4, da_pool=5)
 
 
 def rn18_debug_capture(ctx, kind, index, dst):
@@ -262,13 +262,19 @@ def rn18_debug_copy(ctx, N, H, W, which, index, dst):
 class Worker:
     """One training context (a parameter-server worker): the library context
     plus a torch-allocated device workspace sized for the largest shape seen.
-    Holds no state of its own beyond memory ownership."""
+    Holds no state of its own beyond memory ownership.
 
-    def __init__(self, arch, num_classes, prec="fp32", seed=0, state=None, **hyper):
+    The context is bound to `stream` (torch's current stream at construction
+    by default); the workspace is allocated on that stream, so torch's
+    allocator hands a replaced workspace to later allocations only in that
+    stream's order, after every step that used it."""
+
+    def __init__(self, arch, num_classes, prec="fp32", seed=0, state=None, stream=None, **hyper):
         import torch
         self.cfg = make_config(arch, num_classes, prec, **hyper)
         self.n_state, self.n_trainable = rn18_state_floats(self.cfg)
-        self.ctx = rn18_init(self.cfg, seed, state)
+        self.stream = stream if stream is not None else torch.cuda.current_stream()
+        self.ctx = rn18_init(self.cfg, seed, state, stream=self.stream)
         self.ws = None
         self.torch = torch
 
@@ -277,8 +283,10 @@ class Worker:
         if need == 0:
             raise Rn18Error(RN18_EINVAL, rn18_last_error())
         if self.ws is None or self.ws.numel() < need:
-            self.ws = self.torch.empty(need, dtype=self.torch.uint8, device="cuda")
-            rn18_set_workspace(self.ctx, self.ws)
+            with self.torch.cuda.stream(self.stream):
+                ws = self.torch.empty(need, dtype=self.torch.uint8, device="cuda")
+            rn18_set_workspace(self.ctx, ws)
+            self.ws = ws
 
     def train_step(self, state, images, labels, lr, loss=None):
         N, _, H, W = images.shape

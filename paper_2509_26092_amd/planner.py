@@ -2,10 +2,10 @@
 split, small batch size and model-update factor, fitted to step times
 measured on this GPU.
 
-Sec. 3.1 models the time of one batch of x images as a*x + b (linear
+Sec. 3.2 models the time of one batch of x images as a*x + b (linear
 regression over measured batches), so an epoch over d images takes
 (a*x + b) * ceil(d/x) (Eq. 2), approximately (a + b/x) * d (Eq. 3).
-Sec. 3.2 balances n_L large-batch and n_S small-batch workers: every worker
+Sec. 3.3 balances n_L large-batch and n_S small-batch workers: every worker
 gets the time k * (a + b/B_L) * d/n of an all-large run (k > 1, the extra
 training-time ratio), which gives d_L = k*d/n (Eq. 4), d_S from
 d = n_L*d_L + n_S*d_S (Eq. 6) and the small batch size
@@ -23,7 +23,7 @@ import numpy as np
 
 
 def fit_linear(batches, times):
-    """Least-squares a, b of time = a*batch + b (Sec. 3.1)."""
+    """Least-squares a, b of time = a*batch + b (Sec. 3.2)."""
     x = np.asarray(batches, dtype=np.float64)
     t = np.asarray(times, dtype=np.float64)
     if x.size < 2 or np.ptp(x) == 0:
