@@ -48,6 +48,21 @@ int rn18op_conv2d_wgrad(int prec, const void* dy, const void* x, float* dw_oihw,
                         int cin_real, int Cout, int k, int s, int p, void* workspace, size_t workspace_bytes,
                         void* hip_stream);
 
+/* Allocation-free variant of rn18op_conv2d_wgrad, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same kernels and the same result,
+ * with the split-K partial sums in a static device array of the library
+ * (rn18op_conv2d_wgrad_noalloc_limit() bytes, 48 MiB; each GPU the library
+ * runs on holds its own copy until the process ends) instead of a caller
+ * workspace. Nothing is allocated or freed. A shape whose partials need more
+ * than the limit returns RN18_EINVAL before any launch (every ResNet-18
+ * layer of the library's split rule fits). Every call on one GPU shares that
+ * GPU's array: calls that overlap on one GPU (different streams, or
+ * different threads on one stream's queue without ordering) race. */
+size_t rn18op_conv2d_wgrad_noalloc_limit(void);
+int rn18op_conv2d_wgrad_noalloc(int prec, const void* dy, const void* x, float* dw_oihw, int N, int H, int W,
+                                int Cin, int cin_real, int Cout, int k, int s, int p, void* hip_stream);
+
 /* Max pool 3x3, stride 2, padding 1 (padding never wins):
  *   y[n,i,j,c] = max over the window; arg[n,i,j,c] = kh*3+kw of the FIRST
  *   maximum in row-major (kh,kw) order (uint8).

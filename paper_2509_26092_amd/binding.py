@@ -26,7 +26,7 @@ EXPORTED = [
     "rn18_profile_read",
     "rn18op_conv2d_fwd", "rn18op_conv2d_dgrad", "rn18op_conv2d_wgrad_workspace", "rn18op_conv2d_wgrad",
     "rn18op_maxpool_fwd", "rn18op_maxpool_bwd", "rn18_debug_set", "rn18_debug_copy",
-    "rn18_debug_capture", "rn18op_round_bf16"
+    "rn18_debug_capture", "rn18op_round_bf16", "rn18op_conv2d_wgrad_noalloc_limit", "rn18op_conv2d_wgrad_noalloc",
 ]
 
 
@@ -86,6 +86,8 @@ def lib():
         "rn18op_conv2d_dgrad": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P]),
         "rn18op_conv2d_wgrad_workspace": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
         "rn18op_conv2d_wgrad": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _Z, _P]),
+        "rn18op_conv2d_wgrad_noalloc_limit": (_Z, []),
+        "rn18op_conv2d_wgrad_noalloc": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P]),
         "rn18op_maxpool_fwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _P]),
         "rn18op_maxpool_bwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _P]),
         "rn18op_round_bf16": (_I, [_P, _P, _Z, _P]),
@@ -218,6 +220,15 @@ def rn18op_conv2d_wgrad_workspace(prec, N, H, W, Cin, Cout, k, s, p):
 def rn18op_conv2d_wgrad(prec, dy, x, dw, N, H, W, Cin, cin_real, Cout, k, s, p, ws, stream=None):
     return _check(lib().rn18op_conv2d_wgrad(prec, _ptr(dy), _ptr(x), _ptr(dw), N, H, W, Cin, cin_real, Cout, k, s, p,
                                             _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def rn18op_conv2d_wgrad_noalloc_limit():
+    return lib().rn18op_conv2d_wgrad_noalloc_limit()
+
+
+def rn18op_conv2d_wgrad_noalloc(prec, dy, x, dw, N, H, W, Cin, cin_real, Cout, k, s, p, stream=None):
+    return _check(lib().rn18op_conv2d_wgrad_noalloc(prec, _ptr(dy), _ptr(x), _ptr(dw), N, H, W, Cin, cin_real, Cout,
+                                                    k, s, p, _stream(stream)))
 
 
 def rn18op_maxpool_fwd(prec, x, y, arg, N, H, W, C, stream=None):

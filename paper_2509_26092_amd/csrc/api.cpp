@@ -12,6 +12,7 @@
 
 #include <algorithm>
 #include <map>
+#include <mutex>
 #include <string>
 #include <tuple>
 #include <vector>
@@ -1427,6 +1428,63 @@ int rn18op_conv2d_wgrad(int prec, const void* dy, const void* x, float* dw, int 
   const int splits = wgrad_op_splits(prec, N, H, W, Cin, Ho, Wo, Cout, k, s, p, &pps);
   if (ws_bytes < (size_t)splits * Cout * k * k * Cin * 4) return fail(RN18_ENOMEM, "workspace too small");
   LCHK(launch_wgrad_full(prec, dy, x, dw, (float*)ws, N, H, W, Cin, cin_real, Ho, Wo, Cout, k, s, p, splits, pps,
+                         (hipStream_t)stream));
+  return RN18_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Allocation-free weight gradient: the split-K partials live in a static
+// device array of the library instead of a caller workspace. Every GPU the
+// library runs on holds its own copy of the array until the process ends.
+// ---------------------------------------------------------------------------
+namespace {
+constexpr size_t kNoAllocScratchBytes = (size_t)48 << 20;
+__device__ __align__(256) unsigned char g_noalloc_scratch[kNoAllocScratchBytes];
+constexpr int kMaxDevices = 64;
+void* g_noalloc_ptr[kMaxDevices] = {};
+std::mutex g_noalloc_mu;
+
+// Device address of this GPU's copy of the scratch array, looked up once per
+// device with that device current. (The array's name in host code is a host
+// stand-in, never a device address.)
+int noalloc_scratch(void** out) {
+  int dev = -1;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(RN18_EINVAL, "device %d beyond the %d the library tracks", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  if (!g_noalloc_ptr[dev]) {
+    void* p = nullptr;
+    HIPCHK(hipGetSymbolAddress(&p, HIP_SYMBOL(g_noalloc_scratch)));
+    if (!p || ((uintptr_t)p & 255u)) return fail(RN18_EHIP, "static scratch has no usable device address");
+    g_noalloc_ptr[dev] = p;
+  }
+  *out = g_noalloc_ptr[dev];
+  return RN18_OK;
+}
+}  // namespace
+
+extern "C" {
+
+size_t rn18op_conv2d_wgrad_noalloc_limit(void) { return kNoAllocScratchBytes; }
+
+int rn18op_conv2d_wgrad_noalloc(int prec, const void* dy, const void* x, float* dw, int N, int H, int W, int Cin,
+                                int cin_real, int Cout, int k, int s, int p, void* stream) {
+  int Ho, Wo;
+  int r = op_check(prec, N, H, W, Cin, Cout, k, s, p, &Ho, &Wo);
+  if (r) return r;
+  if (cin_real < 1 || cin_real > Cin) return fail(RN18_EINVAL, "cin_real must be in [1, Cin]");
+  if (!dy || !x || !dw || !aligned16(dy) || !aligned16(x)) return fail(RN18_EINVAL, "bad pointer");
+  int pps;
+  const int splits = wgrad_op_splits(prec, N, H, W, Cin, Ho, Wo, Cout, k, s, p, &pps);
+  const size_t need = (size_t)splits * Cout * k * k * Cin * 4;
+  if (need > kNoAllocScratchBytes)
+    return fail(RN18_EINVAL, "this shape needs %zu bytes of split-K scratch, beyond the %zu-byte static scratch", need,
+                kNoAllocScratchBytes);
+  void* scratch = nullptr;
+  if ((r = noalloc_scratch(&scratch))) return r;
+  LCHK(launch_wgrad_full(prec, dy, x, dw, (float*)scratch, N, H, W, Cin, cin_real, Ho, Wo, Cout, k, s, p, splits, pps,
                          (hipStream_t)stream));
   return RN18_OK;
 }
