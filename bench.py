@@ -395,28 +395,68 @@ def memory_model(B, torch):
     return {"workload": "memory_model_eq9", "configs": out}
 
 
-def cpu_baseline(arch, classes, prec, H, n_img, seed=3):
-    """The fp64 oracle's training step, timed on the host cores on a bounded
-    sample of the workload (n_img images at the workload's resolution)."""
-    import numpy as np
-    from oracle import net
-    from paper_2509_26092_amd import inputs
+def host_info():
+    """CPU model, logical CPUs visible to this process and the BLAS thread count."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count()
+    try:
+        visible = len(os.sched_getaffinity(0))
+    except AttributeError:
+        visible = os.cpu_count()
+    return model, visible, threads
+
+
+# train GFLOP per image of the workload's net (real channels): ImageNet at 224,
+# CIFAR at 32; other resolutions scale with the pixel count
+_GFLOP_IMG = {"imagenet": (10.648, 224), "cifar": (3.329, 32), "tiny": (0.0075, 16)}
+
+
+def cpu_sample_images(arch, H, N, budget_gflop=60.0):
+    """Images of a bounded oracle sample of a step shape: about budget_gflop
+    of training work (a few seconds of fp64 on the host), at least 2, at
+    most the batch."""
+    g, h0 = _GFLOP_IMG[arch]
+    per = g * (H / h0) ** 2
+    return max(2, min(N, int(round(budget_gflop / per))))
+
+
+def cpu_baseline(arch, classes, prec, H, n_img, seed=3, reps=3):
+    """The fp64 oracle's training step, timed on the host cores on a bounded
+    sample of the workload (n_img images at the workload's resolution): the
+    median of `reps` steps (one if a step takes 60 s or more)."""
+    import numpy as np
+    from oracle import net
+    from paper_2509_26092_amd import inputs
+    model, visible, threads = host_info()
     L = net.Layout(arch, classes)
     cfg = net.Config(arch, classes, bf16=(prec == "bf16"))
     st = net.init_state(L, seed)
     x = inputs.images(seed, n_img, H, H)
     y = inputs.labels(seed, n_img, classes)
-    t0 = time.perf_counter()
-    net.train_step(cfg, L, st, np.zeros(L.n_trainable), x, y, 0.01)
-    dt = time.perf_counter() - t0
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        net.train_step(cfg, L, st, np.zeros(L.n_trainable), x, y, 0.01)
+        times.append(time.perf_counter() - t0)
+        if times[-1] >= 60.0:
+            break
+    dt = float(np.median(times))
     return {"value": round(n_img / dt, 3), "unit": "images/s", "cores": threads, "kind": "oracle",
-            "sample": "one fp64 oracle training step of %d images at %dx%d (%s %s net), %.1f s on %d host threads "
-                      "(os.cpu_count %d)" % (n_img, H, H, arch, prec, dt, threads, os.cpu_count())}
+            "s_per_step_sample": round(dt, 3),
+            "sample": "fp64 oracle training step of %d images at %dx%d (%s %s net), median of %d: %.2f s; "
+                      "%d BLAS threads, %d logical CPUs visible, %s" % (n_img, H, H, arch, prec, len(times), dt,
+                                                                       threads, visible, model)}
 
 
 def main():
@@ -430,7 +470,7 @@ def main():
     ap.add_argument("--serial", action="store_true",
                     help="keep every launch of the headline steps on one stream (no weight-gradient overlap), so "
                          "that a kernel trace times each kernel alone, as the profiled step does")
-    ap.add_argument("--cpu-images", type=int, default=40)
+    ap.add_argument("--cpu-images", type=int, default=20)
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/hbm_traffic.json from the counter_collection.csv files of a FETCH_SIZE "
                          "and a WRITE_SIZE rocprofv3 --pmc run of this script with --calibrate, then exit")
@@ -481,6 +521,10 @@ def main():
                               "conv_tflops": ssum["conv_tflops"], "conv_mfma_frac": ssum["conv_mfma_frac"],
                               "stream_GBps": ssum["stream_GBps"], "stream_hbm_frac": ssum["stream_hbm_frac"],
                               "status": sstatus})
+            if not args.no_cpu:
+                per_shape[-1]["cpu_baseline"] = cpu_baseline(sarch, scls, sprec, sH,
+                                                             cpu_sample_images(sarch, sH, sN))
+                progress("%s oracle sample: %s" % (sname, per_shape[-1]["cpu_baseline"]["sample"]))
         # the headline shape with the classifier-input dropout of the 224
         # sub-stage of the ImageNet hybrid schedule (rate 0.2, Table 9)
         ddt, _, dstatus, _ = run_shape(B, torch, inputs, arch, classes, prec, N, H, args.shape_steps, 2, dropout=0.2)
