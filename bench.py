@@ -24,7 +24,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK = {"bf16": 2500.0, "fp32": 157.3}     # dense MFMA TFLOP/s, MI355X published
+PEAK = {"bf16": 2500.0, "fp16": 2500.0, "fp32": 157.3}     # dense MFMA TFLOP/s, MI355X published
 HBM_PEAK = 8000.0                           # GB/s
 MFMA_CLASSES = {"conv_fwd", "conv_dgrad", "conv_wgrad"}
 
@@ -235,6 +235,10 @@ def run_shape(B, torch, inputs, arch, classes, prec, N, H, steps, warmup, seed=1
     B.rn18_profile_enable(w.ctx, False)
     status = w.sync_status()
     lval = float(loss.item())
+    if prec == "fp16":
+        # the dynamic loss scale after all steps, and how many were skipped
+        scale, skipped = B.rn18_get_loss_scale(w.ctx)
+        recs.append({"cls": "loss_scale", "scale": scale, "skipped": skipped, "steps": warmup + steps + 1})
     w.close()
     return dt, recs, status, lval
 
@@ -525,6 +529,19 @@ def main():
                 per_shape[-1]["cpu_baseline"] = cpu_baseline(sarch, scls, sprec, sH,
                                                              cpu_sample_images(sarch, sH, sN))
                 progress("%s oracle sample: %s" % (sname, per_shape[-1]["cpu_baseline"]["sample"]))
+        # the headline shape in fp16 with dynamic loss scaling (the 16-bit
+        # mixed precision of Sec. 5.2.3 with the loss scaling it cites)
+        fdt, frecs, fstatus, _ = run_shape(B, torch, inputs, arch, classes, "fp16", N, H, args.shape_steps, 2)
+        fls = [r for r in frecs if r.get("cls") == "loss_scale"][0]
+        fsum, _ = summarize([r for r in frecs if r.get("cls") != "loss_scale"], "fp16")
+        per_shape.append({"workload": "imagenet_resnet18_fp16_b256_224", "batch": N, "resolution": H,
+                          "dtype": "fp16", "images_per_s": round(N / fdt, 1), "ms_per_step": round(fdt * 1e3, 3),
+                          "conv_tflops": fsum["conv_tflops"], "conv_mfma_frac": fsum["conv_mfma_frac"],
+                          "stream_GBps": fsum["stream_GBps"], "stream_hbm_frac": fsum["stream_hbm_frac"],
+                          "loss_scale": fls["scale"], "skipped_steps": fls["skipped"], "steps_run": fls["steps"],
+                          "status": fstatus})
+        progress("imagenet_resnet18_fp16_b256_224: %.3f ms/step, loss scale %g, %d of %d steps skipped"
+                 % (fdt * 1e3, fls["scale"], fls["skipped"], fls["steps"]))
         # the headline shape with the classifier-input dropout of the 224
         # sub-stage of the ImageNet hybrid schedule (rate 0.2, Table 9)
         ddt, _, dstatus, _ = run_shape(B, torch, inputs, arch, classes, prec, N, H, args.shape_steps, 2, dropout=0.2)

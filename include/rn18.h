@@ -71,8 +71,16 @@ typedef enum { RN18_TINY = 0, RN18_CIFAR = 1, RN18_IMAGENET = 2 } rn18_arch;
  * RN18_BF16: images, conv weights and activations (and their gradients) in
  * bf16 with fp32 accumulation; master weights, momentum, BN statistics, the
  * classifier and the loss in fp32. This is the mixed precision of the
- * paper's ImageNet runs (Sec. 5.2.3), taken as bf16 without loss scaling. */
-typedef enum { RN18_FP32 = 0, RN18_BF16 = 1 } rn18_prec;
+ * paper's ImageNet runs (Sec. 5.2.3), taken as bf16 without loss scaling.
+ * RN18_FP16: the same tensors in IEEE fp16 (round to nearest even) with
+ * dynamic loss scaling, the 16-bit mixed-precision training that Sec. 5.2.3
+ * cites: the backward pass starts from scale x loss, so every stored
+ * gradient is scaled; the weight update multiplies the gradient by 1/scale,
+ * or is skipped when a gradient value is not finite (an fp16 overflow). The
+ * scale (a power of two, initially 65536) halves after a skipped step and
+ * doubles after 2000 steps in a row without one (rn18_set_loss_scale). BN
+ * running statistics are updated in the forward pass of a skipped step too. */
+typedef enum { RN18_FP32 = 0, RN18_BF16 = 1, RN18_FP16 = 2 } rn18_prec;
 
 typedef struct {
   int arch;            /* rn18_arch */
@@ -163,6 +171,16 @@ int rn18_set_momentum(rn18_ctx* ctx, const float* src);
  * successful rn18_train_step (whether or not dropout is on); evaluation never
  * drops. RN18_EINVAL for a NULL ctx or p outside [0, 1). */
 int rn18_set_dropout(rn18_ctx* ctx, float p, uint64_t seed, uint64_t step);
+
+/* Loss scaling of an RN18_FP16 context (RN18_EINVAL for other precisions).
+ * rn18_set_loss_scale waits for the context's stream, then sets the scale
+ * (a power of two in [1, 2^24]) and the growth interval (steps without an
+ * overflow before the scale doubles, >= 1) and clears the counters.
+ * rn18_get_loss_scale waits for the stream and reads the current scale and
+ * the number of steps skipped because of a non-finite gradient (either
+ * pointer may be NULL). */
+int rn18_set_loss_scale(rn18_ctx* ctx, float scale, unsigned growth_interval);
+int rn18_get_loss_scale(rn18_ctx* ctx, float* scale, uint64_t* skipped_steps);
 
 /* Synchronise and free everything the context allocated. */
 void rn18_destroy(rn18_ctx* ctx);

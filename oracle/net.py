@@ -110,17 +110,30 @@ def init_state(layout, seed):
 
 class Config:
     def __init__(self, arch, num_classes, bf16=False, momentum=0.9, weight_decay=5e-4,
-                 bn_eps=1e-5, bn_momentum=0.1, round_acts=False, dropout=0.0, dropout_seed=0, dropout_step=0):
+                 bn_eps=1e-5, bn_momentum=0.1, round_acts=False, dropout=0.0, dropout_seed=0, dropout_step=0,
+                 fp16=False, loss_scale=1.0):
+        assert not (bf16 and fp16)
         self.arch = arch
         self.num_classes = num_classes
         self.bf16 = bf16
+        # fp16 configurations: IEEE binary16 in place of bf16 at every
+        # rounding point, with loss scaling: the backward pass starts from
+        # loss_scale x dLoss/dlogits, so every stored gradient is scaled,
+        # and the parameter gradient is divided by loss_scale at the end (a
+        # power of two: exact in float64). A step whose gradient is not
+        # finite (an fp16 overflow) updates no parameter (train_step).
+        self.fp16 = fp16
+        self.loss_scale = float(loss_scale)
+        self.half = bf16 or fp16
+        self.round16 = ops.round_bf16 if bf16 else ops.round_fp16 if fp16 else None
         self.momentum = momentum
         self.weight_decay = weight_decay
         self.bn_eps = bn_eps
         self.bn_momentum = bn_momentum
         # round_acts: additionally round every stored activation and
-        # activation gradient to bf16 at the points where a bf16 training
-        # step stores them (see ROUNDING_POINTS). Off by default.
+        # activation gradient to the 16-bit type at the points where a
+        # 16-bit training step stores them (see ROUNDING_POINTS). Off by
+        # default.
         self.round_acts = round_acts
         # dropout before the classifier in training-mode passes (the paper's
         # adaptive regularisation, Sec. 4.1): rate, generator key and the
@@ -130,7 +143,8 @@ class Config:
         self.dropout_step = dropout_step
 
 
-# Where a bf16 training step stores a tensor in bf16 (rounded once, RNE):
+# Where a 16-bit (bf16 or fp16) training step stores a tensor in the 16-bit
+# type (rounded once, RNE):
 #   ("y", conv)     conv output, before BN (BN statistics are taken of it)
 #   ("z", site)     ReLU output: stem, block z1, block output
 #   ("da_avg", 0)   gradient entering the last block (avg-pool backward)
@@ -163,28 +177,30 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
     block); rounding points: ROUNDING_POINTS); the default is mask = pre > 0,
     the first maximum and round-to-nearest-even.
 
-    bf16 configurations (the training configuration's mixed precision): the
-    images and the conv weights are rounded to bf16 (round-to-nearest-even)
-    and then used in float64; BN statistics, the FC layer, the loss, the
-    master weights and the momentum stay in full precision."""
+    16-bit configurations (the mixed precision of Sec. 5.2.3, bf16 or fp16):
+    the images and the conv weights are rounded to the 16-bit type
+    (round-to-nearest-even) and then used in float64; BN statistics, the FC
+    layer, the loss, the master weights and the momentum stay in full
+    precision. fp16 configurations scale the backward pass by
+    cfg.loss_scale and divide the gradient by it at the end."""
     x = np.asarray(images, dtype=np.float64)
-    if cfg.bf16:
-        x = ops.round_bf16(x)
+    if cfg.half:
+        x = cfg.round16(x)
     eps = cfg.bn_eps
 
     def W(name):
         w = layout.get(state, name + ".w")
-        return ops.round_bf16(w) if cfg.bf16 else w
+        return cfg.round16(w) if cfg.half else w
 
     caches = {}
     run_stats = []
     masks = {}
-    rounding = cfg.bf16 and cfg.round_acts
+    rounding = cfg.half and cfg.round_acts
 
     def rb(point, v):
         if not rounding:
             return v
-        r = ops.round_bf16(v)
+        r = cfg.round16(v)
         if decide is not None:
             r = decide("round", point, v, r)
         return r
@@ -241,6 +257,8 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
     if not need_grad:
         return None, logits, None, run_stats
     loss, dz = ops.softmax_ce(logits, labels)
+    if cfg.fp16:
+        dz = dz * cfg.loss_scale
 
     grad = np.zeros(layout.n_trainable)
     df, dwfc, dbfc = ops.fc_backward(dz, f, wfc)
@@ -277,17 +295,27 @@ def forward_backward(cfg, layout, state, images, labels, train=True, need_grad=T
         da = rb(("da_pool", 0), ops.maxpool_backward(da, pool_arg, stem_out.shape))
     g0 = da * masks["stem"]
     bn_conv_back("stem", g0)
+    if cfg.fp16:
+        with np.errstate(invalid="ignore", over="ignore"):
+            grad = grad / cfg.loss_scale
     return loss, logits, grad, run_stats
 
 
 def train_step(cfg, layout, state, momentum_buf, images, labels, lr, decide=None):
     """Forward, backward, BN running-stat update and SGD-momentum update of
     every trainable parameter (conv W, gamma, beta, FC W and b; weight decay
-    on all of them). Returns (new_state, new_momentum, loss, grad)."""
+    on all of them). Returns (new_state, new_momentum, loss, grad).
+
+    fp16 configurations skip the parameter and momentum update when the
+    gradient is not finite (the loss-scaled backward pass overflowed fp16);
+    the BN running statistics of the forward pass are kept either way."""
     loss, logits, grad, run_stats = forward_backward(cfg, layout, state, images, labels, decide=decide)
     new_state = np.array(state, dtype=np.float64, copy=True)
     P = layout.n_trainable
-    w_new, v_new = ops.sgd_momentum(new_state[:P], grad, momentum_buf, lr, cfg.momentum, cfg.weight_decay)
+    if cfg.fp16 and not np.all(np.isfinite(grad)):
+        w_new, v_new = new_state[:P].copy(), np.array(momentum_buf, dtype=np.float64, copy=True)
+    else:
+        w_new, v_new = ops.sgd_momentum(new_state[:P], grad, momentum_buf, lr, cfg.momentum, cfg.weight_decay)
     new_state[:P] = w_new
     for name, rm, rv in run_stats:
         layout.put(new_state, name + ".rm", rm)

@@ -225,3 +225,26 @@ def round_bf16(x):
     if nan.any():
         out = np.where(nan, np.nan, out)
     return out
+
+
+# ----------------------------------------------------------------------------
+# fp16 (IEEE-754 binary16) round-to-nearest-even of float32 values (result
+# widened back to f64). binary16 has an 11-bit significand (10 stored bits),
+# normal exponents -14..15 and subnormals in steps of 2^-24 below 2^-14. A
+# value is rounded to the nearest multiple of its binade's quantum (ties to
+# the even multiple); a result beyond the largest finite value 65504 is an
+# infinity of the value's sign. NaN stays NaN, infinities stay infinite.
+# ----------------------------------------------------------------------------
+def round_fp16(x):
+    f = np.asarray(x, dtype=np.float32).astype(np.float64)
+    a = np.abs(f)
+    finite = np.isfinite(a) & (a > 0)
+    safe = np.where(finite, a, 1.0)
+    _, e = np.frexp(safe)                      # safe = m * 2^e, m in [0.5, 1)
+    e = np.maximum(e - 1, -14)                 # binade exponent; subnormals share 2^-14's quantum
+    q = np.ldexp(1.0, e - 10)                  # quantum of the binade
+    r = np.rint(safe / q) * q                  # exact quotient; rint rounds half to even
+    r = np.where(r > 65504.0, np.inf, r)
+    out = np.where(finite, np.copysign(r, f), f)
+    return out
+

@@ -14,15 +14,16 @@ LIB_PATH = os.path.join(HERE, "librn18.so")
 
 RN18_OK, RN18_EINVAL, RN18_ELABEL, RN18_ENOMEM, RN18_EHIP, RN18_ENONFINITE = 0, -1, -2, -3, -4, -5
 RN18_TINY, RN18_CIFAR, RN18_IMAGENET = 0, 1, 2
-RN18_FP32, RN18_BF16 = 0, 1
+RN18_FP32, RN18_BF16, RN18_FP16 = 0, 1, 2
 ARCH_IDS = {"tiny": RN18_TINY, "cifar": RN18_CIFAR, "imagenet": RN18_IMAGENET}
-PREC_IDS = {"fp32": RN18_FP32, "bf16": RN18_BF16}
+PREC_IDS = {"fp32": RN18_FP32, "bf16": RN18_BF16, "fp16": RN18_FP16}
 
 # Every symbol the headers declare (checked by the CPU test suite).
 EXPORTED = [
     "rn18_state_floats", "rn18_init", "rn18_workspace_bytes", "rn18_set_workspace", "rn18_train_step",
     "rn18_eval_logits", "ps_dual_merge", "ps_worker_delta", "rn18_sync_status", "rn18_get_momentum",
-    "rn18_set_momentum", "rn18_set_dropout", "rn18_destroy", "rn18_last_error", "rn18_profile_enable",
+    "rn18_set_momentum", "rn18_set_dropout", "rn18_set_loss_scale", "rn18_get_loss_scale", "rn18_destroy",
+    "rn18_last_error", "rn18_profile_enable",
     "rn18_profile_read",
     "rn18op_conv2d_fwd", "rn18op_conv2d_dgrad", "rn18op_conv2d_wgrad_workspace", "rn18op_conv2d_wgrad",
     "rn18op_maxpool_fwd", "rn18op_maxpool_bwd", "rn18_debug_set", "rn18_debug_copy",
@@ -80,6 +81,8 @@ def lib():
         "rn18_get_momentum": (_I, [_P, _P]),
         "rn18_set_momentum": (_I, [_P, _P]),
         "rn18_set_dropout": (_I, [_P, _F, ctypes.c_uint64, ctypes.c_uint64]),
+        "rn18_set_loss_scale": (_I, [_P, _F, ctypes.c_uint]),
+        "rn18_get_loss_scale": (_I, [_P, ctypes.POINTER(_F), ctypes.POINTER(ctypes.c_uint64)]),
         "rn18_destroy": (None, [_P]),
         "rn18_last_error": (ctypes.c_char_p, []),
         "rn18op_conv2d_fwd": (_I, [_I, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _P]),
@@ -172,6 +175,17 @@ def rn18_sync_status(ctx):
 
 def rn18_set_dropout(ctx, p, seed, step):
     return _check(lib().rn18_set_dropout(ctx, ctypes.c_float(p), ctypes.c_uint64(seed), ctypes.c_uint64(step)))
+
+
+def rn18_set_loss_scale(ctx, scale, growth_interval=2000):
+    return _check(lib().rn18_set_loss_scale(ctx, ctypes.c_float(scale), ctypes.c_uint(growth_interval)))
+
+
+def rn18_get_loss_scale(ctx):
+    """(scale, skipped steps) of an fp16 context."""
+    sc, sk = _F(0.0), ctypes.c_uint64(0)
+    _check(lib().rn18_get_loss_scale(ctx, ctypes.byref(sc), ctypes.byref(sk)))
+    return sc.value, sk.value
 
 
 def rn18_get_momentum(ctx, dst):

@@ -65,6 +65,10 @@ constexpr size_t kMaxTensorBytes = ((size_t)1 << 31) - ((size_t)1 << 24);
 // the bound above.
 constexpr size_t kMaxWholeTensorBytes = 16 * kMaxTensorBytes;
 
+// fp16 loss scaling defaults: initial scale and growth interval (steps)
+constexpr float kLossScaleInit = 65536.0f;
+constexpr unsigned kLossScaleInterval = 2000;
+
 // ----------------------------------------------------------------------------
 // Architecture
 // ----------------------------------------------------------------------------
@@ -87,8 +91,8 @@ struct Arch {
 };
 
 bool build_arch(const rn18_config& c, Arch* a) {
-  if (c.num_classes < 1 || c.arch < 0 || c.arch > 2 || c.prec < 0 || c.prec > 1) return false;
-  const int cp = c.prec == RN18_BF16 ? 8 : 4;
+  if (c.num_classes < 1 || c.arch < 0 || c.arch > 2 || c.prec < 0 || c.prec > 2) return false;
+  const int cp = prec_vw(c.prec);
   int stem_c, stem_k, stem_s, stem_p;
   std::vector<int> widths, nblk, fstride;
   if (c.arch == RN18_TINY) {
@@ -195,6 +199,7 @@ struct Ctx {
   int ntab = 0, nttab = 0, ntiles = 0;
   long tab_total = 0;           // elements over the element-wise entries
   unsigned* err = nullptr;
+  LossScale* ls = nullptr;      // fp16 contexts: dynamic loss scale (device)
   // dropout before the classifier: on iff the rate is > 0, keep threshold,
   // scale, and the Philox key and step counter of the next training step
   bool drop_on = false;
@@ -771,7 +776,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   TIMED(RN18_K_HEAD, 0, 0, "gemm_f32_kernel", fcf, 0.0, gemm_f32_launch(f, F, 1, state + a.fc_w, 1, F, state + a.fc_b, logits, N, C, F, hpart, st));
   TIMED(RN18_K_HEAD, 1, 0, "softmax_ce_kernel", 0.0, 8.0 * N * C,
         softmax_ce_launch(logits, labels, N, C, dlog, (float*)(ws + pl.rowloss),
-                          loss ? loss : (float*)(ws + pl.lossbuf), c->err, st));
+                          loss ? loss : (float*)(ws + pl.lossbuf), c->err, st, c->ls));
   // classifier backward: dW = dz^T f, db = sum dz, df = dz W
   TIMED(RN18_K_HEAD, 2, 0, "gemm_f32_kernel", fcf, 0.0, gemm_f32_launch(dlog, 1, C, f, F, 1, nullptr, grad + a.fc_w, C, F, N, hpart, st));
   TIMED(RN18_K_HEAD, 3, 0, "colsum_kernel", 0.0, 4.0 * N * C, colsum_launch(dlog, N, C, grad + a.fc_b, st));
@@ -955,8 +960,10 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     return join(), r;
   }
   if ((r = wgrad(0, pl.gy)) || (r = join())) return join(), r;
+  if (c->ls) TIMED(RN18_K_SGD, 1, 0, "grad_check_kernel", 0.0, 4.0 * a.P, grad_check_launch(grad, a.P, c->ls, st));
   TIMED(RN18_K_SGD, 0, 0, "sgd_kernel", 0.0, 20.0 * a.P,
-        sgd_launch(state, grad, c->momentum, a.P, lr, c->cfg.momentum, c->cfg.weight_decay, st));
+        sgd_launch(state, grad, c->momentum, a.P, lr, c->cfg.momentum, c->cfg.weight_decay, st, c->ls));
+  if (c->ls) TIMED(RN18_K_SGD, 2, 0, "loss_scale_update_kernel", 0.0, 0.0, loss_scale_update_launch(c->ls, st));
   return RN18_OK;
 }
 
@@ -992,7 +999,7 @@ void host_init(const Arch& a, uint64_t seed, std::vector<float>& st) {
 int check_cfg(const rn18_config* cfg) {
   if (!cfg) return fail(RN18_EINVAL, "config is NULL");
   if (cfg->arch < 0 || cfg->arch > 2) return fail(RN18_EINVAL, "unknown arch %d", cfg->arch);
-  if (cfg->prec < 0 || cfg->prec > 1) return fail(RN18_EINVAL, "unknown precision %d", cfg->prec);
+  if (cfg->prec < 0 || cfg->prec > 2) return fail(RN18_EINVAL, "unknown precision %d", cfg->prec);
   if (cfg->num_classes < 1) return fail(RN18_EINVAL, "num_classes must be >= 1");
   if (!isfinite(cfg->momentum) || !isfinite(cfg->weight_decay) || !isfinite(cfg->bn_eps) ||
       !isfinite(cfg->bn_momentum) || cfg->bn_eps < 0.f)
@@ -1029,7 +1036,7 @@ int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* st
   c.cfg = *cfg;
   build_arch(*cfg, &c.arch);
   c.prec = cfg->prec;
-  c.es = cfg->prec == RN18_BF16 ? 2 : 4;
+  c.es = prec_bytes(cfg->prec);
   c.stream = (hipStream_t)hip_stream;
   const Arch& a = c.arch;
   auto bail = [&](int code, const char* what) {
@@ -1038,6 +1045,7 @@ int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* st
     if (c.wd) (void)hipFree(c.wd);
     if (c.tab) (void)hipFree(c.tab);
     if (c.err) (void)hipFree(c.err);
+    if (c.ls) (void)hipFree(c.ls);
     delete h;
     return fail(code, "%s", what);
   };
@@ -1045,6 +1053,12 @@ int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* st
   if (hipMalloc(&c.wf, a.wf_total * c.es + 16) != hipSuccess) return bail(RN18_ENOMEM, "weight shadow allocation failed");
   if (hipMalloc(&c.wd, a.wd_total * c.es + 16) != hipSuccess) return bail(RN18_ENOMEM, "weight shadow allocation failed");
   if (hipMalloc(&c.err, 256) != hipSuccess) return bail(RN18_ENOMEM, "flag allocation failed");
+  if (cfg->prec == RN18_FP16) {
+    if (hipMalloc(&c.ls, 256) != hipSuccess) return bail(RN18_ENOMEM, "loss-scale allocation failed");
+    const LossScale init{kLossScaleInit, 1.0f / kLossScaleInit, 0u, 0u, kLossScaleInterval, 0u};
+    if (hipMemcpy(c.ls, &init, sizeof init, hipMemcpyHostToDevice) != hipSuccess)
+      return bail(RN18_EHIP, "loss-scale upload failed");
+  }
   if (hipStreamCreateWithFlags(&c.side, hipStreamNonBlocking) != hipSuccess ||
       hipEventCreateWithFlags(&c.ev_fork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c.ev_join, hipEventDisableTiming) != hipSuccess ||
@@ -1146,6 +1160,33 @@ int rn18_train_step(rn18_ctx* h, float* state, const float* images, const int32_
   return RN18_OK;
 }
 
+int rn18_set_loss_scale(rn18_ctx* h, float scale, unsigned growth_interval) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  Ctx& c = h->c;
+  if (!c.ls) return fail(RN18_EINVAL, "loss scaling belongs to fp16 contexts");
+  int e = 0;
+  const float m = frexpf(scale, &e);
+  if (!(scale >= 1.0f && scale <= 16777216.0f) || m != 0.5f)
+    return fail(RN18_EINVAL, "the loss scale must be a power of two in [1, 2^24]");
+  if (growth_interval < 1) return fail(RN18_EINVAL, "the growth interval must be >= 1");
+  const LossScale x{scale, 1.0f / scale, 0u, 0u, growth_interval, 0u};
+  HIPCHK(hipStreamSynchronize(c.stream));
+  HIPCHK(hipMemcpy(c.ls, &x, sizeof x, hipMemcpyHostToDevice));
+  return RN18_OK;
+}
+
+int rn18_get_loss_scale(rn18_ctx* h, float* scale, uint64_t* skipped_steps) {
+  if (!h) return fail(RN18_EINVAL, "ctx is NULL");
+  Ctx& c = h->c;
+  if (!c.ls) return fail(RN18_EINVAL, "loss scaling belongs to fp16 contexts");
+  LossScale x{};
+  HIPCHK(hipStreamSynchronize(c.stream));
+  HIPCHK(hipMemcpy(&x, c.ls, sizeof x, hipMemcpyDeviceToHost));
+  if (scale) *scale = x.scale;
+  if (skipped_steps) *skipped_steps = x.skipped;
+  return RN18_OK;
+}
+
 int rn18_set_dropout(rn18_ctx* h, float p, uint64_t seed, uint64_t step) {
   if (!h) return fail(RN18_EINVAL, "ctx is NULL");
   if (!(p >= 0.f && p < 1.f)) return fail(RN18_EINVAL, "dropout rate must be in [0, 1)");
@@ -1235,6 +1276,7 @@ void rn18_destroy(rn18_ctx* h) {
   if (c.wd) (void)hipFree(c.wd);
   if (c.tab) (void)hipFree(c.tab);
   if (c.err) (void)hipFree(c.err);
+  if (c.ls) (void)hipFree(c.ls);
   if (c.ws_owned && c.ws) (void)hipFree(c.ws);
   destroy_side(c);
   for (auto& ev : c.prof) { (void)hipEventDestroy(ev.a); (void)hipEventDestroy(ev.b); }
@@ -1363,8 +1405,8 @@ int rn18_debug_copy(rn18_ctx* h, int N, int H, int W, int which, int index, void
 // Single-operator entry points
 // ---------------------------------------------------------------------------
 static int op_check(int prec, int N, int H, int W, int Cin, int Cout, int k, int s, int p, int* Ho, int* Wo) {
-  if (prec != RN18_FP32 && prec != RN18_BF16) return fail(RN18_EINVAL, "bad precision");
-  const int vw = prec == RN18_BF16 ? 8 : 4;
+  if (prec != RN18_FP32 && prec != RN18_BF16 && prec != RN18_FP16) return fail(RN18_EINVAL, "bad precision");
+  const int vw = prec_vw(prec);
   if (N < 1 || H < 1 || W < 1 || Cin < 1 || Cout < 1 || k < 1 || s < 1 || p < 0)
     return fail(RN18_EINVAL, "non-positive size");
   if (Cin % vw || Cout % vw) return fail(RN18_EINVAL, "channel counts must be multiples of %d", vw);
@@ -1372,7 +1414,7 @@ static int op_check(int prec, int N, int H, int W, int Cin, int Cout, int k, int
   *Ho = out_size(H, k, s, p);
   *Wo = out_size(W, k, s, p);
   if (*Ho < 1 || *Wo < 1) return fail(RN18_EINVAL, "empty output");
-  const size_t es = prec == RN18_BF16 ? 2 : 4;
+  const size_t es = prec_bytes(prec);
   const size_t pix = std::max((size_t)H * W, (size_t)*Ho * *Wo), ch = std::max(Cin, Cout);
   if ((size_t)N * pix * ch * es > kMaxTensorBytes || (size_t)Cout * k * k * Cin * es > kMaxTensorBytes)
     return fail(RN18_EINVAL, "tensor larger than the kernels' per-tensor limit of %zu bytes", kMaxTensorBytes);

@@ -502,15 +502,13 @@ inline int ok() { return hipGetLastError() == hipSuccess ? 0 : -4; }
 int bn_apply_launch(int prec, const void* y, const float* scale, const float* shift, int relu, int res_mode,
                     const void* r, const float* scale2, const float* shift2, void* z, long M, int C, hipStream_t s,
                     uint8_t* mbits) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
-  const long nchunks = M * C / vw;
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(bn_apply_kernel<bf16_t>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const bf16_t*)y,
-                       scale, shift, relu, res_mode, (const bf16_t*)r, scale2, shift2, (bf16_t*)z, nchunks, C, mbits);
-  else
-    hipLaunchKernelGGL(bn_apply_kernel<float>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const float*)y, scale,
-                       shift, relu, res_mode, (const float*)r, scale2, shift2, (float*)z, nchunks, C, mbits);
-  return ok();
+  const long nchunks = M * C / prec_vw(prec);
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(bn_apply_kernel<T>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const T*)y, scale, shift,
+                       relu, res_mode, (const T*)r, scale2, shift2, (T*)z, nchunks, C, mbits);
+    return ok();
+  });
 }
 
 int bn_eval_coef_launch(const float* gamma, const float* beta, const float* rm, const float* rv, float eps, int C,
@@ -521,13 +519,11 @@ int bn_eval_coef_launch(const float* gamma, const float* beta, const float* rm, 
 }
 
 int bn_bwd_partial_blocks(int prec, long M, int C) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
-  return pick_blocks(M, 256 / (C / vw));
+  return pick_blocks(M, 256 / (C / prec_vw(prec)));
 }
 
 int bn_bwd_partial_pool_blocks(int prec, int N, int H, int W, int C) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
-  const int rpi = 256 / (C / vw);
+  const int rpi = 256 / (C / prec_vw(prec));
   return pick_blocks((long)N * ((H + 1) / 2) * ((W + 1) / 2), rpi);
 }
 
@@ -536,13 +532,12 @@ int bn_bwd_partial_launch(int prec, const void* dz, const uint8_t* mb, const voi
                           const float* mscale, const float* mshift) {
   const int nb = bn_bwd_partial_blocks(prec, M, C);
   *nblk = nb;
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(bn_bwd_partial_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, (const bf16_t*)dz, mb,
-                       (const bf16_t*)y, mean, rstd, mscale, mshift, M, C, part);
-  else
-    hipLaunchKernelGGL(bn_bwd_partial_kernel<float>, dim3(nb), dim3(256), 0, s, (const float*)dz, mb,
-                       (const float*)y, mean, rstd, mscale, mshift, M, C, part);
-  return ok();
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(bn_bwd_partial_kernel<T>, dim3(nb), dim3(256), 0, s, (const T*)dz, mb, (const T*)y, mean, rstd,
+                       mscale, mshift, M, C, part);
+    return ok();
+  });
 }
 
 int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float* gamma, const float* rstd,
@@ -554,63 +549,55 @@ int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float*
 
 int bn_bwd_apply_launch(int prec, const void* dz, const uint8_t* mb, const void* y, const float* mean, const float* coef,
                         void* dy, long M, int C, hipStream_t s, const float* mscale, const float* mshift) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
-  const long nchunks = M * C / vw;
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(bn_bwd_apply_kernel<bf16_t>, dim3(stream_blocks(nchunks)), dim3(256), 0, s,
-                       (const bf16_t*)dz, mb, (const bf16_t*)y, mean, coef, mscale, mshift,
-                       (bf16_t*)dy, nchunks, C);
-  else
-    hipLaunchKernelGGL(bn_bwd_apply_kernel<float>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const float*)dz,
-                       mb, (const float*)y, mean, coef, mscale, mshift, (float*)dy, nchunks, C);
-  return ok();
+  const long nchunks = M * C / prec_vw(prec);
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(bn_bwd_apply_kernel<T>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const T*)dz, mb,
+                       (const T*)y, mean, coef, mscale, mshift, (T*)dy, nchunks, C);
+    return ok();
+  });
 }
 
 int bn_apply_pool_launch(int prec, const void* y, const float* scale, const float* shift, void* pool, uint8_t* arg,
                          int N, int H, int W, int C, int Ho, int Wo, hipStream_t s) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const int vw = prec_vw(prec);
   if (C > kMaxC || (long)N * H * W * (C / vw) >= (1l << 31)) return -1;  // 32-bit chunk indices
   const long total = (long)N * Ho * Wo * (C / vw);
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(bn_apply_pool_kernel<bf16_t>, dim3(stream_blocks(total)), dim3(256), 0, s, (const bf16_t*)y,
-                       scale, shift, (bf16_t*)pool, arg, N, H, W, C, Ho, Wo);
-  else
-    hipLaunchKernelGGL(bn_apply_pool_kernel<float>, dim3(stream_blocks(total)), dim3(256), 0, s, (const float*)y,
-                       scale, shift, (float*)pool, arg, N, H, W, C, Ho, Wo);
-  return ok();
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(bn_apply_pool_kernel<T>, dim3(stream_blocks(total)), dim3(256), 0, s, (const T*)y, scale, shift,
+                       (T*)pool, arg, N, H, W, C, Ho, Wo);
+    return ok();
+  });
 }
 
 int bn_bwd_partial_pool_launch(int prec, const void* dpool, const uint8_t* arg, const void* y, const float* scale,
                                const float* shift, const float* mean, const float* rstd, int N, int H, int W, int C,
                                int Ho, int Wo, float* part, int* nblk, hipStream_t s) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const int vw = prec_vw(prec);
   if (C > kMaxC || (long)N * H * W * (C / vw) >= (1l << 31)) return -1;  // 32-bit chunk indices
   const int nb = bn_bwd_partial_pool_blocks(prec, N, H, W, C);
   *nblk = nb;
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(bn_bwd_partial_pool_kernel<bf16_t>, dim3(nb), dim3(256), 0, s, (const bf16_t*)dpool, arg,
-                       (const bf16_t*)y, scale, shift, mean, rstd, N, H, W, C, Ho, Wo, part);
-  else
-    hipLaunchKernelGGL(bn_bwd_partial_pool_kernel<float>, dim3(nb), dim3(256), 0, s, (const float*)dpool, arg,
-                       (const float*)y, scale, shift, mean, rstd, N, H, W, C, Ho, Wo, part);
-  return ok();
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(bn_bwd_partial_pool_kernel<T>, dim3(nb), dim3(256), 0, s, (const T*)dpool, arg, (const T*)y,
+                       scale, shift, mean, rstd, N, H, W, C, Ho, Wo, part);
+    return ok();
+  });
 }
 
 int bn_bwd_apply_pool_launch(int prec, const void* dpool, const uint8_t* arg, const void* y, const float* scale,
                              const float* shift, const float* mean, const float* coef, void* dy, int N, int H, int W,
                              int C, int Ho, int Wo, hipStream_t s) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const int vw = prec_vw(prec);
   if (C > kMaxC || (long)N * H * W * (C / vw) >= (1l << 31)) return -1;  // 32-bit chunk indices
   const long nchunks = (long)N * ((H + 1) / 2) * ((W + 1) / 2) * (C / vw);
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(bn_bwd_apply_pool_kernel<bf16_t>, dim3(stream_blocks(nchunks)), dim3(256), 0, s,
-                       (const bf16_t*)dpool, arg, (const bf16_t*)y, scale, shift, mean, coef, (bf16_t*)dy, N, H, W,
-                       C, Ho, Wo);
-  else
-    hipLaunchKernelGGL(bn_bwd_apply_pool_kernel<float>, dim3(stream_blocks(nchunks)), dim3(256), 0, s,
-                       (const float*)dpool, arg, (const float*)y, scale, shift, mean, coef, (float*)dy, N, H, W, C,
-                       Ho, Wo);
-  return ok();
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(bn_bwd_apply_pool_kernel<T>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const T*)dpool,
+                       arg, (const T*)y, scale, shift, mean, coef, (T*)dy, N, H, W, C, Ho, Wo);
+    return ok();
+  });
 }
 
 int bn_stats_tiles_chunks(int ntiles) {

@@ -54,6 +54,13 @@ template <> struct Mma<bf16_t> {
                                                   __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
   }
 };
+template <> struct Mma<f16_t> {
+  static constexpr int SUB = 1;
+  __device__ static inline void run(floatx4_t& acc, const uint4& a, const uint4& b, int) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), acc,
+                                                 0, 0, 0);
+  }
+};
 template <> struct Mma<float> {
   static constexpr int SUB = 4;
   __device__ static inline float el(const uint4& q, int t) {
@@ -877,9 +884,8 @@ constexpr int HALO_PROWS = 640;  // patch pixels per half-patch buffer
 constexpr int HALO_WAVES = 8;    // waves per block = statistics entries per block
 constexpr int HALO_BM = 64 * HALO_WAVES;
 
-template <int MODE, bool STATS>
+template <typename T, int MODE, bool STATS>
 __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo h) {
-  typedef bf16_t T;
   constexpr int NW = HALO_WAVES, FM = 4, FN = 4;
   constexpr int B_U4 = 9 * 64 * 8;                  // resident weights, uint4 units (128-byte rows)
   constexpr int P_U4 = HALO_PROWS * 4;              // one half-patch buffer (64-byte rows)
@@ -1064,7 +1070,7 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
           const uint32_t rw[2] = {(uint32_t)ld0[i][j].x, (uint32_t)ld0[i][j].y};
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float rv = bf2f((bf16_t)(e & 1 ? rw[e >> 1] >> 16 : rw[e >> 1] & 0xffffu));
+            const float rv = s16_to_f<T>((uint16_t)(e & 1 ? rw[e >> 1] >> 16 : rw[e >> 1] & 0xffffu));
             if constexpr (MODE == 2) {
               // this lane's 4 channels are the low or high half of the byte
               x[e] += (ld1[i][j] >> ((chl & 4) + e)) & 1u ? rv : 0.f;
@@ -1073,12 +1079,12 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
             }
           }
         }
-        const uint2 pk = make_uint2(f2bf2(x[0], x[1]), f2bf2(x[2], x[3]));
+        const uint2 pk = make_uint2(pack2<T>(x[0], x[1]), pack2<T>(x[2], x[3]));
         __builtin_amdgcn_raw_buffer_store_b64(i32x2_t{(int)pk.x, (int)pk.y}, rsC,
                                               okq[i] ? (obase[i] + j * 16) * 2 : kOutOfRange, 0, 0);
         if constexpr (STATS) {
-          const float vr[4] = {bf2f((bf16_t)(pk.x & 0xffffu)), bf2f((bf16_t)(pk.x >> 16)),
-                               bf2f((bf16_t)(pk.y & 0xffffu)), bf2f((bf16_t)(pk.y >> 16))};
+          const float vr[4] = {s16_to_f<T>((uint16_t)(pk.x & 0xffffu)), s16_to_f<T>((uint16_t)(pk.x >> 16)),
+                               s16_to_f<T>((uint16_t)(pk.y & 0xffffu)), s16_to_f<T>((uint16_t)(pk.y >> 16))};
           if (!have_shift && i == 0) {
             // the wave's first pixel (of its first tile) is its statistics shift
 #pragma unroll
@@ -1138,9 +1144,8 @@ constexpr int HALO16_PROWS = 640;   // patch pixels per buffer
 constexpr int HALO16_WAVES = 4;     // waves per block; two blocks per CU overlap each other's epilogues
 constexpr int HALO16_BM = 64 * HALO16_WAVES;
 
-template <bool STATS>
+template <typename T, bool STATS>
 __global__ __launch_bounds__(64 * HALO16_WAVES, 2) void conv_halo16_kernel(ConvHalo h) {
-  typedef bf16_t T;
   typedef int i32x2_t __attribute__((ext_vector_type(2)));
   constexpr int NW = HALO16_WAVES, FM = 4, FN = 4;
   constexpr int B_U4 = 16 * 64 * 2;                 // resident weights, uint4 units (32-byte rows)
@@ -1274,12 +1279,12 @@ __global__ __launch_bounds__(64 * HALO16_WAVES, 2) void conv_halo16_kernel(ConvH
       const uint32_t ob = (uint32_t)((m0 + (ok ? q : 0)) * g.Cols) + chl;
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
-        const uint2 pk = make_uint2(f2bf2(acc[i][j][0], acc[i][j][1]), f2bf2(acc[i][j][2], acc[i][j][3]));
+        const uint2 pk = make_uint2(pack2<T>(acc[i][j][0], acc[i][j][1]), pack2<T>(acc[i][j][2], acc[i][j][3]));
         __builtin_amdgcn_raw_buffer_store_b64(i32x2_t{(int)pk.x, (int)pk.y}, rsC, ok ? (ob + j * 16) * 2 : kOutOfRange,
                                               0, 0);
         if constexpr (STATS) {
-          const float vr[4] = {bf2f((bf16_t)(pk.x & 0xffffu)), bf2f((bf16_t)(pk.x >> 16)),
-                               bf2f((bf16_t)(pk.y & 0xffffu)), bf2f((bf16_t)(pk.y >> 16))};
+          const float vr[4] = {s16_to_f<T>((uint16_t)(pk.x & 0xffffu)), s16_to_f<T>((uint16_t)(pk.x >> 16)),
+                               s16_to_f<T>((uint16_t)(pk.y & 0xffffu)), s16_to_f<T>((uint16_t)(pk.y >> 16))};
           if (!have_shift && i == 0) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) sh[j][e] = __shfl(vr[e], lane & 48, 64);
@@ -1320,382 +1325,6 @@ __global__ __launch_bounds__(64 * HALO16_WAVES, 2) void conv_halo16_kernel(ConvH
 }
 
 // ---------------------------------------------------------------------------
-// Halo conv with streamed weights for the 3x3 stride-1 convolutions with 128
-// or more input channels (bf16; forward and stride-1 data gradient). A tile is
-// TH whole output rows of one image by 128 output columns. For each half of a
-// 64-channel block (32 channels) the input patch (TH + 2) x (W + 2) with its
-// zero halo is staged in LDS once (double-buffered across halves) and all
-// nine taps read it at a fixed pixel offset, so an input pixel crosses from L2
-// about (TH + 2) / TH times per half instead of nine; the weights of a (half,
-// tap) step, 128 columns x 64 bytes, stream through an LDS ring of HW_RING
-// slots, HW_RING - 2 steps ahead.
-// The GEMM rows of a tile are the patch-width grid: row v = r (W + 2) + c is
-// output pixel (r, c) for c < W, and the two columns past the row end are
-// computed and dropped. Tap (th, tw) of row v then reads patch pixel v + th
-// (W + 2) + tw: 16 consecutive rows read 16 consecutive patch pixels (no LDS
-// bank conflicts) at a constant offset per tap (no per-step address
-// arithmetic).
-// Four waves, one per SIMD: two along rows (7 groups of 16 each, so at most
-// 224 rows per tile) and two along columns (64 each), 16x16x32 MFMAs with the
-// weight fragment as the first operand, so a lane holds four consecutive
-// channels of one row. Persistent blocks walk the tiles; the epilogue stores
-// from registers and, in the forward pass, writes BN partial statistics per
-// (tile, row wave): 2 entries per tile.
-// Patch and ring rows are 64 bytes; chunk c of row p sits in slot c ^ ((p / 4)
-// % 4), which keeps 16 consecutive rows of an operand read on distinct banks,
-// and since a shift by 16 rows keeps the swizzle, the 16-row groups of one tap
-// are constant offsets from one address per tap. One LDS-DMA instruction
-// fills 16 rows (16 cache lines).
-// ---------------------------------------------------------------------------
-struct ConvHaloW {
-  ConvGather g;
-  int TH;          // output rows per tile
-  int PW;          // patch columns (W + 2)
-  int PP;          // patch pixels (TH + 2) * PW
-  int tiles_img;   // ceil(Hm / TH)
-  int tiles_m;     // N * tiles_img
-  int tiles;       // tiles_m * Cols / 128
-  FastDiv fd_pw;   // division by PW
-};
-
-#ifndef RN18_HW_RING
-#define RN18_HW_RING 3
-#endif
-#ifndef RN18_HW_BPC
-#define RN18_HW_BPC 1
-#endif
-#ifndef RN18_HW_WGN
-#define RN18_HW_WGN 4
-#endif
-constexpr int HW_WGN = RN18_HW_WGN;          // column waves: 2 (64 columns each) or 4 (32 each)
-constexpr int HW_WAVES = 2 * HW_WGN;
-constexpr int HW_FM = 7;                     // 16-row groups per row wave
-constexpr int HW_ROWS = 2 * HW_FM * 16;      // GEMM rows per tile (224)
-constexpr int HW_BN = 128;
-constexpr int HW_PROWS = HW_WGN == 2 ? 320 : 384;  // patch pixels per half buffer
-constexpr int HW_RING = RN18_HW_RING;        // weight ring slots: 3 or 6 (a divisor of 18)
-constexpr int HW_BPC = RN18_HW_BPC;          // blocks per CU
-// (at most 6: the weights that the wait before a half's first read covers are
-// issued after that half's patch pieces)
-static_assert(HW_RING == 3 || HW_RING == 6, "ring depth");
-
-// s_waitcnt vmcnt(n) for a wave-uniform n in 0..31
-__device__ inline void wait_vmcnt_dyn(int n) {
-  switch (n) {
-#define RN18_W(N) case N: wait_vmcnt<N>(); break;
-    RN18_W(0) RN18_W(1) RN18_W(2) RN18_W(3) RN18_W(4) RN18_W(5) RN18_W(6) RN18_W(7) RN18_W(8) RN18_W(9)
-    RN18_W(10) RN18_W(11) RN18_W(12) RN18_W(13) RN18_W(14) RN18_W(15) RN18_W(16) RN18_W(17) RN18_W(18)
-    RN18_W(19) RN18_W(20) RN18_W(21) RN18_W(22) RN18_W(23) RN18_W(24) RN18_W(25) RN18_W(26) RN18_W(27)
-    RN18_W(28) RN18_W(29) RN18_W(30)
-#undef RN18_W
-    default: wait_vmcnt<0>(); break;
-  }
-}
-
-template <int MODE, bool STATS>
-__global__ __launch_bounds__(64 * HW_WAVES, HW_BPC) void conv_halo_wide_kernel(ConvHaloW h) {
-  typedef bf16_t T;
-  constexpr int NW = HW_WAVES, FM = HW_FM, FN = HW_BN / HW_WGN / 16, WTN = HW_BN / HW_WGN;
-  constexpr int BUF_P = HW_PROWS * 64;              // bytes of one patch buffer
-  constexpr int SLOT_R = HW_BN * 64;                // one ring slot
-  constexpr int PI = HW_PROWS / 16 / NW;            // patch load instructions per wave, one per step
-  constexpr int BI = HW_BN / 16 / NW;               // ring load instructions per wave and step
-  static_assert(PI <= 5 && BI >= 1 && HW_PROWS % (16 * NW) == 0 && HW_BN % (16 * NW) == 0,
-                "patch pieces at steps 0..4, whole ring loads per wave");
-  __shared__ uint4 smem[(2 * BUF_P + HW_RING * SLOT_R) / 16];
-  static_assert(HW_BPC * (2 * BUF_P + HW_RING * SLOT_R) <= 163840, "LDS");
-  const ConvGather& g = h.g;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / HW_WGN, wn = wave % HW_WGN;
-  const uint32_t smem_lds = lds_addr(smem);
-  const int rowb = g.Cin * 2;                        // bytes per input pixel and per weight tap row
-  const int HC = g.Cin / 32;                         // channel halves (even)
-  const i32x4_t rsA = buffer_rsrc(g.A, (uint32_t)((long)g.N * g.Hin * g.Win * rowb));
-  const i32x4_t rsB = buffer_rsrc(g.B, (uint32_t)((long)g.Cols * g.KHW * rowb));
-  const int G = gridDim.x;
-  const int slot = xcd_remap(blockIdx.x, G);
-  const int NT = g.Cols / HW_BN;
-
-  // patch loads: instruction u of wave w covers patch pixels (w + 4 u) * 16 ..
-  // + 15; the lane's 16 bytes go to slot lane % 4 of pixel p and hold chunk
-  // (lane % 4) ^ ((p / 4) % 4)
-  int prel[PI], prow[PI];
-#pragma unroll
-  for (int u = 0; u < PI; ++u) {
-    const int p = (wave + NW * u) * 16 + (lane >> 2);
-    const int pr = p / h.PW, pc = p - pr * h.PW;
-    const int ir = -g.ip + g.dh0 + pr, ic = -g.ip + g.dw0 + pc;
-    const bool ok = p < h.PP && (unsigned)ic < (unsigned)g.Win;
-    prel[u] = (ir * g.Win + ic) * rowb + (((lane & 3) ^ ((p >> 2) & 3)) * 16);
-    prow[u] = ok ? ir : -0x40000000;
-  }
-  auto issue_patch = [&](int tile, int half, int buf, int u) {
-    const int mt = tile / NT;
-    const int n = mt / h.tiles_img, i0 = (mt - n * h.tiles_img) * h.TH;
-    const int base = (n * g.Hin + i0) * g.Win * rowb + half * 64;
-    const bool ok = (unsigned)(i0 + prow[u]) < (unsigned)g.Hin;
-    lds_dma16_buf(ok ? (uint32_t)(base + prel[u]) : kOutOfRange, rsA,
-                  smem_lds + (uint32_t)(buf * BUF_P + (wave + NW * u) * 1024));
-  };
-  // weight loads: instruction v of wave w covers tile columns (w + 4 v) * 16
-  // .. + 15, same slot layout. wlane[v]: the lane's column offset within the
-  // tile's first column (set per tile); a step adds a scalar offset.
-  const int colstride = g.KHW * rowb;                // bytes between weight columns
-  uint32_t wlane[BI];
-  auto issue_w = [&](int half, int t, int rs) {
-    const int th = t / 3, tw = t - th * 3;
-    const int wt = (g.wkh0 + th * g.wkhs) * g.KW + g.wkw0 + tw * g.wkws;
-    const uint32_t so = (uint32_t)(wt * rowb + half * 64);
-#pragma unroll
-    for (int v = 0; v < BI; ++v)
-      lds_dma16_buf(wlane[v] + so, rsB,
-                    smem_lds + (uint32_t)(2 * BUF_P + rs * SLOT_R + (wave + NW * v) * 1024));
-  };
-
-  const int kq = lane >> 4;
-  const int chl = 4 * (lane >> 4);
-  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-  typedef __attribute__((address_space(3))) const u32x4_t* lds_u4_t;
-  // B operand rows of this lane in ring slot 0 (a slot or 16-column group is a
-  // constant element offset)
-  const int bcol = wn * WTN + (lane & 15);
-  const lds_u4_t bptr = (lds_u4_t)smem + (2 * BUF_P) / 16 + bcol * 4 + (kq ^ ((bcol >> 2) & 3));
-  const int v0 = wm * FM * 16 + (lane & 15);          // this lane's GEMM row in group 0
-  const uint32_t out_bytes = (uint32_t)((long)g.N * g.Hout * g.Wout * g.Cols * 2);
-  const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, out_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rsR = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<void*>(g.mode == 1 || !g.R ? (const void*)g.C : g.R), 0, out_bytes, 0x00020000);
-  // ReLU mask bytes of the residual: one byte per 8 output elements
-  const __amdgpu_buffer_rsrc_t rsRm = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<void*>(g.Rm ? g.Rm : (const void*)g.C), 0, out_bytes / 16, 0x00020000);
-  typedef int i32x2_t __attribute__((ext_vector_type(2)));
-
-  bool first = true;
-  if (slot < h.tiles) {
-#pragma unroll
-    for (int u = 0; u < PI; ++u) issue_patch(slot, 0, 0, u);
-  }
-  for (int tile = slot; tile < h.tiles; tile += G) {
-    const int mt = tile / NT, n0 = (tile % NT) * HW_BN;
-    const int n = mt / h.tiles_img, i0 = (mt - n * h.tiles_img) * h.TH;
-    const int rows_t = min(h.TH, g.Hm - i0);          // output rows of this tile
-    // A operand rows per tap (patch buffer 0, group 0): group i adds 16 rows
-    // (same swizzle), the buffer a constant
-    lds_u4_t atap[9];
-#pragma unroll
-    for (int t = 0; t < 9; ++t) {
-      const int p = v0 + (t / 3) * h.PW + t % 3;
-      atap[t] = (lds_u4_t)smem + p * 4 + (kq ^ ((p >> 2) & 3));
-    }
-#pragma unroll
-    for (int v = 0; v < BI; ++v) {
-      const int col = n0 + (wave + NW * v) * 16 + (lane >> 2);
-      wlane[v] = (uint32_t)(col * colstride + ((lane & 3) ^ ((col >> 2) & 3)) * 16);
-    }
-    floatx4_t acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-
-    // tile prologue: the ring slots are reloaded with the tile's first
-    // HW_RING - 1 steps once every wave is done with the previous tile's
-    // reads; the tile's first half-patch was issued before (block start or
-    // the previous tile's last half)
-    if (!first) {
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      barrier_only();
-    }
-    first = false;
-#pragma unroll
-    for (int q = 0; q < HW_RING - 1; ++q) issue_w(0, q, q);
-    wait_vmcnt<BI * (HW_RING - 2)>();
-    barrier_only();
-    const int next = tile + G < h.tiles ? tile + G : -1;
-    // operands of pair step k (half k / 9 of the pair, tap t = k % 9): patch
-    // buffer (k / 9) % 2 at tap offset t / 3 rows, t % 3 columns; ring slot
-    // k % HW_RING
-    auto read_step = [&](int k, uint4(&a)[FM], uint4(&b)[FN]) {
-      const int t = k % 9;
-      const int bo = ((k / 9) & 1) * (BUF_P / 16);
-#pragma unroll
-      for (int i = 0; i < FM; ++i) a[i] = __builtin_bit_cast(uint4, atap[t][i * 64 + bo]);
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        b[j] = __builtin_bit_cast(uint4, bptr[(k % HW_RING) * (SLOT_R / 16) + j * 64]);
-    };
-    auto mma_step = [&](const uint4(&a)[FM], const uint4(&b)[FN]) {
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) Mma<T>::run(acc[i][j], b[j], a[i], 0);
-    };
-    uint4 a0[FM], b0[FN], a1[FM], b1[FN];
-    read_step(0, a0, b0);
-    // pairs of halves: 18 steps, step k reads step k+1's operands (the next
-    // pair's first step at k = 17) into the other register set before its
-    // MFMAs. The next half-patch (or the next tile's first) goes out one
-    // piece per step at the first PI steps of a half.
-    for (int hp = 0; hp < HC; hp += 2) {
-      const bool more_pair = hp + 2 < HC;
-      const bool pn2 = more_pair || next >= 0;       // the pair's second half issues patch pieces
-#pragma unroll
-      for (int k = 0; k < 18; ++k) {
-        const int half = hp + k / 9, t = k % 9;
-        const bool more = k < 9 || more_pair;        // a half follows this one in the tile
-        const bool patch_next = more || next >= 0;
-        const bool last = !more_pair && k == 17;
-        if (!last) {
-          // the weights of step k+1 (issued HW_RING - 2 steps ago, or in the
-          // prologue) have landed; the weights and patch pieces issued after
-          // them may stay in flight. Vector memory operations complete in
-          // issue order.
-          {
-            // later weight steps: k+2 .. k+HW_RING-2 that exist in the tile
-            int later = HW_RING - 3;
-            if (!more_pair) later = min(later, 16 - k);
-            later *= BI;
-            // patch pieces from steps max(k - HW_RING + 2, tile start) .. k-1
-#pragma unroll
-            for (int d = 1; d <= HW_RING - 2; ++d) {
-              const int kp = k - d;
-              const int tp = ((kp % 9) + 9) % 9;
-              if (tp >= PI) continue;
-              if (kp < 0) {
-                if (hp > 0) later += 1;                 // previous pair's second half (more follows)
-              } else if (kp < 9) {
-                later += 1;                             // this pair's first half (more follows)
-              } else if (pn2) {
-                later += 1;
-              }
-            }
-            // before the next half's first read, its patch pieces (steps
-            // 0..PI-1 of this half) must have landed too
-            if (t == 8) later = min(later, BI * (8 - PI));
-            wait_vmcnt_dyn(later);
-          }
-          barrier_only();
-          // the weights of step k + HW_RING - 1 into the slot step k-1 used
-          {
-            const int kn = k + HW_RING - 1;
-            const int rs = kn % HW_RING;
-            if (kn < 18) issue_w(hp + kn / 9, kn % 9, rs);
-            else if (more_pair) issue_w(hp + 2, kn - 18, rs);
-          }
-          if (t < PI && patch_next) {
-            if (more) issue_patch(tile, half + 1, (half + 1) & 1, t);
-            else issue_patch(next, 0, 0, t);
-          }
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        if ((k & 1) == 0) {
-          read_step(k + 1, a1, b1);
-          __builtin_amdgcn_sched_barrier(0);
-          mma_step(a0, b0);
-        } else {
-          if (!last) read_step((k + 1) % 18, a0, b0);
-          __builtin_amdgcn_sched_barrier(0);
-          mma_step(a1, b1);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-
-    // ---- epilogue straight from registers
-    const long m0 = ((long)n * g.Hm + i0) * g.Wm;
-    float s1[FN][4], s2[FN][4], sh[FN][4];
-    float cnt = 0.f;
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) s1[j][e] = s2[j][e] = sh[j][e] = 0.f;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int v = v0 + i * 16;
-      const int r = (int)h.fd_pw.div(v), c = v - r * h.PW;
-      const bool okq = r < rows_t && c < g.Wm;
-      const uint32_t ob = (uint32_t)((m0 + (okq ? r * g.Wm + c : 0)) * g.Cols) + n0 + wn * WTN + chl;
-      i32x2_t ld0[FN];
-      uint32_t ld1[FN];
-      if constexpr (MODE != 0) {
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const uint32_t o = okq ? (ob + j * 16) * 2 : kOutOfRange;
-          ld0[j] = __builtin_amdgcn_raw_buffer_load_b64(rsR, o, 0, 0);
-          if constexpr (MODE == 2)
-            ld1[j] = __builtin_amdgcn_raw_buffer_load_b8(rsRm, okq ? (ob + j * 16) >> 3 : kOutOfRange, 0, 0);
-        }
-      }
-      cnt += okq ? 1.f : 0.f;
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        float x[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-        if constexpr (MODE != 0) {
-          const uint32_t rw[2] = {(uint32_t)ld0[j].x, (uint32_t)ld0[j].y};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float rv = bf2f((bf16_t)(e & 1 ? rw[e >> 1] >> 16 : rw[e >> 1] & 0xffffu));
-            if constexpr (MODE == 2) {
-              // this lane's 4 channels are the low or high half of the byte
-              x[e] += (ld1[j] >> ((chl & 4) + e)) & 1u ? rv : 0.f;
-            } else {
-              x[e] += rv;
-            }
-          }
-        }
-        const uint2 pk = make_uint2(f2bf2(x[0], x[1]), f2bf2(x[2], x[3]));
-        __builtin_amdgcn_raw_buffer_store_b64(i32x2_t{(int)pk.x, (int)pk.y}, rsC,
-                                              okq ? (ob + j * 16) * 2 : kOutOfRange, 0, 0);
-        if constexpr (STATS) {
-          const float vr[4] = {bf2f((bf16_t)(pk.x & 0xffffu)), bf2f((bf16_t)(pk.x >> 16)),
-                               bf2f((bf16_t)(pk.y & 0xffffu)), bf2f((bf16_t)(pk.y >> 16))};
-          if (i == 0) {
-            // the value of the wave's first GEMM row is its statistics shift
-            // (a conv output of the tile's data, valid or one of the dropped
-            // columns)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) sh[j][e] = __shfl(vr[e], lane & 48, 64);
-          }
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float d = okq ? vr[e] - sh[j][e] : 0.f;
-            s1[j][e] += d;
-            s2[j][e] = __builtin_fmaf(d, d, s2[j][e]);
-          }
-        }
-      }
-    }
-    if constexpr (STATS) {
-      // one entry per (tile, row wave) for this wave's 64 columns: the sums
-      // over the 16 rows of a lane group are shuffled together, then each
-      // lane writes one channel
-      const int kk = lane & 15, jj = kk >> 2, rr = kk & 3;
-      float o1 = 0.f, o2 = 0.f, osh = 0.f;
-#pragma unroll
-      for (int dd = 1; dd < 16; dd <<= 1) cnt += __shfl_xor(cnt, dd, 16);
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float a1v = s1[j][r], a2v = s2[j][r];
-#pragma unroll
-          for (int dd = 1; dd < 16; dd <<= 1) {
-            a1v += __shfl_xor(a1v, dd, 16);
-            a2v += __shfl_xor(a2v, dd, 16);
-          }
-          if (j == jj && r == rr) { o1 = a1v; o2 = a2v; osh = sh[j][r]; }
-        }
-      if (jj < FN) {
-        float4* out = (float4*)g.stats + ((long)(mt * 2 + wm) * g.Cols + n0 + wn * WTN + jj * 16 + chl + rr);
-        *out = cnt > 0.f ? make_float4(cnt, osh, o1, o2) : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-    }
-  }
-  wait_vmcnt<0>();
-}
-
-// ---------------------------------------------------------------------------
 // Weight gradient
 // ---------------------------------------------------------------------------
 template <typename T> struct Tr;
@@ -1718,6 +1347,7 @@ template <> struct Tr<bf16_t> {
     }
   }
 };
+template <> struct Tr<f16_t> : Tr<bf16_t> {};
 template <> struct Tr<float> {
   __device__ static inline void run(const uint4 (&in)[4], uint4 (&out)[4]) {
     out[0] = make_uint4(in[0].x, in[1].x, in[2].x, in[3].x);
@@ -1893,6 +1523,12 @@ template <> struct WOp<bf16_t> {
   __device__ static inline void mma(floatx4_t& acc, const uint4& a, const uint4& b) {
     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
                                                   acc, 0, 0, 0);
+  }
+};
+template <> struct WOp<f16_t> : WOp<bf16_t> {
+  __device__ static inline void mma(floatx4_t& acc, const uint4& a, const uint4& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), acc,
+                                                 0, 0, 0);
   }
 };
 template <> struct WOp<float> {
@@ -2123,6 +1759,7 @@ struct WgradHalo {
 constexpr int WGH_PROWS = 384;   // patch rows per buffer
 constexpr int WGH_YROWS = 256;   // dY rows per buffer
 
+template <typename T>
 __global__ __launch_bounds__(256, 1) void conv_wgrad_halo_kernel(WgradHalo h) {
   constexpr int P_U4 = WGH_PROWS * 8, Y_U4 = WGH_YROWS * 8;
   constexpr int BUF_U4 = P_U4 + Y_U4;
@@ -2255,8 +1892,7 @@ __global__ __launch_bounds__(256, 1) void conv_wgrad_halo_kernel(WgradHalo h) {
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int t = 0; t < 9; ++t)
-          acc[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[i]),
-                                                              __builtin_bit_cast(bf16x8_t, b[t]), acc[i][t], 0, 0, 0);
+          Mma<T>::run(acc[i][t], a[i], b[t], 0);
     };
     uint4 a0[4], b0[9], a1[4], b1[9];
     const int S = (npx + 31) / 32;
@@ -2457,7 +2093,7 @@ int launch_gather_ps(const ConvGather* probs, int np, hipStream_t s) {
 // one it handles (bf16, 64 -> 64 channels, 3x3 taps walked forward with
 // stride 1, output rows = GEMM rows, whole-row tiles that divide the image).
 int halo_rows(int prec, const ConvGather& g) {
-  if (prec != PREC_BF16 || g.Cin != 64 || g.Cols != 64 || g.nth != 3 || g.ntw != 3 || g.KHW != 9 || g.K != 576)
+  if (prec == PREC_F32 || g.Cin != 64 || g.Cols != 64 || g.nth != 3 || g.ntw != 3 || g.KHW != 9 || g.K != 576)
     return 0;
   if (g.is != 1 || g.os != 1 || g.oph != 0 || g.opw != 0 || g.dhs != 1 || g.dws != 1) return 0;
   if (g.Hout != g.Hm || g.Wout != g.Wm || g.Hm < 1 || g.Wm < 1) return 0;
@@ -2476,7 +2112,7 @@ int halo_rows(int prec, const ConvGather& g) {
 // Tile height of the stem halo kernel, or 0 when the launch is not one it
 // handles (bf16, 16 -> 64 channels, a forward 4x4 stride-1 tap walk, mode 0).
 int halo16_rows(int prec, const ConvGather& g) {
-  if (prec != PREC_BF16 || g.Cin != 16 || g.Cols != 64 || g.nth != 4 || g.ntw != 4 || g.KHW != 16 || g.KW != 4 ||
+  if (prec == PREC_F32 || g.Cin != 16 || g.Cols != 64 || g.nth != 4 || g.ntw != 4 || g.KHW != 16 || g.KW != 4 ||
       g.K != 256)
     return 0;
   if (g.is != 1 || g.os != 1 || g.oph != 0 || g.opw != 0 || g.dh0 != 0 || g.dw0 != 0 || g.dhs != 1 || g.dws != 1 ||
@@ -2493,6 +2129,7 @@ int halo16_rows(int prec, const ConvGather& g) {
   return th;
 }
 
+template <typename T>
 int launch_halo16(const ConvGather& g0, int th, hipStream_t s) {
   ConvHalo h{};
   h.g = g0;
@@ -2508,11 +2145,12 @@ int launch_halo16(const ConvGather& g0, int th, hipStream_t s) {
   if (slots < 1) return -4;
   const int grid = h.tiles < slots ? h.tiles : slots;
   constexpr int NT = 64 * HALO16_WAVES;
-  if (g0.stats) hipLaunchKernelGGL((conv_halo16_kernel<true>), dim3(grid), dim3(NT), 0, s, h);
-  else hipLaunchKernelGGL((conv_halo16_kernel<false>), dim3(grid), dim3(NT), 0, s, h);
+  if (g0.stats) hipLaunchKernelGGL((conv_halo16_kernel<T, true>), dim3(grid), dim3(NT), 0, s, h);
+  else hipLaunchKernelGGL((conv_halo16_kernel<T, false>), dim3(grid), dim3(NT), 0, s, h);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
+template <typename T>
 int launch_halo(const ConvGather& g0, int th, hipStream_t s) {
   ConvHalo h{};
   h.g = g0;
@@ -2529,72 +2167,14 @@ int launch_halo(const ConvGather& g0, int th, hipStream_t s) {
   const int grid = h.tiles < cus ? h.tiles : cus;
   const bool st = g0.stats != nullptr;
   constexpr int NT = 64 * HALO_WAVES;
-  if (g0.mode == 0 && st) hipLaunchKernelGGL((conv_halo_kernel<0, true>), dim3(grid), dim3(NT), 0, s, h);
-  else if (g0.mode == 0) hipLaunchKernelGGL((conv_halo_kernel<0, false>), dim3(grid), dim3(NT), 0, s, h);
-  else if (g0.mode == 1 && !st) hipLaunchKernelGGL((conv_halo_kernel<1, false>), dim3(grid), dim3(NT), 0, s, h);
-  else if (g0.mode == 2 && !st) hipLaunchKernelGGL((conv_halo_kernel<2, false>), dim3(grid), dim3(NT), 0, s, h);
+  if (g0.mode == 0 && st) hipLaunchKernelGGL((conv_halo_kernel<T, 0, true>), dim3(grid), dim3(NT), 0, s, h);
+  else if (g0.mode == 0) hipLaunchKernelGGL((conv_halo_kernel<T, 0, false>), dim3(grid), dim3(NT), 0, s, h);
+  else if (g0.mode == 1 && !st) hipLaunchKernelGGL((conv_halo_kernel<T, 1, false>), dim3(grid), dim3(NT), 0, s, h);
+  else if (g0.mode == 2 && !st) hipLaunchKernelGGL((conv_halo_kernel<T, 2, false>), dim3(grid), dim3(NT), 0, s, h);
   else return -1;
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
-// Tile height of the streamed-weight halo kernel, or 0 when the launch is
-// not one it handles (bf16, 128..512 input channels in 64-channel blocks,
-// output columns in 128-column tiles, a 3x3 stride-1 tap walk, modes 0-2 with
-// statistics only in mode 0). Rows are balanced across an image's tiles;
-// tiles of fewer than 128 pixels (small images) are left to the gather kernel.
-int haloW_rows(int prec, const ConvGather& g) {
-  if (prec != PREC_BF16 || g.Cin % 64 != 0 || g.Cin < 128 || g.Cin > 512 || g.Cols % HW_BN != 0 || g.nth != 3 ||
-      g.ntw != 3 || g.KHW != 9 || g.K != 9 * g.Cin)
-    return 0;
-  if (g.is != 1 || g.os != 1 || g.oph != 0 || g.opw != 0 || g.dhs != 1 || g.dws != 1) return 0;
-  if (g.Hout != g.Hm || g.Wout != g.Wm || g.Hm < 1 || g.Wm < 1) return 0;
-  if (g.mode < 0 || g.mode > 2 || (g.mode != 0 && g.stats)) return 0;
-  if ((long)g.N * g.Hin * g.Win * g.Cin * 2 >= (1l << 31) || (long)g.N * g.Hout * g.Wout * g.Cols * 2 >= (1l << 31) ||
-      (long)g.Cols * g.KHW * g.Cin * 2 >= (1l << 31))
-    return 0;
-  // GEMM rows TH (W + 2) <= 224; every row's taps stay inside the patch
-  // buffer: 224 + 2 (W + 2) + 2 <= 320
-  const int pw = g.Wm + 2;
-  if (HW_ROWS + 2 * pw + 2 > HW_PROWS) return 0;
-  int thmax = HW_ROWS / pw;
-  if (thmax > g.Hm) thmax = g.Hm;
-  if (thmax < 1) return 0;
-  const int tiles_img = (g.Hm + thmax - 1) / thmax;
-  const int th = (g.Hm + tiles_img - 1) / tiles_img;
-  const int last = g.Hm - (tiles_img - 1) * th;
-  if (last * g.Wm < 96) return 0;
-  // two statistics entries per tile: at most one per 32 GEMM rows
-  if (g.stats && (long)g.N * tiles_img * 2 > ((long)g.M + 31) / 32) return 0;
-  return th;
-}
-
-int launch_haloW(const ConvGather& g0, int th, hipStream_t s) {
-  ConvHaloW h{};
-  h.g = g0;
-  h.g.fd_hw = FastDiv((uint32_t)(g0.Hm * g0.Wm));
-  h.g.fd_w = FastDiv((uint32_t)g0.Wm);
-  h.TH = th;
-  h.PW = g0.Wm + 2;
-  h.PP = (th + 2) * h.PW;
-  h.fd_pw = FastDiv((uint32_t)h.PW);
-  h.tiles_img = (g0.Hm + th - 1) / th;
-  h.tiles_m = g0.N * h.tiles_img;
-  h.tiles = h.tiles_m * (g0.Cols / HW_BN);
-  if (h.tiles <= 0) return 0;
-  if (h.PP > HW_PROWS || th * h.PW > HW_ROWS || HW_ROWS + 2 * h.PW + 2 > HW_PROWS) return -1;
-  const int cus = cu_count();
-  if (cus < 1) return -4;
-  const int slots = HW_BPC * cus;
-  const int grid = h.tiles < slots ? h.tiles : slots;
-  const bool st = g0.stats != nullptr;
-  constexpr int NT = 64 * HW_WAVES;
-  if (g0.mode == 0 && st) hipLaunchKernelGGL((conv_halo_wide_kernel<0, true>), dim3(grid), dim3(NT), 0, s, h);
-  else if (g0.mode == 0) hipLaunchKernelGGL((conv_halo_wide_kernel<0, false>), dim3(grid), dim3(NT), 0, s, h);
-  else if (g0.mode == 1 && !st) hipLaunchKernelGGL((conv_halo_wide_kernel<1, false>), dim3(grid), dim3(NT), 0, s, h);
-  else if (g0.mode == 2 && !st) hipLaunchKernelGGL((conv_halo_wide_kernel<2, false>), dim3(grid), dim3(NT), 0, s, h);
-  else return -1;
-  return hipGetLastError() == hipSuccess ? 0 : -4;
-}
 
 // Kernel configurations: id -> (BM, BN, waves along M, waves along N, stages,
 // kind: 0 plain loop, 1 register-prefetched loop, 2 persistent).
@@ -2638,17 +2218,10 @@ bool use_halo(int prec, const ConvGather& g) {
 bool use_halo16(int prec, const ConvGather& g) {
   return (g_gather_override == 0 || g_gather_override == kGatherHalo) && halo16_rows(prec, g) > 0;
 }
-// Measured on MI355X (bf16, batch 256, 28x28x128 and 14x14x256): within a
-// few percent of the 128x128 gather tile, so the automatic choice keeps the
-// gather kernel and this one runs when selected explicitly.
-bool use_haloW(int prec, const ConvGather& g) {
-  return g_gather_override == kGatherHalo && haloW_rows(prec, g) > 0;
-}
 
 int gather_tile(int prec, const ConvGather& g) {
   if (use_halo(prec, g)) return HALO_BM * 1000 + 64;
   if (use_halo16(prec, g)) return HALO16_BM * 1000 + 64;
-  if (use_haloW(prec, g)) return haloW_rows(prec, g) * (g.Wm + 2) * 1000 + HW_BN;
   const int id = gather_cfg(g);
   return id >= 1 && id <= kGatherCfgs ? kGather[id].bm * 1000 + kGather[id].bn : 0;
 }
@@ -2673,11 +2246,13 @@ int gather_cfg_multi(const ConvGather* g, int np) {
 
 template <typename T>
 int gather_dispatch(const ConvGather* g, int np, hipStream_t s) {
-  const int prec = sizeof(T) == 2 ? PREC_BF16 : PREC_F32;
+  const int prec = prec_of<T>();
   const bool seg2 = gather_has_seg2(g, np);
-  if (!seg2 && np == 1 && use_halo(prec, g[0])) return launch_halo(g[0], halo_rows(prec, g[0]), s);
-  if (!seg2 && np == 1 && use_halo16(prec, g[0])) return launch_halo16(g[0], halo16_rows(prec, g[0]), s);
-  if (!seg2 && np == 1 && use_haloW(prec, g[0])) return launch_haloW(g[0], haloW_rows(prec, g[0]), s);
+  if constexpr (sizeof(T) == 2) {
+    // the halo kernels are instantiated for the 16-bit storage types only
+    if (!seg2 && np == 1 && use_halo(prec, g[0])) return launch_halo<T>(g[0], halo_rows(prec, g[0]), s);
+    if (!seg2 && np == 1 && use_halo16(prec, g[0])) return launch_halo16<T>(g[0], halo16_rows(prec, g[0]), s);
+  }
   switch (gather_cfg_multi(g, np)) {
 #define RN18_X(id, bm, bn, wgm, wgn, st, kind)                                               \
   case id:                                                                                 \
@@ -2723,7 +2298,7 @@ int g_wgrad_override = 0;
 int wgrad_cfg(int prec, int Cout, int Kcols) {
   if (g_wgrad_override) return g_wgrad_override;
   if (Cout <= 16) return 1;
-  if (prec == PREC_BF16) {
+  if (prec != PREC_F32) {
     if (Cout <= 64) return 4;
     return Kcols <= 576 ? 9 : 10;
   }
@@ -2740,7 +2315,7 @@ void wgrad_tile(int prec, int Cout, int Kcols, int* bm, int* bn) {
 
 template <typename T>
 int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
-  switch (wgrad_cfg(sizeof(T) == 2 ? PREC_BF16 : PREC_F32, g.Cout, g.Kcols)) {
+  switch (wgrad_cfg(prec_of<T>(), g.Cout, g.Kcols)) {
     case 1: return launch_wgrad<T, 16, 64, 1, 4>(g, s);
     case 2: return launch_wgrad<T, 64, 64, 2, 2>(g, s);
     case 3: return launch_wgrad<T, 128, 128, 2, 2>(g, s);
@@ -2760,7 +2335,7 @@ int wgrad_dispatch(const ConvWgrad& g, hipStream_t s) {
 int wgrad_halo_pw(const ConvWgrad& g) { return (g.W + 2 + 7) / 8 * 8; }
 
 int wgrad_halo_rows(int prec, const ConvWgrad& g) {
-  if (prec != PREC_BF16 || g.Cin != 64 || g.Cout != 64 || g.KH != 3 || g.KW != 3 || g.stride != 1 || g.pad != 1)
+  if (prec == PREC_F32 || g.Cin != 64 || g.Cout != 64 || g.KH != 3 || g.KW != 3 || g.stride != 1 || g.pad != 1)
     return 0;
   if (g.Ho != g.H || g.Wo != g.W || g.H < 1 || g.W < 1 || g.W > 256) return 0;
   if ((long)g.N * g.H * g.W * 128 >= (1l << 31)) return 0;
@@ -2779,16 +2354,17 @@ int wgrad_halo_grid(int prec, const ConvWgrad& g) {
   return (int)(strips < cus ? strips : cus);
 }
 
+template <typename T>
 int launch_wgrad_halo(const ConvWgrad& g, hipStream_t s) {
   WgradHalo h{};
   h.DY = g.DY; h.X = g.X; h.P = g.P;
   h.N = g.N; h.H = g.H; h.W = g.W;
-  h.TH = wgrad_halo_rows(PREC_BF16, g);
+  h.TH = wgrad_halo_rows(prec_of<T>(), g);
   h.PW = wgrad_halo_pw(g); h.PH = h.TH + 2;
   h.strips_img = (g.H + h.TH - 1) / h.TH;
   h.strips = g.N * h.strips_img;
-  if (g.splits != wgrad_halo_grid(PREC_BF16, g) || g.splits < 1) return -1;   // split count planned for this kernel
-  hipLaunchKernelGGL(conv_wgrad_halo_kernel, dim3(g.splits), dim3(256), 0, s, h);
+  if (g.splits != wgrad_halo_grid(prec_of<T>(), g) || g.splits < 1) return -1;   // split count planned for this kernel
+  hipLaunchKernelGGL(conv_wgrad_halo_kernel<T>, dim3(g.splits), dim3(256), 0, s, h);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
@@ -2805,7 +2381,7 @@ const char* intern_name(const std::string& s) {
   return names.insert(s).first->c_str();
 }
 
-const char* type_name(int prec) { return prec == PREC_BF16 ? "bf16" : "float"; }
+const char* type_name(int prec) { return prec == PREC_BF16 ? "bf16" : prec == PREC_F16 ? "_Float16" : "float"; }
 
 }  // namespace
 
@@ -2813,14 +2389,13 @@ const char* gather_kernel_name(int prec, const ConvGather& g, int id);
 
 const char* conv_gather_kernel_name(int prec, const ConvGather& g) {
   if (use_halo(prec, g)) {
-    char buf[64];
-    snprintf(buf, sizeof buf, "conv_halo_kernel<%d, %s>", g.mode, g.stats ? "true" : "false");
+    char buf[80];
+    snprintf(buf, sizeof buf, "conv_halo_kernel<%s, %d, %s>", type_name(prec), g.mode, g.stats ? "true" : "false");
     return intern_name(buf);
   }
-  if (use_halo16(prec, g)) return g.stats ? "conv_halo16_kernel<true>" : "conv_halo16_kernel<false>";
-  if (use_haloW(prec, g)) {
-    char buf[64];
-    snprintf(buf, sizeof buf, "conv_halo_wide_kernel<%d, %s>", g.mode, g.stats ? "true" : "false");
+  if (use_halo16(prec, g)) {
+    char buf[80];
+    snprintf(buf, sizeof buf, "conv_halo16_kernel<%s, %s>", type_name(prec), g.stats ? "true" : "false");
     return intern_name(buf);
   }
   return gather_kernel_name(prec, g, gather_cfg(g));
@@ -2834,7 +2409,7 @@ const char* conv_gather_kernel_name_multi(int prec, const ConvGather* g, int np)
 const char* gather_kernel_name(int prec, const ConvGather& g, int id) {
   if (id < 1 || id > kGatherCfgs) return "conv_gather2_kernel";
   const GatherCfg& c = kGather[id];
-  const int kt = prec == PREC_BF16 ? 64 : 32;
+  const int kt = 128 / prec_bytes(prec);
   char buf[128];
   if (c.kind == 2 && gather_uniform(g, kt))
     snprintf(buf, sizeof buf, "conv_gather_ps_kernel<%s, %d, %d, %d, %d, %d>", type_name(prec), c.bm, c.bn, c.wgm,
@@ -2886,10 +2461,6 @@ int conv_gather_stat_entries(int prec, const ConvGather& g) {
     const int tiles = g.N * ((g.Hm + th - 1) / th), slots = 2 * cu_count();
     return (tiles < slots ? tiles : slots) * HALO16_WAVES;
   }
-  if (use_haloW(prec, g)) {
-    const int th = haloW_rows(prec, g);
-    return g.N * ((g.Hm + th - 1) / th) * 2;
-  }
   const int bm = gather_tile(prec, g) / 1000;
   return bm > 0 ? ceil_div(g.M, bm) : 0;
 }
@@ -2914,16 +2485,16 @@ int conv_wgrad_tile(int prec, int Cout, int Kcols) {
 
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s) {
   if (g.M <= 0) return 0;
-  return prec == PREC_BF16 ? gather_dispatch<bf16_t>(&g, 1, s) : gather_dispatch<float>(&g, 1, s);
+  return with_prec(prec, [&](auto tag) { return gather_dispatch<decltype(tag)>(&g, 1, s); });
 }
 
 int conv_gather_launch_multi(int prec, const ConvGather* g, int np, hipStream_t s) {
   if (np < 1 || np > 4) return -1;
-  return prec == PREC_BF16 ? gather_dispatch<bf16_t>(g, np, s) : gather_dispatch<float>(g, np, s);
+  return with_prec(prec, [&](auto tag) { return gather_dispatch<decltype(tag)>(g, np, s); });
 }
 
 int conv_wgrad_splits(int prec, int Cout, int Kcols, long Mpix, int* pix_per_split) {
-  const int ktp = prec == PREC_BF16 ? 64 : 32;
+  const int ktp = 128 / prec_bytes(prec);
   int bm, bn;
   wgrad_tile(prec, Cout, Kcols, &bm, &bn);
   const long tiles = (long)ceil_div(Cout, bm) * ceil_div(Kcols, bn);
@@ -2953,16 +2524,21 @@ int conv_wgrad_splits_shape(int prec, const ConvWgrad& g, int* pix_per_split) {
 }
 
 const char* conv_wgrad_kernel_name_shape(int prec, const ConvWgrad& g) {
-  if (use_wgrad_halo(prec, g)) return "conv_wgrad_halo_kernel";
+  if (use_wgrad_halo(prec, g)) return prec == PREC_F16 ? "conv_wgrad_halo_kernel<_Float16>" : "conv_wgrad_halo_kernel<bf16>";
   return conv_wgrad_kernel_name(prec, g.Cout, g.KH * g.KW * g.Cin);
 }
 
 int conv_wgrad_launch(int prec, const ConvWgrad& g, hipStream_t s) {
-  if (use_wgrad_halo(prec, g)) return launch_wgrad_halo(g, s);
+  if (use_wgrad_halo(prec, g))
+    return with_prec(prec, [&](auto tag) {
+      using T = decltype(tag);
+      if constexpr (sizeof(T) == 2) return launch_wgrad_halo<T>(g, s);
+      return -1;
+    });
   // the pipelined kernels address both operands with 31-bit byte offsets
-  const long es = prec == PREC_BF16 ? 2 : 4;
+  const long es = prec_bytes(prec);
   if ((long)g.Mpix * g.Cout * es >= (1l << 31) || (long)g.N * g.H * g.W * g.Cin * es >= (1l << 31)) return -1;
-  return prec == PREC_BF16 ? wgrad_dispatch<bf16_t>(g, s) : wgrad_dispatch<float>(g, s);
+  return with_prec(prec, [&](auto tag) { return wgrad_dispatch<decltype(tag)>(g, s); });
 }
 
 int wgrad_reduce_launch(const float* P, int splits, int Cout, int KHW, int Cin, int Cin_real,

@@ -178,13 +178,28 @@ size_t gemm_f32_workspace(int M, int N, int K);
 int gemm_f32_launch(const float* A, long sam, long sak, const float* B, long sbk, long sbn, const float* bias,
                     float* C, int M, int N, int K, float* part, hipStream_t s);
 int colsum_launch(const float* A, int M, int N, float* out, hipStream_t s);
+// Dynamic loss scaling of the fp16 precision (device state of a context).
+struct LossScale {
+  float scale;        // current scale, a power of two in [1, 2^24]
+  float inv_scale;    // 1 / scale
+  unsigned overflow;  // set by the finiteness check of this step's gradient
+  unsigned good;      // steps in a row without an overflow
+  unsigned interval;  // growth interval: the scale doubles after this many
+  unsigned skipped;   // steps skipped because of an overflow
+};
+// ls != NULL: dz is multiplied by ls->scale.
 int softmax_ce_launch(const float* z, const int32_t* labels, int N, int C, float* dz, float* row_loss,
-                      float* loss, unsigned* err, hipStream_t s);
+                      float* loss, unsigned* err, hipStream_t s, const LossScale* ls = nullptr);
 // In-place dropout of n (a multiple of 4) fp32 values with the Philox4x32-10
 // mask of (seed, step) and keep threshold thresh (top 24 bits of a word),
 // kept values multiplied by scale.
 int dropout_launch(float* x, long n, uint64_t seed, uint64_t step, uint32_t thresh, float scale, hipStream_t s);
-int sgd_launch(float* w, const float* g, float* v, long n, float lr, float mom, float wd, hipStream_t s);
+// ls != NULL: g holds scale x gradient; the update is skipped after an
+// overflow, else g is multiplied by 1/scale.
+int sgd_launch(float* w, const float* g, float* v, long n, float lr, float mom, float wd, hipStream_t s,
+               const LossScale* ls = nullptr);
+int grad_check_launch(const float* g, long n, LossScale* ls, hipStream_t s);
+int loss_scale_update_launch(LossScale* ls, hipStream_t s);
 int merge_launch(float* p, const float* ds, const float* dl, long n, float f, hipStream_t s);
 int delta_launch(const float* pulled, const float* local, float* delta, long n, hipStream_t s);
 int fill_zero_launch(void* p, size_t bytes, hipStream_t s);

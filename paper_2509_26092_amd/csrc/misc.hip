@@ -368,7 +368,8 @@ __device__ inline float block_reduce(float v, float* sh, bool is_max) {
 
 __global__ __launch_bounds__(256) void softmax_ce_kernel(const float* __restrict__ z, const int32_t* __restrict__ y,
                                                          int N, int C, float* __restrict__ dz,
-                                                         float* __restrict__ row_loss, unsigned* err) {
+                                                         float* __restrict__ row_loss, unsigned* err,
+                                                         const LossScale* __restrict__ ls) {
   __shared__ float sh[256];
   const int n = blockIdx.x;
   const float* zr = z + (long)n * C;
@@ -382,9 +383,12 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(const float* __restrict
   for (int c = threadIdx.x; c < C; c += 256) s += expf(zr[c] - mx);
   s = block_reduce(s, sh, false);
   const float inv_s = 1.0f / s, inv_n = 1.0f / (float)N;
+  // loss scaling: the backward pass starts from (scale x loss); the scale
+  // is a power of two, so the product is exact
+  const float sc = ls ? ls->scale : 1.0f;
   for (int c = threadIdx.x; c < C; c += 256) {
     const float p = expf(zr[c] - mx) * inv_s;
-    dr[c] = bad ? 0.f : (p - (c == lab ? 1.f : 0.f)) * inv_n;
+    dr[c] = bad ? 0.f : (p - (c == lab ? 1.f : 0.f)) * inv_n * sc;
   }
   if (threadIdx.x == 0) {
     if (bad) {
@@ -415,11 +419,20 @@ __global__ __launch_bounds__(256) void loss_reduce_kernel(const float* __restric
 }
 
 // ------------------------------------------------------------------ flat fp32 streams
+// With loss scaling (ls != NULL) the gradient holds scale x g: the update is
+// skipped when the finiteness check found a non-finite value, else the
+// gradient is multiplied by 1/scale (exact, a power of two) first.
 __global__ void sgd_kernel(float* __restrict__ w, const float* __restrict__ g, float* __restrict__ v, long n,
-                           float lr, float mom, float wd) {
+                           float lr, float mom, float wd, const LossScale* __restrict__ ls) {
+  float inv = 1.0f;
+  if (ls) {
+    if (ls->overflow) return;
+    inv = ls->inv_scale;
+  }
   const long n4 = n >> 2;
   for (long i = blockIdx.x * 256l + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
     float4 ww = ((float4*)w)[i], gg = ((const float4*)g)[i], vv = ((float4*)v)[i];
+    gg.x *= inv; gg.y *= inv; gg.z *= inv; gg.w *= inv;
     vv.x = mom * vv.x + (gg.x + wd * ww.x); ww.x -= lr * vv.x;
     vv.y = mom * vv.y + (gg.y + wd * ww.y); ww.y -= lr * vv.y;
     vv.z = mom * vv.z + (gg.z + wd * ww.z); ww.z -= lr * vv.z;
@@ -428,10 +441,42 @@ __global__ void sgd_kernel(float* __restrict__ w, const float* __restrict__ g, f
     ((float4*)v)[i] = vv;
   }
   for (long i = (n4 << 2) + blockIdx.x * 256l + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
-    const float vv = mom * v[i] + (g[i] + wd * w[i]);
+    const float vv = mom * v[i] + (g[i] * inv + wd * w[i]);
     v[i] = vv;
     w[i] -= lr * vv;
   }
+}
+
+// Finiteness of the scaled gradient: any Inf or NaN sets ls->overflow (a
+// vector atomic from one lane per wave that found one).
+__global__ void grad_check_kernel(const float* __restrict__ g, long n, LossScale* ls) {
+  bool bad = false;
+  const long n4 = n >> 2;
+  for (long i = blockIdx.x * 256l + threadIdx.x; i < n4; i += (long)gridDim.x * 256) {
+    const float4 x = ((const float4*)g)[i];
+    bad |= !(__builtin_isfinite(x.x) && __builtin_isfinite(x.y) && __builtin_isfinite(x.z) && __builtin_isfinite(x.w));
+  }
+  for (long i = (n4 << 2) + blockIdx.x * 256l + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+    bad |= !__builtin_isfinite(g[i]);
+  if (__any(bad) && (threadIdx.x & 63) == __ffsll(__ballot(bad)) - 1) atomicOr(&ls->overflow, 1u);
+}
+
+// Dynamic loss scale after a step: halve it (and count a skipped step)
+// after an overflow, double it after `interval` steps in a row without one.
+__global__ void loss_scale_update_kernel(LossScale* ls) {
+  if (threadIdx.x != 0) return;
+  LossScale x = *ls;
+  if (x.overflow) {
+    x.scale = fmaxf(x.scale * 0.5f, 1.0f);
+    x.good = 0;
+    ++x.skipped;
+  } else if (++x.good >= x.interval) {
+    x.scale = fminf(x.scale * 2.0f, 16777216.0f);
+    x.good = 0;
+  }
+  x.inv_scale = 1.0f / x.scale;
+  x.overflow = 0;
+  *ls = x;
 }
 
 __global__ void merge_kernel(float* __restrict__ p, const float* __restrict__ ds, const float* __restrict__ dl,
@@ -474,25 +519,23 @@ __global__ void fill_zero_kernel(uint32_t* __restrict__ p, long nwords) {
 
 int ingest_launch(int prec, const float* img, void* x, int N, int H, int W, int Cp, unsigned* err, hipStream_t s) {
   const long npix = (long)N * H * W;
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(ingest_kernel<bf16_t>, dim3(grid_for(npix)), dim3(256), 0, s, img, (bf16_t*)x, npix, H * W, Cp,
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(ingest_kernel<T>, dim3(grid_for(npix)), dim3(256), 0, s, img, (T*)x, npix, H * W, Cp,
                        err);
-  else
-    hipLaunchKernelGGL(ingest_kernel<float>, dim3(grid_for(npix)), dim3(256), 0, s, img, (float*)x, npix, H * W, Cp,
-                       err);
-  return ok();
+    return ok();
+  });
 }
 
 int ingest_s2d_launch(int prec, const float* img, void* x, int N, int H, int W, unsigned* err, hipStream_t s) {
   if (H % 2 || W % 2) return -1;
   const long npix = (long)N * (H / 2) * (W / 2);
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(ingest_s2d_kernel<bf16_t>, dim3(grid_for(npix)), dim3(256), 0, s, img, (bf16_t*)x, npix, H, W,
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(ingest_s2d_kernel<T>, dim3(grid_for(npix)), dim3(256), 0, s, img, (T*)x, npix, H, W,
                        err);
-  else
-    hipLaunchKernelGGL(ingest_s2d_kernel<float>, dim3(grid_for(npix)), dim3(256), 0, s, img, (float*)x, npix, H, W,
-                       err);
-  return ok();
+    return ok();
+  });
 }
 
 int round_bf16_launch(const float* x, uint16_t* y, long n, hipStream_t s) {
@@ -505,26 +548,24 @@ int repack_launch(int prec, const float* state, void* wf, void* wd, const Repack
                   hipStream_t s) {
   if (nent > 24) return -1;
   if (total <= 0) return 0;
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(repack_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, s, state, (bf16_t*)wf,
-                       (bf16_t*)wd, tab, nent, total);
-  else
-    hipLaunchKernelGGL(repack_kernel<float>, dim3(grid_for(total)), dim3(256), 0, s, state, (float*)wf, (float*)wd,
-                       tab, nent, total);
-  return ok();
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(repack_kernel<T>, dim3(grid_for(total)), dim3(256), 0, s, state, (T*)wf,
+                       (T*)wd, tab, nent, total);
+    return ok();
+  });
 }
 
 int repack_tiled_launch(int prec, const float* state, void* wf, void* wd, const RepackEntry* tab, int nent,
                         int ntiles, hipStream_t s) {
   if (nent > 24) return -1;
   if (ntiles <= 0) return 0;
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(repack_tiled_kernel<bf16_t>, dim3(ntiles), dim3(256), 0, s, state, (bf16_t*)wf, (bf16_t*)wd,
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(repack_tiled_kernel<T>, dim3(ntiles), dim3(256), 0, s, state, (T*)wf, (T*)wd,
                        tab, nent);
-  else
-    hipLaunchKernelGGL(repack_tiled_kernel<float>, dim3(ntiles), dim3(256), 0, s, state, (float*)wf, (float*)wd, tab,
-                       nent);
-  return ok();
+    return ok();
+  });
 }
 
 bool repack_tiled_fits(int khw) { return khw <= kRepackMaxKHW; }
@@ -534,52 +575,49 @@ int repack_tiles(int cout, int cin_p) {
 
 int maxpool_fwd_launch(int prec, const void* x, void* y, uint8_t* arg, int N, int H, int W, int C, int Ho, int Wo,
                        hipStream_t s) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const int vw = prec_vw(prec);
   const long work = (long)N * Ho * Wo * (C / vw);
   if ((long)N * H * W * C >= (1l << 31)) return -1;  // 32-bit chunk indices
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(maxpool_fwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, (const bf16_t*)x,
-                       (bf16_t*)y, arg, N, H, W, C, Ho, Wo);
-  else
-    hipLaunchKernelGGL(maxpool_fwd_kernel<float>, dim3(grid_for(work)), dim3(256), 0, s, (const float*)x, (float*)y,
-                       arg, N, H, W, C, Ho, Wo);
-  return ok();
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(maxpool_fwd_kernel<T>, dim3(grid_for(work)), dim3(256), 0, s, (const T*)x,
+                       (T*)y, arg, N, H, W, C, Ho, Wo);
+    return ok();
+  });
 }
 
 int maxpool_bwd_launch(int prec, const void* dy, const uint8_t* arg, void* dx, int N, int H, int W, int C, int Ho,
                        int Wo, hipStream_t s) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const int vw = prec_vw(prec);
   const long work = (long)N * ((H + 1) / 2) * ((W + 1) / 2) * (C / vw);
   if ((long)N * H * W * C >= (1l << 31)) return -1;  // 32-bit chunk indices
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(maxpool_bwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, (const bf16_t*)dy, arg,
-                       (bf16_t*)dx, N, H, W, C, Ho, Wo);
-  else
-    hipLaunchKernelGGL(maxpool_bwd_kernel<float>, dim3(grid_for(work)), dim3(256), 0, s, (const float*)dy, arg,
-                       (float*)dx, N, H, W, C, Ho, Wo);
-  return ok();
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(maxpool_bwd_kernel<T>, dim3(grid_for(work)), dim3(256), 0, s, (const T*)dy, arg,
+                       (T*)dx, N, H, W, C, Ho, Wo);
+    return ok();
+  });
 }
 
 int avgpool_fwd_launch(int prec, const void* x, float* f, int N, int HW, int C, hipStream_t s) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const int vw = prec_vw(prec);
   const long work = (long)N * (C / vw);
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(avgpool_fwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, (const bf16_t*)x, f, N, HW,
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(avgpool_fwd_kernel<T>, dim3(grid_for(work)), dim3(256), 0, s, (const T*)x, f, N, HW,
                        C);
-  else
-    hipLaunchKernelGGL(avgpool_fwd_kernel<float>, dim3(grid_for(work)), dim3(256), 0, s, (const float*)x, f, N, HW,
-                       C);
-  return ok();
+    return ok();
+  });
 }
 
 int avgpool_bwd_launch(int prec, const float* df, void* dx, int N, int HW, int C, hipStream_t s) {
-  const int vw = prec == PREC_BF16 ? 8 : 4;
+  const int vw = prec_vw(prec);
   const long work = (long)N * HW * (C / vw);
-  if (prec == PREC_BF16)
-    hipLaunchKernelGGL(avgpool_bwd_kernel<bf16_t>, dim3(grid_for(work)), dim3(256), 0, s, df, (bf16_t*)dx, N, HW, C);
-  else
-    hipLaunchKernelGGL(avgpool_bwd_kernel<float>, dim3(grid_for(work)), dim3(256), 0, s, df, (float*)dx, N, HW, C);
-  return ok();
+  return with_prec(prec, [&](auto tag) {
+    using T = decltype(tag);
+    hipLaunchKernelGGL(avgpool_bwd_kernel<T>, dim3(grid_for(work)), dim3(256), 0, s, df, (T*)dx, N, HW, C);
+    return ok();
+  });
 }
 
 int gemm_f32_splits(int M, int N, int K) {
@@ -616,8 +654,8 @@ int colsum_launch(const float* A, int M, int N, float* out, hipStream_t s) {
 }
 
 int softmax_ce_launch(const float* z, const int32_t* labels, int N, int C, float* dz, float* row_loss, float* loss,
-                      unsigned* err, hipStream_t s) {
-  hipLaunchKernelGGL(softmax_ce_kernel, dim3(N), dim3(256), 0, s, z, labels, N, C, dz, row_loss, err);
+                      unsigned* err, hipStream_t s, const LossScale* ls) {
+  hipLaunchKernelGGL(softmax_ce_kernel, dim3(N), dim3(256), 0, s, z, labels, N, C, dz, row_loss, err, ls);
   hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, row_loss, N, loss, err);
   return ok();
 }
@@ -633,8 +671,21 @@ int dropout_launch(float* x, long n, uint64_t seed, uint64_t step, uint32_t thre
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
-int sgd_launch(float* w, const float* g, float* v, long n, float lr, float mom, float wd, hipStream_t s) {
-  hipLaunchKernelGGL(sgd_kernel, dim3(grid_for((n + 3) / 4, 256, 8192)), dim3(256), 0, s, w, g, v, n, lr, mom, wd);
+int sgd_launch(float* w, const float* g, float* v, long n, float lr, float mom, float wd, hipStream_t s,
+               const LossScale* ls) {
+  hipLaunchKernelGGL(sgd_kernel, dim3(grid_for((n + 3) / 4, 256, 8192)), dim3(256), 0, s, w, g, v, n, lr, mom, wd,
+                     ls);
+  return ok();
+}
+
+int grad_check_launch(const float* g, long n, LossScale* ls, hipStream_t s) {
+  if ((uintptr_t)g & 15) return -1;
+  hipLaunchKernelGGL(grad_check_kernel, dim3(grid_for((n + 3) / 4, 256, 4096)), dim3(256), 0, s, g, n, ls);
+  return ok();
+}
+
+int loss_scale_update_launch(LossScale* ls, hipStream_t s) {
+  hipLaunchKernelGGL(loss_scale_update_kernel, dim3(1), dim3(64), 0, s, ls);
   return ok();
 }
 

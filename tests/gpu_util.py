@@ -7,13 +7,15 @@ from oracle import net, ops
 from paper_2509_26092_amd import binding as B
 from paper_2509_26092_amd import inputs
 
-PREC = {"fp32": B.RN18_FP32, "bf16": B.RN18_BF16}
-TOL = {"fp32": 1e-3, "bf16": 2e-2}
+PREC = {"fp32": B.RN18_FP32, "bf16": B.RN18_BF16, "fp16": B.RN18_FP16}
+# fp32 and the 16-bit mixed precisions (bf16, fp16 with loss scaling)
+TOL = {"fp32": 1e-3, "bf16": 2e-2, "fp16": 2e-2}
+HALF = ("bf16", "fp16")
 
 
 def torch_dtype(prec):
     import torch
-    return torch.float32 if prec == "fp32" else torch.bfloat16
+    return {"fp32": torch.float32, "bf16": torch.bfloat16, "fp16": torch.float16}[prec]
 
 
 def to_dev_nhwc(x_nchw, prec, cpad=None):
@@ -32,7 +34,11 @@ def from_dev_nhwc(t):
 
 def rounded(x, prec):
     """What the device holds for an fp32 input in the given precision, as f64."""
-    return ops.round_bf16(x) if prec == "bf16" else np.asarray(x, np.float32).astype(np.float64)
+    if prec == "bf16":
+        return ops.round_bf16(x)
+    if prec == "fp16":
+        return ops.round_fp16(x)
+    return np.asarray(x, np.float32).astype(np.float64)
 
 
 def rel_errors(gpu, ref):
@@ -181,15 +187,30 @@ def _bf16_other_neighbor(exact, b):
     return un.astype(np.uint32).view(np.float32).astype(np.float64)
 
 
+def _fp16_other_neighbor(exact, b):
+    """The fp16 value on the other side of `exact` from its rounding b
+    (b finite; the neighbour of the largest finite value is infinite)."""
+    with np.errstate(over="ignore"):
+        b16 = np.asarray(b, np.float64).astype(np.float16)
+    u = b16.view(np.uint16).astype(np.int64)
+    neg = (u >> 15) & 1
+    up = exact > b
+    inc_mag = np.where(up, neg == 0, neg == 1)
+    un = np.where(inc_mag, u + 1, u - 1)
+    un = np.where(b16 == 0, np.where(up, 0x0001, 0x8001), un)
+    return un.astype(np.uint16).view(np.float16).astype(np.float64)
+
+
 class Mirror(Decider):
-    """Decider for bf16 steps that also mirrors the kernel's bf16 rounding
-    decisions where they are not unique: a value whose exact (fp64) result
-    lies within TAU_ROUND ulp (or TAU_ABS * rms) of a rounding midpoint may
-    round either way in a kernel that computes it in fp32; there the
-    kernel's stored value is taken, after checking it is one of the two
-    bf16 neighbours. Everywhere else the kernel's stored value must equal
-    the oracle's round-to-nearest-even result exactly. Backward tensors are
-    captured from the kernel as they are produced."""
+    """Decider for 16-bit (bf16, fp16) steps that also mirrors the kernel's
+    rounding decisions where they are not unique: a value whose exact (fp64)
+    result lies within TAU_ROUND ulp (or TAU_ABS * rms) of a rounding
+    midpoint may round either way in a kernel that computes it in fp32;
+    there the kernel's stored value is taken, after checking it is one of
+    the two neighbours in the 16-bit type. Everywhere else the kernel's
+    stored value must equal the oracle's round-to-nearest-even result
+    exactly. Backward tensors are captured from the kernel as they are
+    produced (scaled by the loss scale in fp16 steps, on both sides)."""
     TAU_ROUND = 0.02
     TAU_ABS = 1e-5
 
@@ -240,7 +261,7 @@ class Mirror(Decider):
             return super().__call__(kind, site, pre, default)
         exact, b = pre, default
         g = self._gpu_value(site)
-        nb = _bf16_other_neighbor(exact, b)
+        nb = (_fp16_other_neighbor if self.prec == "fp16" else _bf16_other_neighbor)(exact, b)
         ulp = np.abs(nb - b)
         rms = np.sqrt(np.mean(exact * exact))
         band = np.abs(exact - 0.5 * (b + nb)) <= self.TAU_ROUND * ulp + self.TAU_ABS * rms

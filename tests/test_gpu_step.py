@@ -19,20 +19,21 @@ import pytest
 from oracle import net
 from paper_2509_26092_amd import binding as B
 from paper_2509_26092_amd import inputs
-from gpu_util import TAU, TOL, Decider, Mirror, compare_step, gpu_train_step, make_state
+from gpu_util import HALF, TAU, TOL, Decider, Mirror, compare_step, gpu_train_step, make_state
 
 pytestmark = pytest.mark.gpu
 
 LR = 0.1
 
 
-def _run_parity(arch, classes, prec, N, H, seed, lr=LR, dropout=None, chunk=0):
+def _run_parity(arch, classes, prec, N, H, seed, lr=LR, dropout=None, chunk=0, loss_scale=1024.0):
     """One step on both sides. The oracle takes the kernel's choice only at
     non-unique points inside the rounding band (ReLU kinks, pool ties and,
     for bf16, rounding midpoints of the stored tensors; see gpu_util), and
     every kernel decision outside the band must agree with the oracle's.
     dropout: (rate, seed, step) of the classifier-input dropout on both.
-    chunk: launch every convolution over batch chunks of this many images."""
+    chunk: launch every convolution over batch chunks of this many images.
+    loss_scale: the loss scale of fp16 steps (a power of two), on both sides."""
     L, st = make_state(arch, classes, seed)
     x = inputs.images(seed, N, H, H)
     y = inputs.labels(seed, N, classes)
@@ -43,11 +44,14 @@ def _run_parity(arch, classes, prec, N, H, seed, lr=LR, dropout=None, chunk=0):
     if dropout is not None:
         B.rn18_set_dropout(w.ctx, *dropout)
         drop = dict(dropout=dropout[0], dropout_seed=dropout[1], dropout_step=dropout[2])
-    bf = prec == "bf16"
+    bf = prec in HALF
+    if prec == "fp16":
+        B.rn18_set_loss_scale(w.ctx, loss_scale, 1 << 30)
+        drop.update(fp16=True, loss_scale=loss_scale)
     dec = Mirror(w, L, N, H, prec, TAU) if bf else Decider(w, N, H, prec, TAU)
     gs, gv, losses, status = gpu_train_step(arch, classes, prec, st, x, y, lr, worker=w)
     assert status == B.RN18_OK
-    cfg = net.Config(arch, classes, bf16=bf, round_acts=bf, **drop)
+    cfg = net.Config(arch, classes, bf16=(prec == "bf16"), round_acts=bf, **drop)
     t0 = time.time()
     try:
         report, loss = compare_step(L, cfg, st, x, y, lr, gs, gv, losses[0], TOL[prec], decide=dec)
@@ -55,7 +59,7 @@ def _run_parity(arch, classes, prec, N, H, seed, lr=LR, dropout=None, chunk=0):
         print("oracle step and comparison %.1f s, host peak RSS %.1f GB" %
               (time.time() - t0, resource.getrusage(resource.RUSAGE_SELF).ru_maxrss / 2 ** 20), flush=True)
         if bf:
-            print("bf16 rounding band %d, kernel choices taken %d, invalid %d, outside %d %s" %
+            print("16-bit rounding band %d, kernel choices taken %d, invalid %d, outside %d %s" %
                   (dec.round_band, dec.round_taken, dec.round_invalid, dec.round_outside, dec.round_log[:4]))
         print("relu/pool band %d, taken %d, invalid %d, outside %d" % (dec.ambiguous, dec.taken, dec.invalid,
                                                                        dec.outside))
