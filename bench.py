@@ -590,7 +590,13 @@ def main():
         "cpu_baseline": cpu,
         "per_shape": per_shape,
     }
-    print(json.dumps(out))
+    print(json.dumps(out), flush=True)
+    try:
+        import psutil
+        kids = psutil.Process().children(recursive=True)
+        progress("child processes at exit: %d %s" % (len(kids), [k.name() for k in kids]))
+    except Exception as e:  # psutil is optional here
+        progress("child processes at exit: unknown (%s)" % e)
 
 
 if __name__ == "__main__":
