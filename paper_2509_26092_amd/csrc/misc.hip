@@ -139,17 +139,30 @@ __global__ __launch_bounds__(256) void repack_tiled_kernel(const float* __restri
     }
   }
   __syncthreads();
+  // Both layouts are written in 16-byte runs (VS consecutive channels per
+  // thread): channel counts are multiples of the vector width and every
+  // layout offset is a multiple of its run length.
+  constexpr int VS = TT<T>::VW;
   // forward layout [Cout][KHW][Cin_p]: consecutive input channels
-  for (int idx = threadIdx.x; idx < nco * KHW * nci; idx += 256) {
-    const int ci = idx % nci, rest = idx / nci, tap = rest % KHW, co = rest / KHW;
-    wf[r.dst_f + ((long)(co0 + co) * KHW + tap) * Cin_p + ci0 + ci] = TT<T>::from_f(s[co * RS + ci * KHW + tap]);
+  const int nciv = nci / VS;
+  for (int idx = threadIdx.x; idx < nco * KHW * nciv; idx += 256) {
+    const int cv = idx % nciv, rest = idx / nciv, tap = rest % KHW, co = rest / KHW;
+    float v[VS];
+#pragma unroll
+    for (int e = 0; e < VS; ++e) v[e] = s[co * RS + (cv * VS + e) * KHW + tap];
+    *(uint4*)(wf + r.dst_f + ((long)(co0 + co) * KHW + tap) * Cin_p + ci0 + cv * VS) = pack<T>(v);
   }
   // data-gradient layout [Cin_p][KHW][Cout]: consecutive output channels
-  if (r.dst_d >= 0)
-    for (int idx = threadIdx.x; idx < nci * KHW * nco; idx += 256) {
-      const int co = idx % nco, rest = idx / nco, tap = rest % KHW, ci = rest / KHW;
-      wd[r.dst_d + ((long)(ci0 + ci) * KHW + tap) * Cout + co0 + co] = TT<T>::from_f(s[co * RS + ci * KHW + tap]);
+  if (r.dst_d >= 0) {
+    const int ncov = nco / VS;
+    for (int idx = threadIdx.x; idx < nci * KHW * ncov; idx += 256) {
+      const int cv = idx % ncov, rest = idx / ncov, tap = rest % KHW, ci = rest / KHW;
+      float v[VS];
+#pragma unroll
+      for (int e = 0; e < VS; ++e) v[e] = s[(cv * VS + e) * RS + ci * KHW + tap];
+      *(uint4*)(wd + r.dst_d + ((long)(ci0 + ci) * KHW + tap) * Cout + co0 + cv * VS) = pack<T>(v);
     }
+  }
 }
 
 // ------------------------------------------------------------------ dropout
