@@ -97,9 +97,11 @@ __device__ inline void mma_stage(floatx4_t (&acc)[FM][FN], const uint4* As, cons
 // memory straight into an LDS ring of STAGES buffers (gfx950
 // global_load_lds_dwordx4, one 16-byte chunk per lane, written lane-contiguous
 // at the instruction's LDS base), so STAGES-1 stages are in flight while one
-// is multiplied. Rows are 128 bytes without padding; the chunk of row r that
-// goes to slot q is q ^ (r & 7), which spreads the 16 rows of an MFMA operand
-// read over all LDS banks. Taps outside the image and K beyond the end load
+// is multiplied. Rows are 128 bytes without padding; the chunk q of row r
+// goes to slot q ^ ((r / 2) & 7). Consecutive rows sit in alternate halves of
+// the 64 banks, so this puts the 16 rows of an MFMA operand read on 16
+// distinct 16-byte bank groups (q ^ (r & 7) would pair rows r and r + 8 on
+// one group). Taps outside the image and K beyond the end load
 // from a zero page. When Cin is a multiple of the stage width, a stage is one
 // tap and a contiguous block of channels, and the tap arithmetic is uniform.
 // ---------------------------------------------------------------------------
@@ -188,7 +190,9 @@ __device__ inline void gather_impl(const ConvGather& g) {
   const T* __restrict__ A = (const T*)g.A;
   const T* __restrict__ B = (const T*)g.B;
   const int HWm = g.Hm * g.Wm;
-  const int c = (lane & 7) ^ (lane >> 3);          // chunk this lane loads (slot lane&7, row lane>>3)
+  // chunk this lane loads into slot lane & 7 of row 8 j + lane / 8 (j = wave
+  // + NW u, of the wave's parity as NW and the A rows per stage are even)
+  const int c = (lane & 7) ^ (((wave & 1) << 2) | (lane >> 4));
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const uint32_t smem_lds = lds_addr(smem);
   const void* const zero = g.zero;
@@ -314,7 +318,7 @@ __device__ inline void gather_impl(const ConvGather& g) {
 
   const int S = (g.K + KT - 1) / KT;
   const int arow0 = wm * WTM, brow0 = wn * WTN;
-  const int sw = lane & 7;
+  const int sw = (lane >> 1) & 7;                 // (row / 2) % 8 of the operand rows
   if constexpr (RP) {
     // Register-prefetched loop: the operand fragments of stage s+1 are read
     // from LDS while the MFMAs of stage s run from registers, and a ring
@@ -577,14 +581,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave_u / WGN, wn = wave_u % WGN;
-  const int c = (lane & 7) ^ (lane >> 3);
+  const int c = (lane & 7) ^ (((wave_u & 1) << 2) | (lane >> 4));   // see gather_impl
   const uint32_t smem_lds = lds_addr(smem);
   const int G = gridDim.x;
   const int slot = xcd_remap(blockIdx.x, G);
   const int total = gs.tile_begin[gs.np];
   const int es = (int)sizeof(T);
   const int arow0 = wm * WTM, brow0 = wn * WTN;
-  const int sw = lane & 7;
+  const int sw = (lane >> 1) & 7;                 // (row / 2) % 8 of the operand rows
 
   // ---- issue side: the tile whose stages are being loaded
   constexpr int UB = IPW - UA;
