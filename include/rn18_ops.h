@@ -105,7 +105,14 @@ enum {
   /* per context: value != 0 keeps every launch of a training step on the
    * caller's stream (the weight gradients otherwise run on a second stream
    * beside the data-gradient chain). For timing kernels one at a time. */
-  RN18_DBG_SERIAL = 4
+  RN18_DBG_SERIAL = 4,
+  /* process-wide: split count of the K reduction of every forward and
+   * stride-1 data-gradient gather launch of a training step or eval pass
+   * (at most the launch's K stages, at most 64; 0 = automatic: only
+   * launches with fewer output tiles than the chip has compute units
+   * split; 1 = never). Plans built afterwards size their split-K scratch
+   * for it. ctx may be NULL. For tuning and for testing the split path. */
+  RN18_DBG_GATHER_SPLIT = 5
 };
 enum {
   RN18_DBG_Y = 0, RN18_DBG_Z1 = 1, RN18_DBG_OUT = 2, RN18_DBG_GA = 3, RN18_DBG_GB = 4, RN18_DBG_GZ = 5,

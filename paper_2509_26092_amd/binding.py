@@ -262,6 +262,7 @@ DBG = dict(y=0, z1=1, out=2, gA=3, gB=4, gz=5, gy=6, gyd=7, grad=8, wf=9, wd=10,
 
 
 RN18_DBG_STOP_BLOCKS, RN18_DBG_GATHER_CONFIG, RN18_DBG_WGRAD_CONFIG, RN18_DBG_CONV_CHUNK, RN18_DBG_SERIAL = 0, 1, 2, 3, 4
+RN18_DBG_GATHER_SPLIT = 5
 
 
 def rn18_debug_set(ctx, key, value):

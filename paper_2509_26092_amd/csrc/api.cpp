@@ -171,6 +171,8 @@ struct ConvP {
 // mbits: ReLU mask bytes of the block output (one byte per 16-byte chunk)
 struct BlockP { size_t in, z1, out, mbits; };
 
+constexpr size_t kSplitScratchBytes = (size_t)64 << 20;
+
 struct Plan {
   int N, H, W;
   std::vector<ConvP> cp;
@@ -183,6 +185,7 @@ struct Plan {
   size_t part, wpart, grad;
   size_t bnst;                  // forward conv epilogue BN partials (one entry per 32 rows at most)
   size_t bnst2, part2;          // the same scratch for the projection convs, which run on the side stream
+  size_t gsplit, gsplit_bytes;  // split-K partials of the forward and data-gradient convs (caller's stream)
   size_t total;
 };
 
@@ -263,6 +266,42 @@ int run_captures(Ctx* c, int kind, int index, const void* src, size_t avail) {
     HIPCHK(hipMemcpyAsync(cp.dst, src, cp.bytes, hipMemcpyDeviceToDevice, c->stream));
   }
   return RN18_OK;
+}
+
+ConvGather gather_fwd(const void* x, const void* w, void* y, int N, int Hin, int Win, int Cin, int Ho, int Wo,
+                      int Cout, int k, int s, int p) {
+  ConvGather g{};
+  g.A = x; g.B = w; g.C = y;
+  g.N = N; g.Hin = Hin; g.Win = Win; g.Cin = Cin;
+  g.Hm = Ho; g.Wm = Wo; g.M = N * Ho * Wo;
+  g.Hout = Ho; g.Wout = Wo; g.Cols = Cout;
+  g.os = 1; g.oph = 0; g.opw = 0;
+  g.is = s; g.ip = p;
+  g.nth = k; g.ntw = k;
+  g.dh0 = 0; g.dhs = 1; g.dw0 = 0; g.dws = 1;
+  g.wkh0 = 0; g.wkhs = 1; g.wkw0 = 0; g.wkws = 1; g.KW = k; g.KHW = k * k;
+  g.K = k * k * Cin;
+  g.mode = 0;
+  return g;
+}
+
+// Data gradient of a stride-1 conv (input [N][H][W][Cin], output
+// [N][Ho][Wo][Cout]) as a forward conv of dY with the taps mirrored.
+ConvGather gather_dgrad1(const void* dy, const void* wd, void* dx, int N, int H, int W, int Cin, int Ho, int Wo,
+                         int Cout, int k, int p, int mode, const void* R, const void* Rm) {
+  ConvGather g{};
+  g.A = dy; g.B = wd; g.C = dx; g.R = R; g.Rm = Rm;
+  g.N = N; g.Hin = Ho; g.Win = Wo; g.Cin = Cout;
+  g.Hm = H; g.Wm = W; g.M = N * H * W;
+  g.Hout = H; g.Wout = W; g.Cols = Cin;
+  g.os = 1; g.oph = 0; g.opw = 0;
+  g.is = 1; g.ip = k - 1 - p;
+  g.nth = k; g.ntw = k;
+  g.dh0 = 0; g.dhs = 1; g.dw0 = 0; g.dws = 1;
+  g.wkh0 = k - 1; g.wkhs = -1; g.wkw0 = k - 1; g.wkws = -1; g.KW = k; g.KHW = k * k;
+  g.K = k * k * Cout;
+  g.mode = mode;
+  return g;
 }
 
 int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
@@ -430,6 +469,16 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     pl->bnst2 = alloc(mb);
     pl->part2 = alloc(mp);
   }
+  // (kernels address the split-K scratch with 64-bit offsets: not a tensor
+  // under the per-tensor limit)
+  // Split-K scratch of one fixed size at every shape, so that the workspace
+  // stays linear in the batch (the memory model of Sec. 5.3). It holds the
+  // largest automatic split (3 ranges of 284 fp32 tiles of 128x128, 56 MB);
+  // the launcher cuts a larger forced split to fit. Kernels address it with
+  // 64-bit offsets: it is not a tensor under the per-tensor limit.
+  pl->gsplit_bytes = kSplitScratchBytes;
+  pl->gsplit = off;
+  off += align256(kSplitScratchBytes);
   // the weight-gradient split-K scratch also holds the classifier's split-K
   // partials (the classifier runs before any weight gradient)
   for (size_t hw : {gemm_f32_workspace(N, C, a.feat), gemm_f32_workspace(C, a.feat, N),
@@ -450,22 +499,6 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
 // ----------------------------------------------------------------------------
 // Conv launch helpers
 // ----------------------------------------------------------------------------
-ConvGather gather_fwd(const void* x, const void* w, void* y, int N, int Hin, int Win, int Cin, int Ho, int Wo,
-                      int Cout, int k, int s, int p) {
-  ConvGather g{};
-  g.A = x; g.B = w; g.C = y;
-  g.N = N; g.Hin = Hin; g.Win = Win; g.Cin = Cin;
-  g.Hm = Ho; g.Wm = Wo; g.M = N * Ho * Wo;
-  g.Hout = Ho; g.Wout = Wo; g.Cols = Cout;
-  g.os = 1; g.oph = 0; g.opw = 0;
-  g.is = s; g.ip = p;
-  g.nth = k; g.ntw = k;
-  g.dh0 = 0; g.dhs = 1; g.dw0 = 0; g.dws = 1;
-  g.wkh0 = 0; g.wkhs = 1; g.wkw0 = 0; g.wkws = 1; g.KW = k; g.KHW = k * k;
-  g.K = k * k * Cin;
-  g.mode = 0;
-  return g;
-}
 
 // Data gradient of a conv with input [N][H][W][Cin] and output [N][Ho][Wo][Cout].
 // mode: 0 store, 1 accumulate, 2 add masked residual (R, Rm).
@@ -476,22 +509,12 @@ ConvGather gather_fwd(const void* x, const void* w, void* y, int N, int Hin, int
 int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int H, int W, int Cin, int Ho, int Wo,
                  int Cout, int k, int s, int p, int mode, const void* R, const void* Rm, hipStream_t st,
                  Ctx* c = nullptr, int layer = -1, int cin_real = 0, const void* dy2 = nullptr,
-                 const void* wd2 = nullptr) {
+                 const void* wd2 = nullptr, void* sws = nullptr, size_t sws_bytes = 0) {
   const double creal = cin_real > 0 ? cin_real : Cin;
   if (dy2 && (s != 2 || !wd2)) return -1;
   if (s == 1) {
-    ConvGather g{};
-    g.A = dy; g.B = wd; g.C = dx; g.R = R; g.Rm = Rm;
-    g.N = N; g.Hin = Ho; g.Win = Wo; g.Cin = Cout;
-    g.Hm = H; g.Wm = W; g.M = N * H * W;
-    g.Hout = H; g.Wout = W; g.Cols = Cin;
-    g.os = 1; g.oph = 0; g.opw = 0;
-    g.is = 1; g.ip = k - 1 - p;
-    g.nth = k; g.ntw = k;
-    g.dh0 = 0; g.dhs = 1; g.dw0 = 0; g.dws = 1;
-    g.wkh0 = k - 1; g.wkhs = -1; g.wkw0 = k - 1; g.wkws = -1; g.KW = k; g.KHW = k * k;
-    g.K = k * k * Cout;
-    g.mode = mode;
+    ConvGather g = gather_dgrad1(dy, wd, dx, N, H, W, Cin, Ho, Wo, Cout, k, p, mode, R, Rm);
+    g.ws = sws; g.ws_bytes = sws_bytes;
     const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(prec, g), conv_gather_kernel_name(prec, g), 2.0 * g.M * creal * g.K, 0.0);
     const int r = conv_gather_launch(prec, g, st);
     prof_end(c, pi);
@@ -521,6 +544,7 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
       g.wkh0 = kh0; g.wkhs = 2; g.wkw0 = kw0; g.wkws = 2; g.KW = k; g.KHW = k * k;
       g.K = nth * ntw * Cout;
       g.mode = mode;
+      g.ws = sws; g.ws_bytes = sws_bytes;
       if (dy2 && ph == 0 && pw == 0) {
         // output pixel (2i, 2j) of the projection's data gradient is dy2[i][j] x wd2
         g.A2 = dy2; g.B2 = wd2; g.K2 = Cout;
@@ -658,7 +682,7 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
 
   // conv + BN statistics of layer li on stream cs with the BN scratch at
   // bnst_off / part_off
-  auto conv_bn_on = [&](int li, hipStream_t cs, size_t bnst_off, size_t part_off) -> int {
+  auto conv_bn_on = [&](int li, hipStream_t cs, size_t bnst_off, size_t part_off, bool split) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     // training: the conv epilogue also writes per-tile BN partials of its
@@ -671,6 +695,7 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
       ConvGather g = gather_fwd(ws + P.x + n0 * in_img, W(li), ws + P.y + n0 * out_img, nc, P.Hin, P.Win, P.cin,
                                 P.Ho, P.Wo, L.cout, P.k, P.s, P.p);
       if (train) g.stats = tstats + ntiles * L.cout * 4;
+      if (split) { g.ws = ws + pl.gsplit; g.ws_bytes = pl.gsplit_bytes; }
       const double mc = (double)nc * P.Ho * P.Wo;
       TIMED(RN18_K_CONV_FWD, li, conv_gather_tile(prec, g), conv_gather_kernel_name(prec, g),
             2.0 * mc * L.cout * L.k * L.k * L.cin,
@@ -691,7 +716,7 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     }
     return 0;
   };
-  auto conv_bn = [&](int li) -> int { return conv_bn_on(li, st, pl.bnst, pl.part); };
+  auto conv_bn = [&](int li) -> int { return conv_bn_on(li, st, pl.bnst, pl.part, true); };
   // the projection conv of a downsampling block reads only the block input:
   // with the side stream it runs there beside the block's first two convs
   const bool ovf = c->side && !c->dbg_serial && !c->prof_on && c->captures.empty();
@@ -730,7 +755,7 @@ int run_forward(Ctx* c, const Plan& pl, const float* state_c, float* state_rs, c
     if (side_ds) {
       HIPCHK(hipEventRecord(c->ev_fork, st));
       HIPCHK(hipStreamWaitEvent(c->side, c->ev_fork, 0));
-      if ((r = conv_bn_on(B.ds, c->side, pl.bnst2, pl.part2))) return r;
+      if ((r = conv_bn_on(B.ds, c->side, pl.bnst2, pl.part2, false))) return r;
       HIPCHK(hipEventRecord(c->ev_ds, c->side));
     }
     if ((r = conv_bn(B.c1))) return r;
@@ -900,7 +925,8 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
       LCHK(launch_dgrad(prec, ws + dy + n0 * out_img, W_d(li), ws + dx + n0 * in_img, nc, P.Hin, P.Win, L.cin_p,
                         P.Ho, P.Wo, L.cout, L.k, L.s, L.p, mode, mode == 2 ? ws + R + n0 * in_img : nullptr,
                         mode == 2 ? ws + Rm + n0 * in_img / 16 : nullptr, st, c, li, L.cin,
-                        lds >= 0 ? ws + dys + n0 * out_img : nullptr, lds >= 0 ? W_d(lds) : nullptr));
+                        lds >= 0 ? ws + dys + n0 * out_img : nullptr, lds >= 0 ? W_d(lds) : nullptr,
+                        ws + pl.gsplit, pl.gsplit_bytes));
     }
     return 0;
   };
@@ -1322,6 +1348,10 @@ int rn18_debug_set(rn18_ctx* h, int key, long value) {
   }
   if (key == RN18_DBG_WGRAD_CONFIG) {
     if (conv_wgrad_override((int)value)) return fail(RN18_EINVAL, "unknown wgrad configuration %ld", value);
+    return RN18_OK;
+  }
+  if (key == RN18_DBG_GATHER_SPLIT) {
+    if (conv_gather_split_override((int)value)) return fail(RN18_EINVAL, "bad split count %ld", value);
     return RN18_OK;
   }
   if (!h) return fail(RN18_EINVAL, "ctx is NULL");

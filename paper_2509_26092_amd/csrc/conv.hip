@@ -185,8 +185,16 @@ __device__ inline void gather_impl(const ConvGather& g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
   const int tiles_n = (g.Cols + BN - 1) / BN;
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  // split-K: logical block = range * tiles + tile, so the tiles of one K
+  // range sit together on an XCD (they share operand rows of that range)
+  const int ksplit = g.ksplit > 1 ? g.ksplit : 1;
+  const int tiles = ((g.M + BM - 1) / BM) * tiles_n;
+  const int tk = xcd_remap(blockIdx.x, gridDim.x);
+  const int ks = ksplit > 1 ? tk / tiles : 0;
+  const int t = tk - ks * tiles;
   const int m0 = (t / tiles_n) * BM, n0 = (t % tiles_n) * BN;
+  const int S_all = (g.K + KT - 1) / KT;
+  const int s_lo = ks * S_all / ksplit;            // this block's stages [s_lo, s_lo + S)
   const T* __restrict__ A = (const T*)g.A;
   const T* __restrict__ B = (const T*)g.B;
   const int HWm = g.Hm * g.Wm;
@@ -240,6 +248,12 @@ __device__ inline void gather_impl(const ConvGather& g) {
   i32x4_t rsA, rsB;
   int st_ti = 0, st_th = 0, st_tw = 0, st_cb = 0;  // tap (th, tw group), channel block of the next stage issued
   if (UNI) {
+    // stage s is channel block s / (nth ntw_g), tap s % (nth ntw_g) (w group fastest)
+    const int per_cb = g.nth * ntw_g;
+    st_cb = s_lo / per_cb;
+    st_ti = s_lo - st_cb * per_cb;
+    st_th = st_ti / ntw_g;
+    st_tw = st_ti - st_th * ntw_g;
     rsA = buffer_rsrc(A, (uint32_t)((long)g.N * g.Hin * g.Win * g.Cin * es));
     rsB = buffer_rsrc(B, (uint32_t)((long)g.Cols * g.KHW * g.Cin * es));
     const int lane_px = (c * VW) / g.Cin;              // pixel of this lane's chunk within a row
@@ -286,7 +300,7 @@ __device__ inline void gather_impl(const ConvGather& g) {
   // General path (channel chunks of different taps in one row): per-lane tap
   // arithmetic and 64-bit addresses, padding read from the zero page.
   auto issue = [&](int s, int buf) {
-    const int k = s * KT + c * VW;
+    const int k = (s_lo + s) * KT + c * VW;
     const bool kok = k < g.K;
     const int tap = kok ? k / g.Cin : 0;
     const int ci = k - tap * g.Cin;
@@ -316,7 +330,7 @@ __device__ inline void gather_impl(const ConvGather& g) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int S = (g.K + KT - 1) / KT;
+  const int S = (ks + 1) * S_all / ksplit - s_lo;
   const int arow0 = wm * WTM, brow0 = wn * WTN;
   const int sw = (lane >> 1) & 7;                 // (row / 2) % 8 of the operand rows
   if constexpr (RP) {
@@ -429,6 +443,27 @@ __device__ inline void gather_impl(const ConvGather& g) {
   // well conditioned), summed over lanes and waves in a fixed order and
   // written to g.stats[tile_m][col] as (rows, shift, sum, sum of squares).
   float* Ws = (float*)smem + wave_u * 16 * WSTR;
+  if (ksplit > 1) {
+    // split-K: the raw fp32 tile of this K range, row m at m * Cols
+    float* __restrict__ P = g.part + (size_t)ks * g.M * g.Cols;
+    constexpr int C4 = WTN / 4;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Ws[(4 * (lane >> 4) + r) * WSTR + j * 16 + (lane & 15)] = acc[i][j][r];
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      for (int idx = lane; idx < 16 * C4; idx += 64) {
+        const int row = idx / C4, c4 = idx - row * C4;
+        const int m = m0 + arow0 + i * 16 + row, col = n0 + brow0 + c4 * 4;
+        if (m >= g.M || col >= g.Cols) continue;
+        *(float4*)(P + (size_t)m * g.Cols + col) = *(const float4*)(Ws + row * WSTR + c4 * 4);
+      }
+    }
+    return;
+  }
   constexpr int CPW = WTN / VW;                    // chunks per strip row; a lane's chunk column is lane % CPW
   static_assert(64 % CPW == 0, "lane chunk column fixed across strips");
   T* __restrict__ Cg = (T*)g.C;
@@ -521,6 +556,102 @@ template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool UNI>
 __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather g) {
   gather_impl<T, BM, BN, WGM, WGN, STAGES, UNI, false>(g);
 }
+// Split-K reduce: the ksplit fp32 partial tiles of a gather launch summed in
+// range order, then the gather epilogue on the sum (mode 0 store, 1
+// accumulate, 2 masked residual; storage rounding). With g.stats set, the BN
+// partials are written per block of SK_ROWS rows as (rows, shift, sum of
+// v - shift, sum of squares), the shift being the block's first stored value
+// of the channel, like the gather kernel's entries per tile.
+constexpr int SK_ROWS = 32;   // GEMM rows per block (and per BN partial entry)
+constexpr int SK_COLS = 64;   // output channels per block
+template <typename T>
+__global__ __launch_bounds__(256) void gather_splitk_reduce_kernel(ConvGather g) {
+  constexpr int VW = TT<T>::VW;
+  constexpr int CC = SK_COLS / VW;    // chunks per row
+  constexpr int RL = 256 / CC;        // row lanes
+  static_assert(RL <= SK_ROWS && SK_ROWS % RL == 0, "row lanes");
+  __shared__ float red[RL][SK_COLS][2];
+  __shared__ float shs[SK_COLS];
+  const int tid = threadIdx.x, cc = tid % CC, rl = tid / CC;
+  const int tiles_n = (g.Cols + SK_COLS - 1) / SK_COLS;
+  const int bm = blockIdx.x / tiles_n, bn = blockIdx.x - bm * tiles_n;
+  const int m0 = bm * SK_ROWS, col = bn * SK_COLS + cc * VW;
+  const int rows = min(SK_ROWS, g.M - m0);
+  const bool cok = col < g.Cols;
+  const size_t slice = (size_t)g.M * g.Cols;
+  const int HWm = g.Hm * g.Wm;
+  T* __restrict__ Cg = (T*)g.C;
+  auto sum_row = [&](int m, float (&v)[VW]) {
+    const float* p = g.part + (size_t)m * g.Cols + col;
+#pragma unroll
+    for (int e = 0; e < VW; ++e) v[e] = 0.f;
+    for (int k = 0; k < g.ksplit; ++k, p += slice) {
+#pragma unroll
+      for (int q = 0; q < VW / 4; ++q) {
+        const float4 f = *(const float4*)(p + 4 * q);
+        v[4 * q] += f.x; v[4 * q + 1] += f.y; v[4 * q + 2] += f.z; v[4 * q + 3] += f.w;
+      }
+    }
+  };
+  const bool stats = g.stats != nullptr;
+  float ssh[VW], s1[VW], s2[VW];
+#pragma unroll
+  for (int e = 0; e < VW; ++e) ssh[e] = s1[e] = s2[e] = 0.f;
+  if (stats && cok) {
+    float v[VW];
+    sum_row(m0, v);
+    unpack<T>(pack<T>(v), ssh);
+  }
+  if (cok) {
+    for (int r = rl; r < rows; r += RL) {
+      const int m = m0 + r;
+      float v[VW];
+      sum_row(m, v);
+      const int n = (int)g.fd_hw.div(m), rem = m - n * HWm;
+      const int ii = (int)g.fd_w.div(rem), jj = rem - ii * g.Wm;
+      const uint32_t off = ((uint32_t)((n * g.Hout + ii * g.os + g.oph) * g.Wout + jj * g.os + g.opw)) * g.Cols + col;
+      if (g.mode == 1) {
+        float o[VW];
+        unpack<T>(*(const uint4*)(Cg + off), o);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) v[e] += o[e];
+      } else if (g.mode == 2) {
+        float rr[VW];
+        unpack<T>(*(const uint4*)((const T*)g.R + off), rr);
+        const uint32_t mk = ((const uint8_t*)g.Rm)[off / VW];
+#pragma unroll
+        for (int e = 0; e < VW; ++e) v[e] += (mk >> e) & 1u ? rr[e] : 0.f;
+      }
+      const uint4 pk = pack<T>(v);
+      *(uint4*)(Cg + off) = pk;
+      if (stats) {
+        float vr[VW];
+        unpack<T>(pk, vr);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          const float d = vr[e] - ssh[e];
+          s1[e] += d;
+          s2[e] = __builtin_fmaf(d, d, s2[e]);
+        }
+      }
+    }
+  }
+  if (!stats) return;
+#pragma unroll
+  for (int e = 0; e < VW; ++e) {
+    red[rl][cc * VW + e][0] = s1[e];
+    red[rl][cc * VW + e][1] = s2[e];
+    if (rl == 0) shs[cc * VW + e] = ssh[e];
+  }
+  __syncthreads();
+  if (tid < SK_COLS && bn * SK_COLS + tid < g.Cols) {
+    float a1 = 0.f, a2 = 0.f;
+    for (int k = 0; k < RL; ++k) { a1 += red[k][tid][0]; a2 += red[k][tid][1]; }
+    float4* out = (float4*)g.stats + ((long)bm * g.Cols + bn * SK_COLS + tid);
+    *out = make_float4((float)rows, shs[tid], a1, a2);
+  }
+}
+
 // Blocks per CU that the LDS ring of a configuration allows (160 KB per CU),
 // and the waves per SIMD they make; the register allocation of the kernels
 // that use this is bounded to match.
@@ -2027,19 +2158,26 @@ int launch_gather2(const ConvGather& g0, hipStream_t s) {
   if ((long)g.N * g.Hout * g.Wout * g.Cols >= (1l << 31)) return -1;  // 32-bit output offsets
   g.zero = zero_page();
   if (!g.zero) return -4;
+  if (g.ksplit > 1 && (!g.part || ((uintptr_t)g.part & 15))) return -1;
+  const int ks = g.ksplit > 1 ? g.ksplit : 1;
   const int tiles = ceil_div(g.M, BM) * ceil_div(g.Cols, BN);
   const int kt = 128 / (int)sizeof(T);
   const int nt = 64 * WGM * WGN;
+  const dim3 grid(tiles * ks);
   if constexpr (RP) {
     if (gather_uniform(g, kt))
-      hipLaunchKernelGGL((conv_gather_rp_kernel<T, BM, BN, WGM, WGN, STAGES, true>), dim3(tiles), dim3(nt), 0, s, g);
+      hipLaunchKernelGGL((conv_gather_rp_kernel<T, BM, BN, WGM, WGN, STAGES, true>), grid, dim3(nt), 0, s, g);
     else
-      hipLaunchKernelGGL((conv_gather_rp_kernel<T, BM, BN, WGM, WGN, STAGES, false>), dim3(tiles), dim3(nt), 0, s, g);
+      hipLaunchKernelGGL((conv_gather_rp_kernel<T, BM, BN, WGM, WGN, STAGES, false>), grid, dim3(nt), 0, s, g);
   } else {
     if (gather_uniform(g, kt))
-      hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, true>), dim3(tiles), dim3(nt), 0, s, g);
+      hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, true>), grid, dim3(nt), 0, s, g);
     else
-      hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, false>), dim3(tiles), dim3(nt), 0, s, g);
+      hipLaunchKernelGGL((conv_gather2_kernel<T, BM, BN, WGM, WGN, STAGES, false>), grid, dim3(nt), 0, s, g);
+  }
+  if (ks > 1) {
+    const int rb = ceil_div(g.M, SK_ROWS) * ceil_div(g.Cols, SK_COLS);
+    hipLaunchKernelGGL(gather_splitk_reduce_kernel<T>, dim3(rb), dim3(256), 0, s, g);
   }
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
@@ -2216,6 +2354,47 @@ int gather_cfg(const ConvGather& g) {
   return (long)ceil_div(g.M, 128) * ceil_div(g.Cols, 128) >= 256 ? 16 : 14;
 }
 
+// Split-K for launches whose grid leaves CUs idle (fewer tiles than CUs:
+// small batches at the late stages, e.g. 1024 GEMM rows x 512 channels at
+// batch 64, 128x128 images): the K stages are cut into ranges of at least
+// kSplitMinStages, for about kSplitBlocks blocks in all. Measured on MI355X,
+// whole training steps: batch 64 at 128x128 2.07 -> 1.87 ms, at 160x160
+// 2.27 -> 2.11 ms. Grids of 256..448 tiles, split, won alone but lost in the
+// step beside the weight-gradient stream (batch 256 at 224x224 +0.1 ms,
+// fp32 batch 128 at 32x32 +0.09 ms), so they stay whole. Only the
+// non-persistent kernels split.
+int g_gather_split = 0;
+constexpr long kSplitBlocks = 640;
+constexpr long kSplitMaxTiles = 255;
+constexpr int kSplitMinStages = 8;
+
+int gather_split_want(int prec, const ConvGather& g, int id) {
+  if (id < 1 || id > kGatherCfgs || kGather[id].kind == 2 || g.K2 || g_gather_split == 1) return 1;
+  const int S = ceil_div(g.K, 128 / prec_bytes(prec));
+  int k;
+  if (g_gather_split > 1) {
+    k = g_gather_split;
+  } else {
+    const long tiles = (long)ceil_div(g.M, kGather[id].bm) * ceil_div(g.Cols, kGather[id].bn);
+    if (tiles > kSplitMaxTiles) return 1;
+    k = (int)((kSplitBlocks + tiles / 2) / tiles);
+    if (k > S / kSplitMinStages) k = S / kSplitMinStages;
+  }
+  if (k > S) k = S;
+  return k < 2 ? 1 : k;
+}
+
+// The split count a launch runs: the wanted one, cut to what the caller's
+// scratch holds (none without scratch).
+int gather_split(int prec, const ConvGather& g, int id) {
+  int k = gather_split_want(prec, g, id);
+  if (k < 2 || !g.ws || ((uintptr_t)g.ws & 15)) return 1;
+  const size_t per = (size_t)g.M * g.Cols * 4;
+  if (per == 0) return 1;
+  if ((size_t)k > g.ws_bytes / per) k = (int)(g.ws_bytes / per);
+  return k < 2 ? 1 : k;
+}
+
 bool use_halo(int prec, const ConvGather& g) {
   return (g_gather_override == 0 || g_gather_override == kGatherHalo) && halo_rows(prec, g) > 0;
 }
@@ -2265,7 +2444,11 @@ int gather_dispatch(const ConvGather* g, int np, hipStream_t s) {
       if (r != -1 || seg2) return r;                                                       \
     }                                                                                      \
     for (int i = 0; i < np; ++i) {                                                         \
-      const int r = g[i].M > 0 ? launch_gather2<T, bm, bn, wgm, wgn, st, kind == 1>(g[i], s) : 0; \
+      if (g[i].M <= 0) continue;                                                           \
+      ConvGather gi = g[i];                                                                \
+      gi.ksplit = gather_split(prec, gi, id);                                              \
+      gi.part = (float*)gi.ws;                                                             \
+      const int r = launch_gather2<T, bm, bn, wgm, wgn, st, kind == 1>(gi, s);             \
       if (r) return r;                                                                     \
     }                                                                                      \
     return 0;
@@ -2465,8 +2648,20 @@ int conv_gather_stat_entries(int prec, const ConvGather& g) {
     const int tiles = g.N * ((g.Hm + th - 1) / th), slots = 2 * cu_count();
     return (tiles < slots ? tiles : slots) * HALO16_WAVES;
   }
+  if (gather_split(prec, g, gather_cfg(g)) > 1) return ceil_div(g.M, SK_ROWS);
   const int bm = gather_tile(prec, g) / 1000;
   return bm > 0 ? ceil_div(g.M, bm) : 0;
+}
+
+int conv_gather_split_count(int prec, const ConvGather& g) {
+  if (use_halo(prec, g) || use_halo16(prec, g)) return 1;
+  return gather_split(prec, g, gather_cfg(g));
+}
+
+int conv_gather_split_override(int k) {
+  if (k < 0 || k > 64) return -1;
+  g_gather_split = k;
+  return 0;
 }
 
 int conv_gather_override(int id) {

@@ -37,6 +37,16 @@ struct ConvGather {
   const void* A2;
   const void* B2;
   int K2;
+  // Optional split-K scratch of the caller (nullptr: never split). A launch
+  // with too few tiles to fill the chip may cut its K stages into ksplit
+  // contiguous ranges: block (tile, range) writes its fp32 tile to
+  // part[range][M][Cols], and a reduce pass sums the ranges in a fixed order
+  // and applies the epilogue (mode, storage rounding, BN partials). ksplit
+  // and part are set by the launcher.
+  void* ws;
+  size_t ws_bytes;
+  int ksplit;
+  float* part;
 };
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s);
 // Up to four sub-problems of one operation (the parity phases of a stride-2
@@ -50,6 +60,11 @@ int conv_gather_tile(int prec, const ConvGather& g);
 int conv_gather_stat_entries(int prec, const ConvGather& g);
 // Force one kernel configuration for every gather launch (0 = automatic choice).
 int conv_gather_override(int id);
+// Split-K: number of K ranges a launch of g runs with its scratch (1 = none).
+int conv_gather_split_count(int prec, const ConvGather& g);
+// Force the split count of every gather launch that has scratch for it
+// (0 = automatic choice, 1 = never split; at most the launch's K stages).
+int conv_gather_split_override(int k);
 
 // Weight gradient: P[split][co][tap*Cin+ci] = sum_pixels dY[p][co] * Xcol[p][tap,ci]
 struct ConvWgrad {

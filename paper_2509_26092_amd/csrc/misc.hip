@@ -295,29 +295,41 @@ __global__ void avgpool_bwd_kernel(const float* __restrict__ df, T* __restrict__
 // over blockIdx.z; with several splits each writes its partial product to
 // P[z][M][N] and gemm_splitk_reduce_kernel adds them in split order
 // (deterministic). Tiles are loaded along whichever operand stride is 1.
+// They are latency-bound: a block takes its K range in passes of GK rows,
+// issuing every global load of a pass before the first is used (16 per
+// operand and thread), so each pass costs one memory round trip.
+constexpr int GK = 64;
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, long sam, long sak,
                                                        const float* __restrict__ B, long sbk, long sbn,
                                                        const float* __restrict__ bias, float* __restrict__ C,
                                                        int M, int N, int K, int kchunk, float* __restrict__ P) {
-  __shared__ float As[16][65], Bs[16][65];
+  __shared__ float As[GK][65], Bs[GK][65];
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
   const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
   const int kb = blockIdx.z * kchunk, ke = min(K, kb + kchunk);
   float acc[4][4] = {};
-  for (int k0 = kb; k0 < ke; k0 += 16) {
+  for (int k0 = kb; k0 < ke; k0 += GK) {
+    float ra[16], rb[16];
 #pragma unroll
-    for (int l = 0; l < 4; ++l) {
+    for (int l = 0; l < 16; ++l) {
       const int e = tid + 256 * l;
-      int mm, kk;
-      if (sak == 1) { kk = e & 15; mm = e >> 4; } else { mm = e & 63; kk = e >> 6; }
-      As[kk][mm] = (m0 + mm < M && k0 + kk < ke) ? A[(long)(m0 + mm) * sam + (long)(k0 + kk) * sak] : 0.f;
-      int nn, kq;
-      if (sbk == 1) { kq = e & 15; nn = e >> 4; } else { nn = e & 63; kq = e >> 6; }
-      Bs[kq][nn] = (n0 + nn < N && k0 + kq < ke) ? B[(long)(k0 + kq) * sbk + (long)(n0 + nn) * sbn] : 0.f;
+      const int mm = sak == 1 ? e >> 6 : e & 63, kk = sak == 1 ? e & 63 : e >> 6;
+      ra[l] = (m0 + mm < M && k0 + kk < ke) ? A[(long)(m0 + mm) * sam + (long)(k0 + kk) * sak] : 0.f;
+      const int nn = sbk == 1 ? e >> 6 : e & 63, kq = sbk == 1 ? e & 63 : e >> 6;
+      rb[l] = (n0 + nn < N && k0 + kq < ke) ? B[(long)(k0 + kq) * sbk + (long)(n0 + nn) * sbn] : 0.f;
+    }
+    __syncthreads();   // the previous pass's reads of the tiles are done
+#pragma unroll
+    for (int l = 0; l < 16; ++l) {
+      const int e = tid + 256 * l;
+      const int mm = sak == 1 ? e >> 6 : e & 63, kk = sak == 1 ? e & 63 : e >> 6;
+      As[kk][mm] = ra[l];
+      const int nn = sbk == 1 ? e >> 6 : e & 63, kq = sbk == 1 ? e & 63 : e >> 6;
+      Bs[kq][nn] = rb[l];
     }
     __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
+#pragma unroll 16
+    for (int kk = 0; kk < GK; ++kk) {
       float a[4], b[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) { a[i] = As[kk][ty * 4 + i]; b[i] = Bs[kk][tx * 4 + i]; }
@@ -326,7 +338,6 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * b[j];
     }
-    __syncthreads();
   }
   float* __restrict__ out = P ? P + (long)blockIdx.z * M * N : C;
 #pragma unroll
@@ -636,7 +647,8 @@ int avgpool_bwd_launch(int prec, const float* df, void* dx, int N, int HW, int C
 int gemm_f32_splits(int M, int N, int K) {
   const long tiles = (long)ceil_div(N, 64) * ceil_div(M, 64);
   int splits = 1;
-  while (tiles * splits < 512 && K / (2 * splits) >= 64) splits *= 2;
+  // at least 512 blocks or K ranges of one pass (GK) each
+  while (tiles * splits < 512 && K > GK * splits) splits *= 2;
   return splits;
 }
 

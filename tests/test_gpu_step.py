@@ -123,16 +123,21 @@ def test_imagenet_bf16_b256_224_full_step():
     _run_parity("imagenet", 1000, "bf16", 256, 224, seed=175)
 
 
-def test_imagenet_bf16_halo_configuration():
-    """The step with every convolution the halo kernels handle routed to them
-    (gather configuration 45): the streamed-weight halo kernel then runs the
-    stage-2 and stage-3 3x3 convolutions, forward with the BN statistics
-    epilogue and data gradients with the masked-residual epilogue."""
+@pytest.mark.parametrize("arch,classes,prec,N,H,split", [("imagenet", 1000, "bf16", 3, 64, 3),
+                                                         ("imagenet", 1000, "fp16", 2, 96, 5),
+                                                         ("imagenet", 1000, "fp32", 3, 64, 7),
+                                                         ("cifar", 100, "fp32", 6, 24, 2)])
+def test_split_k_forced(arch, classes, prec, N, H, split):
+    """Every forward and stride-1 data-gradient gather launch of the step
+    with its K stages cut into `split` ranges (3, 5 and 7 leave ranges of
+    unequal length), the partial tiles summed by the reduce pass, which also
+    writes the forward launches' BN partials and applies the data
+    gradients' masked-residual epilogue."""
     try:
-        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 45)
-        _run_parity("imagenet", 1000, "bf16", 2, 224, seed=131)
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_SPLIT, split)
+        _run_parity(arch, classes, prec, N, H, seed=140 + split)
     finally:
-        B.rn18_debug_set(None, B.RN18_DBG_GATHER_CONFIG, 0)
+        B.rn18_debug_set(None, B.RN18_DBG_GATHER_SPLIT, 0)
 
 
 def test_imagenet_fp32_small():
