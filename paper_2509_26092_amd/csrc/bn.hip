@@ -50,8 +50,40 @@ __device__ inline double block_sum_d(double v, double* sh) {
 // per channel, 4 thread groups over the chunks, fixed-order combine, then
 // mean = K + S1/M, biased variance
 // S2/M - (S1/M)^2 for normalising, unbiased (M/(M-1)) for the running one.
+// With a single chunk (at most 64 tiles) stage 1 finishes the statistics
+// itself and stage 2 is not launched.
+struct BnStatsOut {
+  const float* gamma;
+  const float* beta;
+  float eps, mom;
+  float* rm;
+  float* rv;
+  float* mean;
+  float* rstd;
+  float* scale;
+  float* shift;
+};
+
+__device__ inline void bn_stats_finish(int c, double N, double S1, double S2, double K, const BnStatsOut& o) {
+  const double m1 = S1 / N;
+  double var = S2 / N - m1 * m1;
+  if (var < 0.0) var = 0.0;
+  const double mean = K + m1;
+  const double rstd = 1.0 / sqrt(var + (double)o.eps);
+  const double sc = (double)o.gamma[c] * rstd;
+  o.mean[c] = (float)mean;
+  o.rstd[c] = (float)rstd;
+  o.scale[c] = (float)sc;
+  o.shift[c] = (float)((double)o.beta[c] - mean * sc);
+  if (o.rm) {
+    o.rm[c] = (float)((1.0 - o.mom) * (double)o.rm[c] + o.mom * mean);
+    o.rv[c] = (float)((1.0 - o.mom) * (double)o.rv[c] + o.mom * (N > 1.0 ? var * (N / (N - 1.0)) : 0.0));
+  }
+}
+
 __global__ __launch_bounds__(256) void bn_stats_tiles_reduce_kernel(const float* __restrict__ st, int ntiles, int C,
-                                                                    int per_chunk, double* __restrict__ red) {
+                                                                    int per_chunk, double* __restrict__ red,
+                                                                    BnStatsOut o) {
   __shared__ double sh[3][4][64];
   const int cl = threadIdx.x & 63, q = threadIdx.x >> 6;
   const int c = blockIdx.x * 64 + cl;
@@ -71,17 +103,22 @@ __global__ __launch_bounds__(256) void bn_stats_tiles_reduce_kernel(const float*
   sh[0][q][cl] = N; sh[1][q][cl] = S1; sh[2][q][cl] = S2;
   __syncthreads();
   if (q == 0 && c < C) {
-    double* o = red + ((long)blockIdx.y * C + c) * 3;
+    double v[3];
 #pragma unroll
-    for (int k = 0; k < 3; ++k) o[k] = ((sh[k][0][cl] + sh[k][1][cl]) + sh[k][2][cl]) + sh[k][3][cl];
+    for (int k = 0; k < 3; ++k) v[k] = ((sh[k][0][cl] + sh[k][1][cl]) + sh[k][2][cl]) + sh[k][3][cl];
+    if (gridDim.y == 1) {
+      bn_stats_finish(c, v[0], v[1], v[2], (double)((const float4*)st)[c].y, o);
+    } else {
+      double* out = red + ((long)blockIdx.y * C + c) * 3;
+#pragma unroll
+      for (int k = 0; k < 3; ++k) out[k] = v[k];
+    }
   }
 }
 
 __global__ __launch_bounds__(256) void bn_stats_tiles_final_kernel(const float* __restrict__ st,
                                                                    const double* __restrict__ red, int nchunks, int C,
-                                                                   const float* gamma, const float* beta, float eps,
-                                                                   float mom, float* rm, float* rv, float* mean_o,
-                                                                   float* rstd_o, float* scale_o, float* shift_o) {
+                                                                   BnStatsOut o) {
   __shared__ double sh[3][4][64];
   const int cl = threadIdx.x & 63, q = threadIdx.x >> 6;
   const int c = blockIdx.x * 64 + cl;
@@ -101,21 +138,7 @@ __global__ __launch_bounds__(256) void bn_stats_tiles_final_kernel(const float* 
   N = ((sh[0][0][cl] + sh[0][1][cl]) + sh[0][2][cl]) + sh[0][3][cl];
   S1 = ((sh[1][0][cl] + sh[1][1][cl]) + sh[1][2][cl]) + sh[1][3][cl];
   S2 = ((sh[2][0][cl] + sh[2][1][cl]) + sh[2][2][cl]) + sh[2][3][cl];
-  const double K = (double)((const float4*)st)[c].y;
-  const double m1 = S1 / N;
-  double var = S2 / N - m1 * m1;
-  if (var < 0.0) var = 0.0;
-  const double mean = K + m1;
-  const double rstd = 1.0 / sqrt(var + (double)eps);
-  const double sc = (double)gamma[c] * rstd;
-  mean_o[c] = (float)mean;
-  rstd_o[c] = (float)rstd;
-  scale_o[c] = (float)sc;
-  shift_o[c] = (float)((double)beta[c] - mean * sc);
-  if (rm) {
-    rm[c] = (float)((1.0 - mom) * (double)rm[c] + mom * mean);
-    rv[c] = (float)((1.0 - mom) * (double)rv[c] + mom * (N > 1.0 ? var * (N / (N - 1.0)) : 0.0));
-  }
+  bn_stats_finish(c, N, S1, S2, (double)((const float4*)st)[c].y, o);
 }
 
 // relu(bn(y)) as the forward pass stores it (rounded to the storage type):
@@ -610,10 +633,12 @@ int bn_stats_tiles_final_launch(const float* tile_stats, int ntiles, int C, doub
                                 float* mean, float* rstd, float* scale, float* shift, hipStream_t s) {
   const int chunks = bn_stats_tiles_chunks(ntiles);
   const int per_chunk = (ntiles + chunks - 1) / chunks;
+  const BnStatsOut o{gamma, beta, eps, momentum, run_mean, run_var, mean, rstd, scale, shift};
   hipLaunchKernelGGL(bn_stats_tiles_reduce_kernel, dim3((C + 63) / 64, chunks), dim3(256), 0, s, tile_stats, ntiles,
-                     C, per_chunk, scratch);
-  hipLaunchKernelGGL(bn_stats_tiles_final_kernel, dim3((C + 63) / 64), dim3(256), 0, s, tile_stats, scratch, chunks, C,
-                     gamma, beta, eps, momentum, run_mean, run_var, mean, rstd, scale, shift);
+                     C, per_chunk, scratch, o);
+  if (chunks > 1)
+    hipLaunchKernelGGL(bn_stats_tiles_final_kernel, dim3((C + 63) / 64), dim3(256), 0, s, tile_stats, scratch, chunks,
+                       C, o);
   return ok();
 }
 

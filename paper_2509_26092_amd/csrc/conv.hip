@@ -38,14 +38,6 @@ namespace {
 
 constexpr int RSTR = 9;  // LDS row stride in 16-byte units: 8 data chunks + 1 pad
 
-__device__ inline int xcd_remap(int b, int nb) {
-  // Blocks are dealt round-robin to the 8 XCDs; give each XCD a contiguous
-  // range of logical tiles so neighbouring tiles share its L2.
-  int per = nb >> 3, rem = nb & 7;
-  int x = b & 7, r = b >> 3;
-  return x * per + (x < rem ? x : rem) + r;
-}
-
 template <typename T> struct Mma;
 template <> struct Mma<bf16_t> {
   static constexpr int SUB = 1;

@@ -698,6 +698,7 @@ int dropout_launch(float* x, long n, uint64_t seed, uint64_t step, uint32_t thre
 
 int sgd_launch(float* w, const float* g, float* v, long n, float lr, float mom, float wd, hipStream_t s,
                const LossScale* ls) {
+  if (((uintptr_t)w | (uintptr_t)g | (uintptr_t)v) & 15) return -1;   // float4 accesses
   hipLaunchKernelGGL(sgd_kernel, dim3(grid_for((n + 3) / 4, 256, 8192)), dim3(256), 0, s, w, g, v, n, lr, mom, wd,
                      ls);
   return ok();
