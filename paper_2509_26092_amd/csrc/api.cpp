@@ -506,21 +506,42 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
 // projection of the same input ([N][Ho][Wo][Cout] and [Cin][Cout]) is added
 // inside the GEMM of parity phase (0,0), the only phase it reaches, so the
 // block-input gradient is rounded once.
+// The BN whose backward pass the data gradient feeds (see ConvGather::bstats):
+// its partials go to `out`, and the launch adds the entries it wrote to
+// *entries.
+struct BwdFeed {
+  float* out;
+  const void* y;
+  const uint8_t* mask;
+  const float* mean;
+  const float* rstd;
+  const float* sc;
+  const float* sf;
+  int* entries;
+};
+
 int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int H, int W, int Cin, int Ho, int Wo,
                  int Cout, int k, int s, int p, int mode, const void* R, const void* Rm, hipStream_t st,
                  Ctx* c = nullptr, int layer = -1, int cin_real = 0, const void* dy2 = nullptr,
-                 const void* wd2 = nullptr, void* sws = nullptr, size_t sws_bytes = 0) {
+                 const void* wd2 = nullptr, void* sws = nullptr, size_t sws_bytes = 0,
+                 const BwdFeed* feed = nullptr) {
   const double creal = cin_real > 0 ? cin_real : Cin;
   if (dy2 && (s != 2 || !wd2)) return -1;
   if (s == 1) {
     ConvGather g = gather_dgrad1(dy, wd, dx, N, H, W, Cin, Ho, Wo, Cout, k, p, mode, R, Rm);
     g.ws = sws; g.ws_bytes = sws_bytes;
+    if (feed) {
+      g.bstats = feed->out; g.by = feed->y; g.bmask = feed->mask;
+      g.bmean = feed->mean; g.brstd = feed->rstd; g.bsc = feed->sc; g.bsf = feed->sf;
+      if (!conv_gather_bwd_ok(prec, g)) return -1;
+      *feed->entries += conv_gather_bwd_entries(prec, g);
+    }
     const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(prec, g), conv_gather_kernel_name(prec, g), 2.0 * g.M * creal * g.K, 0.0);
     const int r = conv_gather_launch(prec, g, st);
     prof_end(c, pi);
     return r;
   }
-  if (s != 2) return -1;
+  if (s != 2 || feed) return -1;
   // the four parity phases, launched together
   ConvGather ph4[4];
   int np = 0;
@@ -821,6 +842,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   // mb: the ReLU mask bytes of the block output, or RECOMPUTE when the mask
   // is that of relu(bn(y)) of this layer itself (recomputed from y)
   const size_t RECOMPUTE = ~(size_t)0;
+  int fed_li = -1, fed_entries = 0;   // BN whose backward partials the last data gradient wrote, and their count
   auto bn_back = [&](int li, size_t dz, size_t mb, size_t dy) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
@@ -831,10 +853,17 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const uint8_t* mzp = rc ? nullptr : (const uint8_t*)(ws + mb);
     const float* msc = rc ? (const float*)(ws + P.scale) : nullptr;
     const float* msf = rc ? (const float*)(ws + P.shift) : nullptr;
-    TIMED(RN18_K_BN_BWD_REDUCE, li, 0, kernel_instance_name("bn_bwd_partial_kernel", prec), 0.0,
-          2 * tb + (rc ? 0.0 : tb / 16),
-          bn_bwd_partial_launch(prec, ws + dz, mzp, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.rstd), P.M,
-                                L.cout, part, &nblk, st, msc, msf));
+    if (fed_li == li) {
+      // the data gradient that produced dz wrote this BN's partials
+      part = (float*)(ws + pl.bnst);
+      nblk = fed_entries;
+      fed_li = -1;
+    } else {
+      TIMED(RN18_K_BN_BWD_REDUCE, li, 0, kernel_instance_name("bn_bwd_partial_kernel", prec), 0.0,
+            2 * tb + (rc ? 0.0 : tb / 16),
+            bn_bwd_partial_launch(prec, ws + dz, mzp, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.rstd), P.M,
+                                  L.cout, part, &nblk, st, msc, msf));
+    }
     TIMED(RN18_K_BN_BWD_REDUCE, li, 1, "bn_bwd_final_kernel", 0.0, 0.0,
           bn_bwd_final_launch(part, nblk, P.M, L.cout, state + L.g, (float*)(ws + P.rstd), grad + L.g, grad + L.b,
                               (float*)(ws + P.coef), st));
@@ -908,11 +937,23 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   // bytes Rm (1/16 of its size) are cut at the same images. With lds >= 0
   // (the block's projection conv, dY in dys) the projection's data gradient
   // is summed into the same GEMM (phase (0,0) of the stride-2 data gradient).
+  // bn_li >= 0: the data gradient is the input of conv bn_li's BN backward
+  // (ReLU mask from the mask bytes at bn_mb, or recomputed when bn_mb is
+  // RECOMPUTE); where the kernels allow it, the launch also writes that
+  // BN's partial sums (to pl.bnst, free during the backward pass) and
+  // bn_back then only combines them.
   auto dgrad = [&](int li, size_t dy, size_t dx, int mode, size_t R, size_t Rm, int lds = -1,
-                   size_t dys = 0) -> int {
+                   size_t dys = 0, int bn_li = -1, size_t bn_mb = 0) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     const size_t in_img = (size_t)P.Hin * P.Win * L.cin_p * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
+    bool feed_on = bn_li >= 0 && L.s == 1 && lds < 0;
+    for (int n0 = 0; feed_on && n0 < N; n0 += P.nb) {
+      const ConvGather probe = gather_dgrad1(nullptr, nullptr, nullptr, std::min(P.nb, N - n0), P.Hin, P.Win,
+                                             L.cin_p, P.Ho, P.Wo, L.cout, L.k, L.p, mode, nullptr, nullptr);
+      feed_on = conv_gather_bwd_ok(prec, probe);
+    }
+    int entries = 0;
     if (lds >= 0) {
       const ConvL& D = a.convs[lds];
       const ConvP& PD = pl.cp[lds];
@@ -922,12 +963,22 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     }
     for (int n0 = 0; n0 < N; n0 += P.nb) {
       const int nc = std::min(P.nb, N - n0);
+      BwdFeed feed{};
+      if (feed_on) {
+        const ConvP& PB = pl.cp[bn_li];
+        const bool rc = bn_mb == RECOMPUTE;
+        feed = BwdFeed{(float*)(ws + pl.bnst) + (size_t)entries * L.cin_p * 2, ws + PB.y + n0 * in_img,
+                       rc ? nullptr : (const uint8_t*)(ws + bn_mb + n0 * in_img / 16), (const float*)(ws + PB.mean),
+                       (const float*)(ws + PB.rstd), rc ? (const float*)(ws + PB.scale) : nullptr,
+                       rc ? (const float*)(ws + PB.shift) : nullptr, &entries};
+      }
       LCHK(launch_dgrad(prec, ws + dy + n0 * out_img, W_d(li), ws + dx + n0 * in_img, nc, P.Hin, P.Win, L.cin_p,
                         P.Ho, P.Wo, L.cout, L.k, L.s, L.p, mode, mode == 2 ? ws + R + n0 * in_img : nullptr,
                         mode == 2 ? ws + Rm + n0 * in_img / 16 : nullptr, st, c, li, L.cin,
                         lds >= 0 ? ws + dys + n0 * out_img : nullptr, lds >= 0 ? W_d(lds) : nullptr,
-                        ws + pl.gsplit, pl.gsplit_bytes));
+                        ws + pl.gsplit, pl.gsplit_bytes, feed_on ? &feed : nullptr));
     }
+    if (feed_on) { fed_li = bn_li; fed_entries = entries; }
     return 0;
   };
 
@@ -940,7 +991,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     if ((r = before_write(pl.gy)) || (r = bn_back(B.c2, gA, bp.mbits, pl.gy))) return join(), r;
     if (B.ds >= 0 && ((r = before_write(pl.gyd)) || (r = bn_back(B.ds, gA, bp.mbits, pl.gyd)))) return join(), r;
     if ((r = wgrad(B.c2, pl.gy))) return join(), r;
-    if ((r = dgrad(B.c2, pl.gy, pl.gz, 0, 0, 0))) return join(), r;
+    if ((r = dgrad(B.c2, pl.gy, pl.gz, 0, 0, 0, -1, 0, B.c1, RECOMPUTE))) return join(), r;
     const size_t z1b = (size_t)pl.cp[B.c1].M * a.convs[B.c1].cout * es;
     const size_t inb = (size_t)N * pl.cp[B.c1].Hin * pl.cp[B.c1].Win * a.convs[B.c1].cin_p * es;
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DZ1, bi, ws + pl.gz, z1b))) return r;
@@ -950,7 +1001,11 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
       if ((r = wgrad(B.ds, pl.gyd))) return join(), r;
       if ((r = dgrad(B.c1, pl.gy2, gB, 0, 0, 0, B.ds, pl.gyd))) return join(), r;
     } else {
-      if ((r = dgrad(B.c1, pl.gy2, gB, 2, gA, bp.mbits))) return join(), r;
+      // gB enters the previous block's second BN (its output mask), or the
+      // CIFAR stem's BN (mask recomputed); the ImageNet stem takes the pool path
+      const int nbn = bi > 0 ? a.blocks[bi - 1].c2 : a.imagenet ? -1 : 0;
+      const size_t nmb = bi > 0 ? pl.bp[bi - 1].mbits : RECOMPUTE;
+      if ((r = dgrad(B.c1, pl.gy2, gB, 2, gA, bp.mbits, -1, 0, nbn, nmb))) return join(), r;
     }
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX, bi, ws + gB, inb))) return r;
     std::swap(gA, gB);

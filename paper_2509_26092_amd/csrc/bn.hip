@@ -141,14 +141,6 @@ __global__ __launch_bounds__(256) void bn_stats_tiles_final_kernel(const float* 
   bn_stats_finish(c, N, S1, S2, (double)((const float4*)st)[c].y, o);
 }
 
-// relu(bn(y)) as the forward pass stores it (rounded to the storage type):
-// the backward pass recomputes ReLU masks from y with this, so each mask
-// decision equals the one the stored activation encodes.
-template <typename T>
-__device__ inline float relu_stored(float y, float sc, float sf) {
-  const float t = bn_affine(y, sc, sf);
-  return TT<T>::to_f(TT<T>::from_f(t > 0.f ? t : 0.f));
-}
 
 template <typename T>
 __global__ __launch_bounds__(256) void bn_apply_kernel(const T* __restrict__ y, const float* __restrict__ scale,

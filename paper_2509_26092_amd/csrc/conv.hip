@@ -26,6 +26,7 @@
 // of the pixel range go to a scratch buffer that is summed in a fixed order
 // (deterministic, no float atomics).
 #include "kernels.h"
+#include "pool.h"
 
 #include <cstdio>
 #include <mutex>
@@ -152,6 +153,45 @@ __device__ inline void wait_stage(int later_issued) {
   if (later_issued >= 2) wait_vmcnt<2 * IPW>();
   else if (later_issued == 1) wait_vmcnt<IPW>();
   else wait_vmcnt<0>();
+}
+
+// One stored 16-byte output chunk (pk, at element offset off, channels c0 ..)
+// into the BN backward partials of g.bstats: g = the stored value where the
+// BN's ReLU passed, s1 += g, s2 += g * (y - mean) * rstd, the arithmetic of
+// the standalone BN backward reduction.
+template <typename T>
+__device__ inline void bwd_partial_add(const ConvGather& g, const uint4& pk, uint32_t off, int c0,
+                                       float (&s1)[TT<T>::VW], float (&s2)[TT<T>::VW]) {
+  constexpr int VW = TT<T>::VW;
+  // the chunk's VW per-channel constants as 16-byte loads (c0 is a multiple of VW)
+  auto ld = [&](const float* p, float (&o)[VW]) {
+#pragma unroll
+    for (int q = 0; q < VW / 4; ++q) {
+      const float4 f = ((const float4*)(p + c0))[q];
+      o[4 * q] = f.x; o[4 * q + 1] = f.y; o[4 * q + 2] = f.z; o[4 * q + 3] = f.w;
+    }
+  };
+  float vr[VW], yy[VW], mu[VW], rs[VW];
+  unpack<T>(pk, vr);
+  unpack<T>(*(const uint4*)((const T*)g.by + off), yy);
+  ld(g.bmean, mu);
+  ld(g.brstd, rs);
+  uint32_t mk = 0;
+  if (g.bmask) {
+    mk = g.bmask[off / VW];
+  } else {
+    float sc[VW], sf[VW];
+    ld(g.bsc, sc);
+    ld(g.bsf, sf);
+#pragma unroll
+    for (int e = 0; e < VW; ++e) mk |= relu_stored<T>(yy[e], sc[e], sf[e]) > 0.f ? 1u << e : 0u;
+  }
+#pragma unroll
+  for (int e = 0; e < VW; ++e) {
+    const float gv = (mk >> e) & 1u ? vr[e] : 0.f;
+    s1[e] += gv;
+    s2[e] += gv * ((yy[e] - mu[e]) * rs[e]);
+  }
 }
 
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool UNI, bool RP>
@@ -434,6 +474,9 @@ __device__ inline void gather_impl(const ConvGather& g) {
   // tile's first row as the shift (a sample of the channel keeps the sums
   // well conditioned), summed over lanes and waves in a fixed order and
   // written to g.stats[tile_m][col] as (rows, shift, sum, sum of squares).
+  // With g.bstats set (a data gradient entering a BN's backward pass), they
+  // feed that BN's backward partials instead: sum g and sum g * xhat of the
+  // stored values g where its ReLU passed, written as g.bstats[tile_m][col].
   float* Ws = (float*)smem + wave_u * 16 * WSTR;
   if (ksplit > 1) {
     // split-K: the raw fp32 tile of this K range, row m at m * Cols
@@ -460,11 +503,13 @@ __device__ inline void gather_impl(const ConvGather& g) {
   static_assert(64 % CPW == 0, "lane chunk column fixed across strips");
   T* __restrict__ Cg = (T*)g.C;
   const bool stats = g.stats != nullptr;
+  const bool bstats = g.bstats != nullptr;
   float* Sh = (float*)smem + SM_EPI * 4;           // [BN] shifts, then [NW][64][ST_F] lane sums
   float* St = Sh + BN;
   float ssh[VW], ss1[VW], ss2[VW];
 #pragma unroll
   for (int e = 0; e < VW; ++e) ssh[e] = ss1[e] = ss2[e] = 0.f;
+  const int bc0 = n0 + brow0 + (lane % CPW) * VW;  // first channel of this lane's chunk column
   if (stats) {
     // tile row 0 sits in strip 0, register 0 of lanes 0..15 of the waves with wm == 0
     if (wm == 0 && lane < 16) {
@@ -517,10 +562,12 @@ __device__ inline void gather_impl(const ConvGather& g) {
           ss1[e] += d;
           ss2[e] = __builtin_fmaf(d, d, ss2[e]);
         }
+      } else if (bstats) {
+        bwd_partial_add<T>(g, pk, off, bc0, ss1, ss2);
       }
     }
   }
-  if (!stats) return;
+  if (!stats && !bstats) return;
   {
     float* o = St + (wave_u * 64 + lane) * ST_F;
 #pragma unroll
@@ -539,8 +586,8 @@ __device__ inline void gather_impl(const ConvGather& g) {
         a1 += p[e];
         a2 += p[VW + e];
       }
-    float4* out = (float4*)g.stats + ((long)(m0 / BM) * g.Cols + col);
-    *out = make_float4((float)rows, Sh[cl], a1, a2);
+    if (bstats) ((float2*)g.bstats)[(long)(m0 / BM) * g.Cols + col] = make_float2(a1, a2);
+    else ((float4*)g.stats)[(long)(m0 / BM) * g.Cols + col] = make_float4((float)rows, Sh[cl], a1, a2);
   }
 }
 
@@ -553,7 +600,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_gather2_kernel(ConvGather
 // accumulate, 2 masked residual; storage rounding). With g.stats set, the BN
 // partials are written per block of SK_ROWS rows as (rows, shift, sum of
 // v - shift, sum of squares), the shift being the block's first stored value
-// of the channel, like the gather kernel's entries per tile.
+// of the channel, like the gather kernel's entries per tile; with g.bstats
+// set, the BN backward partials of the stored values per block of rows.
 constexpr int SK_ROWS = 32;   // GEMM rows per block (and per BN partial entry)
 constexpr int SK_COLS = 64;   // output channels per block
 template <typename T>
@@ -585,7 +633,7 @@ __global__ __launch_bounds__(256) void gather_splitk_reduce_kernel(ConvGather g)
       }
     }
   };
-  const bool stats = g.stats != nullptr;
+  const bool stats = g.stats != nullptr, bstats = g.bstats != nullptr;
   float ssh[VW], s1[VW], s2[VW];
 #pragma unroll
   for (int e = 0; e < VW; ++e) ssh[e] = s1[e] = s2[e] = 0.f;
@@ -616,6 +664,7 @@ __global__ __launch_bounds__(256) void gather_splitk_reduce_kernel(ConvGather g)
       }
       const uint4 pk = pack<T>(v);
       *(uint4*)(Cg + off) = pk;
+      if (bstats) bwd_partial_add<T>(g, pk, off, col, s1, s2);
       if (stats) {
         float vr[VW];
         unpack<T>(pk, vr);
@@ -628,7 +677,7 @@ __global__ __launch_bounds__(256) void gather_splitk_reduce_kernel(ConvGather g)
       }
     }
   }
-  if (!stats) return;
+  if (!stats && !bstats) return;
 #pragma unroll
   for (int e = 0; e < VW; ++e) {
     red[rl][cc * VW + e][0] = s1[e];
@@ -639,8 +688,9 @@ __global__ __launch_bounds__(256) void gather_splitk_reduce_kernel(ConvGather g)
   if (tid < SK_COLS && bn * SK_COLS + tid < g.Cols) {
     float a1 = 0.f, a2 = 0.f;
     for (int k = 0; k < RL; ++k) { a1 += red[k][tid][0]; a2 += red[k][tid][1]; }
-    float4* out = (float4*)g.stats + ((long)bm * g.Cols + bn * SK_COLS + tid);
-    *out = make_float4((float)rows, shs[tid], a1, a2);
+    const long at = (long)bm * g.Cols + bn * SK_COLS + tid;
+    if (bstats) ((float2*)g.bstats)[at] = make_float2(a1, a2);
+    else ((float4*)g.stats)[at] = make_float4((float)rows, shs[tid], a1, a2);
   }
 }
 
@@ -2423,6 +2473,8 @@ template <typename T>
 int gather_dispatch(const ConvGather* g, int np, hipStream_t s) {
   const int prec = prec_of<T>();
   const bool seg2 = gather_has_seg2(g, np);
+  for (int i = 0; i < np; ++i)
+    if (g[i].bstats && (np != 1 || !conv_gather_bwd_ok(prec, g[i]))) return -1;   // not computed on this path
   if constexpr (sizeof(T) == 2) {
     // the halo kernels are instantiated for the 16-bit storage types only
     if (!seg2 && np == 1 && use_halo(prec, g[0])) return launch_halo<T>(g[0], halo_rows(prec, g[0]), s);
@@ -2648,6 +2700,20 @@ int conv_gather_stat_entries(int prec, const ConvGather& g) {
 int conv_gather_split_count(int prec, const ConvGather& g) {
   if (use_halo(prec, g) || use_halo16(prec, g)) return 1;
   return gather_split(prec, g, gather_cfg(g));
+}
+
+// The BN backward partials are computed by the non-persistent gather
+// kernels and the split-K reduce (one launch of one sub-problem).
+bool conv_gather_bwd_ok(int prec, const ConvGather& g) {
+  if (g.K2 || use_halo(prec, g) || use_halo16(prec, g)) return false;
+  const int id = gather_cfg(g);
+  return id >= 1 && id <= kGatherCfgs && kGather[id].kind != 2;
+}
+
+int conv_gather_bwd_entries(int prec, const ConvGather& g) {
+  if (!conv_gather_bwd_ok(prec, g)) return 0;
+  const int id = gather_cfg(g);
+  return gather_split(prec, g, id) > 1 ? ceil_div(g.M, SK_ROWS) : ceil_div(g.M, kGather[id].bm);
 }
 
 int conv_gather_split_override(int k) {

@@ -47,6 +47,20 @@ struct ConvGather {
   size_t ws_bytes;
   int ksplit;
   float* part;
+  // Optional BN backward partials of the stored output (the output is the
+  // gradient entering the backward pass of a BN whose forward output by has
+  // the shape of C): per tile of rows and channel, sum g and sum g * xhat,
+  // g = the stored value where that BN's ReLU passed, xhat = (by - bmean) *
+  // brstd. The ReLU mask is bit e of the chunk's byte in bmask, or, with
+  // bmask null, relu(by * bsc + bsf) > 0 as stored. Written as float2
+  // entries bstats[entry][Cols]; conv_gather_bwd_entries gives the count.
+  float* bstats;
+  const void* by;
+  const uint8_t* bmask;
+  const float* bmean;
+  const float* brstd;
+  const float* bsc;
+  const float* bsf;
 };
 int conv_gather_launch(int prec, const ConvGather& g, hipStream_t s);
 // Up to four sub-problems of one operation (the parity phases of a stride-2
@@ -62,6 +76,10 @@ int conv_gather_stat_entries(int prec, const ConvGather& g);
 int conv_gather_override(int id);
 // Split-K: number of K ranges a launch of g runs with its scratch (1 = none).
 int conv_gather_split_count(int prec, const ConvGather& g);
+// BN backward partials in the epilogue (g.bstats): whether the kernel a
+// launch of g runs computes them, and how many entries it writes.
+bool conv_gather_bwd_ok(int prec, const ConvGather& g);
+int conv_gather_bwd_entries(int prec, const ConvGather& g);
 // Force the split count of every gather launch that has scratch for it
 // (0 = automatic choice, 1 = never split; at most the launch's K stages).
 int conv_gather_split_override(int k);

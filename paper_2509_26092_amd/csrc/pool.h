@@ -1,5 +1,6 @@
-// Device helpers shared by the max-pool kernels and the batch-norm kernels
-// that are fused with the stem's 3x3 stride-2 pad-1 max pool.
+// Device helpers shared by the batch-norm, pooling and convolution kernels:
+// the BN affine and the stored ReLU output that the backward passes recompute
+// masks from, and the stem's 3x3 stride-2 pad-1 max-pool arithmetic.
 #ifndef RN18_POOL_H
 #define RN18_POOL_H
 
@@ -13,6 +14,15 @@ namespace rn18 {
 // multiply-add, so that every kernel that recomputes an activation (or its
 // ReLU mask) from y gets the bits the forward pass stored.
 __device__ inline float bn_affine(float y, float scale, float shift) { return __builtin_fmaf(y, scale, shift); }
+
+// relu(bn(y)) as the forward pass stores it (rounded to the storage type):
+// the backward pass recomputes ReLU masks from y with this, so each mask
+// decision equals the one the stored activation encodes.
+template <typename T>
+__device__ inline float relu_stored(float y, float sc, float sf) {
+  const float t = bn_affine(y, sc, sf);
+  return TT<T>::to_f(TT<T>::from_f(t > 0.f ? t : 0.f));
+}
 
 // The VW argmax bytes of one 16-byte chunk as one word load / store.
 template <int VW> struct ArgVec;
