@@ -508,7 +508,7 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
 // block-input gradient is rounded once.
 // The BN whose backward pass the data gradient feeds (see ConvGather::bstats):
 // its partials go to `out`, and the launch adds the entries it wrote to
-// *entries.
+// *entries, or clears *ok when the kernels it runs do not compute them.
 struct BwdFeed {
   float* out;
   const void* y;
@@ -518,6 +518,7 @@ struct BwdFeed {
   const float* sc;
   const float* sf;
   int* entries;
+  bool* ok;
 };
 
 int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int H, int W, int Cin, int Ho, int Wo,
@@ -530,18 +531,19 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
   if (s == 1) {
     ConvGather g = gather_dgrad1(dy, wd, dx, N, H, W, Cin, Ho, Wo, Cout, k, p, mode, R, Rm);
     g.ws = sws; g.ws_bytes = sws_bytes;
-    if (feed) {
+    if (feed && conv_gather_bwd_ok(prec, g)) {
       g.bstats = feed->out; g.by = feed->y; g.bmask = feed->mask;
       g.bmean = feed->mean; g.brstd = feed->rstd; g.bsc = feed->sc; g.bsf = feed->sf;
-      if (!conv_gather_bwd_ok(prec, g)) return -1;
       *feed->entries += conv_gather_bwd_entries(prec, g);
+    } else if (feed) {
+      *feed->ok = false;
     }
     const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile(prec, g), conv_gather_kernel_name(prec, g), 2.0 * g.M * creal * g.K, 0.0);
     const int r = conv_gather_launch(prec, g, st);
     prof_end(c, pi);
     return r;
   }
-  if (s != 2 || feed) return -1;
+  if (s != 2) return -1;
   // the four parity phases, launched together
   ConvGather ph4[4];
   int np = 0;
@@ -574,10 +576,21 @@ int launch_dgrad(int prec, const void* dy, const void* wd, void* dx, int N, int 
         if (mode == 1) continue;   // nothing to add
         g.nth = 1; g.ntw = 1;      // K = 0: the kernel writes acc = 0 (+ residual)
       }
+      if (feed) {
+        g.bstats = feed->out; g.by = feed->y; g.bmask = feed->mask;
+        g.bmean = feed->mean; g.brstd = feed->rstd; g.bsc = feed->sc; g.bsf = feed->sf;
+      }
       flops += 2.0 * g.M * creal * (g.K + g.K2);
       ph4[np++] = g;
     }
   if (np == 0) return 0;
+  if (feed && conv_gather_bwd_ok_multi(prec, ph4, np)) {
+    // the phases partition the output pixels: one entry row per row tile of each
+    *feed->entries += conv_gather_bwd_entries_multi(prec, ph4, np);
+  } else if (feed) {
+    *feed->ok = false;
+    for (int i = 0; i < np; ++i) ph4[i].bstats = nullptr;
+  }
   const int pi = prof_begin(c, RN18_K_CONV_DGRAD, layer, conv_gather_tile_multi(prec, ph4, np),
                             conv_gather_kernel_name_multi(prec, ph4, np),
                             flops, 0.0);
@@ -947,12 +960,8 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     const size_t in_img = (size_t)P.Hin * P.Win * L.cin_p * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
-    bool feed_on = bn_li >= 0 && L.s == 1 && lds < 0;
-    for (int n0 = 0; feed_on && n0 < N; n0 += P.nb) {
-      const ConvGather probe = gather_dgrad1(nullptr, nullptr, nullptr, std::min(P.nb, N - n0), P.Hin, P.Win,
-                                             L.cin_p, P.Ho, P.Wo, L.cout, L.k, L.p, mode, nullptr, nullptr);
-      feed_on = conv_gather_bwd_ok(prec, probe);
-    }
+    const bool feed_on = bn_li >= 0;
+    bool feed_ok = true;
     int entries = 0;
     if (lds >= 0) {
       const ConvL& D = a.convs[lds];
@@ -970,7 +979,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
         feed = BwdFeed{(float*)(ws + pl.bnst) + (size_t)entries * L.cin_p * 2, ws + PB.y + n0 * in_img,
                        rc ? nullptr : (const uint8_t*)(ws + bn_mb + n0 * in_img / 16), (const float*)(ws + PB.mean),
                        (const float*)(ws + PB.rstd), rc ? (const float*)(ws + PB.scale) : nullptr,
-                       rc ? (const float*)(ws + PB.shift) : nullptr, &entries};
+                       rc ? (const float*)(ws + PB.shift) : nullptr, &entries, &feed_ok};
       }
       LCHK(launch_dgrad(prec, ws + dy + n0 * out_img, W_d(li), ws + dx + n0 * in_img, nc, P.Hin, P.Win, L.cin_p,
                         P.Ho, P.Wo, L.cout, L.k, L.s, L.p, mode, mode == 2 ? ws + R + n0 * in_img : nullptr,
@@ -978,7 +987,8 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
                         lds >= 0 ? ws + dys + n0 * out_img : nullptr, lds >= 0 ? W_d(lds) : nullptr,
                         ws + pl.gsplit, pl.gsplit_bytes, feed_on ? &feed : nullptr));
     }
-    if (feed_on) { fed_li = bn_li; fed_entries = entries; }
+    // every batch chunk must have written its partials
+    if (feed_on && feed_ok) { fed_li = bn_li; fed_entries = entries; }
     return 0;
   };
 
@@ -997,14 +1007,14 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DZ1, bi, ws + pl.gz, z1b))) return r;
     if ((r = before_write(pl.gy2)) || (r = bn_back(B.c1, pl.gz, RECOMPUTE, pl.gy2))) return join(), r;
     if ((r = wgrad(B.c1, pl.gy2))) return join(), r;
+    // gB enters the previous block's second BN (its output mask), or the
+    // CIFAR stem's BN (mask recomputed); the ImageNet stem takes the pool path
+    const int nbn = bi > 0 ? a.blocks[bi - 1].c2 : a.imagenet ? -1 : 0;
+    const size_t nmb = bi > 0 ? pl.bp[bi - 1].mbits : RECOMPUTE;
     if (B.ds >= 0) {
       if ((r = wgrad(B.ds, pl.gyd))) return join(), r;
-      if ((r = dgrad(B.c1, pl.gy2, gB, 0, 0, 0, B.ds, pl.gyd))) return join(), r;
+      if ((r = dgrad(B.c1, pl.gy2, gB, 0, 0, 0, B.ds, pl.gyd, nbn, nmb))) return join(), r;
     } else {
-      // gB enters the previous block's second BN (its output mask), or the
-      // CIFAR stem's BN (mask recomputed); the ImageNet stem takes the pool path
-      const int nbn = bi > 0 ? a.blocks[bi - 1].c2 : a.imagenet ? -1 : 0;
-      const size_t nmb = bi > 0 ? pl.bp[bi - 1].mbits : RECOMPUTE;
       if ((r = dgrad(B.c1, pl.gy2, gB, 2, gA, bp.mbits, -1, 0, nbn, nmb))) return join(), r;
     }
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX, bi, ws + gB, inb))) return r;

@@ -163,34 +163,31 @@ template <typename T>
 __device__ inline void bwd_partial_add(const ConvGather& g, const uint4& pk, uint32_t off, int c0,
                                        float (&s1)[TT<T>::VW], float (&s2)[TT<T>::VW]) {
   constexpr int VW = TT<T>::VW;
-  // the chunk's VW per-channel constants as 16-byte loads (c0 is a multiple of VW)
-  auto ld = [&](const float* p, float (&o)[VW]) {
-#pragma unroll
-    for (int q = 0; q < VW / 4; ++q) {
-      const float4 f = ((const float4*)(p + c0))[q];
-      o[4 * q] = f.x; o[4 * q + 1] = f.y; o[4 * q + 2] = f.z; o[4 * q + 3] = f.w;
-    }
-  };
-  float vr[VW], yy[VW], mu[VW], rs[VW];
+  float vr[VW], yy[VW];
   unpack<T>(pk, vr);
   unpack<T>(*(const uint4*)((const T*)g.by + off), yy);
-  ld(g.bmean, mu);
-  ld(g.brstd, rs);
-  uint32_t mk = 0;
-  if (g.bmask) {
-    mk = g.bmask[off / VW];
-  } else {
-    float sc[VW], sf[VW];
-    ld(g.bsc, sc);
-    ld(g.bsf, sf);
+  const uint32_t mb = g.bmask ? g.bmask[off / VW] : 0u;
+  // four channels at a time: their constants as one 16-byte load each (c0 is a
+  // multiple of VW), few registers live in the epilogue
 #pragma unroll
-    for (int e = 0; e < VW; ++e) mk |= relu_stored<T>(yy[e], sc[e], sf[e]) > 0.f ? 1u << e : 0u;
-  }
+  for (int q = 0; q < VW / 4; ++q) {
+    const float4 mu = ((const float4*)(g.bmean + c0))[q], rs = ((const float4*)(g.brstd + c0))[q];
+    const float m4[4] = {mu.x, mu.y, mu.z, mu.w}, r4[4] = {rs.x, rs.y, rs.z, rs.w};
+    uint32_t mk = mb >> (4 * q);
+    if (!g.bmask) {
+      const float4 sc = ((const float4*)(g.bsc + c0))[q], sf = ((const float4*)(g.bsf + c0))[q];
+      const float c4[4] = {sc.x, sc.y, sc.z, sc.w}, f4[4] = {sf.x, sf.y, sf.z, sf.w};
+      mk = 0u;
 #pragma unroll
-  for (int e = 0; e < VW; ++e) {
-    const float gv = (mk >> e) & 1u ? vr[e] : 0.f;
-    s1[e] += gv;
-    s2[e] += gv * ((yy[e] - mu[e]) * rs[e]);
+      for (int t = 0; t < 4; ++t) mk |= relu_stored<T>(yy[4 * q + t], c4[t], f4[t]) > 0.f ? 1u << t : 0u;
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int e = 4 * q + t;
+      const float gv = (mk >> t) & 1u ? vr[e] : 0.f;
+      s1[e] += gv;
+      s2[e] += gv * ((yy[e] - m4[t]) * r4[t]);
+    }
   }
 }
 
@@ -929,7 +926,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
     float* Sh = E + NW * 16 * WSTR;
     float* Sp = Sh + BN;
     T* __restrict__ Cg = (T*)g.C;
-    const bool stats = g.stats != nullptr;
+    const bool stats = g.stats != nullptr, bstats = g.bstats != nullptr;
     barrier_only();  // every wave is done with the stage data in E
     float ssh[VW], ss1[VW], ss2[VW];
 #pragma unroll
@@ -987,10 +984,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
             ss1[e] += d;
             ss2[e] = __builtin_fmaf(d, d, ss2[e]);
           }
+        } else if (bstats) {
+          bwd_partial_add<T>(g, pk, off, col, ss1, ss2);
         }
       }
     }
-    if (stats) {
+    if (stats || bstats) {
       // lanes with the same chunk column hold the same channels: butterfly sum
 #pragma unroll
       for (int d = CPW; d < 64; d <<= 1)
@@ -1018,8 +1017,13 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
           a1 += Sp[((wmi * WGN + wn_c) * WTN + cw) * 2];
           a2 += Sp[((wmi * WGN + wn_c) * WTN + cw) * 2 + 1];
         }
-        float4* out = (float4*)g.stats + ((long)tm * g.Cols + col);
-        *out = make_float4((float)rows, Sh[cl], a1, a2);
+        if (bstats) {
+          // the sub-problems' row tiles follow one another in the entries
+          const long row = gs.tile_begin[pr] / tiles_n + tm;
+          ((float2*)g.bstats)[row * g.Cols + col] = make_float2(a1, a2);
+        } else {
+          ((float4*)g.stats)[(long)tm * g.Cols + col] = make_float4((float)rows, Sh[cl], a1, a2);
+        }
       }
     }
   }
@@ -2473,8 +2477,7 @@ template <typename T>
 int gather_dispatch(const ConvGather* g, int np, hipStream_t s) {
   const int prec = prec_of<T>();
   const bool seg2 = gather_has_seg2(g, np);
-  for (int i = 0; i < np; ++i)
-    if (g[i].bstats && (np != 1 || !conv_gather_bwd_ok(prec, g[i]))) return -1;   // not computed on this path
+  if (g[0].bstats && !conv_gather_bwd_ok_multi(prec, g, np)) return -1;   // not computed on this path
   if constexpr (sizeof(T) == 2) {
     // the halo kernels are instantiated for the 16-bit storage types only
     if (!seg2 && np == 1 && use_halo(prec, g[0])) return launch_halo<T>(g[0], halo_rows(prec, g[0]), s);
@@ -2714,6 +2717,33 @@ int conv_gather_bwd_entries(int prec, const ConvGather& g) {
   if (!conv_gather_bwd_ok(prec, g)) return 0;
   const int id = gather_cfg(g);
   return gather_split(prec, g, id) > 1 ? ceil_div(g.M, SK_ROWS) : ceil_div(g.M, kGather[id].bm);
+}
+
+// Several sub-problems: the persistent kernel computes them when it runs the
+// launch (its configuration, every sub-problem in the uniform row layout)
+// and the output has more than 64 channels. Measured on MI355X at batch 256,
+// 224x224: the 64-channel stride-2 data gradient of stage 2 (256x64 tiles,
+// 3,136 per launch) took 164 -> 258 us with the epilogue reading y, more
+// than the 44 us reduction it replaces; the 128- and 256-channel ones did not
+// slow down.
+bool conv_gather_bwd_ok_multi(int prec, const ConvGather* g, int np) {
+  if (np == 1 && !g[0].K2) return conv_gather_bwd_ok(prec, g[0]);
+  if (np < 1 || np > 4 || g[0].Cols <= 64) return false;
+  const int id = gather_cfg_multi(g, np);
+  if (id < 1 || id > kGatherCfgs || kGather[id].kind != 2) return false;
+  const int kt = 128 / prec_bytes(prec);
+  for (int i = 0; i < np; ++i)
+    if (!gather_uniform(g[i], kt)) return false;
+  return true;
+}
+
+int conv_gather_bwd_entries_multi(int prec, const ConvGather* g, int np) {
+  if (np == 1 && !g[0].K2) return conv_gather_bwd_entries(prec, g[0]);
+  if (!conv_gather_bwd_ok_multi(prec, g, np)) return 0;
+  const int bm = kGather[gather_cfg_multi(g, np)].bm;
+  int n = 0;
+  for (int i = 0; i < np; ++i) n += g[i].M > 0 ? ceil_div(g[i].M, bm) : 0;
+  return n;
 }
 
 int conv_gather_split_override(int k) {

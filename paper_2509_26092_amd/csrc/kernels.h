@@ -80,6 +80,8 @@ int conv_gather_split_count(int prec, const ConvGather& g);
 // launch of g runs computes them, and how many entries it writes.
 bool conv_gather_bwd_ok(int prec, const ConvGather& g);
 int conv_gather_bwd_entries(int prec, const ConvGather& g);
+bool conv_gather_bwd_ok_multi(int prec, const ConvGather* g, int np);
+int conv_gather_bwd_entries_multi(int prec, const ConvGather* g, int np);
 // Force the split count of every gather launch that has scratch for it
 // (0 = automatic choice, 1 = never split; at most the launch's K stages).
 int conv_gather_split_override(int k);
