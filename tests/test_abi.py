@@ -64,3 +64,25 @@ def test_operator_tensor_limit_is_checked_on_the_host():
     assert "per-tensor limit" in B.rn18_last_error()
     r = f(B.RN18_BF16, fake, fake, fake, 4096, 64, 64, 64, 64, 3, 1, 1, None)   # 2 GiB in bf16
     assert r == B.RN18_EINVAL
+
+
+def test_process_wide_debug_keys_validate_on_the_host():
+    """The process-wide tuning keys take no context and touch no device:
+    out-of-range gather configurations, weight-gradient configurations and
+    split-K counts are refused, in-range ones accepted, and 0 restores the
+    automatic choice."""
+    if not os.path.exists(B.LIB_PATH):
+        pytest.skip("library not built")
+    for key, good, bad in ((B.RN18_DBG_GATHER_CONFIG, (1, 44, 45), (-1, 46)),
+                           (B.RN18_DBG_WGRAD_CONFIG, (1, 10), (-1, 11)),
+                           (B.RN18_DBG_GATHER_SPLIT, (1, 2, 7, 64), (-1, 65))):
+        try:
+            for v in good:
+                B.rn18_debug_set(None, key, v)
+            for v in bad:
+                with pytest.raises(B.Rn18Error):
+                    B.rn18_debug_set(None, key, v)
+        finally:
+            B.rn18_debug_set(None, key, 0)
+    with pytest.raises(B.Rn18Error):              # per-context keys need a context
+        B.rn18_debug_set(None, B.RN18_DBG_SERIAL, 1)
