@@ -172,6 +172,7 @@ struct ConvP {
 struct BlockP { size_t in, z1, out, mbits; };
 
 constexpr size_t kSplitScratchBytes = (size_t)64 << 20;
+constexpr size_t kFuseBwdMaxBytes = (size_t)32 << 20;   // largest BN tensor whose backward partials a data gradient writes
 
 struct Plan {
   int N, H, W;
@@ -960,7 +961,11 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     const size_t in_img = (size_t)P.Hin * P.Win * L.cin_p * es, out_img = (size_t)P.Ho * P.Wo * L.cout * es;
-    const bool feed_on = bn_li >= 0;
+    // Only where the BN's tensor is small: the epilogue's y loads cost about
+    // what a standalone reduction pass costs, so the fusion pays by the
+    // launch it removes (measured at batch 256, 224x224: +25-30 us per
+    // stage-2 data gradient against a 27 us reduction).
+    const bool feed_on = bn_li >= 0 && (size_t)pl.cp[bn_li].M * a.convs[bn_li].cout * es <= kFuseBwdMaxBytes;
     bool feed_ok = true;
     int entries = 0;
     if (lds >= 0) {
