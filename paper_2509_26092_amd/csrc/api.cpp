@@ -172,7 +172,7 @@ struct ConvP {
 struct BlockP { size_t in, z1, out, mbits; };
 
 constexpr size_t kSplitScratchBytes = (size_t)64 << 20;
-constexpr size_t kFuseBwdMaxBytes = (size_t)32 << 20;   // largest BN tensor whose backward partials a data gradient writes
+constexpr size_t kFuseBwdMaxBytes = (size_t)16 << 20;   // largest BN tensor whose backward partials a data gradient writes
 
 struct Plan {
   int N, H, W;
@@ -964,7 +964,8 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     // Only where the BN's tensor is small: the epilogue's y loads cost about
     // what a standalone reduction pass costs, so the fusion pays by the
     // launch it removes (measured at batch 256, 224x224: +25-30 us per
-    // stage-2 data gradient against a 27 us reduction).
+    // stage-2 data gradient against a 27 us reduction, +13-16 us at stage 3
+    // against 20 us; at batch 64 every BN tensor is at most 12.8 MB).
     const bool feed_on = bn_li >= 0 && (size_t)pl.cp[bn_li].M * a.convs[bn_li].cout * es <= kFuseBwdMaxBytes;
     bool feed_ok = true;
     int entries = 0;
