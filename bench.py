@@ -171,6 +171,35 @@ def ingest_counters(fetch_csv, write_csv, command):
     return tab
 
 
+def copy_ceiling(B, torch, n=1 << 27, reps=10):
+    """HBM bandwidth that plain streaming reaches on this GPU, in bytes moved
+    per second: the better of a device-to-device copy of n floats (torch's
+    copy, one read and one write) and the library's ps_worker_delta over n
+    floats (two reads and one write), best of `reps` runs each, on arrays
+    of 512 MiB that no cache holds. It is the practical ceiling the stream
+    kernels are also reported against (measured 5.0-5.4 TB/s; reads alone
+    reach about 6.3)."""
+    a, b, d = (torch.ones(n, device="cuda") for _ in range(3))
+
+    def best(run, nbytes):
+        run()
+        torch.cuda.synchronize()
+        t = None
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            run()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            t = ms if t is None else min(t, ms)
+        return nbytes / t / 1e6
+
+    gbs = max(best(lambda: d.copy_(a), 8.0 * n), best(lambda: B.ps_worker_delta(a, b, d, n), 12.0 * n))
+    del a, b, d
+    return round(gbs, 1)
+
+
 def counters_summary(csv_path, title, command):
     """Markdown table of a rocprofv3 --pmc run's SQ counters per kernel
     (averaged over its dispatches). With SQ_VALU_MFMA_BUSY_CYCLES and
@@ -574,6 +603,7 @@ def main():
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(arch, classes, prec, H, args.cpu_images)
+    ceil = copy_ceiling(B, torch)
 
     out = {
         "metric": "ResNet-18 train images/sec/GPU", "value": round(N / dt, 1), "unit": "images/s",
@@ -586,6 +616,8 @@ def main():
         "roofline": roof,
         "conv_mfma_frac": head_sum["conv_mfma_frac"], "conv_tflops": head_sum["conv_tflops"],
         "stream_GBps": head_sum["stream_GBps"], "stream_hbm_frac": head_sum["stream_hbm_frac"],
+        "hbm_copy_ceiling_GBps": ceil,
+        "stream_ceiling_frac": round(head_sum["stream_GBps"] / ceil, 4) if ceil and head_sum["stream_GBps"] else None,
         "kernel_breakdown_ms": head_sum["classes"],
         "cpu_baseline": cpu,
         "per_shape": per_shape,
