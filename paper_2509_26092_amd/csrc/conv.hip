@@ -1072,6 +1072,8 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
   constexpr int P_U4 = HALO_PROWS * 4;              // one half-patch buffer (64-byte rows)
   constexpr int PI = HALO_PROWS / 16 / NW;          // half-patch load instructions per wave (16 rows each)
   constexpr int BI = 9 * 64 / 8 / NW;               // weight load instructions per wave (8 rows each)
+  constexpr int kResidualLoads = MODE == 0 ? 0 : FM * FN * (MODE == 2 ? 2 : 1);   // per wave and tile
+  static_assert(kResidualLoads < 64, "vmcnt range");
   __shared__ uint4 smem[B_U4 + 2 * P_U4];
   static_assert((B_U4 + 2 * P_U4) * 16 <= 163840, "LDS");
   static_assert(HALO_PROWS % (16 * NW) == 0 && (9 * 64) % (8 * NW) == 0, "whole load instructions per wave");
@@ -1158,6 +1160,20 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
   for (int tile = slot; tile < h.tiles; tile += G) {
     const int n = tile / h.tiles_img, i0 = (tile - n * h.tiles_img) * h.TH;
     const int npx = min(h.TH, g.Hm - i0) * g.Wm;    // output pixels of this tile
+    const long m0 = ((long)n * g.Hm + i0) * g.Wm;    // GEMM row of the tile's first pixel
+    uint32_t obase[FM];
+    bool okq[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int q = wave * 64 + i * 16 + (lane & 15);
+      okq[i] = q < npx;
+      obase[i] = (uint32_t)((m0 + (okq[i] ? q : 0)) * g.Cols) + chl;
+    }
+    // residual operands of modes 1 and 2, requested during the first half so
+    // that they have landed by the epilogue
+    typedef int i32x2_t __attribute__((ext_vector_type(2)));
+    i32x2_t ld0[MODE ? FM : 1][FN];
+    uint32_t ld1[MODE == 2 ? FM : 1][FN];
     floatx4_t acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -1166,15 +1182,31 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
 #pragma unroll
     for (int half = 0; half < 2; ++half, buf ^= 1) {
       // this half-patch has landed. Vector memory operations complete in
-      // issue order; after the first half of a tile was requested, only the
-      // previous tile's epilogue issued vector memory instructions: its
-      // residual loads (consumed there) and exactly FM * FN stores, which
-      // may stay in flight.
+      // issue order. After the first half of a tile was requested, only the
+      // previous tile's epilogue issued vector memory instructions: exactly
+      // FM * FN stores, which may stay in flight. After the second half was
+      // requested, only the tile's own residual loads were issued.
       if (half == 0 && tile != slot) wait_vmcnt<FM * FN>();
+      else if (half == 1) wait_vmcnt<kResidualLoads>();
       else wait_vmcnt<0>();
       barrier_only();
-      if (half == 0) issue_patch(tile, 1, buf ^ 1);
-      else if (tile + G < h.tiles) issue_patch(tile + G, 0, buf ^ 1);
+      if (half == 0) {
+        issue_patch(tile, 1, buf ^ 1);
+        if constexpr (MODE != 0) {
+#pragma unroll
+          for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+              const uint32_t ob = okq[i] ? (obase[i] + j * 16) * 2 : kOutOfRange;
+              ld0[i][j] = __builtin_amdgcn_raw_buffer_load_b64(rsR, ob, 0, 0);
+              if constexpr (MODE == 2)
+                ld1[i][j] = __builtin_amdgcn_raw_buffer_load_b8(
+                    rsRm, okq[i] ? (obase[i] + j * 16) >> 3 : kOutOfRange, 0, 0);
+            }
+        }
+      } else if (tile + G < h.tiles) {
+        issue_patch(tile + G, 0, buf ^ 1);
+      }
       const uint4* P = smem + B_U4 + buf * P_U4;
       // the patch width is made opaque here so that the operand addresses are
       // recomputed per phase rather than held in registers across phases
@@ -1217,31 +1249,7 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
     // every wave must be done with the patch buffers before they are reloaded
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 
-    // ---- epilogue straight from registers; the residual operands of modes
-    // 1 and 2 are all requested before the first is used
-    const long m0 = ((long)n * g.Hm + i0) * g.Wm;    // GEMM row of the tile's first pixel
-    uint32_t obase[FM];
-    bool okq[FM];
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int q = wave * 64 + i * 16 + (lane & 15);
-      okq[i] = q < npx;
-      obase[i] = (uint32_t)((m0 + (okq[i] ? q : 0)) * g.Cols) + chl;
-    }
-    typedef int i32x2_t __attribute__((ext_vector_type(2)));
-    i32x2_t ld0[MODE ? FM : 1][FN];
-    uint32_t ld1[MODE == 2 ? FM : 1][FN];
-    if constexpr (MODE != 0) {
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const uint32_t ob = okq[i] ? (obase[i] + j * 16) * 2 : kOutOfRange;
-          ld0[i][j] = __builtin_amdgcn_raw_buffer_load_b64(rsR, ob, 0, 0);
-          if constexpr (MODE == 2)
-            ld1[i][j] = __builtin_amdgcn_raw_buffer_load_b8(rsRm, okq[i] ? (obase[i] + j * 16) >> 3 : kOutOfRange, 0, 0);
-        }
-    }
+    // ---- epilogue straight from registers
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
