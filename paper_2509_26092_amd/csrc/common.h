@@ -43,8 +43,6 @@ inline int with_prec(int prec, F&& f) {
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float floatx2_t __attribute__((ext_vector_type(2)));
 
-// Round-to-nearest-even float -> bf16 (gfx950 v_cvt_pk_bf16_f32; a NaN stays
-// a NaN).
 // Blocks are dealt round-robin to the 8 XCDs (block b to XCD b % 8), each
 // with its own L2: this maps block b to a logical block index so that each
 // XCD takes a contiguous range of them and neighbouring work shares its L2.
@@ -54,6 +52,8 @@ __device__ inline int xcd_remap(int b, int nb) {
   return x * per + (x < rem ? x : rem) + r;
 }
 
+// Round-to-nearest-even float -> bf16 (gfx950 v_cvt_pk_bf16_f32; a NaN stays
+// a NaN).
 __device__ inline bf16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 __device__ inline uint32_t f2bf2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2_t{lo, hi}, bf16x2_t));
