@@ -1043,9 +1043,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, gather_occupancy(BM, BN, WGM * WGN,
 // Eight waves (two per SIMD, for LDS throughput) each own 64 pixels x 64
 // columns; the operand fragments of the next K step are read while the
 // MFMAs of the current one run.
-// LDS rows are swizzled so that the 16 consecutive rows of an MFMA operand
-// read hit distinct banks: 128-byte weight rows by (row / 2) mod 8, 64-byte
-// patch rows by (row / 4) mod 4.
+// LDS rows are swizzled so that an MFMA operand read (16 consecutive rows,
+// four 16-byte chunks of each) runs without bank conflicts: 128-byte weight
+// rows by (row / 2) mod 8, 64-byte patch rows by (row / 2) mod 4. (Measured
+// with ds_read_b128 on gfx950 at 8 waves per CU: these take 5.1-5.2 cycles
+// per read at every row offset; the (row / 4) mod 4 patch swizzle, or none,
+// takes 8.)
 // The MFMAs take the weights as their first operand, so a lane's
 // accumulators are 4 consecutive output channels of one pixel: the epilogue
 // stores them as 8-byte chunks straight from registers. The BN partial
@@ -1100,7 +1103,7 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
                   smem_lds + (uint32_t)((wave + NW * u) * 1024));
   }
   // half-patch load geometry: row p = patch pixel; the lane's 16 bytes go to
-  // slot lane % 4 and hold chunk (lane % 4) ^ ((p / 4) % 4) of the half
+  // slot lane % 4 and hold chunk (lane % 4) ^ ((p / 2) % 4) of the half
   int prel[PI], prow[PI];
 #pragma unroll
   for (int u = 0; u < PI; ++u) {
@@ -1108,7 +1111,7 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
     const int pr = p / h.PW, pc = p - pr * h.PW;
     const int ir = -g.ip + g.dh0 + pr, ic = -g.ip + g.dw0 + pc;   // input row (relative to i0) and column
     const bool ok = p < h.PH * h.PW && (unsigned)ic < (unsigned)g.Win;
-    const int c = (lane & 3) ^ ((p >> 2) & 3);
+    const int c = (lane & 3) ^ ((p >> 1) & 3);
     prel[u] = (ir * g.Win + ic) * rowb + c * 16;
     prow[u] = ok ? ir : -0x40000000;
   }
@@ -1219,7 +1222,7 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           const int pix = abase[i] + off;
-          a[i] = P[pix * 4 + (kq ^ ((pix >> 2) & 3))];
+          a[i] = P[pix * 4 + (kq ^ ((pix >> 1) & 3))];
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) b[j] = smem[(t * 64 + j * 16 + (lane & 15)) * 8 + ((half * 4 + kq) ^ wsw)];
@@ -1326,8 +1329,10 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
 // CU and one block's epilogue (stores and statistics) overlaps the other's
 // MFMAs. A K step of 32 covers two taps of the same tap row;
 // the lane group kq reads tap 2 * (step % 2) + kq / 2, channels 8 (kq % 2) ..
-// +8. LDS rows of 32 bytes are swizzled by (row / 8) mod 2, which keeps the
-// 16 consecutive rows of an operand read on distinct banks.
+// +8. LDS rows of 32 bytes are not swizzled: an operand read (16 consecutive
+// rows, both halves) is conflict-free as laid out (measured on gfx950 with
+// ds_read_b128 at 8 waves per CU: 5.1-5.2 cycles per read at every row
+// offset, where a (row / 8) mod 2 swizzle takes 8).
 // ---------------------------------------------------------------------------
 constexpr int HALO16_PROWS = 640;   // patch pixels per buffer
 constexpr int HALO16_WAVES = 4;     // waves per block; two blocks per CU overlap each other's epilogues
@@ -1354,12 +1359,12 @@ __global__ __launch_bounds__(64 * HALO16_WAVES, 2) void conv_halo16_kernel(ConvH
   const int slot = xcd_remap(blockIdx.x, G);
 
   // weights: row r = tap * 64 + column; the lane's 16 bytes go to slot
-  // lane % 2 and hold half (lane % 2) ^ ((r / 8) % 2) of the tap's channels
+  // lane % 2 and hold half lane % 2 of the tap's channels
 #pragma unroll
   for (int u = 0; u < BI; ++u) {
     const int r = (wave + NW * u) * 32 + (lane >> 1);
     const int t = r >> 6, col = r & 63;
-    const int c = (lane & 1) ^ ((r >> 3) & 1);
+    const int c = lane & 1;
     lds_dma16_buf((uint32_t)((col * 16 + t) * 32 + c * 16), rsB, smem_lds + (uint32_t)((wave + NW * u) * 1024));
   }
   int prel[PI], prow[PI];
@@ -1369,7 +1374,7 @@ __global__ __launch_bounds__(64 * HALO16_WAVES, 2) void conv_halo16_kernel(ConvH
     const int pr = p / h.PW, pc = p - pr * h.PW;
     const int ir = -g.ip + pr, ic = -g.ip + pc;      // input row (relative to i0) and column
     const bool ok = p < h.PH * h.PW && (unsigned)ic < (unsigned)g.Win;
-    const int c = (lane & 1) ^ ((p >> 3) & 1);
+    const int c = lane & 1;
     prel[u] = (ir * g.Win + ic) * 32 + c * 16;
     prow[u] = ok ? ir : -0x40000000;
   }
@@ -1392,7 +1397,6 @@ __global__ __launch_bounds__(64 * HALO16_WAVES, 2) void conv_halo16_kernel(ConvH
   }
   const int kq = lane >> 4, kh = kq & 1, kt = kq >> 1;
   const int chl = 4 * (lane >> 4);
-  const int bsw = (lane >> 3) & 1;                   // weight rows: (row / 8) % 2 == (lane % 16) / 8
   const uint32_t out_bytes = (uint32_t)((long)g.N * g.Hout * g.Wout * g.Cols * 2);
   const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(g.C, 0, out_bytes, 0x00020000);
 
@@ -1432,11 +1436,11 @@ __global__ __launch_bounds__(64 * HALO16_WAVES, 2) void conv_halo16_kernel(ConvH
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const int pix = abase[i] + off;
-        a[i] = P[pix * 2 + (kh ^ ((pix >> 3) & 1))];
+        a[i] = P[pix * 2 + kh];
       }
       const int t = th * 4 + tw;
 #pragma unroll
-      for (int j = 0; j < FN; ++j) b[j] = smem[(t * 64 + j * 16 + (lane & 15)) * 2 + (kh ^ bsw)];
+      for (int j = 0; j < FN; ++j) b[j] = smem[(t * 64 + j * 16 + (lane & 15)) * 2 + kh];
     };
     uint4 a0[FM], b0[FN], a1[FM], b1[FN];
     read_step(0, a0, b0);
