@@ -182,7 +182,9 @@ struct Plan {
   int Hs, Ws, Hp, Wp;           // stem output and pool output sizes
   int Hf, Wf;                   // final feature map
   size_t f, logits, dlogits, df, rowloss, lossbuf;
-  size_t gA, gB, gz, gy, gy2, gyd;  // gy, gy2: dY of the second and first conv of a block
+  // gy[p], gy2[p]: dY of the second and first conv of the blocks of index
+  // parity p (gy[1] also takes the stem's dY); gyd: dY of a projection
+  size_t gA, gB, gz, gy[2], gy2[2], gyd;
   size_t part, wpart, grad;
   size_t bnst;                  // forward conv epilogue BN partials (one entry per 32 rows at most)
   size_t bnst2, part2;          // the same scratch for the projection convs, which run on the side stream
@@ -213,7 +215,9 @@ struct Ctx {
   // weight gradients run on a second stream (default priority) beside the
   // data-gradient chain: events hand each dY buffer over and back
   hipStream_t side = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_ds = nullptr, ev_buf[3] = {nullptr, nullptr, nullptr};
+  // ev_blk[p]: end of the side-stream weight gradients of the last block of
+  // index parity p
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_ds = nullptr, ev_blk[2] = {nullptr, nullptr};
   void* ws = nullptr;
   size_t ws_bytes = 0;
   bool ws_owned = false;
@@ -322,7 +326,7 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   auto act = [&](int h, int w, int ch) { return alloc((size_t)N * h * w * ch * es); };
   pl->cp.assign(a.convs.size(), ConvP{});
   pl->bp.assign(a.blocks.size(), BlockP{});
-  size_t max_blockio = 0, max_z1 = 0, max_y = 0, max_yd = 0, max_wpart = 0;
+  size_t max_blockio = 0, max_z1 = 0, max_y = 0, max_yb = 0, max_yd = 0, max_wpart = 0;
   long max_partC = 0;
 
   auto conv_plan = [&](int li, int hin, int win, size_t xin) -> bool {
@@ -369,6 +373,7 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
     P.coef = alloc(3 * L.cout * 4);
     const size_t ybytes = (size_t)P.M * L.cout * es;
     if (ybytes > max_y) max_y = ybytes;
+    if (li > 0 && ybytes > max_yb) max_yb = ybytes;   // block convs (not the stem)
     {
       ConvWgrad wg{};
       wg.N = P.nb; wg.H = P.Hin; wg.W = P.Win; wg.Cin = P.cin; wg.Ho = P.Ho; wg.Wo = P.Wo; wg.Cout = L.cout;
@@ -446,8 +451,10 @@ int build_plan(const Ctx& c, int N, int H, int W, Plan* pl, std::string* why) {
   pl->gA = alloc(max_blockio);
   pl->gB = alloc(max_blockio);
   pl->gz = alloc(max_z1 ? max_z1 : 16);
-  pl->gy = alloc(max_y);
-  pl->gy2 = alloc(max_y);
+  pl->gy[0] = alloc(max_yb ? max_yb : 16);
+  pl->gy2[0] = alloc(max_yb ? max_yb : 16);
+  pl->gy[1] = alloc(max_y);
+  pl->gy2[1] = alloc(max_yb ? max_yb : 16);
   pl->gyd = alloc(max_yd ? max_yd : 16);
   pl->part = alloc((size_t)max_partC * 4);
   size_t max_bnst = 0;
@@ -686,7 +693,7 @@ void destroy_side(Ctx& c) {
     (void)hipStreamDestroy(c.side);
     c.side = nullptr;
   }
-  for (hipEvent_t* e : {&c.ev_fork, &c.ev_join, &c.ev_ds, &c.ev_buf[0], &c.ev_buf[1], &c.ev_buf[2]})
+  for (hipEvent_t* e : {&c.ev_fork, &c.ev_join, &c.ev_ds, &c.ev_blk[0], &c.ev_blk[1]})
     if (*e) { (void)hipEventDestroy(*e); *e = nullptr; }
 }
 
@@ -909,33 +916,56 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     LCHK(launch_wgrad_reduce(wpart, used, L.cout, P.k, P.cin, L.cin, grad + L.w, P.s2d, ws_st, c, li));
     return 0;
   };
-  // With the side stream (not while profiling or capturing): a weight
-  // gradient starts on it once its dY buffer is written on the main stream,
-  // and the main stream waits for it before it writes that buffer again and
-  // before the SGD update. The weight gradients only read dY, the forward
-  // activations and their own split-K scratch, and write their own slices
-  // of the gradient, so the data-gradient chain runs on meanwhile.
+  // With the side stream (not while profiling or capturing): the weight
+  // gradients of a block run on it once their dY buffers are written. The
+  // blocks alternate between two pairs of dY buffers by index parity, so the
+  // main stream next writes a block's buffers two blocks later and waits
+  // for that block's weight gradients only then (one wait per block); the
+  // stem's dY goes to the pair of block 1. Each event record or wait costs
+  // the queue several microseconds. With 16-bit storage the side stream has
+  // slack and a block's weight gradients start together, after its second
+  // BN backward (one fork per block). In fp32 the convolutions are bound by
+  // the slower fp32 MFMAs and the data gradients they would overlap slow
+  // down as much as the weight gradients gain, so each weight gradient
+  // starts as soon as its dY is written, overlapping the memory-bound BN
+  // passes (measured, CIFAR batch 128: one fork per block 5.15 -> 5.41 ms).
+  // The weight gradients only read dY, the forward activations and their
+  // own split-K scratch, and write their own slices of the gradient, so the
+  // data-gradient chain runs on meanwhile. The stem's weight gradient runs
+  // on the main stream after a join, since it shares that scratch.
   const bool ov = c->side && !c->dbg_serial && !c->prof_on && c->captures.empty();
-  const size_t dybuf[3] = {pl.gy, pl.gy2, pl.gyd};
-  bool pending[3] = {false, false, false}, forked = false;
-  auto buf_id = [&](size_t b) { return b == pl.gy ? 0 : b == pl.gy2 ? 1 : 2; };
-  auto before_write = [&](size_t b) -> int {
-    const int i = buf_id(b);
-    if (ov && pending[i]) {
-      HIPCHK(hipStreamWaitEvent(st, c->ev_buf[i], 0));
-      pending[i] = false;
-    }
+  const bool fork_each = prec == PREC_F32;
+  const int nblocks = (int)a.blocks.size();
+  int done_from = nblocks;          // side work of blocks >= done_from is known complete on the main stream
+  int rec_blk[2] = {nblocks, nblocks};   // block whose side work ev_blk[p] marks the end of
+  bool forked = false;
+  // main stream: wait until the side work of block k (and of every block
+  // forked before it) is complete
+  auto need_done = [&](int k) -> int {
+    if (!ov || k >= done_from || k >= nblocks) return 0;
+    const int p = k & 1;
+    if (rec_blk[p] > k) return 0;   // block k did not fork onto the side stream
+    HIPCHK(hipStreamWaitEvent(st, c->ev_blk[p], 0));
+    done_from = rec_blk[p];
     return 0;
   };
-  auto wgrad = [&](int li, size_t dy) -> int {
-    if (!ov) return wgrad_on(li, dy, st);
+  // weight gradients of block bi from their dY buffers; last: the block's
+  // final ones (its end is then recorded for need_done)
+  auto fork = [&](int bi, const int* li, const size_t* dy, int n, bool last) -> int {
+    if (!ov) {
+      for (int k = 0; k < n; ++k)
+        if (int r2 = wgrad_on(li[k], dy[k], st)) return r2;
+      return 0;
+    }
     HIPCHK(hipEventRecord(c->ev_fork, st));
     HIPCHK(hipStreamWaitEvent(c->side, c->ev_fork, 0));
     forked = true;
-    if (int r2 = wgrad_on(li, dy, c->side)) return r2;
-    const int i = buf_id(dy);
-    HIPCHK(hipEventRecord(c->ev_buf[i], c->side));
-    pending[i] = true;
+    for (int k = 0; k < n; ++k)
+      if (int r2 = wgrad_on(li[k], dy[k], c->side)) return r2;
+    if (last) {
+      HIPCHK(hipEventRecord(c->ev_blk[bi & 1], c->side));
+      rec_blk[bi & 1] = bi;
+    }
     return 0;
   };
   auto join = [&]() -> int {
@@ -943,10 +973,9 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     HIPCHK(hipEventRecord(c->ev_join, c->side));
     HIPCHK(hipStreamWaitEvent(st, c->ev_join, 0));
     forked = false;
-    pending[0] = pending[1] = pending[2] = false;
+    done_from = 0;
     return 0;
   };
-  (void)dybuf;
   // data gradient over the batch chunks; R (shaped like dx) and its mask
   // bytes Rm (1/16 of its size) are cut at the same images. With lds >= 0
   // (the block's projection conv, dY in dys) the projection's data gradient
@@ -998,34 +1027,49 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     return 0;
   };
 
-  int done = 0;
-  for (int bi = (int)a.blocks.size() - 1; bi >= 0; --bi) {
+  int done = 0, prev_ds = -1;
+  for (int bi = nblocks - 1; bi >= 0; --bi) {
     if (c->dbg_stop_blocks >= 0 && done++ == c->dbg_stop_blocks) return join();
     const BlockL& B = a.blocks[bi];
     const BlockP& bp = pl.bp[bi];
+    const size_t gy = pl.gy[bi & 1], gy2 = pl.gy2[bi & 1];
+    // this block's dY buffers were last read by the weight gradients of
+    // block bi + 2, the projection's by those of the previous projection block
+    if ((r = need_done(bi + 2)) || (B.ds >= 0 && prev_ds >= 0 && (r = need_done(prev_ds)))) return join(), r;
     // gA = gradient wrt the block output (before its ReLU mask)
-    if ((r = before_write(pl.gy)) || (r = bn_back(B.c2, gA, bp.mbits, pl.gy))) return join(), r;
-    if (B.ds >= 0 && ((r = before_write(pl.gyd)) || (r = bn_back(B.ds, gA, bp.mbits, pl.gyd)))) return join(), r;
-    if ((r = wgrad(B.c2, pl.gy))) return join(), r;
-    if ((r = dgrad(B.c2, pl.gy, pl.gz, 0, 0, 0, -1, 0, B.c1, RECOMPUTE))) return join(), r;
+    if ((r = bn_back(B.c2, gA, bp.mbits, gy))) return join(), r;
+    if (B.ds >= 0 && (r = bn_back(B.ds, gA, bp.mbits, pl.gyd))) return join(), r;
+    const int li_a[2] = {B.c2, B.ds};
+    const size_t dy_a[2] = {gy, pl.gyd};
+    if (fork_each && (r = fork(bi, li_a, dy_a, B.ds >= 0 ? 2 : 1, false))) return join(), r;
+    if ((r = dgrad(B.c2, gy, pl.gz, 0, 0, 0, -1, 0, B.c1, RECOMPUTE))) return join(), r;
     const size_t z1b = (size_t)pl.cp[B.c1].M * a.convs[B.c1].cout * es;
     const size_t inb = (size_t)N * pl.cp[B.c1].Hin * pl.cp[B.c1].Win * a.convs[B.c1].cin_p * es;
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DZ1, bi, ws + pl.gz, z1b))) return r;
-    if ((r = before_write(pl.gy2)) || (r = bn_back(B.c1, pl.gz, RECOMPUTE, pl.gy2))) return join(), r;
-    if ((r = wgrad(B.c1, pl.gy2))) return join(), r;
+    if ((r = bn_back(B.c1, pl.gz, RECOMPUTE, gy2))) return join(), r;
+    if (fork_each) {
+      if ((r = fork(bi, &B.c1, &gy2, 1, true))) return join(), r;
+    } else {
+      const int li[3] = {B.c2, B.c1, B.ds};
+      const size_t dy[3] = {gy, gy2, pl.gyd};
+      if ((r = fork(bi, li, dy, B.ds >= 0 ? 3 : 2, true))) return join(), r;
+    }
     // gB enters the previous block's second BN (its output mask), or the
     // CIFAR stem's BN (mask recomputed); the ImageNet stem takes the pool path
     const int nbn = bi > 0 ? a.blocks[bi - 1].c2 : a.imagenet ? -1 : 0;
     const size_t nmb = bi > 0 ? pl.bp[bi - 1].mbits : RECOMPUTE;
     if (B.ds >= 0) {
-      if ((r = wgrad(B.ds, pl.gyd))) return join(), r;
-      if ((r = dgrad(B.c1, pl.gy2, gB, 0, 0, 0, B.ds, pl.gyd, nbn, nmb))) return join(), r;
+      if ((r = dgrad(B.c1, gy2, gB, 0, 0, 0, B.ds, pl.gyd, nbn, nmb))) return join(), r;
+      prev_ds = bi;
     } else {
-      if ((r = dgrad(B.c1, pl.gy2, gB, 2, gA, bp.mbits, -1, 0, nbn, nmb))) return join(), r;
+      if ((r = dgrad(B.c1, gy2, gB, 2, gA, bp.mbits, -1, 0, nbn, nmb))) return join(), r;
     }
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DX, bi, ws + gB, inb))) return r;
     std::swap(gA, gB);
   }
+  // the stem's dY goes to gy[1], last read by the weight gradients of block 1
+  const size_t gys = pl.gy[1];
+  if ((r = need_done(1))) return join(), r;
   if (a.imagenet) {
     // stem BN backward straight from the pooled gradient (gA) and the argmax
     const ConvL& L = a.convs[0];
@@ -1042,7 +1086,6 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const float* sc = (const float*)(ws + P.scale);
     const float* sf = (const float*)(ws + P.shift);
     const double yb = (double)P.M * C0 * es, pb = (double)N * pl.Hp * pl.Wp * C0 * (es + 1);
-    if ((r = before_write(pl.gy))) return join(), r;
     TIMED(RN18_K_BN_BWD_REDUCE, 0, 0, kernel_instance_name("bn_bwd_partial_pool_kernel", prec), 0.0, yb + pb,
           bn_bwd_partial_pool_launch(prec, ws + gA, parg, ws + P.y, sc, sf, (float*)(ws + P.mean),
                                      (float*)(ws + P.rstd), N, pl.Hs, pl.Ws, C0, pl.Hp, pl.Wp, part, &nblk, st));
@@ -1051,12 +1094,12 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
                               (float*)(ws + P.coef), st));
     TIMED(RN18_K_BN_BWD_APPLY, 0, 0, kernel_instance_name("bn_bwd_apply_pool_kernel", prec), 0.0, 2 * yb + pb,
           bn_bwd_apply_pool_launch(prec, ws + gA, parg, ws + P.y, sc, sf, (float*)(ws + P.mean),
-                                   (float*)(ws + P.coef), ws + pl.gy, N, pl.Hs, pl.Ws, C0, pl.Hp, pl.Wp, st));
-    if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DY, 0, ws + pl.gy, (size_t)P.M * C0 * es))) return r;
-  } else if ((r = before_write(pl.gy)) || (r = bn_back(0, gA, RECOMPUTE, pl.gy))) {
+                                   (float*)(ws + P.coef), ws + gys, N, pl.Hs, pl.Ws, C0, pl.Hp, pl.Wp, st));
+    if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DY, 0, ws + gys, (size_t)P.M * C0 * es))) return r;
+  } else if ((r = bn_back(0, gA, RECOMPUTE, gys))) {
     return join(), r;
   }
-  if ((r = wgrad(0, pl.gy)) || (r = join())) return join(), r;
+  if ((r = join()) || (r = wgrad_on(0, gys, st))) return join(), r;
   if (c->ls) TIMED(RN18_K_SGD, 1, 0, "grad_check_kernel", 0.0, 4.0 * a.P, grad_check_launch(grad, a.P, c->ls, st));
   TIMED(RN18_K_SGD, 0, 0, "sgd_kernel", 0.0, 20.0 * a.P,
         sgd_launch(state, grad, c->momentum, a.P, lr, c->cfg.momentum, c->cfg.weight_decay, st, c->ls));
@@ -1160,9 +1203,8 @@ int rn18_init(const rn18_config* cfg, uint64_t seed, void* hip_stream, float* st
       hipEventCreateWithFlags(&c.ev_fork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c.ev_join, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c.ev_ds, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&c.ev_buf[0], hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&c.ev_buf[1], hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&c.ev_buf[2], hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&c.ev_blk[0], hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c.ev_blk[1], hipEventDisableTiming) != hipSuccess) {
     destroy_side(c);
     return bail(RN18_EHIP, "stream or event creation failed");
   }
@@ -1471,7 +1513,7 @@ int rn18_debug_copy(rn18_ctx* h, int N, int H, int W, int which, int index, void
     case RN18_DBG_GA: src = ws + pl->gA; break;
     case RN18_DBG_GB: src = ws + pl->gB; break;
     case RN18_DBG_GZ: src = ws + pl->gz; break;
-    case RN18_DBG_GY: src = ws + pl->gy; break;
+    case RN18_DBG_GY: src = ws + pl->gy[1]; break;
     case RN18_DBG_GYD: src = ws + pl->gyd; break;
     case RN18_DBG_GRAD: src = ws + pl->grad; break;
     case RN18_DBG_WF: if (conv_ok()) src = (char*)c.wf + (size_t)a.convs[index].wf * c.es; break;
