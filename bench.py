@@ -512,6 +512,8 @@ def main():
                          "(the command recorded with --traffic-command), then exit")
     ap.add_argument("--traffic-command", default="",
                     help="the command the counter runs used, recorded with --traffic-from")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the HBM copy-ceiling measurement (for kernel-trace runs of the step)")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run ps_worker_delta over 2^26 floats (reads 512 MiB, writes 256 MiB) as the "
                          "known-size kernel that scales HBM counters")
@@ -603,7 +605,10 @@ def main():
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(arch, classes, prec, H, args.cpu_images)
-    ceil = copy_ceiling(B, torch)
+    # the ceiling's copies and delta streams would enter a profile of the
+    # step (and the counter calibration, which reads delta_kernel), so runs
+    # under a profiler skip it
+    ceil = None if args.calibrate or args.no_ceiling else copy_ceiling(B, torch)
 
     out = {
         "metric": "ResNet-18 train images/sec/GPU", "value": round(N / dt, 1), "unit": "images/s",
