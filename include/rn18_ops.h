@@ -85,7 +85,10 @@ int rn18op_round_bf16(const float* x, uint16_t* y, size_t n, void* hip_stream);
  * rn18_debug_copy: copy `bytes` of a workspace tensor of the (N,H,W) plan to
  * the device buffer dst, enqueued on the context's stream. `which` selects
  * the tensor (NHWC in the compute type, or fp32 for grad/mean/rstd),
- * `index` the conv layer (forward order) or the residual block. */
+ * `index` the conv layer (forward order) or the residual block. The
+ * backward buffers hold what the last step left there: GA / GB the
+ * gradients of block outputs (ping-pong), GZ the data gradient of a block's
+ * second conv, GY the stem conv's dY, GYD a projection conv's dY. */
 enum {
   RN18_DBG_STOP_BLOCKS = 0,
   /* process-wide: force gather-conv kernel configuration `value` (1..45,
