@@ -1188,7 +1188,10 @@ __global__ __launch_bounds__(64 * HALO_WAVES, 1) void conv_halo_kernel(ConvHalo 
       // issue order. After the first half of a tile was requested, only the
       // previous tile's epilogue issued vector memory instructions: exactly
       // FM * FN stores, which may stay in flight. After the second half was
-      // requested, only the tile's own residual loads were issued.
+      // requested, only the tile's own residual loads were issued: at least
+      // kResidualLoads instructions (their addresses are 32 and 2 bytes apart,
+      // so none merge; the compiler splits some masked ones in two), so
+      // waiting down to that many leaves the patch landed.
       if (half == 0 && tile != slot) wait_vmcnt<FM * FN>();
       else if (half == 1) wait_vmcnt<kResidualLoads>();
       else wait_vmcnt<0>();
