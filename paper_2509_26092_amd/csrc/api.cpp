@@ -864,7 +864,8 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
   // is that of relu(bn(y)) of this layer itself (recomputed from y)
   const size_t RECOMPUTE = ~(size_t)0;
   int fed_li = -1, fed_entries = 0;   // BN whose backward partials the last data gradient wrote, and their count
-  auto bn_back = [&](int li, size_t dz, size_t mb, size_t dy) -> int {
+  // done (optional): an event the apply launch itself completes
+  auto bn_back = [&](int li, size_t dz, size_t mb, size_t dy, hipEvent_t done = nullptr) -> int {
     const ConvL& L = a.convs[li];
     const ConvP& P = pl.cp[li];
     int nblk = 0;
@@ -891,7 +892,7 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     TIMED(RN18_K_BN_BWD_APPLY, li, 0, kernel_instance_name("bn_bwd_apply_kernel", prec), 0.0,
           3 * tb + (rc ? 0.0 : tb / 16),
           bn_bwd_apply_launch(prec, ws + dz, mzp, ws + P.y, (float*)(ws + P.mean), (float*)(ws + P.coef), ws + dy,
-                              P.M, L.cout, st, msc, msf));
+                              P.M, L.cout, st, msc, msf, done));
     if (!c->captures.empty()) return run_captures(c, RN18_CAP_DY, li, ws + dy, (size_t)P.M * L.cout * es);
     return 0;
   };
@@ -950,14 +951,15 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     return 0;
   };
   // weight gradients of block bi from their dY buffers; last: the block's
-  // final ones (its end is then recorded for need_done)
-  auto fork = [&](int bi, const int* li, const size_t* dy, int n, bool last) -> int {
+  // final ones (its end is then recorded for need_done); bound: ev_fork
+  // was already bound to the launch that wrote the last dY buffer
+  auto fork = [&](int bi, const int* li, const size_t* dy, int n, bool last, bool bound = false) -> int {
     if (!ov) {
       for (int k = 0; k < n; ++k)
         if (int r2 = wgrad_on(li[k], dy[k], st)) return r2;
       return 0;
     }
-    HIPCHK(hipEventRecord(c->ev_fork, st));
+    if (!bound) HIPCHK(hipEventRecord(c->ev_fork, st));
     HIPCHK(hipStreamWaitEvent(c->side, c->ev_fork, 0));
     forked = true;
     for (int k = 0; k < n; ++k)
@@ -1046,13 +1048,14 @@ int run_train(Ctx* c, const Plan& pl, float* state, const float* images, const i
     const size_t z1b = (size_t)pl.cp[B.c1].M * a.convs[B.c1].cout * es;
     const size_t inb = (size_t)N * pl.cp[B.c1].Hin * pl.cp[B.c1].Win * a.convs[B.c1].cin_p * es;
     if (!c->captures.empty() && (r = run_captures(c, RN18_CAP_DZ1, bi, ws + pl.gz, z1b))) return r;
-    if ((r = bn_back(B.c1, pl.gz, RECOMPUTE, gy2))) return join(), r;
+    // the BN apply that writes gy2 also completes the fork event
+    if ((r = bn_back(B.c1, pl.gz, RECOMPUTE, gy2, ov ? c->ev_fork : nullptr))) return join(), r;
     if (fork_each) {
-      if ((r = fork(bi, &B.c1, &gy2, 1, true))) return join(), r;
+      if ((r = fork(bi, &B.c1, &gy2, 1, true, ov))) return join(), r;
     } else {
       const int li[3] = {B.c2, B.c1, B.ds};
       const size_t dy[3] = {gy, gy2, pl.gyd};
-      if ((r = fork(bi, li, dy, B.ds >= 0 ? 3 : 2, true))) return join(), r;
+      if ((r = fork(bi, li, dy, B.ds >= 0 ? 3 : 2, true, ov))) return join(), r;
     }
     // gB enters the previous block's second BN (its output mask), or the
     // CIFAR stem's BN (mask recomputed); the ImageNet stem takes the pool path

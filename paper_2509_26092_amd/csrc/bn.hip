@@ -10,6 +10,8 @@
 //
 // The elementwise passes (apply + ReLU + residual, backward apply) are 16-byte
 // HBM streams with the per-channel coefficients staged in LDS.
+#include <hip/hip_ext.h>
+
 #include "kernels.h"
 #include "pool.h"
 
@@ -570,12 +572,19 @@ int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float*
 }
 
 int bn_bwd_apply_launch(int prec, const void* dz, const uint8_t* mb, const void* y, const float* mean, const float* coef,
-                        void* dy, long M, int C, hipStream_t s, const float* mscale, const float* mshift) {
+                        void* dy, long M, int C, hipStream_t s, const float* mscale, const float* mshift,
+                        hipEvent_t done) {
   const long nchunks = M * C / prec_vw(prec);
   return with_prec(prec, [&](auto tag) {
     using T = decltype(tag);
-    hipLaunchKernelGGL(bn_bwd_apply_kernel<T>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const T*)dz, mb,
-                       (const T*)y, mean, coef, mscale, mshift, (T*)dy, nchunks, C);
+    if (done) {
+      // the event completes with this kernel: no separate marker on the queue
+      hipExtLaunchKernelGGL(bn_bwd_apply_kernel<T>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, nullptr, done, 0,
+                            (const T*)dz, mb, (const T*)y, mean, coef, mscale, mshift, (T*)dy, nchunks, C);
+    } else {
+      hipLaunchKernelGGL(bn_bwd_apply_kernel<T>, dim3(stream_blocks(nchunks)), dim3(256), 0, s, (const T*)dz, mb,
+                         (const T*)y, mean, coef, mscale, mshift, (T*)dy, nchunks, C);
+    }
     return ok();
   });
 }

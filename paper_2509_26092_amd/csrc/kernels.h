@@ -169,10 +169,11 @@ int bn_bwd_apply_pool_launch(int prec, const void* dpool, const uint8_t* arg, co
                              int C, int Ho, int Wo, hipStream_t s);
 int bn_bwd_final_launch(const float* part, int nblk, long M, int C, const float* gamma, const float* rstd,
                         float* dgamma, float* dbeta, float* coef, hipStream_t s);
-// dy = k1*g + k2*(y-mean) + k3
+// dy = k1*g + k2*(y-mean) + k3; done (optional) is recorded by the kernel
+// launch itself, completing when the kernel does
 int bn_bwd_apply_launch(int prec, const void* dz, const uint8_t* mb, const void* y, const float* mean,
                         const float* coef, void* dy, long M, int C, hipStream_t s, const float* mscale = nullptr,
-                        const float* mshift = nullptr);
+                        const float* mshift = nullptr, hipEvent_t done = nullptr);
 
 // ---------------------------------------------------------------------------
 // Misc streams
