@@ -166,11 +166,14 @@ def test_chunked_convolutions(arch, classes, prec, N, H, chunk):
     _run_parity(arch, classes, prec, N, H, seed=180 + N, chunk=chunk)
 
 
-@pytest.mark.parametrize("arch,classes,prec,N,H", [("imagenet", 1000, "bf16", 16, 64), ("cifar", 100, "fp32", 16, 32)])
+@pytest.mark.parametrize("arch,classes,prec,N,H", [("imagenet", 1000, "bf16", 16, 64), ("imagenet", 1000, "bf16", 64, 128),
+                                                 ("cifar", 100, "fp32", 16, 32)])
 def test_weight_gradients_on_side_stream_match_serial(arch, classes, prec, N, H):
     """The weight gradients run on a second stream beside the data-gradient
     chain; with profiling on, every launch stays on the caller's stream. Two
-    steps from the same state, one each way, agree bit for bit."""
+    steps from the same state, one each way, agree bit for bit. The batch-64
+    128x128 case has BN applies long enough (10-20 us) that a weight
+    gradient started before its dY buffer was complete would change bits."""
     L, st = make_state(arch, classes, 190)
     x = inputs.images(190, N, H, H)
     y = inputs.labels(190, N, classes)
